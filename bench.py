@@ -1,0 +1,220 @@
+"""DAR attention benchmark on one MI355X.
+
+One step = the whole hot path once:
+  * causal prefill of the Pythia-70M-shaped batch (B8 H8 T2048 d64 d_down16
+    w256, bf16): window-exit latent pre-pass + two-region attention kernel;
+  * one decode step of the 1B-scale batch over its split cache (B32 Hq32
+    Hkv8 d64 d_down16 w512, 32768 cached tokens): cache append of the new
+    token (window exit projected to its latent) + split-KV decode.
+Inputs are seeded synthetic N(0,1) tensors of those shapes, resident in HBM
+before timing starts. `value` is the prefill's algorithmic TFLOP/s; the decode
+KV GB/s is reported beside it.
+
+Prints ONE JSON line (rank 0). Only one GPU is used: --gpus above 1 exits.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def prefill_flops(B, Hq, T, d, dd, w):
+    """Algorithmic flops: QK^T and PV at 2 flop/MAC, d wide inside the window,
+    d_down wide beyond it; masked and skipped work is not counted."""
+    i = np.arange(T, dtype=np.int64)
+    n_loc = np.minimum(i + 1, w).sum()
+    n_dist = (i + 1).sum() - n_loc
+    return float(B * Hq * (4 * d * n_loc + 4 * dd * n_dist))
+
+
+def decode_bytes(B, Hq, Hkv, d, dd, w, L, esize=2):
+    """Algorithmic HBM bytes of one decode step at cache length L: ring and
+    latents (keys and values) once, plus query, output and W_down."""
+    n_win = min(L, w)
+    n_lat = L - n_win
+    kv = B * Hkv * 2 * (n_win * d + n_lat * dd) * esize
+    return float(kv + 2 * B * Hq * d * esize + Hkv * d * dd * esize)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only; this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import dar_inputs as di
+    import paper_2606_18587_amd as dar
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+
+    def up(t):
+        if t is None:
+            return None
+        if t.dtype == "bf16":
+            return torch.from_numpy(t.store.view(np.int16)).view(torch.bfloat16).to(dev)
+        return torch.from_numpy(t.store).to(dev)
+
+    # ---------------- prefill workload
+    pw = di.WORKLOADS["pythia70m"]
+    pin = di.make_prefill_inputs(pw)
+    q, k, v, wd = (up(pin[x]) for x in ("q", "k", "v", "wd"))
+    o = torch.empty_like(q)
+    shape = dar.make_shape(pw.B, pw.Hq, pw.Hkv, pw.d, pw.dd, pw.w, torch.bfloat16)
+    ws = torch.empty(max(1, dar.dar_prefill_workspace_bytes(shape, pw.T)), dtype=torch.uint8,
+                     device=dev)
+    flops = prefill_flops(pw.B, pw.Hq, pw.T, pw.d, pw.dd, pw.w)
+
+    # ---------------- decode workload
+    dw = di.WORKLOADS["decode1b"]
+    t0 = time.time()
+    pre = di.make_decode_prefix(dw, dw.T)
+    cap = dw.T + args.warmup + args.steps + 1
+    cache = dar.DarCache(dw.B, dw.Hkv, dw.d, dw.dd, dw.w, cap, torch.bfloat16, device=dev)
+    dwd = up(pre["wd"])
+    kpre, vpre = up(pre["k"]), up(pre["v"])
+    del pre
+    dar.dar_cache_append(cache, kpre, vpre, dwd, Hq=dw.Hq)
+    del kpre, vpre
+    dshape = dar.make_shape(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, torch.bfloat16)
+    dws = torch.empty(dar.dar_decode_workspace_bytes(dshape, cap), dtype=torch.uint8, device=dev)
+    n_step_inputs = args.warmup + args.steps
+    step_in = []
+    for t in range(n_step_inputs):
+        st = di.make_decode_step(dw, t)
+        step_in.append((up(st["q"]), up(st["k"]), up(st["v"])))
+    dout = torch.empty(dw.B, dw.Hq, dw.d, dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    setup_s = time.time() - t0
+
+    def one_step(idx, evs=None):
+        qd, kd, vd = step_in[idx]
+        if evs:
+            evs[0].record()
+        dar.dar_attn_prefill(q, k, v, wd, None, pw.w, o=o, ws=ws, check=False)
+        if evs:
+            evs[1].record()
+        dar.dar_cache_append(cache, kd, vd, dwd, Hq=dw.Hq)
+        if evs:
+            evs[2].record()
+        dar.dar_attn_decode(cache, qd, dwd, None, o=dout, ws=dws)
+        if evs:
+            evs[3].record()
+
+    for i in range(args.warmup):
+        one_step(i)
+    torch.cuda.synchronize()
+
+    L_first = cache.len + 1
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for i in range(args.steps):
+        one_step(args.warmup + i, events[i])
+    stop.record()
+    torch.cuda.synchronize()
+    total_ms = start.elapsed_time(stop)
+    pre_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
+    app_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
+    dec_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
+    L_last = cache.len
+
+    pre_us = float(pre_ms.mean() * 1e3)
+    dec_us = float(dec_ms.mean() * 1e3)
+    tflops = flops / (pre_us * 1e-6) / 1e12
+    dbytes = np.mean([decode_bytes(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, L)
+                      for L in range(L_first, L_last + 1)])
+    gbs = dbytes / (dec_us * 1e-6) / 1e9
+
+    result = {
+        "metric": "DAR prefill TFLOP/s + decode KV GB/s, as fraction of MI355X peak, 1 GPU",
+        "value": round(tflops, 3),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) tensors of the workload shapes; no dataset)",
+        "config": {
+            "workload": "prefill pythia70m-shaped B8 H8 T2048 d64 d_down16 w256 + decode "
+                        "1B-shaped B32 Hq32 Hkv8 d64 d_down16 w512 L32768",
+            "global_batch": pw.B, "seq_len": pw.T, "parallelism": "none (1 GPU)",
+        },
+        "prefill": {"us": round(pre_us, 2), "us_median": round(float(np.median(pre_ms) * 1e3), 2),
+                    "tflops": round(tflops, 2), "frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+                    "alg_flop": flops},
+        "decode": {"us": round(dec_us, 2), "us_median": round(float(np.median(dec_ms) * 1e3), 2),
+                   "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
+                   "alg_bytes": dbytes, "cache_len": [L_first, L_last],
+                   "append_us": round(float(app_ms.mean() * 1e3), 2)},
+        "roofline": {"kernel": "dar_attn_prefill (latent pre-pass + attention kernel)",
+                     "bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None},
+        "roofline_decode": {"kernel": "dar_attn_decode (split + combine)", "bound": "hbm",
+                            "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                            "frac": round(gbs / PEAK_HBM_GBS, 4), "traffic": None},
+        "setup_s": round(setup_s, 1),
+    }
+
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(pw, pin, args.cpu_seconds)
+
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(pw, pin, budget_s):
+    """The fp64 oracle on the host cores, on whole (batch, head) slices of the
+    same prefill workload, until the time budget is used."""
+    from oracle import oracle
+
+    grp = pw.Hq // pw.Hkv
+    pos = np.arange(pw.T)
+    per_head = prefill_flops(1, 1, pw.T, pw.d, pw.dd, pw.w)
+    done = 0
+    t0 = time.time()
+    for b in range(pw.B):
+        for h in range(pw.Hq):
+            g = h // grp
+            oracle.rows(pin["k"].f64[b, g], pin["v"].f64[b, g], pin["wd"].f64[g], None, pw.w, pos,
+                        pin["q"].f64[b, h])
+            done += 1
+            if time.time() - t0 >= budget_s:
+                break
+        if time.time() - t0 >= budget_s:
+            break
+    el = time.time() - t0
+    return {"value": round(done * per_head / el / 1e12, 6), "unit": "TFLOP/s",
+            "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": "%d of %d (batch, head) slices of the pythia70m prefill, all %d rows each, "
+                      "%.1f s" % (done, pw.B * pw.Hq, pw.T, el)}
+
+
+if __name__ == "__main__":
+    main()

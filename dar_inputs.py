@@ -68,13 +68,18 @@ def seed_for(cfg_id: int, tensor_id: int) -> int:
 def round_bf16_bits(x: np.ndarray) -> np.ndarray:
     """fp32 -> bfloat16 bit patterns (uint16), round to nearest even."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16).astype(np.uint16)
-    nan = np.isnan(x)
+    flat = x.reshape(-1)
+    out = np.empty(flat.shape, np.uint16)
+    step = 1 << 24
+    for s in range(0, flat.size, step):
+        u = flat[s:s + step].view(np.uint32)
+        # finite values cannot overflow 32 bits here; NaNs are replaced below
+        r = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
+        out[s:s + step] = r.astype(np.uint16)
+    nan = np.isnan(flat)
     if nan.any():
-        r[nan] = 0x7FC0
-    return r
+        out[nan] = 0x7FC0
+    return out.reshape(x.shape)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -98,6 +103,33 @@ class Tensor:
             self.f64 = self.store.astype(np.float64)
         else:
             raise ValueError(dtype)
+
+    @classmethod
+    def from_store(cls, store: np.ndarray, dtype: str) -> "Tensor":
+        """Wrap already-rounded storage (uint16 bf16 bits or float32); the
+        float64 view is made on demand to keep large caches cheap."""
+        t = cls.__new__(cls)
+        t.dtype = dtype
+        t.store = store
+        t._f64 = None
+        return t
+
+    @property
+    def f64(self) -> np.ndarray:
+        if self._f64 is None:
+            src = bf16_bits_to_f32(self.store) if self.dtype == "bf16" else self.store
+            self._f64 = src.astype(np.float64)
+        return self._f64
+
+    @f64.setter
+    def f64(self, value):
+        self._f64 = value
+
+    def f64_slice(self, idx) -> np.ndarray:
+        """float64 values of store[idx] without widening the whole tensor."""
+        part = self.store[idx]
+        src = bf16_bits_to_f32(part) if self.dtype == "bf16" else part
+        return np.asarray(src, dtype=np.float64)
 
     @property
     def shape(self):
@@ -127,6 +159,24 @@ def make_prefill_inputs(wl: Workload, untied: bool = False, seed_shift: int = 0,
     if untied:
         wu = normal((wl.Hkv, wl.dd, wl.d), seed_for(wl.cfg_id, TID_WU) + s, std=1.0 / np.sqrt(wl.dd))
         out["wu"] = Tensor(wu, wl.dtype)
+    return out
+
+
+def make_decode_prefix(wl: Workload, L: int) -> dict:
+    """Keys and values [B,Hkv,L,d] of the tokens already in the cache before
+    the decode steps, drawn batch by batch from one stream per tensor."""
+    out = {}
+    for name, tid in (("k", TID_K), ("v", TID_V)):
+        g = np.random.Generator(np.random.PCG64(seed_for(wl.cfg_id, tid)))
+        parts = []
+        for _ in range(wl.B):
+            x = g.standard_normal(size=(wl.Hkv, L, wl.d), dtype=np.float32)
+            parts.append(round_bf16_bits(x) if wl.dtype == "bf16" else x)
+        store = np.stack(parts)
+        out[name] = Tensor.from_store(store, wl.dtype)
+    wd = normal((wl.Hkv, wl.d, wl.dd), seed_for(wl.cfg_id, TID_WD), std=1.0 / np.sqrt(wl.d))
+    out["wd"] = Tensor(wd, wl.dtype)
+    out["wu"] = None
     return out
 
 

@@ -1,0 +1,122 @@
+/*
+ * dar.h — C ABI of libdar, Distance-Adaptive Representation (DAR) attention
+ * on AMD Instinct MI355X (gfx950).
+ *
+ * Method (arXiv 2606.18587, "Dual Dimensionality for Local and Global
+ * Attention", Section 2):
+ *   Eq. 1  a token's bottleneck representation is c_j = x_j W_down (d -> d_down);
+ *   Eq. 2  it is lifted back with W_up (d_down -> d) before use;
+ *   Eq. 3  for query position i, token j <= i is used at full dimension if
+ *          i - j < w (the window includes the current token) and in lifted
+ *          form otherwise, for keys and for values alike;
+ *   Eq. 4  o_i = softmax_j(q_i . k_j / sqrt(d)) v_j over j = 0..i, one softmax
+ *          for both regions, d being the full per-head key dimension.
+ * The Limitations section's efficient cache is what this library keeps for
+ * decoding: full-dimension K/V for the last w tokens, the d_down latent for
+ * every older token, with W_up absorbed into the query and the output:
+ *   q . ((k W_down) W_up) = (q W_up^T) . (k W_down),
+ *   sum_j p_j (c_j W_up) = (sum_j p_j c_j) W_up.
+ *
+ * Conventions for every entry point
+ *   - Bottleneck per KV head: W_down [Hkv][d][d_down] maps each KV head's key
+ *     and value (one matrix shared by K and V); W_up [Hkv][d_down][d], or NULL
+ *     for the tied form W_up = W_down^T.
+ *   - GQA: query head h reads KV head h / (Hq / Hkv).
+ *   - Layout: row-major, contiguous, [B][H][T][d]. Every tensor of a call has
+ *     the dtype of the shape (fp32 or bf16); bf16 runs accumulate in fp32.
+ *   - Positions are 0-based and implicit (prefill: 0..T-1; decode: the query
+ *     sits at position len-1 of the cache). Rotary position embedding, if any,
+ *     is applied by the caller before these calls.
+ *   - Ownership: every tensor pointer is device memory owned by the caller.
+ *     The library allocates nothing and keeps no state between calls beyond
+ *     one-time per-device kernel attributes; calls on different streams with
+ *     disjoint buffers may run concurrently.
+ *   - Asynchrony: work is enqueued on `stream` (NULL = the default stream) and
+ *     the call returns without synchronising. Kernel faults surface at the
+ *     caller's next synchronisation.
+ *   - Errors: arguments are validated before anything is enqueued; on any
+ *     error status nothing has been written and the cache length is unchanged.
+ *     Device pointers must be non-NULL and 16-byte aligned (W_up may be NULL).
+ *     No exception crosses the ABI.
+ */
+#ifndef DAR_H
+#define DAR_H
+
+#include <stddef.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    DAR_OK = 0,
+    DAR_E_ARG = 1,          /* bad shape, NULL or misaligned pointer          */
+    DAR_E_UNSUPPORTED = 2,  /* valid, but outside what the kernels implement  */
+    DAR_E_CAPACITY = 3,     /* cache append would exceed its capacity         */
+    DAR_E_WORKSPACE = 4,    /* workspace missing or smaller than required     */
+    DAR_E_HIP = 5           /* the HIP runtime refused a launch               */
+} dar_status;
+
+typedef enum { DAR_F32 = 0, DAR_BF16 = 1 } dar_dtype;
+
+/* B batch, Hq query heads, Hkv KV heads (Hq % Hkv == 0), d head dimension,
+ * d_down bottleneck dimension (1 <= d_down <= d), w window (w >= 0; w = 0
+ * puts every token, including the query's own, in the bottleneck form). */
+typedef struct {
+    int B, Hq, Hkv, d, d_down, w;
+    dar_dtype dtype;
+} dar_shape;
+
+/* Split KV cache (device buffers owned by the caller, this struct on the host).
+ *   k_win, v_win [B][Hkv][w][d]       ring: token p lives in slot p % w while
+ *                                       p >= len - w (unused when w == 0)
+ *   k_lat, v_lat [B][Hkv][cap][d_down] latent of token e (= x_e W_down) in
+ *                                       slot e for every e < len - w
+ *   cap   maximum number of tokens     len   tokens appended so far          */
+typedef struct {
+    void *k_win, *v_win, *k_lat, *v_lat;
+    int cap;
+    int len;
+} dar_cache;
+
+/* Causal prefill over positions 0..T-1 (Eq. 3-4 for every row).
+ *   q [B][Hq][T][d], k, v [B][Hkv][T][d], w_down [Hkv][d][d_down],
+ *   w_up [Hkv][d_down][d] or NULL (tied), o [B][Hq][T][d] (output).
+ *   ws: device workspace of at least dar_prefill_workspace_bytes(s, T) bytes
+ *   (may be NULL when that size is 0). T >= 1.
+ * Supported: fp32 with d <= 256; bf16 with d <= 256 (d in {64, 128} with
+ * d_down in {16, 32} take the matrix-core path). */
+dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void* k,
+                            const void* v, const void* w_down, const void* w_up, void* o,
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Append n >= 1 tokens k_new, v_new [B][Hkv][n][d] at positions len..len+n-1.
+ * Every token that leaves the window (position len+t-w for t < n) is
+ * down-projected with W_down (Eq. 1, fp32 accumulation, rounded to the cache
+ * dtype) into its latent slot; the newest min(n, w) tokens are written to the
+ * ring. The result is bit-identical to n single-token appends. On success
+ * c->len += n (host side, at enqueue time). Fails with DAR_E_CAPACITY if
+ * len + n > cap. */
+dar_status dar_cache_append(const dar_shape* s, dar_cache* c, const void* k_new,
+                            const void* v_new, int n, const void* w_down, hipStream_t stream);
+
+/* One decode step for the query q [B][Hq][d] at position c->len - 1, whose own
+ * key and value must already have been appended. o [B][Hq][d] (output).
+ * ws: device workspace of at least dar_decode_workspace_bytes(s, c->cap)
+ * bytes. Requires c->len >= 1. */
+dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q,
+                           const void* w_down, const void* w_up, void* o, void* ws,
+                           size_t ws_bytes, hipStream_t stream);
+
+/* Workspace sizes (0 on an invalid shape). */
+size_t dar_prefill_workspace_bytes(const dar_shape* s, int T);
+size_t dar_decode_workspace_bytes(const dar_shape* s, int cap);
+
+/* Static English text for a status code. */
+const char* dar_status_string(dar_status st);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* DAR_H */

@@ -1,0 +1,194 @@
+"""DAR attention on MI355X: Python binding of libdar (include/dar.h).
+
+Argument marshalling only: torch provides device memory and the current HIP
+stream; every step of the computation runs in the library's HIP kernels.
+The library must have been built (paper_2606_18587_amd.build); importing this
+package without it raises, there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libdar.so")
+
+DAR_OK, DAR_E_ARG, DAR_E_UNSUPPORTED, DAR_E_CAPACITY, DAR_E_WORKSPACE, DAR_E_HIP = range(6)
+DAR_F32, DAR_BF16 = 0, 1
+
+
+class DarShape(ctypes.Structure):
+    _fields_ = [("B", ctypes.c_int), ("Hq", ctypes.c_int), ("Hkv", ctypes.c_int),
+                ("d", ctypes.c_int), ("d_down", ctypes.c_int), ("w", ctypes.c_int),
+                ("dtype", ctypes.c_int)]
+
+
+class DarCacheStruct(ctypes.Structure):
+    _fields_ = [("k_win", ctypes.c_void_p), ("v_win", ctypes.c_void_p),
+                ("k_lat", ctypes.c_void_p), ("v_lat", ctypes.c_void_p),
+                ("cap", ctypes.c_int), ("len", ctypes.c_int)]
+
+
+class DarError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__("%s: %s (status %d)" % (where, status_string(status), status))
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError("libdar.so is not built; run `python -m paper_2606_18587_amd.build` "
+                          "(there is no non-HIP fallback)")
+    lib = ctypes.CDLL(LIB_PATH)
+    vp, sz, ci = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int
+    shp = ctypes.POINTER(DarShape)
+    cp = ctypes.POINTER(DarCacheStruct)
+    lib.dar_attn_prefill.restype = ci
+    lib.dar_attn_prefill.argtypes = [shp, ci, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.dar_cache_append.restype = ci
+    lib.dar_cache_append.argtypes = [shp, cp, vp, vp, ci, vp, vp]
+    lib.dar_attn_decode.restype = ci
+    lib.dar_attn_decode.argtypes = [shp, cp, vp, vp, vp, vp, vp, sz, vp]
+    lib.dar_prefill_workspace_bytes.restype = sz
+    lib.dar_prefill_workspace_bytes.argtypes = [shp, ci]
+    lib.dar_decode_workspace_bytes.restype = sz
+    lib.dar_decode_workspace_bytes.argtypes = [shp, ci]
+    lib.dar_status_string.restype = ctypes.c_char_p
+    lib.dar_status_string.argtypes = [ci]
+    return lib
+
+
+lib = _load()
+
+EXPORTS = ("dar_attn_prefill", "dar_cache_append", "dar_attn_decode",
+           "dar_prefill_workspace_bytes", "dar_decode_workspace_bytes", "dar_status_string")
+
+
+def status_string(st: int) -> str:
+    return lib.dar_status_string(int(st)).decode()
+
+
+def _dtype_code(t: torch.dtype) -> int:
+    if t == torch.float32:
+        return DAR_F32
+    if t == torch.bfloat16:
+        return DAR_BF16
+    raise TypeError("DAR tensors must be float32 or bfloat16, got %s" % t)
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("DAR tensors must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def make_shape(B, Hq, Hkv, d, d_down, w, dtype) -> DarShape:
+    return DarShape(int(B), int(Hq), int(Hkv), int(d), int(d_down), int(w), _dtype_code(dtype))
+
+
+def dar_prefill_workspace_bytes(shape: DarShape, T: int) -> int:
+    return int(lib.dar_prefill_workspace_bytes(ctypes.byref(shape), int(T)))
+
+
+def dar_decode_workspace_bytes(shape: DarShape, cap: int) -> int:
+    return int(lib.dar_decode_workspace_bytes(ctypes.byref(shape), int(cap)))
+
+
+def dar_status_string(st: int) -> str:
+    return status_string(st)
+
+
+def _workspace(nbytes, device):
+    if nbytes == 0:
+        return None
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
+
+
+def dar_attn_prefill(q, k, v, w_down, w_up, w, o=None, ws=None, stream=None, check=True):
+    """Causal DAR prefill. q [B,Hq,T,d]; k, v [B,Hkv,T,d]; w_down [Hkv,d,dd];
+    w_up [Hkv,dd,d] or None (tied). Returns o [B,Hq,T,d]."""
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    dd = w_down.shape[2]
+    shape = make_shape(B, Hq, Hkv, d, dd, w, q.dtype)
+    if check:
+        for name, t, want in (("k", k, (B, Hkv, T, d)), ("v", v, (B, Hkv, T, d)),
+                              ("w_down", w_down, (Hkv, d, dd))):
+            if tuple(t.shape) != want or t.dtype != q.dtype:
+                raise ValueError("%s: expected %s %s, got %s %s" % (name, want, q.dtype,
+                                                                   tuple(t.shape), t.dtype))
+        if w_up is not None and (tuple(w_up.shape) != (Hkv, dd, d) or w_up.dtype != q.dtype):
+            raise ValueError("w_up: expected %s" % ((Hkv, dd, d),))
+    if o is None:
+        o = torch.empty_like(q)
+    need = dar_prefill_workspace_bytes(shape, T)
+    if ws is None:
+        ws = _workspace(need, q.device)
+    st = lib.dar_attn_prefill(ctypes.byref(shape), int(T), _ptr(q), _ptr(k), _ptr(v),
+                              _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(ws),
+                              0 if ws is None else ws.numel() * ws.element_size(),
+                              _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_prefill")
+    return o
+
+
+class DarCache:
+    """Split KV cache owned by torch: ring [B,Hkv,w,d] for the window and
+    latents [B,Hkv,cap,dd] for older tokens (see dar_cache in include/dar.h)."""
+
+    def __init__(self, B, Hkv, d, d_down, w, cap, dtype, device="cuda"):
+        self.B, self.Hkv, self.d, self.d_down, self.w, self.cap = B, Hkv, d, d_down, w, cap
+        self.dtype = dtype
+        wl = max(w, 1)  # keep valid pointers for w = 0 (the ring is never touched then)
+        self.k_win = torch.zeros(B, Hkv, wl, d, dtype=dtype, device=device)
+        self.v_win = torch.zeros(B, Hkv, wl, d, dtype=dtype, device=device)
+        self.k_lat = torch.zeros(B, Hkv, cap, d_down, dtype=dtype, device=device)
+        self.v_lat = torch.zeros(B, Hkv, cap, d_down, dtype=dtype, device=device)
+        self.struct = DarCacheStruct(self.k_win.data_ptr(), self.v_win.data_ptr(),
+                                     self.k_lat.data_ptr(), self.v_lat.data_ptr(), int(cap), 0)
+
+    @property
+    def len(self) -> int:
+        return int(self.struct.len)
+
+
+def dar_cache_append(cache: DarCache, k_new, v_new, w_down, Hq=None, stream=None):
+    """Append n tokens k_new, v_new [B,Hkv,n,d]; projects window exits to latents."""
+    B, Hkv, n, d = k_new.shape
+    shape = make_shape(B, Hq if Hq is not None else Hkv, Hkv, d, cache.d_down, cache.w,
+                       k_new.dtype)
+    if tuple(v_new.shape) != (B, Hkv, n, d) or (B, Hkv, d) != (cache.B, cache.Hkv, cache.d):
+        raise ValueError("k_new/v_new do not match the cache")
+    st = lib.dar_cache_append(ctypes.byref(shape), ctypes.byref(cache.struct), _ptr(k_new),
+                              _ptr(v_new), int(n), _ptr(w_down), _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_cache_append")
+    return cache
+
+
+def dar_attn_decode(cache: DarCache, q, w_down, w_up=None, o=None, ws=None, stream=None):
+    """One decode step: q [B,Hq,d] at position cache.len - 1. Returns o [B,Hq,d]."""
+    B, Hq, d = q.shape
+    shape = make_shape(B, Hq, cache.Hkv, d, cache.d_down, cache.w, q.dtype)
+    if o is None:
+        o = torch.empty_like(q)
+    if ws is None:
+        ws = _workspace(dar_decode_workspace_bytes(shape, cache.cap), q.device)
+    st = lib.dar_attn_decode(ctypes.byref(shape), ctypes.byref(cache.struct), _ptr(q),
+                             _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(ws),
+                             0 if ws is None else ws.numel() * ws.element_size(),
+                             _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_decode")
+    return o

@@ -1,0 +1,212 @@
+// C ABI of libdar: argument validation, workspace sizing, cache bookkeeping
+// and kernel dispatch. Nothing is enqueued unless every check passes.
+#include "../../include/dar.h"
+#include "dar_kernels.hpp"
+
+#include <stdint.h>
+#include <stdio.h>
+#include <stdlib.h>
+
+namespace dar {
+
+PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize) {
+    PrefillWs ws{0, 0, 0};
+    const int Tl = T - w;
+    if (Tl <= 0) return ws;
+    const size_t Tp = (size_t)round_up(Tl, 64);
+    const size_t one = (size_t)B * Hkv * Tp * dd * esize;
+    const size_t one_al = (one + 255) & ~(size_t)255;
+    ws.ck_off = 0;
+    ws.cv_off = one_al;
+    ws.bytes = 2 * one_al;
+    return ws;
+}
+
+// Both fast paths (matrix-core prefill) and the generic kernels live in this
+// library; the generic path handles everything the fast one does not.
+bool prefill_mfma_supported(const dar_shape* s);
+hipError_t launch_prefill_mfma(const dar_shape* s, int T, const void* q, const void* k,
+                               const void* v, const void* wd, const void* wu, void* o,
+                               const void* cK, const void* cVt, hipStream_t st);
+
+}  // namespace dar
+
+using namespace dar;
+
+namespace {
+
+bool log_enabled() {
+    static int on = -1;
+    if (on < 0) {
+        const char* e = getenv("DAR_LOG");
+        on = (e && e[0] == '1') ? 1 : 0;
+    }
+    return on == 1;
+}
+
+size_t esize_of(dar_dtype t) { return t == DAR_BF16 ? 2 : 4; }
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// A device tensor argument: non-NULL and 16-byte aligned.
+bool dev_ok(const void* p) { return p != nullptr && aligned16(p); }
+
+dar_status check_shape(const dar_shape* s) {
+    if (!s) return DAR_E_ARG;
+    if (s->B < 1 || s->Hq < 1 || s->Hkv < 1 || s->d < 1 || s->d_down < 1 || s->w < 0)
+        return DAR_E_ARG;
+    if (s->Hq % s->Hkv != 0) return DAR_E_ARG;
+    if (s->d_down > s->d) return DAR_E_ARG;
+    if (s->dtype != DAR_F32 && s->dtype != DAR_BF16) return DAR_E_ARG;
+    if (s->d > 256) return DAR_E_UNSUPPORTED;
+    if ((long long)s->B * s->Hq > 65535) return DAR_E_UNSUPPORTED;
+    return DAR_OK;
+}
+
+bool group_supported(const dar_shape* s) {
+    const int G = s->Hq / s->Hkv;
+    return G == 1 || G == 2 || G == 4 || G == 8;
+}
+
+void clear_hip_error() { (void)hipGetLastError(); }
+
+}  // namespace
+
+extern "C" {
+
+const char* dar_status_string(dar_status st) {
+    switch (st) {
+        case DAR_OK: return "ok";
+        case DAR_E_ARG: return "invalid argument";
+        case DAR_E_UNSUPPORTED: return "unsupported shape or dtype";
+        case DAR_E_CAPACITY: return "cache capacity exceeded";
+        case DAR_E_WORKSPACE: return "workspace missing or too small";
+        case DAR_E_HIP: return "HIP launch failure";
+    }
+    return "unknown status";
+}
+
+size_t dar_prefill_workspace_bytes(const dar_shape* s, int T) {
+    if (check_shape(s) != DAR_OK || T < 1) return 0;
+    return prefill_ws_layout(s->B, s->Hkv, T, s->d_down, s->w, esize_of(s->dtype)).bytes;
+}
+
+size_t dar_decode_workspace_bytes(const dar_shape* s, int cap) {
+    if (check_shape(s) != DAR_OK || cap < 1 || !group_supported(s)) return 0;
+    const int S = decode_max_splits(cap, s->w, s->d, s->d_down, s->Hq / s->Hkv);
+    return (size_t)s->B * s->Hq * S * (2 + s->d) * sizeof(float);
+}
+
+dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void* k,
+                            const void* v, const void* w_down, const void* w_up, void* o,
+                            void* ws, size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (T < 1) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(w_down) || !dev_ok(o)) return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    const PrefillWs L = prefill_ws_layout(s->B, s->Hkv, T, s->d_down, s->w, esize_of(s->dtype));
+    if (L.bytes > 0 && (ws == nullptr || ws_bytes < L.bytes)) return DAR_E_WORKSPACE;
+    if (L.bytes > 0 && !aligned16(ws)) return DAR_E_ARG;
+
+    clear_hip_error();
+    char* wsb = (char*)ws;
+    const void* cK = L.bytes ? wsb + L.ck_off : nullptr;
+    const void* cV = L.bytes ? wsb + L.cv_off : nullptr;
+    hipError_t e = hipSuccess;
+    const bool fast = prefill_mfma_supported(s);
+    if (log_enabled())
+        fprintf(stderr, "[dar] prefill B=%d Hq=%d Hkv=%d T=%d d=%d dd=%d w=%d %s path=%s\n", s->B,
+                s->Hq, s->Hkv, T, s->d, s->d_down, s->w, s->dtype == DAR_BF16 ? "bf16" : "f32",
+                fast ? "mfma" : "valu");
+    if (s->dtype == DAR_BF16) {
+        e = launch_prefill_latent<bf16_t>((const bf16_t*)k, (const bf16_t*)v,
+                                          (const bf16_t*)w_down, (bf16_t*)cK, (bf16_t*)cV, s->B,
+                                          s->Hkv, T, s->d, s->d_down, s->w, fast, stream);
+        if (e == hipSuccess) {
+            if (fast)
+                e = launch_prefill_mfma(s, T, q, k, v, w_down, w_up, o, cK, cV, stream);
+            else
+                e = launch_prefill_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k,
+                                                (const bf16_t*)v, (const bf16_t*)w_down,
+                                                (const bf16_t*)w_up, (const bf16_t*)cK,
+                                                (const bf16_t*)cV, (bf16_t*)o, s->B, s->Hq,
+                                                s->Hkv, T, s->d, s->d_down, s->w, stream);
+        }
+    } else {
+        e = launch_prefill_latent<float>((const float*)k, (const float*)v, (const float*)w_down,
+                                         (float*)cK, (float*)cV, s->B, s->Hkv, T, s->d,
+                                         s->d_down, s->w, false, stream);
+        if (e == hipSuccess)
+            e = launch_prefill_valu<float>((const float*)q, (const float*)k, (const float*)v,
+                                           (const float*)w_down, (const float*)w_up,
+                                           (const float*)cK, (const float*)cV, (float*)o, s->B,
+                                           s->Hq, s->Hkv, T, s->d, s->d_down, s->w, stream);
+    }
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+dar_status dar_cache_append(const dar_shape* s, dar_cache* c, const void* k_new,
+                            const void* v_new, int n, const void* w_down, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (!c || n < 1 || c->cap < 1 || c->len < 0 || c->len > c->cap) return DAR_E_ARG;
+    if (!dev_ok(k_new) || !dev_ok(v_new) || !dev_ok(w_down)) return DAR_E_ARG;
+    if (!dev_ok(c->k_lat) || !dev_ok(c->v_lat)) return DAR_E_ARG;
+    if (s->w > 0 && (!dev_ok(c->k_win) || !dev_ok(c->v_win))) return DAR_E_ARG;
+    if ((long long)c->len + n > (long long)c->cap) return DAR_E_CAPACITY;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+
+    clear_hip_error();
+    hipError_t e;
+    if (s->dtype == DAR_BF16)
+        e = launch_append<bf16_t>((const bf16_t*)k_new, (const bf16_t*)v_new,
+                                  (const bf16_t*)w_down, (bf16_t*)c->k_win, (bf16_t*)c->v_win,
+                                  (bf16_t*)c->k_lat, (bf16_t*)c->v_lat, s->B, s->Hkv, s->d,
+                                  s->d_down, s->w, c->cap, c->len, n, stream);
+    else
+        e = launch_append<float>((const float*)k_new, (const float*)v_new, (const float*)w_down,
+                                 (float*)c->k_win, (float*)c->v_win, (float*)c->k_lat,
+                                 (float*)c->v_lat, s->B, s->Hkv, s->d, s->d_down, s->w, c->cap,
+                                 c->len, n, stream);
+    if (e != hipSuccess) return DAR_E_HIP;
+    c->len += n;
+    return DAR_OK;
+}
+
+dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q,
+                           const void* w_down, const void* w_up, void* o, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (!c || c->cap < 1 || c->len < 1 || c->len > c->cap) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(w_down) || !dev_ok(o)) return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if (!dev_ok(c->k_lat) || !dev_ok(c->v_lat)) return DAR_E_ARG;
+    if (s->w > 0 && (!dev_ok(c->k_win) || !dev_ok(c->v_win))) return DAR_E_ARG;
+    if (!group_supported(s)) return DAR_E_UNSUPPORTED;
+    const int G = s->Hq / s->Hkv;
+    if (decode_max_splits(c->cap, s->w, s->d, s->d_down, G) > 1024) return DAR_E_UNSUPPORTED;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+    const size_t need = dar_decode_workspace_bytes(s, c->cap);
+    if (ws == nullptr || ws_bytes < need) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+
+    clear_hip_error();
+    hipError_t e;
+    if (s->dtype == DAR_BF16)
+        e = launch_decode<bf16_t>((const bf16_t*)q, (const bf16_t*)w_down, (const bf16_t*)w_up,
+                                  (const bf16_t*)c->k_win, (const bf16_t*)c->v_win,
+                                  (const bf16_t*)c->k_lat, (const bf16_t*)c->v_lat, (bf16_t*)o,
+                                  (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, c->cap,
+                                  c->len, stream);
+    else
+        e = launch_decode<float>((const float*)q, (const float*)w_down, (const float*)w_up,
+                                 (const float*)c->k_win, (const float*)c->v_win,
+                                 (const float*)c->k_lat, (const float*)c->v_lat, (float*)o,
+                                 (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, c->cap,
+                                 c->len, stream);
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+}  // extern "C"

@@ -1,0 +1,52 @@
+// Launchers of the DAR kernels (host side). All of them enqueue on `st` and
+// return the launch status; shapes have been validated by the C ABI layer.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace dar {
+
+typedef uint16_t bf16_t;
+
+static inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
+
+// Prefill workspace: latents of tokens [0, T - w) per (batch, KV head),
+// token count padded to Tp = round_up(T - w, 64):
+//   cK  [B*Hkv][Tp][dd]            token-major
+//   cVt [B*Hkv][Tp/64][dd][64]     64-token blocks, transposed inside a block
+struct PrefillWs {
+    size_t ck_off, cv_off, bytes;
+};
+PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize);
+
+// Decode workspace: per (batch, query head, split) partial softmax state
+// {m, l, acc[max(d, dd)]} in fp32.
+struct DecodeSplits {
+    int chunk_lat, chunk_win;   // tokens per split in each region
+    int n_lat_split, n_win_split;
+};
+DecodeSplits decode_splits(int len, int w, int d, int dd, int G);
+int decode_max_splits(int cap, int w, int d, int dd, int G);
+
+template <typename T>
+hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt, int B,
+                                 int Hkv, int T_, int d, int dd, int w, bool perm, hipStream_t st);
+
+template <typename T>
+hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, T* v_win,
+                         T* k_lat, T* v_lat, int B, int Hkv, int d, int dd, int w, int cap, int len,
+                         int n, hipStream_t st);
+
+template <typename T>
+hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, const T* wu,
+                               const T* cK, const T* cVt, T* o, int B, int Hq, int Hkv, int T_,
+                               int d, int dd, int w, hipStream_t st);
+
+template <typename T>
+hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
+                         const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
+                         int d, int dd, int w, int cap, int len, hipStream_t st);
+
+}  // namespace dar

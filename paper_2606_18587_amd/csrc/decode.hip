@@ -1,0 +1,348 @@
+// Split-KV DAR decode over the split cache (Limitations section: the last w
+// tokens at full d in a ring, every older token as its d_down latent).
+//
+// Stage 1 (decode_split_kernel): one block per (batch, KV head, split). A
+// split is a run of consecutive tokens of one region: latent tokens
+// [0, len - w) are read from k_lat/v_lat and scored with q~ = q W_up^T
+// (W_up absorbed into the query); window tokens [len - w, len) are read from
+// the ring and scored with q. All G = Hq/Hkv query heads of the KV head are
+// handled by the block, so every cache byte is read once per step. Two
+// passes over the split: keys (scores kept in LDS, exact per-head max), then
+// values with p = exp2(s - max). Output per (head, split): {m, l, acc} with
+// acc in d_down space for latent splits and in d space for window splits.
+//
+// Stage 2 (decode_combine_kernel): one block per (batch, query head) merges
+// the splits under one max (Eq. 4 is a single softmax over both regions),
+// lifts the latent part once, o = (o_win + o_lat W_up) / l.
+#include "dar_common.hpp"
+#include "dar_kernels.hpp"
+
+namespace dar {
+
+static constexpr int kDecThreads = 256;
+static constexpr int kDecScoreSlots = 8192;  // G * tokens-per-split scores in LDS
+
+// Each lane owns an 8-element segment of a row; lanes_per_token lanes cover
+// one row. Loads are 16-byte vectors when the segment is whole.
+template <typename T>
+__device__ __forceinline__ void load_seg(const T* __restrict__ row, int off, int dim, bool vec,
+                                         float (&x)[8]);
+
+template <>
+__device__ __forceinline__ void load_seg<bf16_t>(const bf16_t* __restrict__ row, int off, int dim,
+                                                 bool vec, float (&x)[8]) {
+    if (vec) {
+        const uint4 u = *reinterpret_cast<const uint4*>(row + off);
+        const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            x[2 * j] = __uint_as_float(w4[j] << 16);
+            x[2 * j + 1] = __uint_as_float(w4[j] & 0xffff0000u);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = (off + j < dim) ? bf16_to_f32(row[off + j]) : 0.f;
+    }
+}
+
+template <>
+__device__ __forceinline__ void load_seg<float>(const float* __restrict__ row, int off, int dim,
+                                                bool vec, float (&x)[8]) {
+    if (vec) {
+        const float4 a = *reinterpret_cast<const float4*>(row + off);
+        const float4 b = *reinterpret_cast<const float4*>(row + off + 4);
+        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+        x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = (off + j < dim) ? row[off + j] : 0.f;
+    }
+}
+
+static __host__ __device__ inline int lanes_per_row(int dim) {
+    int lpt = 1;
+    while (lpt * 8 < dim) lpt <<= 1;
+    return lpt;
+}
+
+template <typename T, int G>
+__global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
+    const T* __restrict__ q, const T* __restrict__ wd, const T* __restrict__ wu,
+    const T* __restrict__ k_win, const T* __restrict__ v_win, const T* __restrict__ k_lat,
+    const T* __restrict__ v_lat, float* __restrict__ part, int Hq, int Hkv, int d, int dd, int w,
+    int cap, int len, int chunk_lat, int chunk_win, int n_lat_split, int S, float qscale) {
+    static_assert(4 * G * 256 <= kDecScoreSlots, "partial sums must fit in the score buffer");
+    __shared__ float qsh[G][256];
+    __shared__ float ssh[kDecScoreSlots];
+    __shared__ float mred[4][G];
+    // after pass 2 the score buffer holds the cross-wave partial sums
+    float (*red)[G][256] = reinterpret_cast<float (*)[G][256]>(ssh);
+
+    const int s = blockIdx.x;
+    const int bg = blockIdx.y;
+    const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63, wave = tid >> 6;
+    const int n_lat = imax(0, len - w);
+    const bool latent = s < n_lat_split;
+    const int dim = latent ? dd : d;
+    int t_begin, ntok;
+    if (latent) {
+        t_begin = s * chunk_lat;
+        ntok = imin(chunk_lat, n_lat - t_begin);
+    } else {
+        t_begin = n_lat + (s - n_lat_split) * chunk_win;
+        ntok = imin(chunk_win, len - t_begin);
+    }
+    const T* wdg = wd + (size_t)g * d * dd;
+    const T* wug = wu ? wu + (size_t)g * dd * d : nullptr;
+
+    // query (window region) or absorbed query q W_up^T (latent region),
+    // scaled by log2(e)/sqrt(d)
+    for (int idx = tid; idx < G * dim; idx += kDecThreads) {
+        const int hh = idx / dim, c = idx - (idx / dim) * dim;
+        const T* qrow = q + ((size_t)b * Hq + (size_t)g * G + hh) * d;
+        float acc;
+        if (latent) {
+            acc = 0.f;
+            for (int e = 0; e < d; ++e) {
+                const float u = wug ? elem<T>::load(wug + (size_t)c * d + e)
+                                    : elem<T>::load(wdg + (size_t)e * dd + c);
+                acc = __builtin_fmaf(elem<T>::load(qrow + e), u, acc);
+            }
+        } else {
+            acc = elem<T>::load(qrow + c);
+        }
+        qsh[hh][c] = acc * qscale;
+    }
+    __syncthreads();
+
+    const int lpt = lanes_per_row(dim);
+    const int sub = tid & (lpt - 1);
+    const int tpi = kDecThreads / lpt;  // tokens per block iteration
+    const int off = sub * 8;
+    const bool vec = (dim % 8) == 0 && off < dim;
+    float qreg[G][8];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) qreg[hh][j] = (off + j < dim) ? qsh[hh][off + j] : 0.f;
+
+    const T* kbase = latent ? k_lat + (size_t)bg * cap * dd : k_win + (size_t)bg * w * d;
+    const T* vbase = latent ? v_lat + (size_t)bg * cap * dd : v_win + (size_t)bg * w * d;
+    auto row_of = [&](const T* base, int t) -> const T* {
+        const int pos = t_begin + t;
+        return latent ? base + (size_t)pos * dd : base + (size_t)(pos % w) * d;
+    };
+
+    // pass 1: scores
+    float mloc[G];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) mloc[hh] = -INFINITY;
+    for (int t0 = 0; t0 < ntok; t0 += tpi) {
+        const int t = t0 + tid / lpt;
+        float x[8];
+        if (t < ntok) load_seg<T>(row_of(kbase, t), off, dim, vec, x);
+        else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) x[j] = 0.f;
+        }
+        float sc[G];
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) {
+            float a = 0.f;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) a = __builtin_fmaf(qreg[hh][j], x[j], a);
+            for (int o2 = 1; o2 < lpt; o2 <<= 1) a += __shfl_xor(a, o2, 64);
+            sc[hh] = a;
+        }
+        if (t < ntok) {
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) {
+                mloc[hh] = fmaxf(mloc[hh], sc[hh]);
+                if (sub == 0) ssh[hh * (kDecScoreSlots / G) + t] = sc[hh];
+            }
+        }
+    }
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) {
+        const float mw = wave_max(mloc[hh]);
+        if (lane == 0) mred[wave][hh] = mw;
+    }
+    __syncthreads();
+    float mx[G];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh)
+        mx[hh] = fmaxf(fmaxf(mred[0][hh], mred[1][hh]), fmaxf(mred[2][hh], mred[3][hh]));
+
+    // pass 2: values
+    float acc[G][8];
+    float lsum[G];
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) {
+        lsum[hh] = 0.f;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) acc[hh][j] = 0.f;
+    }
+    for (int t0 = 0; t0 < ntok; t0 += tpi) {
+        const int t = t0 + tid / lpt;
+        if (t < ntok) {
+            float x[8];
+            load_seg<T>(row_of(vbase, t), off, dim, vec, x);
+#pragma unroll
+            for (int hh = 0; hh < G; ++hh) {
+                const float p = exp2f(ssh[hh * (kDecScoreSlots / G) + t] - mx[hh]);
+                if (sub == 0) lsum[hh] += p;
+#pragma unroll
+                for (int j = 0; j < 8; ++j) acc[hh][j] = __builtin_fmaf(p, x[j], acc[hh][j]);
+            }
+        }
+    }
+    // reduce over the lanes that share a segment (same sub), then over waves
+#pragma unroll
+    for (int hh = 0; hh < G; ++hh) {
+        lsum[hh] = wave_sum(lsum[hh]);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            float a = acc[hh][j];
+            for (int o2 = lpt; o2 < 64; o2 <<= 1) a += __shfl_xor(a, o2, 64);
+            acc[hh][j] = a;
+        }
+    }
+    __syncthreads();  // scores and mred are reused below
+    if (lane < lpt) {
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh)
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                if (off + j < dim) red[wave][hh][off + j] = acc[hh][j];
+    }
+    if (lane == 0) {
+#pragma unroll
+        for (int hh = 0; hh < G; ++hh) mred[wave][hh] = lsum[hh];
+    }
+    __syncthreads();
+    const int stride = 2 + d;
+    for (int idx = tid; idx < G * (dim + 2); idx += kDecThreads) {
+        const int hh = idx / (dim + 2), f = idx - (idx / (dim + 2)) * (dim + 2);
+        float val;
+        if (f == 0) val = mx[hh];
+        else if (f == 1) val = mred[0][hh] + mred[1][hh] + mred[2][hh] + mred[3][hh];
+        else val = red[0][hh][f - 2] + red[1][hh][f - 2] + red[2][hh][f - 2] + red[3][hh][f - 2];
+        const size_t bh = (size_t)b * Hq + (size_t)g * G + hh;
+        part[(bh * S + s) * stride + f] = val;
+    }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void decode_combine_kernel(
+    const float* __restrict__ part, const T* __restrict__ wd, const T* __restrict__ wu,
+    T* __restrict__ o, int Hq, int Hkv, int d, int dd, int n_lat_split, int S) {
+    __shared__ float lat[256];
+    __shared__ float scale_s[1024];
+    __shared__ float inv_l;
+    const int bh = blockIdx.x;
+    const int h = bh % Hq;
+    const int g = h / (Hq / Hkv);
+    const int stride = 2 + d;
+    const float* pp = part + (size_t)bh * S * stride;
+    // global max and per-split weights (S <= 1024 is guaranteed by the host)
+    float mx = -INFINITY;
+    for (int s = 0; s < S; ++s) mx = fmaxf(mx, pp[(size_t)s * stride]);
+    for (int s = threadIdx.x; s < S; s += 256) scale_s[s] = exp2f(pp[(size_t)s * stride] - mx);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        float l = 0.f;
+        for (int s = 0; s < S; ++s) l += scale_s[s] * pp[(size_t)s * stride + 1];
+        inv_l = 1.f / l;
+    }
+    for (int c = threadIdx.x; c < dd; c += 256) {
+        float a = 0.f;
+        for (int s = 0; s < n_lat_split; ++s) a += scale_s[s] * pp[(size_t)s * stride + 2 + c];
+        lat[c] = a;
+    }
+    __syncthreads();
+    const T* wdg = wd + (size_t)g * d * dd;
+    const T* wug = wu ? wu + (size_t)g * dd * d : nullptr;
+    for (int e = threadIdx.x; e < d; e += 256) {
+        float a = 0.f;
+        for (int s = n_lat_split; s < S; ++s) a += scale_s[s] * pp[(size_t)s * stride + 2 + e];
+        if (n_lat_split > 0)
+            for (int c = 0; c < dd; ++c) {
+                const float u = wug ? elem<T>::load(wug + (size_t)c * d + e)
+                                    : elem<T>::load(wdg + (size_t)e * dd + c);
+                a = __builtin_fmaf(lat[c], u, a);
+            }
+        o[(size_t)bh * d + e] = elem<T>::from_f32(a * inv_l);
+    }
+}
+
+static int group_chunk(int G) { return kDecScoreSlots / G; }
+
+DecodeSplits decode_splits(int len, int w, int d, int dd, int G) {
+    DecodeSplits sp;
+    const int n_lat = len - w > 0 ? len - w : 0;
+    const int n_win = len - n_lat;
+    const int cmax = group_chunk(G);
+    // about 64 KB of keys+values per split in each region
+    int cl = 65536 / (4 * (dd > 0 ? dd : 1));
+    int cw = 65536 / (4 * d);
+    cl = cl < 64 ? 64 : (cl > cmax ? cmax : cl);
+    cw = cw < 64 ? 64 : (cw > cmax ? cmax : cw);
+    sp.chunk_lat = cl;
+    sp.chunk_win = cw;
+    sp.n_lat_split = (n_lat + cl - 1) / cl;
+    sp.n_win_split = (n_win + cw - 1) / cw;
+    return sp;
+}
+
+int decode_max_splits(int cap, int w, int d, int dd, int G) {
+    // the split count is largest when every cached token is latent, or when
+    // the window is full and the rest latent; take the sum of both bounds
+    DecodeSplits a = decode_splits(cap, w, d, dd, G);
+    DecodeSplits b = decode_splits(cap, 0, d, dd, G);
+    int m1 = a.n_lat_split + a.n_win_split;
+    int m2 = b.n_lat_split + b.n_win_split;
+    return (m1 > m2 ? m1 : m2) + 1;
+}
+
+template <typename T, int G>
+static hipError_t launch_decode_g(const T* q, const T* wd, const T* wu, const T* k_win,
+                                  const T* v_win, const T* k_lat, const T* v_lat, T* o,
+                                  float* part, int B, int Hq, int Hkv, int d, int dd, int w,
+                                  int cap, int len, hipStream_t st) {
+    DecodeSplits sp = decode_splits(len, w, d, dd, G);
+    const int S = sp.n_lat_split + sp.n_win_split;
+    const float qscale = 1.4426950408889634f / sqrtf((float)d);
+    hipLaunchKernelGGL((decode_split_kernel<T, G>), dim3(S, B * Hkv), dim3(kDecThreads), 0, st, q,
+                       wd, wu, k_win, v_win, k_lat, v_lat, part, Hq, Hkv, d, dd, w, cap, len,
+                       sp.chunk_lat, sp.chunk_win, sp.n_lat_split, S, qscale);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(256), 0, st, part, wd, wu, o,
+                       Hq, Hkv, d, dd, sp.n_lat_split, S);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
+                         const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
+                         int d, int dd, int w, int cap, int len, hipStream_t st) {
+    switch (Hq / Hkv) {
+        case 1: return launch_decode_g<T, 1>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
+        case 2: return launch_decode_g<T, 2>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
+        case 4: return launch_decode_g<T, 4>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
+        case 8: return launch_decode_g<T, 8>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
+        default: return hipErrorInvalidValue;
+    }
+}
+
+template hipError_t launch_decode<float>(const float*, const float*, const float*, const float*,
+                                         const float*, const float*, const float*, float*, float*,
+                                         int, int, int, int, int, int, int, int, hipStream_t);
+template hipError_t launch_decode<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
+                                          const bf16_t*, const bf16_t*, const bf16_t*,
+                                          const bf16_t*, bf16_t*, float*, int, int, int, int, int,
+                                          int, int, int, hipStream_t);
+
+}  // namespace dar

@@ -1,0 +1,150 @@
+"""The C ABI without a GPU: the library loads, exports every declared entry
+point, sizes workspaces, and rejects bad arguments before touching HIP.
+
+The rejection tests pass fake (never dereferenced) device addresses; they run
+only where no GPU is visible, so a validation bug can never hand such an
+address to a kernel.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+import torch
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dar.h")
+
+dar = pytest.importorskip("paper_2606_18587_amd", reason="libdar.so not built")
+
+no_gpu = pytest.mark.skipif(torch.cuda.is_available(),
+                            reason="fake device addresses are only used where no GPU exists")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dar_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol():
+    names = declared_functions()
+    assert set(names) == {"dar_attn_prefill", "dar_cache_append", "dar_attn_decode",
+                          "dar_prefill_workspace_bytes", "dar_decode_workspace_bytes",
+                          "dar_status_string"}
+    raw = ctypes.CDLL(dar.LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+
+
+def test_status_strings():
+    for st in range(6):
+        assert dar.status_string(st)
+    assert dar.status_string(99) == "unknown status"
+
+
+def S(B=2, Hq=4, Hkv=2, d=64, dd=16, w=8, dtype=torch.bfloat16):
+    return dar.make_shape(B, Hq, Hkv, d, dd, w, dtype)
+
+
+def test_prefill_workspace_size():
+    # two latent buffers, tokens [0, T-w) padded to 64, 256-byte aligned
+    s = S()
+    T = 100
+    Tp = 128
+    one = 2 * 2 * Tp * 16 * 2
+    assert dar.dar_prefill_workspace_bytes(s, T) == 2 * ((one + 255) // 256 * 256)
+    assert dar.dar_prefill_workspace_bytes(s, 8) == 0       # T <= w: no distant tokens
+    assert dar.dar_prefill_workspace_bytes(S(w=0, dtype=torch.float32), 64) == 2 * 2 * 2 * 64 * 16 * 4
+    assert dar.dar_prefill_workspace_bytes(S(Hq=3), 64) == 0   # invalid shape
+
+
+def test_decode_workspace_size_grows_with_capacity():
+    s = S()
+    a = dar.dar_decode_workspace_bytes(s, 1000)
+    b = dar.dar_decode_workspace_bytes(s, 100000)
+    assert 0 < a < b
+    assert a % (s.B * s.Hq * (2 + s.d) * 4) == 0
+    assert dar.dar_decode_workspace_bytes(S(Hq=12, Hkv=4), 100) == 0  # group of 3: unsupported
+
+
+FAKE = ctypes.c_void_p(1 << 20)       # aligned, never dereferenced
+MISALIGNED = ctypes.c_void_p((1 << 20) + 2)
+
+
+def call_prefill(shape, T=16, q=FAKE, k=FAKE, v=FAKE, wd=FAKE, wu=None, o=FAKE, ws=FAKE,
+                 ws_bytes=1 << 30):
+    return dar.lib.dar_attn_prefill(ctypes.byref(shape), T, q, k, v, wd, wu, o, ws, ws_bytes,
+                                    None)
+
+
+@no_gpu
+@pytest.mark.parametrize("kw,shape_kw,expect", [
+    ({}, {"Hq": 3}, dar.DAR_E_ARG),                 # Hq % Hkv != 0
+    ({}, {"dd": 65}, dar.DAR_E_ARG),                # d_down > d
+    ({}, {"w": -1}, dar.DAR_E_ARG),
+    ({}, {"B": 0}, dar.DAR_E_ARG),
+    ({}, {"d": 512, "dd": 16}, dar.DAR_E_UNSUPPORTED),
+    ({"T": 0}, {}, dar.DAR_E_ARG),
+    ({"q": None}, {}, dar.DAR_E_ARG),
+    ({"k": MISALIGNED}, {}, dar.DAR_E_ARG),
+    ({"wu": MISALIGNED}, {}, dar.DAR_E_ARG),
+    ({"ws": None, "ws_bytes": 0}, {}, dar.DAR_E_WORKSPACE),
+    ({"ws_bytes": 16}, {}, dar.DAR_E_WORKSPACE),
+])
+def test_prefill_rejects(kw, shape_kw, expect):
+    assert call_prefill(S(**shape_kw), **kw) == expect
+
+
+@no_gpu
+def test_prefill_bad_dtype():
+    s = S()
+    s.dtype = 7
+    assert call_prefill(s) == dar.DAR_E_ARG
+
+
+def cache_struct(cap=64, length=0, win=FAKE):
+    return dar.DarCacheStruct(win.value if win else None, win.value if win else None,
+                              FAKE.value, FAKE.value, cap, length)
+
+
+@no_gpu
+def test_append_capacity_and_arguments():
+    s = S()
+    c = cache_struct(cap=64, length=60)
+    st = dar.lib.dar_cache_append(ctypes.byref(s), ctypes.byref(c), FAKE, FAKE, 5, FAKE, None)
+    assert st == dar.DAR_E_CAPACITY and c.len == 60
+    st = dar.lib.dar_cache_append(ctypes.byref(s), ctypes.byref(c), FAKE, FAKE, 0, FAKE, None)
+    assert st == dar.DAR_E_ARG and c.len == 60
+    st = dar.lib.dar_cache_append(ctypes.byref(s), ctypes.byref(c), MISALIGNED, FAKE, 1, FAKE,
+                                  None)
+    assert st == dar.DAR_E_ARG and c.len == 60
+    c2 = cache_struct(win=None)  # a ring is required when w > 0
+    st = dar.lib.dar_cache_append(ctypes.byref(s), ctypes.byref(c2), FAKE, FAKE, 1, FAKE, None)
+    assert st == dar.DAR_E_ARG and c2.len == 0
+    c3 = cache_struct(cap=64, length=65)
+    st = dar.lib.dar_cache_append(ctypes.byref(s), ctypes.byref(c3), FAKE, FAKE, 1, FAKE, None)
+    assert st == dar.DAR_E_ARG
+
+
+@no_gpu
+def test_decode_rejects():
+    s = S()
+    need = dar.dar_decode_workspace_bytes(s, 64)
+    empty = cache_struct(cap=64, length=0)
+    st = dar.lib.dar_attn_decode(ctypes.byref(s), ctypes.byref(empty), FAKE, FAKE, None, FAKE,
+                                 FAKE, need, None)
+    assert st == dar.DAR_E_ARG  # nothing cached yet
+    c = cache_struct(cap=64, length=10)
+    st = dar.lib.dar_attn_decode(ctypes.byref(s), ctypes.byref(c), FAKE, FAKE, None, FAKE, FAKE,
+                                 need - 4, None)
+    assert st == dar.DAR_E_WORKSPACE
+    s3 = S(Hq=6, Hkv=2)
+    st = dar.lib.dar_attn_decode(ctypes.byref(s3), ctypes.byref(c), FAKE, FAKE, None, FAKE, FAKE,
+                                 1 << 30, None)
+    assert st == dar.DAR_E_UNSUPPORTED
+
+
+def test_python_binding_names_match_abi():
+    for n in declared_functions():
+        assert hasattr(dar, n), n

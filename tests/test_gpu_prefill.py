@@ -1,0 +1,137 @@
+"""GPU prefill parity: dar_attn_prefill (through the C ABI) against the fp64
+oracle on the same seeded inputs, element by element.
+
+Tolerance (max abs, unit-scale data): 1e-4 for fp32, 2e-2 for bf16 storage
+with fp32 accumulation.
+"""
+import numpy as np
+import pytest
+import torch
+
+import dar_inputs as di
+from oracle import oracle
+from tests.dev import to_dev, to_host64, tol
+
+pytestmark = pytest.mark.gpu
+
+dar = pytest.importorskip("paper_2606_18587_amd")
+
+
+def run_gpu(inp, w):
+    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
+    wd, wu = to_dev(inp["wd"]), to_dev(inp["wu"])
+    o = dar.dar_attn_prefill(q, k, v, wd, wu, w)
+    torch.cuda.synchronize()
+    return o
+
+
+def full_compare(wl, untied=False, seed_shift=0, q_scale=1.0):
+    inp = di.make_prefill_inputs(wl, untied=untied, seed_shift=seed_shift, q_scale=q_scale)
+    o = to_host64(run_gpu(inp, wl.w))
+    ref = oracle.prefill(inp["q"].f64, inp["k"].f64, inp["v"].f64, inp["wd"].f64,
+                         None if inp["wu"] is None else inp["wu"].f64, wl.w)
+    err = np.abs(o - ref)
+    assert np.isfinite(o).all()
+    assert err.max() <= tol(wl.dtype), "max abs err %.3g at %s" % (
+        err.max(), np.unravel_index(err.argmax(), err.shape))
+    return err.max()
+
+
+def test_tiny_fp32_workload():
+    full_compare(di.WORKLOADS["tiny"])
+
+
+@pytest.mark.parametrize("w", [0, 1, 8, 63, 64, 65, 200])
+def test_tiny_fp32_window_sweep(w):
+    full_compare(di.WORKLOADS["tiny"].with_(w=w, T=100, B=2, Hq=4, Hkv=2), untied=(w % 2 == 1))
+
+
+BF16_SMALL = di.Workload("bf16_small", 10, 1, 4, 2, 300, 64, 16, 128, "bf16")
+
+
+@pytest.mark.parametrize("w", [0, 1, 16, 64, 128, 129, 299, 300, 1000])
+@pytest.mark.parametrize("untied", [False, True])
+def test_bf16_d64_window_sweep(w, untied):
+    full_compare(BF16_SMALL.with_(w=w), untied=untied)
+
+
+@pytest.mark.parametrize("T", [1, 2, 61, 127, 128, 129, 257, 500])
+def test_bf16_d64_ragged_lengths(T):
+    full_compare(BF16_SMALL.with_(T=T, w=32, B=2))
+
+
+@pytest.mark.parametrize("w", [0, 64, 100, 512])
+def test_bf16_d128_gqa(w):
+    full_compare(di.Workload("bf16_d128", 11, 1, 8, 2, 400, 128, 32, w, "bf16"), untied=(w == 100))
+
+
+@pytest.mark.parametrize("d,dd,w,T", [(64, 32, 40, 333), (128, 16, 77, 290), (64, 16, 33, 97)])
+@pytest.mark.parametrize("untied", [False, True])
+def test_bf16_other_matrix_core_shapes(d, dd, w, T, untied):
+    full_compare(di.Workload("bf16_mixed", 13, 2, 4, 1, T, d, dd, w, "bf16"), untied=untied)
+
+
+def test_bf16_peaky_queries():
+    # queries scaled by 4: sharp softmax rows, large running-max changes
+    full_compare(BF16_SMALL.with_(w=64, T=400), q_scale=4.0)
+
+
+@pytest.mark.parametrize("shape", [(1, 3, 1, 90, 48, 12, 10), (2, 2, 2, 70, 32, 32, 5),
+                                   (1, 2, 1, 50, 256, 64, 7)])
+def test_generic_shapes(shape):
+    B, Hq, Hkv, T, d, dd, w = shape
+    for dt in ("f32", "bf16"):
+        full_compare(di.Workload("generic", 12, B, Hq, Hkv, T, d, dd, w, dt), untied=True)
+
+
+def test_deterministic():
+    inp = di.make_prefill_inputs(BF16_SMALL)
+    a = run_gpu(inp, BF16_SMALL.w)
+    b = run_gpu(inp, BF16_SMALL.w)
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_gqa_equals_repeated_mha():
+    wl = BF16_SMALL.with_(Hq=4, Hkv=2, T=200, w=50)
+    inp = di.make_prefill_inputs(wl, untied=True)
+    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
+    wd, wu = to_dev(inp["wd"]), to_dev(inp["wu"])
+    o1 = dar.dar_attn_prefill(q, k, v, wd, wu, wl.w)
+    rep = lambda x: x.repeat_interleave(2, dim=0 if x.dim() == 3 else 1).contiguous()
+    o2 = dar.dar_attn_prefill(q, rep(k), rep(v), rep(wd), rep(wu), wl.w)
+    torch.cuda.synchronize()
+    assert (o1.float() - o2.float()).abs().max().item() <= 2e-2
+
+
+# ---------------------------------------------------------------- full sizes
+
+def sample_rows(T, w, rng, n_random=6):
+    rows = {0, 1, T - 1, T - 2}
+    for x in (w - 1, w, w + 1, 2 * w, T // 2):
+        if 0 <= x < T:
+            rows.add(x)
+    rows.update(int(r) for r in rng.integers(0, T, n_random))
+    return np.array(sorted(rows))
+
+
+@pytest.mark.parametrize("name", ["pythia70m", "pythia410m_w128", "pythia410m_w512", "long16k"])
+def test_full_size_sampled_rows(name):
+    wl = di.WORKLOADS[name]
+    inp = di.make_prefill_inputs(wl)
+    o = run_gpu(inp, wl.w)
+    rng = np.random.Generator(np.random.PCG64(7))
+    rows = sample_rows(wl.T, wl.w, rng)
+    grp = wl.Hq // wl.Hkv
+    worst = 0.0
+    pairs = {(0, 0), (wl.B - 1, wl.Hq - 1)}
+    pairs.add((int(rng.integers(wl.B)), int(rng.integers(wl.Hq))))
+    for b, h in sorted(pairs):
+        g = h // grp
+        ref = oracle.rows(inp["k"].f64[b, g], inp["v"].f64[b, g], inp["wd"].f64[g], None, wl.w,
+                          rows, inp["q"].f64[b, h, rows])
+        got = to_host64(o[b, h, torch.from_numpy(rows).to(o.device)])
+        worst = max(worst, float(np.abs(got - ref).max()))
+    assert worst <= tol(wl.dtype), worst
+    # properties at every row: finite, and a convex combination bound
+    of = o.float()
+    assert torch.isfinite(of).all()
