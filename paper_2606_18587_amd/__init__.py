@@ -39,7 +39,7 @@ class DarError(RuntimeError):
 
 def _load():
     if not os.path.exists(LIB_PATH):
-        raise ImportError("libdar.so is not built; run `python -m paper_2606_18587_amd.build` "
+        raise ImportError("libdar.so is not built; run `python paper_2606_18587_amd/build.py` "
                           "(there is no non-HIP fallback)")
     lib = ctypes.CDLL(LIB_PATH)
     vp, sz, ci = ctypes.c_void_p, ctypes.c_size_t, ctypes.c_int

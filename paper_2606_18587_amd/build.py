@@ -1,7 +1,9 @@
 """Build libdar.so (all HIP kernels + the C ABI) for gfx950 with hipcc.
 
-Usage: python -m paper_2606_18587_amd.build   (or build() from Python)
-The library is built in-tree, next to this file.
+Usage: python paper_2606_18587_amd/build.py [-v]
+This file is run as a script (or loaded by path) rather than imported as part
+of the package: importing the package needs the library it builds. The
+library is built in-tree, next to this file.
 """
 from __future__ import annotations
 
@@ -20,6 +22,12 @@ HIPCC_FLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC",
     # no packed-fp32 instructions in device code
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # MFMA accumulators in ordinary VGPRs (no AGPR round trips next to the
+    # softmax VALU work)
+    "-mllvm", "-amdgpu-mfma-vgpr-form",
+    # no NaN inputs are produced or expected (masked scores are -inf): run with
+    # IEEE mode off so min/max need no quieting of their operands
+    "-mno-amdgpu-ieee", "-fno-honor-nans",
     "-I", os.path.join(ROOT, "include"),
 ]
 

@@ -10,15 +10,16 @@
 namespace dar {
 
 PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize) {
-    PrefillWs ws{0, 0, 0};
-    const int Tl = T - w;
-    if (Tl <= 0) return ws;
-    const size_t Tp = (size_t)round_up(Tl, 64);
-    const size_t one = (size_t)B * Hkv * Tp * dd * esize;
-    const size_t one_al = (one + 255) & ~(size_t)255;
+    PrefillWs ws{0, 0, 0, 0, 0};
+    const size_t Tp = (size_t)prefill_tp(T, w);
+    if (Tp == 0) return ws;
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t one = al((size_t)B * Hkv * Tp * dd * esize);
     ws.ck_off = 0;
-    ws.cv_off = one_al;
-    ws.bytes = 2 * one_al;
+    ws.cv_off = one;
+    ws.norm_off = 2 * one;
+    ws.const_off = ws.norm_off + al((size_t)B * Hkv * (Tp / 32) * sizeof(float));
+    ws.bytes = ws.const_off + 256;
     return ws;
 }
 
@@ -27,7 +28,8 @@ PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize) 
 bool prefill_mfma_supported(const dar_shape* s);
 hipError_t launch_prefill_mfma(const dar_shape* s, int T, const void* q, const void* k,
                                const void* v, const void* wd, const void* wu, void* o,
-                               const void* cK, const void* cVt, hipStream_t st);
+                               const void* cK, const void* cVt, const float* cnorm,
+                               const void* consts, hipStream_t st);
 
 }  // namespace dar
 
@@ -113,6 +115,8 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
     char* wsb = (char*)ws;
     const void* cK = L.bytes ? wsb + L.ck_off : nullptr;
     const void* cV = L.bytes ? wsb + L.cv_off : nullptr;
+    void* consts = L.bytes ? wsb + L.const_off : nullptr;
+    float* cnorm = L.bytes ? (float*)(wsb + L.norm_off) : nullptr;
     hipError_t e = hipSuccess;
     const bool fast = prefill_mfma_supported(s);
     if (log_enabled())
@@ -121,11 +125,12 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
                 fast ? "mfma" : "valu");
     if (s->dtype == DAR_BF16) {
         e = launch_prefill_latent<bf16_t>((const bf16_t*)k, (const bf16_t*)v,
-                                          (const bf16_t*)w_down, (bf16_t*)cK, (bf16_t*)cV, s->B,
-                                          s->Hkv, T, s->d, s->d_down, s->w, fast, stream);
+                                          (const bf16_t*)w_down, (bf16_t*)cK, (bf16_t*)cV, cnorm,
+                                          (bf16_t*)consts, s->B, s->Hkv, T, s->d, s->d_down, s->w,
+                                          fast, stream);
         if (e == hipSuccess) {
             if (fast)
-                e = launch_prefill_mfma(s, T, q, k, v, w_down, w_up, o, cK, cV, stream);
+                e = launch_prefill_mfma(s, T, q, k, v, w_down, w_up, o, cK, cV, cnorm, consts, stream);
             else
                 e = launch_prefill_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k,
                                                 (const bf16_t*)v, (const bf16_t*)w_down,
@@ -135,8 +140,8 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
         }
     } else {
         e = launch_prefill_latent<float>((const float*)k, (const float*)v, (const float*)w_down,
-                                         (float*)cK, (float*)cV, s->B, s->Hkv, T, s->d,
-                                         s->d_down, s->w, false, stream);
+                                         (float*)cK, (float*)cV, cnorm, (float*)consts, s->B,
+                                         s->Hkv, T, s->d, s->d_down, s->w, false, stream);
         if (e == hipSuccess)
             e = launch_prefill_valu<float>((const float*)q, (const float*)k, (const float*)v,
                                            (const float*)w_down, (const float*)w_up,

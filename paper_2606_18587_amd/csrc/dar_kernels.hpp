@@ -12,13 +12,22 @@ typedef uint16_t bf16_t;
 
 static inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 
-// Prefill workspace: latents of tokens [0, T - w) per (batch, KV head),
-// token count padded to Tp = round_up(T - w, 64):
-//   cK  [B*Hkv][Tp][dd]            token-major
-//   cVt [B*Hkv][Tp/64][dd][64]     64-token blocks, transposed inside a block
+// Prefill workspace: latents of tokens [0, T - w) per (batch, KV head). The
+// token count is padded to Tp = round_up(T - w, 32) + 64 (the padding rows
+// are zero, so readers may prefetch two 32-token subtiles past the end):
+//   cK     [B*Hkv][Tp][dd]            token-major
+//   cVt    [B*Hkv][Tp/32][dd][32]     32-token blocks, transposed in a block
+//   cnorm  [B*Hkv][Tp/32] fp32        max L2 norm of the stored c^K rows of each
+//                                     32-token block (matrix-core path only)
+//   consts 256 bytes; starts with 8 bf16 ones then 8 bf16 zeros (operand rows
+//          of the matrix-core kernel that carry no latent column)
 struct PrefillWs {
-    size_t ck_off, cv_off, bytes;
+    size_t ck_off, cv_off, norm_off, const_off, bytes;
 };
+static inline int prefill_tp(int T, int w) {
+    const int Tl = T - w;
+    return Tl > 0 ? round_up(Tl, 32) + 64 : 0;
+}
 PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize);
 
 // Decode workspace: per (batch, query head, split) partial softmax state
@@ -31,8 +40,9 @@ DecodeSplits decode_splits(int len, int w, int d, int dd, int G);
 int decode_max_splits(int cap, int w, int d, int dd, int G);
 
 template <typename T>
-hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt, int B,
-                                 int Hkv, int T_, int d, int dd, int w, bool perm, hipStream_t st);
+hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt,
+                                 float* cnorm, T* consts, int B, int Hkv, int T_, int d, int dd,
+                                 int w, bool perm, hipStream_t st);
 
 template <typename T>
 hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, T* v_win,

@@ -17,7 +17,7 @@ namespace dar {
 // share the 2*dd output columns (K and V) in chunks of 8.
 //   cK:  [B*Hkv][Tp][dd]               token-major (columns in latent_pos order
 //                                       when perm is set)
-//   cVt: [B*Hkv][Tp/64][dd][64]        64-token blocks, transposed inside
+//   cVt: [B*Hkv][Tp/32][dd][32]        32-token blocks, transposed inside
 // Rows [Tl, Tp) are written as zeros.
 template <typename T>
 __global__ __launch_bounds__(256) void prefill_latent_kernel(
@@ -65,10 +65,10 @@ __global__ __launch_bounds__(256) void prefill_latent_kernel(
                     if (c0 + j < dd)
                         out[perm ? latent_pos(c0 + j) : c0 + j] = elem<T>::from_f32(acc[j]);
             } else {
-                T* out = cVt + ((size_t)bg * Tp + (size_t)(t >> 6) * 64) * dd;
+                T* out = cVt + ((size_t)bg * Tp + (size_t)(t >> 5) * 32) * dd;
 #pragma unroll
                 for (int j = 0; j < 8; ++j)
-                    if (c0 + j < dd) out[(size_t)(c0 + j) * 64 + (t & 63)] = elem<T>::from_f32(acc[j]);
+                    if (c0 + j < dd) out[(size_t)(c0 + j) * 32 + (t & 31)] = elem<T>::from_f32(acc[j]);
             }
         }
     }
@@ -157,13 +157,183 @@ __global__ __launch_bounds__(256) void append_kernel(
     }
 }
 
+// ---------------------------------------------------------------------------
+// Matrix-core projection for bf16 (d % 16 == 0, d_down <= 32). Per group of 32
+// tokens, latent^T = W_down^T x^T with v_mfma_f32_32x32x16_bf16: A = W_down^T
+// (row = latent column c, k = e), B = x^T (column = token, k = e, a 16-byte
+// load from the token's row). The accumulator of lane l holds token l%32 and
+// latent columns c = 8*(r/4) + 4*(l/32) + r%4 for register r. A token's
+// latent depends only on its own row and W_down, and every bf16 path (prefill
+// pre-pass, bulk and single-token append) runs this same instruction
+// sequence, so their latents are bit-identical.
+typedef __bf16 lbf16x8 __attribute__((ext_vector_type(8)));
+typedef float lf32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ lbf16x8 lload8(const bf16_t* p) {
+    return __builtin_bit_cast(lbf16x8, *reinterpret_cast<const uint4*>(p));
+}
+
+template <int D>
+__device__ __forceinline__ void load_wd_operand(const bf16_t* __restrict__ wdg, int dd, int lane,
+                                                lbf16x8 (&wa)[D / 16]) {
+    const int c = lane & 31, hg = lane >> 5;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) {
+        uint16_t t8[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) t8[j] = (c < dd) ? wdg[(size_t)(s * 16 + hg * 8 + j) * dd + c] : 0;
+        wa[s] = __builtin_bit_cast(lbf16x8, t8);
+    }
+}
+
+template <int D>
+__device__ __forceinline__ lf32x16 project_mfma(const lbf16x8 (&wa)[D / 16], const lbf16x8 (&x)[D / 16]) {
+    lf32x16 acc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+#pragma unroll
+    for (int s = 0; s < D / 16; ++s) acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(wa[s], x[s], acc, 0, 0, 0);
+    return acc;
+}
+
+__device__ __forceinline__ int acc_col(int r, int hg) { return 8 * (r >> 2) + 4 * hg + (r & 3); }
+
+// Prefill pre-pass, one wavefront per 32 tokens, 4 wavefronts per block.
+// Also writes, per 32-token block, the largest L2 norm of the stored c^K rows
+// (the matrix-core prefill bounds its distant scores with it).
+template <int D>
+__global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
+    const bf16_t* __restrict__ k, const bf16_t* __restrict__ v, const bf16_t* __restrict__ wd,
+    bf16_t* __restrict__ cK, bf16_t* __restrict__ cVt, float* __restrict__ cnorm,
+    bf16_t* __restrict__ consts, int Hkv, int T_, int dd, int Tl, int Tp, int perm) {
+    constexpr int KS = D / 16;
+    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < 16)
+        consts[threadIdx.x] = threadIdx.x < 8 ? (bf16_t)0x3f80 : (bf16_t)0;
+    const int bg = blockIdx.y;
+    const int g = bg % Hkv;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int tl = lane & 31, hg = lane >> 5;
+    const int t = blockIdx.x * 128 + wave * 32 + tl;
+    if (blockIdx.x * 128 + wave * 32 >= Tp) return;
+    lbf16x8 wa[KS];
+    load_wd_operand<D>(wd + (size_t)g * D * dd, dd, lane, wa);
+    for (int which = 0; which < 2; ++which) {
+        const bf16_t* xr = (which ? v : k) + ((size_t)bg * T_ + (t < Tl ? t : 0)) * D;
+        lbf16x8 x[KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s) {
+            x[s] = lload8(xr + s * 16 + hg * 8);
+            if (t >= Tl) x[s] = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
+        }
+        const lf32x16 acc = project_mfma<D>(wa, x);
+        if (which == 0) {
+            // squared norm of the rounded latent, both halves of the wavefront
+            float n2 = 0.f;
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                if (acc_col(r, hg) < dd) {
+                    const float cr = bf16_to_f32(f32_to_bf16(acc[r]));
+                    n2 = __builtin_fmaf(cr, cr, n2);
+                }
+            n2 += __shfl_xor(n2, 32, 64);
+            const float nmax = wave_max(n2);
+            if (lane == 0) cnorm[(size_t)bg * (Tp / 32) + (t >> 5)] = sqrtf(nmax);
+            bf16_t* out = cK + ((size_t)bg * Tp + t) * dd;
+            if (perm) {
+                // latent_pos order: positions 16s + 8hg + j hold registers 8s + j
+#pragma unroll
+                for (int s = 0; s < 2; ++s)
+                    if (16 * s < dd) {
+                        uint4 u;
+                        u.x = (uint32_t)f32_to_bf16(acc[8 * s + 0]) | ((uint32_t)f32_to_bf16(acc[8 * s + 1]) << 16);
+                        u.y = (uint32_t)f32_to_bf16(acc[8 * s + 2]) | ((uint32_t)f32_to_bf16(acc[8 * s + 3]) << 16);
+                        u.z = (uint32_t)f32_to_bf16(acc[8 * s + 4]) | ((uint32_t)f32_to_bf16(acc[8 * s + 5]) << 16);
+                        u.w = (uint32_t)f32_to_bf16(acc[8 * s + 6]) | ((uint32_t)f32_to_bf16(acc[8 * s + 7]) << 16);
+                        *reinterpret_cast<uint4*>(out + 16 * s + 8 * hg) = u;
+                    }
+            } else {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int c = acc_col(r, hg);
+                    if (c < dd) out[c] = f32_to_bf16(acc[r]);
+                }
+            }
+        } else {
+            bf16_t* out = cVt + ((size_t)bg * Tp + (size_t)(t >> 5) * 32) * dd + (t & 31);
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int c = acc_col(r, hg);
+                if (c < dd) out[(size_t)c * 32] = f32_to_bf16(acc[r]);
+            }
+        }
+    }
+}
+
+// Cache append for bf16 with the matrix-core projection. One wavefront per 32
+// new tokens of one (batch, KV head); modes as in append_kernel. The lane that
+// reads elements [16s + 8hg, +8) of the token leaving ring slot p % w is the
+// lane that writes the same elements of the new token into that slot, after
+// its read, so mode 0 needs no barrier.
+template <int D>
+__global__ __launch_bounds__(64) void append_mfma_kernel(
+    const bf16_t* __restrict__ k_new, const bf16_t* __restrict__ v_new, const bf16_t* __restrict__ wd,
+    bf16_t* k_win, bf16_t* v_win, bf16_t* __restrict__ k_lat, bf16_t* __restrict__ v_lat, int Hkv,
+    int dd, int w, int cap, int len, int n, int mode) {
+    constexpr int KS = D / 16;
+    const int bg = blockIdx.y;
+    const int g = bg % Hkv;
+    const int lane = threadIdx.x;
+    const int tl = lane & 31, hg = lane >> 5;
+    const int tt = blockIdx.x * 32 + tl;      // new token index
+    const int ex = len + tt - w;              // position leaving the window
+    const bool valid = tt < n;
+    const bool project = mode != 2 && valid && ex >= 0;
+    const bool to_ring = mode != 1 && valid && w > 0 && tt >= n - w;
+    lbf16x8 wa[KS];
+    if (mode != 2) load_wd_operand<D>(wd + (size_t)g * D * dd, dd, lane, wa);
+    for (int which = 0; which < 2; ++which) {
+        const bf16_t* src_new = (which ? v_new : k_new) + (size_t)bg * n * D;
+        bf16_t* ring = (which ? v_win : k_win) + (size_t)bg * w * D;
+        if (mode != 2) {
+            const bf16_t* row = src_new;
+            if (project) row = (ex < len) ? ring + (size_t)(ex % w) * D : src_new + (size_t)(ex - len) * D;
+            lbf16x8 x[KS];
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                x[s] = lload8(row + s * 16 + hg * 8);
+                if (!project) x[s] = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
+            }
+            const lf32x16 acc = project_mfma<D>(wa, x);
+            if (project) {
+                bf16_t* out = (which ? v_lat : k_lat) + ((size_t)bg * cap + ex) * dd;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int c = acc_col(r, hg);
+                    if (c < dd) out[c] = f32_to_bf16(acc[r]);
+                }
+            }
+        }
+        if (to_ring) {
+            const bf16_t* src = src_new + (size_t)tt * D;
+            bf16_t* dst = ring + (size_t)((len + tt) % w) * D;
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                *reinterpret_cast<uint4*>(dst + s * 16 + hg * 8) = *reinterpret_cast<const uint4*>(src + s * 16 + hg * 8);
+        }
+    }
+}
+
+static bool mfma_projection(int d, int dd) { return (d == 64 || d == 128) && dd <= 32; }
+
 template <typename T>
-hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt, int B,
-                                 int Hkv, int T_, int d, int dd, int w, bool perm, hipStream_t st) {
+static hipError_t launch_prefill_latent_valu(const T* k, const T* v, const T* wd, T* cK, T* cVt,
+                                             int B, int Hkv, int T_, int d, int dd, int w,
+                                             bool perm, hipStream_t st) {
     const int Tl = T_ - w;
     if (Tl <= 0) return hipSuccess;
-    const int Tp = round_up(Tl, 64);
-    dim3 grid(Tp / 64, B * Hkv);
+    const int Tp = prefill_tp(T_, w);
+    dim3 grid((Tp + 63) / 64, B * Hkv);
     const size_t lds = sizeof(float) * 2 * 64 * (d + 1);
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute((const void*)prefill_latent_kernel<T>,
@@ -176,9 +346,9 @@ hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* 
 }
 
 template <typename T>
-hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, T* v_win,
-                         T* k_lat, T* v_lat, int B, int Hkv, int d, int dd, int w, int cap, int len,
-                         int n, hipStream_t st) {
+static hipError_t launch_append_valu(const T* k_new, const T* v_new, const T* wd, T* k_win,
+                                     T* v_win, T* k_lat, T* v_lat, int B, int Hkv, int d, int dd,
+                                     int w, int cap, int len, int n, hipStream_t st) {
     dim3 grid((n + 63) / 64, B * Hkv);
     const size_t lds = sizeof(float) * 2 * 64 * (d + 1);
     if (lds > 65536) {
@@ -200,17 +370,64 @@ hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, 
     return hipGetLastError();
 }
 
+template <>
+hipError_t launch_prefill_latent<bf16_t>(const bf16_t* k, const bf16_t* v, const bf16_t* wd,
+                                         bf16_t* cK, bf16_t* cVt, float* cnorm, bf16_t* consts,
+                                         int B, int Hkv, int T_, int d, int dd, int w, bool perm,
+                                         hipStream_t st) {
+    const int Tl = T_ - w;
+    if (Tl <= 0) return hipSuccess;
+    const int Tp = prefill_tp(T_, w);
+    if (!mfma_projection(d, dd)) return launch_prefill_latent_valu<bf16_t>(k, v, wd, cK, cVt, B, Hkv, T_, d, dd, w, perm, st);
+    dim3 grid((Tp + 127) / 128, B * Hkv);
+    if (d == 64)
+        hipLaunchKernelGGL(prefill_latent_mfma_kernel<64>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, consts, Hkv, T_, dd, Tl, Tp, perm ? 1 : 0);
+    else
+        hipLaunchKernelGGL(prefill_latent_mfma_kernel<128>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, consts, Hkv, T_, dd, Tl, Tp, perm ? 1 : 0);
+    return hipGetLastError();
+}
+
+template <>
+hipError_t launch_append<bf16_t>(const bf16_t* k_new, const bf16_t* v_new, const bf16_t* wd,
+                                 bf16_t* k_win, bf16_t* v_win, bf16_t* k_lat, bf16_t* v_lat, int B,
+                                 int Hkv, int d, int dd, int w, int cap, int len, int n,
+                                 hipStream_t st) {
+    if (!mfma_projection(d, dd))
+        return launch_append_valu<bf16_t>(k_new, v_new, wd, k_win, v_win, k_lat, v_lat, B, Hkv, d, dd, w, cap, len, n, st);
+    dim3 grid((n + 31) / 32, B * Hkv);
+    auto kern = (d == 64) ? append_mfma_kernel<64> : append_mfma_kernel<128>;
+    if (n <= w || w == 0) {
+        hipLaunchKernelGGL(kern, grid, dim3(64), 0, st, k_new, v_new, wd, k_win, v_win, k_lat, v_lat, Hkv, dd, w, cap, len, n, 0);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(kern, grid, dim3(64), 0, st, k_new, v_new, wd, k_win, v_win, k_lat, v_lat, Hkv, dd, w, cap, len, n, 1);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, grid, dim3(64), 0, st, k_new, v_new, wd, k_win, v_win, k_lat, v_lat, Hkv, dd, w, cap, len, n, 2);
+    return hipGetLastError();
+}
+
+template <typename T>
+hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt,
+                                 float* cnorm, T* consts, int B, int Hkv, int T_, int d, int dd,
+                                 int w, bool perm, hipStream_t st) {
+    (void)cnorm;   // only the matrix-core prefill reads the norms
+    (void)consts;  // and the constant rows
+    return launch_prefill_latent_valu<T>(k, v, wd, cK, cVt, B, Hkv, T_, d, dd, w, perm, st);
+}
+
+template <typename T>
+hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, T* v_win,
+                         T* k_lat, T* v_lat, int B, int Hkv, int d, int dd, int w, int cap, int len,
+                         int n, hipStream_t st) {
+    return launch_append_valu<T>(k_new, v_new, wd, k_win, v_win, k_lat, v_lat, B, Hkv, d, dd, w, cap, len, n, st);
+}
+
 template hipError_t launch_prefill_latent<float>(const float*, const float*, const float*, float*,
-                                                 float*, int, int, int, int, int, int, bool,
-                                                 hipStream_t);
-template hipError_t launch_prefill_latent<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
-                                                  bf16_t*, bf16_t*, int, int, int, int, int, int,
-                                                  bool, hipStream_t);
+                                                 float*, float*, float*, int, int, int, int, int,
+                                                 int, bool, hipStream_t);
 template hipError_t launch_append<float>(const float*, const float*, const float*, float*, float*,
                                          float*, float*, int, int, int, int, int, int, int, int,
                                          hipStream_t);
-template hipError_t launch_append<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*, bf16_t*,
-                                          bf16_t*, bf16_t*, bf16_t*, int, int, int, int, int, int,
-                                          int, int, hipStream_t);
 
 }  // namespace dar

@@ -48,6 +48,7 @@ typedef __attribute__((address_space(3))) s16x4_t lds_s16x4_t;
 
 static constexpr float kTau = 8.0f;
 
+
 __device__ __forceinline__ bf16x8_t load_bf16x8(const bf16_t* p) {
     return __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(p));
 }
@@ -68,11 +69,17 @@ __device__ __forceinline__ bf16x8_t pack8(float a0, float a1, float a2, float a3
     return __builtin_bit_cast(bf16x8_t, make_uint4(pack2(a0, a1), pack2(a2, a3), pack2(a4, a5), pack2(a6, a7)));
 }
 
-// value of lane l ^ 32
-__device__ __forceinline__ float swap32(float x) {
+// Combine lane l with lane l ^ 32. After the swap one result holds the lane's
+// own value and the other its partner's, in an order that depends on the
+// half, so max and sum can use both without a select.
+__device__ __forceinline__ float pair_max(float x) {
     auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    // lanes 0-31 receive the upper half in r[1], lanes 32-63 the lower half in r[0]
-    return (threadIdx.x & 32) ? __uint_as_float(r[0]) : __uint_as_float(r[1]);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+__device__ __forceinline__ float pair_sum(float x) {
+    auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
 __device__ __forceinline__ f32x16_t mfma(bf16x8_t a, bf16x8_t b, f32x16_t c) {
@@ -96,10 +103,37 @@ __device__ __forceinline__ int perm_row(int R) {
     return 16 * (a >> 1) + 8 * gg + 4 * (a & 1) + b;
 }
 
+// p = exp2(x) for the 16 scores, packed to bf16 as the two P^T operands; with
+// SUM_VALU the bf16-rounded p are also added to the row sum l.
+template <bool SUM_VALU>
+__device__ __forceinline__ void exp_pack(const f32x16_t& x, float& l, bf16x8_t& p0, bf16x8_t& p1) {
+    float p[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(x[r]);
+    p0 = pack8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
+    p1 = pack8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
+    if (SUM_VALU) {
+        const bf16x2_t one2 = {(__bf16)1.0f, (__bf16)1.0f};
+        const uint4 u0 = __builtin_bit_cast(uint4, p0), u1 = __builtin_bit_cast(uint4, p1);
+        float s = l;
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u0.x), one2, s, false);
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u0.y), one2, s, false);
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u0.z), one2, s, false);
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u0.w), one2, s, false);
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u1.x), one2, s, false);
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u1.y), one2, s, false);
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u1.z), one2, s, false);
+        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u1.w), one2, s, false);
+        l = s;
+    }
+}
+
 struct SoftmaxState {
-    float m;    // reference (scaled log2 units); -inf until the row has seen a key
-    float cm;   // -m, or 0 while m is -inf
-    float l;    // partial row sum of this lane (bf16-rounded p)
+    float m;       // reference (scaled log2 units); -inf until the row has seen a key
+    float cm;      // -m, or 0 while m is -inf
+    float thr;     // a subtile maximum above thr moves m: -inf until m is set, then kTau
+    float l;       // partial row sum of this lane (bf16-rounded p)
+    f32x16_t cmv;  // cm in every register: the accumulator input of distant S^T
 };
 
 // One 32-key subtile of the online softmax on x[16] (already relative to the
@@ -112,10 +146,10 @@ __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x
     mx = fmaxf(fmaxf(mx, x[8]), fmaxf(x[9], x[10]));
     mx = fmaxf(fmaxf(mx, x[11]), fmaxf(x[12], x[13]));
     mx = fmaxf(fmaxf(mx, x[14]), x[15]);
-    mx = fmaxf(mx, swap32(mx));
-    const bool fresh = st.m == -INFINITY;
-    const bool need = fresh ? (mx > -INFINITY) : (mx > kTau);
+    mx = pair_max(mx);
+    const bool need = mx > st.thr;
     if (__builtin_amdgcn_ballot_w64(need)) {
+        const bool fresh = st.m == -INFINITY;
         const float delta = need ? mx : 0.f;
         const float fac = need ? (fresh ? 0.f : exp2f(-delta)) : 1.f;
 #pragma unroll
@@ -127,36 +161,22 @@ __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x
         st.l *= fac;
         if (need) st.m = fresh ? mx : st.m + delta;
         st.cm = (st.m == -INFINITY) ? 0.f : -st.m;
+        st.thr = (st.m == -INFINITY) ? -INFINITY : kTau;
+        st.cmv = splat16(st.cm);
 #pragma unroll
         for (int r = 0; r < 16; ++r) x[r] -= delta;
     }
-    float p[16];
-#pragma unroll
-    for (int r = 0; r < 16; ++r) p[r] = __builtin_amdgcn_exp2f(x[r]);
-    p0 = pack8(p[0], p[1], p[2], p[3], p[4], p[5], p[6], p[7]);
-    p1 = pack8(p[8], p[9], p[10], p[11], p[12], p[13], p[14], p[15]);
-    if (SUM_VALU) {
-        const bf16x2_t one2 = {(__bf16)1.0f, (__bf16)1.0f};
-        const uint4 u0 = __builtin_bit_cast(uint4, p0), u1 = __builtin_bit_cast(uint4, p1);
-        float s = st.l;
-        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u0.x), one2, s, false);
-        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u0.y), one2, s, false);
-        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u0.z), one2, s, false);
-        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u0.w), one2, s, false);
-        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u1.x), one2, s, false);
-        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u1.y), one2, s, false);
-        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u1.z), one2, s, false);
-        s = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, u1.w), one2, s, false);
-        st.l = s;
-    }
+    exp_pack<SUM_VALU>(x, st.l, p0, p1);
 }
 
 template <int D, int DD, int NW>
-__global__ __launch_bounds__(NW * 64) void prefill_mfma_kernel(
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void prefill_mfma_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu, const bf16_t* __restrict__ cK,
-    const bf16_t* __restrict__ cVt, bf16_t* __restrict__ o, int Hq, int Hkv, int T, int w, int Tp,
-    int nblk, int BH, float c_scale) {
+    const bf16_t* __restrict__ cVt, const float* __restrict__ cnorm,
+    const bf16_t* __restrict__ consts, bf16_t* __restrict__ o, int Hq, int Hkv, int T, int w,
+    int Tp, int nblk, int BH, float c_scale) {
     constexpr int BM = NW * 32;
     constexpr int KS = D / 16;   // 16-wide k slabs of q . k
     constexpr int DS = DD / 16;  // 16-wide k slabs of q~ . c^K
@@ -169,254 +189,349 @@ __global__ __launch_bounds__(NW * 64) void prefill_mfma_kernel(
     bf16_t* lds_k = smem;                    // [2][BN][LDK]
     bf16_t* lds_v = smem + 2 * BN * LDK;     // [2][BN][LDK]
 
-    const int idx = blockIdx.x;
-    const int rb = nblk - 1 - idx / BH;  // longest row blocks first
-    const int bh = idx - (idx / BH) * BH;
+    // Each workgroup takes row blocks p and nblk-1-p of one (batch, head): a
+    // short and a long causal row block, so every workgroup has the same work.
+    // Workgroups are dealt to the 8 XCDs round-robin; when BH % 8 == 0 all
+    // workgroups of a head are placed on one XCD so its L2 holds only the
+    // K/V/latents of BH/8 heads.
+    int pair, bh;
+    if ((BH & 7) == 0) {
+        const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+        const int hpx = BH >> 3;  // heads per XCD
+        pair = local / hpx;
+        bh = (local - pair * hpx) * 8 + xcd;
+    } else {
+        pair = blockIdx.x / BH;
+        bh = blockIdx.x - pair * BH;
+    }
     const int b = bh / Hq, h = bh - (bh / Hq) * Hq;
     const int g = h / (Hq / Hkv);
     const int bg = b * Hkv + g;
-    const int i0 = rb * BM;
     const int tid = threadIdx.x;
-    const int wave = tid >> 6, lane = tid & 63;
-    const int qc = lane & 31, hg = lane >> 5;
-    const int r0 = i0 + wave * 32;
-    const int i = r0 + qc;
-    const int i_hi = imin(r0 + 31, T - 1);  // last real row of this wavefront (< r0 if none)
-
-    // ---- query operand (B of S^T = K Q^T): q[i][s*16 + hg*8 + 0..7]
-    bf16x8_t qop[KS];
-    {
-        const bf16_t* qrow = q + ((size_t)bh * T + imin(i, T - 1)) * D;
-#pragma unroll
-        for (int s = 0; s < KS; ++s) qop[s] = (i < T) ? load_bf16x8(qrow + s * 16 + hg * 8) : zero_bf16x8();
-    }
-
-    SoftmaxState st{-INFINITY, 0.f, 0.f};
-    f32x16_t ow[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) ow[t] = splat16(0.f);
-    f32x16_t ol = splat16(0.f);
-
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bf16_t* wdg = wd + (size_t)g * D * DD;
     const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
 
-    // ---------------------------------------------------------------- distant region
-    const int jd_end = (r0 < T) ? i_hi - w : -1;  // last distant key of any row here
-    if (jd_end >= 0) {
-        // q~^T = W_up q^T (scaled): A rows = latent column c, k = e.
-        f32x16_t qt = splat16(0.f);
+#pragma nounroll
+    for (int part = 0; part < 2; ++part) {
+        // Lane-dependent addresses are recomputed for each row block from an
+        // opaque copy of the lane id: hoisted out of this loop they would hold
+        // (and spill) dozens of registers across both blocks.
+        int lane = tid & 63;
+        __asm__ volatile("" : "+v"(lane));
+        const int qc = lane & 31, hg = lane >> 5;
+        const int prow = perm_row(qc);
+        const int rb = part == 0 ? nblk - 1 - pair : pair;
+        if (part == 1 && rb >= nblk - 1 - pair) break;  // odd block count: middle block once
+        const int i0 = rb * BM;
+        const int r0 = i0 + wave * 32;
+        const int i = r0 + qc;
+        const int i_hi = imin(r0 + 31, T - 1);  // last real row of this wavefront (< r0 if none)
+
+        // ---- query operand (B of S^T = K Q^T): q[i][s*16 + hg*8 + 0..7]. It is
+        // loaded for the W_up absorption and again for the local region, so it
+        // holds no registers during the distant loop.
+        const bf16_t* qrow = q + ((size_t)bh * T + imin(i, T - 1)) * D;
+        auto load_q = [&](bf16x8_t (&qop)[KS]) {
 #pragma unroll
-        for (int s = 0; s < KS; ++s) {
-            bf16x8_t a = zero_bf16x8();
-            if (qc < DD) {
-                if (wug) {
-                    a = load_bf16x8(wug + (size_t)qc * D + s * 16 + hg * 8);
-                } else {
-                    uint16_t t8[8];
+            for (int s = 0; s < KS; ++s) qop[s] = (i < T) ? load_bf16x8(qrow + s * 16 + hg * 8) : zero_bf16x8();
+        };
+
+        SoftmaxState st;
+        st.m = -INFINITY;
+        st.cm = 0.f;
+        st.thr = -INFINITY;
+        st.l = 0.f;
+        st.cmv = splat16(0.f);
+        f32x16_t ow[NT];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) t8[j] = wdg[(size_t)(s * 16 + hg * 8 + j) * DD + qc];
-                    a = __builtin_bit_cast(bf16x8_t, t8);
+        for (int t = 0; t < NT; ++t) ow[t] = splat16(0.f);
+        f32x16_t ol = splat16(0.f);
+
+        // ------------------------------------------------------------ distant region
+        const int jd_end = (r0 < T) ? i_hi - w : -1;  // last distant key of any row here
+        if (jd_end >= 0) {
+            // q~^T = W_up q^T (scaled): A rows = latent column c, k = e.
+            f32x16_t qt = splat16(0.f);
+            bf16x8_t qop[KS];
+            load_q(qop);
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                bf16x8_t a = zero_bf16x8();
+                if (qc < DD) {
+                    if (wug) {
+                        a = load_bf16x8(wug + (size_t)qc * D + s * 16 + hg * 8);
+                    } else {
+                        uint16_t t8[8];
+#pragma unroll
+                        for (int j = 0; j < 8; ++j) t8[j] = wdg[(size_t)(s * 16 + hg * 8 + j) * DD + qc];
+                        a = __builtin_bit_cast(bf16x8_t, t8);
+                    }
+                }
+                qt = mfma(a, qop[s], qt);
+            }
+            // accumulator register 8*s + j holds latent column 16*s + (j<4 ? 4hg+j : 8+4hg+j-4)
+            bf16x8_t qtop[DS];
+            float qn2 = 0.f;
+#pragma unroll
+            for (int s = 0; s < DS; ++s) {
+                qtop[s] = pack8(qt[8 * s + 0] * c_scale, qt[8 * s + 1] * c_scale, qt[8 * s + 2] * c_scale,
+                                qt[8 * s + 3] * c_scale, qt[8 * s + 4] * c_scale, qt[8 * s + 5] * c_scale,
+                                qt[8 * s + 6] * c_scale, qt[8 * s + 7] * c_scale);
+                const uint4 u = __builtin_bit_cast(uint4, qtop[s]);
+                const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float lo = __uint_as_float(w4[j] << 16), hi = __uint_as_float(w4[j] & 0xffff0000u);
+                    qn2 = __builtin_fmaf(lo, lo, qn2);
+                    qn2 = __builtin_fmaf(hi, hi, qn2);
                 }
             }
-            qt = mfma(a, qop[s], qt);
-        }
-        // accumulator register 8*s + j holds latent column 16*s + (j<4 ? 4hg+j : 8+4hg+j-4)
-        bf16x8_t qtop[DS];
-#pragma unroll
-        for (int s = 0; s < DS; ++s)
-            qtop[s] = pack8(qt[8 * s + 0] * c_scale, qt[8 * s + 1] * c_scale, qt[8 * s + 2] * c_scale,
-                            qt[8 * s + 3] * c_scale, qt[8 * s + 4] * c_scale, qt[8 * s + 5] * c_scale,
-                            qt[8 * s + 6] * c_scale, qt[8 * s + 7] * c_scale);
+            qn2 = pair_sum(qn2);
 
-        const bf16_t* ckb = cK + (size_t)bg * Tp * DD;
-        const bf16_t* cvb = cVt + (size_t)bg * Tp * DD;
-        const int prow = perm_row(qc);
-        auto load_k = [&](int js, bf16x8_t (&ak)[DS]) {
+            const int js_last = jd_end & ~31;
+            const int n_sub = (js_last >> 5) + 1;
+            // Upper bound of every distant score of this row: |q~ . c| <= |q~| |c|
+            // (Cauchy-Schwarz on the bf16 values the MFMA multiplies), inflated
+            // slightly for fp32 rounding inside the accumulation.
+            float cmax = 0.f;
+            for (int sb = lane; sb < n_sub; sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * (Tp / 32) + sb]);
+            cmax = wave_max(cmax);
+            const float bound = sqrtf(qn2) * cmax * 1.001f + 1e-6f;
+
+            // operand streams; the workspace is padded past the last subtile so
+            // prefetches need no clamping
+            const bf16_t* ckl = cK + ((size_t)bg * Tp + prow) * DD + hg * 8;
+            const bool vrow = qc < DD;
+            const bf16_t* cvl = vrow ? cVt + (size_t)bg * Tp * DD + (size_t)qc * 32 + hg * 8
+                                     : consts + ((DD == 16 && qc == 16) ? 0 : 8);
+            const int vinc = vrow ? 32 * DD : 0;
+            auto load_k = [&](int sub, bf16x8_t (&ak)[DS]) {
+                const bf16_t* p = ckl + (size_t)sub * 32 * DD;
 #pragma unroll
-            for (int s = 0; s < DS; ++s) ak[s] = load_bf16x8(ckb + (size_t)(js + prow) * DD + s * 16 + hg * 8);
-        };
-        auto load_v = [&](int js, bf16x8_t& a0, bf16x8_t& a1) {
-            if (qc < DD) {
-                const bf16_t* base = cvb + ((size_t)(js >> 6) * DD + qc) * 64 + (js & 63) + hg * 8;
-                a0 = load_bf16x8(base);
-                a1 = load_bf16x8(base + 16);
-            } else if (DD == 16 && qc == 16) {
-                a0 = ones_bf16x8();
-                a1 = ones_bf16x8();
+                for (int s = 0; s < DS; ++s) ak[s] = load_bf16x8(p + s * 16);
+            };
+            auto load_v = [&](int sub, bf16x8_t (&av)[2]) {
+                const bf16_t* p = cvl + (size_t)sub * vinc;
+                av[0] = load_bf16x8(p);
+                av[1] = load_bf16x8(p + (vrow ? 16 : 0));
+            };
+            auto scores = [&](int sub, const bf16x8_t (&ak)[DS]) {
+                f32x16_t x = mfma(ak[0], qtop[0], st.cmv);
+#pragma unroll
+                for (int s = 1; s < DS; ++s) x = mfma(ak[s], qtop[s], x);
+                const int js = sub * 32;
+                if (js + 31 > r0 - w) {  // staircase subtile: keep j <= i - w
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        if (js + acc_key(r, hg) > i - w) x[r] = -INFINITY;
+                }
+                return x;
+            };
+            auto tracked = [&](int sub, const bf16x8_t (&ak)[DS], const bf16x8_t (&av)[2]) {
+                f32x16_t x = scores(sub, ak);
+                bf16x8_t p0, p1;
+                softmax_step<NT, DD != 16>(x, st, ow, ol, p0, p1);
+                ol = mfma(av[0], p0, ol);
+                ol = mfma(av[1], p1, ol);
+            };
+            // fixed reference (x <= 0 by the bound): no maximum, no rescaling
+            auto fixed = [&](int sub, const bf16x8_t (&ak)[DS], const bf16x8_t (&av)[2]) {
+                f32x16_t x = scores(sub, ak);
+                bf16x8_t p0, p1;
+                exp_pack<DD != 16>(x, st.l, p0, p1);
+                ol = mfma(av[0], p0, ol);
+                ol = mfma(av[1], p1, ol);
+            };
+
+            bf16x8_t akA[DS], avA[2], akB[DS], avB[2];
+            load_k(0, akA);
+            load_v(0, avA);
+            load_k(1, akB);
+            load_v(1, avB);
+            // the first subtile tracks the maximum: it gives every row with a
+            // distant key a real score to compare the bound with
+            tracked(0, akA, avA);
+            load_k(2, akA);
+            load_v(2, avA);
+            // the bound is used when it is within 2^-100 of a seen score for every row
+            const bool seen = st.m != -INFINITY;
+            const bool use_bound = !__builtin_amdgcn_ballot_w64(seen && bound - st.m > 100.f);
+            if (use_bound) {
+                if (seen) {
+                    const float fac = exp2f(st.m - bound);
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) ol[r] *= fac;
+                    st.l *= fac;
+                    st.m = bound;
+                    st.cm = -bound;
+                    st.thr = kTau;
+                }
+                st.cmv = splat16(-bound);
+                int sub = 1;
+                for (; sub + 1 < n_sub; sub += 2) {
+                    fixed(sub, akB, avB);
+                    load_k(sub + 2, akB);
+                    load_v(sub + 2, avB);
+                    fixed(sub + 1, akA, avA);
+                    load_k(sub + 3, akA);
+                    load_v(sub + 3, avA);
+                }
+                if (sub < n_sub) fixed(sub, akB, avB);
+                st.cmv = splat16(st.cm);
             } else {
-                a0 = zero_bf16x8();
-                a1 = zero_bf16x8();
-            }
-        };
-        bf16x8_t ak[DS], av0, av1;
-        load_k(0, ak);
-        load_v(0, av0, av1);
-        for (int js = 0; js <= jd_end; js += 32) {
-            bf16x8_t akn[DS], avn0, avn1;
-            const bool more = js + 32 <= jd_end;
-            if (more) {
-                load_k(js + 32, akn);
-                load_v(js + 32, avn0, avn1);
-            }
-            f32x16_t x = splat16(st.cm);
-#pragma unroll
-            for (int s = 0; s < DS; ++s) x = mfma(ak[s], qtop[s], x);
-            if (js + 31 > r0 - w) {  // staircase subtile: keep j <= i - w
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (js + acc_key(r, hg) > i - w) x[r] = -INFINITY;
-            }
-            bf16x8_t p0, p1;
-            softmax_step<NT, DD != 16>(x, st, ow, ol, p0, p1);
-            ol = mfma(av0, p0, ol);
-            ol = mfma(av1, p1, ol);
-            if (more) {
-#pragma unroll
-                for (int s = 0; s < DS; ++s) ak[s] = akn[s];
-                av0 = avn0;
-                av1 = avn1;
+                int sub = 1;
+                for (; sub + 1 < n_sub; sub += 2) {
+                    tracked(sub, akB, avB);
+                    load_k(sub + 2, akB);
+                    load_v(sub + 2, avB);
+                    tracked(sub + 1, akA, avA);
+                    load_k(sub + 3, akA);
+                    load_v(sub + 3, avA);
+                }
+                if (sub < n_sub) tracked(sub, akB, avB);
             }
         }
-    }
 
-    // ---------------------------------------------------------------- local region
-    const int iwg_hi = imin(i0 + BM - 1, T - 1);
-    const int jb_lo = imax(0, i0 - w + 1);
-    if (w > 0 && jb_lo <= iwg_hi) {
-        const int t_first = jb_lo & ~(BN - 1);
-        const int ntile = (iwg_hi - t_first) / BN + 1;
-        const bf16_t* kb = k + (size_t)bg * T * D;
-        const bf16_t* vb = v + (size_t)bg * T * D;
-        uint4 pk[CH], pv[CH];
-        auto gload = [&](int t0) {
+        // ------------------------------------------------------------ local region
+        const int iwg_hi = imin(i0 + BM - 1, T - 1);
+        const int jb_lo = imax(0, i0 - w + 1);
+        if (w > 0 && jb_lo <= iwg_hi) {
+            const int t_first = jb_lo & ~(BN - 1);
+            const int ntile = (iwg_hi - t_first) / BN + 1;
+            const bf16_t* kb = k + (size_t)bg * T * D;
+            const bf16_t* vb = v + (size_t)bg * T * D;
+            uint4 pk[CH], pv[CH];
+            auto gload = [&](int t0) {
 #pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                const int chunk = tid + c * NW * 64;
-                const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
-                const int key = t0 + row;
-                if (key < T) {
-                    pk[c] = *reinterpret_cast<const uint4*>(kb + (size_t)key * D + col);
-                    pv[c] = *reinterpret_cast<const uint4*>(vb + (size_t)key * D + col);
-                } else {
-                    pk[c] = make_uint4(0, 0, 0, 0);
-                    pv[c] = make_uint4(0, 0, 0, 0);
-                }
-            }
-        };
-        auto lstore = [&](int buf) {
-#pragma unroll
-            for (int c = 0; c < CH; ++c) {
-                const int chunk = tid + c * NW * 64;
-                const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
-                *reinterpret_cast<uint4*>(lds_k + (size_t)buf * BN * LDK + row * LDK + col) = pk[c];
-                *reinterpret_cast<uint4*>(lds_v + (size_t)buf * BN * LDK + row * LDK + col) = pv[c];
-            }
-        };
-        gload(t_first);
-        lstore(0);
-        __syncthreads();
-        const int prow = perm_row(qc);
-        const int quad = lane >> 4, sl = lane & 15;
-        for (int n = 0; n < ntile; ++n) {
-            const int t0 = t_first + n * BN;
-            const int buf = n & 1;
-            if (n + 1 < ntile) gload(t0 + BN);
-            const bf16_t* lk = lds_k + (size_t)buf * BN * LDK;
-            const bf16_t* lv = lds_v + (size_t)buf * BN * LDK;
-#pragma unroll
-            for (int sub = 0; sub < BN / 32; ++sub) {
-                const int js = t0 + sub * 32;
-                if (r0 < T && js <= i_hi && js + 31 > r0 - w) {
-                    f32x16_t s = splat16(0.f);
-#pragma unroll
-                    for (int ks = 0; ks < KS; ++ks)
-                        s = mfma(load_bf16x8(lk + (sub * 32 + prow) * LDK + ks * 16 + hg * 8), qop[ks], s);
-                    f32x16_t x;
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(s[r], c_scale, st.cm);
-                    if (!(js > i_hi - w && js + 31 <= r0)) {  // edge subtile: keep i - w < j <= i
-#pragma unroll
-                        for (int r = 0; r < 16; ++r) {
-                            const int j = js + acc_key(r, hg);
-                            if (j <= i - w || j > i) x[r] = -INFINITY;
-                        }
-                    }
-                    bf16x8_t p0, p1;
-                    softmax_step<NT, true>(x, st, ow, ol, p0, p1);
-                    // O_win^T += V^T P^T; V^T operand via transposing LDS reads
-#pragma unroll
-                    for (int t = 0; t < NT; ++t) {
-#pragma unroll
-                        for (int half = 0; half < 2; ++half) {
-                            const int key = sub * 32 + half * 16 + 8 * (quad >> 1) + (sl >> 2);
-                            const int col = t * 32 + 16 * (quad & 1) + 4 * (sl & 3);
-                            const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                (lds_s16x4_t*)(lv + key * LDK + col));
-                            const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                (lds_s16x4_t*)(lv + (key + 4) * LDK + col));
-                            const uint2 ulo = __builtin_bit_cast(uint2, lo), uhi = __builtin_bit_cast(uint2, hi);
-                            const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(ulo.x, ulo.y, uhi.x, uhi.y));
-                            ow[t] = mfma(a, half ? p1 : p0, ow[t]);
-                        }
+                for (int c = 0; c < CH; ++c) {
+                    const int chunk = tid + c * NW * 64;
+                    const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
+                    const int key = t0 + row;
+                    if (key < T) {
+                        pk[c] = *reinterpret_cast<const uint4*>(kb + (size_t)key * D + col);
+                        pv[c] = *reinterpret_cast<const uint4*>(vb + (size_t)key * D + col);
+                    } else {
+                        pk[c] = make_uint4(0, 0, 0, 0);
+                        pv[c] = make_uint4(0, 0, 0, 0);
                     }
                 }
-            }
-            if (n + 1 < ntile) lstore(buf ^ 1);
+            };
+            auto lstore = [&](int buf) {
+#pragma unroll
+                for (int c = 0; c < CH; ++c) {
+                    const int chunk = tid + c * NW * 64;
+                    const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
+                    *reinterpret_cast<uint4*>(lds_k + (size_t)buf * BN * LDK + row * LDK + col) = pk[c];
+                    *reinterpret_cast<uint4*>(lds_v + (size_t)buf * BN * LDK + row * LDK + col) = pv[c];
+                }
+            };
+            bf16x8_t qop[KS];
+            load_q(qop);
+            gload(t_first);
+            lstore(0);
             __syncthreads();
-        }
-    }
-
-    if (r0 >= T) return;
-
-    // ---------------------------------------------------------------- epilogue
-    float lt = st.l;
-    if (DD == 16) lt += ol[8];  // ones row (row 16, held by lanes of half 0)
-    lt += swap32(lt);
-
-    if (jd_end >= 0) {
-        // O^T += W_up^T O_lat^T, O_lat split into bf16 hi + lo parts
+            const int quad = lane >> 4, sl = lane & 15;
+            for (int n = 0; n < ntile; ++n) {
+                const int t0 = t_first + n * BN;
+                const int buf = n & 1;
+                if (n + 1 < ntile) gload(t0 + BN);
+                const bf16_t* lk = lds_k + (size_t)buf * BN * LDK;
+                const bf16_t* lv = lds_v + (size_t)buf * BN * LDK;
 #pragma unroll
-        for (int s = 0; s < DS; ++s) {
-            float hi_f[8], lo_f[8];
+                for (int sub = 0; sub < BN / 32; ++sub) {
+                    const int js = t0 + sub * 32;
+                    if (r0 < T && js <= i_hi && js + 31 > r0 - w) {
+                        f32x16_t s = splat16(0.f);
 #pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                const float x = ol[8 * s + j];
-                const uint32_t hb = pack2(x, 0.f) & 0xffffu;
-                const float hv = __uint_as_float(hb << 16);
-                hi_f[j] = hv;
-                lo_f[j] = x - hv;
+                        for (int ks = 0; ks < KS; ++ks)
+                            s = mfma(load_bf16x8(lk + (sub * 32 + prow) * LDK + ks * 16 + hg * 8), qop[ks], s);
+                        f32x16_t x;
+#pragma unroll
+                        for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(s[r], c_scale, st.cm);
+                        if (!(js > i_hi - w && js + 31 <= r0)) {  // edge subtile: keep i - w < j <= i
+#pragma unroll
+                            for (int r = 0; r < 16; ++r) {
+                                const int j = js + acc_key(r, hg);
+                                if (j <= i - w || j > i) x[r] = -INFINITY;
+                            }
+                        }
+                        bf16x8_t p0, p1;
+                        softmax_step<NT, true>(x, st, ow, ol, p0, p1);
+                        // O_win^T += V^T P^T; V^T operand via transposing LDS reads
+#pragma unroll
+                        for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                            for (int half = 0; half < 2; ++half) {
+                                const int key = sub * 32 + half * 16 + 8 * (quad >> 1) + (sl >> 2);
+                                const int col = t * 32 + 16 * (quad & 1) + 4 * (sl & 3);
+                                const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                    (lds_s16x4_t*)(lv + key * LDK + col));
+                                const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                    (lds_s16x4_t*)(lv + (key + 4) * LDK + col));
+                                const uint2 ulo = __builtin_bit_cast(uint2, lo), uhi = __builtin_bit_cast(uint2, hi);
+                                const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(ulo.x, ulo.y, uhi.x, uhi.y));
+                                ow[t] = mfma(a, half ? p1 : p0, ow[t]);
+                            }
+                        }
+                    }
+                }
+                if (n + 1 < ntile) lstore(buf ^ 1);
+                __syncthreads();
             }
-            const bf16x8_t bhi = pack8(hi_f[0], hi_f[1], hi_f[2], hi_f[3], hi_f[4], hi_f[5], hi_f[6], hi_f[7]);
-            const bf16x8_t blo = pack8(lo_f[0], lo_f[1], lo_f[2], lo_f[3], lo_f[4], lo_f[5], lo_f[6], lo_f[7]);
+        }
+
+        if (r0 >= T) continue;
+
+        // ------------------------------------------------------------ epilogue
+        float lt = st.l;
+        if (DD == 16) lt += ol[8];  // ones row (row 16, held by lanes of half 0)
+        lt = pair_sum(lt);
+
+        if (jd_end >= 0) {
+            // O^T += W_up^T O_lat^T, O_lat split into bf16 hi + lo parts
 #pragma unroll
-            for (int t = 0; t < NT; ++t) {
-                const int e = t * 32 + qc;
-                uint16_t a8[8];
+            for (int s = 0; s < DS; ++s) {
+                float hi_f[8], lo_f[8];
 #pragma unroll
                 for (int j = 0; j < 8; ++j) {
-                    const int c = s * 16 + ((j < 4) ? 4 * hg + j : 8 + 4 * hg + (j - 4));
-                    a8[j] = wug ? wug[(size_t)c * D + e] : wdg[(size_t)e * DD + c];
+                    const float x = ol[8 * s + j];
+                    const float hv = __uint_as_float((pack2(x, 0.f) & 0xffffu) << 16);
+                    hi_f[j] = hv;
+                    lo_f[j] = x - hv;
                 }
-                const bf16x8_t a = __builtin_bit_cast(bf16x8_t, a8);
-                ow[t] = mfma(a, bhi, ow[t]);
-                ow[t] = mfma(a, blo, ow[t]);
+                const bf16x8_t bhi = pack8(hi_f[0], hi_f[1], hi_f[2], hi_f[3], hi_f[4], hi_f[5], hi_f[6], hi_f[7]);
+                const bf16x8_t blo = pack8(lo_f[0], lo_f[1], lo_f[2], lo_f[3], lo_f[4], lo_f[5], lo_f[6], lo_f[7]);
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    const int e = t * 32 + qc;
+                    uint16_t a8[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const int c = s * 16 + ((j < 4) ? 4 * hg + j : 8 + 4 * hg + (j - 4));
+                        a8[j] = wug ? wug[(size_t)c * D + e] : wdg[(size_t)e * DD + c];
+                    }
+                    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, a8);
+                    ow[t] = mfma(a, bhi, ow[t]);
+                    ow[t] = mfma(a, blo, ow[t]);
+                }
             }
         }
-    }
 
-    if (i < T) {
-        const float inv = 1.f / lt;
-        bf16_t* orow = o + ((size_t)bh * T + i) * D;
+        if (i < T) {
+            const float inv = 1.f / lt;
+            bf16_t* orow = o + ((size_t)bh * T + i) * D;
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
+            for (int t = 0; t < NT; ++t)
 #pragma unroll
-            for (int grp = 0; grp < 4; ++grp) {
-                const int e = t * 32 + grp * 8 + hg * 4;
-                uint2 u;
-                u.x = pack2(ow[t][grp * 4 + 0] * inv, ow[t][grp * 4 + 1] * inv);
-                u.y = pack2(ow[t][grp * 4 + 2] * inv, ow[t][grp * 4 + 3] * inv);
-                *reinterpret_cast<uint2*>(orow + e) = u;
-            }
+                for (int grp = 0; grp < 4; ++grp) {
+                    const int e = t * 32 + grp * 8 + hg * 4;
+                    uint2 u;
+                    u.x = pack2(ow[t][grp * 4 + 0] * inv, ow[t][grp * 4 + 1] * inv);
+                    u.y = pack2(ow[t][grp * 4 + 2] * inv, ow[t][grp * 4 + 3] * inv);
+                    *reinterpret_cast<uint2*>(orow + e) = u;
+                }
+        }
     }
 }
 
@@ -430,12 +545,14 @@ bool prefill_mfma_supported(const dar_shape* s) {
 template <int D, int DD>
 static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q, const void* k,
                             const void* v, const void* wd, const void* wu, void* o,
-                            const void* cK, const void* cVt, hipStream_t st) {
+                            const void* cK, const void* cVt, const float* cnorm,
+                            const void* consts, hipStream_t st) {
     constexpr int NW = 4;
     constexpr int BM = NW * 32;
     const int nblk = (T + BM - 1) / BM;
+    const int npair = (nblk + 1) / 2;
     const int BH = B * Hq;
-    const int Tp = (T - w > 0) ? round_up(T - w, 64) : 0;
+    const int Tp = prefill_tp(T, w);
     const float c_scale = 1.4426950408889634f / sqrtf((float)D);
     const size_t lds = sizeof(bf16_t) * 4 * 64 * (D + 8);
     auto kern = prefill_mfma_kernel<D, DD, NW>;
@@ -443,21 +560,22 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q,
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
     }
-    hipLaunchKernelGGL(kern, dim3(nblk * BH), dim3(NW * 64), lds, st, (const bf16_t*)q,
+    hipLaunchKernelGGL(kern, dim3(npair * BH), dim3(NW * 64), lds, st, (const bf16_t*)q,
                        (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)wd, (const bf16_t*)wu,
-                       (const bf16_t*)cK, (const bf16_t*)cVt, (bf16_t*)o, Hq, Hkv, T, w, Tp, nblk,
-                       BH, c_scale);
+                       (const bf16_t*)cK, (const bf16_t*)cVt, cnorm, (const bf16_t*)consts,
+                       (bf16_t*)o, Hq, Hkv, T, w, Tp, nblk, BH, c_scale);
     return hipGetLastError();
 }
 
 hipError_t launch_prefill_mfma(const dar_shape* s, int T, const void* q, const void* k,
                                const void* v, const void* wd, const void* wu, void* o,
-                               const void* cK, const void* cVt, hipStream_t st) {
+                               const void* cK, const void* cVt, const float* cnorm,
+                               const void* consts, hipStream_t st) {
     const int B = s->B, Hq = s->Hq, Hkv = s->Hkv, w = s->w;
-    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, st);
-    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, st);
-    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, st);
-    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, st);
+    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, consts, st);
+    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, consts, st);
+    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, consts, st);
+    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, consts, st);
     return hipErrorNotSupported;
 }
 

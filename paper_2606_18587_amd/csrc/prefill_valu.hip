@@ -80,11 +80,11 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
         for (int jj = 0; jj < cnt; ++jj) {
             const float pj = ps[jj];
             const int jx = j0 + jj;
-            const T* vb = cVg + (size_t)(jx >> 6) * 64 * dd + (jx & 63);
+            const T* vb = cVg + (size_t)(jx >> 5) * 32 * dd + (jx & 31);
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int c = lane + 64 * r;
-                if (c < dd) al[r] = __builtin_fmaf(pj, elem<T>::load(vb + (size_t)c * 64), al[r]);
+                if (c < dd) al[r] = __builtin_fmaf(pj, elem<T>::load(vb + (size_t)c * 32), al[r]);
             }
         }
         __syncthreads();
@@ -154,7 +154,7 @@ template <typename T>
 hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, const T* wu,
                                const T* cK, const T* cVt, T* o, int B, int Hq, int Hkv, int T_,
                                int d, int dd, int w, hipStream_t st) {
-    const int Tp = (T_ - w > 0) ? round_up(T_ - w, 64) : 0;
+    const int Tp = prefill_tp(T_, w);
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
     dim3 grid(T_, B * Hq);
     hipLaunchKernelGGL(prefill_valu_kernel<T>, grid, dim3(64), 0, st, q, k, v, wd, wu, cK, cVt, o,
