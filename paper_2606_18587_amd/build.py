@@ -15,7 +15,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdar.so")
-SOURCES = ["dar_api.hip", "latent.hip", "prefill_valu.hip", "prefill_mfma.hip", "decode.hip"]
+SOURCES = ["dar_api.hip", "latent.hip", "prefill_valu.hip", "prefill_mfma.hip", "decode.hip",
+           "decode_mfma.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

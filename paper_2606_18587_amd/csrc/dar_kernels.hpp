@@ -54,6 +54,16 @@ hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, 
                                const T* cK, const T* cVt, T* o, int B, int Hq, int Hkv, int T_,
                                int d, int dd, int w, hipStream_t st);
 
+// Matrix-core decode (bf16, d in {64,128}, d_down in {16,32}, <= 8 query heads
+// per KV head); shares decode_combine_kernel with the vector-ALU path.
+bool decode_mfma_supported(int d, int dd, int G, bool bf16);
+void decode_mfma_splits(int len, int w, int& n_lat_split, int& n_win_split);
+hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
+                              const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_lat,
+                              const bf16_t* v_lat, float* part, int B, int Hq, int Hkv, int d,
+                              int dd, int w, int cap, int len, int& n_lat_split, int& S,
+                              hipStream_t st);
+
 template <typename T>
 hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,

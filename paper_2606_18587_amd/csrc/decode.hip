@@ -297,13 +297,18 @@ DecodeSplits decode_splits(int len, int w, int d, int dd, int G) {
 }
 
 int decode_max_splits(int cap, int w, int d, int dd, int G) {
-    // the split count is largest when every cached token is latent, or when
-    // the window is full and the rest latent; take the sum of both bounds
+    // the split count grows with the cache length; bound it at len = cap for
+    // both split schemes (vector-ALU and matrix-core)
     DecodeSplits a = decode_splits(cap, w, d, dd, G);
     DecodeSplits b = decode_splits(cap, 0, d, dd, G);
-    int m1 = a.n_lat_split + a.n_win_split;
-    int m2 = b.n_lat_split + b.n_win_split;
-    return (m1 > m2 ? m1 : m2) + 1;
+    int m = a.n_lat_split + a.n_win_split;
+    m = m > b.n_lat_split + b.n_win_split ? m : b.n_lat_split + b.n_win_split;
+    int l1, w1, l2, w2;
+    decode_mfma_splits(cap, w, l1, w1);
+    decode_mfma_splits(cap, 0, l2, w2);
+    m = m > l1 + w1 ? m : l1 + w1;
+    m = m > l2 + w2 ? m : l2 + w2;
+    return m + 1;
 }
 
 template <typename T, int G>
@@ -328,6 +333,17 @@ template <typename T>
 hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
                          int d, int dd, int w, int cap, int len, hipStream_t st) {
+    if (decode_mfma_supported(d, dd, Hq / Hkv, sizeof(T) == 2)) {
+        int n_lat_split = 0, S = 0;
+        hipError_t e = launch_decode_mfma((const bf16_t*)q, (const bf16_t*)wd, (const bf16_t*)wu,
+                                          (const bf16_t*)k_win, (const bf16_t*)v_win,
+                                          (const bf16_t*)k_lat, (const bf16_t*)v_lat, part, B, Hq,
+                                          Hkv, d, dd, w, cap, len, n_lat_split, S, st);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(256), 0, st, part, wd, wu,
+                           o, Hq, Hkv, d, dd, n_lat_split, S);
+        return hipGetLastError();
+    }
     switch (Hq / Hkv) {
         case 1: return launch_decode_g<T, 1>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
         case 2: return launch_decode_g<T, 2>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
