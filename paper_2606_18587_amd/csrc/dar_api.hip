@@ -10,15 +10,15 @@
 namespace dar {
 
 PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize) {
-    PrefillWs ws{0, 0, 0, 0, 0};
+    PrefillWs ws{0, 0, 0, 0, 0, 0};
     const size_t Tp = (size_t)prefill_tp(T, w);
-    if (Tp == 0) return ws;
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     const size_t one = al((size_t)B * Hkv * Tp * dd * esize);
     ws.ck_off = 0;
     ws.cv_off = one;
     ws.norm_off = 2 * one;
-    ws.const_off = ws.norm_off + al((size_t)B * Hkv * (Tp / 32) * sizeof(float));
+    ws.knorm_off = ws.norm_off + al((size_t)B * Hkv * (Tp / 32) * sizeof(float));
+    ws.const_off = ws.knorm_off + al((size_t)B * Hkv * ((T + 31) / 32) * sizeof(float));
     ws.bytes = ws.const_off + 256;
     return ws;
 }
@@ -29,7 +29,7 @@ bool prefill_mfma_supported(const dar_shape* s);
 hipError_t launch_prefill_mfma(const dar_shape* s, int T, const void* q, const void* k,
                                const void* v, const void* wd, const void* wu, void* o,
                                const void* cK, const void* cVt, const float* cnorm,
-                               const void* consts, hipStream_t st);
+                               const float* knorm, const void* consts, hipStream_t st);
 
 }  // namespace dar
 
@@ -108,15 +108,16 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
     if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(w_down) || !dev_ok(o)) return DAR_E_ARG;
     if (w_up && !aligned16(w_up)) return DAR_E_ARG;
     const PrefillWs L = prefill_ws_layout(s->B, s->Hkv, T, s->d_down, s->w, esize_of(s->dtype));
-    if (L.bytes > 0 && (ws == nullptr || ws_bytes < L.bytes)) return DAR_E_WORKSPACE;
-    if (L.bytes > 0 && !aligned16(ws)) return DAR_E_ARG;
+    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
 
     clear_hip_error();
     char* wsb = (char*)ws;
-    const void* cK = L.bytes ? wsb + L.ck_off : nullptr;
-    const void* cV = L.bytes ? wsb + L.cv_off : nullptr;
-    void* consts = L.bytes ? wsb + L.const_off : nullptr;
-    float* cnorm = L.bytes ? (float*)(wsb + L.norm_off) : nullptr;
+    const void* cK = wsb + L.ck_off;
+    const void* cV = wsb + L.cv_off;
+    void* consts = wsb + L.const_off;
+    float* cnorm = (float*)(wsb + L.norm_off);
+    float* knorm = (float*)(wsb + L.knorm_off);
     hipError_t e = hipSuccess;
     const bool fast = prefill_mfma_supported(s);
     if (log_enabled())
@@ -126,11 +127,12 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
     if (s->dtype == DAR_BF16) {
         e = launch_prefill_latent<bf16_t>((const bf16_t*)k, (const bf16_t*)v,
                                           (const bf16_t*)w_down, (bf16_t*)cK, (bf16_t*)cV, cnorm,
-                                          (bf16_t*)consts, s->B, s->Hkv, T, s->d, s->d_down, s->w,
-                                          fast, stream);
+                                          knorm, (bf16_t*)consts, s->B, s->Hkv, T, s->d,
+                                          s->d_down, s->w, fast, stream);
         if (e == hipSuccess) {
             if (fast)
-                e = launch_prefill_mfma(s, T, q, k, v, w_down, w_up, o, cK, cV, cnorm, consts, stream);
+                e = launch_prefill_mfma(s, T, q, k, v, w_down, w_up, o, cK, cV, cnorm, knorm, consts,
+                                       stream);
             else
                 e = launch_prefill_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k,
                                                 (const bf16_t*)v, (const bf16_t*)w_down,
@@ -140,8 +142,8 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
         }
     } else {
         e = launch_prefill_latent<float>((const float*)k, (const float*)v, (const float*)w_down,
-                                         (float*)cK, (float*)cV, cnorm, (float*)consts, s->B,
-                                         s->Hkv, T, s->d, s->d_down, s->w, false, stream);
+                                         (float*)cK, (float*)cV, cnorm, knorm, (float*)consts,
+                                         s->B, s->Hkv, T, s->d, s->d_down, s->w, false, stream);
         if (e == hipSuccess)
             e = launch_prefill_valu<float>((const float*)q, (const float*)k, (const float*)v,
                                            (const float*)w_down, (const float*)w_up,

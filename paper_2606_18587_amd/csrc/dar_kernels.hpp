@@ -19,10 +19,13 @@ static inline int round_up(int x, int m) { return (x + m - 1) / m * m; }
 //   cVt    [B*Hkv][Tp/32][dd][32]     32-token blocks, transposed in a block
 //   cnorm  [B*Hkv][Tp/32] fp32        max L2 norm of the stored c^K rows of each
 //                                     32-token block (matrix-core path only)
+//   knorm  [B*Hkv][ceil(T/32)] fp32   max L2 norm of the key rows of each 32-token
+//                                     block (matrix-core path only)
 //   consts 256 bytes; starts with 8 bf16 ones then 8 bf16 zeros (operand rows
 //          of the matrix-core kernel that carry no latent column)
+// The latent parts are empty when T <= w.
 struct PrefillWs {
-    size_t ck_off, cv_off, norm_off, const_off, bytes;
+    size_t ck_off, cv_off, norm_off, knorm_off, const_off, bytes;
 };
 static inline int prefill_tp(int T, int w) {
     const int Tl = T - w;
@@ -41,8 +44,8 @@ int decode_max_splits(int cap, int w, int d, int dd, int G);
 
 template <typename T>
 hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt,
-                                 float* cnorm, T* consts, int B, int Hkv, int T_, int d, int dd,
-                                 int w, bool perm, hipStream_t st);
+                                 float* cnorm, float* knorm, T* consts, int B, int Hkv, int T_,
+                                 int d, int dd, int w, bool perm, hipStream_t st);
 
 template <typename T>
 hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, T* v_win,

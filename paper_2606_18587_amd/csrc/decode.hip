@@ -234,46 +234,64 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
     }
 }
 
+// One wavefront per (batch, query head). Lanes over splits compute the global
+// maximum and the merged row sum; lanes over output columns accumulate the
+// latent (d_down) and window (d) parts, then lift the latent part with W_up.
 template <typename T>
-__global__ __launch_bounds__(256) void decode_combine_kernel(
+__global__ __launch_bounds__(64) void decode_combine_kernel(
     const float* __restrict__ part, const T* __restrict__ wd, const T* __restrict__ wu,
     T* __restrict__ o, int Hq, int Hkv, int d, int dd, int n_lat_split, int S) {
-    __shared__ float lat[256];
-    __shared__ float scale_s[1024];
-    __shared__ float inv_l;
     const int bh = blockIdx.x;
     const int h = bh % Hq;
     const int g = h / (Hq / Hkv);
+    const int lane = threadIdx.x;
     const int stride = 2 + d;
     const float* pp = part + (size_t)bh * S * stride;
-    // global max and per-split weights (S <= 1024 is guaranteed by the host)
-    float mx = -INFINITY;
-    for (int s = 0; s < S; ++s) mx = fmaxf(mx, pp[(size_t)s * stride]);
-    for (int s = threadIdx.x; s < S; s += 256) scale_s[s] = exp2f(pp[(size_t)s * stride] - mx);
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        float l = 0.f;
-        for (int s = 0; s < S; ++s) l += scale_s[s] * pp[(size_t)s * stride + 1];
-        inv_l = 1.f / l;
-    }
-    for (int c = threadIdx.x; c < dd; c += 256) {
-        float a = 0.f;
-        for (int s = 0; s < n_lat_split; ++s) a += scale_s[s] * pp[(size_t)s * stride + 2 + c];
-        lat[c] = a;
-    }
-    __syncthreads();
     const T* wdg = wd + (size_t)g * d * dd;
     const T* wug = wu ? wu + (size_t)g * dd * d : nullptr;
-    for (int e = threadIdx.x; e < d; e += 256) {
-        float a = 0.f;
-        for (int s = n_lat_split; s < S; ++s) a += scale_s[s] * pp[(size_t)s * stride + 2 + e];
-        if (n_lat_split > 0)
-            for (int c = 0; c < dd; ++c) {
-                const float u = wug ? elem<T>::load(wug + (size_t)c * d + e)
-                                    : elem<T>::load(wdg + (size_t)e * dd + c);
-                a = __builtin_fmaf(lat[c], u, a);
-            }
-        o[(size_t)bh * d + e] = elem<T>::from_f32(a * inv_l);
+
+    // split weights: w_s = 2^(m_s - M), L = sum_s w_s l_s
+    float M = -INFINITY;
+    for (int s = lane; s < S; s += 64) M = fmaxf(M, pp[(size_t)s * stride]);
+    M = wave_max(M);
+    float L = 0.f;
+    for (int s = lane; s < S; s += 64) L += exp2f(pp[(size_t)s * stride] - M) * pp[(size_t)s * stride + 1];
+    L = wave_sum(L);
+    const float inv = 1.f / L;
+
+    // latent part (columns c < dd) and window part (columns e < d)
+    float lat[4] = {0.f, 0.f, 0.f, 0.f};
+    float win[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < S; ++s) {
+        const float ws = exp2f(pp[(size_t)s * stride] - M);
+        const float* a = pp + (size_t)s * stride + 2;
+        if (s < n_lat_split) {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                if (lane + 64 * r < dd) lat[r] = __builtin_fmaf(ws, a[lane + 64 * r], lat[r]);
+        } else {
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+                if (lane + 64 * r < d) win[r] = __builtin_fmaf(ws, a[lane + 64 * r], win[r]);
+        }
+    }
+    // o[e] = (win[e] + sum_c lat[c] W_up[c][e]) / L
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+        const int e = lane + 64 * r;
+        float acc = win[r];
+        if (n_lat_split > 0) {
+#pragma unroll
+            for (int r2 = 0; r2 < 4; ++r2)
+                for (int c2 = 0; c2 < 64 && 64 * r2 + c2 < dd; ++c2) {
+                    const int c = 64 * r2 + c2;
+                    const float lc = __shfl(lat[r2], c2, 64);
+                    const float u = wug ? elem<T>::load(wug + (size_t)c * d + (e < d ? e : 0))
+                                        : elem<T>::load(wdg + (size_t)(e < d ? e : 0) * dd + c);
+                    acc = __builtin_fmaf(lc, u, acc);
+                }
+        }
+        if (e < d) o[(size_t)bh * d + e] = elem<T>::from_f32(acc * inv);
     }
 }
 
@@ -324,7 +342,7 @@ static hipError_t launch_decode_g(const T* q, const T* wd, const T* wu, const T*
                        sp.chunk_lat, sp.chunk_win, sp.n_lat_split, S, qscale);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(256), 0, st, part, wd, wu, o,
+    hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu, o,
                        Hq, Hkv, d, dd, sp.n_lat_split, S);
     return hipGetLastError();
 }
@@ -340,7 +358,7 @@ hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, c
                                           (const bf16_t*)k_lat, (const bf16_t*)v_lat, part, B, Hq,
                                           Hkv, d, dd, w, cap, len, n_lat_split, S, st);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(256), 0, st, part, wd, wu,
+        hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu,
                            o, Hq, Hkv, d, dd, n_lat_split, S);
         return hipGetLastError();
     }

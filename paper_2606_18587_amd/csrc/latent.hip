@@ -200,12 +200,14 @@ __device__ __forceinline__ int acc_col(int r, int hg) { return 8 * (r >> 2) + 4 
 
 // Prefill pre-pass, one wavefront per 32 tokens, 4 wavefronts per block.
 // Also writes, per 32-token block, the largest L2 norm of the stored c^K rows
-// (the matrix-core prefill bounds its distant scores with it).
+// (over tokens [0, T - w)) and of the key rows (over all tokens [0, T)); the
+// matrix-core prefill bounds its scores with them.
 template <int D>
 __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
     const bf16_t* __restrict__ k, const bf16_t* __restrict__ v, const bf16_t* __restrict__ wd,
     bf16_t* __restrict__ cK, bf16_t* __restrict__ cVt, float* __restrict__ cnorm,
-    bf16_t* __restrict__ consts, int Hkv, int T_, int dd, int Tl, int Tp, int perm) {
+    float* __restrict__ knorm, bf16_t* __restrict__ consts, int Hkv, int T_, int dd, int Tl,
+    int Tp, int perm) {
     constexpr int KS = D / 16;
     if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < 16)
         consts[threadIdx.x] = threadIdx.x < 8 ? (bf16_t)0x3f80 : (bf16_t)0;
@@ -214,17 +216,45 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int tl = lane & 31, hg = lane >> 5;
-    const int t = blockIdx.x * 128 + wave * 32 + tl;
-    if (blockIdx.x * 128 + wave * 32 >= Tp) return;
+    const int ts = blockIdx.x * 128 + wave * 32;  // first token of this wavefront
+    const int t = ts + tl;
+    const int Tk = (T_ + 31) & ~31;
+    if (ts >= (Tp > Tk ? Tp : Tk)) return;
+    const bool project = ts < Tp;
     lbf16x8 wa[KS];
-    load_wd_operand<D>(wd + (size_t)g * D * dd, dd, lane, wa);
+    if (project) load_wd_operand<D>(wd + (size_t)g * D * dd, dd, lane, wa);
     for (int which = 0; which < 2; ++which) {
-        const bf16_t* xr = (which ? v : k) + ((size_t)bg * T_ + (t < Tl ? t : 0)) * D;
+        if (which == 1 && !project) break;
+        const int tmax = which == 0 ? T_ : Tl;  // keys: norms of all rows; values: latents only
+        const bf16_t* xr = (which ? v : k) + ((size_t)bg * T_ + (t < tmax ? t : 0)) * D;
         lbf16x8 x[KS];
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             x[s] = lload8(xr + s * 16 + hg * 8);
-            if (t >= Tl) x[s] = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
+            if (t >= tmax) x[s] = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
+        }
+        if (which == 0 && ts < T_) {
+            float n2 = 0.f;
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                const uint4 u = __builtin_bit_cast(uint4, x[s]);
+                const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const float lo = __uint_as_float(w4[j] << 16), hi = __uint_as_float(w4[j] & 0xffff0000u);
+                    n2 = __builtin_fmaf(lo, lo, n2);
+                    n2 = __builtin_fmaf(hi, hi, n2);
+                }
+            }
+            n2 += __shfl_xor(n2, 32, 64);
+            const float nmax = wave_max(n2);
+            if (lane == 0) knorm[(size_t)bg * (Tk / 32) + (ts >> 5)] = sqrtf(nmax);
+        }
+        if (!project) break;
+        if (which == 0) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                if (t >= Tl) x[s] = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
         }
         const lf32x16 acc = project_mfma<D>(wa, x);
         if (which == 0) {
@@ -370,20 +400,26 @@ static hipError_t launch_append_valu(const T* k_new, const T* v_new, const T* wd
     return hipGetLastError();
 }
 
+// perm is set exactly when the matrix-core prefill consumes the workspace: it
+// then needs the norms and constant rows even when no token is distant.
 template <>
 hipError_t launch_prefill_latent<bf16_t>(const bf16_t* k, const bf16_t* v, const bf16_t* wd,
-                                         bf16_t* cK, bf16_t* cVt, float* cnorm, bf16_t* consts,
-                                         int B, int Hkv, int T_, int d, int dd, int w, bool perm,
-                                         hipStream_t st) {
+                                         bf16_t* cK, bf16_t* cVt, float* cnorm, float* knorm,
+                                         bf16_t* consts, int B, int Hkv, int T_, int d, int dd,
+                                         int w, bool perm, hipStream_t st) {
     const int Tl = T_ - w;
-    if (Tl <= 0) return hipSuccess;
     const int Tp = prefill_tp(T_, w);
-    if (!mfma_projection(d, dd)) return launch_prefill_latent_valu<bf16_t>(k, v, wd, cK, cVt, B, Hkv, T_, d, dd, w, perm, st);
-    dim3 grid((Tp + 127) / 128, B * Hkv);
+    if (!perm || !mfma_projection(d, dd)) {
+        if (Tl <= 0) return hipSuccess;
+        return launch_prefill_latent_valu<bf16_t>(k, v, wd, cK, cVt, B, Hkv, T_, d, dd, w, perm, st);
+    }
+    const int Tk = (T_ + 31) & ~31;
+    const int ntok = Tp > Tk ? Tp : Tk;
+    dim3 grid((ntok + 127) / 128, B * Hkv);
     if (d == 64)
-        hipLaunchKernelGGL(prefill_latent_mfma_kernel<64>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, consts, Hkv, T_, dd, Tl, Tp, perm ? 1 : 0);
+        hipLaunchKernelGGL(prefill_latent_mfma_kernel<64>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv, T_, dd, Tl, Tp, 1);
     else
-        hipLaunchKernelGGL(prefill_latent_mfma_kernel<128>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, consts, Hkv, T_, dd, Tl, Tp, perm ? 1 : 0);
+        hipLaunchKernelGGL(prefill_latent_mfma_kernel<128>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv, T_, dd, Tl, Tp, 1);
     return hipGetLastError();
 }
 
@@ -409,10 +445,12 @@ hipError_t launch_append<bf16_t>(const bf16_t* k_new, const bf16_t* v_new, const
 
 template <typename T>
 hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt,
-                                 float* cnorm, T* consts, int B, int Hkv, int T_, int d, int dd,
-                                 int w, bool perm, hipStream_t st) {
+                                 float* cnorm, float* knorm, T* consts, int B, int Hkv, int T_,
+                                 int d, int dd, int w, bool perm, hipStream_t st) {
     (void)cnorm;   // only the matrix-core prefill reads the norms
+    (void)knorm;
     (void)consts;  // and the constant rows
+    if (T_ - w <= 0) return hipSuccess;
     return launch_prefill_latent_valu<T>(k, v, wd, cK, cVt, B, Hkv, T_, d, dd, w, perm, st);
 }
 
@@ -424,8 +462,8 @@ hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, 
 }
 
 template hipError_t launch_prefill_latent<float>(const float*, const float*, const float*, float*,
-                                                 float*, float*, float*, int, int, int, int, int,
-                                                 int, bool, hipStream_t);
+                                                 float*, float*, float*, float*, int, int, int, int,
+                                                 int, int, bool, hipStream_t);
 template hipError_t launch_append<float>(const float*, const float*, const float*, float*, float*,
                                          float*, float*, int, int, int, int, int, int, int, int,
                                          hipStream_t);

@@ -169,22 +169,190 @@ __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x
     exp_pack<SUM_VALU>(x, st.l, p0, p1);
 }
 
+// dot product of two 8-element bf16 operands (fp32 accumulation)
+__device__ __forceinline__ float dot8(bf16x8_t a, bf16x8_t b, float acc) {
+    const uint4 ua = __builtin_bit_cast(uint4, a), ub = __builtin_bit_cast(uint4, b);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, ua.x), __builtin_bit_cast(bf16x2_t, ub.x), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, ua.y), __builtin_bit_cast(bf16x2_t, ub.y), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, ua.z), __builtin_bit_cast(bf16x2_t, ub.z), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, ua.w), __builtin_bit_cast(bf16x2_t, ub.w), acc, false);
+    return acc;
+}
+
+// Everything a wavefront needs to walk one row block.
+struct RowCtx {
+    int T, w, Tp, r0, i, i_hi, qc, hg, prow, bg, tid;
+    float c_scale;
+};
+
+// Distant region: subtiles of 32 keys [0, js_last], latents streamed from
+// L2 two subtiles ahead (the workspace is padded, so no clamping).
+// FIXED: the reference is final, every score is <= 0 relative to it: no
+// maximum, no rescaling. Otherwise the online maximum is tracked.
+template <int D, int DD, bool FIXED>
+__device__ __forceinline__ void distant_region(const RowCtx& c, const bf16_t* __restrict__ cK,
+                                               const bf16_t* __restrict__ cVt,
+                                               const bf16_t* __restrict__ consts,
+                                               const bf16x8_t (&qtop)[DD / 16], int js_last,
+                                               SoftmaxState& st, f32x16_t (&ow)[D / 32],
+                                               f32x16_t& ol) {
+    constexpr int DS = DD / 16, NT = D / 32;
+    const int n_sub = (js_last >> 5) + 1;
+    const bf16_t* ckl = cK + ((size_t)c.bg * c.Tp + c.prow) * DD + c.hg * 8;
+    const bool vrow = c.qc < DD;
+    const bf16_t* cvl = vrow ? cVt + (size_t)c.bg * c.Tp * DD + (size_t)c.qc * 32 + c.hg * 8
+                             : consts + ((DD == 16 && c.qc == 16) ? 0 : 8);
+    const int vinc = vrow ? 32 * DD : 0;
+    const int vhalf = vrow ? 16 : 0;
+    auto load = [&](int sub, bf16x8_t (&ak)[DS], bf16x8_t (&av)[2]) {
+        const bf16_t* pk = ckl + (size_t)sub * 32 * DD;
+#pragma unroll
+        for (int s = 0; s < DS; ++s) ak[s] = load_bf16x8(pk + s * 16);
+        const bf16_t* pv = cvl + (size_t)sub * vinc;
+        av[0] = load_bf16x8(pv);
+        av[1] = load_bf16x8(pv + vhalf);
+    };
+    auto subtile = [&](int sub, const bf16x8_t (&ak)[DS], const bf16x8_t (&av)[2]) {
+        f32x16_t x = mfma(ak[0], qtop[0], st.cmv);
+#pragma unroll
+        for (int s = 1; s < DS; ++s) x = mfma(ak[s], qtop[s], x);
+        const int js = sub * 32;
+        if (js + 31 > c.r0 - c.w) {  // staircase subtile: keep j <= i - w
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                if (js + acc_key(r, c.hg) > c.i - c.w) x[r] = -INFINITY;
+        }
+        bf16x8_t p0, p1;
+        if (FIXED) exp_pack<DD != 16>(x, st.l, p0, p1);
+        else softmax_step<NT, DD != 16>(x, st, ow, ol, p0, p1);
+        ol = mfma(av[0], p0, ol);
+        ol = mfma(av[1], p1, ol);
+    };
+    bf16x8_t akA[DS], avA[2], akB[DS], avB[2];
+    load(0, akA, avA);
+    load(1, akB, avB);
+    int sub = 0;
+    for (; sub + 1 < n_sub; sub += 2) {
+        subtile(sub, akA, avA);
+        load(sub + 2, akA, avA);
+        subtile(sub + 1, akB, avB);
+        load(sub + 3, akB, avB);
+    }
+    if (sub < n_sub) subtile(sub, akA, avA);
+}
+
+// Local region: 64-key K/V tiles staged through LDS for the workgroup. The
+// query operand is the unscaled bf16 query (scaling it in bf16 would add a
+// rounding proportional to the score); one FMA per score applies
+// log2(e)/sqrt(d) and the reference.
+template <int D, int DD, int NW, bool FIXED>
+__device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __restrict__ k,
+                                             const bf16_t* __restrict__ v, bf16_t* lds_k,
+                                             bf16_t* lds_v, const bf16x8_t (&qop)[D / 16],
+                                             int i0, int iwg_hi, SoftmaxState& st,
+                                             f32x16_t (&ow)[D / 32], f32x16_t& ol) {
+    constexpr int KS = D / 16, NT = D / 32, BN = 64, LDK = D + 8;
+    constexpr int CH = BN * D / 8 / (NW * 64);
+    const int T = c.T, w = c.w;
+    const int jb_lo = imax(0, i0 - w + 1);
+    const int t_first = jb_lo & ~(BN - 1);
+    const int ntile = (iwg_hi - t_first) / BN + 1;
+    const bf16_t* kb = k + (size_t)c.bg * T * D;
+    const bf16_t* vb = v + (size_t)c.bg * T * D;
+    uint4 pk[CH], pv[CH];
+    auto gload = [&](int t0) {
+#pragma unroll
+        for (int q = 0; q < CH; ++q) {
+            const int chunk = c.tid + q * NW * 64;
+            const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
+            const int key = t0 + row;
+            if (key < T) {
+                pk[q] = *reinterpret_cast<const uint4*>(kb + (size_t)key * D + col);
+                pv[q] = *reinterpret_cast<const uint4*>(vb + (size_t)key * D + col);
+            } else {
+                pk[q] = make_uint4(0, 0, 0, 0);
+                pv[q] = make_uint4(0, 0, 0, 0);
+            }
+        }
+    };
+    auto lstore = [&](int buf) {
+#pragma unroll
+        for (int q = 0; q < CH; ++q) {
+            const int chunk = c.tid + q * NW * 64;
+            const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
+            *reinterpret_cast<uint4*>(lds_k + (size_t)buf * BN * LDK + row * LDK + col) = pk[q];
+            *reinterpret_cast<uint4*>(lds_v + (size_t)buf * BN * LDK + row * LDK + col) = pv[q];
+        }
+    };
+    gload(t_first);
+    lstore(0);
+    __syncthreads();
+    const int lane = c.tid & 63;
+    const int quad = lane >> 4, sl = lane & 15;
+    for (int n = 0; n < ntile; ++n) {
+        const int t0 = t_first + n * BN;
+        const int buf = n & 1;
+        if (n + 1 < ntile) gload(t0 + BN);
+        const bf16_t* lk = lds_k + (size_t)buf * BN * LDK;
+        const bf16_t* lv = lds_v + (size_t)buf * BN * LDK;
+#pragma unroll
+        for (int sub = 0; sub < BN / 32; ++sub) {
+            const int js = t0 + sub * 32;
+            if (c.r0 < T && js <= c.i_hi && js + 31 > c.r0 - w) {
+                f32x16_t sc = mfma(load_bf16x8(lk + (sub * 32 + c.prow) * LDK + c.hg * 8), qop[0], splat16(0.f));
+#pragma unroll
+                for (int ks = 1; ks < KS; ++ks)
+                    sc = mfma(load_bf16x8(lk + (sub * 32 + c.prow) * LDK + ks * 16 + c.hg * 8), qop[ks], sc);
+                f32x16_t x;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], c.c_scale, st.cm);
+                if (!(js > c.i_hi - w && js + 31 <= c.r0)) {  // edge subtile: keep i - w < j <= i
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int j = js + acc_key(r, c.hg);
+                        if (j <= c.i - w || j > c.i) x[r] = -INFINITY;
+                    }
+                }
+                bf16x8_t p0, p1;
+                if (FIXED) exp_pack<true>(x, st.l, p0, p1);
+                else softmax_step<NT, true>(x, st, ow, ol, p0, p1);
+                // O_win^T += V^T P^T; V^T operand via transposing LDS reads
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                    for (int half = 0; half < 2; ++half) {
+                        const int key = sub * 32 + half * 16 + 8 * (quad >> 1) + (sl >> 2);
+                        const int col = t * 32 + 16 * (quad & 1) + 4 * (sl & 3);
+                        const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_s16x4_t*)(lv + key * LDK + col));
+                        const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_s16x4_t*)(lv + (key + 4) * LDK + col));
+                        const uint2 ulo = __builtin_bit_cast(uint2, lo), uhi = __builtin_bit_cast(uint2, hi);
+                        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(ulo.x, ulo.y, uhi.x, uhi.y));
+                        ow[t] = mfma(a, half ? p1 : p0, ow[t]);
+                    }
+                }
+            }
+        }
+        if (n + 1 < ntile) lstore(buf ^ 1);
+        __syncthreads();
+    }
+}
+
 template <int D, int DD, int NW>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void prefill_mfma_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu, const bf16_t* __restrict__ cK,
     const bf16_t* __restrict__ cVt, const float* __restrict__ cnorm,
-    const bf16_t* __restrict__ consts, bf16_t* __restrict__ o, int Hq, int Hkv, int T, int w,
-    int Tp, int nblk, int BH, float c_scale) {
+    const float* __restrict__ knorm, const bf16_t* __restrict__ consts, bf16_t* __restrict__ o,
+    int Hq, int Hkv, int T, int w, int Tp, int nblk, int BH, float c_scale) {
     constexpr int BM = NW * 32;
     constexpr int KS = D / 16;   // 16-wide k slabs of q . k
     constexpr int DS = DD / 16;  // 16-wide k slabs of q~ . c^K
     constexpr int NT = D / 32;   // 32-row tiles of O_win^T
     constexpr int BN = 64;       // keys per LDS tile (local region)
     constexpr int LDK = D + 8;   // padded LDS row (bf16 elements)
-    constexpr int CH = BN * D / 8 / (NW * 64);  // 16-byte chunks per thread per tile
-    static_assert(CH >= 1 && BN * D / 8 == CH * NW * 64, "tile load split");
     extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
     bf16_t* lds_k = smem;                    // [2][BN][LDK]
     bf16_t* lds_v = smem + 2 * BN * LDK;     // [2][BN][LDK]
@@ -211,6 +379,7 @@ void prefill_mfma_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bf16_t* wdg = wd + (size_t)g * D * DD;
     const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
+    const int nkb = (T + 31) >> 5;  // 32-key blocks with a key norm
 
 #pragma nounroll
     for (int part = 0; part < 2; ++part) {
@@ -219,23 +388,32 @@ void prefill_mfma_kernel(
         // (and spill) dozens of registers across both blocks.
         int lane = tid & 63;
         __asm__ volatile("" : "+v"(lane));
-        const int qc = lane & 31, hg = lane >> 5;
-        const int prow = perm_row(qc);
         const int rb = part == 0 ? nblk - 1 - pair : pair;
         if (part == 1 && rb >= nblk - 1 - pair) break;  // odd block count: middle block once
+        RowCtx c;
+        c.T = T;
+        c.w = w;
+        c.Tp = Tp;
+        c.qc = lane & 31;
+        c.hg = lane >> 5;
+        c.prow = perm_row(c.qc);
+        c.bg = bg;
+        c.tid = tid;
+        c.c_scale = c_scale;
         const int i0 = rb * BM;
-        const int r0 = i0 + wave * 32;
-        const int i = r0 + qc;
-        const int i_hi = imin(r0 + 31, T - 1);  // last real row of this wavefront (< r0 if none)
+        c.r0 = i0 + wave * 32;
+        c.i = c.r0 + c.qc;
+        c.i_hi = imin(c.r0 + 31, T - 1);  // last real row of this wavefront (< r0 if none)
+        const int qc = c.qc, hg = c.hg, i = c.i;
 
-        // ---- query operand (B of S^T = K Q^T): q[i][s*16 + hg*8 + 0..7]. It is
-        // loaded for the W_up absorption and again for the local region, so it
-        // holds no registers during the distant loop.
         const bf16_t* qrow = q + ((size_t)bh * T + imin(i, T - 1)) * D;
-        auto load_q = [&](bf16x8_t (&qop)[KS]) {
+        bf16x8_t qop[KS];  // B operand of S^T = K Q^T: q[i][s*16 + hg*8 + 0..7]
 #pragma unroll
-            for (int s = 0; s < KS; ++s) qop[s] = (i < T) ? load_bf16x8(qrow + s * 16 + hg * 8) : zero_bf16x8();
-        };
+        for (int s = 0; s < KS; ++s) qop[s] = (i < T) ? load_bf16x8(qrow + s * 16 + hg * 8) : zero_bf16x8();
+        float qs2 = dot8(qop[0], qop[0], 0.f);
+#pragma unroll
+        for (int s = 1; s < KS; ++s) qs2 = dot8(qop[s], qop[s], qs2);
+        qs2 = pair_sum(qs2);
 
         SoftmaxState st;
         st.m = -INFINITY;
@@ -248,13 +426,16 @@ void prefill_mfma_kernel(
         for (int t = 0; t < NT; ++t) ow[t] = splat16(0.f);
         f32x16_t ol = splat16(0.f);
 
-        // ------------------------------------------------------------ distant region
-        const int jd_end = (r0 < T) ? i_hi - w : -1;  // last distant key of any row here
+        const int jd_end = (c.r0 < T) ? c.i_hi - w : -1;  // last distant key of any row here
+        const int js_last = jd_end & ~31;
+        const int iwg_hi = imin(i0 + BM - 1, T - 1);
+        const bool has_local = w > 0 && imax(0, i0 - w + 1) <= iwg_hi;
+
+        // ---- absorbed query q~ = q W_up^T (scaled): A rows = latent column c, k = e
+        bf16x8_t qtop[DS];
+        float bound = -INFINITY;
         if (jd_end >= 0) {
-            // q~^T = W_up q^T (scaled): A rows = latent column c, k = e.
             f32x16_t qt = splat16(0.f);
-            bf16x8_t qop[KS];
-            load_q(qop);
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
                 bf16x8_t a = zero_bf16x8();
@@ -271,217 +452,69 @@ void prefill_mfma_kernel(
                 qt = mfma(a, qop[s], qt);
             }
             // accumulator register 8*s + j holds latent column 16*s + (j<4 ? 4hg+j : 8+4hg+j-4)
-            bf16x8_t qtop[DS];
             float qn2 = 0.f;
 #pragma unroll
             for (int s = 0; s < DS; ++s) {
                 qtop[s] = pack8(qt[8 * s + 0] * c_scale, qt[8 * s + 1] * c_scale, qt[8 * s + 2] * c_scale,
                                 qt[8 * s + 3] * c_scale, qt[8 * s + 4] * c_scale, qt[8 * s + 5] * c_scale,
                                 qt[8 * s + 6] * c_scale, qt[8 * s + 7] * c_scale);
-                const uint4 u = __builtin_bit_cast(uint4, qtop[s]);
-                const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const float lo = __uint_as_float(w4[j] << 16), hi = __uint_as_float(w4[j] & 0xffff0000u);
-                    qn2 = __builtin_fmaf(lo, lo, qn2);
-                    qn2 = __builtin_fmaf(hi, hi, qn2);
-                }
+                qn2 = dot8(qtop[s], qtop[s], qn2);
             }
             qn2 = pair_sum(qn2);
-
-            const int js_last = jd_end & ~31;
-            const int n_sub = (js_last >> 5) + 1;
-            // Upper bound of every distant score of this row: |q~ . c| <= |q~| |c|
-            // (Cauchy-Schwarz on the bf16 values the MFMA multiplies), inflated
-            // slightly for fp32 rounding inside the accumulation.
+            // |q~ . c| <= |q~| |c| on the bf16 values the MFMA multiplies (Cauchy-Schwarz)
             float cmax = 0.f;
-            for (int sb = lane; sb < n_sub; sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * (Tp / 32) + sb]);
+            for (int sb = lane; sb <= (js_last >> 5); sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * (Tp / 32) + sb]);
             cmax = wave_max(cmax);
-            const float bound = sqrtf(qn2) * cmax * 1.001f + 1e-6f;
-
-            // operand streams; the workspace is padded past the last subtile so
-            // prefetches need no clamping
-            const bf16_t* ckl = cK + ((size_t)bg * Tp + prow) * DD + hg * 8;
-            const bool vrow = qc < DD;
-            const bf16_t* cvl = vrow ? cVt + (size_t)bg * Tp * DD + (size_t)qc * 32 + hg * 8
-                                     : consts + ((DD == 16 && qc == 16) ? 0 : 8);
-            const int vinc = vrow ? 32 * DD : 0;
-            auto load_k = [&](int sub, bf16x8_t (&ak)[DS]) {
-                const bf16_t* p = ckl + (size_t)sub * 32 * DD;
+            bound = sqrtf(qn2) * cmax;
+        }
+        if (has_local) {
+            float kmax = 0.f;
+            const int kb_lo = imax(0, c.r0 - w + 1) >> 5, kb_hi = imax(0, c.i_hi) >> 5;
+            for (int kb = kb_lo + lane; kb <= kb_hi; kb += 64) kmax = fmaxf(kmax, knorm[(size_t)bg * nkb + kb]);
+            kmax = wave_max(kmax);
+            bound = fmaxf(bound, c_scale * sqrtf(qs2) * kmax);
+        }
+        // Fixed reference: the bound (inflated for fp32 rounding) is used when,
+        // for every row, it is within 2^100 of a real score of that row (its own
+        // key), so no row's weights can all underflow.
+        bound = bound * 1.001f + 1e-6f;
+        float witness;
+        {
+            const int ii = imin(i, T - 1);
+            if (w >= 1) {
+                const bf16_t* krow = k + ((size_t)bg * T + ii) * D;
+                witness = 0.f;
 #pragma unroll
-                for (int s = 0; s < DS; ++s) ak[s] = load_bf16x8(p + s * 16);
-            };
-            auto load_v = [&](int sub, bf16x8_t (&av)[2]) {
-                const bf16_t* p = cvl + (size_t)sub * vinc;
-                av[0] = load_bf16x8(p);
-                av[1] = load_bf16x8(p + (vrow ? 16 : 0));
-            };
-            auto scores = [&](int sub, const bf16x8_t (&ak)[DS]) {
-                f32x16_t x = mfma(ak[0], qtop[0], st.cmv);
-#pragma unroll
-                for (int s = 1; s < DS; ++s) x = mfma(ak[s], qtop[s], x);
-                const int js = sub * 32;
-                if (js + 31 > r0 - w) {  // staircase subtile: keep j <= i - w
-#pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        if (js + acc_key(r, hg) > i - w) x[r] = -INFINITY;
-                }
-                return x;
-            };
-            auto tracked = [&](int sub, const bf16x8_t (&ak)[DS], const bf16x8_t (&av)[2]) {
-                f32x16_t x = scores(sub, ak);
-                bf16x8_t p0, p1;
-                softmax_step<NT, DD != 16>(x, st, ow, ol, p0, p1);
-                ol = mfma(av[0], p0, ol);
-                ol = mfma(av[1], p1, ol);
-            };
-            // fixed reference (x <= 0 by the bound): no maximum, no rescaling
-            auto fixed = [&](int sub, const bf16x8_t (&ak)[DS], const bf16x8_t (&av)[2]) {
-                f32x16_t x = scores(sub, ak);
-                bf16x8_t p0, p1;
-                exp_pack<DD != 16>(x, st.l, p0, p1);
-                ol = mfma(av[0], p0, ol);
-                ol = mfma(av[1], p1, ol);
-            };
-
-            bf16x8_t akA[DS], avA[2], akB[DS], avB[2];
-            load_k(0, akA);
-            load_v(0, avA);
-            load_k(1, akB);
-            load_v(1, avB);
-            // the first subtile tracks the maximum: it gives every row with a
-            // distant key a real score to compare the bound with
-            tracked(0, akA, avA);
-            load_k(2, akA);
-            load_v(2, avA);
-            // the bound is used when it is within 2^-100 of a seen score for every row
-            const bool seen = st.m != -INFINITY;
-            const bool use_bound = !__builtin_amdgcn_ballot_w64(seen && bound - st.m > 100.f);
-            if (use_bound) {
-                if (seen) {
-                    const float fac = exp2f(st.m - bound);
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) ol[r] *= fac;
-                    st.l *= fac;
-                    st.m = bound;
-                    st.cm = -bound;
-                    st.thr = kTau;
-                }
-                st.cmv = splat16(-bound);
-                int sub = 1;
-                for (; sub + 1 < n_sub; sub += 2) {
-                    fixed(sub, akB, avB);
-                    load_k(sub + 2, akB);
-                    load_v(sub + 2, avB);
-                    fixed(sub + 1, akA, avA);
-                    load_k(sub + 3, akA);
-                    load_v(sub + 3, avA);
-                }
-                if (sub < n_sub) fixed(sub, akB, avB);
-                st.cmv = splat16(st.cm);
+                for (int s = 0; s < KS; ++s) witness = dot8(qop[s], load_bf16x8(krow + s * 16 + hg * 8), witness);
+                witness *= c_scale;
             } else {
-                int sub = 1;
-                for (; sub + 1 < n_sub; sub += 2) {
-                    tracked(sub, akB, avB);
-                    load_k(sub + 2, akB);
-                    load_v(sub + 2, avB);
-                    tracked(sub + 1, akA, avA);
-                    load_k(sub + 3, akA);
-                    load_v(sub + 3, avA);
-                }
-                if (sub < n_sub) tracked(sub, akB, avB);
+                const bf16_t* crow = cK + ((size_t)bg * Tp + ii) * DD;
+                witness = 0.f;
+#pragma unroll
+                for (int s = 0; s < DS; ++s) witness = dot8(qtop[s], load_bf16x8(crow + s * 16 + hg * 8), witness);
             }
+            witness = pair_sum(witness);
+        }
+        const bool fixed = c.r0 < T && !__builtin_amdgcn_ballot_w64(i < T && bound - witness > 100.f);
+        if (fixed) {
+            st.m = bound;
+            st.cm = -bound;
+            st.thr = kTau;
+            st.cmv = splat16(-bound);
         }
 
+        // ------------------------------------------------------------ distant region
+        if (jd_end >= 0) {
+            if (fixed) distant_region<D, DD, true>(c, cK, cVt, consts, qtop, js_last, st, ow, ol);
+            else distant_region<D, DD, false>(c, cK, cVt, consts, qtop, js_last, st, ow, ol);
+        }
         // ------------------------------------------------------------ local region
-        const int iwg_hi = imin(i0 + BM - 1, T - 1);
-        const int jb_lo = imax(0, i0 - w + 1);
-        if (w > 0 && jb_lo <= iwg_hi) {
-            const int t_first = jb_lo & ~(BN - 1);
-            const int ntile = (iwg_hi - t_first) / BN + 1;
-            const bf16_t* kb = k + (size_t)bg * T * D;
-            const bf16_t* vb = v + (size_t)bg * T * D;
-            uint4 pk[CH], pv[CH];
-            auto gload = [&](int t0) {
-#pragma unroll
-                for (int c = 0; c < CH; ++c) {
-                    const int chunk = tid + c * NW * 64;
-                    const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
-                    const int key = t0 + row;
-                    if (key < T) {
-                        pk[c] = *reinterpret_cast<const uint4*>(kb + (size_t)key * D + col);
-                        pv[c] = *reinterpret_cast<const uint4*>(vb + (size_t)key * D + col);
-                    } else {
-                        pk[c] = make_uint4(0, 0, 0, 0);
-                        pv[c] = make_uint4(0, 0, 0, 0);
-                    }
-                }
-            };
-            auto lstore = [&](int buf) {
-#pragma unroll
-                for (int c = 0; c < CH; ++c) {
-                    const int chunk = tid + c * NW * 64;
-                    const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
-                    *reinterpret_cast<uint4*>(lds_k + (size_t)buf * BN * LDK + row * LDK + col) = pk[c];
-                    *reinterpret_cast<uint4*>(lds_v + (size_t)buf * BN * LDK + row * LDK + col) = pv[c];
-                }
-            };
-            bf16x8_t qop[KS];
-            load_q(qop);
-            gload(t_first);
-            lstore(0);
-            __syncthreads();
-            const int quad = lane >> 4, sl = lane & 15;
-            for (int n = 0; n < ntile; ++n) {
-                const int t0 = t_first + n * BN;
-                const int buf = n & 1;
-                if (n + 1 < ntile) gload(t0 + BN);
-                const bf16_t* lk = lds_k + (size_t)buf * BN * LDK;
-                const bf16_t* lv = lds_v + (size_t)buf * BN * LDK;
-#pragma unroll
-                for (int sub = 0; sub < BN / 32; ++sub) {
-                    const int js = t0 + sub * 32;
-                    if (r0 < T && js <= i_hi && js + 31 > r0 - w) {
-                        f32x16_t s = splat16(0.f);
-#pragma unroll
-                        for (int ks = 0; ks < KS; ++ks)
-                            s = mfma(load_bf16x8(lk + (sub * 32 + prow) * LDK + ks * 16 + hg * 8), qop[ks], s);
-                        f32x16_t x;
-#pragma unroll
-                        for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(s[r], c_scale, st.cm);
-                        if (!(js > i_hi - w && js + 31 <= r0)) {  // edge subtile: keep i - w < j <= i
-#pragma unroll
-                            for (int r = 0; r < 16; ++r) {
-                                const int j = js + acc_key(r, hg);
-                                if (j <= i - w || j > i) x[r] = -INFINITY;
-                            }
-                        }
-                        bf16x8_t p0, p1;
-                        softmax_step<NT, true>(x, st, ow, ol, p0, p1);
-                        // O_win^T += V^T P^T; V^T operand via transposing LDS reads
-#pragma unroll
-                        for (int t = 0; t < NT; ++t) {
-#pragma unroll
-                            for (int half = 0; half < 2; ++half) {
-                                const int key = sub * 32 + half * 16 + 8 * (quad >> 1) + (sl >> 2);
-                                const int col = t * 32 + 16 * (quad & 1) + 4 * (sl & 3);
-                                const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                    (lds_s16x4_t*)(lv + key * LDK + col));
-                                const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-                                    (lds_s16x4_t*)(lv + (key + 4) * LDK + col));
-                                const uint2 ulo = __builtin_bit_cast(uint2, lo), uhi = __builtin_bit_cast(uint2, hi);
-                                const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(ulo.x, ulo.y, uhi.x, uhi.y));
-                                ow[t] = mfma(a, half ? p1 : p0, ow[t]);
-                            }
-                        }
-                    }
-                }
-                if (n + 1 < ntile) lstore(buf ^ 1);
-                __syncthreads();
-            }
+        if (has_local) {
+            if (fixed) local_region<D, DD, NW, true>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+            else local_region<D, DD, NW, false>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
         }
 
-        if (r0 >= T) continue;
+        if (c.r0 >= T) continue;
 
         // ------------------------------------------------------------ epilogue
         float lt = st.l;
@@ -508,8 +541,8 @@ void prefill_mfma_kernel(
                     uint16_t a8[8];
 #pragma unroll
                     for (int j = 0; j < 8; ++j) {
-                        const int c = s * 16 + ((j < 4) ? 4 * hg + j : 8 + 4 * hg + (j - 4));
-                        a8[j] = wug ? wug[(size_t)c * D + e] : wdg[(size_t)e * DD + c];
+                        const int cc = s * 16 + ((j < 4) ? 4 * hg + j : 8 + 4 * hg + (j - 4));
+                        a8[j] = wug ? wug[(size_t)cc * D + e] : wdg[(size_t)e * DD + cc];
                     }
                     const bf16x8_t a = __builtin_bit_cast(bf16x8_t, a8);
                     ow[t] = mfma(a, bhi, ow[t]);
@@ -546,7 +579,7 @@ template <int D, int DD>
 static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q, const void* k,
                             const void* v, const void* wd, const void* wu, void* o,
                             const void* cK, const void* cVt, const float* cnorm,
-                            const void* consts, hipStream_t st) {
+                            const float* knorm, const void* consts, hipStream_t st) {
     constexpr int NW = 4;
     constexpr int BM = NW * 32;
     const int nblk = (T + BM - 1) / BM;
@@ -562,7 +595,7 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q,
     }
     hipLaunchKernelGGL(kern, dim3(npair * BH), dim3(NW * 64), lds, st, (const bf16_t*)q,
                        (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)wd, (const bf16_t*)wu,
-                       (const bf16_t*)cK, (const bf16_t*)cVt, cnorm, (const bf16_t*)consts,
+                       (const bf16_t*)cK, (const bf16_t*)cVt, cnorm, knorm, (const bf16_t*)consts,
                        (bf16_t*)o, Hq, Hkv, T, w, Tp, nblk, BH, c_scale);
     return hipGetLastError();
 }
@@ -570,12 +603,12 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q,
 hipError_t launch_prefill_mfma(const dar_shape* s, int T, const void* q, const void* k,
                                const void* v, const void* wd, const void* wu, void* o,
                                const void* cK, const void* cVt, const float* cnorm,
-                               const void* consts, hipStream_t st) {
+                               const float* knorm, const void* consts, hipStream_t st) {
     const int B = s->B, Hq = s->Hq, Hkv = s->Hkv, w = s->w;
-    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, consts, st);
-    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, consts, st);
-    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, consts, st);
-    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, consts, st);
+    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, knorm, consts, st);
     return hipErrorNotSupported;
 }
 

@@ -48,19 +48,20 @@ def S(B=2, Hq=4, Hkv=2, d=64, dd=16, w=8, dtype=torch.bfloat16):
 
 
 def expected_prefill_ws(B, Hkv, T, dd, w, esize):
-    """Two latent buffers over Tp = round_up(T - w, 32) + 64 tokens, per-32-token
-    norms (fp32), 256 bytes of constant rows; every part 256-byte aligned."""
-    if T - w <= 0:
-        return 0
+    """Two latent buffers over Tp = round_up(T - w, 32) + 64 tokens (none when
+    T <= w), per-32-token latent norms and key norms (fp32), 256 bytes of
+    constant rows; every part 256-byte aligned."""
     al = lambda x: (x + 255) // 256 * 256
-    Tp = (T - w + 31) // 32 * 32 + 64
-    return 2 * al(B * Hkv * Tp * dd * esize) + al(B * Hkv * (Tp // 32) * 4) + 256
+    Tp = (T - w + 31) // 32 * 32 + 64 if T > w else 0
+    return (2 * al(B * Hkv * Tp * dd * esize) + al(B * Hkv * (Tp // 32) * 4)
+            + al(B * Hkv * ((T + 31) // 32) * 4) + 256)
 
 
 def test_prefill_workspace_size():
     s = S()
     assert dar.dar_prefill_workspace_bytes(s, 100) == expected_prefill_ws(2, 2, 100, 16, 8, 2)
-    assert dar.dar_prefill_workspace_bytes(s, 8) == 0       # T <= w: no distant tokens
+    assert dar.dar_prefill_workspace_bytes(s, 8) == expected_prefill_ws(2, 2, 8, 16, 8, 2)
+    assert dar.dar_prefill_workspace_bytes(s, 8) < 1024     # T <= w: no latents, only norms
     assert dar.dar_prefill_workspace_bytes(S(w=0, dtype=torch.float32), 64) == \
         expected_prefill_ws(2, 2, 64, 16, 0, 4)
     assert dar.dar_prefill_workspace_bytes(S(Hq=3), 64) == 0   # invalid shape
