@@ -84,7 +84,9 @@ typedef struct {
  *   q [B][Hq][T][d], k, v [B][Hkv][T][d], w_down [Hkv][d][d_down],
  *   w_up [Hkv][d_down][d] or NULL (tied), o [B][Hq][T][d] (output).
  *   ws: device workspace of at least dar_prefill_workspace_bytes(s, T) bytes
- *   (may be NULL when that size is 0). T >= 1.
+ *   (never NULL; caller-owned, overwritten by the call): latents of the
+ *   tokens that are distant for some row (Eq. 1), per-32-token norm maxima
+ *   and constant operand rows. T >= 1.
  * Supported: fp32 with d <= 256; bf16 with d <= 256 (d in {64, 128} with
  * d_down in {16, 32} take the matrix-core path). */
 dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void* k,
