@@ -95,8 +95,8 @@ size_t dar_prefill_workspace_bytes(const dar_shape* s, int T) {
 
 size_t dar_decode_workspace_bytes(const dar_shape* s, int cap) {
     if (check_shape(s) != DAR_OK || cap < 1 || !group_supported(s)) return 0;
-    const int S = decode_max_splits(cap, s->w, s->d, s->d_down, s->Hq / s->Hkv);
-    return (size_t)s->B * s->Hq * S * (2 + s->d) * sizeof(float);
+    const int S = decode_max_partials(s->B, s->Hkv, cap, s->w, s->d, s->d_down, s->Hq / s->Hkv);
+    return (size_t)s->B * s->Hq * S * (2 + s->d_down + s->d) * sizeof(float);
 }
 
 dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void* k,
@@ -193,7 +193,8 @@ dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q
     if (s->w > 0 && (!dev_ok(c->k_win) || !dev_ok(c->v_win))) return DAR_E_ARG;
     if (!group_supported(s)) return DAR_E_UNSUPPORTED;
     const int G = s->Hq / s->Hkv;
-    if (decode_max_splits(c->cap, s->w, s->d, s->d_down, G) > 1024) return DAR_E_UNSUPPORTED;
+    if (decode_max_partials(s->B, s->Hkv, c->cap, s->w, s->d, s->d_down, G) > 1024)
+        return DAR_E_UNSUPPORTED;
     if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
     const size_t need = dar_decode_workspace_bytes(s, c->cap);
     if (ws == nullptr || ws_bytes < need) return DAR_E_WORKSPACE;

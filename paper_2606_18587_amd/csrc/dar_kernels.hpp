@@ -33,14 +33,15 @@ static inline int prefill_tp(int T, int w) {
 }
 PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize);
 
-// Decode workspace: per (batch, query head, split) partial softmax state
-// {m, l, acc[max(d, dd)]} in fp32.
+// Decode workspace: per (batch, query head, partial) softmax state
+// {m, l, acc_lat[dd], acc_win[d]} in fp32.
 struct DecodeSplits {
     int chunk_lat, chunk_win;   // tokens per split in each region
     int n_lat_split, n_win_split;
 };
 DecodeSplits decode_splits(int len, int w, int d, int dd, int G);
-int decode_max_splits(int cap, int w, int d, int dd, int G);
+int decode_mfma_parts(int B, int Hkv, int len, int w, int d);
+int decode_max_partials(int B, int Hkv, int cap, int w, int d, int dd, int G);
 
 template <typename T>
 hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt,
@@ -60,12 +61,11 @@ hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, 
 // Matrix-core decode (bf16, d in {64,128}, d_down in {16,32}, <= 8 query heads
 // per KV head); shares decode_combine_kernel with the vector-ALU path.
 bool decode_mfma_supported(int d, int dd, int G, bool bf16);
-void decode_mfma_splits(int len, int w, int& n_lat_split, int& n_win_split);
+// P = partial records per query head; P == 1: the output is already written.
 hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
                               const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_lat,
-                              const bf16_t* v_lat, float* part, int B, int Hq, int Hkv, int d,
-                              int dd, int w, int cap, int len, int& n_lat_split, int& S,
-                              hipStream_t st);
+                              const bf16_t* v_lat, float* part, bf16_t* o, int B, int Hq, int Hkv,
+                              int d, int dd, int w, int cap, int len, int& P, hipStream_t st);
 
 template <typename T>
 hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,

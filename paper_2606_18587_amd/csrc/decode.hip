@@ -11,9 +11,9 @@
 // values with p = exp2(s - max). Output per (head, split): {m, l, acc} with
 // acc in d_down space for latent splits and in d space for window splits.
 //
-// Stage 2 (decode_combine_kernel): one block per (batch, query head) merges
-// the splits under one max (Eq. 4 is a single softmax over both regions),
-// lifts the latent part once, o = (o_win + o_lat W_up) / l.
+// Stage 2 (decode_combine_kernel): one wavefront per (batch, query head)
+// merges the partial records under one max (Eq. 4 is a single softmax over
+// both regions) and lifts the latent part once, o = (o_win + o_lat W_up) / l.
 #include "dar_common.hpp"
 #include "dar_kernels.hpp"
 
@@ -222,75 +222,120 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
         for (int hh = 0; hh < G; ++hh) mred[wave][hh] = lsum[hh];
     }
     __syncthreads();
-    const int stride = 2 + d;
-    for (int idx = tid; idx < G * (dim + 2); idx += kDecThreads) {
-        const int hh = idx / (dim + 2), f = idx - (idx / (dim + 2)) * (dim + 2);
-        float val;
+    // partial record {m, l, acc_lat[dd], acc_win[d]}: this split fills the
+    // part of its region and zeroes the other
+    const int stride = 2 + dd + d;
+    const int lo = latent ? 2 : 2 + dd;
+    for (int idx = tid; idx < G * stride; idx += kDecThreads) {
+        const int hh = idx / stride, f = idx - (idx / stride) * stride;
+        float val = 0.f;
         if (f == 0) val = mx[hh];
         else if (f == 1) val = mred[0][hh] + mred[1][hh] + mred[2][hh] + mred[3][hh];
-        else val = red[0][hh][f - 2] + red[1][hh][f - 2] + red[2][hh][f - 2] + red[3][hh][f - 2];
+        else if (f >= lo && f < lo + dim)
+            val = red[0][hh][f - lo] + red[1][hh][f - lo] + red[2][hh][f - lo] + red[3][hh][f - lo];
         const size_t bh = (size_t)b * Hq + (size_t)g * G + hh;
         part[(bh * S + s) * stride + f] = val;
     }
 }
 
-// One wavefront per (batch, query head). Lanes over splits compute the global
-// maximum and the merged row sum; lanes over output columns accumulate the
-// latent (d_down) and window (d) parts, then lift the latent part with W_up.
+// One wavefront per (batch, query head) merges its S partial records
+// {m, l, acc_lat[dd], acc_win[d]} under one maximum (Eq. 4 is a single
+// softmax over both regions), lifts the latent part once and normalises:
+// o = (acc_win + acc_lat W_up) / l. Every global load of a phase is
+// independent of the others, so each phase costs one memory round trip: the
+// W_up column of the lane is fetched first, split weights are broadcast from
+// the lane that owns the split, and partial rows are read eight at a time.
 template <typename T>
 __global__ __launch_bounds__(64) void decode_combine_kernel(
     const float* __restrict__ part, const T* __restrict__ wd, const T* __restrict__ wu,
-    T* __restrict__ o, int Hq, int Hkv, int d, int dd, int n_lat_split, int S) {
+    T* __restrict__ o, int Hq, int Hkv, int d, int dd, int S) {
+    constexpr int kLiftCols = 32;  // W_up rows held in registers (d_down <= 32, d <= 64)
     const int bh = blockIdx.x;
     const int h = bh % Hq;
     const int g = h / (Hq / Hkv);
     const int lane = threadIdx.x;
-    const int stride = 2 + d;
+    const int stride = 2 + dd + d;
     const float* pp = part + (size_t)bh * S * stride;
     const T* wdg = wd + (size_t)g * d * dd;
     const T* wug = wu ? wu + (size_t)g * dd * d : nullptr;
+    const bool lift_regs = dd <= kLiftCols && d <= 64;
+
+    const T* wp = wug ? wug + imin(lane, d - 1) : wdg + (size_t)imin(lane, d - 1) * dd;
+    const int wstep = wug ? d : 1;  // distance between consecutive latent columns c
+    float wcol[kLiftCols];
+#pragma unroll
+    for (int c = 0; c < kLiftCols; ++c)
+        wcol[c] = (lift_regs && c < dd) ? elem<T>::load(wp + (size_t)c * wstep) : 0.f;
 
     // split weights: w_s = 2^(m_s - M), L = sum_s w_s l_s
     float M = -INFINITY;
     for (int s = lane; s < S; s += 64) M = fmaxf(M, pp[(size_t)s * stride]);
     M = wave_max(M);
     float L = 0.f;
-    for (int s = lane; s < S; s += 64) L += exp2f(pp[(size_t)s * stride] - M) * pp[(size_t)s * stride + 1];
+    for (int s = lane; s < S; s += 64) {
+        const float ms = pp[(size_t)s * stride];
+        if (ms != -INFINITY) L += exp2f(ms - M) * pp[(size_t)s * stride + 1];
+    }
     L = wave_sum(L);
     const float inv = 1.f / L;
 
-    // latent part (columns c < dd) and window part (columns e < d)
+    // lane owns latent columns lane + 64 r (< dd) and window columns lane + 64 r (< d)
     float lat[4] = {0.f, 0.f, 0.f, 0.f};
     float win[4] = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < S; ++s) {
-        const float ws = exp2f(pp[(size_t)s * stride] - M);
-        const float* a = pp + (size_t)s * stride + 2;
-        if (s < n_lat_split) {
+    for (int s0 = 0; s0 < S; s0 += 64) {
+        float wl = 0.f;  // weight of split s0 + lane, broadcast below
+        if (s0 + lane < S) {
+            const float ms = pp[(size_t)(s0 + lane) * stride];
+            wl = ms == -INFINITY ? 0.f : exp2f(ms - M);
+        }
+        const int ns = imin(64, S - s0);
+        for (int j0 = 0; j0 < ns; j0 += 8) {
+            float al[8][4], aw[8][4];
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                if (lane + 64 * r < dd) lat[r] = __builtin_fmaf(ws, a[lane + 64 * r], lat[r]);
-        } else {
+            for (int j = 0; j < 8; ++j) {
+                const float* row = pp + (size_t)(s0 + imin(j0 + j, ns - 1)) * stride + 2;
 #pragma unroll
-            for (int r = 0; r < 4; ++r)
-                if (lane + 64 * r < d) win[r] = __builtin_fmaf(ws, a[lane + 64 * r], win[r]);
+                for (int r = 0; r < 4; ++r) {
+                    const int e = lane + 64 * r;
+                    al[j][r] = e < dd ? row[e] : 0.f;
+                    aw[j][r] = e < d ? row[dd + e] : 0.f;
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float ws = (j0 + j < ns) ? __shfl(wl, j0 + j, 64) : 0.f;
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    lat[r] = __builtin_fmaf(ws, al[j][r], lat[r]);
+                    win[r] = __builtin_fmaf(ws, aw[j][r], win[r]);
+                }
+            }
         }
     }
-    // o[e] = (win[e] + sum_c lat[c] W_up[c][e]) / L
+    if (lift_regs) {
+        float acc = win[0];
+#pragma unroll
+        for (int c = 0; c < kLiftCols; ++c) {
+            if (c >= dd) break;
+            acc = __builtin_fmaf(__shfl(lat[0], c, 64), wcol[c], acc);
+        }
+        if (lane < d) o[(size_t)bh * d + lane] = elem<T>::from_f32(acc * inv);
+        return;
+    }
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int e = lane + 64 * r;
         float acc = win[r];
-        if (n_lat_split > 0) {
 #pragma unroll
-            for (int r2 = 0; r2 < 4; ++r2)
-                for (int c2 = 0; c2 < 64 && 64 * r2 + c2 < dd; ++c2) {
-                    const int c = 64 * r2 + c2;
-                    const float lc = __shfl(lat[r2], c2, 64);
-                    const float u = wug ? elem<T>::load(wug + (size_t)c * d + (e < d ? e : 0))
-                                        : elem<T>::load(wdg + (size_t)(e < d ? e : 0) * dd + c);
-                    acc = __builtin_fmaf(lc, u, acc);
-                }
-        }
+        for (int r2 = 0; r2 < 4; ++r2)
+#pragma unroll 1
+            for (int c2 = 0; c2 < 64 && 64 * r2 + c2 < dd; ++c2) {
+                const int c = 64 * r2 + c2;
+                const float lc = __shfl(lat[r2], c2, 64);
+                const float u = wug ? elem<T>::load(wug + (size_t)c * d + (e < d ? e : 0))
+                                    : elem<T>::load(wdg + (size_t)(e < d ? e : 0) * dd + c);
+                acc = __builtin_fmaf(lc, u, acc);
+            }
         if (e < d) o[(size_t)bh * d + e] = elem<T>::from_f32(acc * inv);
     }
 }
@@ -314,19 +359,14 @@ DecodeSplits decode_splits(int len, int w, int d, int dd, int G) {
     return sp;
 }
 
-int decode_max_splits(int cap, int w, int d, int dd, int G) {
-    // the split count grows with the cache length; bound it at len = cap for
-    // both split schemes (vector-ALU and matrix-core)
+int decode_max_partials(int B, int Hkv, int cap, int w, int d, int dd, int G) {
+    // both counts grow with the cache length: bound them at len = cap
     DecodeSplits a = decode_splits(cap, w, d, dd, G);
     DecodeSplits b = decode_splits(cap, 0, d, dd, G);
     int m = a.n_lat_split + a.n_win_split;
     m = m > b.n_lat_split + b.n_win_split ? m : b.n_lat_split + b.n_win_split;
-    int l1, w1, l2, w2;
-    decode_mfma_splits(cap, w, l1, w1);
-    decode_mfma_splits(cap, 0, l2, w2);
-    m = m > l1 + w1 ? m : l1 + w1;
-    m = m > l2 + w2 ? m : l2 + w2;
-    return m + 1;
+    const int p = decode_mfma_parts(B, Hkv, cap, w, d);
+    return m > p ? m : p;
 }
 
 template <typename T, int G>
@@ -343,7 +383,7 @@ static hipError_t launch_decode_g(const T* q, const T* wd, const T* wu, const T*
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu, o,
-                       Hq, Hkv, d, dd, sp.n_lat_split, S);
+                       Hq, Hkv, d, dd, S);
     return hipGetLastError();
 }
 
@@ -352,14 +392,14 @@ hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, c
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
                          int d, int dd, int w, int cap, int len, hipStream_t st) {
     if (decode_mfma_supported(d, dd, Hq / Hkv, sizeof(T) == 2)) {
-        int n_lat_split = 0, S = 0;
+        int P = 0;
         hipError_t e = launch_decode_mfma((const bf16_t*)q, (const bf16_t*)wd, (const bf16_t*)wu,
                                           (const bf16_t*)k_win, (const bf16_t*)v_win,
-                                          (const bf16_t*)k_lat, (const bf16_t*)v_lat, part, B, Hq,
-                                          Hkv, d, dd, w, cap, len, n_lat_split, S, st);
-        if (e != hipSuccess) return e;
+                                          (const bf16_t*)k_lat, (const bf16_t*)v_lat, part,
+                                          (bf16_t*)o, B, Hq, Hkv, d, dd, w, cap, len, P, st);
+        if (e != hipSuccess || P == 1) return e;
         hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu,
-                           o, Hq, Hkv, d, dd, n_lat_split, S);
+                           o, Hq, Hkv, d, dd, P);
         return hipGetLastError();
     }
     switch (Hq / Hkv) {

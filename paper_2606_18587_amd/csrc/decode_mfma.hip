@@ -1,8 +1,11 @@
 // Split-KV DAR decode on the matrix cores (bf16; d in {64, 128}, d_down in
 // {16, 32}, up to 8 query heads per KV head).
 //
-// One workgroup = 4 wavefronts = one split of one (batch, KV head); each
-// wavefront walks its own run of 32-token subtiles of one region:
+// Work split: each (batch, KV head) gets P workgroups of NW wavefronts, P
+// chosen so that the whole grid is about one round of resident workgroups
+// (no tail). The P*NW wavefronts are dealt to the two regions in proportion
+// to the cache bytes each region holds, and each wavefront walks one
+// contiguous run of 32-token subtiles of one region:
 //   latent region (tokens [0, len - w)): S = C^K Q~^T with q~ = q W_up^T
 //     (W_up absorbed, Limitations section), values in d_down space;
 //   window region (the ring, tokens [len - w, len)): S = K Q^T, full d.
@@ -16,9 +19,11 @@
 // subtile maximum exceeds it by kTau. With d_down = 16 the V^T operand rows
 // 16..31 carry a constant [1, 0, 0, 0] chunk, so O^T row 16 is the row sum.
 //
-// Per split the four wavefronts merge through LDS and write one partial
-// {m, l, acc} per query head; decode_combine_kernel merges the splits, lifts
-// the latent part with W_up and normalises (Eq. 4, one softmax).
+// The wavefronts of a workgroup merge through LDS. With one workgroup per
+// (batch, KV head) it lifts the latent part with W_up, normalises (Eq. 4, one
+// softmax) and writes the output itself; otherwise it writes one partial
+// {m, l, acc_lat[d_down], acc_win[d]} per query head and
+// decode_combine_kernel finishes.
 #include "../../include/dar.h"
 #include "dar_common.hpp"
 #include "dar_kernels.hpp"
@@ -73,15 +78,49 @@ __device__ __forceinline__ int dperm(int R) {
     return 16 * (a >> 1) + 8 * gg + 4 * (a & 1) + b;
 }
 
+// The reference m is kept exactly representable in bf16 (rounded up when it
+// moves), so that the latent scores can subtract it inside the MFMA: a rank-1
+// product of a constant operand (1 in contraction slot 0 of every key row)
+// and negm (-m of each head in slot 0) yields -m in every accumulator.
 struct DecState {
     float m, cm, thr, l;
+    dbf16x8 negm;  // B operand: -m at contraction slot 0 (lanes of half 0), zeros elsewhere
 };
+
+// Marks a rarely taken, wave-uniform branch: the compiler may not execute its
+// body unconditionally (if-converted, every subtile would pay for it).
+__device__ __forceinline__ void keep_branch() { __asm__ volatile(""); }
+
+// A pointer every lane of the wavefront holds, moved to scalar registers.
+__device__ __forceinline__ const bf16_t* uniform_ptr(const bf16_t* p) {
+    const uint64_t u = (uint64_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+    return (const bf16_t*)(((uint64_t)hi << 32) | lo);
+}
+
+// bf16 value >= x (x finite): round the fp32 bit pattern up to 16 bits
+__device__ __forceinline__ float bf16_ceil(float x) {
+    uint32_t u = __float_as_uint(x);
+    const uint32_t low = u & 0xffffu;
+    u &= 0xffff0000u;
+    if (low != 0) u += (x > 0.f) ? 0x10000u : 0u;  // away from zero for positives, truncation for negatives
+    return __uint_as_float(u);
+}
 
 // Online softmax over one subtile's 16 scores per lane (already relative to
 // the reference). Rescales acc on a reference move; packs P^T; adds the
 // bf16-rounded p to l when SUMV.
+// B operand with -m (= cm, bf16-exact) at contraction slot 0: lane half 0,
+// element 0 of the 8-element run
+__device__ __forceinline__ dbf16x8 negm_operand(float cm, int hg) {
+    const uint32_t b = __float_as_uint(cm) >> 16;  // exact: cm is a bf16 value
+    return __builtin_bit_cast(dbf16x8, make_uint4(hg == 0 ? b : 0u, 0u, 0u, 0u));
+}
+
 template <int NT, bool SUMV>
-__device__ __forceinline__ void dstep(df32x16& x, DecState& st, df32x16 (&acc)[NT], dbf16x8& p0, dbf16x8& p1) {
+__device__ __forceinline__ void dstep(df32x16& x, DecState& st, df32x16 (&acc)[NT], dbf16x8& p0, dbf16x8& p1,
+                                      int hg) {
     float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), x[2]), fmaxf(x[3], x[4]));
     mx = fmaxf(fmaxf(mx, x[5]), fmaxf(x[6], x[7]));
     mx = fmaxf(fmaxf(mx, x[8]), fmaxf(x[9], x[10]));
@@ -90,17 +129,21 @@ __device__ __forceinline__ void dstep(df32x16& x, DecState& st, df32x16 (&acc)[N
     mx = pmax(mx);
     const bool need = mx > st.thr;
     if (__builtin_amdgcn_ballot_w64(need)) {
+        keep_branch();
+        // new reference: the subtile maximum, rounded up to a bf16 value
         const bool fresh = st.m == -INFINITY;
-        const float delta = need ? mx : 0.f;
+        const float mnew = need ? bf16_ceil(fresh ? mx : st.m + mx) : st.m;
+        const float delta = need ? (fresh ? mnew : mnew - st.m) : 0.f;  // x is relative to the old reference (0 if none)
         const float fac = need ? (fresh ? 0.f : exp2f(-delta)) : 1.f;
 #pragma unroll
         for (int t = 0; t < NT; ++t)
 #pragma unroll
             for (int r = 0; r < 16; ++r) acc[t][r] *= fac;
         st.l *= fac;
-        if (need) st.m = fresh ? mx : st.m + delta;
+        st.m = mnew;
         st.cm = (st.m == -INFINITY) ? 0.f : -st.m;
         st.thr = (st.m == -INFINITY) ? -INFINITY : kTau;
+        st.negm = negm_operand(st.cm, hg);
 #pragma unroll
         for (int r = 0; r < 16; ++r) x[r] -= delta;
     }
@@ -127,25 +170,81 @@ __device__ __forceinline__ void dstep(df32x16& x, DecState& st, df32x16 (&acc)[N
 
 }  // namespace
 
-// Tokens per wavefront in each region (multiples of 32).
-constexpr int kDecWaveLat = 512;
-constexpr int kDecWaveWin = 128;
-constexpr int kDecMaxGroup = 8;  // query heads per KV head on this path
+constexpr int kDecMaxGroup = 8;   // query heads per KV head on this path
+// Word 3 of a raw buffer descriptor on gfx9-family parts (32-bit data
+// format; with stride 0, accesses at or past num_records return zero).
+constexpr int kBufWord3 = 0x00020000;
+constexpr int kDecMinSub = 4;     // fewest subtiles a wavefront is given, when possible
 
+// Subtile run of wavefront `idx` (of nwave per (batch, KV head)). Waves
+// [0, nwl) share the latent subtiles, waves [nwl, nwave) the ring subtiles;
+// nwl is proportional to the latent region's share of the cache bytes.
+struct WaveRun {
+    int latent;        // 1: latent region, 0: window region
+    int t_begin, t_end;  // token positions [t_begin, t_end)
+};
+
+__host__ __device__ inline WaveRun decode_wave_run(int len, int w, int D, int DD, int nwave, int idx) {
+    const int n_lat = len - w > 0 ? len - w : 0;
+    const int n_win = len - n_lat;
+    const long long nls = (n_lat + 31) / 32, nws = (n_win + 31) / 32;
+    int nwr = 0;  // wavefronts on the ring
+    if (nws > 0) {
+        if (nls == 0) {
+            nwr = nwave;
+        } else {
+            const long long cw = nws * D, cl = nls * DD;
+            nwr = (int)((2 * nwave * cw + cl + cw) / (2 * (cl + cw)));  // rounded share
+            nwr = nwr < 1 ? 1 : (nwr > nwave - 1 ? nwave - 1 : nwr);
+        }
+    }
+    const int nwl = nwave - nwr;
+    WaveRun r;
+    if (idx < nwl) {
+        const long long s0 = nls * idx / nwl, s1 = nls * (idx + 1) / nwl;
+        r.latent = 1;
+        r.t_begin = (int)(32 * s0);
+        r.t_end = (int)(32 * s1 < n_lat ? 32 * s1 : n_lat);
+    } else {
+        const int j = idx - nwl;
+        const long long s0 = nws * j / nwr, s1 = nws * (j + 1) / nwr;
+        r.latent = 0;
+        r.t_begin = n_lat + (int)(32 * s0);
+        r.t_end = n_lat + (int)(32 * s1 < n_win ? 32 * s1 : n_win);
+    }
+    return r;
+}
+
+// NW = 8 wavefronts per workgroup: one workgroup per compute unit, 2 waves
+// per SIMD, so that each wavefront can keep many subtiles in flight.
+template <int D>
+struct DecWaves {
+    static constexpr int value = 8;
+};
+// Latent subtiles in flight per wavefront (register budget of 2 waves/SIMD).
 template <int D, int DD>
-__global__ __launch_bounds__(256) void decode_mfma_kernel(
+struct DecStages {
+    static constexpr int value = D <= 64 ? (DD <= 16 ? 12 : 7) : (DD <= 16 ? 10 : 5);
+};
+
+template <int D, int DD, int NW>
+__global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
     const bf16_t* __restrict__ k_win, const bf16_t* __restrict__ v_win,
     const bf16_t* __restrict__ k_lat, const bf16_t* __restrict__ v_lat, float* __restrict__ part,
-    int Hq, int Hkv, int w, int cap, int len, int n_lat_split, int S, float qscale) {
+    bf16_t* __restrict__ o, int Hq, int Hkv, int w, int cap, int len, int P, float qscale) {
     constexpr int KS = D / 16, DS = DD / 16, NT = D / 32;
     constexpr int LDW = D + 8;                      // padded ring row in LDS (bf16)
     constexpr int VBUF = 32 * LDW;                  // per-wave V staging (bf16 elements)
-    __shared__ __attribute__((aligned(16))) bf16_t vbuf[kWaves][VBUF + 8];
-    __shared__ float red_m[kWaves][kDecMaxGroup], red_l[kWaves][kDecMaxGroup];
-    __shared__ float red_o[kWaves][kDecMaxGroup][D + 1];
+    constexpr int stride = 2 + DD + D;              // partial record {m, l, acc_lat, acc_win}
+    __shared__ __attribute__((aligned(16))) bf16_t vbuf[NW][VBUF + 8];
+    __shared__ float red_m[NW][kDecMaxGroup], red_l[NW][kDecMaxGroup];
+    __shared__ float red_o[NW][kDecMaxGroup][D + 1];
+    __shared__ int red_lat[NW];
+    __shared__ float wsh[DD][D];                    // W_up (fp32), used when P == 1
+    __shared__ float mrg[kDecMaxGroup][stride];     // merged record, used when P == 1
 
-    const int s = blockIdx.x;
+    const int s = blockIdx.x;  // part of this (batch, KV head), < P
     const int bg = blockIdx.y;
     const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
     const int G = Hq / Hkv;
@@ -153,17 +252,18 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
     const int col = lane & 31, hg = lane >> 5;
-    const int n_lat = imax(0, len - w);
-    const bool latent = s < n_lat_split;
-    int t_begin, t_end;  // this wavefront's token range (positions)
-    if (latent) {
-        t_begin = imin(n_lat, s * kWaves * kDecWaveLat + wave * kDecWaveLat);
-        t_end = imin(n_lat, t_begin + kDecWaveLat);
-    } else {
-        const int s2 = s - n_lat_split;
-        t_begin = imin(len, n_lat + s2 * kWaves * kDecWaveWin + wave * kDecWaveWin);
-        t_end = imin(len, t_begin + kDecWaveWin);
+    const bool fuse = P == 1;  // one workgroup per (batch, KV head): finish here
+    if (fuse) {
+        const bf16_t* wdg = wd + (size_t)g * D * DD;
+        const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
+        for (int idx = tid; idx < DD * D; idx += NW * 64) {
+            const int c = idx / D, e = idx - (idx / D) * D;
+            wsh[c][e] = bf16_to_f32(wug ? wug[(size_t)c * D + e] : wdg[(size_t)e * DD + c]);
+        }
     }
+    const WaveRun run = decode_wave_run(len, w, D, DD, P * NW, s * NW + wave);
+    const bool latent = run.latent != 0;
+    const int t_begin = run.t_begin, t_end = run.t_end;  // this wavefront's tokens
     bf16_t* vb = vbuf[wave];
     // constant chunk [1, 0, 0, 0] for the rows of the latent V^T operand past d_down
     if (lane == 0) {
@@ -180,14 +280,46 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(
 #pragma unroll
     for (int k = 0; k < KS; ++k) qop[k] = hval ? ld8(qrow + k * 16 + hg * 8) : zero8();
 
-    DecState st{-INFINITY, 0.f, -INFINITY, 0.f};
-    df32x16 acc[NT];
-#pragma unroll
-    for (int t = 0; t < NT; ++t) acc[t] = fill16(0.f);
+    DecState st{-INFINITY, 0.f, -INFINITY, 0.f, zero8()};
     const int quad = lane >> 4, sl = lane & 15;
     const int prow = dperm(col);
 
     if (t_begin < t_end && latent) {
+        df32x16 acc[1] = {fill16(0.f)};  // O_lat^T (rows < d_down; row 16 = row sum when d_down = 16)
+        // Latent rows through buffer loads whose size ends at the run's last
+        // token: rows at or past t_end read as zeros, so the prefetches past
+        // the run need no clamping and stay inside this head's latents.
+        const bf16_t* kl = k_lat + (size_t)bg * cap * DD;
+        const bf16_t* vl = v_lat + (size_t)bg * cap * DD;
+        const int last = t_end - 1;
+        // the descriptors are wave-uniform: keep them in scalar registers
+        const int nbytes = __builtin_amdgcn_readfirstlane(t_end * DD * 2);
+        const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(kl), (short)0, nbytes, kBufWord3);
+        const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(vl), (short)0, nbytes, kBufWord3);
+        const int koff = (t_begin + prow) * DD * 2 + hg * 16;  // A-operand row of subtile 0
+        const int voff = t_begin * DD * 2 + lane * 16;         // 16-byte chunk of subtile 0
+        constexpr int kSubBytes = 32 * DD * 2;
+        // A operand of the rank-1 reference product: 1 at contraction slot 0
+        const dbf16x8 ones_a = __builtin_bit_cast(dbf16x8, make_uint4(hg == 0 ? 0x3f80u : 0u, 0u, 0u, 0u));
+        auto load = [&](int t0, dbf16x8 (&ak)[DS], uint4 (&vv)[DS]) {
+            const int o = (t0 - t_begin) * DD * 2;
+#pragma unroll
+            for (int k = 0; k < DS; ++k)
+                ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + o + k * 32, 0, 0));
+#pragma unroll
+            for (int k = 0; k < DS; ++k)
+                vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + o + k * 1024, 0, 0));
+        };
+        static_assert(kSubBytes == 1024 * DS, "one V chunk of 16 bytes per lane per 16 latent columns");
+        // NST subtiles in flight per wavefront (the stream is latency bound:
+        // the depth, not the arithmetic, sets its rate), issued before the
+        // query absorption below so that its latency overlaps theirs
+        constexpr int NST = DecStages<D, DD>::value;
+        dbf16x8 aks[NST][DS];
+        uint4 vs[NST][DS];
+#pragma unroll
+        for (int j = 0; j < NST; ++j) load(t_begin + 32 * j, aks[j], vs[j]);
+
         // ---- q~^T = W_up q^T, scaled; rearranged from the accumulator layout
         // (lane half g holds columns 4g..4g+3, 8+4g..8+4g+3 of each 16) to the
         // B-operand layout (half g holds 8g..8g+7) with one swap across halves.
@@ -223,34 +355,20 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(
             qtop[k] = pk8(v8);
         }
 
-        const bf16_t* kl = k_lat + (size_t)bg * cap * DD;
-        const bf16_t* vl = v_lat + (size_t)bg * cap * DD;
-        const int last = t_end - 1;
-        // V subtile copy: lane l moves 16 bytes (DS chunks of 64 lanes)
-        auto load = [&](int t0, dbf16x8 (&ak)[DS], uint4 (&vv)[DS]) {
-            const int kr = imin(t0 + prow, last);
-#pragma unroll
-            for (int k = 0; k < DS; ++k) ak[k] = ld8(kl + (size_t)kr * DD + k * 16 + hg * 8);
-#pragma unroll
-            for (int k = 0; k < DS; ++k) {
-                const int chunk = lane + 64 * k;            // 16-byte chunk of the 32 x DD tile
-                const int tr = imin(t0 + chunk / (DD / 8), last);
-                vv[k] = *reinterpret_cast<const uint4*>(vl + (size_t)tr * DD + (chunk % (DD / 8)) * 8);
-            }
-        };
         auto body = [&](int t0, const dbf16x8 (&ak)[DS], const uint4 (&vv)[DS]) {
 #pragma unroll
             for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vb + (lane + 64 * k) * 8) = vv[k];
-            df32x16 x = mma(ak[0], qtop[0], fill16(st.cm));
+            df32x16 x = mma(ak[0], qtop[0], mma(ones_a, st.negm, fill16(0.f)));
 #pragma unroll
             for (int k = 1; k < DS; ++k) x = mma(ak[k], qtop[k], x);
             if (t0 + 31 > last) {
+                keep_branch();
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     if (t0 + dkey(r, hg) > last) x[r] = -INFINITY;
             }
             dbf16x8 p0, p1;
-            dstep<NT, DD != 16>(x, st, acc, p0, p1);
+            dstep<1, DD != 16>(x, st, acc, p0, p1, hg);
             // V^T operand: rows c = lane%32 of the DD-wide tile
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
@@ -272,21 +390,30 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(
                 acc[0] = mma(a, half ? p1 : p0, acc[0]);
             }
         };
-        dbf16x8 akA[DS], akB[DS];
-        uint4 vA[DS], vB[DS];
-        load(t_begin, akA, vA);
-        load(t_begin + 32, akB, vB);
         int t0 = t_begin;
-        for (; t0 + 32 < t_end; t0 += 64) {
-            body(t0, akA, vA);
-            load(t0 + 64, akA, vA);
-            body(t0 + 32, akB, vB);
-            load(t0 + 96, akB, vB);
+        for (; t0 + 32 * (NST - 1) < t_end; t0 += 32 * NST) {
+#pragma unroll
+            for (int j = 0; j < NST; ++j) {
+                body(t0 + 32 * j, aks[j], vs[j]);
+                load(t0 + 32 * (j + NST), aks[j], vs[j]);
+            }
         }
-        if (t0 < t_end) body(t0, akA, vA);
+#pragma unroll
+        for (int j = 0; j < NST - 1; ++j)
+            if (t0 + 32 * j < t_end) body(t0 + 32 * j, aks[j], vs[j]);
         if (DD == 16) st.l = acc[0][8];  // ones row: full row sum on both halves
         else st.l = psum(st.l);
+        if (col < G) {
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int row = 8 * (r >> 2) + 4 * hg + (r & 3);
+                if (row < DD) red_o[wave][col][row] = acc[0][r];
+            }
+        }
     } else if (t_begin < t_end) {
+        df32x16 acc[NT];  // O_win^T
+#pragma unroll
+        for (int t = 0; t < NT; ++t) acc[t] = fill16(0.f);
         // ---- window region: full-d keys and values from the ring
         const bf16_t* kw = k_win + (size_t)bg * w * D;
         const bf16_t* vw = v_win + (size_t)bg * w * D;
@@ -316,12 +443,13 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(
 #pragma unroll
             for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], qscale, st.cm);
             if (t0 + 31 > last) {
+                keep_branch();
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
                     if (t0 + dkey(r, hg) > last) x[r] = -INFINITY;
             }
             dbf16x8 p0, p1;
-            dstep<NT, true>(x, st, acc, p0, p1);
+            dstep<NT, true>(x, st, acc, p0, p1, hg);
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -342,45 +470,59 @@ __global__ __launch_bounds__(256) void decode_mfma_kernel(
             body(t0, akA, vA);
         }
         st.l = psum(st.l);
+        if (col < G) {
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) red_o[wave][col][t * 32 + 8 * (r >> 2) + 4 * hg + (r & 3)] = acc[t][r];
+        }
     }
 
-    // ---- merge the wavefronts of this split and write the partials
-    const int dim = latent ? DD : D;
+    // ---- merge the wavefronts of this workgroup and write the partials
+    // {m, l, acc_lat[DD], acc_win[D]}; each wavefront contributes to the part
+    // of its region (an empty run has m = -inf and contributes nothing)
     if (col < G && hg == 0) {
         red_m[wave][col] = st.m;
         red_l[wave][col] = st.l;
     }
-    if (col < G) {
-#pragma unroll
-        for (int t = 0; t < NT; ++t)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int row = t * 32 + 8 * (r >> 2) + 4 * hg + (r & 3);
-                if (row < dim) red_o[wave][col][row] = acc[t][r];
-            }
-    }
+    if (lane == 0) red_lat[wave] = latent ? 1 : 0;
     __syncthreads();
-    const int stride = 2 + D;
-    for (int idx = tid; idx < G * (dim + 2); idx += 256) {
-        const int h = idx / (dim + 2), f = idx - (idx / (dim + 2)) * (dim + 2);
+    for (int idx = tid; idx < G * stride; idx += NW * 64) {
+        const int h = idx / stride, f = idx - (idx / stride) * stride;
         float M = -INFINITY;
 #pragma unroll
-        for (int v = 0; v < kWaves; ++v) M = fmaxf(M, red_m[v][h]);
+        for (int v = 0; v < NW; ++v) M = fmaxf(M, red_m[v][h]);
         float val = 0.f;
         if (f == 0) {
             val = M;
         } else {
+            const int want_lat = f < 2 + DD ? 1 : 0;
+            const int row = f < 2 + DD ? f - 2 : f - 2 - DD;
 #pragma unroll
-            for (int v = 0; v < kWaves; ++v) {
+            for (int v = 0; v < NW; ++v) {
                 const float mv = red_m[v][h];
-                if (mv != -INFINITY) {
+                if (mv != -INFINITY && (f == 1 || red_lat[v] == want_lat)) {
                     const float wgt = exp2f(mv - M);
-                    val += wgt * (f == 1 ? red_l[v][h] : red_o[v][h][f - 2]);
+                    val += wgt * (f == 1 ? red_l[v][h] : red_o[v][h][row]);
                 }
             }
         }
-        const size_t bh = (size_t)b * Hq + (size_t)g * G + h;
-        part[(bh * S + s) * stride + f] = val;
+        if (fuse) {
+            mrg[h][f] = val;
+        } else {
+            const size_t bh = (size_t)b * Hq + (size_t)g * G + h;
+            part[(bh * P + s) * stride + f] = val;
+        }
+    }
+    if (!fuse) return;
+    // o = (acc_win + acc_lat W_up) / l (Eq. 2 lift applied once, Eq. 4 normalisation)
+    __syncthreads();
+    for (int idx = tid; idx < G * D; idx += NW * 64) {
+        const int h = idx / D, e = idx - (idx / D) * D;
+        float acc = mrg[h][2 + DD + e];
+#pragma unroll
+        for (int c = 0; c < DD; ++c) acc = __builtin_fmaf(mrg[h][2 + c], wsh[c][e], acc);
+        o[((size_t)b * Hq + (size_t)g * G + h) * D + e] = f32_to_bf16(acc / mrg[h][1]);
     }
 }
 
@@ -388,26 +530,33 @@ bool decode_mfma_supported(int d, int dd, int G, bool bf16) {
     return bf16 && (d == 64 || d == 128) && (dd == 16 || dd == 32) && G >= 1 && G <= kDecMaxGroup;
 }
 
-void decode_mfma_splits(int len, int w, int& n_lat_split, int& n_win_split) {
+int decode_mfma_parts(int B, int Hkv, int len, int w, int d) {
+    // about one round of resident workgroups on the 256 compute units of a
+    // gfx950 part, one workgroup per unit. Fixed, so that the workspace size
+    // is a pure function of the shape.
+    const int nw = d <= 64 ? DecWaves<64>::value : DecWaves<128>::value;
+    const long long pairs = (long long)B * Hkv;
+    long long P = (256 + pairs - 1) / pairs;
     const int n_lat = len - w > 0 ? len - w : 0;
-    const int n_win = len - n_lat;
-    n_lat_split = (n_lat + kWaves * kDecWaveLat - 1) / (kWaves * kDecWaveLat);
-    n_win_split = (n_win + kWaves * kDecWaveWin - 1) / (kWaves * kDecWaveWin);
+    const long long nsub = (n_lat + 31) / 32 + (len - n_lat + 31) / 32;
+    const long long by_work = nsub / (nw * kDecMinSub);
+    if (P > by_work) P = by_work;
+    if (P < 1) P = 1;
+    if (P > 1024) P = 1024;
+    return (int)P;
 }
 
 hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
                               const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_lat,
-                              const bf16_t* v_lat, float* part, int B, int Hq, int Hkv, int d,
-                              int dd, int w, int cap, int len, int& n_lat_split, int& S,
-                              hipStream_t st) {
-    int n_win_split;
-    decode_mfma_splits(len, w, n_lat_split, n_win_split);
-    S = n_lat_split + n_win_split;
+                              const bf16_t* v_lat, float* part, bf16_t* o, int B, int Hq, int Hkv,
+                              int d, int dd, int w, int cap, int len, int& P, hipStream_t st) {
+    P = decode_mfma_parts(B, Hkv, len, w, d);
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
-    dim3 grid(S, B * Hkv);
-#define DAR_DEC_LAUNCH(D_, DD_)                                                                   \
-    hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_>), grid, dim3(256), 0, st, q, wd, wu, k_win,   \
-                       v_win, k_lat, v_lat, part, Hq, Hkv, w, cap, len, n_lat_split, S, qscale)
+    dim3 grid(P, B * Hkv);
+#define DAR_DEC_LAUNCH(D_, DD_)                                                                     \
+    hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value>), grid,                    \
+                       dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
+                       part, o, Hq, Hkv, w, cap, len, P, qscale)
     if (d == 64 && dd == 16) DAR_DEC_LAUNCH(64, 16);
     else if (d == 64 && dd == 32) DAR_DEC_LAUNCH(64, 32);
     else if (d == 128 && dd == 16) DAR_DEC_LAUNCH(128, 16);

@@ -149,6 +149,7 @@ __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x
     mx = pair_max(mx);
     const bool need = mx > st.thr;
     if (__builtin_amdgcn_ballot_w64(need)) {
+        __asm__ volatile("");  // a real branch: never if-converted into every subtile
         const bool fresh = st.m == -INFINITY;
         const float delta = need ? mx : 0.f;
         const float fac = need ? (fresh ? 0.f : exp2f(-delta)) : 1.f;

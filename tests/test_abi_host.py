@@ -72,7 +72,7 @@ def test_decode_workspace_size_grows_with_capacity():
     a = dar.dar_decode_workspace_bytes(s, 1000)
     b = dar.dar_decode_workspace_bytes(s, 100000)
     assert 0 < a < b
-    assert a % (s.B * s.Hq * (2 + s.d) * 4) == 0
+    assert a % (s.B * s.Hq * (2 + s.d_down + s.d) * 4) == 0
     assert dar.dar_decode_workspace_bytes(S(Hq=12, Hkv=4), 100) == 0  # group of 3: unsupported
 
 

@@ -119,3 +119,11 @@ def test_decode_full_size_sampled_heads():
     wl = di.WORKLOADS["decode1b"]
     heads = [(0, 0), (0, 3), (17, 12), (31, 31)]
     run_decode(wl, wl.T, 2, cap=wl.T + wl.steps, check_heads=heads)
+
+
+@pytest.mark.parametrize("L0,d,dd,untied", [(5000, 64, 16, False), (20000, 64, 16, True),
+                                             (3000, 128, 32, False), (9000, 64, 32, False)])
+def test_decode_several_workgroups_per_head(L0, d, dd, untied):
+    """Few (batch, KV head) pairs and a long cache: each pair is split over
+    several workgroups whose partial records the combine kernel merges."""
+    run_decode(SMALL.with_(d=d, dd=dd), L0, 2, untied=untied)
