@@ -354,9 +354,11 @@ void prefill_mfma_kernel(
     constexpr int NT = D / 32;   // 32-row tiles of O_win^T
     constexpr int BN = 64;       // keys per LDS tile (local region)
     constexpr int LDK = D + 8;   // padded LDS row (bf16 elements)
+    constexpr int LDU = D + 8;   // padded row of wU (bf16 elements)
     extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
     bf16_t* lds_k = smem;                    // [2][BN][LDK]
     bf16_t* lds_v = smem + 2 * BN * LDK;     // [2][BN][LDK]
+    bf16_t* wU = smem + 4 * BN * LDK;        // [DD][LDU]: U[c][e] = W_up[c][e]
 
     // Each workgroup takes row blocks p and nblk-1-p of one (batch, head): a
     // short and a long causal row block, so every workgroup has the same work.
@@ -381,6 +383,15 @@ void prefill_mfma_kernel(
     const bf16_t* wdg = wd + (size_t)g * D * DD;
     const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
     const int nkb = (T + 31) >> 5;  // 32-key blocks with a key norm
+
+    // U = W_up (W_down^T when tied), once per workgroup: its rows are the A
+    // operand of q~ = q W_up^T, its columns that of the lift
+    // O^T += W_up^T O_lat^T.
+    for (int idx = tid; idx < DD * D; idx += NW * 64) {
+        const int cc = idx / D, e = idx - (idx / D) * D;
+        wU[cc * LDU + e] = wug ? wug[(size_t)cc * D + e] : wdg[(size_t)e * DD + cc];
+    }
+    __syncthreads();
 
 #pragma nounroll
     for (int part = 0; part < 2; ++part) {
@@ -407,10 +418,37 @@ void prefill_mfma_kernel(
         c.i_hi = imin(c.r0 + 31, T - 1);  // last real row of this wavefront (< r0 if none)
         const int qc = c.qc, hg = c.hg, i = c.i;
 
-        const bf16_t* qrow = q + ((size_t)bh * T + imin(i, T - 1)) * D;
+        const int jd_end = (c.r0 < T) ? c.i_hi - w : -1;  // last distant key of any row here
+        const int js_last = jd_end & ~31;
+        const int iwg_hi = imin(i0 + BM - 1, T - 1);
+        const bool has_local = w > 0 && imax(0, i0 - w + 1) <= iwg_hi;
+        const int ii = imin(i, T - 1);
+
+        // Every global load of the setup is issued here, before any of its
+        // results is used: the query row, the row's own key or latent (the
+        // witness), and the first norm maxima of both regions.
+        const bf16_t* qrow = q + ((size_t)bh * T + ii) * D;
         bf16x8_t qop[KS];  // B operand of S^T = K Q^T: q[i][s*16 + hg*8 + 0..7]
 #pragma unroll
-        for (int s = 0; s < KS; ++s) qop[s] = (i < T) ? load_bf16x8(qrow + s * 16 + hg * 8) : zero_bf16x8();
+        for (int s = 0; s < KS; ++s) qop[s] = load_bf16x8(qrow + s * 16 + hg * 8);
+        bf16x8_t wit[KS];  // own key (w >= 1) or own latent key (w = 0)
+        if (w >= 1) {
+            const bf16_t* krow = k + ((size_t)bg * T + ii) * D;
+#pragma unroll
+            for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(krow + s * 16 + hg * 8);
+        } else {
+            const bf16_t* crow = cK + ((size_t)bg * Tp + ii) * DD;
+#pragma unroll
+            for (int s = 0; s < KS; ++s) wit[s] = s < DS ? load_bf16x8(crow + s * 16 + hg * 8) : zero_bf16x8();
+        }
+        const int nsb = jd_end >= 0 ? (js_last >> 5) + 1 : 0;  // latent blocks with a norm
+        const int kb_lo = imax(0, c.r0 - w + 1) >> 5, kb_hi = imax(0, c.i_hi) >> 5;
+        float cmax = lane < nsb ? cnorm[(size_t)bg * (Tp / 32) + lane] : 0.f;
+        float kmax = (has_local && kb_lo + lane <= kb_hi) ? knorm[(size_t)bg * nkb + kb_lo + lane] : 0.f;
+        if (i >= T) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s) qop[s] = zero_bf16x8();
+        }
         float qs2 = dot8(qop[0], qop[0], 0.f);
 #pragma unroll
         for (int s = 1; s < KS; ++s) qs2 = dot8(qop[s], qop[s], qs2);
@@ -427,11 +465,6 @@ void prefill_mfma_kernel(
         for (int t = 0; t < NT; ++t) ow[t] = splat16(0.f);
         f32x16_t ol = splat16(0.f);
 
-        const int jd_end = (c.r0 < T) ? c.i_hi - w : -1;  // last distant key of any row here
-        const int js_last = jd_end & ~31;
-        const int iwg_hi = imin(i0 + BM - 1, T - 1);
-        const bool has_local = w > 0 && imax(0, i0 - w + 1) <= iwg_hi;
-
         // ---- absorbed query q~ = q W_up^T (scaled): A rows = latent column c, k = e
         bf16x8_t qtop[DS];
         float bound = -INFINITY;
@@ -439,17 +472,7 @@ void prefill_mfma_kernel(
             f32x16_t qt = splat16(0.f);
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
-                bf16x8_t a = zero_bf16x8();
-                if (qc < DD) {
-                    if (wug) {
-                        a = load_bf16x8(wug + (size_t)qc * D + s * 16 + hg * 8);
-                    } else {
-                        uint16_t t8[8];
-#pragma unroll
-                        for (int j = 0; j < 8; ++j) t8[j] = wdg[(size_t)(s * 16 + hg * 8 + j) * DD + qc];
-                        a = __builtin_bit_cast(bf16x8_t, t8);
-                    }
-                }
+                const bf16x8_t a = qc < DD ? load_bf16x8(wU + qc * LDU + s * 16 + hg * 8) : zero_bf16x8();
                 qt = mfma(a, qop[s], qt);
             }
             // accumulator register 8*s + j holds latent column 16*s + (j<4 ? 4hg+j : 8+4hg+j-4)
@@ -463,15 +486,12 @@ void prefill_mfma_kernel(
             }
             qn2 = pair_sum(qn2);
             // |q~ . c| <= |q~| |c| on the bf16 values the MFMA multiplies (Cauchy-Schwarz)
-            float cmax = 0.f;
-            for (int sb = lane; sb <= (js_last >> 5); sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * (Tp / 32) + sb]);
+            for (int sb = lane + 64; sb < nsb; sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * (Tp / 32) + sb]);
             cmax = wave_max(cmax);
             bound = sqrtf(qn2) * cmax;
         }
         if (has_local) {
-            float kmax = 0.f;
-            const int kb_lo = imax(0, c.r0 - w + 1) >> 5, kb_hi = imax(0, c.i_hi) >> 5;
-            for (int kb = kb_lo + lane; kb <= kb_hi; kb += 64) kmax = fmaxf(kmax, knorm[(size_t)bg * nkb + kb]);
+            for (int kb = kb_lo + lane + 64; kb <= kb_hi; kb += 64) kmax = fmaxf(kmax, knorm[(size_t)bg * nkb + kb]);
             kmax = wave_max(kmax);
             bound = fmaxf(bound, c_scale * sqrtf(qs2) * kmax);
         }
@@ -479,23 +499,16 @@ void prefill_mfma_kernel(
         // for every row, it is within 2^100 of a real score of that row (its own
         // key), so no row's weights can all underflow.
         bound = bound * 1.001f + 1e-6f;
-        float witness;
-        {
-            const int ii = imin(i, T - 1);
-            if (w >= 1) {
-                const bf16_t* krow = k + ((size_t)bg * T + ii) * D;
-                witness = 0.f;
+        float witness = 0.f;
+        if (w >= 1) {
 #pragma unroll
-                for (int s = 0; s < KS; ++s) witness = dot8(qop[s], load_bf16x8(krow + s * 16 + hg * 8), witness);
-                witness *= c_scale;
-            } else {
-                const bf16_t* crow = cK + ((size_t)bg * Tp + ii) * DD;
-                witness = 0.f;
+            for (int s = 0; s < KS; ++s) witness = dot8(qop[s], wit[s], witness);
+            witness *= c_scale;
+        } else {
 #pragma unroll
-                for (int s = 0; s < DS; ++s) witness = dot8(qtop[s], load_bf16x8(crow + s * 16 + hg * 8), witness);
-            }
-            witness = pair_sum(witness);
+            for (int s = 0; s < DS; ++s) witness = dot8(qtop[s], wit[s], witness);
         }
+        witness = pair_sum(witness);
         const bool fixed = c.r0 < T && !__builtin_amdgcn_ballot_w64(i < T && bound - witness > 100.f);
         if (fixed) {
             st.m = bound;
@@ -538,12 +551,13 @@ void prefill_mfma_kernel(
                 const bf16x8_t blo = pack8(lo_f[0], lo_f[1], lo_f[2], lo_f[3], lo_f[4], lo_f[5], lo_f[6], lo_f[7]);
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
-                    const int e = t * 32 + qc;
+                    // A row e = t*32 + qc, k = latent columns s*16 + {4hg..4hg+3, 8+4hg..8+4hg+3}
+                    const bf16_t* ur = wU + (s * 16 + 4 * hg) * LDU + t * 32 + qc;
                     uint16_t a8[8];
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) {
-                        const int cc = s * 16 + ((j < 4) ? 4 * hg + j : 8 + 4 * hg + (j - 4));
-                        a8[j] = wug ? wug[(size_t)cc * D + e] : wdg[(size_t)e * DD + cc];
+                    for (int j = 0; j < 4; ++j) {
+                        a8[j] = ur[j * LDU];
+                        a8[4 + j] = ur[(8 + j) * LDU];
                     }
                     const bf16x8_t a = __builtin_bit_cast(bf16x8_t, a8);
                     ow[t] = mfma(a, bhi, ow[t]);
@@ -588,7 +602,7 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q,
     const int BH = B * Hq;
     const int Tp = prefill_tp(T, w);
     const float c_scale = 1.4426950408889634f / sqrtf((float)D);
-    const size_t lds = sizeof(bf16_t) * 4 * 64 * (D + 8);
+    const size_t lds = sizeof(bf16_t) * (4 * 64 * (D + 8) + DD * (D + 8));
     auto kern = prefill_mfma_kernel<D, DD, NW>;
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
