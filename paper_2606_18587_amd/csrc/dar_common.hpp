@@ -54,6 +54,33 @@ __device__ __forceinline__ float wave_max(float x) {
     return x;
 }
 
+// Maximum over the 64 lanes with DPP lane moves (no LDS crossbar): quads,
+// half rows, rows, then the two row broadcasts; lane 63 ends with the
+// maximum, which is broadcast through a scalar register.
+__device__ __forceinline__ float wave_max_dpp(float x) {
+    auto step = [](float v, int ctrl, int row_mask) -> float {
+        const int u = __float_as_int(v);
+        int t;
+        switch (ctrl) {  // the DPP control must be a constant
+            case 0xB1: t = __builtin_amdgcn_update_dpp(u, u, 0xB1, 0xF, 0xF, false); break;
+            case 0x4E: t = __builtin_amdgcn_update_dpp(u, u, 0x4E, 0xF, 0xF, false); break;
+            case 0x141: t = __builtin_amdgcn_update_dpp(u, u, 0x141, 0xF, 0xF, false); break;
+            case 0x140: t = __builtin_amdgcn_update_dpp(u, u, 0x140, 0xF, 0xF, false); break;
+            case 0x142: t = __builtin_amdgcn_update_dpp(u, u, 0x142, 0xA, 0xF, false); break;
+            default: t = __builtin_amdgcn_update_dpp(u, u, 0x143, 0xC, 0xF, false); break;
+        }
+        (void)row_mask;
+        return fmaxf(v, __int_as_float(t));
+    };
+    x = step(x, 0xB1, 0xF);   // quad_perm [1,0,3,2]
+    x = step(x, 0x4E, 0xF);   // quad_perm [2,3,0,1]
+    x = step(x, 0x141, 0xF);  // row_half_mirror
+    x = step(x, 0x140, 0xF);  // row_mirror
+    x = step(x, 0x142, 0xA);  // row_bcast:15
+    x = step(x, 0x143, 0xC);  // row_bcast:31
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 63));
+}
+
 __device__ __forceinline__ float wave_sum(float x) {
 #pragma unroll
     for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off, 64);

@@ -198,46 +198,81 @@ __device__ __forceinline__ lf32x16 project_mfma(const lbf16x8 (&wa)[D / 16], con
 
 __device__ __forceinline__ int acc_col(int r, int hg) { return 8 * (r >> 2) + 4 * hg + (r & 3); }
 
-// Prefill pre-pass, one wavefront per 32 tokens, 4 wavefronts per block.
-// Also writes, per 32-token block, the largest L2 norm of the stored c^K rows
-// (over tokens [0, T - w)) and of the key rows (over all tokens [0, T)); the
-// matrix-core prefill bounds its scores with them.
+// Prefill pre-pass. Block (x, y) serves 128-token chunk x of (batch, KV
+// head) y; wavefront w takes tokens [32w, 32w + 32) of it. Also writes, per
+// 32-token block, the largest L2 norm of the stored c^K rows (over tokens
+// [0, T - w)) and of the key rows (over all tokens [0, T)); the matrix-core
+// prefill bounds its scores with them.
+//
+// Latency layout: W_down is requested first and brought into LDS (stored
+// transposed as the A operand rows); the key and value rows are in flight
+// meanwhile; the transposed value latents go out through LDS as 16-byte
+// stores.
 template <int D>
 __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
     const bf16_t* __restrict__ k, const bf16_t* __restrict__ v, const bf16_t* __restrict__ wd,
     bf16_t* __restrict__ cK, bf16_t* __restrict__ cVt, float* __restrict__ cnorm,
     float* __restrict__ knorm, bf16_t* __restrict__ consts, int Hkv, int T_, int dd, int Tl,
-    int Tp, int perm) {
+    int Tp) {
     constexpr int KS = D / 16;
+    constexpr int LDW = D + 8;   // W^T row in LDS (bf16 elements)
+    constexpr int LDT = 32 + 8;  // transposed value-latent row in LDS
+    __shared__ __attribute__((aligned(16))) bf16_t wsh[32 * LDW];
+    __shared__ __attribute__((aligned(16))) bf16_t vtr[4][32 * LDT];
     if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < 16)
         consts[threadIdx.x] = threadIdx.x < 8 ? (bf16_t)0x3f80 : (bf16_t)0;
     const int bg = blockIdx.y;
     const int g = bg % Hkv;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int tl = lane & 31, hg = lane >> 5;
-    const int ts = blockIdx.x * 128 + wave * 32;  // first token of this wavefront
-    const int t = ts + tl;
     const int Tk = (T_ + 31) & ~31;
-    if (ts >= (Tp > Tk ? Tp : Tk)) return;
-    const bool project = ts < Tp;
-    lbf16x8 wa[KS];
-    if (project) load_wd_operand<D>(wd + (size_t)g * D * dd, dd, lane, wa);
-    for (int which = 0; which < 2; ++which) {
-        if (which == 1 && !project) break;
-        const int tmax = which == 0 ? T_ : Tl;  // keys: norms of all rows; values: latents only
-        const bf16_t* xr = (which ? v : k) + ((size_t)bg * T_ + (t < tmax ? t : 0)) * D;
-        lbf16x8 x[KS];
+    const bf16_t* kbase = k + (size_t)bg * T_ * D;
+    const bf16_t* vbase = v + (size_t)bg * T_ * D;
+    const int vlast = imax(Tl, 1) - 1;
+
+    // key and value rows of a wavefront's 32 tokens (indices clamped; rows
+    // out of range are zeroed before use)
+    struct Rows {
+        lbf16x8 k[KS], v[KS];
+    };
+    auto load = [&](int chunk) {
+        Rows r;
+        const int t = chunk * 128 + wave * 32 + tl;
+        const bf16_t* kr = kbase + (size_t)imin(t, T_ - 1) * D;
+        const bf16_t* vr = vbase + (size_t)imin(t, vlast) * D;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
-            x[s] = lload8(xr + s * 16 + hg * 8);
-            if (t >= tmax) x[s] = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
+            r.k[s] = lload8(kr + s * 16 + hg * 8);
+            r.v[s] = lload8(vr + s * 16 + hg * 8);
         }
-        if (which == 0 && ts < T_) {
+        return r;
+    };
+
+    // W_down^T into LDS: row c (latent column, zero for c >= dd), k = e.
+    // Requested before any key or value row (loads return in order).
+    const bf16_t* wdg = wd + (size_t)g * D * dd;
+    for (int idx = tid; idx < D * 32; idx += 256) {
+        const int e = idx >> 5, c = idx & 31;
+        wsh[c * LDW + e] = c < dd ? wdg[(size_t)e * dd + c] : (bf16_t)0;
+    }
+    const int chunk = blockIdx.x;
+    const Rows cur = load(chunk);
+    __syncthreads();
+    lbf16x8 wa[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) wa[s] = *reinterpret_cast<const lbf16x8*>(wsh + tl * LDW + s * 16 + hg * 8);
+    const lbf16x8 zero8 = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
+
+    {
+        const int ts = chunk * 128 + wave * 32;  // first token of this wavefront
+        const int t = ts + tl;
+        if (ts < T_) {
             float n2 = 0.f;
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
-                const uint4 u = __builtin_bit_cast(uint4, x[s]);
+                const uint4 u = __builtin_bit_cast(uint4, t < T_ ? cur.k[s] : zero8);
                 const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
@@ -247,30 +282,30 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
                 }
             }
             n2 += __shfl_xor(n2, 32, 64);
-            const float nmax = wave_max(n2);
+            const float nmax = wave_max_dpp(n2);
             if (lane == 0) knorm[(size_t)bg * (Tk / 32) + (ts >> 5)] = sqrtf(nmax);
         }
-        if (!project) break;
-        if (which == 0) {
+        if (ts < Tp) {
+            lbf16x8 xk[KS], xv[KS];
 #pragma unroll
-            for (int s = 0; s < KS; ++s)
-                if (t >= Tl) x[s] = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
-        }
-        const lf32x16 acc = project_mfma<D>(wa, x);
-        if (which == 0) {
-            // squared norm of the rounded latent, both halves of the wavefront
-            float n2 = 0.f;
+            for (int s = 0; s < KS; ++s) {
+                xk[s] = t < Tl ? cur.k[s] : zero8;
+                xv[s] = t < Tl ? cur.v[s] : zero8;
+            }
+            // key latents: token-major, columns in latent_pos order, plus the norm
+            {
+                const lf32x16 acc = project_mfma<D>(wa, xk);
+                float n2 = 0.f;
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-                if (acc_col(r, hg) < dd) {
-                    const float cr = bf16_to_f32(f32_to_bf16(acc[r]));
-                    n2 = __builtin_fmaf(cr, cr, n2);
-                }
-            n2 += __shfl_xor(n2, 32, 64);
-            const float nmax = wave_max(n2);
-            if (lane == 0) cnorm[(size_t)bg * (Tp / 32) + (t >> 5)] = sqrtf(nmax);
-            bf16_t* out = cK + ((size_t)bg * Tp + t) * dd;
-            if (perm) {
+                for (int r = 0; r < 16; ++r)
+                    if (acc_col(r, hg) < dd) {
+                        const float cr = bf16_to_f32(f32_to_bf16(acc[r]));
+                        n2 = __builtin_fmaf(cr, cr, n2);
+                    }
+                n2 += __shfl_xor(n2, 32, 64);
+                const float nmax = wave_max_dpp(n2);
+                if (lane == 0) cnorm[(size_t)bg * (Tp / 32) + (ts >> 5)] = sqrtf(nmax);
+                bf16_t* out = cK + ((size_t)bg * Tp + t) * dd;
                 // latent_pos order: positions 16s + 8hg + j hold registers 8s + j
 #pragma unroll
                 for (int s = 0; s < 2; ++s)
@@ -282,19 +317,22 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
                         u.w = (uint32_t)f32_to_bf16(acc[8 * s + 6]) | ((uint32_t)f32_to_bf16(acc[8 * s + 7]) << 16);
                         *reinterpret_cast<uint4*>(out + 16 * s + 8 * hg) = u;
                     }
-            } else {
+            }
+            // value latents, transposed per 32-token block: [c][token], via LDS
+            {
+                const lf32x16 acc = project_mfma<D>(wa, xv);
+                bf16_t* tb = vtr[wave];
 #pragma unroll
                 for (int r = 0; r < 16; ++r) {
                     const int c = acc_col(r, hg);
-                    if (c < dd) out[c] = f32_to_bf16(acc[r]);
+                    if (c < dd) tb[c * LDT + tl] = f32_to_bf16(acc[r]);
                 }
-            }
-        } else {
-            bf16_t* out = cVt + ((size_t)bg * Tp + (size_t)(t >> 5) * 32) * dd + (t & 31);
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int c = acc_col(r, hg);
-                if (c < dd) out[(size_t)c * 32] = f32_to_bf16(acc[r]);
+                // same wavefront: its LDS writes complete before its reads
+                bf16_t* out = cVt + ((size_t)bg * Tp + (size_t)ts) * dd;  // block of dd x 32
+                for (int q = lane; q < dd * 4; q += 64) {
+                    const int c = q >> 2, t0 = (q & 3) * 8;
+                    *reinterpret_cast<uint4*>(out + q * 8) = *reinterpret_cast<const uint4*>(tb + c * LDT + t0);
+                }
             }
         }
     }
@@ -417,9 +455,9 @@ hipError_t launch_prefill_latent<bf16_t>(const bf16_t* k, const bf16_t* v, const
     const int ntok = Tp > Tk ? Tp : Tk;
     dim3 grid((ntok + 127) / 128, B * Hkv);
     if (d == 64)
-        hipLaunchKernelGGL(prefill_latent_mfma_kernel<64>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv, T_, dd, Tl, Tp, 1);
+        hipLaunchKernelGGL(prefill_latent_mfma_kernel<64>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv, T_, dd, Tl, Tp);
     else
-        hipLaunchKernelGGL(prefill_latent_mfma_kernel<128>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv, T_, dd, Tl, Tp, 1);
+        hipLaunchKernelGGL(prefill_latent_mfma_kernel<128>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv, T_, dd, Tl, Tp);
     return hipGetLastError();
 }
 

@@ -242,12 +242,13 @@ __device__ __forceinline__ void distant_region(const RowCtx& c, const bf16_t* __
     if (sub < n_sub) subtile(sub, akA, avA);
 }
 
-// Local region: 64-key K/V tiles staged through LDS for the workgroup. The
+// Local region with one tile of prefetch (d = 128, where a second register
+// set does not fit): 64-key K/V tiles staged through LDS for the workgroup. The
 // query operand is the unscaled bf16 query (scaling it in bf16 would add a
 // rounding proportional to the score); one FMA per score applies
 // log2(e)/sqrt(d) and the reference.
 template <int D, int DD, int NW, bool FIXED>
-__device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __restrict__ k,
+__device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t* __restrict__ k,
                                              const bf16_t* __restrict__ v, bf16_t* lds_k,
                                              bf16_t* lds_v, const bf16x8_t (&qop)[D / 16],
                                              int i0, int iwg_hi, SoftmaxState& st,
@@ -336,6 +337,123 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
             }
         }
         if (n + 1 < ntile) lstore(buf ^ 1);
+        __syncthreads();
+    }
+}
+
+// Local region: 64-key K/V tiles staged through LDS for the workgroup. The
+// query operand is the unscaled bf16 query (scaling it in bf16 would add a
+// rounding proportional to the score); one FMA per score applies
+// log2(e)/sqrt(d) and the reference.
+template <int D, int DD, int NW, bool FIXED>
+__device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __restrict__ k,
+                                             const bf16_t* __restrict__ v, bf16_t* lds_k,
+                                             bf16_t* lds_v, const bf16x8_t (&qop)[D / 16],
+                                             int i0, int iwg_hi, SoftmaxState& st,
+                                             f32x16_t (&ow)[D / 32], f32x16_t& ol) {
+    constexpr int KS = D / 16, NT = D / 32, BN = 64, LDK = D + 8;
+    constexpr int CH = BN * D / 8 / (NW * 64);
+    const int T = c.T, w = c.w;
+    const int jb_lo = imax(0, i0 - w + 1);
+    const int t_first = jb_lo & ~(BN - 1);
+    const int ntile = (iwg_hi - t_first) / BN + 1;
+    const bf16_t* kb = k + (size_t)c.bg * T * D;
+    const bf16_t* vb = v + (size_t)c.bg * T * D;
+    // d = 64: two register sets; the loads of tile n+2 are issued when tile n
+    // starts and reach LDS when tile n+1 ends, so two tiles of work cover
+    // their latency.
+    // (tiles travel by value: no array of them ever has its address taken,
+    // so they stay in registers whatever the compiler does with the loop)
+    struct Tile {
+        uint4 k[CH], v[CH];
+    };
+    auto gload = [&](int t0) {
+        Tile r;
+#pragma unroll
+        for (int q = 0; q < CH; ++q) {
+            const int chunk = c.tid + q * NW * 64;
+            const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
+            // keys past the sequence repeat its last key: their scores are
+            // masked (j > i) and their weights are zero
+            const int key = imin(t0 + row, T - 1);
+            r.k[q] = *reinterpret_cast<const uint4*>(kb + (size_t)key * D + col);
+            r.v[q] = *reinterpret_cast<const uint4*>(vb + (size_t)key * D + col);
+        }
+        return r;
+    };
+    auto lstore = [&](int buf, const Tile& tl) {
+#pragma unroll
+        for (int q = 0; q < CH; ++q) {
+            const int chunk = c.tid + q * NW * 64;
+            const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
+            *reinterpret_cast<uint4*>(lds_k + (size_t)buf * BN * LDK + row * LDK + col) = tl.k[q];
+            *reinterpret_cast<uint4*>(lds_v + (size_t)buf * BN * LDK + row * LDK + col) = tl.v[q];
+        }
+    };
+    const int lane = c.tid & 63;
+    const int quad = lane >> 4, sl = lane & 15;
+    auto compute = [&](int buf, int t0) {
+        const bf16_t* lk = lds_k + (size_t)buf * BN * LDK;
+        const bf16_t* lv = lds_v + (size_t)buf * BN * LDK;
+#pragma unroll
+        for (int sub = 0; sub < BN / 32; ++sub) {
+            const int js = t0 + sub * 32;
+            if (c.r0 < T && js <= c.i_hi && js + 31 > c.r0 - w) {
+                f32x16_t sc = mfma(load_bf16x8(lk + (sub * 32 + c.prow) * LDK + c.hg * 8), qop[0], splat16(0.f));
+#pragma unroll
+                for (int ks = 1; ks < KS; ++ks)
+                    sc = mfma(load_bf16x8(lk + (sub * 32 + c.prow) * LDK + ks * 16 + c.hg * 8), qop[ks], sc);
+                f32x16_t x;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], c.c_scale, st.cm);
+                if (!(js > c.i_hi - w && js + 31 <= c.r0)) {  // edge subtile: keep i - w < j <= i
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int j = js + acc_key(r, c.hg);
+                        if (j <= c.i - w || j > c.i) x[r] = -INFINITY;
+                    }
+                }
+                bf16x8_t p0, p1;
+                if (FIXED) exp_pack<true>(x, st.l, p0, p1);
+                else softmax_step<NT, true>(x, st, ow, ol, p0, p1);
+                // O_win^T += V^T P^T; V^T operand via transposing LDS reads
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+#pragma unroll
+                    for (int half = 0; half < 2; ++half) {
+                        const int key = sub * 32 + half * 16 + 8 * (quad >> 1) + (sl >> 2);
+                        const int col = t * 32 + 16 * (quad & 1) + 4 * (sl & 3);
+                        const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_s16x4_t*)(lv + key * LDK + col));
+                        const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                            (lds_s16x4_t*)(lv + (key + 4) * LDK + col));
+                        const uint2 ulo = __builtin_bit_cast(uint2, lo), uhi = __builtin_bit_cast(uint2, hi);
+                        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(ulo.x, ulo.y, uhi.x, uhi.y));
+                        ow[t] = mfma(a, half ? p1 : p0, ow[t]);
+                    }
+                }
+            }
+        }
+    };
+    // The loads are unconditional (tiles past the last one read clamped keys
+    // and are never used): a load under a branch would make every later wait
+    // drain all loads in flight.
+    Tile ta = gload(t_first);
+    Tile tb = gload(t_first + BN);
+    lstore(0, ta);
+    __syncthreads();
+    for (int n = 0; n < ntile; n += 2) {
+        const int t0 = t_first + n * BN;
+        // tile n is in LDS buffer 0, tile n+1 in tb
+        ta = gload(t0 + 2 * BN);
+        compute(0, t0);
+        lstore(1, tb);
+        __syncthreads();
+        if (n + 1 >= ntile) break;
+        // tile n+1 is in LDS buffer 1, tile n+2 in ta
+        tb = gload(t0 + 3 * BN);
+        compute(1, t0 + BN);
+        lstore(0, ta);
         __syncthreads();
     }
 }
@@ -524,8 +642,13 @@ void prefill_mfma_kernel(
         }
         // ------------------------------------------------------------ local region
         if (has_local) {
-            if (fixed) local_region<D, DD, NW, true>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
-            else local_region<D, DD, NW, false>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+            if constexpr (D > 64) {
+                if (fixed) local_region_1deep<D, DD, NW, true>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+                else local_region_1deep<D, DD, NW, false>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+            } else {
+                if (fixed) local_region<D, DD, NW, true>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+                else local_region<D, DD, NW, false>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+            }
         }
 
         if (c.r0 >= T) continue;
