@@ -13,10 +13,12 @@ PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize) 
     PrefillWs ws{0, 0, 0, 0, 0, 0};
     const size_t Tp = (size_t)prefill_tp(T, w);
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    const size_t one = al((size_t)B * Hkv * Tp * dd * esize);
+    // c^K: Tp rows of dd; c^V^T: Tp/32 blocks of up to dd + 1 rows of 32
+    const size_t kbytes = al((size_t)B * Hkv * Tp * dd * esize);
+    const size_t vbytes = al((size_t)B * Hkv * Tp * (dd + 1) * esize);
     ws.ck_off = 0;
-    ws.cv_off = one;
-    ws.norm_off = 2 * one;
+    ws.cv_off = kbytes;
+    ws.norm_off = kbytes + vbytes;
     ws.knorm_off = ws.norm_off + al((size_t)B * Hkv * (Tp / 32) * sizeof(float));
     ws.const_off = ws.knorm_off + al((size_t)B * Hkv * ((T + 31) / 32) * sizeof(float));
     ws.bytes = ws.const_off + 256;

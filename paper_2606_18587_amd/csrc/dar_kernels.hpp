@@ -32,6 +32,10 @@ static inline int prefill_tp(int T, int w) {
     return Tl > 0 ? round_up(Tl, 32) + 64 : 0;
 }
 PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize);
+// Rows of a 32-token block of the transposed value latents written by the
+// matrix-core pre-pass: d_down, plus a row of ones when d_down == 16 (the
+// padding row of the 32-row MFMA operand, which then yields the row sums).
+__host__ __device__ inline int cvt_rows(int dd) { return dd == 16 ? 17 : dd; }
 
 // Decode workspace: per (batch, query head, partial) softmax state
 // {m, l, acc_lat[dd], acc_win[d]} in fp32.

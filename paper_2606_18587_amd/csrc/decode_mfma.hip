@@ -87,6 +87,12 @@ struct DecState {
     dbf16x8 negm;  // B operand: -m at contraction slot 0 (lanes of half 0), zeros elsewhere
 };
 
+// 16-byte non-temporal load (a cache byte read once per step)
+typedef unsigned int du32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ du32x4 ld_stream(const bf16_t* p) {
+    return __builtin_nontemporal_load(reinterpret_cast<const du32x4*>(p));
+}
+
 // Marks a rarely taken, wave-uniform branch: the compiler may not execute its
 // body unconditionally (if-converted, every subtile would pay for it).
 __device__ __forceinline__ void keep_branch() { __asm__ volatile(""); }
@@ -120,7 +126,7 @@ __device__ __forceinline__ dbf16x8 negm_operand(float cm, int hg) {
 
 template <int NT, bool SUMV>
 __device__ __forceinline__ void dstep(df32x16& x, DecState& st, df32x16 (&acc)[NT], dbf16x8& p0, dbf16x8& p1,
-                                      int hg) {
+                                      int hg, df32x16* xnext = nullptr) {
     float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), x[2]), fmaxf(x[3], x[4]));
     mx = fmaxf(fmaxf(mx, x[5]), fmaxf(x[6], x[7]));
     mx = fmaxf(fmaxf(mx, x[8]), fmaxf(x[9], x[10]));
@@ -146,6 +152,10 @@ __device__ __forceinline__ void dstep(df32x16& x, DecState& st, df32x16 (&acc)[N
         st.negm = negm_operand(st.cm, hg);
 #pragma unroll
         for (int r = 0; r < 16; ++r) x[r] -= delta;
+        if (xnext) {  // scores already computed against the old reference
+#pragma unroll
+            for (int r = 0; r < 16; ++r) (*xnext)[r] -= delta;
+        }
     }
     float p[16];
 #pragma unroll
@@ -174,6 +184,9 @@ constexpr int kDecMaxGroup = 8;   // query heads per KV head on this path
 // Word 3 of a raw buffer descriptor on gfx9-family parts (32-bit data
 // format; with stride 0, accesses at or past num_records return zero).
 constexpr int kBufWord3 = 0x00020000;
+// Cache policy of the cache streams: non-temporal (every cache byte is read
+// once per step; measured 12% faster than the default policy at 32K tokens).
+constexpr int kStream = 2;
 constexpr int kDecMinSub = 4;     // fewest subtiles a wavefront is given, when possible
 
 // Subtile run of wavefront `idx` (of nwave per (batch, KV head)). Waves
@@ -305,10 +318,10 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             const int o = (t0 - t_begin) * DD * 2;
 #pragma unroll
             for (int k = 0; k < DS; ++k)
-                ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + o + k * 32, 0, 0));
+                ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + o + k * 32, 0, kStream));
 #pragma unroll
             for (int k = 0; k < DS; ++k)
-                vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + o + k * 1024, 0, 0));
+                vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + o + k * 1024, 0, kStream));
         };
         static_assert(kSubBytes == 1024 * DS, "one V chunk of 16 bytes per lane per 16 latent columns");
         // NST subtiles in flight per wavefront (the stream is latency bound:
@@ -355,9 +368,9 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             qtop[k] = pk8(v8);
         }
 
-        auto body = [&](int t0, const dbf16x8 (&ak)[DS], const uint4 (&vv)[DS]) {
-#pragma unroll
-            for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vb + (lane + 64 * k) * 8) = vv[k];
+        // Software pipelined: the scores of subtile n+1 are on the matrix
+        // cores while the exponentials of subtile n run.
+        auto scores = [&](int t0, const dbf16x8 (&ak)[DS]) {
             df32x16 x = mma(ak[0], qtop[0], mma(ones_a, st.negm, fill16(0.f)));
 #pragma unroll
             for (int k = 1; k < DS; ++k) x = mma(ak[k], qtop[k], x);
@@ -367,8 +380,13 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
                 for (int r = 0; r < 16; ++r)
                     if (t0 + dkey(r, hg) > last) x[r] = -INFINITY;
             }
+            return x;
+        };
+        auto finish = [&](df32x16& x, const uint4 (&vv)[DS], df32x16* xnext) {
+#pragma unroll
+            for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vb + (lane + 64 * k) * 8) = vv[k];
             dbf16x8 p0, p1;
-            dstep<1, DD != 16>(x, st, acc, p0, p1, hg);
+            dstep<1, DD != 16>(x, st, acc, p0, p1, hg, xnext);
             // V^T operand: rows c = lane%32 of the DD-wide tile
 #pragma unroll
             for (int half = 0; half < 2; ++half) {
@@ -391,16 +409,30 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             }
         };
         int t0 = t_begin;
+        df32x16 x = scores(t_begin, aks[0]);
         for (; t0 + 32 * (NST - 1) < t_end; t0 += 32 * NST) {
 #pragma unroll
             for (int j = 0; j < NST; ++j) {
-                body(t0 + 32 * j, aks[j], vs[j]);
-                load(t0 + 32 * (j + NST), aks[j], vs[j]);
+                const int tj = t0 + 32 * j;
+                df32x16 xn = scores(tj + 32, aks[(j + 1) % NST]);
+                finish(x, vs[j], &xn);
+                load(tj + 32 * NST, aks[j], vs[j]);
+                x = xn;
             }
         }
 #pragma unroll
-        for (int j = 0; j < NST - 1; ++j)
-            if (t0 + 32 * j < t_end) body(t0 + 32 * j, aks[j], vs[j]);
+        for (int j = 0; j < NST - 1; ++j) {
+            const int tj = t0 + 32 * j;
+            if (tj < t_end) {
+                if (tj + 32 < t_end) {
+                    df32x16 xn = scores(tj + 32, aks[j + 1]);
+                    finish(x, vs[j], &xn);
+                    x = xn;
+                } else {
+                    finish(x, vs[j], nullptr);
+                }
+            }
+        }
         if (DD == 16) st.l = acc[0][8];  // ones row: full row sum on both halves
         else st.l = psum(st.l);
         if (col < G) {
@@ -422,12 +454,12 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         auto load = [&](int t0, dbf16x8 (&ak)[KS], uint4 (&vv)[CPT]) {
             const int kr = imin(t0 + prow, last) % w;
 #pragma unroll
-            for (int k = 0; k < KS; ++k) ak[k] = ld8(kw + (size_t)kr * D + k * 16 + hg * 8);
+            for (int k = 0; k < KS; ++k) ak[k] = __builtin_bit_cast(dbf16x8, ld_stream(kw + (size_t)kr * D + k * 16 + hg * 8));
 #pragma unroll
             for (int k = 0; k < CPT; ++k) {
                 const int chunk = lane + 64 * k;
                 const int tr = imin(t0 + chunk / (D / 8), last) % w;
-                vv[k] = *reinterpret_cast<const uint4*>(vw + (size_t)tr * D + (chunk % (D / 8)) * 8);
+                vv[k] = __builtin_bit_cast(uint4, ld_stream(vw + (size_t)tr * D + (chunk % (D / 8)) * 8));
             }
         };
         auto body = [&](int t0, const dbf16x8 (&ak)[KS], const uint4 (&vv)[CPT]) {

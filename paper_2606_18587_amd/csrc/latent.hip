@@ -328,11 +328,15 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
                     if (c < dd) tb[c * LDT + tl] = f32_to_bf16(acc[r]);
                 }
                 // same wavefront: its LDS writes complete before its reads
-                bf16_t* out = cVt + ((size_t)bg * Tp + (size_t)ts) * dd;  // block of dd x 32
+                const int rb = cvt_rows(dd);  // block rows: dd, plus a ones row when dd == 16
+                bf16_t* out = cVt + ((size_t)bg * (Tp / 32) + (size_t)(ts >> 5)) * rb * 32;
                 for (int q = lane; q < dd * 4; q += 64) {
                     const int c = q >> 2, t0 = (q & 3) * 8;
                     *reinterpret_cast<uint4*>(out + q * 8) = *reinterpret_cast<const uint4*>(tb + c * LDT + t0);
                 }
+                if (rb > dd && lane < 4)
+                    *reinterpret_cast<uint4*>(out + dd * 32 + lane * 8) =
+                        make_uint4(0x3f803f80u, 0x3f803f80u, 0x3f803f80u, 0x3f803f80u);
             }
         }
     }

@@ -140,7 +140,8 @@ struct SoftmaxState {
 // reference). Returns P^T as two bf16x8 operands; rescales ow/ol if needed.
 template <int NT, bool SUM_VALU>
 __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x16_t (&ow)[NT],
-                                             f32x16_t& ol, bf16x8_t& p0, bf16x8_t& p1) {
+                                             f32x16_t& ol, bf16x8_t& p0, bf16x8_t& p1,
+                                             f32x16_t* xnext = nullptr) {
     float mx = fmaxf(fmaxf(fmaxf(x[0], x[1]), x[2]), fmaxf(x[3], x[4]));
     mx = fmaxf(fmaxf(mx, x[5]), fmaxf(x[6], x[7]));
     mx = fmaxf(fmaxf(mx, x[8]), fmaxf(x[9], x[10]));
@@ -166,6 +167,10 @@ __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x
         st.cmv = splat16(st.cm);
 #pragma unroll
         for (int r = 0; r < 16; ++r) x[r] -= delta;
+        if (xnext) {  // scores already computed against the old reference
+#pragma unroll
+            for (int r = 0; r < 16; ++r) (*xnext)[r] -= delta;
+        }
     }
     exp_pack<SUM_VALU>(x, st.l, p0, p1);
 }
@@ -186,60 +191,137 @@ struct RowCtx {
     float c_scale;
 };
 
-// Distant region: subtiles of 32 keys [0, js_last], latents streamed from
-// L2 two subtiles ahead (the workspace is padded, so no clamping).
+// Word 3 of a raw buffer descriptor on gfx9-family parts (32-bit data
+// format; with stride 0, lanes whose offset is past num_records read zero).
+static constexpr int kBufWord3 = 0x00020000;
+
+// A pointer every lane of the wavefront holds, moved to scalar registers.
+__device__ __forceinline__ const bf16_t* uniform_ptr(const bf16_t* p) {
+    const uint64_t u = (uint64_t)p;
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)u);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(u >> 32));
+    return (const bf16_t*)(((uint64_t)hi << 32) | lo);
+}
+
+// Distant region: subtiles of 32 keys [0, js_last] against the latents of
+// the pre-pass. With d = 64, d_down = 16 it is software pipelined: the scores of subtile n+1 are on the
+// matrix cores while the exponentials of subtile n run, so neither unit
+// waits for the other. Latent keys are loaded three subtiles ahead, values
+// three ahead of their use, through buffer loads whose subtile offset is a
+// scalar (no per-subtile address arithmetic); lanes of the V^T operand past
+// the stored rows read zeros (out-of-range offset), and with d_down = 16 the
+// stored ones row makes O_lat^T row 16 the row sum.
 // FIXED: the reference is final, every score is <= 0 relative to it: no
 // maximum, no rescaling. Otherwise the online maximum is tracked.
 template <int D, int DD, bool FIXED>
 __device__ __forceinline__ void distant_region(const RowCtx& c, const bf16_t* __restrict__ cK,
                                                const bf16_t* __restrict__ cVt,
-                                               const bf16_t* __restrict__ consts,
                                                const bf16x8_t (&qtop)[DD / 16], int js_last,
                                                SoftmaxState& st, f32x16_t (&ow)[D / 32],
                                                f32x16_t& ol) {
     constexpr int DS = DD / 16, NT = D / 32;
+    constexpr int RB = DD == 16 ? 17 : DD;  // stored rows per 32-token block of c^V^T
     const int n_sub = (js_last >> 5) + 1;
-    const bf16_t* ckl = cK + ((size_t)c.bg * c.Tp + c.prow) * DD + c.hg * 8;
-    const bool vrow = c.qc < DD;
-    const bf16_t* cvl = vrow ? cVt + (size_t)c.bg * c.Tp * DD + (size_t)c.qc * 32 + c.hg * 8
-                             : consts + ((DD == 16 && c.qc == 16) ? 0 : 8);
-    const int vinc = vrow ? 32 * DD : 0;
-    const int vhalf = vrow ? 16 : 0;
-    auto load = [&](int sub, bf16x8_t (&ak)[DS], bf16x8_t (&av)[2]) {
-        const bf16_t* pk = ckl + (size_t)sub * 32 * DD;
-#pragma unroll
-        for (int s = 0; s < DS; ++s) ak[s] = load_bf16x8(pk + s * 16);
-        const bf16_t* pv = cvl + (size_t)sub * vinc;
-        av[0] = load_bf16x8(pv);
-        av[1] = load_bf16x8(pv + vhalf);
+    const int max_sub = (c.Tp >> 5) - 1;    // last subtile with storage
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)uniform_ptr(cK + (size_t)c.bg * c.Tp * DD), (short)0, c.Tp * DD * 2, kBufWord3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(
+        (void*)uniform_ptr(cVt + (size_t)c.bg * (c.Tp / 32) * RB * 32), (short)0, (c.Tp / 32) * RB * 64,
+        kBufWord3);
+    const int koff = (c.prow * DD + c.hg * 8) * 2;
+    const int voff = c.qc < RB ? (c.qc * 32 + c.hg * 8) * 2 : 0x40000000;  // past the end: zeros
+    struct KT {
+        bf16x8_t k[DS];
     };
-    auto subtile = [&](int sub, const bf16x8_t (&ak)[DS], const bf16x8_t (&av)[2]) {
-        f32x16_t x = mfma(ak[0], qtop[0], st.cmv);
+    struct VT {
+        bf16x8_t v[2];
+    };
+    auto loadK = [&](int sub) {
+        const int so = __builtin_amdgcn_readfirstlane(imin(sub, max_sub) * 32 * DD * 2);
+        KT r;
 #pragma unroll
-        for (int s = 1; s < DS; ++s) x = mfma(ak[s], qtop[s], x);
+        for (int s = 0; s < DS; ++s)
+            r.k[s] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + s * 32, so, 0));
+        return r;
+    };
+    auto loadV = [&](int sub) {
+        const int so = __builtin_amdgcn_readfirstlane(imin(sub, max_sub) * RB * 64);
+        VT r;
+        r.v[0] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rv, voff, so, 0));
+        r.v[1] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + 32, so, 0));
+        return r;
+    };
+    auto scores = [&](int sub, const KT& kt) {
+        f32x16_t x = mfma(kt.k[0], qtop[0], st.cmv);
+#pragma unroll
+        for (int s = 1; s < DS; ++s) x = mfma(kt.k[s], qtop[s], x);
         const int js = sub * 32;
         if (js + 31 > c.r0 - c.w) {  // staircase subtile: keep j <= i - w
 #pragma unroll
             for (int r = 0; r < 16; ++r)
                 if (js + acc_key(r, c.hg) > c.i - c.w) x[r] = -INFINITY;
         }
+        return x;
+    };
+    auto finish = [&](f32x16_t& x, const VT& vt, f32x16_t* xnext) {
         bf16x8_t p0, p1;
         if (FIXED) exp_pack<DD != 16>(x, st.l, p0, p1);
-        else softmax_step<NT, DD != 16>(x, st, ow, ol, p0, p1);
-        ol = mfma(av[0], p0, ol);
-        ol = mfma(av[1], p1, ol);
+        else softmax_step<NT, DD != 16>(x, st, ow, ol, p0, p1, xnext);
+        ol = mfma(vt.v[0], p0, ol);
+        ol = mfma(vt.v[1], p1, ol);
     };
-    bf16x8_t akA[DS], avA[2], akB[DS], avB[2];
-    load(0, akA, avA);
-    load(1, akB, avB);
-    int sub = 0;
-    for (; sub + 1 < n_sub; sub += 2) {
-        subtile(sub, akA, avA);
-        load(sub + 2, akA, avA);
-        subtile(sub + 1, akB, avB);
-        load(sub + 3, akB, avB);
+    if constexpr (D != 64 || DD != 16) {
+        // wider heads: no room for the pipeline's registers; two subtiles of
+        // loads in flight, scores and exponentials in sequence
+        KT ka = loadK(0), kb = loadK(1);
+        VT va = loadV(0), vb = loadV(1);
+        int n = 0;
+        for (; n + 1 < n_sub; n += 2) {
+            f32x16_t x = scores(n, ka);
+            ka = loadK(n + 2);
+            finish(x, va, nullptr);
+            va = loadV(n + 2);
+            x = scores(n + 1, kb);
+            kb = loadK(n + 3);
+            finish(x, vb, nullptr);
+            vb = loadV(n + 3);
+        }
+        if (n < n_sub) {
+            f32x16_t x = scores(n, ka);
+            finish(x, va, nullptr);
+        }
+        return;
     }
-    if (sub < n_sub) subtile(sub, akA, avA);
+    KT ka = loadK(0), kb = loadK(1), kc = loadK(2);
+    VT va = loadV(0), vb = loadV(1), vc = loadV(2);
+    f32x16_t x = scores(0, ka);
+    ka = loadK(3);
+    int n = 0;
+    for (; n + 2 < n_sub; n += 3) {
+        // x = scores of n; kb, kc, ka hold keys n+1..n+3; va, vb, vc values n..n+2
+        f32x16_t xn = scores(n + 1, kb);
+        kb = loadK(n + 4);
+        finish(x, va, &xn);
+        va = loadV(n + 3);
+        x = xn;
+        xn = scores(n + 2, kc);
+        kc = loadK(n + 5);
+        finish(x, vb, &xn);
+        vb = loadV(n + 4);
+        x = xn;
+        xn = scores(n + 3, ka);
+        ka = loadK(n + 6);
+        finish(x, vc, &xn);
+        vc = loadV(n + 5);
+        x = xn;
+    }
+    if (n + 1 < n_sub) {
+        f32x16_t xn = scores(n + 1, kb);
+        finish(x, va, &xn);
+        finish(xn, vb, nullptr);
+    } else if (n < n_sub) {
+        finish(x, va, nullptr);
+    }
 }
 
 // Local region with one tile of prefetch (d = 128, where a second register
@@ -637,8 +719,8 @@ void prefill_mfma_kernel(
 
         // ------------------------------------------------------------ distant region
         if (jd_end >= 0) {
-            if (fixed) distant_region<D, DD, true>(c, cK, cVt, consts, qtop, js_last, st, ow, ol);
-            else distant_region<D, DD, false>(c, cK, cVt, consts, qtop, js_last, st, ow, ol);
+            if (fixed) distant_region<D, DD, true>(c, cK, cVt, qtop, js_last, st, ow, ol);
+            else distant_region<D, DD, false>(c, cK, cVt, qtop, js_last, st, ow, ol);
         }
         // ------------------------------------------------------------ local region
         if (has_local) {

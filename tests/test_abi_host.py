@@ -48,13 +48,14 @@ def S(B=2, Hq=4, Hkv=2, d=64, dd=16, w=8, dtype=torch.bfloat16):
 
 
 def expected_prefill_ws(B, Hkv, T, dd, w, esize):
-    """Two latent buffers over Tp = round_up(T - w, 32) + 64 tokens (none when
-    T <= w), per-32-token latent norms and key norms (fp32), 256 bytes of
+    """Latent keys (Tp rows of dd) and transposed latent values (Tp/32 blocks
+    of up to dd + 1 rows of 32) over Tp = round_up(T - w, 32) + 64 tokens (none
+    when T <= w), per-32-token latent norms and key norms (fp32), 256 bytes of
     constant rows; every part 256-byte aligned."""
     al = lambda x: (x + 255) // 256 * 256
     Tp = (T - w + 31) // 32 * 32 + 64 if T > w else 0
-    return (2 * al(B * Hkv * Tp * dd * esize) + al(B * Hkv * (Tp // 32) * 4)
-            + al(B * Hkv * ((T + 31) // 32) * 4) + 256)
+    return (al(B * Hkv * Tp * dd * esize) + al(B * Hkv * Tp * (dd + 1) * esize)
+            + al(B * Hkv * (Tp // 32) * 4) + al(B * Hkv * ((T + 31) // 32) * 4) + 256)
 
 
 def test_prefill_workspace_size():
