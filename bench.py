@@ -37,10 +37,10 @@ CSRC = os.path.join(ROOT, "paper_2606_18587_amd", "csrc")
 MEASURED_TRAFFIC = {
     "prefill": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "latent.hip",
                           "prefill_mfma.hip"],
-                "sha256_16": "e7dfba8f6c8545e2", "bytes": 123410446},
+                "sha256_16": "e198041d0833cae5", "bytes": 130073991},
     "decode": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "decode.hip",
                          "decode_mfma.hip"],
-               "sha256_16": "f0f552842bced98b", "bytes": 572829238},
+               "sha256_16": "11223b6b26fe7967", "bytes": 581715433},
 }
 
 
@@ -209,7 +209,9 @@ def main():
                      "bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic("prefill")},
-        "roofline_decode": {"kernel": "dar_attn_decode (split + combine)", "bound": "hbm",
+        "roofline_decode": {"kernel": "dar_attn_decode (split-KV kernel; with one workgroup per "
+                                      "(batch, KV head) it also finishes the output, else a "
+                                      "combine kernel follows)", "bound": "hbm",
                             "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                             "frac": round(gbs / PEAK_HBM_GBS, 4),
                             "traffic": measured_traffic("decode")},
