@@ -180,3 +180,156 @@ int dar_oracle_num_threads(void)
     return 1;
 #endif
 }
+
+/*
+ * Backward of the causal prefill (the training setting of the paper's
+ * Section 2.3, Eq. 5): gradients of L = sum(dO * O) with respect to Q, K, V,
+ * W_down and W_up, by the chain rule applied to the definition above:
+ *
+ *   S_ij = q_i . key_ij / sqrt(d),  P_i = softmax_j(S_i),  O_i = sum_j P_ij val_ij
+ *   with key_ij = k_j (i - j < w) or k'_j = (k_j W_down) W_up, and the same for
+ *   val_ij (Eq. 3).
+ *   dP_ij = dO_i . val_ij,  dS_ij = P_ij (dP_ij - sum_l P_il dP_il)
+ *   dq_i = sum_j dS_ij key_ij / sqrt(d)
+ *   window pairs:  dk_j += dS_ij q_i / sqrt(d),  dv_j += P_ij dO_i
+ *   lifted pairs:  dk'_j += dS_ij q_i / sqrt(d),  dv'_j += P_ij dO_i, then
+ *   through x' = (x W_down) W_up (Eq. 1-2):
+ *     dx_j += dx'_j (W_down W_up)^T,
+ *     dW_down += x_j^T (dx'_j W_up^T),  dW_up += (x_j W_down)^T dx'_j.
+ *   Tied (wu NULL, W_up = W_down^T): dwd receives dW_down + dW_up^T and dwu
+ *   is not written.
+ *
+ *   q, dout, dq [B][Hq][T][d]; k, v, dk, dv [B][Hkv][T][d];
+ *   wd, dwd [Hkv][d][dd]; wu, dwu [Hkv][dd][d] (both NULL when tied).
+ * dk, dv, dwd, dwu are overwritten (not accumulated into).
+ * Returns 0, or -1 on a bad argument / allocation failure.
+ */
+int dar_oracle_backward(int B, int Hq, int Hkv, int T, int d, int dd, int w, const double* q,
+                        const double* k, const double* v, const double* wd, const double* wu,
+                        const double* dout, double* dq, double* dk, double* dv, double* dwd,
+                        double* dwu, int nthreads)
+{
+    if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || T < 1 || d < 1 || dd < 1 || w < 0)
+        return -1;
+    if ((wu == NULL) != (dwu == NULL)) return -1;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    const int group = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)d);
+    const size_t wsz = (size_t)d * dd;
+    /* per (b, g) partial weight gradients, summed over b afterwards in order */
+    double* pwd = (double*)calloc((size_t)B * Hkv * wsz, sizeof(double));
+    double* pwu = (double*)calloc((size_t)B * Hkv * wsz, sizeof(double));
+    if (!pwd || !pwu) { free(pwd); free(pwu); return -1; }
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int bg = 0; bg < B * Hkv; ++bg) {
+        const int b = bg / Hkv, g = bg % Hkv;
+        const double* kb = k + (size_t)bg * T * d;
+        const double* vb = v + (size_t)bg * T * d;
+        const double* wdg = wd + (size_t)g * wsz;
+        const double* wug = wu ? wu + (size_t)g * wsz : NULL;
+        double* dkb = dk + (size_t)bg * T * d;
+        double* dvb = dv + (size_t)bg * T * d;
+        double* kl = lift_all(T, d, dd, kb, wdg, wug);
+        double* vl = lift_all(T, d, dd, vb, wdg, wug);
+        double* dkl = (double*)calloc((size_t)T * d, sizeof(double));  /* dk'_j */
+        double* dvl = (double*)calloc((size_t)T * d, sizeof(double));  /* dv'_j */
+        double* p = (double*)malloc(sizeof(double) * (size_t)T);
+        double* s = (double*)malloc(sizeof(double) * (size_t)T);
+        double* dp = (double*)malloc(sizeof(double) * (size_t)T);
+        double* oi = (double*)malloc(sizeof(double) * (size_t)d);
+        if (!kl || !vl || !dkl || !dvl || !p || !s || !dp || !oi) {
+#pragma omp atomic write
+            bad = 1;
+        } else {
+            for (size_t x = 0; x < (size_t)T * d; ++x) { dkb[x] = 0.0; dvb[x] = 0.0; }
+            for (int hh = 0; hh < group; ++hh) {
+                const int h = g * group + hh;
+                const double* qh = q + ((size_t)b * Hq + h) * T * d;
+                const double* doh = dout + ((size_t)b * Hq + h) * T * d;
+                double* dqh = dq + ((size_t)b * Hq + h) * T * d;
+                for (int i = 0; i < T; ++i) {
+                    const double* qi = qh + (size_t)i * d;
+                    const double* doi = doh + (size_t)i * d;
+                    one_row(d, w, i, qi, kb, vb, kl, vl, s, oi, p);
+                    double delta = 0.0;
+                    for (int j = 0; j <= i; ++j) {
+                        const double* val = (i - j < w) ? vb + (size_t)j * d : vl + (size_t)j * d;
+                        double acc = 0.0;
+                        for (int e = 0; e < d; ++e) acc += doi[e] * val[e];
+                        dp[j] = acc;
+                        delta += p[j] * acc;
+                    }
+                    double* dqi = dqh + (size_t)i * d;
+                    for (int e = 0; e < d; ++e) dqi[e] = 0.0;
+                    for (int j = 0; j <= i; ++j) {
+                        const double ds = p[j] * (dp[j] - delta);
+                        const int local = i - j < w;
+                        const double* key = local ? kb + (size_t)j * d : kl + (size_t)j * d;
+                        double* dkey = local ? dkb + (size_t)j * d : dkl + (size_t)j * d;
+                        double* dval = local ? dvb + (size_t)j * d : dvl + (size_t)j * d;
+                        for (int e = 0; e < d; ++e) {
+                            dqi[e] += ds * key[e] * scale;
+                            dkey[e] += ds * qi[e] * scale;
+                            dval[e] += p[j] * doi[e];
+                        }
+                    }
+                }
+            }
+            /* through the lift x' = (x W_down) W_up, for keys and for values */
+            double* pwdg = pwd + (size_t)bg * wsz;
+            double* pwug = pwu + (size_t)bg * wsz;
+            for (int which = 0; which < 2; ++which) {
+                const double* xb = which ? vb : kb;
+                const double* dxl = which ? dvl : dkl;
+                double* dxb = which ? dvb : dkb;
+                for (int j = 0; j < T; ++j) {
+                    const double* xj = xb + (size_t)j * d;
+                    const double* gj = dxl + (size_t)j * d;
+                    for (int c = 0; c < dd; ++c) {
+                        /* u_c = (dx'_j W_up^T)[c], h_c = (x_j W_down)[c] */
+                        double u = 0.0, hc = 0.0;
+                        for (int e = 0; e < d; ++e) {
+                            const double wup = wug ? wug[(size_t)c * d + e] : wdg[(size_t)e * dd + c];
+                            u += gj[e] * wup;
+                            hc += xj[e] * wdg[(size_t)e * dd + c];
+                        }
+                        for (int e = 0; e < d; ++e) {
+                            dxb[(size_t)j * d + e] += u * wdg[(size_t)e * dd + c];
+                            pwdg[(size_t)e * dd + c] += xj[e] * u;
+                            pwug[(size_t)c * d + e] += hc * gj[e];
+                        }
+                    }
+                }
+            }
+        }
+        free(kl); free(vl); free(dkl); free(dvl); free(p); free(s); free(dp); free(oi);
+    }
+    if (!bad) {
+        for (int g = 0; g < Hkv; ++g) {
+            double* dwdg = dwd + (size_t)g * wsz;
+            double* dwug = dwu ? dwu + (size_t)g * wsz : NULL;
+            for (size_t x = 0; x < wsz; ++x) {
+                dwdg[x] = 0.0;
+                if (dwug) dwug[x] = 0.0;
+            }
+            for (int b = 0; b < B; ++b) {
+                const double* a = pwd + ((size_t)b * Hkv + g) * wsz;
+                const double* u = pwu + ((size_t)b * Hkv + g) * wsz;
+                for (int e = 0; e < d; ++e)
+                    for (int c = 0; c < dd; ++c) {
+                        dwdg[(size_t)e * dd + c] += a[(size_t)e * dd + c];
+                        if (dwug) dwug[(size_t)c * d + e] += u[(size_t)c * d + e];
+                        else dwdg[(size_t)e * dd + c] += u[(size_t)c * d + e];  /* tied: + dW_up^T */
+                    }
+            }
+        }
+    }
+    free(pwd);
+    free(pwu);
+    return bad ? -1 : 0;
+}

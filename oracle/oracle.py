@@ -8,6 +8,8 @@ Functions follow the paper's method section:
   lift()      Eq. 1 then Eq. 2, x' = (x W_down) W_up
   rows()      Eq. 3-4 for chosen query rows of one head
   prefill()   Eq. 3-4 for every row of a batch (causal prefill)
+  backward()  gradients of sum(dO * O) of the prefill (Section 2.3, the
+              training setting) with respect to Q, K, V, W_down, W_up
   cache_model()  where the split cache keeps each token after n appends
                  (the efficient cache of the Limitations section: full K/V for
                  the last w tokens, the d_down latent for older ones)
@@ -68,6 +70,8 @@ class Oracle:
         lib.dar_oracle_up.restype = None
         lib.dar_oracle_up.argtypes = [ctypes.c_int] * 3 + [_dp, _dp, _dp, _dp]
         lib.dar_oracle_num_threads.restype = ctypes.c_int
+        lib.dar_oracle_backward.restype = ctypes.c_int
+        lib.dar_oracle_backward.argtypes = [ctypes.c_int] * 7 + [_dp] * 11 + [ctypes.c_int]
         self.lib = lib
 
     def num_threads(self) -> int:
@@ -133,6 +137,32 @@ class Oracle:
         return o
 
 
+    def backward(self, q, k, v, wd, wu, w, dout, threads=0):
+        """Gradients of sum(dout * O) of the causal prefill (Section 2.3's
+        training setting): returns dq, dk, dv, dwd, dwu (dwu is None when
+        tied; dwd then holds the gradient of the tied matrix)."""
+        q = _c64(q)
+        k = _c64(k)
+        v = _c64(v)
+        wd = _c64(wd)
+        wu_c = None if wu is None else _c64(wu)
+        dout = _c64(dout)
+        B, Hq, T, d = q.shape
+        Hkv = k.shape[1]
+        dd = wd.shape[2]
+        dq = np.empty_like(q)
+        dk = np.empty_like(k)
+        dv = np.empty_like(v)
+        dwd = np.empty_like(wd)
+        dwu = None if wu is None else np.empty_like(wu_c)
+        rc = self.lib.dar_oracle_backward(B, Hq, Hkv, T, d, dd, int(w), _ptr(q), _ptr(k), _ptr(v),
+                                          _ptr(wd), _ptr(wu_c), _ptr(dout), _ptr(dq), _ptr(dk),
+                                          _ptr(dv), _ptr(dwd), _ptr(dwu), int(threads))
+        if rc != 0:
+            raise ValueError("dar_oracle_backward rejected its arguments")
+        return dq, dk, dv, dwd, dwu
+
+
 _default = None
 
 
@@ -161,6 +191,10 @@ def rows(k, v, wd, wu, w, pos, qr, want_p=False):
 
 def prefill(q, k, v, wd, wu, w, threads=0):
     return default().prefill(q, k, v, wd, wu, w, threads)
+
+
+def backward(q, k, v, wd, wu, w, dout, threads=0):
+    return default().backward(q, k, v, wd, wu, w, dout, threads)
 
 
 def cache_model(n_tokens: int, w: int, cap: int):

@@ -18,6 +18,17 @@ References for what is pinned:
     here with the library routine torch.nn.functional.scaled_dot_product_attention.
   * Hand-derived closed forms (tests/golden/hand_examples.json).
   * Pure-Python brute force (oracle/brute.py) on tiny inputs.
+
+Backward (gradients of sum(dO * O), the training setting of Section 2.3):
+  * central finite differences of the forward prefill (itself pinned above);
+  * torch fp64 autograd of the dual-store masked attention, written here with
+    plain tensor ops;
+  * w >= T: ordinary causal attention's autograd, and exactly zero gradient
+    for W_down and W_up, which the paper says are updated only from positions
+    whose query takes the global path;
+  * closed forms: T = 1, Euler's identity <dV, V> = sum(dO * O) (O is linear
+    in V), and the gauge identity W_down^T dW_down = dW_up W_up^T that follows
+    from the invariance under W_down -> W_down M, W_up -> M^-1 W_up.
 """
 from __future__ import annotations
 
@@ -262,6 +273,150 @@ def check_rows_match_prefill(orc, seed=13):
                                    atol=0)
 
 
+# ---------------------------------------------------------------- backward
+
+def torch_dual_store(q, k, v, wd, wu, w):
+    """Eq. 3-4 over the dual store with plain torch ops (differentiable):
+    [lifted tokens ; full tokens] as 2T keys, the distance picking one of each
+    pair through the mask."""
+    B, Hq, T, d = q.shape
+    G = Hq // k.shape[1]
+    wu_full = wd.transpose(1, 2) if wu is None else wu
+    lift = lambda x: torch.matmul(torch.matmul(x, wd[None]), wu_full[None])
+    K2 = torch.cat([lift(k), k], dim=2).repeat_interleave(G, dim=1)
+    V2 = torch.cat([lift(v), v], dim=2).repeat_interleave(G, dim=1)
+    s = torch.matmul(q, K2.transpose(-1, -2)) / math.sqrt(d)
+    i = torch.arange(T)[:, None]
+    j = torch.arange(T)[None, :]
+    causal = j <= i
+    near = (i - j) < w
+    mask = torch.cat([causal & ~near, causal & near], dim=1)
+    s = s.masked_fill(~mask, float("-inf"))
+    return torch.matmul(torch.softmax(s, dim=-1), V2)
+
+
+def torch_grads(fn, dout, *arrays):
+    """Gradients of sum(dout * fn(*arrays)) by fp64 autograd on the CPU; a
+    None array stays None."""
+    ts = [None if a is None else torch.tensor(a, dtype=torch.float64, requires_grad=True)
+          for a in arrays]
+    out = fn(*ts)
+    (out * torch.tensor(dout)).sum().backward()
+    return [None if t is None else t.grad.numpy() for t in ts]
+
+
+def _bwd_case(seed, untied, **kw):
+    q, k, v, wd, wu = rand_case(seed, untied=untied, **kw)
+    dout = rng(seed + 1000).standard_normal(q.shape)
+    return q, k, v, wd, wu, dout
+
+
+def _assert_grads(got, ref, atol, what):
+    names = ("dq", "dk", "dv", "dwd", "dwu")
+    for n, a, b in zip(names, got, ref):
+        if b is None:
+            assert a is None, what + " " + n
+            continue
+        np.testing.assert_allclose(a, b, rtol=0, atol=atol, err_msg=what + " " + n)
+
+
+def check_backward_finite_differences(orc, seed=21):
+    """Central differences of L = sum(dO * O) through the forward prefill."""
+    h = 1e-5
+    for untied in (False, True):
+        for w in (0, 2, 9):
+            q, k, v, wd, wu, dout = _bwd_case(seed + w, untied, B=1, Hq=2, Hkv=1, T=7, d=4,
+                                              dd=2)
+            got = orc.backward(q, k, v, wd, wu, w, dout)
+            args = [q, k, v, wd, wu]
+            for a_i, a in enumerate(args):
+                if a is None:
+                    continue
+                fd = np.empty_like(a)
+                flat = a.reshape(-1)
+                for x in range(flat.size):
+                    keep = flat[x]
+                    flat[x] = keep + h
+                    lp = np.sum(dout * orc.prefill(*args, w))
+                    flat[x] = keep - h
+                    lm = np.sum(dout * orc.prefill(*args, w))
+                    flat[x] = keep
+                    fd.reshape(-1)[x] = (lp - lm) / (2 * h)
+                np.testing.assert_allclose(got[a_i], fd, rtol=0, atol=1e-7,
+                                           err_msg="fd untied=%s w=%d arg %d" % (untied, w, a_i))
+
+
+def check_backward_dual_store_autograd(orc, seed=22):
+    for untied in (False, True):
+        for w in (0, 1, 5, 22, 30):
+            q, k, v, wd, wu, dout = _bwd_case(seed + w, untied)
+            ref = torch_grads(lambda *t: torch_dual_store(*t, w), dout, q, k, v, wd, wu)
+            got = orc.backward(q, k, v, wd, wu, w, dout)
+            _assert_grads(got, ref, 1e-11, "dual store untied=%s w=%d" % (untied, w))
+
+
+def check_backward_vanilla_no_bottleneck_gradient(orc, seed=23):
+    """w >= T: plain causal attention's gradients; W_down and W_up get none."""
+    for untied in (False, True):
+        q, k, v, wd, wu, dout = _bwd_case(seed, untied)
+        T, Hq = q.shape[2], q.shape[1]
+
+        def vanilla(tq, tk, tv):
+            G = Hq // tk.shape[1]
+            return torch.nn.functional.scaled_dot_product_attention(
+                tq, tk.repeat_interleave(G, dim=1), tv.repeat_interleave(G, dim=1),
+                is_causal=True)
+
+        rq, rk, rv = torch_grads(vanilla, dout, q, k, v)
+        for w in (T, T + 5):
+            dq, dk, dv, dwd, dwu = orc.backward(q, k, v, wd, wu, w, dout)
+            _assert_grads((dq, dk, dv), (rq, rk, rv), 1e-12, "vanilla w=%d" % w)
+            assert np.all(dwd == 0.0)
+            assert dwu is None or np.all(dwu == 0.0)
+
+
+def check_backward_single_token(orc, seed=24):
+    """T = 1: O is the first value (full or lifted), so dq = dk = 0 and the
+    value and bottleneck gradients have closed forms."""
+    for untied in (False, True):
+        q, k, v, wd, wu, dout = _bwd_case(seed, untied, B=2, Hq=4, Hkv=2, T=1, d=6, dd=2)
+        dsum = dout.reshape(2, 2, 2, 1, 6).sum(axis=2)      # summed over each head group
+        for w in (0, 1, 3):
+            dq, dk, dv, dwd, dwu = orc.backward(q, k, v, wd, wu, w, dout)
+            assert np.all(dq == 0.0) and np.all(dk == 0.0)
+            if w >= 1:
+                np.testing.assert_allclose(dv, dsum, rtol=0, atol=1e-14)
+                assert np.all(dwd == 0.0)
+                continue
+            wu_f = np.swapaxes(wd, 1, 2) if wu is None else wu
+            for b in range(2):
+                for g in range(2):
+                    np.testing.assert_allclose(dv[b, g, 0], dsum[b, g, 0] @ (wd[g] @ wu_f[g]).T,
+                                               rtol=0, atol=1e-13)
+            u = np.einsum("bge,gce->bgc", dsum[:, :, 0], wu_f)          # dO W_up^T
+            gwd = np.einsum("bgd,bgc->gdc", v[:, :, 0], u)
+            gwu = np.einsum("bgc,bge->gce", np.einsum("bgd,gdc->bgc", v[:, :, 0], wd),
+                            dsum[:, :, 0])
+            if wu is None:
+                np.testing.assert_allclose(dwd, gwd + np.swapaxes(gwu, 1, 2), rtol=0, atol=1e-13)
+            else:
+                np.testing.assert_allclose(dwd, gwd, rtol=0, atol=1e-13)
+                np.testing.assert_allclose(dwu, gwu, rtol=0, atol=1e-13)
+
+
+def check_backward_identities(orc, seed=25):
+    """<dV, V> = sum(dO * O) (O is homogeneous of degree one in V, through
+    both paths), and W_down^T dW_down = dW_up W_up^T (gauge invariance)."""
+    for w in (0, 3, 10):
+        q, k, v, wd, wu, dout = _bwd_case(seed + w, True)
+        dq, dk, dv, dwd, dwu = orc.backward(q, k, v, wd, wu, w, dout)
+        L = np.sum(dout * orc.prefill(q, k, v, wd, wu, w))
+        assert abs(np.sum(dv * v) - L) < 1e-10 * max(1.0, abs(L))
+        lhs = np.einsum("gdc,gde->gce", wd, dwd)
+        rhs = np.einsum("gcd,ged->gce", dwu, wu)
+        np.testing.assert_allclose(lhs, rhs, rtol=0, atol=1e-10)
+
+
 ALL_CHECKS = [
     check_vanilla_when_window_covers,
     check_rows_inside_window_are_vanilla,
@@ -277,4 +432,9 @@ ALL_CHECKS = [
     check_first_row,
     check_gqa_is_repeated_mha,
     check_rows_match_prefill,
+    check_backward_finite_differences,
+    check_backward_dual_store_autograd,
+    check_backward_vanilla_no_bottleneck_gradient,
+    check_backward_single_token,
+    check_backward_identities,
 ]

@@ -28,6 +28,21 @@ MUTANTS = [
     ("lift_only_keys", "double* vl = lift_all(T, d, dd, v, wd, wu);",
      "double* vl = lift_all(T, d, dd, k, wd, wu);"),
     ("max_not_subtracted_sign", "s[j] = exp(s[j] - m);", "s[j] = exp(m - s[j]);"),
+    # backward
+    ("bwd_softmax_jacobian_drops_delta", "const double ds = p[j] * (dp[j] - delta);",
+     "const double ds = p[j] * dp[j];"),
+    ("bwd_dq_unscaled", "dqi[e] += ds * key[e] * scale;", "dqi[e] += ds * key[e];"),
+    ("bwd_dv_uses_ds", "dval[e] += p[j] * doi[e];", "dval[e] += ds * doi[e];"),
+    ("bwd_window_edge_le", "const int local = i - j < w;", "const int local = i - j <= w;"),
+    ("bwd_tied_misses_up_term", "else dwdg[(size_t)e * dd + c] += u[(size_t)c * d + e];",
+     "else (void)0;"),
+    ("bwd_lift_skips_input_gradient", "dxb[(size_t)j * d + e] += u * wdg[(size_t)e * dd + c];",
+     "(void)dxb;"),
+    ("bwd_dwd_uses_latent", "pwdg[(size_t)e * dd + c] += xj[e] * u;",
+     "pwdg[(size_t)e * dd + c] += xj[e] * hc;"),
+    ("bwd_delta_from_key", "delta += p[j] * acc;", "delta += p[j] * acc * (j > 0);"),
+    ("bwd_dwu_from_gradient_of_key_only", "const double* dxl = which ? dvl : dkl;",
+     "const double* dxl = dkl;"),
 ]
 
 
