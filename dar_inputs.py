@@ -28,7 +28,7 @@ import numpy as np
 SEED_BASE = 260618587
 
 # tensor ids inside one workload's seed space
-TID_Q, TID_K, TID_V, TID_WD, TID_WU = 0, 1, 2, 3, 4
+TID_Q, TID_K, TID_V, TID_WD, TID_WU, TID_DO = 0, 1, 2, 3, 4, 5
 
 
 @dataclass(frozen=True)
@@ -159,6 +159,15 @@ def make_prefill_inputs(wl: Workload, untied: bool = False, seed_shift: int = 0,
     if untied:
         wu = normal((wl.Hkv, wl.dd, wl.d), seed_for(wl.cfg_id, TID_WU) + s, std=1.0 / np.sqrt(wl.dd))
         out["wu"] = Tensor(wu, wl.dtype)
+    return out
+
+
+def make_backward_inputs(wl: Workload, untied: bool = False, seed_shift: int = 0,
+                         q_scale: float = 1.0) -> dict:
+    """The prefill inputs plus the incoming gradient dout [B,Hq,T,d] ~ N(0,1)."""
+    out = make_prefill_inputs(wl, untied=untied, seed_shift=seed_shift, q_scale=q_scale)
+    dout = normal((wl.B, wl.Hq, wl.T, wl.d), seed_for(wl.cfg_id, TID_DO) + seed_shift)
+    out["dout"] = Tensor(dout, wl.dtype)
     return out
 
 

@@ -23,7 +23,8 @@
  *     for the tied form W_up = W_down^T.
  *   - GQA: query head h reads KV head h / (Hq / Hkv).
  *   - Layout: row-major, contiguous, [B][H][T][d]. Every tensor of a call has
- *     the dtype of the shape (fp32 or bf16); bf16 runs accumulate in fp32.
+ *     the dtype of the shape (fp32 or bf16), except the weight gradients of
+ *     the backward, which are fp32; bf16 runs accumulate in fp32.
  *   - Positions are 0-based and implicit (prefill: 0..T-1; decode: the query
  *     sits at position len-1 of the cache). Rotary position embedding, if any,
  *     is applied by the caller before these calls.
@@ -111,9 +112,35 @@ dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q
                            const void* w_down, const void* w_up, void* o, void* ws,
                            size_t ws_bytes, hipStream_t stream);
 
+/* Backward of dar_attn_prefill: the gradients of L = sum(dout * o) with
+ * respect to q, k, v, W_down and W_up (the training setting of Section 2.3,
+ * whose objective is Eq. 5; the bottleneck weights receive gradient only
+ * through the pairs whose query takes the distant path).
+ *   q, k, v, w_down, w_up: the forward's inputs (w_up NULL = tied);
+ *   o [B][Hq][T][d]: the forward's output (used for delta_i = dout_i . o_i);
+ *   dout [B][Hq][T][d]: the incoming gradient;
+ *   dq [B][Hq][T][d], dk, dv [B][Hkv][T][d]: outputs in the shape's dtype;
+ *   dw_down [Hkv][d][d_down], dw_up [Hkv][d_down][d]: fp32 outputs whatever
+ *   the shape's dtype (sums over every row of the batch). Tied (w_up NULL):
+ *   dw_up must be NULL and dw_down receives the gradient of the shared matrix,
+ *   dW_down + dW_up^T. Untied: dw_up must be non-NULL.
+ *   Every output is overwritten (not accumulated into); the row softmax
+ *   statistics are recomputed, nothing from the forward call besides o is
+ *   needed.
+ *   ws: device workspace of at least dar_prefill_backward_workspace_bytes(s, T)
+ *   bytes (caller-owned, overwritten). The result does not depend on the
+ *   stream or on timing: every reduction runs in a fixed order.
+ * Supported: as dar_attn_prefill. */
+dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, const void* k,
+                                     const void* v, const void* w_down, const void* w_up,
+                                     const void* o, const void* dout, void* dq, void* dk,
+                                     void* dv, float* dw_down, float* dw_up, void* ws,
+                                     size_t ws_bytes, hipStream_t stream);
+
 /* Workspace sizes (0 on an invalid shape). */
 size_t dar_prefill_workspace_bytes(const dar_shape* s, int T);
 size_t dar_decode_workspace_bytes(const dar_shape* s, int cap);
+size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T);
 
 /* Static English text for a status code. */
 const char* dar_status_string(dar_status st);

@@ -55,6 +55,10 @@ def _load():
     lib.dar_prefill_workspace_bytes.argtypes = [shp, ci]
     lib.dar_decode_workspace_bytes.restype = sz
     lib.dar_decode_workspace_bytes.argtypes = [shp, ci]
+    lib.dar_attn_prefill_backward.restype = ci
+    lib.dar_attn_prefill_backward.argtypes = [shp, ci] + [vp] * 13 + [sz, vp]
+    lib.dar_prefill_backward_workspace_bytes.restype = sz
+    lib.dar_prefill_backward_workspace_bytes.argtypes = [shp, ci]
     lib.dar_status_string.restype = ctypes.c_char_p
     lib.dar_status_string.argtypes = [ci]
     return lib
@@ -63,7 +67,9 @@ def _load():
 lib = _load()
 
 EXPORTS = ("dar_attn_prefill", "dar_cache_append", "dar_attn_decode",
-           "dar_prefill_workspace_bytes", "dar_decode_workspace_bytes", "dar_status_string")
+           "dar_attn_prefill_backward", "dar_prefill_workspace_bytes",
+           "dar_decode_workspace_bytes", "dar_prefill_backward_workspace_bytes",
+           "dar_status_string")
 
 
 def status_string(st: int) -> str:
@@ -104,6 +110,10 @@ def dar_decode_workspace_bytes(shape: DarShape, cap: int) -> int:
     return int(lib.dar_decode_workspace_bytes(ctypes.byref(shape), int(cap)))
 
 
+def dar_prefill_backward_workspace_bytes(shape: DarShape, T: int) -> int:
+    return int(lib.dar_prefill_backward_workspace_bytes(ctypes.byref(shape), int(T)))
+
+
 def dar_status_string(st: int) -> str:
     return status_string(st)
 
@@ -141,6 +151,42 @@ def dar_attn_prefill(q, k, v, w_down, w_up, w, o=None, ws=None, stream=None, che
     if st != DAR_OK:
         raise DarError(st, "dar_attn_prefill")
     return o
+
+
+def dar_attn_prefill_backward(q, k, v, w_down, w_up, w, o, dout, ws=None, stream=None,
+                              check=True):
+    """Gradients of sum(dout * o) of the causal DAR prefill. Returns
+    (dq, dk, dv, dw_down, dw_up): dq/dk/dv in the input dtype, the weight
+    gradients fp32; dw_up is None when tied (w_up None), dw_down then holds the
+    gradient of the shared matrix."""
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    dd = w_down.shape[2]
+    shape = make_shape(B, Hq, Hkv, d, dd, w, q.dtype)
+    if check:
+        for name, t, want in (("k", k, (B, Hkv, T, d)), ("v", v, (B, Hkv, T, d)),
+                              ("w_down", w_down, (Hkv, d, dd)), ("o", o, (B, Hq, T, d)),
+                              ("dout", dout, (B, Hq, T, d))):
+            if tuple(t.shape) != want or t.dtype != q.dtype:
+                raise ValueError("%s: expected %s %s, got %s %s" % (name, want, q.dtype,
+                                                                   tuple(t.shape), t.dtype))
+        if w_up is not None and (tuple(w_up.shape) != (Hkv, dd, d) or w_up.dtype != q.dtype):
+            raise ValueError("w_up: expected %s" % ((Hkv, dd, d),))
+    dq = torch.empty_like(q)
+    dk = torch.empty_like(k)
+    dv = torch.empty_like(v)
+    dwd = torch.empty(Hkv, d, dd, dtype=torch.float32, device=q.device)
+    dwu = None if w_up is None else torch.empty(Hkv, dd, d, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = _workspace(dar_prefill_backward_workspace_bytes(shape, T), q.device)
+    st = lib.dar_attn_prefill_backward(ctypes.byref(shape), int(T), _ptr(q), _ptr(k), _ptr(v),
+                                       _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(dout), _ptr(dq),
+                                       _ptr(dk), _ptr(dv), _ptr(dwd), _ptr(dwu), _ptr(ws),
+                                       0 if ws is None else ws.numel() * ws.element_size(),
+                                       _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_prefill_backward")
+    return dq, dk, dv, dwd, dwu
 
 
 class DarCache:

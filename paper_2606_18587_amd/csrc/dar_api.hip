@@ -101,6 +101,11 @@ size_t dar_decode_workspace_bytes(const dar_shape* s, int cap) {
     return (size_t)s->B * s->Hq * S * (2 + s->d_down + s->d) * sizeof(float);
 }
 
+size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T) {
+    if (check_shape(s) != DAR_OK || T < 1) return 0;
+    return bwd_ws_layout(s->B, s->Hq, s->Hkv, T, s->d, s->d_down).bytes;
+}
+
 dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void* k,
                             const void* v, const void* w_down, const void* w_up, void* o,
                             void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -152,6 +157,45 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
                                            (const float*)cK, (const float*)cV, (float*)o, s->B,
                                            s->Hq, s->Hkv, T, s->d, s->d_down, s->w, stream);
     }
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, const void* k,
+                                     const void* v, const void* w_down, const void* w_up,
+                                     const void* o, const void* dout, void* dq, void* dk,
+                                     void* dv, float* dw_down, float* dw_up, void* ws,
+                                     size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (T < 1) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(w_down) || !dev_ok(o) || !dev_ok(dout))
+        return DAR_E_ARG;
+    if (!dev_ok(dq) || !dev_ok(dk) || !dev_ok(dv) || !dev_ok(dw_down)) return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if ((w_up == nullptr) != (dw_up == nullptr)) return DAR_E_ARG;
+    if (dw_up && !aligned16(dw_up)) return DAR_E_ARG;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+    const BwdWs L = bwd_ws_layout(s->B, s->Hq, s->Hkv, T, s->d, s->d_down);
+    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+
+    clear_hip_error();
+    if (log_enabled())
+        fprintf(stderr, "[dar] prefill_backward B=%d Hq=%d Hkv=%d T=%d d=%d dd=%d w=%d %s\n", s->B,
+                s->Hq, s->Hkv, T, s->d, s->d_down, s->w, s->dtype == DAR_BF16 ? "bf16" : "f32");
+    hipError_t e;
+    if (s->dtype == DAR_BF16)
+        e = launch_bwd_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v,
+                                    (const bf16_t*)o, (const bf16_t*)dout, (const bf16_t*)w_down,
+                                    (const bf16_t*)w_up, (bf16_t*)dq, (bf16_t*)dk, (bf16_t*)dv,
+                                    dw_down, dw_up, (char*)ws, L, s->B, s->Hq, s->Hkv, T, s->d,
+                                    s->d_down, s->w, stream);
+    else
+        e = launch_bwd_valu<float>((const float*)q, (const float*)k, (const float*)v,
+                                   (const float*)o, (const float*)dout, (const float*)w_down,
+                                   (const float*)w_up, (float*)dq, (float*)dk, (float*)dv,
+                                   dw_down, dw_up, (char*)ws, L, s->B, s->Hq, s->Hkv, T, s->d,
+                                   s->d_down, s->w, stream);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 

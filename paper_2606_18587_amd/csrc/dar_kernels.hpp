@@ -76,4 +76,37 @@ hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, c
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
                          int d, int dd, int w, int cap, int len, hipStream_t st);
 
+// Prefill backward workspace (all fp32, 256-byte aligned parts):
+//   lse, delta        [B*Hq][T]        log2-domain log-sum-exp of each row; dO . O
+//   qt, dot, hk, ol   [B*Hq][T][dd]    q W_up^T, dO W_up^T, sum dS c^K, sum P c^V
+//   ck, cv, gk, gv    [B*Hkv][T][dd]   latents; sum dS q~, sum P dO~ per key
+//   wpart             [2][Hkv][nchunk][d][dd]  weight-gradient partials per chunk
+struct BwdWs {
+    size_t lse_off, delta_off, qt_off, dot_off, hk_off, ol_off, ck_off, cv_off, gk_off, gv_off,
+        wpart_off, bytes;
+    int nchunk_d, nchunk_u, nchunk;
+};
+// Row chunks of the weight-gradient reduction: about 256 rows each, at most 128.
+static inline int bwd_nchunk(long long rows) {
+    long long n = (rows + 255) / 256;
+    return (int)(n < 1 ? 1 : (n > 128 ? 128 : n));
+}
+BwdWs bwd_ws_layout(int B, int Hq, int Hkv, int T, int d, int dd);
+
+template <typename T>
+hipError_t launch_bwd_prep(const T* q, const T* k, const T* v, const T* o, const T* dout,
+                           const T* wd, const T* wu, float* ck, float* cv, float* qt, float* dot,
+                           float* delta, int B, int Hq, int Hkv, int T_, int d, int dd,
+                           hipStream_t st);
+template <typename T>
+hipError_t launch_bwd_weights(const T* q, const T* k, const T* v, const T* dout, const float* gk,
+                              const float* gv, const float* hk, const float* ol, float* part,
+                              float* dwd, float* dwu, int B, int Hq, int Hkv, int T_, int d,
+                              int dd, const BwdWs& L, hipStream_t st);
+template <typename T>
+hipError_t launch_bwd_valu(const T* q, const T* k, const T* v, const T* o, const T* dout,
+                           const T* wd, const T* wu, T* dq, T* dk, T* dv, float* dwd, float* dwu,
+                           char* ws, const BwdWs& L, int B, int Hq, int Hkv, int T_, int d, int dd,
+                           int w, hipStream_t st);
+
 }  // namespace dar

@@ -30,7 +30,8 @@ def declared_functions():
 def test_exports_every_declared_symbol():
     names = declared_functions()
     assert set(names) == {"dar_attn_prefill", "dar_cache_append", "dar_attn_decode",
-                          "dar_prefill_workspace_bytes", "dar_decode_workspace_bytes",
+                          "dar_attn_prefill_backward", "dar_prefill_workspace_bytes",
+                          "dar_decode_workspace_bytes", "dar_prefill_backward_workspace_bytes",
                           "dar_status_string"}
     raw = ctypes.CDLL(dar.LIB_PATH)
     for n in names:
@@ -157,3 +158,53 @@ def test_decode_rejects():
 def test_python_binding_names_match_abi():
     for n in declared_functions():
         assert hasattr(dar, n), n
+
+
+def expected_backward_ws(B, Hq, Hkv, T, d, dd):
+    """fp32: log-sum-exp and delta per row, four d_down-wide row arrays (q W_up^T,
+    dO W_up^T and the two distant sums), four d_down-wide key arrays (latents
+    and the two distant sums), weight partials over min(128, ceil(rows/256))
+    chunks; every part 256-byte aligned."""
+    al = lambda x: (x + 255) // 256 * 256
+    rows, toks = B * Hq * T, B * Hkv * T
+    nch = lambda r: min(128, max(1, (r + 255) // 256))
+    nchunk = max(nch(B * T), nch(B * (Hq // Hkv) * T))
+    return (2 * al(rows * 4) + 4 * al(rows * dd * 4) + 4 * al(toks * dd * 4)
+            + al(2 * Hkv * nchunk * d * dd * 4))
+
+
+def test_backward_workspace_size():
+    for kw, T in (({}, 100), ({"Hq": 8, "Hkv": 2}, 3000), ({"d": 128, "dd": 32}, 1)):
+        s = S(**kw)
+        assert dar.dar_prefill_backward_workspace_bytes(s, T) == expected_backward_ws(
+            s.B, s.Hq, s.Hkv, T, s.d, s.d_down)
+    assert dar.dar_prefill_backward_workspace_bytes(S(Hq=3), 64) == 0
+    assert dar.dar_prefill_backward_workspace_bytes(S(), 0) == 0
+
+
+def call_backward(shape, T=16, wu=None, dwu=None, ws=FAKE, ws_bytes=1 << 30, **kw):
+    args = dict(q=FAKE, k=FAKE, v=FAKE, wd=FAKE, o=FAKE, dout=FAKE, dq=FAKE, dk=FAKE, dv=FAKE,
+                dwd=FAKE)
+    args.update(kw)
+    return dar.lib.dar_attn_prefill_backward(
+        ctypes.byref(shape), T, args["q"], args["k"], args["v"], args["wd"], wu, args["o"],
+        args["dout"], args["dq"], args["dk"], args["dv"], args["dwd"], dwu, ws, ws_bytes, None)
+
+
+@no_gpu
+@pytest.mark.parametrize("kw,shape_kw,expect", [
+    ({}, {"Hq": 3}, dar.DAR_E_ARG),
+    ({"T": 0}, {}, dar.DAR_E_ARG),
+    ({"dout": None}, {}, dar.DAR_E_ARG),
+    ({"o": MISALIGNED}, {}, dar.DAR_E_ARG),
+    ({"dwd": None}, {}, dar.DAR_E_ARG),
+    ({"wu": FAKE}, {}, dar.DAR_E_ARG),             # untied needs dw_up
+    ({"dwu": FAKE}, {}, dar.DAR_E_ARG),            # tied must not pass dw_up
+    ({"wu": FAKE, "dwu": MISALIGNED}, {}, dar.DAR_E_ARG),
+    ({"ws": None, "ws_bytes": 0}, {}, dar.DAR_E_WORKSPACE),
+    ({"ws_bytes": 16}, {}, dar.DAR_E_WORKSPACE),
+    ({}, {"d": 512, "dd": 16}, dar.DAR_E_UNSUPPORTED),
+])
+def test_backward_rejects(kw, shape_kw, expect):
+    assert call_backward(S(**shape_kw), **kw) == expect
+

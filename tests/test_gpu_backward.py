@@ -1,0 +1,140 @@
+"""GPU prefill backward parity: dar_attn_prefill_backward (through the C ABI)
+against the fp64 oracle's backward on the same seeded inputs.
+
+The GPU backward is fed the GPU forward's own output o (as a training step
+would); the oracle needs no o. Tolerances extend the forward's unit-scale
+bounds (1e-4 fp32, 2e-2 bf16) to gradients that are not unit-scale:
+  dq, dk, dv: |got - ref| <= tol * max(1, |ref|) element by element;
+  dW_down, dW_up (fp32 sums over every row of the batch):
+              |got - ref| <= tol * max(1, max |ref|) over the tensor.
+"""
+import numpy as np
+import pytest
+import torch
+
+import dar_inputs as di
+from oracle import oracle
+from tests.dev import to_dev, to_host64, tol
+
+pytestmark = pytest.mark.gpu
+
+dar = pytest.importorskip("paper_2606_18587_amd")
+
+
+def run_gpu(inp, w):
+    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
+    wd, wu = to_dev(inp["wd"]), to_dev(inp["wu"])
+    dout = to_dev(inp["dout"])
+    o = dar.dar_attn_prefill(q, k, v, wd, wu, w)
+    grads = dar.dar_attn_prefill_backward(q, k, v, wd, wu, w, o, dout)
+    torch.cuda.synchronize()
+    return [None if g is None else to_host64(g) for g in grads]
+
+
+def compare(got, ref, dtype, what="", scale=1.0):
+    t = tol(dtype) * scale
+    names = ("dq", "dk", "dv", "dwd", "dwu")
+    worst = {}
+    for n, a, b in zip(names, got, ref):
+        if b is None:
+            assert a is None, n
+            continue
+        assert a.shape == b.shape, (n, a.shape, b.shape)
+        assert np.isfinite(a).all(), what + " " + n + " not finite"
+        err = np.abs(a - b)
+        if n in ("dwd", "dwu"):
+            bound = t * max(1.0, np.abs(b).max())
+            ratio = err.max() / bound
+        else:
+            ratio_all = err / (t * np.maximum(1.0, np.abs(b)))
+            ratio = ratio_all.max()
+        worst[n] = ratio
+        assert ratio <= 1.0, "%s %s: error %.3g of the bound (max abs err %.3g)" % (
+            what, n, ratio, err.max())
+    return worst
+
+
+def full_compare(wl, untied=False, seed_shift=0, q_scale=1.0, tol_scale=1.0):
+    inp = di.make_backward_inputs(wl, untied=untied, seed_shift=seed_shift, q_scale=q_scale)
+    got = run_gpu(inp, wl.w)
+    ref = oracle.backward(inp["q"].f64, inp["k"].f64, inp["v"].f64, inp["wd"].f64,
+                          None if inp["wu"] is None else inp["wu"].f64, wl.w, inp["dout"].f64)
+    worst = compare(got, ref, wl.dtype, "%s w=%d T=%d" % (wl.name, wl.w, wl.T), tol_scale)
+    print(wl.name, wl.w, wl.T, " ".join("%s=%.3f" % kv for kv in worst.items()))
+    return worst
+
+
+@pytest.mark.parametrize("untied", [False, True])
+def test_tiny_fp32_workload(untied):
+    full_compare(di.WORKLOADS["tiny"], untied=untied)
+
+
+@pytest.mark.parametrize("w", [0, 1, 8, 63, 64, 65, 99, 100, 200])
+def test_fp32_window_sweep(w):
+    full_compare(di.WORKLOADS["tiny"].with_(w=w, T=100, B=2, Hq=4, Hkv=2), untied=(w % 2 == 1))
+
+
+BF16_SMALL = di.Workload("bf16_small", 10, 1, 4, 2, 300, 64, 16, 128, "bf16")
+
+
+@pytest.mark.parametrize("w", [0, 1, 16, 64, 128, 129, 299, 300, 1000])
+@pytest.mark.parametrize("untied", [False, True])
+def test_bf16_d64_window_sweep(w, untied):
+    full_compare(BF16_SMALL.with_(w=w), untied=untied)
+
+
+@pytest.mark.parametrize("T", [1, 2, 61, 127, 128, 129, 257, 500])
+def test_bf16_d64_ragged_lengths(T):
+    full_compare(BF16_SMALL.with_(T=T, w=32, B=2))
+
+
+@pytest.mark.parametrize("w", [0, 64, 100, 512])
+def test_bf16_d128_gqa(w):
+    full_compare(di.Workload("bf16_d128", 11, 1, 8, 2, 400, 128, 32, w, "bf16"), untied=(w == 100))
+
+
+@pytest.mark.parametrize("d,dd,w,T", [(64, 32, 40, 333), (128, 16, 77, 290), (64, 16, 33, 97)])
+@pytest.mark.parametrize("untied", [False, True])
+def test_bf16_other_matrix_core_shapes(d, dd, w, T, untied):
+    full_compare(di.Workload("bf16_mixed", 13, 2, 4, 1, T, d, dd, w, "bf16"), untied=untied)
+
+
+@pytest.mark.parametrize("shape", [(1, 3, 1, 90, 48, 12, 10), (2, 2, 2, 70, 32, 32, 5),
+                                   (1, 2, 1, 50, 256, 64, 7)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_generic_shapes(shape, dtype):
+    B, Hq, Hkv, T, d, dd, w = shape
+    full_compare(di.Workload("generic", 14, B, Hq, Hkv, T, d, dd, w, dtype), untied=True)
+
+
+def test_bf16_peaky_queries():
+    # queries scaled by 4: sharp rows. dk = s sum dS q grows with |q| while the
+    # error of delta = dO . o (o stored in bf16) does not shrink, so the bound
+    # scales with the query scale.
+    full_compare(BF16_SMALL.with_(w=64, T=400), q_scale=4.0, tol_scale=4.0)
+
+
+def test_full_size_pythia70m_one_head():
+    """B8 H8 T2048 d64 d_down16 w256 on the GPU; the oracle recomputes the
+    gradients of one KV head over the whole batch (dq/dk/dv of its rows and
+    the head's full dW_down)."""
+    wl = di.WORKLOADS["pythia70m"]
+    inp = di.make_backward_inputs(wl)
+    got = run_gpu(inp, wl.w)
+    g = wl.Hkv - 1
+    G = wl.Hq // wl.Hkv
+    hs = slice(g * G, (g + 1) * G)
+    ref = oracle.backward(inp["q"].f64[:, hs], inp["k"].f64[:, g:g + 1], inp["v"].f64[:, g:g + 1],
+                          inp["wd"].f64[g:g + 1], None, wl.w, inp["dout"].f64[:, hs])
+    sub = [got[0][:, hs], got[1][:, g:g + 1], got[2][:, g:g + 1], got[3][g:g + 1], None]
+    worst = compare(sub, ref, wl.dtype, "pythia70m head %d" % g)
+    print("pythia70m head", g, " ".join("%s=%.3f" % kv for kv in worst.items()))
+
+
+def test_deterministic():
+    wl = BF16_SMALL.with_(w=64, T=333, B=2)
+    inp = di.make_backward_inputs(wl, untied=True)
+    a = run_gpu(inp, wl.w)
+    b = run_gpu(inp, wl.w)
+    for x, y in zip(a, b):
+        assert np.array_equal(x, y)
