@@ -39,8 +39,11 @@ constexpr float kLog2e = 1.4426950408889634f;
 BwdWs bwd_ws_layout(int B, int Hq, int Hkv, int T, int d, int dd) {
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     BwdWs L{};
-    const size_t rows = (size_t)B * Hq * T;
-    const size_t toks = (size_t)B * Hkv * T;
+    // token counts padded to a multiple of 32 (the matrix-core path reads whole
+    // 32-token blocks and keeps two bf16 arrays where this path keeps one fp32)
+    const size_t Tr = (size_t)round_up(T, 32);
+    const size_t rows = (size_t)B * Hq * Tr;
+    const size_t toks = (size_t)B * Hkv * Tr;
     size_t off = 0;
     L.lse_off = off;   off += al(rows * 4);
     L.delta_off = off; off += al(rows * 4);

@@ -48,6 +48,14 @@ bool log_enabled() {
     return on == 1;
 }
 
+// An environment switch ("1" = on), read at each call. DAR_BWD_VALU=1 sends
+// the backward to the vector-ALU kernels for every shape (used to test them
+// on shapes the matrix-core kernels also cover).
+bool env_flag(const char* name) {
+    const char* e = getenv(name);
+    return e && e[0] == '1';
+}
+
 size_t esize_of(dar_dtype t) { return t == DAR_BF16 ? 2 : 4; }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
@@ -181,10 +189,19 @@ dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, c
 
     clear_hip_error();
     if (log_enabled())
-        fprintf(stderr, "[dar] prefill_backward B=%d Hq=%d Hkv=%d T=%d d=%d dd=%d w=%d %s\n", s->B,
-                s->Hq, s->Hkv, T, s->d, s->d_down, s->w, s->dtype == DAR_BF16 ? "bf16" : "f32");
+        fprintf(stderr, "[dar] prefill_backward B=%d Hq=%d Hkv=%d T=%d d=%d dd=%d w=%d %s path=%s\n",
+                s->B, s->Hq, s->Hkv, T, s->d, s->d_down, s->w, s->dtype == DAR_BF16 ? "bf16" : "f32",
+                bwd_mfma_supported(s->d, s->d_down, s->dtype == DAR_BF16) && !env_flag("DAR_BWD_VALU")
+                    ? "mfma" : "valu");
     hipError_t e;
-    if (s->dtype == DAR_BF16)
+    const bool fast = bwd_mfma_supported(s->d, s->d_down, s->dtype == DAR_BF16) &&
+                      !env_flag("DAR_BWD_VALU");
+    if (fast)
+        e = launch_bwd_mfma((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)o,
+                            (const bf16_t*)dout, (const bf16_t*)w_down, (const bf16_t*)w_up,
+                            (bf16_t*)dq, (bf16_t*)dk, (bf16_t*)dv, dw_down, dw_up, (char*)ws, L,
+                            s->B, s->Hq, s->Hkv, T, s->d, s->d_down, s->w, stream);
+    else if (s->dtype == DAR_BF16)
         e = launch_bwd_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v,
                                     (const bf16_t*)o, (const bf16_t*)dout, (const bf16_t*)w_down,
                                     (const bf16_t*)w_up, (bf16_t*)dq, (bf16_t*)dk, (bf16_t*)dv,

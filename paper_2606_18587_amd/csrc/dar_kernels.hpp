@@ -76,11 +76,16 @@ hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, c
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
                          int d, int dd, int w, int cap, int len, hipStream_t st);
 
-// Prefill backward workspace (all fp32, 256-byte aligned parts):
-//   lse, delta        [B*Hq][T]        log2-domain log-sum-exp of each row; dO . O
-//   qt, dot, hk, ol   [B*Hq][T][dd]    q W_up^T, dO W_up^T, sum dS c^K, sum P c^V
-//   ck, cv, gk, gv    [B*Hkv][T][dd]   latents; sum dS q~, sum P dO~ per key
+// Prefill backward workspace (256-byte aligned parts; Tr = round_up(T, 32)):
+//   lse, delta        [B*Hq][Tr] fp32     log2-domain log-sum-exp of each row; dO . O
+//   qt, dot           [B*Hq][Tr][dd] fp32 q W_up^T, dO W_up^T (matrix-core path: the
+//                                         bf16 row-major array, then the bf16
+//                                         transposed 32-row blocks)
+//   hk, ol            [B*Hq][T][dd] fp32  sum dS c^K, sum P c^V per row
+//   ck, cv            [B*Hkv][Tr][dd] fp32 latents (matrix-core path: as qt)
+//   gk, gv            [B*Hkv][T][dd] fp32 sum dS q~, sum P dO~ per key
 //   wpart             [2][Hkv][nchunk][d][dd]  weight-gradient partials per chunk
+// (each array region is sized for Tr tokens).
 struct BwdWs {
     size_t lse_off, delta_off, qt_off, dot_off, hk_off, ol_off, ck_off, cv_off, gk_off, gv_off,
         wpart_off, bytes;
@@ -103,6 +108,13 @@ hipError_t launch_bwd_weights(const T* q, const T* k, const T* v, const T* dout,
                               const float* gv, const float* hk, const float* ol, float* part,
                               float* dwd, float* dwu, int B, int Hq, int Hkv, int T_, int d,
                               int dd, const BwdWs& L, hipStream_t st);
+// Matrix-core backward (bf16, d in {64, 128}, d_down in {16, 32}).
+bool bwd_mfma_supported(int d, int dd, bool bf16);
+hipError_t launch_bwd_mfma(const bf16_t* q, const bf16_t* k, const bf16_t* v, const bf16_t* o,
+                           const bf16_t* dout, const bf16_t* wd, const bf16_t* wu, bf16_t* dq,
+                           bf16_t* dk, bf16_t* dv, float* dwd, float* dwu, char* ws,
+                           const BwdWs& L, int B, int Hq, int Hkv, int T, int d, int dd, int w,
+                           hipStream_t st);
 template <typename T>
 hipError_t launch_bwd_valu(const T* q, const T* k, const T* v, const T* o, const T* dout,
                            const T* wd, const T* wu, T* dq, T* dk, T* dv, float* dwd, float* dwu,

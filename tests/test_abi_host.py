@@ -161,12 +161,14 @@ def test_python_binding_names_match_abi():
 
 
 def expected_backward_ws(B, Hq, Hkv, T, d, dd):
-    """fp32: log-sum-exp and delta per row, four d_down-wide row arrays (q W_up^T,
+    """fp32 (rows padded to a multiple of 32): log-sum-exp and delta per row,
+    four d_down-wide row arrays (q W_up^T,
     dO W_up^T and the two distant sums), four d_down-wide key arrays (latents
     and the two distant sums), weight partials over min(128, ceil(rows/256))
     chunks; every part 256-byte aligned."""
     al = lambda x: (x + 255) // 256 * 256
-    rows, toks = B * Hq * T, B * Hkv * T
+    Tr = (T + 31) // 32 * 32          # token counts padded to whole 32-token blocks
+    rows, toks = B * Hq * Tr, B * Hkv * Tr
     nch = lambda r: min(128, max(1, (r + 255) // 256))
     nchunk = max(nch(B * T), nch(B * (Hq // Hkv) * T))
     return (2 * al(rows * 4) + 4 * al(rows * dd * 4) + 4 * al(toks * dd * 4)
