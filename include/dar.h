@@ -84,6 +84,9 @@ typedef struct {
 /* Causal prefill over positions 0..T-1 (Eq. 3-4 for every row).
  *   q [B][Hq][T][d], k, v [B][Hkv][T][d], w_down [Hkv][d][d_down],
  *   w_up [Hkv][d_down][d] or NULL (tied), o [B][Hq][T][d] (output).
+ *   lse: NULL, or fp32 [B][Hq][T] (output): the natural log of each row's
+ *   softmax denominator, log sum_j exp(S_ij) with S_ij the scaled score of
+ *   Eq. 4; dar_attn_prefill_backward takes it.
  *   ws: device workspace of at least dar_prefill_workspace_bytes(s, T) bytes
  *   (never NULL; caller-owned, overwritten by the call): latents of the
  *   tokens that are distant for some row (Eq. 1), per-32-token norm maxima
@@ -92,7 +95,7 @@ typedef struct {
  * d_down in {16, 32} take the matrix-core path). */
 dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void* k,
                             const void* v, const void* w_down, const void* w_up, void* o,
-                            void* ws, size_t ws_bytes, hipStream_t stream);
+                            float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Append n >= 1 tokens k_new, v_new [B][Hkv][n][d] at positions len..len+n-1.
  * Every token that leaves the window (position len+t-w for t < n) is
@@ -118,23 +121,23 @@ dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q
  * through the pairs whose query takes the distant path).
  *   q, k, v, w_down, w_up: the forward's inputs (w_up NULL = tied);
  *   o [B][Hq][T][d]: the forward's output (used for delta_i = dout_i . o_i);
+ *   lse fp32 [B][Hq][T]: the log-sum-exp the forward call wrote (its lse
+ *   argument); the softmax is recomputed against it, not re-normalised;
  *   dout [B][Hq][T][d]: the incoming gradient;
  *   dq [B][Hq][T][d], dk, dv [B][Hkv][T][d]: outputs in the shape's dtype;
  *   dw_down [Hkv][d][d_down], dw_up [Hkv][d_down][d]: fp32 outputs whatever
  *   the shape's dtype (sums over every row of the batch). Tied (w_up NULL):
  *   dw_up must be NULL and dw_down receives the gradient of the shared matrix,
  *   dW_down + dW_up^T. Untied: dw_up must be non-NULL.
- *   Every output is overwritten (not accumulated into); the row softmax
- *   statistics are recomputed, nothing from the forward call besides o is
- *   needed.
+ *   Every output is overwritten (not accumulated into).
  *   ws: device workspace of at least dar_prefill_backward_workspace_bytes(s, T)
  *   bytes (caller-owned, overwritten). The result does not depend on the
  *   stream or on timing: every reduction runs in a fixed order.
  * Supported: as dar_attn_prefill. */
 dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, const void* k,
                                      const void* v, const void* w_down, const void* w_up,
-                                     const void* o, const void* dout, void* dq, void* dk,
-                                     void* dv, float* dw_down, float* dw_up, void* ws,
+                                     const void* o, const float* lse, const void* dout, void* dq,
+                                     void* dk, void* dv, float* dw_down, float* dw_up, void* ws,
                                      size_t ws_bytes, hipStream_t stream);
 
 /* Workspace sizes (0 on an invalid shape). */

@@ -71,9 +71,11 @@ static double* lift_all(int n, int d, int dd, const double* x, const double* wd,
 
 /* One query row of Eq. 3-4 against tokens [0, i] of one head.
  * k, v, kl, vl are [>= i+1][d]: original and lifted keys and values.
- * p (optional) receives the softmax weights for j in [0, i]. */
+ * p (optional) receives the softmax weights for j in [0, i]; lse (optional)
+ * the log of the softmax denominator, log sum_j exp(S_ij). */
 static void one_row(int d, int w, int i, const double* qi, const double* k, const double* v,
-                    const double* kl, const double* vl, double* s, double* oi, double* p)
+                    const double* kl, const double* vl, double* s, double* oi, double* p,
+                    double* lse)
 {
     const double scale = 1.0 / sqrt((double)d);
     double m = -INFINITY;
@@ -86,6 +88,7 @@ static void one_row(int d, int w, int i, const double* qi, const double* k, cons
     }
     double sum = 0.0;
     for (int j = 0; j <= i; ++j) { s[j] = exp(s[j] - m); sum += s[j]; }
+    if (lse) *lse = m + log(sum);
     for (int e = 0; e < d; ++e) oi[e] = 0.0;
     for (int j = 0; j <= i; ++j) {
         const double pj = s[j] / sum;
@@ -103,11 +106,12 @@ static void one_row(int d, int w, int i, const double* qi, const double* k, cons
  *   qr    [n_rows][d]
  *   o     [n_rows][d]  output
  *   p     optional [n_rows][T]: softmax weights, zero for j > pos
+ *   lse   optional [n_rows]: log sum_j exp(S_ij) of each row (natural log)
  * Returns 0, or -1 on a bad argument / allocation failure.
  */
 int dar_oracle_rows(int T, int d, int dd, int w, const double* k, const double* v,
                     const double* wd, const double* wu, int n_rows, const int* pos,
-                    const double* qr, double* o, double* p)
+                    const double* qr, double* o, double* p, double* lse)
 {
     if (T < 1 || d < 1 || dd < 1 || w < 0 || n_rows < 0) return -1;
     for (int r = 0; r < n_rows; ++r)
@@ -127,7 +131,8 @@ int dar_oracle_rows(int T, int d, int dd, int w, const double* k, const double* 
             for (int r = 0; r < n_rows; ++r) {
                 double* pr = p ? p + (size_t)r * T : NULL;
                 if (pr) for (int j = 0; j < T; ++j) pr[j] = 0.0;
-                one_row(d, w, pos[r], qr + (size_t)r * d, k, v, kl, vl, s, o + (size_t)r * d, pr);
+                one_row(d, w, pos[r], qr + (size_t)r * d, k, v, kl, vl, s, o + (size_t)r * d, pr,
+                        lse ? lse + r : NULL);
             }
             free(s);
         }
@@ -140,12 +145,12 @@ int dar_oracle_rows(int T, int d, int dd, int w, const double* k, const double* 
 /*
  * Full causal prefill of a batch: every row i of every query head.
  *   q [B][Hq][T][d], k, v [B][Hkv][T][d], wd [Hkv][d][dd], wu [Hkv][dd][d] or NULL
- *   o [B][Hq][T][d]
+ *   o [B][Hq][T][d]; lse optional [B][Hq][T]: log sum_j exp(S_ij) of each row
  * nthreads > 0 sets the OpenMP thread count (0 keeps the default).
  */
 int dar_oracle_prefill(int B, int Hq, int Hkv, int T, int d, int dd, int w, const double* q,
                        const double* k, const double* v, const double* wd, const double* wu,
-                       double* o, int nthreads)
+                       double* o, double* lse, int nthreads)
 {
     if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || T < 1 || d < 1 || dd < 1 || w < 0)
         return -1;
@@ -166,7 +171,7 @@ int dar_oracle_prefill(int B, int Hq, int Hkv, int T, int d, int dd, int w, cons
             const size_t q_off = ((size_t)b * Hq + h) * (size_t)T * d;
             rc = dar_oracle_rows(T, d, dd, w, k + kv_off, v + kv_off, wd + (size_t)g * d * dd,
                                  wu ? wu + (size_t)g * dd * d : NULL, T, pos, q + q_off,
-                                 o + q_off, NULL);
+                                 o + q_off, NULL, lse ? lse + ((size_t)b * Hq + h) * T : NULL);
         }
     free(pos);
     return rc;
@@ -255,7 +260,7 @@ int dar_oracle_backward(int B, int Hq, int Hkv, int T, int d, int dd, int w, con
                 for (int i = 0; i < T; ++i) {
                     const double* qi = qh + (size_t)i * d;
                     const double* doi = doh + (size_t)i * d;
-                    one_row(d, w, i, qi, kb, vb, kl, vl, s, oi, p);
+                    one_row(d, w, i, qi, kb, vb, kl, vl, s, oi, p, NULL);
                     double delta = 0.0;
                     for (int j = 0; j <= i; ++j) {
                         const double* val = (i - j < w) ? vb + (size_t)j * d : vl + (size_t)j * d;

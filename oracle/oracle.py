@@ -7,7 +7,8 @@ Functions follow the paper's method section:
   down()      Eq. 1, c = x W_down
   lift()      Eq. 1 then Eq. 2, x' = (x W_down) W_up
   rows()      Eq. 3-4 for chosen query rows of one head
-  prefill()   Eq. 3-4 for every row of a batch (causal prefill)
+  prefill()   Eq. 3-4 for every row of a batch (causal prefill); optionally
+              the log of each row's softmax denominator
   backward()  gradients of sum(dO * O) of the prefill (Section 2.3, the
               training setting) with respect to Q, K, V, W_down, W_up
   cache_model()  where the split cache keeps each token after n appends
@@ -62,9 +63,9 @@ class Oracle:
         lib = ctypes.CDLL(path)
         lib.dar_oracle_rows.restype = ctypes.c_int
         lib.dar_oracle_rows.argtypes = [ctypes.c_int] * 4 + [_dp, _dp, _dp, _dp, ctypes.c_int,
-                                                             _ip, _dp, _dp, _dp]
+                                                             _ip, _dp, _dp, _dp, _dp]
         lib.dar_oracle_prefill.restype = ctypes.c_int
-        lib.dar_oracle_prefill.argtypes = [ctypes.c_int] * 7 + [_dp] * 6 + [ctypes.c_int]
+        lib.dar_oracle_prefill.argtypes = [ctypes.c_int] * 7 + [_dp] * 7 + [ctypes.c_int]
         lib.dar_oracle_down.restype = None
         lib.dar_oracle_down.argtypes = [ctypes.c_int] * 3 + [_dp, _dp, _dp]
         lib.dar_oracle_up.restype = None
@@ -114,13 +115,16 @@ class Oracle:
         o = np.empty((n, d), np.float64)
         p = np.empty((n, T), np.float64) if want_p else None
         rc = self.lib.dar_oracle_rows(T, d, dd, int(w), _ptr(k), _ptr(v), _ptr(wd), _ptr(wu_c),
-                                      n, pos.ctypes.data_as(_ip), _ptr(qr), _ptr(o), _ptr(p))
+                                      n, pos.ctypes.data_as(_ip), _ptr(qr), _ptr(o), _ptr(p),
+                                      None)
         if rc != 0:
             raise ValueError("dar_oracle_rows rejected its arguments")
         return (o, p) if want_p else o
 
-    def prefill(self, q, k, v, wd, wu, w, threads=0):
-        """Causal prefill: q [B,Hq,T,d], k/v [B,Hkv,T,d], wd [Hkv,d,dd], wu [Hkv,dd,d]|None."""
+    def prefill(self, q, k, v, wd, wu, w, threads=0, want_lse=False):
+        """Causal prefill: q [B,Hq,T,d], k/v [B,Hkv,T,d], wd [Hkv,d,dd], wu [Hkv,dd,d]|None.
+        With want_lse also returns lse [B,Hq,T] = log sum_j exp(S_ij), the log of
+        each row's softmax denominator (Eq. 4)."""
         q = _c64(q)
         k = _c64(k)
         v = _c64(v)
@@ -130,11 +134,13 @@ class Oracle:
         Hkv = k.shape[1]
         dd = wd.shape[2]
         o = np.empty_like(q)
+        lse = np.empty((B, Hq, T), np.float64) if want_lse else None
         rc = self.lib.dar_oracle_prefill(B, Hq, Hkv, T, d, dd, int(w), _ptr(q), _ptr(k),
-                                         _ptr(v), _ptr(wd), _ptr(wu_c), _ptr(o), int(threads))
+                                         _ptr(v), _ptr(wd), _ptr(wu_c), _ptr(o), _ptr(lse),
+                                         int(threads))
         if rc != 0:
             raise ValueError("dar_oracle_prefill rejected its arguments")
-        return o
+        return (o, lse) if want_lse else o
 
 
     def backward(self, q, k, v, wd, wu, w, dout, threads=0):
@@ -189,8 +195,8 @@ def rows(k, v, wd, wu, w, pos, qr, want_p=False):
     return default().rows(k, v, wd, wu, w, pos, qr, want_p)
 
 
-def prefill(q, k, v, wd, wu, w, threads=0):
-    return default().prefill(q, k, v, wd, wu, w, threads)
+def prefill(q, k, v, wd, wu, w, threads=0, want_lse=False):
+    return default().prefill(q, k, v, wd, wu, w, threads, want_lse)
 
 
 def backward(q, k, v, wd, wu, w, dout, threads=0):

@@ -46,7 +46,7 @@ def _load():
     shp = ctypes.POINTER(DarShape)
     cp = ctypes.POINTER(DarCacheStruct)
     lib.dar_attn_prefill.restype = ci
-    lib.dar_attn_prefill.argtypes = [shp, ci, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.dar_attn_prefill.argtypes = [shp, ci, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.dar_cache_append.restype = ci
     lib.dar_cache_append.argtypes = [shp, cp, vp, vp, ci, vp, vp]
     lib.dar_attn_decode.restype = ci
@@ -56,7 +56,7 @@ def _load():
     lib.dar_decode_workspace_bytes.restype = sz
     lib.dar_decode_workspace_bytes.argtypes = [shp, ci]
     lib.dar_attn_prefill_backward.restype = ci
-    lib.dar_attn_prefill_backward.argtypes = [shp, ci] + [vp] * 13 + [sz, vp]
+    lib.dar_attn_prefill_backward.argtypes = [shp, ci] + [vp] * 14 + [sz, vp]
     lib.dar_prefill_backward_workspace_bytes.restype = sz
     lib.dar_prefill_backward_workspace_bytes.argtypes = [shp, ci]
     lib.dar_status_string.restype = ctypes.c_char_p
@@ -124,9 +124,12 @@ def _workspace(nbytes, device):
     return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
-def dar_attn_prefill(q, k, v, w_down, w_up, w, o=None, ws=None, stream=None, check=True):
+def dar_attn_prefill(q, k, v, w_down, w_up, w, o=None, ws=None, stream=None, check=True,
+                     lse=None, return_lse=False):
     """Causal DAR prefill. q [B,Hq,T,d]; k, v [B,Hkv,T,d]; w_down [Hkv,d,dd];
-    w_up [Hkv,dd,d] or None (tied). Returns o [B,Hq,T,d]."""
+    w_up [Hkv,dd,d] or None (tied). Returns o [B,Hq,T,d], or (o, lse) with
+    return_lse (lse [B,Hq,T] fp32, the log of each row's softmax denominator,
+    written into `lse` when given)."""
     B, Hq, T, d = q.shape
     Hkv = k.shape[1]
     dd = w_down.shape[2]
@@ -141,21 +144,26 @@ def dar_attn_prefill(q, k, v, w_down, w_up, w, o=None, ws=None, stream=None, che
             raise ValueError("w_up: expected %s" % ((Hkv, dd, d),))
     if o is None:
         o = torch.empty_like(q)
+    if return_lse and lse is None:
+        lse = torch.empty(B, Hq, T, dtype=torch.float32, device=q.device)
+    if lse is not None and (tuple(lse.shape) != (B, Hq, T) or lse.dtype != torch.float32):
+        raise ValueError("lse: expected %s float32" % ((B, Hq, T),))
     need = dar_prefill_workspace_bytes(shape, T)
     if ws is None:
         ws = _workspace(need, q.device)
     st = lib.dar_attn_prefill(ctypes.byref(shape), int(T), _ptr(q), _ptr(k), _ptr(v),
-                              _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(ws),
+                              _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(lse), _ptr(ws),
                               0 if ws is None else ws.numel() * ws.element_size(),
                               _stream(stream))
     if st != DAR_OK:
         raise DarError(st, "dar_attn_prefill")
-    return o
+    return (o, lse) if return_lse else o
 
 
-def dar_attn_prefill_backward(q, k, v, w_down, w_up, w, o, dout, ws=None, stream=None,
+def dar_attn_prefill_backward(q, k, v, w_down, w_up, w, o, lse, dout, ws=None, stream=None,
                               check=True):
-    """Gradients of sum(dout * o) of the causal DAR prefill. Returns
+    """Gradients of sum(dout * o) of the causal DAR prefill, given the forward's
+    o and lse (dar_attn_prefill(..., return_lse=True)). Returns
     (dq, dk, dv, dw_down, dw_up): dq/dk/dv in the input dtype, the weight
     gradients fp32; dw_up is None when tied (w_up None), dw_down then holds the
     gradient of the shared matrix."""
@@ -172,6 +180,8 @@ def dar_attn_prefill_backward(q, k, v, w_down, w_up, w, o, dout, ws=None, stream
                                                                    tuple(t.shape), t.dtype))
         if w_up is not None and (tuple(w_up.shape) != (Hkv, dd, d) or w_up.dtype != q.dtype):
             raise ValueError("w_up: expected %s" % ((Hkv, dd, d),))
+        if tuple(lse.shape) != (B, Hq, T) or lse.dtype != torch.float32:
+            raise ValueError("lse: expected %s float32" % ((B, Hq, T),))
     dq = torch.empty_like(q)
     dk = torch.empty_like(k)
     dv = torch.empty_like(v)
@@ -180,7 +190,8 @@ def dar_attn_prefill_backward(q, k, v, w_down, w_up, w, o, dout, ws=None, stream
     if ws is None:
         ws = _workspace(dar_prefill_backward_workspace_bytes(shape, T), q.device)
     st = lib.dar_attn_prefill_backward(ctypes.byref(shape), int(T), _ptr(q), _ptr(k), _ptr(v),
-                                       _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(dout), _ptr(dq),
+                                       _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(lse), _ptr(dout),
+                                       _ptr(dq),
                                        _ptr(dk), _ptr(dv), _ptr(dwd), _ptr(dwu), _ptr(ws),
                                        0 if ws is None else ws.numel() * ws.element_size(),
                                        _stream(stream))

@@ -20,10 +20,13 @@
 // pairs whose query takes the distant path reach the bottleneck weights,
 // which is how the paper describes their training.
 //
+// The softmax statistics are not recomputed: each row's log-sum-exp comes
+// from the forward call.
+//
 // Kernels, in launch order:
 //   bwd_latent_kernel   c^K, c^V for every token (fp32)
 //   bwd_rowprep_kernel  q~, dO~ and delta for every query row
-//   bwd_rows_valu_kernel   one wave per query row: log-sum-exp, dq, h, ol
+//   bwd_rows_valu_kernel   one wave per query row: dq, h, ol
 //   bwd_cols_valu_kernel   one wave per key: dk, dv, gK, gV
 //   bwd_wpart_kernel / bwd_wreduce_kernel  weight gradients, split over row
 //                          chunks then summed in a fixed order (deterministic)
@@ -36,7 +39,7 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 }
 
-BwdWs bwd_ws_layout(int B, int Hq, int Hkv, int T, int d, int dd) {
+BwdWs bwd_ws_layout(int B, int Hq, int Hkv, int T, int d, int dd, bool mfma) {
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     BwdWs L{};
     // token counts padded to a multiple of 32 (the matrix-core path reads whole
@@ -44,20 +47,30 @@ BwdWs bwd_ws_layout(int B, int Hq, int Hkv, int T, int d, int dd) {
     const size_t Tr = (size_t)round_up(T, 32);
     const size_t rows = (size_t)B * Hq * Tr;
     const size_t toks = (size_t)B * Hkv * Tr;
+    // operand arrays: fp32 [n][dd] here; on the matrix-core path bf16 [n][dd]
+    // followed by the transposed 32-token blocks padded to 32 latent rows
+    const size_t opw = mfma ? (size_t)(dd + 32) * 2 : (size_t)dd * 4;
     size_t off = 0;
     L.lse_off = off;   off += al(rows * 4);
     L.delta_off = off; off += al(rows * 4);
-    L.qt_off = off;    off += al(rows * dd * 4);
-    L.dot_off = off;   off += al(rows * dd * 4);
+    L.qt_off = off;    off += al(rows * opw);
+    L.dot_off = off;   off += al(rows * opw);
+    L.rc_off = off;    off += mfma ? al(rows * 16 * 2) : 0;
     L.hk_off = off;    off += al(rows * dd * 4);
     L.ol_off = off;    off += al(rows * dd * 4);
-    L.ck_off = off;    off += al(toks * dd * 4);
-    L.cv_off = off;    off += al(toks * dd * 4);
+    L.ck_off = off;    off += al(toks * opw);
+    L.cv_off = off;    off += al(toks * opw);
     L.gk_off = off;    off += al(toks * dd * 4);
     L.gv_off = off;    off += al(toks * dd * 4);
     const int G = Hq / Hkv;
-    L.nchunk_d = bwd_nchunk((long long)B * T);
-    L.nchunk_u = bwd_nchunk((long long)B * G * T);
+    if (mfma) {  // one share per workgroup of 128 keys / 128 query rows
+        const int nblk = (T + 127) / 128;
+        L.nchunk_d = B * nblk;
+        L.nchunk_u = B * G * nblk;
+    } else {
+        L.nchunk_d = bwd_nchunk((long long)B * T);
+        L.nchunk_u = bwd_nchunk((long long)B * G * T);
+    }
     L.nchunk = L.nchunk_d > L.nchunk_u ? L.nchunk_d : L.nchunk_u;
     L.wpart_off = off; off += al((size_t)2 * Hkv * L.nchunk * d * dd * 4);
     L.bytes = off;
@@ -75,9 +88,9 @@ __global__ __launch_bounds__(256) void bwd_latent_kernel(const T* __restrict__ k
                                                          float* __restrict__ ck,
                                                          float* __restrict__ cv, int Hkv, int T_,
                                                          int d, int dd) {
-    const int bg = blockIdx.y;
+    const int bg = wg_id_y();
     const int g = bg % Hkv;
-    const long long idx = (long long)blockIdx.x * 256 + threadIdx.x;
+    const long long idx = (long long)wg_id_x() * 256 + lane_id_x();
     if (idx >= (long long)T_ * dd) return;
     const int j = (int)(idx / dd), c = (int)(idx % dd);
     const size_t row = (size_t)bg * T_ + j;
@@ -93,9 +106,9 @@ __global__ __launch_bounds__(64) void bwd_rowprep_kernel(
     const T* __restrict__ q, const T* __restrict__ o, const T* __restrict__ dout,
     const T* __restrict__ wd, const T* __restrict__ wu, float* __restrict__ qt,
     float* __restrict__ dot, float* __restrict__ delta, int Hq, int Hkv, int T_, int d, int dd) {
-    const int lane = threadIdx.x;
-    const int i = blockIdx.x;
-    const int bh = blockIdx.y;
+    const int lane = lane_id_x();
+    const int i = wg_id_x();
+    const int bh = wg_id_y();
     const int g = (bh % Hq) / (Hq / Hkv);
     const size_t row = (size_t)bh * T_ + i;
     const T* qr = q + row * d;
@@ -123,17 +136,17 @@ __global__ __launch_bounds__(64) void bwd_rowprep_kernel(
 
 // ---------------------------------------------------------------- rows (dq)
 
-// One wave per query row i of one (batch, query head). Pass 1 finds the
-// log-sum-exp of the row over both regions (one softmax, Eq. 4); pass 2
-// recomputes P, forms dP and dS and accumulates dq (window keys, d wide),
-// h = sum dS c^K and ol = sum P c^V (distant keys, d_down wide). Scores are
-// kept in the log2 domain (log2(e) / sqrt(d) folded into the query).
+// One wave per query row i of one (batch, query head): recomputes P of the
+// single softmax (Eq. 4) from the forward's log-sum-exp, forms dP and dS and
+// accumulates dq (window keys, d wide), h = sum dS c^K and ol = sum P c^V
+// (distant keys, d_down wide). Scores are kept in the log2 domain
+// (log2(e) / sqrt(d) folded into the query).
 template <typename T>
 __global__ __launch_bounds__(64) void bwd_rows_valu_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ dout, const T* __restrict__ wd, const T* __restrict__ wu,
     const float* __restrict__ ck, const float* __restrict__ cv, const float* __restrict__ qt,
-    const float* __restrict__ dot, const float* __restrict__ delta, float* __restrict__ lse,
+    const float* __restrict__ dot, const float* __restrict__ delta, const float* __restrict__ lse,
     float* __restrict__ hk, float* __restrict__ ol, T* __restrict__ dq, int Hq, int Hkv, int T_,
     int d, int dd, int w, float scale) {
     __shared__ float qs[256];
@@ -143,9 +156,9 @@ __global__ __launch_bounds__(64) void bwd_rows_valu_kernel(
     __shared__ float hs[256];
     __shared__ float ps[64];
     __shared__ float dss[64];
-    const int lane = threadIdx.x;
-    const int i = (T_ - 1) - (int)blockIdx.x;  // longest rows first
-    const int bh = blockIdx.y;
+    const int lane = lane_id_x();
+    const int i = (T_ - 1) - wg_id_x();  // longest rows first
+    const int bh = wg_id_y();
     const int b = bh / Hq, h = bh % Hq;
     const int g = h / (Hq / Hkv);
     const int bg = b * Hkv + g;
@@ -178,20 +191,9 @@ __global__ __launch_bounds__(64) void bwd_rows_valu_kernel(
         return acc;
     };
 
-    // pass 1: row max and sum
-    float m = -INFINITY, l = 0.f;
-    for (int j0 = 0; j0 <= i; j0 += 64) {
-        const int j = j0 + lane;
-        const float s = (j <= i) ? score(j) : -INFINITY;
-        const float mn = fmaxf(m, wave_max(s));
-        const float p = (j <= i) ? exp2f(s - mn) : 0.f;
-        l = l * exp2f(m - mn) + wave_sum(p);
-        m = mn;
-    }
-    const float L2 = m + log2f(l);
-    if (lane == 0) lse[row] = L2;
+    const float L2 = lse[row] * kLog2e;  // the forward's log-sum-exp, log2 units
 
-    // pass 2: gradients
+    // gradients
     float dql[4] = {0.f, 0.f, 0.f, 0.f};
     float ha[4] = {0.f, 0.f, 0.f, 0.f};
     float oa[4] = {0.f, 0.f, 0.f, 0.f};
@@ -288,9 +290,9 @@ __global__ __launch_bounds__(64) void bwd_cols_valu_kernel(
     __shared__ float gvs[256];
     __shared__ float ps[64];
     __shared__ float dss[64];
-    const int lane = threadIdx.x;
-    const int j = blockIdx.x;
-    const int bg = blockIdx.y;
+    const int lane = lane_id_x();
+    const int j = wg_id_x();
+    const int bg = wg_id_y();
     const int b = bg / Hkv, g = bg % Hkv;
     const int G = Hq / Hkv;
     const size_t tok = (size_t)bg * T_ + j;
@@ -333,7 +335,7 @@ __global__ __launch_bounds__(64) void bwd_cols_valu_kernel(
                         dp = __builtin_fmaf(elem<T>::load(dh + (size_t)i * d + e), vs[e], dp);
                     }
                 }
-                p = exp2f(s - lh[i]);
+                p = exp2f(s - lh[i] * kLog2e);
                 ds = p * (dp - delh[i]);
             }
             ps[lane] = p;
@@ -410,7 +412,7 @@ __global__ __launch_bounds__(256) void bwd_wpart_kernel(
     const T* __restrict__ dout, const float* __restrict__ gk, const float* __restrict__ gv,
     const float* __restrict__ hk, const float* __restrict__ ol, float* __restrict__ part, int B,
     int Hq, int Hkv, int T_, int d, int dd, int nchunk_d, int nchunk_u, int nchunk, float scale) {
-    const int chunk = blockIdx.x, g = blockIdx.y, z = blockIdx.z;
+    const int chunk = wg_id_x(), g = wg_id_y(), z = wg_id_z();
     const int G = Hq / Hkv;
     const long long rows = z == 0 ? (long long)B * T_ : (long long)B * G * T_;
     const int nch = z == 0 ? nchunk_d : nchunk_u;
@@ -440,7 +442,7 @@ __global__ __launch_bounds__(256) void bwd_wpart_kernel(
             }
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
-                const int o = o0 + (int)threadIdx.x + 256 * u;
+                const int o = o0 + lane_id_x() + 256 * u;
                 if (o < n_out) {
                     const int e = o / dd, c = o % dd;
                     const float a = elem<T>::load(x1 + xrow * d + e) * (y1[yrow * dd + c] * scale);
@@ -451,28 +453,39 @@ __global__ __launch_bounds__(256) void bwd_wpart_kernel(
         }
 #pragma unroll
         for (int u = 0; u < 8; ++u) {
-            const int o = o0 + (int)threadIdx.x + 256 * u;
+            const int o = o0 + lane_id_x() + 256 * u;
             if (o < n_out) out[o] = acc[u];
         }
     }
 }
 
-// Sum of the chunk partials in chunk order; tied: dw_down = dW_down + dW_up^T.
-// Grid: (ceil(d * dd / 256), Hkv).
+// Sum of the chunk partials; tied: dw_down = dW_down + dW_up^T. A workgroup
+// takes 64 outputs of one KV head; its 4 wavefronts each sum every 4th chunk
+// in chunk order, and the 4 sums are added in wavefront order, so the result
+// is the same on every run. Grid: (ceil(d * dd / 64), Hkv).
 __global__ __launch_bounds__(256) void bwd_wreduce_kernel(const float* __restrict__ part,
                                                           float* __restrict__ dwd,
                                                           float* __restrict__ dwu, int Hkv,
                                                           int d, int dd, int nchunk_d,
                                                           int nchunk_u, int nchunk) {
-    const int g = blockIdx.y;
-    const int o = blockIdx.x * 256 + threadIdx.x;
+    __shared__ float red[2][4][64];
+    const int g = wg_id_y();
+    const int ol = lane_id_x() & 63, grp = lane_id_x() >> 6;
+    const int o = wg_id_x() * 64 + ol;
     const int n_out = d * dd;
-    if (o >= n_out) return;
-    const float* pd = part + ((size_t)g * nchunk) * n_out;
-    const float* pu = part + ((size_t)(Hkv + g) * nchunk) * n_out;
     float sd = 0.f, su = 0.f;
-    for (int c = 0; c < nchunk_d; ++c) sd += pd[(size_t)c * n_out + o];
-    for (int c = 0; c < nchunk_u; ++c) su += pu[(size_t)c * n_out + o];
+    if (o < n_out) {
+        const float* pd = part + ((size_t)g * nchunk) * n_out + o;
+        const float* pu = part + ((size_t)(Hkv + g) * nchunk) * n_out + o;
+        for (int c = grp; c < nchunk_d; c += 4) sd += pd[(size_t)c * n_out];
+        for (int c = grp; c < nchunk_u; c += 4) su += pu[(size_t)c * n_out];
+    }
+    red[0][grp][ol] = sd;
+    red[1][grp][ol] = su;
+    __syncthreads();
+    if (grp != 0 || o >= n_out) return;
+    sd = ((red[0][0][ol] + red[0][1][ol]) + red[0][2][ol]) + red[0][3][ol];
+    su = ((red[1][0][ol] + red[1][1][ol]) + red[1][2][ol]) + red[1][3][ol];
     const int e = o / dd, c = o % dd;
     if (dwu) {
         dwd[(size_t)g * n_out + o] = sd;
@@ -480,6 +493,13 @@ __global__ __launch_bounds__(256) void bwd_wreduce_kernel(const float* __restric
     } else {
         dwd[(size_t)g * n_out + o] = sd + su;
     }
+}
+
+hipError_t launch_bwd_wreduce(const float* part, float* dwd, float* dwu, int Hkv, int d, int dd,
+                              const BwdWs& L, hipStream_t st) {
+    hipLaunchKernelGGL(bwd_wreduce_kernel, dim3((d * dd + 63) / 64, Hkv), dim3(256), 0, st, part,
+                       dwd, dwu, Hkv, d, dd, L.nchunk_d, L.nchunk_u, L.nchunk);
+    return hipGetLastError();
 }
 
 template <typename T>
@@ -504,17 +524,16 @@ hipError_t launch_bwd_weights(const T* q, const T* k, const T* v, const T* dout,
     hipLaunchKernelGGL(bwd_wpart_kernel<T>, dim3(L.nchunk, Hkv, 2), dim3(256), 0, st, q, k, v,
                        dout, gk, gv, hk, ol, part, B, Hq, Hkv, T_, d, dd, L.nchunk_d, L.nchunk_u,
                        L.nchunk, scale);
-    hipLaunchKernelGGL(bwd_wreduce_kernel, dim3((d * dd + 255) / 256, Hkv), dim3(256), 0, st,
-                       (const float*)part, dwd, dwu, Hkv, d, dd, L.nchunk_d, L.nchunk_u, L.nchunk);
-    return hipGetLastError();
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_bwd_wreduce(part, dwd, dwu, Hkv, d, dd, L, st);
 }
 
 template <typename T>
-hipError_t launch_bwd_valu(const T* q, const T* k, const T* v, const T* o, const T* dout,
-                           const T* wd, const T* wu, T* dq, T* dk, T* dv, float* dwd, float* dwu,
-                           char* ws, const BwdWs& L, int B, int Hq, int Hkv, int T_, int d, int dd,
-                           int w, hipStream_t st) {
-    float* lse = (float*)(ws + L.lse_off);
+hipError_t launch_bwd_valu(const T* q, const T* k, const T* v, const T* o, const float* lse,
+                           const T* dout, const T* wd, const T* wu, T* dq, T* dk, T* dv,
+                           float* dwd, float* dwu, char* ws, const BwdWs& L, int B, int Hq,
+                           int Hkv, int T_, int d, int dd, int w, hipStream_t st) {
     float* delta = (float*)(ws + L.delta_off);
     float* qt = (float*)(ws + L.qt_off);
     float* dot = (float*)(ws + L.dot_off);
@@ -551,10 +570,10 @@ hipError_t launch_bwd_valu(const T* q, const T* k, const T* v, const T* o, const
                                               const float*, const float*, const float*,        \
                                               const float*, float*, float*, float*, int, int,  \
                                               int, int, int, int, const BwdWs&, hipStream_t);  \
-    template hipError_t launch_bwd_valu<T>(const T*, const T*, const T*, const T*, const T*,   \
-                                           const T*, const T*, T*, T*, T*, float*, float*,     \
-                                           char*, const BwdWs&, int, int, int, int, int, int,  \
-                                           int, hipStream_t);
+    template hipError_t launch_bwd_valu<T>(const T*, const T*, const T*, const T*,             \
+                                           const float*, const T*, const T*, const T*, T*, T*, \
+                                           T*, float*, float*, char*, const BwdWs&, int, int,  \
+                                           int, int, int, int, int, hipStream_t);
 DAR_BWD_INST(float)
 DAR_BWD_INST(bf16_t)
 #undef DAR_BWD_INST

@@ -1,32 +1,35 @@
 // Matrix-core (MFMA) backward of the causal DAR prefill, bf16 storage, fp32
 // accumulation, gfx950. The gradient formulas are those of the vector-ALU
-// backward (backward.hip): one softmax over both regions, window pairs at
-// full d, distant pairs in d_down space with W_up absorbed.
+// backward (backward.hip): one softmax over both regions (its log-sum-exp is
+// the forward's), window pairs at full d, distant pairs in d_down space with
+// W_up absorbed.
 //
 // Kernels, in launch order:
 //  * bwd_prep_rows_kernel / bwd_prep_keys_kernel: q~ = q W_up^T (scaled by
-//    log2(e)/sqrt(d)), dO~ = dO W_up^T, delta = dO . O per query row, and the
-//    latents c^K, c^V (Eq. 1) per key, all in bf16, each also stored in
-//    32-token blocks transposed ([T/32][d_down][32]) for the operands that
-//    contract over tokens. Token counts are padded to a multiple of 32 with
-//    zero rows.
-//  * bwd_rows_mfma_kernel: one wavefront per 32 query rows, scores
-//    transposed (S^T = K Q^T, one query per lane column, as in the forward).
-//    Pass 1 takes the row log-sum-exp; pass 2 recomputes P, forms
-//    dP^T = V dO^T (or c^V dO~^T) and dS, and accumulates dq^T += K^T dS^T
-//    (window keys, K^T read transposed from LDS) and h^T += c^K^T dS^T,
-//    ol^T += c^V^T P^T (distant keys); the epilogue lifts h with W_up^T.
-//  * bwd_cols_mfma_kernel: one wavefront per 32 keys, scores in the other
-//    orientation (S = Q K^T, one key per lane column), so that P and dS are
-//    directly the B operands of dV^T += dO^T P and dK^T += Q^T dS (window
-//    rows, Q^T and dO^T read transposed from LDS) and of gK^T += q~^T dS,
-//    gV^T += dO~^T P (distant rows); the epilogue lifts gK and gV with
-//    W_down.
-//  * the weight-gradient reduction of backward.hip, on the fp32 h, ol, gK, gV.
-// Masked pairs get a score of -inf (P = 0, dS = 0). The reference of each
-// row's exponentials is its log-sum-exp, fed as the accumulator input of the
-// score product (distant) or through one FMA (window), and -delta is the
-// accumulator input of dP, so dS = P * dP' needs one multiply.
+//    log2(e)/sqrt(d)), dO~ = dO W_up^T, delta = dO . O and the log-sum-exp in
+//    log2 units per query row; the latents c^K, c^V (Eq. 1) per key; all
+//    operands bf16, each also stored in 32-token blocks transposed
+//    ([T/32][d_down][32]) for the products that contract over tokens. Token
+//    counts are padded to a multiple of 32 with zero rows.
+//  * bwd_rows_dist_kernel: one wavefront per 32 query rows, distant keys only
+//    (d_down wide), scores transposed (S^T = c^K q~^T, one query per lane
+//    column, as in the forward): h^T += c^K^T dS^T and ol^T += c^V^T P^T.
+//  * bwd_cols_dist_kernel: one wavefront per 32 keys, distant rows only, scores
+//    in the other orientation (S = q~ c^K^T, one key per lane column) so that
+//    P and dS are directly the B operands of gK^T += q~^T dS, gV^T += dO~^T P.
+//  * bwd_rows_local_kernel: window keys at full d through LDS tiles,
+//    dq^T += K^T dS^T (K^T read transposed from LDS); the epilogue adds the
+//    lifted distant part (h W_up, h as a bf16 hi + lo pair) and the
+//    workgroup's share of dW_up.
+//  * bwd_cols_local_kernel: window rows, dV^T += dO^T P and dK^T += Q^T dS;
+//    the epilogue adds gK W_down^T, gV W_down^T and the workgroup's share of
+//    dW_down.
+//  * bwd_wreduce_kernel (backward.hip): the shares summed in a fixed order.
+// No kernel accumulates with atomics, so the result does not depend on
+// timing. Masked pairs get a score of -inf (P = 0, dS = 0). Each row's
+// exponentials use its log-sum-exp as the reference, fed as the accumulator
+// input of the score product (distant) or through one FMA (window), and
+// -delta is the accumulator input of dP, so dS = P * dP' needs one multiply.
 #include "../../include/dar.h"
 #include "dar_common.hpp"
 #include "dar_kernels.hpp"
@@ -58,14 +61,73 @@ __device__ __forceinline__ void store_bf16x4(bf16_t* p, float a, float b, float 
     *reinterpret_cast<uint2*>(p) = make_uint2(pack2(a, b), pack2(c, d));
 }
 
-// A operand rows of a transposed latent block [d_down][32]: row R carries
-// latent column perm_row(R) (so the accumulator rows come out in B-operand
-// order), tokens 16 * half + 8 g + 0..7; rows past d_down are zero.
-template <int DD>
+// A operand rows of a transposed latent block [32][32] (latent rows past
+// d_down are zero): row R carries latent column perm_row(R), so the
+// accumulator rows come out in B-operand order; tokens 16 half + 8 g + 0..7.
 __device__ __forceinline__ bf16x8_t latT_operand(const bf16_t* blk, int qc, int hg, int half) {
-    const int c = perm_row(qc);
-    if (DD < 32 && c >= DD) return zero_bf16x8();
-    return load_bf16x8(blk + (size_t)c * 32 + 16 * half + 8 * hg);
+    return load_bf16x8(blk + (size_t)perm_row(qc) * 32 + 16 * half + 8 * hg);
+}
+
+// Eight bf16 [hi, mid, lo, 0, 0, 0, 0, 0] of -x: hi + mid + lo carries about
+// 24 significant bits of -x once summed in fp32.
+__device__ __forceinline__ uint4 neg_split3(float x) {
+    const float v = -x;
+    const uint32_t h = pack2(v, 0.f) & 0xffffu;
+    const float r1 = v - __uint_as_float(h << 16);
+    const uint32_t m = pack2(r1, 0.f) & 0xffffu;
+    const float r2 = r1 - __uint_as_float(m << 16);
+    const uint32_t lo = pack2(r2, 0.f) & 0xffffu;
+    return make_uint4(h | (m << 16), lo, 0u, 0u);
+}
+
+// B operand that sums the first three k slots of half `g1` (ones there, zeros
+// elsewhere): with the row-constant A operand it adds -lse (g1 = 0) or
+// -delta (g1 = 1) to every accumulator of the row.
+__device__ __forceinline__ bf16x8_t ones3(int hg, int g1) {
+    return hg == g1 ? __builtin_bit_cast(bf16x8_t, make_uint4(0x3f803f80u, 0x3f80u, 0u, 0u))
+                    : zero_bf16x8();
+}
+
+// 8 fp32 values (16-byte aligned) times f, as a bf16 hi + lo pair.
+__device__ __forceinline__ void split_load8(const float* p, float f, bf16x8_t& hi, bf16x8_t& lo) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    f32x16_t x;
+    x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w; x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+    split8(x, 0, f, hi, lo);
+}
+
+// 8 fp32 values (16-byte aligned) times f, as one bf16 operand.
+__device__ __forceinline__ bf16x8_t pack_load8(const float* p, float f) {
+    const float4 a = *reinterpret_cast<const float4*>(p);
+    const float4 b = *reinterpret_cast<const float4*>(p + 4);
+    return __builtin_bit_cast(bf16x8_t, make_uint4(pack2(a.x * f, a.y * f), pack2(a.z * f, a.w * f),
+                                                   pack2(b.x * f, b.y * f), pack2(b.z * f, b.w * f)));
+}
+
+// Workgroup share of a weight gradient: every wavefront adds its C tiles
+// (rows e = 32 t + accumulator row, column c = lane % 32 < DD) into pbuf in
+// wavefront order, then the workgroup writes pbuf [D][DD] to `out`. Every
+// wavefront of the workgroup must call this (it holds barriers).
+template <int D, int DD, int NW>
+__device__ __forceinline__ void wg_share(const f32x16_t (&acc)[D / 32], float* pbuf, int wave,
+                                         int lane, int tid, float* __restrict__ out) {
+    const int qc = lane & 31, hg = lane >> 5;
+#pragma unroll
+    for (int wv = 0; wv < NW; ++wv) {
+        if (wave == wv && qc < DD) {
+#pragma unroll
+            for (int t = 0; t < D / 32; ++t)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int e = 32 * t + 8 * (r >> 2) + 4 * hg + (r & 3);
+                    float* cell = pbuf + e * DD + qc;
+                    *cell = (wv == 0) ? acc[t][r] : *cell + acc[t][r];
+                }
+        }
+        __syncthreads();
+    }
+    for (int idx = tid; idx < D * DD; idx += NW * 64) out[idx] = pbuf[idx];
 }
 
 }  // namespace
@@ -73,25 +135,28 @@ __device__ __forceinline__ bf16x8_t latT_operand(const bf16_t* blk, int qc, int 
 // ---------------------------------------------------------------- preparation
 
 // Per query row i (padded rows get zeros): q~s = (q W_up^T) log2(e)/sqrt(d),
-// dO~ = dO W_up^T (bf16, row-major and in transposed 32-row blocks) and
-// delta = dO . O (fp32). One thread per row. Grid: (ceil(Tr / 256), B * Hq).
+// dO~ = dO W_up^T (bf16, row-major and in transposed 32-row blocks), and
+// -delta = -dO . O and -lse (the forward's, in log2 units), both in fp32 and
+// as bf16 hi + mid + lo row constants. One thread per row.
+// Grid: (ceil(Tr / 256), B * Hq).
 template <int D, int DD>
 __global__ __launch_bounds__(256) void bwd_prep_rows_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ o, const bf16_t* __restrict__ dout,
-    const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu, bf16_t* __restrict__ qts,
-    bf16_t* __restrict__ qtT, bf16_t* __restrict__ dts, bf16_t* __restrict__ dtT,
-    float* __restrict__ delta, int Hq, int Hkv, int T, int Tr, float qscale) {
+    const float* __restrict__ lse, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
+    bf16_t* __restrict__ qts, bf16_t* __restrict__ qtT, bf16_t* __restrict__ dts,
+    bf16_t* __restrict__ dtT, bf16_t* __restrict__ rc, float* __restrict__ nd,
+    float* __restrict__ nl2, int Hq, int Hkv, int T, int Tr, float qscale) {
     __shared__ float U[DD * D];  // U[c][e] = W_up[c][e]
-    const int bh = blockIdx.y;
+    const int bh = wg_id_y();
     const int g = (bh % Hq) / (Hq / Hkv);
     const bf16_t* wdg = wd + (size_t)g * D * DD;
     const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
-    for (int idx = threadIdx.x; idx < DD * D; idx += 256) {
+    for (int idx = lane_id_x(); idx < DD * D; idx += 256) {
         const int c = idx / D, e = idx % D;
         U[idx] = wug ? bf16_to_f32(wug[(size_t)c * D + e]) : bf16_to_f32(wdg[(size_t)e * DD + c]);
     }
     __syncthreads();
-    const int i = blockIdx.x * 256 + threadIdx.x;
+    const int i = wg_id_x() * 256 + lane_id_x();
     if (i >= Tr) return;
     float aq[DD], ad[DD];
 #pragma unroll
@@ -134,14 +199,19 @@ __global__ __launch_bounds__(256) void bwd_prep_rows_kernel(
             make_uint4(pack2(ad[c8], ad[c8 + 1]), pack2(ad[c8 + 2], ad[c8 + 3]),
                        pack2(ad[c8 + 4], ad[c8 + 5]), pack2(ad[c8 + 6], ad[c8 + 7]));
     }
-    bf16_t* qb = qtT + ((size_t)bh * (Tr / 32) + i / 32) * DD * 32 + (i & 31);
-    bf16_t* db = dtT + ((size_t)bh * (Tr / 32) + i / 32) * DD * 32 + (i & 31);
+    bf16_t* qb = qtT + ((size_t)bh * (Tr / 32) + i / 32) * 32 * 32 + (i & 31);
+    bf16_t* db = dtT + ((size_t)bh * (Tr / 32) + i / 32) * 32 * 32 + (i & 31);
 #pragma unroll
-    for (int c = 0; c < DD; ++c) {
-        qb[c * 32] = f32_to_bf16(aq[c] * qscale);
-        db[c * 32] = f32_to_bf16(ad[c]);
+    for (int c = 0; c < 32; ++c) {
+        qb[c * 32] = c < DD ? f32_to_bf16(aq[c < DD ? c : 0] * qscale) : (bf16_t)0;
+        db[c * 32] = c < DD ? f32_to_bf16(ad[c < DD ? c : 0]) : (bf16_t)0;
     }
-    delta[prow] = dl;
+    const float L2 = i < T ? lse[(size_t)bh * T + i] * kLog2eB : 0.f;
+    nd[prow] = -dl;
+    nl2[prow] = -L2;
+    const uint4 cl = neg_split3(L2), cd = neg_split3(dl);
+    *reinterpret_cast<uint4*>(rc + prow * 16) = cl;
+    *reinterpret_cast<uint4*>(rc + prow * 16 + 8) = cd;
 }
 
 // Per key token j (padded rows get zeros): c^K = k W_down, c^V = v W_down
@@ -153,12 +223,12 @@ __global__ __launch_bounds__(256) void bwd_prep_keys_kernel(
     bf16_t* __restrict__ ckb, bf16_t* __restrict__ ckT, bf16_t* __restrict__ cvb,
     bf16_t* __restrict__ cvT, int Hkv, int T, int Tr) {
     __shared__ float W[D * DD];  // W[e][c] = W_down[e][c]
-    const int bg = blockIdx.y;
+    const int bg = wg_id_y();
     const int g = bg % Hkv;
     const bf16_t* wdg = wd + (size_t)g * D * DD;
-    for (int idx = threadIdx.x; idx < D * DD; idx += 256) W[idx] = bf16_to_f32(wdg[idx]);
+    for (int idx = lane_id_x(); idx < D * DD; idx += 256) W[idx] = bf16_to_f32(wdg[idx]);
     __syncthreads();
-    const int j = blockIdx.x * 256 + threadIdx.x;
+    const int j = wg_id_x() * 256 + lane_id_x();
     if (j >= Tr) return;
     float ak[DD], av[DD];
 #pragma unroll
@@ -194,201 +264,319 @@ __global__ __launch_bounds__(256) void bwd_prep_keys_kernel(
             make_uint4(pack2(av[c8], av[c8 + 1]), pack2(av[c8 + 2], av[c8 + 3]),
                        pack2(av[c8 + 4], av[c8 + 5]), pack2(av[c8 + 6], av[c8 + 7]));
     }
-    bf16_t* kb = ckT + ((size_t)bg * (Tr / 32) + j / 32) * DD * 32 + (j & 31);
-    bf16_t* vb = cvT + ((size_t)bg * (Tr / 32) + j / 32) * DD * 32 + (j & 31);
+    bf16_t* kb = ckT + ((size_t)bg * (Tr / 32) + j / 32) * 32 * 32 + (j & 31);
+    bf16_t* vb = cvT + ((size_t)bg * (Tr / 32) + j / 32) * 32 * 32 + (j & 31);
 #pragma unroll
-    for (int c = 0; c < DD; ++c) {
-        kb[c * 32] = f32_to_bf16(ak[c]);
-        vb[c * 32] = f32_to_bf16(av[c]);
+    for (int c = 0; c < 32; ++c) {
+        kb[c * 32] = c < DD ? f32_to_bf16(ak[c < DD ? c : 0]) : (bf16_t)0;
+        vb[c * 32] = c < DD ? f32_to_bf16(av[c < DD ? c : 0]) : (bf16_t)0;
     }
 }
 
-// ---------------------------------------------------------------- rows: dq, h, ol
+// ---------------------------------------------------------------- distant: h, ol
 
-template <int D, int DD, int NW>
-__global__ __launch_bounds__(NW * 64) void bwd_rows_mfma_kernel(
-    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
-    const bf16_t* __restrict__ dout, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
+// One wavefront per 32 query rows of one (batch, query head), distant keys
+// j <= i - w only. No LDS and no barriers: the d_down-wide operands are read
+// straight from L2, one 32-key subtile ahead (two register sets used in
+// turn). Writes h = sum dS c^K and ol = sum P c^V (fp32) of every real row
+// (zero without distant keys). Grid: (ceil(T / (32 NW)), B * Hq); row blocks
+// with the most keys first.
+template <int DD>
+struct RowDistOps {
+    bf16x8_t ck[DD / 16], cv[DD / 16], kt[2], vt[2];
+};
+
+template <int DD, int NW>
+__global__ __launch_bounds__(NW * 64) void bwd_rows_dist_kernel(
     const bf16_t* __restrict__ ckb, const bf16_t* __restrict__ ckT,
     const bf16_t* __restrict__ cvb, const bf16_t* __restrict__ cvT,
     const bf16_t* __restrict__ qts, const bf16_t* __restrict__ dts,
-    const float* __restrict__ delta, float* __restrict__ lse, float* __restrict__ hk,
-    float* __restrict__ ol, bf16_t* __restrict__ dq, int Hq, int Hkv, int T, int Tr, int w,
-    float qscale, float scale) {
-    constexpr int KS = D / 16, NT = D / 32, DS = DD / 16, BN = 64, LDK = D + 8, LDU = DD + 8;
-    constexpr int BM = NW * 32;
-    __shared__ __attribute__((aligned(16))) bf16_t lds_k[BN * LDK];
-    __shared__ __attribute__((aligned(16))) bf16_t lds_v[BN * LDK];
-    __shared__ __attribute__((aligned(16))) bf16_t ut[D * LDU];  // ut[e][c] = W_up[c][e]
+    const float* __restrict__ nl2, const float* __restrict__ nd, float* __restrict__ hk,
+    float* __restrict__ ol, int Hq, int Hkv, int T, int Tr, int w) {
+    constexpr int DS = DD / 16, BM = NW * 32;
+    const int lane = lane_id_x() & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(lane_id_x() >> 6);
+    const int nblk = (T + BM - 1) / BM;
+    const int rb = nblk - 1 - wg_id_x();
+    const int bh = wg_id_y();
+    const int b = bh / Hq, h = bh % Hq;
+    const int bg = b * Hkv + h / (Hq / Hkv);
+    const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
+    const int r0 = rb * BM + wave * 32, i = r0 + qc;
+    if (r0 >= T) return;  // no barriers in this kernel
+    const int i_hi = imin(r0 + 31, T - 1);
+    const int ii = imin(i, T - 1);
+    const int T32 = Tr / 32;
+    const size_t prw = (size_t)bh * Tr + ii;
 
-    const int tid = threadIdx.x, lane = tid & 63;
+    bf16x8_t qtop[DS], dtop[DS];
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+        qtop[s] = load_bf16x8(qts + prw * DD + s * 16 + hg * 8);
+        dtop[s] = load_bf16x8(dts + prw * DD + s * 16 + hg * 8);
+    }
+    const f32x16_t negL = splat16(nl2[prw]), negd = splat16(nd[prw]);
+    f32x16_t hT = splat16(0.f), olT = splat16(0.f);
+
+    const int jd_end = i_hi - w;  // last distant key of any row here
+    if (jd_end >= 0) {
+        const bf16_t* ckg = ckb + (size_t)bg * Tr * DD + (size_t)prow * DD + hg * 8;
+        const bf16_t* cvg = cvb + (size_t)bg * Tr * DD + (size_t)prow * DD + hg * 8;
+        const bf16_t* ckTg = ckT + (size_t)bg * T32 * 32 * 32;
+        const bf16_t* cvTg = cvT + (size_t)bg * T32 * 32 * 32;
+        const int js_last = jd_end & ~31;
+        auto load = [&](int js) {
+            js = imin(js, js_last);  // loads past the last subtile repeat it
+            RowDistOps<DD> o;
+#pragma unroll
+            for (int s = 0; s < DS; ++s) {
+                o.ck[s] = load_bf16x8(ckg + (size_t)js * DD + s * 16);
+                o.cv[s] = load_bf16x8(cvg + (size_t)js * DD + s * 16);
+            }
+            const bf16_t* kb = ckTg + (size_t)(js >> 5) * 32 * 32;
+            const bf16_t* vb = cvTg + (size_t)(js >> 5) * 32 * 32;
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                o.kt[hf] = latT_operand(kb, qc, hg, hf);
+                o.vt[hf] = latT_operand(vb, qc, hg, hf);
+            }
+            return o;
+        };
+        auto step = [&](const RowDistOps<DD>& c, int js) {
+            f32x16_t x = mfma(c.ck[0], qtop[0], negL);
+            f32x16_t dp = mfma(c.cv[0], dtop[0], negd);
+            if (DS == 2) {
+                x = mfma(c.ck[DS - 1], qtop[DS - 1], x);
+                dp = mfma(c.cv[DS - 1], dtop[DS - 1], dp);
+            }
+            if (js + 31 > r0 - w) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    if (js + acc_row(r, hg) > i - w) x[r] = -INFINITY;
+            }
+            f32x16_t p, ds;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                p[r] = __builtin_amdgcn_exp2f(x[r]);
+                ds[r] = p[r] * dp[r];
+            }
+            hT = mfma(c.kt[0], pack8(ds, 0), hT);
+            hT = mfma(c.kt[1], pack8(ds, 8), hT);
+            olT = mfma(c.vt[0], pack8(p, 0), olT);
+            olT = mfma(c.vt[1], pack8(p, 8), olT);
+        };
+        RowDistOps<DD> ca = load(0), cb;
+        for (int js = 0;; js += 64) {
+            cb = load(js + 32);
+            step(ca, js);
+            if (js + 32 > jd_end) break;
+            ca = load(js + 64);
+            step(cb, js + 32);
+            if (js + 64 > jd_end) break;
+        }
+    }
+    if (i >= T) return;
+    float* hr = hk + ((size_t)bh * T + i) * DD;
+    float* orr = ol + ((size_t)bh * T + i) * DD;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+        const int c = 16 * s + 8 * hg;
+        *reinterpret_cast<float4*>(hr + c) = make_float4(hT[8 * s], hT[8 * s + 1], hT[8 * s + 2], hT[8 * s + 3]);
+        *reinterpret_cast<float4*>(hr + c + 4) = make_float4(hT[8 * s + 4], hT[8 * s + 5], hT[8 * s + 6], hT[8 * s + 7]);
+        *reinterpret_cast<float4*>(orr + c) = make_float4(olT[8 * s], olT[8 * s + 1], olT[8 * s + 2], olT[8 * s + 3]);
+        *reinterpret_cast<float4*>(orr + c + 4) = make_float4(olT[8 * s + 4], olT[8 * s + 5], olT[8 * s + 6], olT[8 * s + 7]);
+    }
+}
+
+// ---------------------------------------------------------------- distant: gK, gV
+
+// One wavefront per 32 keys of one (batch, KV head), the distant rows
+// i >= j + w of every query head of the group. No LDS and no barriers; the
+// row operands are read from L2 one 32-row subtile ahead (two register sets
+// used in turn). Each row's -lse and -delta enter through one more product
+// each, with the row-constant operand (hi + mid + lo) against ones3. Writes
+// gK = sum dS q~ (q~ unscaled) and gV = sum P dO~ (fp32) of every real key.
+// Grid: (ceil(T / (32 NW)), B * Hkv); key block 0 (most rows) first.
+template <int DD>
+struct ColDistOps {
+    bf16x8_t q[DD / 16], d[DD / 16], qt[2], dt[2], cst;
+};
+
+template <int DD, int NW>
+__global__ __launch_bounds__(NW * 64) void bwd_cols_dist_kernel(
+    const bf16_t* __restrict__ ckb, const bf16_t* __restrict__ cvb,
+    const bf16_t* __restrict__ qts, const bf16_t* __restrict__ qtT,
+    const bf16_t* __restrict__ dts, const bf16_t* __restrict__ dtT,
+    const bf16_t* __restrict__ rc, float* __restrict__ gk, float* __restrict__ gv, int Hq,
+    int Hkv, int T, int Tr, int w, float gscale) {
+    constexpr int DS = DD / 16, BK = NW * 32;
+    const int lane = lane_id_x() & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(lane_id_x() >> 6);
+    const int bg = wg_id_y();
+    const int b = bg / Hkv, g = bg % Hkv;
+    const int G = Hq / Hkv;
+    const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
+    const int c0 = wg_id_x() * BK + wave * 32, j = c0 + qc;
+    if (c0 >= T) return;  // no barriers in this kernel
+    const int jj = imin(j, T - 1);
+    const int T32 = Tr / 32;
+
+    bf16x8_t ckop[DS], cvop[DS];
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+        ckop[s] = load_bf16x8(ckb + ((size_t)bg * Tr + jj) * DD + s * 16 + hg * 8);
+        cvop[s] = load_bf16x8(cvb + ((size_t)bg * Tr + jj) * DD + s * 16 + hg * 8);
+    }
+    const bf16x8_t b_lse = ones3(hg, 0), b_del = ones3(hg, 1);
+    f32x16_t gkT = splat16(0.f), gvT = splat16(0.f);
+    const int is0 = (c0 + w) & ~31;  // first row block with a distant pair
+    const int is_last = (T - 1) & ~31;
+    for (int hh = 0; hh < G && is0 < T; ++hh) {
+        const int bh = b * Hq + g * G + hh;
+        const bf16_t* qth = qts + (size_t)bh * Tr * DD + (size_t)prow * DD + hg * 8;
+        const bf16_t* dth = dts + (size_t)bh * Tr * DD + (size_t)prow * DD + hg * 8;
+        const bf16_t* rch = rc + (size_t)bh * Tr * 16 + (size_t)prow * 16 + hg * 8;
+        const bf16_t* qtTh = qtT + (size_t)bh * T32 * 32 * 32;
+        const bf16_t* dtTh = dtT + (size_t)bh * T32 * 32 * 32;
+        auto load = [&](int is) {
+            is = imin(is, is_last);  // loads past the last subtile repeat it
+            ColDistOps<DD> o;
+#pragma unroll
+            for (int s = 0; s < DS; ++s) {
+                o.q[s] = load_bf16x8(qth + (size_t)is * DD + s * 16);
+                o.d[s] = load_bf16x8(dth + (size_t)is * DD + s * 16);
+            }
+            o.cst = load_bf16x8(rch + (size_t)is * 16);
+            const bf16_t* qb = qtTh + (size_t)(is >> 5) * 32 * 32;
+            const bf16_t* db = dtTh + (size_t)(is >> 5) * 32 * 32;
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                o.qt[hf] = latT_operand(qb, qc, hg, hf);
+                o.dt[hf] = latT_operand(db, qc, hg, hf);
+            }
+            return o;
+        };
+        auto step = [&](const ColDistOps<DD>& c, int is) {
+            f32x16_t x = mfma(c.cst, b_lse, splat16(0.f));
+            f32x16_t dp = mfma(c.cst, b_del, splat16(0.f));
+#pragma unroll
+            for (int s = 0; s < DS; ++s) {
+                x = mfma(c.q[s], ckop[s], x);
+                dp = mfma(c.d[s], cvop[s], dp);
+            }
+            if (!(is >= c0 + 31 + w && is + 31 < T)) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int i = is + acc_row(r, hg);
+                    if (i - j < w || i >= T) x[r] = -INFINITY;
+                }
+            }
+            f32x16_t p, ds;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                p[r] = __builtin_amdgcn_exp2f(x[r]);
+                ds[r] = p[r] * dp[r];
+            }
+            gkT = mfma(c.qt[0], pack8(ds, 0), gkT);
+            gkT = mfma(c.qt[1], pack8(ds, 8), gkT);
+            gvT = mfma(c.dt[0], pack8(p, 0), gvT);
+            gvT = mfma(c.dt[1], pack8(p, 8), gvT);
+        };
+        ColDistOps<DD> ca = load(is0), cb;
+        for (int is = is0;; is += 64) {
+            cb = load(is + 32);
+            step(ca, is);
+            if (is + 32 >= T) break;
+            ca = load(is + 64);
+            step(cb, is + 32);
+            if (is + 64 >= T) break;
+        }
+    }
+    if (j >= T) return;
+    float* gkr = gk + ((size_t)bg * T + j) * DD;
+    float* gvr = gv + ((size_t)bg * T + j) * DD;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+        const int c = 16 * s + 8 * hg;
+        *reinterpret_cast<float4*>(gkr + c) =
+            make_float4(gkT[8 * s] * gscale, gkT[8 * s + 1] * gscale, gkT[8 * s + 2] * gscale, gkT[8 * s + 3] * gscale);
+        *reinterpret_cast<float4*>(gkr + c + 4) =
+            make_float4(gkT[8 * s + 4] * gscale, gkT[8 * s + 5] * gscale, gkT[8 * s + 6] * gscale, gkT[8 * s + 7] * gscale);
+        *reinterpret_cast<float4*>(gvr + c) = make_float4(gvT[8 * s], gvT[8 * s + 1], gvT[8 * s + 2], gvT[8 * s + 3]);
+        *reinterpret_cast<float4*>(gvr + c + 4) = make_float4(gvT[8 * s + 4], gvT[8 * s + 5], gvT[8 * s + 6], gvT[8 * s + 7]);
+    }
+}
+
+// ---------------------------------------------------------------- window: dq, dW_up
+
+// One wavefront per 32 query rows, window keys i - w < j <= i through 64-key
+// K/V tiles in LDS. Epilogue: dq = s (dq_win + h W_up) and the workgroup's
+// share of dW_up^T = sum_i q_i^T (s h_i) + dO_i^T ol_i (chunk
+// (b * G + h % G) * nblk + row block). Grid: (ceil(T / (32 NW)), B * Hq).
+template <int D, int DD, int NW>
+__global__ __launch_bounds__(NW * 64) void bwd_rows_local_kernel(
+    const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
+    const bf16_t* __restrict__ dout, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
+    const float* __restrict__ hk, const float* __restrict__ ol, const float* __restrict__ nl2,
+    const float* __restrict__ nd, bf16_t* __restrict__ dq, float* __restrict__ wpart, int Hq,
+    int Hkv, int T, int Tr, int w, float qscale, float scale, int nchunk) {
+    constexpr int KS = D / 16, NT = D / 32, DS = DD / 16, BN = 64, LDK = D + 8, LDH = 40;
+    constexpr int BM = NW * 32;
+    __shared__ __attribute__((aligned(16))) bf16_t lds_kv[2 * BN * LDK];  // K tile, V tile
+    __shared__ __attribute__((aligned(16))) bf16_t lds_h[NW * 32 * LDH];
+    __shared__ __attribute__((aligned(16))) float pbuf[D * DD];
+    bf16_t* lds_k = lds_kv;
+    bf16_t* lds_v = lds_kv + BN * LDK;
+
+    const int tid = lane_id_x(), lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nblk = (T + BM - 1) / BM;
-    const int rb = nblk - 1 - (int)blockIdx.x;  // longest row blocks first
-    const int bh = blockIdx.y;
+    const int rb = nblk - 1 - wg_id_x();
+    const int bh = wg_id_y();
     const int b = bh / Hq, h = bh % Hq;
-    const int g = h / (Hq / Hkv);
+    const int G = Hq / Hkv;
+    const int g = h / G;
     const int bg = b * Hkv + g;
     const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
     const int i0 = rb * BM, r0 = i0 + wave * 32, i = r0 + qc;
-    const bool live = r0 < T;                // this wavefront has real rows
-    const int i_hi = imin(r0 + 31, T - 1);   // its last real row
+    const bool live = r0 < T;
+    const int i_hi = imin(r0 + 31, T - 1);
     const int iwg_hi = imin(i0 + BM - 1, T - 1);
     const int ii = imin(i, T - 1);
-    const int T32 = Tr / 32;
 
-    const bf16_t* wdg = wd + (size_t)g * D * DD;
-    const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
-    for (int idx = tid; idx < D * DD; idx += NW * 64) {
-        const int e = idx / DD, c = idx % DD;
-        ut[e * LDU + c] = wug ? wug[(size_t)c * D + e] : wdg[(size_t)e * DD + c];
-    }
-
-    // B operands of the query row: S^T = K Q^T, dP^T = V dO^T and the distant
-    // forms with q~s, dO~.
     const bf16_t* qrow = q + ((size_t)bh * T + ii) * D;
     const bf16_t* drow = dout + ((size_t)bh * T + ii) * D;
-    bf16x8_t qop[KS], doop[KS], qtop[DS], dtop[DS];
+    bf16x8_t qop[KS], doop[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
         qop[s] = load_bf16x8(qrow + s * 16 + hg * 8);
         doop[s] = load_bf16x8(drow + s * 16 + hg * 8);
     }
     const size_t prw = (size_t)bh * Tr + ii;
-#pragma unroll
-    for (int s = 0; s < DS; ++s) {
-        qtop[s] = load_bf16x8(qts + prw * DD + s * 16 + hg * 8);
-        dtop[s] = load_bf16x8(dts + prw * DD + s * 16 + hg * 8);
-    }
-    const float dl = delta[prw];
-    __syncthreads();
-
-    const int jd_end = live ? i_hi - w : -1;  // last distant key of any row here
-    const bool wg_local = w > 0 && i0 < T;
-    const int jlo = imax(0, i0 - w + 1);
-    const bf16_t* ckg = ckb + (size_t)bg * Tr * DD;
-    const bf16_t* cvg = cvb + (size_t)bg * Tr * DD;
-    const bf16_t* ckTg = ckT + (size_t)bg * T32 * DD * 32;
-    const bf16_t* cvTg = cvT + (size_t)bg * T32 * DD * 32;
-    const bf16_t* kg = k + (size_t)bg * T * D;
-    const bf16_t* vg = v + (size_t)bg * T * D;
-
-    auto load_tile = [&](int t, bool with_v) {
-        constexpr int C8 = D / 8;
-        for (int idx = tid; idx < BN * C8; idx += NW * 64) {
-            const int r = idx / C8, c8 = idx % C8;
-            const int key = t + r;
-            uint4 uk = make_uint4(0, 0, 0, 0), uv = make_uint4(0, 0, 0, 0);
-            if (key < T) {
-                uk = *reinterpret_cast<const uint4*>(kg + (size_t)key * D + c8 * 8);
-                if (with_v) uv = *reinterpret_cast<const uint4*>(vg + (size_t)key * D + c8 * 8);
-            }
-            *reinterpret_cast<uint4*>(lds_k + r * LDK + c8 * 8) = uk;
-            if (with_v) *reinterpret_cast<uint4*>(lds_v + r * LDK + c8 * 8) = uv;
-        }
-    };
-
-    // ---- pass 1: log-sum-exp of the row (log2 domain)
-    float m = -INFINITY, l = 0.f;
-    auto stats = [&](const f32x16_t& x) {
-        float mx = x[0];
-#pragma unroll
-        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, x[r]);
-        mx = pair_max(mx);
-        if (mx > m) {
-            l *= exp2f(m - mx);
-            m = mx;
-        }
-        if (m != -INFINITY) {
-            float s = 0.f;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) s += __builtin_amdgcn_exp2f(x[r] - m);
-            l += s;
-        }
-    };
-    for (int js = 0; js <= jd_end; js += 32) {
-        const bf16_t* cr = ckg + (size_t)(js + prow) * DD + hg * 8;
-        f32x16_t x = mfma(load_bf16x8(cr), qtop[0], splat16(0.f));
-        if (DS == 2) x = mfma(load_bf16x8(cr + 16), qtop[DS - 1], x);
-        if (js + 31 > r0 - w) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                if (js + acc_row(r, hg) > i - w) x[r] = -INFINITY;
-        }
-        stats(x);
-    }
-    if (wg_local) {
-        for (int t = jlo & ~(BN - 1); t <= iwg_hi; t += BN) {
-            __syncthreads();
-            load_tile(t, false);
-            __syncthreads();
-            if (!live) continue;
-#pragma unroll
-            for (int sub = 0; sub < BN / 32; ++sub) {
-                const int js = t + sub * 32;
-                if (js > i_hi || js + 31 <= r0 - w) continue;
-                f32x16_t sc = splat16(0.f);
-#pragma unroll
-                for (int s = 0; s < KS; ++s)
-                    sc = mfma(load_bf16x8(lds_k + (sub * 32 + prow) * LDK + s * 16 + hg * 8), qop[s], sc);
-                f32x16_t x;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) x[r] = sc[r] * qscale;
-                if (!(js > i_hi - w && js + 31 <= r0)) {
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int j = js + acc_row(r, hg);
-                        if (j <= i - w || j > i) x[r] = -INFINITY;
-                    }
-                }
-                stats(x);
-            }
-        }
-    }
-    l = pair_sum(l);
-    const float L = (m == -INFINITY) ? 0.f : m + log2f(l);
-    if (live && i < Tr && hg == 0) lse[(size_t)bh * Tr + i] = L;  // padded rows: finite
-
-    // ---- pass 2: gradients
+    const float nL = nl2[prw];
+    const f32x16_t negd = splat16(nd[prw]);
     f32x16_t dqT[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) dqT[t] = splat16(0.f);
-    f32x16_t hT = splat16(0.f), olT = splat16(0.f);
-    const f32x16_t negL = splat16(-L), negd = splat16(-dl);
 
-    for (int js = 0; js <= jd_end; js += 32) {
-        const bf16_t* cr = ckg + (size_t)(js + prow) * DD + hg * 8;
-        const bf16_t* vr = cvg + (size_t)(js + prow) * DD + hg * 8;
-        f32x16_t x = mfma(load_bf16x8(cr), qtop[0], negL);
-        f32x16_t dp = mfma(load_bf16x8(vr), dtop[0], negd);
-        if (DS == 2) {
-            x = mfma(load_bf16x8(cr + 16), qtop[DS - 1], x);
-            dp = mfma(load_bf16x8(vr + 16), dtop[DS - 1], dp);
-        }
-        if (js + 31 > r0 - w) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-                if (js + acc_row(r, hg) > i - w) x[r] = -INFINITY;
-        }
-        f32x16_t p, ds;
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-            p[r] = __builtin_amdgcn_exp2f(x[r]);
-            ds[r] = p[r] * dp[r];
-        }
-        const bf16x8_t p0 = pack8(p, 0), p1 = pack8(p, 8);
-        const bf16x8_t s0 = pack8(ds, 0), s1 = pack8(ds, 8);
-        const bf16_t* kblk = ckTg + (size_t)(js >> 5) * DD * 32;
-        const bf16_t* vblk = cvTg + (size_t)(js >> 5) * DD * 32;
-        hT = mfma(latT_operand<DD>(kblk, qc, hg, 0), s0, hT);
-        hT = mfma(latT_operand<DD>(kblk, qc, hg, 1), s1, hT);
-        olT = mfma(latT_operand<DD>(vblk, qc, hg, 0), p0, olT);
-        olT = mfma(latT_operand<DD>(vblk, qc, hg, 1), p1, olT);
-    }
-    if (wg_local) {
+    const bf16_t* kg = k + (size_t)bg * T * D;
+    const bf16_t* vg = v + (size_t)bg * T * D;
+    if (w > 0) {
+        const int jlo = imax(0, i0 - w + 1);
         for (int t = jlo & ~(BN - 1); t <= iwg_hi; t += BN) {
             __syncthreads();
-            load_tile(t, true);
+            constexpr int C8 = D / 8;
+            for (int idx = tid; idx < BN * C8; idx += NW * 64) {
+                const int r = idx / C8, c8 = idx % C8;
+                const int key = t + r;
+                uint4 uk = make_uint4(0, 0, 0, 0), uv = make_uint4(0, 0, 0, 0);
+                if (key < T) {
+                    uk = *reinterpret_cast<const uint4*>(kg + (size_t)key * D + c8 * 8);
+                    uv = *reinterpret_cast<const uint4*>(vg + (size_t)key * D + c8 * 8);
+                }
+                *reinterpret_cast<uint4*>(lds_k + r * LDK + c8 * 8) = uk;
+                *reinterpret_cast<uint4*>(lds_v + r * LDK + c8 * 8) = uv;
+            }
             __syncthreads();
             if (!live) continue;
 #pragma unroll
@@ -403,7 +591,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_mfma_kernel(
                 }
                 f32x16_t x;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], qscale, -L);
+                for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], qscale, nL);
                 if (!(js > i_hi - w && js + 31 <= r0)) {
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
@@ -423,67 +611,113 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_mfma_kernel(
             }
         }
     }
-    // ---- epilogue: dq = s (dq_win + h W_up); h and ol (fp32) for dW_up.
-    // The matrix-core lift runs for the whole wavefront (wave-uniform
-    // condition); only the stores are per row.
-    if (!live) return;
-    if (jd_end >= 0) {
-        bf16x8_t hhi[DS], hlo[DS];  // h as hi + lo bf16: the lift keeps ~16 bits of h
+    __syncthreads();  // the K/V tiles are reused below
+
+    // ---- dq = s (dq_win + h W_up), h from the distant kernel as hi + lo bf16
+    const bool real = live && i < T;
+    const float* hrow = hk + ((size_t)bh * T + ii) * DD;
+    const float* orow = ol + ((size_t)bh * T + ii) * DD;
+    const bool any_dist = live && i_hi - w >= 0;  // wave-uniform
+    if (any_dist) {
+        const bf16_t* wdg = wd + (size_t)g * D * DD;
+        const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
 #pragma unroll
-        for (int s = 0; s < DS; ++s) split8(hT, 8 * s, 1.f, hhi[s], hlo[s]);
+        for (int s = 0; s < DS; ++s) {
+            bf16x8_t hhi, hlo;
+            split_load8(hrow + s * 16 + hg * 8, 1.f, hhi, hlo);
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) {
+                // A[e][c] = W_up[c][e], rows e = 32 tt + qc, c = 16 s + 8 hg + 0..7
+                const int e = tt * 32 + qc, cb = s * 16 + hg * 8;
+                bf16x8_t a;
+                if (wug) {
+                    uint16_t a8[8];
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) a8[u] = wug[(size_t)(cb + u) * D + e];
+                    a = __builtin_bit_cast(bf16x8_t, a8);
+                } else {
+                    a = load_bf16x8(wdg + (size_t)e * DD + cb);
+                }
+                dqT[tt] = mfma(a, hhi, dqT[tt]);
+                dqT[tt] = mfma(a, hlo, dqT[tt]);
+            }
+        }
+    }
+    if (real) {
+        bf16_t* dqr = dq + ((size_t)bh * T + i) * D;
 #pragma unroll
         for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
-            for (int s = 0; s < DS; ++s) {
-                const bf16x8_t a = load_bf16x8(ut + (tt * 32 + qc) * LDU + s * 16 + hg * 8);
-                dqT[tt] = mfma(a, hhi[s], dqT[tt]);
-                dqT[tt] = mfma(a, hlo[s], dqT[tt]);
+            for (int a = 0; a < 4; ++a)
+                store_bf16x4(dqr + tt * 32 + 8 * a + 4 * hg, dqT[tt][4 * a] * scale,
+                             dqT[tt][4 * a + 1] * scale, dqT[tt][4 * a + 2] * scale,
+                             dqT[tt][4 * a + 3] * scale);
+    }
+
+    // ---- share of dW_up^T [e][c] = sum_i q_i[e] s h_i[c] + dO_i[e] ol_i[c]
+    f32x16_t pw[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) pw[t] = splat16(0.f);
+    if (any_dist) {
+        bf16_t* xs = lds_kv + wave * 32 * LDK;  // this wavefront's 32 rows of q, then dO
+        bf16_t* ys = lds_h + wave * 32 * LDH;   // its 32 rows of s h, then ol (bf16, zero padded)
+#pragma unroll
+        for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                *reinterpret_cast<bf16x8_t*>(xs + qc * LDK + s * 16 + hg * 8) = pass ? doop[s] : qop[s];
+            const float* yr = pass ? orow : hrow;
+            const float f = real ? (pass ? 1.f : scale) : 0.f;  // rows past T add nothing
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+                const int c = s * 16 + hg * 8;
+                *reinterpret_cast<bf16x8_t*>(ys + qc * LDH + c) =
+                    (c < DD) ? pack_load8(yr + c, f) : zero_bf16x8();
             }
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                const bf16x8_t bop = lds_tr_operand(ys, LDH, hf * 16, 0, lane);
+#pragma unroll
+                for (int tt = 0; tt < NT; ++tt)
+                    pw[tt] = mfma(lds_tr_operand(xs, LDK, hf * 16, tt * 32, lane), bop, pw[tt]);
+            }
+        }
     }
-    if (i >= T) return;
-    bf16_t* dqr = dq + ((size_t)bh * T + i) * D;
-#pragma unroll
-    for (int tt = 0; tt < NT; ++tt)
-#pragma unroll
-        for (int a = 0; a < 4; ++a)
-            store_bf16x4(dqr + tt * 32 + 8 * a + 4 * hg, dqT[tt][4 * a] * scale,
-                         dqT[tt][4 * a + 1] * scale, dqT[tt][4 * a + 2] * scale,
-                         dqT[tt][4 * a + 3] * scale);
-    float* hr = hk + ((size_t)bh * T + i) * DD;
-    float* orr = ol + ((size_t)bh * T + i) * DD;
-#pragma unroll
-    for (int s = 0; s < DS; ++s) {
-        const int c = 16 * s + 8 * hg;
-        *reinterpret_cast<float4*>(hr + c) = make_float4(hT[8 * s], hT[8 * s + 1], hT[8 * s + 2], hT[8 * s + 3]);
-        *reinterpret_cast<float4*>(hr + c + 4) = make_float4(hT[8 * s + 4], hT[8 * s + 5], hT[8 * s + 6], hT[8 * s + 7]);
-        *reinterpret_cast<float4*>(orr + c) = make_float4(olT[8 * s], olT[8 * s + 1], olT[8 * s + 2], olT[8 * s + 3]);
-        *reinterpret_cast<float4*>(orr + c + 4) = make_float4(olT[8 * s + 4], olT[8 * s + 5], olT[8 * s + 6], olT[8 * s + 7]);
-    }
+    const int chunk = (b * G + h % G) * nblk + rb;
+    wg_share<D, DD, NW>(pw, pbuf, wave, lane, tid,
+                        wpart + (((size_t)Hkv + g) * nchunk + chunk) * D * DD);
 }
 
-// ---------------------------------------------------------------- columns: dk, dv, gK, gV
+// ---------------------------------------------------------------- window: dk, dv, dW_down
 
+// One wavefront per 32 keys, window rows j <= i < j + w of every query head
+// of the group through 64-row Q / dO tiles in LDS. Epilogue: the distant part
+// gK W_down^T, gV W_down^T (hi + lo bf16), and the workgroup's share of
+// dW_down = sum_j k_j^T s gK_j + v_j^T gV_j (chunk b * nkb + key block).
+// Grid: (ceil(T / (32 NW)), B * Hkv).
 template <int D, int DD, int NW>
-__global__ __launch_bounds__(NW * 64) void bwd_cols_mfma_kernel(
+__global__ __launch_bounds__(NW * 64) void bwd_cols_local_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ dout, const bf16_t* __restrict__ wd,
-    const bf16_t* __restrict__ ckb, const bf16_t* __restrict__ cvb,
-    const bf16_t* __restrict__ qts, const bf16_t* __restrict__ qtT,
-    const bf16_t* __restrict__ dts, const bf16_t* __restrict__ dtT,
-    const float* __restrict__ lse, const float* __restrict__ delta, float* __restrict__ gk,
-    float* __restrict__ gv, bf16_t* __restrict__ dk, bf16_t* __restrict__ dv, int Hq, int Hkv,
-    int T, int Tr, int w, float qscale, float scale) {
-    constexpr int KS = D / 16, NT = D / 32, DS = DD / 16, BN = 64, LDK = D + 8;
+    const float* __restrict__ gk, const float* __restrict__ gv, const float* __restrict__ nl2,
+    const float* __restrict__ nd, bf16_t* __restrict__ dk, bf16_t* __restrict__ dv,
+    float* __restrict__ wpart, int Hq, int Hkv, int T, int Tr, int w, float qscale, float scale,
+    int nchunk) {
+    constexpr int KS = D / 16, NT = D / 32, DS = DD / 16, BN = 64, LDK = D + 8, LDH = 40;
     constexpr int BK = NW * 32;
-    __shared__ __attribute__((aligned(16))) bf16_t lds_q[BN * LDK];
-    __shared__ __attribute__((aligned(16))) bf16_t lds_do[BN * LDK];
-    __shared__ __attribute__((aligned(16))) float lds_lse[BN];
-    __shared__ __attribute__((aligned(16))) float lds_del[BN];
+    __shared__ __attribute__((aligned(16))) bf16_t lds_qd[2 * BN * LDK];  // Q tile, dO tile
+    __shared__ __attribute__((aligned(16))) float lds_lse[BN];  // -lse (log2 units)
+    __shared__ __attribute__((aligned(16))) float lds_del[BN];  // -delta
+    __shared__ __attribute__((aligned(16))) bf16_t lds_g[NW * 32 * LDH];
+    __shared__ __attribute__((aligned(16))) float pbuf[D * DD];
+    bf16_t* lds_q = lds_qd;
+    bf16_t* lds_do = lds_qd + BN * LDK;
 
-    const int tid = threadIdx.x, lane = tid & 63;
+    const int tid = lane_id_x(), lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int cb = blockIdx.x;  // key block 0 (most rows) first
-    const int bg = blockIdx.y;
+    const int cb = wg_id_x();
+    const int nkb = (T + BK - 1) / BK;
+    const int bg = wg_id_y();
     const int b = bg / Hkv, g = bg % Hkv;
     const int G = Hq / Hkv;
     const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
@@ -493,11 +727,8 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_mfma_kernel(
     const int j_hi = imin(c0 + 31, T - 1);
     const int cwg_hi = imin(cwg_lo + BK - 1, T - 1);
     const int jj = imin(j, T - 1);
-    const int T32 = Tr / 32;
 
-    // B operands of the key column: S = Q K^T, dP = dO V^T and the distant
-    // forms with c^K, c^V.
-    bf16x8_t kop[KS], vop[KS], ckop[DS], cvop[DS];
+    bf16x8_t kop[KS], vop[KS];
     const bf16_t* krow = k + ((size_t)bg * T + jj) * D;
     const bf16_t* vrow = v + ((size_t)bg * T + jj) * D;
 #pragma unroll
@@ -505,46 +736,35 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_mfma_kernel(
         kop[s] = load_bf16x8(krow + s * 16 + hg * 8);
         vop[s] = load_bf16x8(vrow + s * 16 + hg * 8);
     }
-#pragma unroll
-    for (int s = 0; s < DS; ++s) {
-        ckop[s] = load_bf16x8(ckb + ((size_t)bg * Tr + jj) * DD + s * 16 + hg * 8);
-        cvop[s] = load_bf16x8(cvb + ((size_t)bg * Tr + jj) * DD + s * 16 + hg * 8);
-    }
-
     f32x16_t dkT[NT], dvT[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) { dkT[t] = splat16(0.f); dvT[t] = splat16(0.f); }
-    f32x16_t gkT = splat16(0.f), gvT = splat16(0.f);
     const int loc_hi = w > 0 ? imin(T - 1, cwg_hi + w - 1) : -1;  // last row with a window pair
 
     for (int hh = 0; hh < G; ++hh) {
         const int bh = b * Hq + g * G + hh;
         const bf16_t* qh = q + (size_t)bh * T * D;
         const bf16_t* dh = dout + (size_t)bh * T * D;
-        const float* lh = lse + (size_t)bh * Tr;
-        const float* delh = delta + (size_t)bh * Tr;
-
-        // window rows: 64-row Q / dO tiles staged in LDS for the workgroup
+        const float* lh = nl2 + (size_t)bh * Tr;
+        const float* dlh = nd + (size_t)bh * Tr;
         for (int t = cwg_lo; t <= loc_hi; t += BN) {
             __syncthreads();
-            {
-                constexpr int C8 = D / 8;
-                for (int idx = tid; idx < BN * C8; idx += NW * 64) {
-                    const int r = idx / C8, c8 = idx % C8;
-                    const int row = t + r;
-                    uint4 uq = make_uint4(0, 0, 0, 0), ud = make_uint4(0, 0, 0, 0);
-                    if (row < T) {
-                        uq = *reinterpret_cast<const uint4*>(qh + (size_t)row * D + c8 * 8);
-                        ud = *reinterpret_cast<const uint4*>(dh + (size_t)row * D + c8 * 8);
-                    }
-                    *reinterpret_cast<uint4*>(lds_q + r * LDK + c8 * 8) = uq;
-                    *reinterpret_cast<uint4*>(lds_do + r * LDK + c8 * 8) = ud;
+            constexpr int C8 = D / 8;
+            for (int idx = tid; idx < BN * C8; idx += NW * 64) {
+                const int r = idx / C8, c8 = idx % C8;
+                const int row = t + r;
+                uint4 uq = make_uint4(0, 0, 0, 0), ud = make_uint4(0, 0, 0, 0);
+                if (row < T) {
+                    uq = *reinterpret_cast<const uint4*>(qh + (size_t)row * D + c8 * 8);
+                    ud = *reinterpret_cast<const uint4*>(dh + (size_t)row * D + c8 * 8);
                 }
-                for (int r = tid; r < BN; r += NW * 64) {
-                    const bool in = t + r < Tr;
-                    lds_lse[r] = in ? lh[t + r] : 0.f;
-                    lds_del[r] = in ? delh[t + r] : 0.f;
-                }
+                *reinterpret_cast<uint4*>(lds_q + r * LDK + c8 * 8) = uq;
+                *reinterpret_cast<uint4*>(lds_do + r * LDK + c8 * 8) = ud;
+            }
+            for (int r = tid; r < BN; r += NW * 64) {
+                const bool in = t + r < Tr;
+                lds_lse[r] = in ? lh[t + r] : 0.f;
+                lds_del[r] = in ? dlh[t + r] : 0.f;
             }
             __syncthreads();
             if (!live) continue;
@@ -553,7 +773,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_mfma_kernel(
                 const int is = t + sub * 32;
                 if (is + 31 < c0 || is > j_hi + w - 1) continue;
                 f32x16_t sc = splat16(0.f);
-                f32x16_t dp = load_row16(lds_del + sub * 32, hg, -1.f);
+                f32x16_t dp = load_row16(lds_del + sub * 32, hg, 1.f);
 #pragma unroll
                 for (int s = 0; s < KS; ++s) {
                     sc = mfma(load_bf16x8(lds_q + (sub * 32 + prow) * LDK + s * 16 + hg * 8), kop[s], sc);
@@ -562,7 +782,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_mfma_kernel(
                 const f32x16_t ln = load_row16(lds_lse + sub * 32, hg, 1.f);
                 f32x16_t x;
 #pragma unroll
-                for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], qscale, -ln[r]);
+                for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], qscale, ln[r]);
                 if (!(is >= c0 + 31 && is + 31 - c0 < w && is + 31 < T)) {
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
@@ -587,104 +807,80 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_mfma_kernel(
                 }
             }
         }
+    }
+    __syncthreads();  // the Q/dO tiles are reused below
 
-        // distant rows i >= j + w, straight from L2 for each wavefront
-        if (live) {
-            const bf16_t* qth = qts + (size_t)bh * Tr * DD;
-            const bf16_t* dth = dts + (size_t)bh * Tr * DD;
-            const bf16_t* qtTh = qtT + (size_t)bh * T32 * DD * 32;
-            const bf16_t* dtTh = dtT + (size_t)bh * T32 * DD * 32;
-            for (int is = (c0 + w) & ~31; is < T; is += 32) {
-                const bf16_t* ar = qth + (size_t)(is + prow) * DD + hg * 8;
-                const bf16_t* dr = dth + (size_t)(is + prow) * DD + hg * 8;
-                f32x16_t x = mfma(load_bf16x8(ar), ckop[0], load_row16(lh + is, hg, -1.f));
-                f32x16_t dp = mfma(load_bf16x8(dr), cvop[0], load_row16(delh + is, hg, -1.f));
-                if (DS == 2) {
-                    x = mfma(load_bf16x8(ar + 16), ckop[DS - 1], x);
-                    dp = mfma(load_bf16x8(dr + 16), cvop[DS - 1], dp);
-                }
-                if (!(is >= c0 + 31 + w && is + 31 < T)) {
-#pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int i = is + acc_row(r, hg);
-                        if (i - j < w || i >= T) x[r] = -INFINITY;
-                    }
-                }
-                f32x16_t p, ds;
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    p[r] = __builtin_amdgcn_exp2f(x[r]);
-                    ds[r] = p[r] * dp[r];
-                }
-                const bf16x8_t p0 = pack8(p, 0), p1 = pack8(p, 8);
-                const bf16x8_t s0 = pack8(ds, 0), s1 = pack8(ds, 8);
-                const bf16_t* qblk = qtTh + (size_t)(is >> 5) * DD * 32;
-                const bf16_t* dblk = dtTh + (size_t)(is >> 5) * DD * 32;
-                gkT = mfma(latT_operand<DD>(qblk, qc, hg, 0), s0, gkT);
-                gkT = mfma(latT_operand<DD>(qblk, qc, hg, 1), s1, gkT);
-                gvT = mfma(latT_operand<DD>(dblk, qc, hg, 0), p0, gvT);
-                gvT = mfma(latT_operand<DD>(dblk, qc, hg, 1), p1, gvT);
-            }
-        }
-    }
-    // ---- epilogue: dk = s dk_win + (s gK) W_down^T, dv = dv_win + gV W_down^T,
-    // with gK = sum dS q~ (q~ unscaled: the operand above carried qscale).
-    // The matrix-core lift runs for the whole wavefront (wave-uniform
-    // condition; keys without distant rows have gK = gV = 0).
-    if (!live) return;
-    const float gscale = 1.f / qscale;
+    // ---- dk = s dk_win + (s gK) W_down^T, dv = dv_win + gV W_down^T
+    const bool real = live && j < T;
     const bf16_t* wdg = wd + (size_t)g * D * DD;
-    if (c0 + w < T) {
-        // gK and gV as hi + lo bf16 pairs: the lift keeps ~16 bits of them
-        bf16x8_t gkh[DS], gkl[DS], gvh[DS], gvl[DS];
-#pragma unroll
-        for (int s = 0; s < DS; ++s) {
-            split8(gkT, 8 * s, gscale * scale, gkh[s], gkl[s]);
-            split8(gvT, 8 * s, 1.f, gvh[s], gvl[s]);
-        }
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) dkT[tt][r] *= scale;
-#pragma unroll
-            for (int s = 0; s < DS; ++s) {
-                const bf16x8_t a = load_bf16x8(wdg + (size_t)(tt * 32 + qc) * DD + s * 16 + hg * 8);
-                dkT[tt] = mfma(a, gkh[s], dkT[tt]);
-                dkT[tt] = mfma(a, gkl[s], dkT[tt]);
-                dvT[tt] = mfma(a, gvh[s], dvT[tt]);
-                dvT[tt] = mfma(a, gvl[s], dvT[tt]);
-            }
-        }
-    } else {
-#pragma unroll
-        for (int tt = 0; tt < NT; ++tt)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) dkT[tt][r] *= scale;
-    }
-    if (j >= T) return;
-    bf16_t* dkr = dk + ((size_t)bg * T + j) * D;
-    bf16_t* dvr = dv + ((size_t)bg * T + j) * D;
+    const float* gkr = gk + ((size_t)bg * T + jj) * DD;
+    const float* gvr = gv + ((size_t)bg * T + jj) * DD;
+    const bool any_dist = live && c0 + w < T;  // wave-uniform
 #pragma unroll
     for (int tt = 0; tt < NT; ++tt)
 #pragma unroll
-        for (int a = 0; a < 4; ++a) {
-            store_bf16x4(dkr + tt * 32 + 8 * a + 4 * hg, dkT[tt][4 * a], dkT[tt][4 * a + 1],
-                         dkT[tt][4 * a + 2], dkT[tt][4 * a + 3]);
-            store_bf16x4(dvr + tt * 32 + 8 * a + 4 * hg, dvT[tt][4 * a], dvT[tt][4 * a + 1],
-                         dvT[tt][4 * a + 2], dvT[tt][4 * a + 3]);
-        }
-    float* gkr = gk + ((size_t)bg * T + j) * DD;
-    float* gvr = gv + ((size_t)bg * T + j) * DD;
+        for (int r = 0; r < 16; ++r) dkT[tt][r] *= scale;
+    if (any_dist) {
 #pragma unroll
-    for (int s = 0; s < DS; ++s) {
-        const int c = 16 * s + 8 * hg;
-        *reinterpret_cast<float4*>(gkr + c) =
-            make_float4(gkT[8 * s] * gscale, gkT[8 * s + 1] * gscale, gkT[8 * s + 2] * gscale, gkT[8 * s + 3] * gscale);
-        *reinterpret_cast<float4*>(gkr + c + 4) =
-            make_float4(gkT[8 * s + 4] * gscale, gkT[8 * s + 5] * gscale, gkT[8 * s + 6] * gscale, gkT[8 * s + 7] * gscale);
-        *reinterpret_cast<float4*>(gvr + c) = make_float4(gvT[8 * s], gvT[8 * s + 1], gvT[8 * s + 2], gvT[8 * s + 3]);
-        *reinterpret_cast<float4*>(gvr + c + 4) = make_float4(gvT[8 * s + 4], gvT[8 * s + 5], gvT[8 * s + 6], gvT[8 * s + 7]);
+        for (int s = 0; s < DS; ++s) {
+            bf16x8_t khi, klo, vhi, vlo;
+            split_load8(gkr + s * 16 + hg * 8, scale, khi, klo);
+            split_load8(gvr + s * 16 + hg * 8, 1.f, vhi, vlo);
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) {
+                const bf16x8_t a = load_bf16x8(wdg + (size_t)(tt * 32 + qc) * DD + s * 16 + hg * 8);
+                dkT[tt] = mfma(a, khi, dkT[tt]);
+                dkT[tt] = mfma(a, klo, dkT[tt]);
+                dvT[tt] = mfma(a, vhi, dvT[tt]);
+                dvT[tt] = mfma(a, vlo, dvT[tt]);
+            }
+        }
     }
+    if (real) {
+        bf16_t* dkr = dk + ((size_t)bg * T + j) * D;
+        bf16_t* dvr = dv + ((size_t)bg * T + j) * D;
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+            for (int a = 0; a < 4; ++a) {
+                store_bf16x4(dkr + tt * 32 + 8 * a + 4 * hg, dkT[tt][4 * a], dkT[tt][4 * a + 1],
+                             dkT[tt][4 * a + 2], dkT[tt][4 * a + 3]);
+                store_bf16x4(dvr + tt * 32 + 8 * a + 4 * hg, dvT[tt][4 * a], dvT[tt][4 * a + 1],
+                             dvT[tt][4 * a + 2], dvT[tt][4 * a + 3]);
+            }
+    }
+
+    // ---- share of dW_down [e][c] = sum_j k_j[e] s gK_j[c] + v_j[e] gV_j[c]
+    f32x16_t pw[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) pw[t] = splat16(0.f);
+    if (any_dist) {
+        bf16_t* xs = lds_qd + wave * 32 * LDK;  // this wavefront's 32 keys, then values
+        bf16_t* ys = lds_g + wave * 32 * LDH;   // s gK, then gV (bf16, zero padded)
+#pragma unroll
+        for (int pass = 0; pass < 2; ++pass) {
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                *reinterpret_cast<bf16x8_t*>(xs + qc * LDK + s * 16 + hg * 8) = pass ? vop[s] : kop[s];
+            const float* yr = pass ? gvr : gkr;
+            const float f = real ? (pass ? 1.f : scale) : 0.f;  // keys past T add nothing
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+                const int c = s * 16 + hg * 8;
+                *reinterpret_cast<bf16x8_t*>(ys + qc * LDH + c) =
+                    (c < DD) ? pack_load8(yr + c, f) : zero_bf16x8();
+            }
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) {
+                const bf16x8_t bop = lds_tr_operand(ys, LDH, hf * 16, 0, lane);
+#pragma unroll
+                for (int tt = 0; tt < NT; ++tt)
+                    pw[tt] = mfma(lds_tr_operand(xs, LDK, hf * 16, tt * 32, lane), bop, pw[tt]);
+            }
+        }
+    }
+    wg_share<D, DD, NW>(pw, pbuf, wave, lane, tid,
+                        wpart + ((size_t)g * nchunk + b * nkb + cb) * D * DD);
 }
 
 // ---------------------------------------------------------------- host
@@ -695,15 +891,16 @@ bool bwd_mfma_supported(int d, int dd, bool bf16) {
 
 template <int D, int DD>
 static hipError_t launch_bwd_mfma_t(const bf16_t* q, const bf16_t* k, const bf16_t* v,
-                                    const bf16_t* o, const bf16_t* dout, const bf16_t* wd,
-                                    const bf16_t* wu, bf16_t* dq, bf16_t* dk, bf16_t* dv,
-                                    float* dwd, float* dwu, char* ws, const BwdWs& L, int B,
-                                    int Hq, int Hkv, int T, int w, hipStream_t st) {
+                                    const bf16_t* o, const float* lse, const bf16_t* dout,
+                                    const bf16_t* wd, const bf16_t* wu, bf16_t* dq, bf16_t* dk,
+                                    bf16_t* dv, float* dwd, float* dwu, char* ws, const BwdWs& L,
+                                    int B, int Hq, int Hkv, int T, int w, hipStream_t st) {
     constexpr int NW = 4;
     const int Tr = round_up(T, 32);
-    const size_t nrow = (size_t)B * Hq * Tr * DD, ntok = (size_t)B * Hkv * Tr * DD;
-    float* lse = (float*)(ws + L.lse_off);
-    float* delta = (float*)(ws + L.delta_off);
+    const size_t nrow = (size_t)B * Hq * Tr * DD, ntok = (size_t)B * Hkv * Tr * DD;  // bf16
+    float* nl2 = (float*)(ws + L.lse_off);
+    float* nd = (float*)(ws + L.delta_off);
+    bf16_t* rc = (bf16_t*)(ws + L.rc_off);
     bf16_t* qts = (bf16_t*)(ws + L.qt_off);
     bf16_t* qtT = qts + nrow;
     bf16_t* dts = (bf16_t*)(ws + L.dot_off);
@@ -719,37 +916,43 @@ static hipError_t launch_bwd_mfma_t(const bf16_t* q, const bf16_t* k, const bf16
     float* part = (float*)(ws + L.wpart_off);
     const float scale = 1.f / sqrtf((float)D);
     const float qscale = scale * kLog2eB;
+    const int nblk = (T + NW * 32 - 1) / (NW * 32);
 
     hipLaunchKernelGGL((bwd_prep_rows_kernel<D, DD>), dim3((Tr + 255) / 256, B * Hq), dim3(256), 0,
-                       st, q, o, dout, wd, wu, qts, qtT, dts, dtT, delta, Hq, Hkv, T, Tr, qscale);
+                       st, q, o, dout, lse, wd, wu, qts, qtT, dts, dtT, rc, nd, nl2, Hq, Hkv, T, Tr,
+                       qscale);
     hipLaunchKernelGGL((bwd_prep_keys_kernel<D, DD>), dim3((Tr + 255) / 256, B * Hkv), dim3(256),
                        0, st, k, v, wd, ckb, ckT, cvb, cvT, Hkv, T, Tr);
-    const int nblk = (T + NW * 32 - 1) / (NW * 32);
-    hipLaunchKernelGGL((bwd_rows_mfma_kernel<D, DD, NW>), dim3(nblk, B * Hq), dim3(NW * 64), 0, st,
-                       q, k, v, dout, wd, wu, (const bf16_t*)ckb, (const bf16_t*)ckT,
-                       (const bf16_t*)cvb, (const bf16_t*)cvT, (const bf16_t*)qts,
-                       (const bf16_t*)dts, (const float*)delta, lse, hk, ol, dq, Hq, Hkv, T, Tr, w,
-                       qscale, scale);
-    hipLaunchKernelGGL((bwd_cols_mfma_kernel<D, DD, NW>), dim3(nblk, B * Hkv), dim3(NW * 64), 0,
-                       st, q, k, v, dout, wd, (const bf16_t*)ckb, (const bf16_t*)cvb,
-                       (const bf16_t*)qts, (const bf16_t*)qtT, (const bf16_t*)dts,
-                       (const bf16_t*)dtT, (const float*)lse, (const float*)delta, gk, gv, dk, dv,
-                       Hq, Hkv, T, Tr, w, qscale, scale);
+    hipLaunchKernelGGL((bwd_rows_dist_kernel<DD, NW>), dim3(nblk, B * Hq), dim3(NW * 64), 0, st,
+                       (const bf16_t*)ckb, (const bf16_t*)ckT, (const bf16_t*)cvb,
+                       (const bf16_t*)cvT, (const bf16_t*)qts, (const bf16_t*)dts,
+                       (const float*)nl2, (const float*)nd, hk, ol, Hq, Hkv, T, Tr, w);
+    hipLaunchKernelGGL((bwd_cols_dist_kernel<DD, NW>), dim3(nblk, B * Hkv), dim3(NW * 64), 0, st,
+                       (const bf16_t*)ckb, (const bf16_t*)cvb, (const bf16_t*)qts,
+                       (const bf16_t*)qtT, (const bf16_t*)dts, (const bf16_t*)dtT,
+                       (const bf16_t*)rc, gk, gv, Hq, Hkv, T, Tr, w, 1.f / qscale);
+    hipLaunchKernelGGL((bwd_rows_local_kernel<D, DD, NW>), dim3(nblk, B * Hq), dim3(NW * 64), 0,
+                       st, q, k, v, dout, wd, wu, (const float*)hk, (const float*)ol,
+                       (const float*)nl2, (const float*)nd, dq, part, Hq, Hkv, T, Tr, w,
+                       qscale, scale, L.nchunk);
+    hipLaunchKernelGGL((bwd_cols_local_kernel<D, DD, NW>), dim3(nblk, B * Hkv), dim3(NW * 64), 0,
+                       st, q, k, v, dout, wd, (const float*)gk, (const float*)gv,
+                       (const float*)nl2, (const float*)nd, dk, dv, part, Hq, Hkv, T, Tr, w,
+                       qscale, scale, L.nchunk);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    return launch_bwd_weights<bf16_t>(q, k, v, dout, gk, gv, hk, ol, part, dwd, dwu, B, Hq, Hkv, T,
-                                      D, DD, L, st);
+    return launch_bwd_wreduce(part, dwd, dwu, Hkv, D, DD, L, st);
 }
 
 hipError_t launch_bwd_mfma(const bf16_t* q, const bf16_t* k, const bf16_t* v, const bf16_t* o,
-                           const bf16_t* dout, const bf16_t* wd, const bf16_t* wu, bf16_t* dq,
-                           bf16_t* dk, bf16_t* dv, float* dwd, float* dwu, char* ws,
-                           const BwdWs& L, int B, int Hq, int Hkv, int T, int d, int dd, int w,
-                           hipStream_t st) {
+                           const float* lse, const bf16_t* dout, const bf16_t* wd,
+                           const bf16_t* wu, bf16_t* dq, bf16_t* dk, bf16_t* dv, float* dwd,
+                           float* dwu, char* ws, const BwdWs& L, int B, int Hq, int Hkv, int T,
+                           int d, int dd, int w, hipStream_t st) {
 #define DAR_BWD_CASE(D_, DD_)                                                                   \
     if (d == D_ && dd == DD_)                                                                   \
-        return launch_bwd_mfma_t<D_, DD_>(q, k, v, o, dout, wd, wu, dq, dk, dv, dwd, dwu, ws, L, \
-                                          B, Hq, Hkv, T, w, st);
+        return launch_bwd_mfma_t<D_, DD_>(q, k, v, o, lse, dout, wd, wu, dq, dk, dv, dwd, dwu,  \
+                                          ws, L, B, Hq, Hkv, T, w, st);
     DAR_BWD_CASE(64, 16)
     DAR_BWD_CASE(64, 32)
     DAR_BWD_CASE(128, 16)

@@ -29,7 +29,7 @@ PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize) 
 // library; the generic path handles everything the fast one does not.
 bool prefill_mfma_supported(const dar_shape* s);
 hipError_t launch_prefill_mfma(const dar_shape* s, int T, const void* q, const void* k,
-                               const void* v, const void* wd, const void* wu, void* o,
+                               const void* v, const void* wd, const void* wu, void* o, float* lse,
                                const void* cK, const void* cVt, const float* cnorm,
                                const float* knorm, const void* consts, hipStream_t st);
 
@@ -111,17 +111,21 @@ size_t dar_decode_workspace_bytes(const dar_shape* s, int cap) {
 
 size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T) {
     if (check_shape(s) != DAR_OK || T < 1) return 0;
-    return bwd_ws_layout(s->B, s->Hq, s->Hkv, T, s->d, s->d_down).bytes;
+    // enough for either kernel family (DAR_BWD_VALU may pick the generic one)
+    const size_t a = bwd_ws_layout(s->B, s->Hq, s->Hkv, T, s->d, s->d_down, false).bytes;
+    const size_t b = bwd_ws_layout(s->B, s->Hq, s->Hkv, T, s->d, s->d_down, true).bytes;
+    return a > b ? a : b;
 }
 
 dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void* k,
                             const void* v, const void* w_down, const void* w_up, void* o,
-                            void* ws, size_t ws_bytes, hipStream_t stream) {
+                            float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
     dar_status st = check_shape(s);
     if (st != DAR_OK) return st;
     if (T < 1) return DAR_E_ARG;
     if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(w_down) || !dev_ok(o)) return DAR_E_ARG;
     if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if (lse && !aligned16(lse)) return DAR_E_ARG;
     const PrefillWs L = prefill_ws_layout(s->B, s->Hkv, T, s->d_down, s->w, esize_of(s->dtype));
     if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
     if (!aligned16(ws)) return DAR_E_ARG;
@@ -146,14 +150,14 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
                                           s->d_down, s->w, fast, stream);
         if (e == hipSuccess) {
             if (fast)
-                e = launch_prefill_mfma(s, T, q, k, v, w_down, w_up, o, cK, cV, cnorm, knorm, consts,
-                                       stream);
+                e = launch_prefill_mfma(s, T, q, k, v, w_down, w_up, o, lse, cK, cV, cnorm, knorm,
+                                        consts, stream);
             else
                 e = launch_prefill_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k,
                                                 (const bf16_t*)v, (const bf16_t*)w_down,
                                                 (const bf16_t*)w_up, (const bf16_t*)cK,
-                                                (const bf16_t*)cV, (bf16_t*)o, s->B, s->Hq,
-                                                s->Hkv, T, s->d, s->d_down, s->w, stream);
+                                                (const bf16_t*)cV, (bf16_t*)o, lse, s->B,
+                                                s->Hq, s->Hkv, T, s->d, s->d_down, s->w, stream);
         }
     } else {
         e = launch_prefill_latent<float>((const float*)k, (const float*)v, (const float*)w_down,
@@ -162,29 +166,30 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
         if (e == hipSuccess)
             e = launch_prefill_valu<float>((const float*)q, (const float*)k, (const float*)v,
                                            (const float*)w_down, (const float*)w_up,
-                                           (const float*)cK, (const float*)cV, (float*)o, s->B,
-                                           s->Hq, s->Hkv, T, s->d, s->d_down, s->w, stream);
+                                           (const float*)cK, (const float*)cV, (float*)o, lse,
+                                           s->B, s->Hq, s->Hkv, T, s->d, s->d_down, s->w, stream);
     }
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 
 dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, const void* k,
                                      const void* v, const void* w_down, const void* w_up,
-                                     const void* o, const void* dout, void* dq, void* dk,
-                                     void* dv, float* dw_down, float* dw_up, void* ws,
+                                     const void* o, const float* lse, const void* dout, void* dq,
+                                     void* dk, void* dv, float* dw_down, float* dw_up, void* ws,
                                      size_t ws_bytes, hipStream_t stream) {
     dar_status st = check_shape(s);
     if (st != DAR_OK) return st;
     if (T < 1) return DAR_E_ARG;
-    if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(w_down) || !dev_ok(o) || !dev_ok(dout))
+    if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(w_down) || !dev_ok(o) || !dev_ok(dout) ||
+        !dev_ok(lse))
         return DAR_E_ARG;
     if (!dev_ok(dq) || !dev_ok(dk) || !dev_ok(dv) || !dev_ok(dw_down)) return DAR_E_ARG;
     if (w_up && !aligned16(w_up)) return DAR_E_ARG;
     if ((w_up == nullptr) != (dw_up == nullptr)) return DAR_E_ARG;
     if (dw_up && !aligned16(dw_up)) return DAR_E_ARG;
     if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
-    const BwdWs L = bwd_ws_layout(s->B, s->Hq, s->Hkv, T, s->d, s->d_down);
-    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (ws == nullptr || ws_bytes < dar_prefill_backward_workspace_bytes(s, T))
+        return DAR_E_WORKSPACE;
     if (!aligned16(ws)) return DAR_E_ARG;
 
     clear_hip_error();
@@ -196,20 +201,21 @@ dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, c
     hipError_t e;
     const bool fast = bwd_mfma_supported(s->d, s->d_down, s->dtype == DAR_BF16) &&
                       !env_flag("DAR_BWD_VALU");
+    const BwdWs L = bwd_ws_layout(s->B, s->Hq, s->Hkv, T, s->d, s->d_down, fast);
     if (fast)
         e = launch_bwd_mfma((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)o,
-                            (const bf16_t*)dout, (const bf16_t*)w_down, (const bf16_t*)w_up,
+                            lse, (const bf16_t*)dout, (const bf16_t*)w_down, (const bf16_t*)w_up,
                             (bf16_t*)dq, (bf16_t*)dk, (bf16_t*)dv, dw_down, dw_up, (char*)ws, L,
                             s->B, s->Hq, s->Hkv, T, s->d, s->d_down, s->w, stream);
     else if (s->dtype == DAR_BF16)
         e = launch_bwd_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v,
-                                    (const bf16_t*)o, (const bf16_t*)dout, (const bf16_t*)w_down,
+                                    (const bf16_t*)o, lse, (const bf16_t*)dout, (const bf16_t*)w_down,
                                     (const bf16_t*)w_up, (bf16_t*)dq, (bf16_t*)dk, (bf16_t*)dv,
                                     dw_down, dw_up, (char*)ws, L, s->B, s->Hq, s->Hkv, T, s->d,
                                     s->d_down, s->w, stream);
     else
         e = launch_bwd_valu<float>((const float*)q, (const float*)k, (const float*)v,
-                                   (const float*)o, (const float*)dout, (const float*)w_down,
+                                   (const float*)o, lse, (const float*)dout, (const float*)w_down,
                                    (const float*)w_up, (float*)dq, (float*)dk, (float*)dv,
                                    dw_down, dw_up, (char*)ws, L, s->B, s->Hq, s->Hkv, T, s->d,
                                    s->d_down, s->w, stream);

@@ -96,6 +96,16 @@ __host__ __device__ inline int latent_pos(int c) {
     return (c & ~15) | (qq << 2) | (c & 3);
 }
 
+// Workgroup and work-item indices read from the hardware registers. The
+// blockIdx / threadIdx accessors go through device-library functions, which
+// the compiler does not inline into code built with IEEE mode off
+// (-mno-amdgpu-ieee): they become calls, and the workgroup index then lives
+// in a vector register, so everything derived from it looks divergent.
+__device__ __forceinline__ int wg_id_x() { return (int)__builtin_amdgcn_workgroup_id_x(); }
+__device__ __forceinline__ int wg_id_y() { return (int)__builtin_amdgcn_workgroup_id_y(); }
+__device__ __forceinline__ int wg_id_z() { return (int)__builtin_amdgcn_workgroup_id_z(); }
+__device__ __forceinline__ int lane_id_x() { return (int)__builtin_amdgcn_workitem_id_x(); }
+
 __device__ __forceinline__ int imin(int a, int b) { return a < b ? a : b; }
 __device__ __forceinline__ int imax(int a, int b) { return a > b ? a : b; }
 

@@ -59,8 +59,8 @@ hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, 
 
 template <typename T>
 hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, const T* wu,
-                               const T* cK, const T* cVt, T* o, int B, int Hq, int Hkv, int T_,
-                               int d, int dd, int w, hipStream_t st);
+                               const T* cK, const T* cVt, T* o, float* lse, int B, int Hq,
+                               int Hkv, int T_, int d, int dd, int w, hipStream_t st);
 
 // Matrix-core decode (bf16, d in {64,128}, d_down in {16,32}, <= 8 query heads
 // per KV head); shares decode_combine_kernel with the vector-ALU path.
@@ -77,18 +77,22 @@ hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, c
                          int d, int dd, int w, int cap, int len, hipStream_t st);
 
 // Prefill backward workspace (256-byte aligned parts; Tr = round_up(T, 32)):
-//   lse, delta        [B*Hq][Tr] fp32     log2-domain log-sum-exp of each row; dO . O
-//   qt, dot           [B*Hq][Tr][dd] fp32 q W_up^T, dO W_up^T (matrix-core path: the
-//                                         bf16 row-major array, then the bf16
-//                                         transposed 32-row blocks)
+//   lse, delta        [B*Hq][Tr] fp32     dO . O per row (matrix-core path: -lse in
+//                                         log2 units and -delta)
+//   qt, dot           [B*Hq][Tr]          q W_up^T, dO W_up^T: fp32 [dd] per row, or
+//                                         on the matrix-core path bf16 [dd] per row
+//                                         followed by transposed blocks [Tr/32][32][32]
+//                                         (latent rows past dd are zero)
+//   rc                [B*Hq][Tr][16] bf16 matrix-core path: -lse and -delta, each as a
+//                                         hi + mid + lo bf16 triple (row constants)
 //   hk, ol            [B*Hq][T][dd] fp32  sum dS c^K, sum P c^V per row
-//   ck, cv            [B*Hkv][Tr][dd] fp32 latents (matrix-core path: as qt)
+//   ck, cv            [B*Hkv][Tr]         latents, laid out as qt
 //   gk, gv            [B*Hkv][T][dd] fp32 sum dS q~, sum P dO~ per key
 //   wpart             [2][Hkv][nchunk][d][dd]  weight-gradient partials per chunk
 // (each array region is sized for Tr tokens).
 struct BwdWs {
-    size_t lse_off, delta_off, qt_off, dot_off, hk_off, ol_off, ck_off, cv_off, gk_off, gv_off,
-        wpart_off, bytes;
+    size_t lse_off, delta_off, qt_off, dot_off, rc_off, hk_off, ol_off, ck_off, cv_off, gk_off,
+        gv_off, wpart_off, bytes;
     int nchunk_d, nchunk_u, nchunk;
 };
 // Row chunks of the weight-gradient reduction: about 256 rows each, at most 128.
@@ -96,7 +100,11 @@ static inline int bwd_nchunk(long long rows) {
     long long n = (rows + 255) / 256;
     return (int)(n < 1 ? 1 : (n > 128 ? 128 : n));
 }
-BwdWs bwd_ws_layout(int B, int Hq, int Hkv, int T, int d, int dd);
+// mfma: chunks of the weight-gradient shares are the matrix-core kernels'
+// workgroups (else row chunks of the vector-ALU reduction).
+BwdWs bwd_ws_layout(int B, int Hq, int Hkv, int T, int d, int dd, bool mfma);
+hipError_t launch_bwd_wreduce(const float* part, float* dwd, float* dwu, int Hkv, int d, int dd,
+                              const BwdWs& L, hipStream_t st);
 
 template <typename T>
 hipError_t launch_bwd_prep(const T* q, const T* k, const T* v, const T* o, const T* dout,
@@ -111,14 +119,14 @@ hipError_t launch_bwd_weights(const T* q, const T* k, const T* v, const T* dout,
 // Matrix-core backward (bf16, d in {64, 128}, d_down in {16, 32}).
 bool bwd_mfma_supported(int d, int dd, bool bf16);
 hipError_t launch_bwd_mfma(const bf16_t* q, const bf16_t* k, const bf16_t* v, const bf16_t* o,
-                           const bf16_t* dout, const bf16_t* wd, const bf16_t* wu, bf16_t* dq,
-                           bf16_t* dk, bf16_t* dv, float* dwd, float* dwu, char* ws,
-                           const BwdWs& L, int B, int Hq, int Hkv, int T, int d, int dd, int w,
-                           hipStream_t st);
+                           const float* lse, const bf16_t* dout, const bf16_t* wd,
+                           const bf16_t* wu, bf16_t* dq, bf16_t* dk, bf16_t* dv, float* dwd,
+                           float* dwu, char* ws, const BwdWs& L, int B, int Hq, int Hkv, int T,
+                           int d, int dd, int w, hipStream_t st);
 template <typename T>
-hipError_t launch_bwd_valu(const T* q, const T* k, const T* v, const T* o, const T* dout,
-                           const T* wd, const T* wu, T* dq, T* dk, T* dv, float* dwd, float* dwu,
-                           char* ws, const BwdWs& L, int B, int Hq, int Hkv, int T_, int d, int dd,
-                           int w, hipStream_t st);
+hipError_t launch_bwd_valu(const T* q, const T* k, const T* v, const T* o, const float* lse,
+                           const T* dout, const T* wd, const T* wu, T* dq, T* dk, T* dv,
+                           float* dwd, float* dwu, char* ws, const BwdWs& L, int B, int Hq,
+                           int Hkv, int T_, int d, int dd, int w, hipStream_t st);
 
 }  // namespace dar

@@ -78,10 +78,10 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
     // after pass 2 the score buffer holds the cross-wave partial sums
     float (*red)[G][256] = reinterpret_cast<float (*)[G][256]>(ssh);
 
-    const int s = blockIdx.x;
-    const int bg = blockIdx.y;
+    const int s = wg_id_x();
+    const int bg = wg_id_y();
     const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
-    const int tid = threadIdx.x;
+    const int tid = lane_id_x();
     const int lane = tid & 63, wave = tid >> 6;
     const int n_lat = imax(0, len - w);
     const bool latent = s < n_lat_split;
@@ -250,10 +250,10 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
     const float* __restrict__ part, const T* __restrict__ wd, const T* __restrict__ wu,
     T* __restrict__ o, int Hq, int Hkv, int d, int dd, int S) {
     constexpr int kLiftCols = 32;  // W_up rows held in registers (d_down <= 32, d <= 64)
-    const int bh = blockIdx.x;
+    const int bh = wg_id_x();
     const int h = bh % Hq;
     const int g = h / (Hq / Hkv);
-    const int lane = threadIdx.x;
+    const int lane = lane_id_x();
     const int stride = 2 + dd + d;
     const float* pp = part + (size_t)bh * S * stride;
     const T* wdg = wd + (size_t)g * d * dd;

@@ -257,11 +257,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     __shared__ float wsh[DD][D];                    // W_up (fp32), used when P == 1
     __shared__ float mrg[kDecMaxGroup][stride];     // merged record, used when P == 1
 
-    const int s = blockIdx.x;  // part of this (batch, KV head), < P
-    const int bg = blockIdx.y;
+    const int s = wg_id_x();  // part of this (batch, KV head), < P
+    const int bg = wg_id_y();
     const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
     const int G = Hq / Hkv;
-    const int tid = threadIdx.x;
+    const int tid = lane_id_x();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
     const int col = lane & 31, hg = lane >> 5;

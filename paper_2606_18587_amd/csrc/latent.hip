@@ -25,22 +25,22 @@ __global__ __launch_bounds__(256) void prefill_latent_kernel(
     T* __restrict__ cK, T* __restrict__ cVt, int Hkv, int T_, int d, int dd, int Tl, int Tp,
     int perm) {
     extern __shared__ float xs[];  // [2][64][d+1]
-    const int bg = blockIdx.y;
+    const int bg = wg_id_y();
     const int g = bg % Hkv;
-    const int t0 = blockIdx.x * 64;
+    const int t0 = wg_id_x() * 64;
     const int ld = d + 1;
     const T* wdg = wd + (size_t)g * d * dd;
     for (int which = 0; which < 2; ++which) {
         const T* x = (which ? v : k) + (size_t)bg * T_ * d;
         float* dst = xs + which * 64 * ld;
-        for (int idx = threadIdx.x; idx < 64 * d; idx += 256) {
+        for (int idx = lane_id_x(); idx < 64 * d; idx += 256) {
             const int t = idx / d, e = idx - (idx / d) * d;
             dst[t * ld + e] = (t0 + t < Tl) ? elem<T>::load(x + (size_t)(t0 + t) * d + e) : 0.f;
         }
     }
     __syncthreads();
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int lane = lane_id_x() & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(lane_id_x() >> 6);
     const int t = t0 + lane;
     const int nchunk = (dd + 7) / 8;
     for (int ch = wave; ch < 2 * nchunk; ch += 4) {
@@ -88,9 +88,9 @@ __global__ __launch_bounds__(256) void append_kernel(
     T* k_win, T* v_win, T* __restrict__ k_lat, T* __restrict__ v_lat, int Hkv, int d, int dd,
     int w, int cap, int len, int n, int mode) {
     extern __shared__ float xs[];  // [2][64][d+1]
-    const int bg = blockIdx.y;
+    const int bg = wg_id_y();
     const int g = bg % Hkv;
-    const int t0 = blockIdx.x * 64;
+    const int t0 = wg_id_x() * 64;
     const int ld = d + 1;
     const size_t new_base = (size_t)bg * n * d;
     const size_t win_base = (size_t)bg * w * d;
@@ -99,7 +99,7 @@ __global__ __launch_bounds__(256) void append_kernel(
             const T* src_new = (which ? v_new : k_new) + new_base;
             const T* src_win = (which ? v_win : k_win) + win_base;
             float* dst = xs + which * 64 * ld;
-            for (int idx = threadIdx.x; idx < 64 * d; idx += 256) {
+            for (int idx = lane_id_x(); idx < 64 * d; idx += 256) {
                 const int tl = idx / d, e = idx - (idx / d) * d;
                 const int tt = t0 + tl;
                 const int ex = len + tt - w;  // position leaving the window
@@ -115,8 +115,8 @@ __global__ __launch_bounds__(256) void append_kernel(
     }
     __syncthreads();  // every ring read of this block is done before any ring write
     if (mode != 2) {
-        const int lane = threadIdx.x & 63;
-        const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+        const int lane = lane_id_x() & 63;
+        const int wave = __builtin_amdgcn_readfirstlane(lane_id_x() >> 6);
         const int tt = t0 + lane;
         const int ex = len + tt - w;
         const int nchunk = (dd + 7) / 8;
@@ -147,7 +147,7 @@ __global__ __launch_bounds__(256) void append_kernel(
         for (int which = 0; which < 2; ++which) {
             const T* src = (which ? v_new : k_new) + new_base;
             T* ring = (which ? v_win : k_win) + win_base;
-            for (int idx = threadIdx.x; idx < 64 * d; idx += 256) {
+            for (int idx = lane_id_x(); idx < 64 * d; idx += 256) {
                 const int tl = idx / d, e = idx - (idx / d) * d;
                 const int tt = t0 + tl;
                 if (tt < n && tt >= n - w)
@@ -219,11 +219,11 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
     constexpr int LDT = 32 + 8;  // transposed value-latent row in LDS
     __shared__ __attribute__((aligned(16))) bf16_t wsh[32 * LDW];
     __shared__ __attribute__((aligned(16))) bf16_t vtr[4][32 * LDT];
-    if (blockIdx.x == 0 && blockIdx.y == 0 && threadIdx.x < 16)
-        consts[threadIdx.x] = threadIdx.x < 8 ? (bf16_t)0x3f80 : (bf16_t)0;
-    const int bg = blockIdx.y;
+    if (wg_id_x() == 0 && wg_id_y() == 0 && lane_id_x() < 16)
+        consts[lane_id_x()] = lane_id_x() < 8 ? (bf16_t)0x3f80 : (bf16_t)0;
+    const int bg = wg_id_y();
     const int g = bg % Hkv;
-    const int tid = threadIdx.x;
+    const int tid = lane_id_x();
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int tl = lane & 31, hg = lane >> 5;
@@ -257,7 +257,7 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
         const int e = idx >> 5, c = idx & 31;
         wsh[c * LDW + e] = c < dd ? wdg[(size_t)e * dd + c] : (bf16_t)0;
     }
-    const int chunk = blockIdx.x;
+    const int chunk = wg_id_x();
     const Rows cur = load(chunk);
     __syncthreads();
     lbf16x8 wa[KS];
@@ -353,11 +353,11 @@ __global__ __launch_bounds__(64) void append_mfma_kernel(
     bf16_t* k_win, bf16_t* v_win, bf16_t* __restrict__ k_lat, bf16_t* __restrict__ v_lat, int Hkv,
     int dd, int w, int cap, int len, int n, int mode) {
     constexpr int KS = D / 16;
-    const int bg = blockIdx.y;
+    const int bg = wg_id_y();
     const int g = bg % Hkv;
-    const int lane = threadIdx.x;
+    const int lane = lane_id_x();
     const int tl = lane & 31, hg = lane >> 5;
-    const int tt = blockIdx.x * 32 + tl;      // new token index
+    const int tt = wg_id_x() * 32 + tl;      // new token index
     const int ex = len + tt - w;              // position leaving the window
     const bool valid = tt < n;
     const bool project = mode != 2 && valid && ex >= 0;

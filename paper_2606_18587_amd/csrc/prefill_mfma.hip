@@ -547,7 +547,8 @@ void prefill_mfma_kernel(
     const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu, const bf16_t* __restrict__ cK,
     const bf16_t* __restrict__ cVt, const float* __restrict__ cnorm,
     const float* __restrict__ knorm, const bf16_t* __restrict__ consts, bf16_t* __restrict__ o,
-    int Hq, int Hkv, int T, int w, int Tp, int nblk, int BH, float c_scale) {
+    float* __restrict__ lse, int Hq, int Hkv, int T, int w, int Tp, int nblk, int BH,
+    float c_scale) {
     constexpr int BM = NW * 32;
     constexpr int KS = D / 16;   // 16-wide k slabs of q . k
     constexpr int DS = DD / 16;  // 16-wide k slabs of q~ . c^K
@@ -567,18 +568,18 @@ void prefill_mfma_kernel(
     // K/V/latents of BH/8 heads.
     int pair, bh;
     if ((BH & 7) == 0) {
-        const int xcd = blockIdx.x & 7, local = blockIdx.x >> 3;
+        const int xcd = wg_id_x() & 7, local = wg_id_x() >> 3;
         const int hpx = BH >> 3;  // heads per XCD
         pair = local / hpx;
         bh = (local - pair * hpx) * 8 + xcd;
     } else {
-        pair = blockIdx.x / BH;
-        bh = blockIdx.x - pair * BH;
+        pair = wg_id_x() / BH;
+        bh = wg_id_x() - pair * BH;
     }
     const int b = bh / Hq, h = bh - (bh / Hq) * Hq;
     const int g = h / (Hq / Hkv);
     const int bg = b * Hkv + g;
-    const int tid = threadIdx.x;
+    const int tid = lane_id_x();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bf16_t* wdg = wd + (size_t)g * D * DD;
     const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
@@ -772,6 +773,8 @@ void prefill_mfma_kernel(
         }
 
         if (i < T) {
+            // log of the row's softmax denominator (natural log), for a backward pass
+            if (lse && hg == 0) lse[(size_t)bh * T + i] = (st.m + log2f(lt)) * 0.6931471805599453f;
             const float inv = 1.f / lt;
             bf16_t* orow = o + ((size_t)bh * T + i) * D;
 #pragma unroll
@@ -797,7 +800,7 @@ bool prefill_mfma_supported(const dar_shape* s) {
 
 template <int D, int DD>
 static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q, const void* k,
-                            const void* v, const void* wd, const void* wu, void* o,
+                            const void* v, const void* wd, const void* wu, void* o, float* lse,
                             const void* cK, const void* cVt, const float* cnorm,
                             const float* knorm, const void* consts, hipStream_t st) {
     constexpr int NW = 4;
@@ -816,19 +819,19 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q,
     hipLaunchKernelGGL(kern, dim3(npair * BH), dim3(NW * 64), lds, st, (const bf16_t*)q,
                        (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)wd, (const bf16_t*)wu,
                        (const bf16_t*)cK, (const bf16_t*)cVt, cnorm, knorm, (const bf16_t*)consts,
-                       (bf16_t*)o, Hq, Hkv, T, w, Tp, nblk, BH, c_scale);
+                       (bf16_t*)o, lse, Hq, Hkv, T, w, Tp, nblk, BH, c_scale);
     return hipGetLastError();
 }
 
 hipError_t launch_prefill_mfma(const dar_shape* s, int T, const void* q, const void* k,
-                               const void* v, const void* wd, const void* wu, void* o,
+                               const void* v, const void* wd, const void* wu, void* o, float* lse,
                                const void* cK, const void* cVt, const float* cnorm,
                                const float* knorm, const void* consts, hipStream_t st) {
     const int B = s->B, Hq = s->Hq, Hkv = s->Hkv, w = s->w;
-    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, knorm, consts, st);
-    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, knorm, consts, st);
-    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, knorm, consts, st);
-    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
     return hipErrorNotSupported;
 }
 

@@ -18,15 +18,15 @@ template <typename T>
 __global__ __launch_bounds__(64) void prefill_valu_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ wd, const T* __restrict__ wu, const T* __restrict__ cK,
-    const T* __restrict__ cVt, T* __restrict__ o, int Hq, int Hkv, int T_, int d, int dd, int w,
-    int Tp, float qscale) {
+    const T* __restrict__ cVt, T* __restrict__ o, float* __restrict__ lse, int Hq, int Hkv,
+    int T_, int d, int dd, int w, int Tp, float qscale) {
     __shared__ float qs[256];
     __shared__ float qts[256];
     __shared__ float ps[64];
     __shared__ float lat[256];
-    const int lane = threadIdx.x;
-    const int i = (T_ - 1) - (int)blockIdx.x;  // longest rows are launched first
-    const int bh = blockIdx.y;
+    const int lane = lane_id_x();
+    const int i = (T_ - 1) - wg_id_x();  // longest rows are launched first
+    const int bh = wg_id_y();
     const int b = bh / Hq, h = bh - (bh / Hq) * Hq;
     const int g = h / (Hq / Hkv);
     const int bg = b * Hkv + g;
@@ -134,6 +134,8 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
     __syncthreads();
     T* orow = o + ((size_t)bh * T_ + i) * d;
     const float inv_l = 1.f / l;
+    // log of the row's softmax denominator (natural log), for a backward pass
+    if (lse && lane == 0) lse[(size_t)bh * T_ + i] = (m + log2f(l)) * 0.6931471805599453f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int e = lane + 64 * r;
@@ -152,23 +154,23 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
 
 template <typename T>
 hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, const T* wu,
-                               const T* cK, const T* cVt, T* o, int B, int Hq, int Hkv, int T_,
-                               int d, int dd, int w, hipStream_t st) {
+                               const T* cK, const T* cVt, T* o, float* lse, int B, int Hq,
+                               int Hkv, int T_, int d, int dd, int w, hipStream_t st) {
     const int Tp = prefill_tp(T_, w);
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
     dim3 grid(T_, B * Hq);
     hipLaunchKernelGGL(prefill_valu_kernel<T>, grid, dim3(64), 0, st, q, k, v, wd, wu, cK, cVt, o,
-                       Hq, Hkv, T_, d, dd, w, Tp, qscale);
+                       lse, Hq, Hkv, T_, d, dd, w, Tp, qscale);
     return hipGetLastError();
 }
 
 template hipError_t launch_prefill_valu<float>(const float*, const float*, const float*,
                                                const float*, const float*, const float*,
-                                               const float*, float*, int, int, int, int, int, int,
-                                               int, hipStream_t);
+                                               const float*, float*, float*, int, int, int, int,
+                                               int, int, int, hipStream_t);
 template hipError_t launch_prefill_valu<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
                                                 const bf16_t*, const bf16_t*, const bf16_t*,
-                                                const bf16_t*, bf16_t*, int, int, int, int, int,
-                                                int, int, hipStream_t);
+                                                const bf16_t*, bf16_t*, float*, int, int, int, int,
+                                                int, int, int, hipStream_t);
 
 }  // namespace dar

@@ -273,6 +273,24 @@ def check_rows_match_prefill(orc, seed=13):
                                    atol=0)
 
 
+def check_log_sum_exp(orc, seed=14):
+    """The row log-sum-exp equals torch.logsumexp of the masked dual-store
+    scores (library routine), and, with w >= T, of plain causal scores."""
+    for untied in (False, True):
+        for w in (0, 3, 23, 40):
+            q, k, v, wd, wu = rand_case(seed + w, untied=untied)
+            _, lse = orc.prefill(q, k, v, wd, wu, w, want_lse=True)
+            B, Hq, T, d = q.shape
+            kl = lifted(k, wd, wu)
+            K2 = np.concatenate([expand_kv(kl, Hq), expand_kv(k, Hq)], axis=2)
+            S = torch.from_numpy(np.einsum("bhid,bhjd->bhij", q, K2) / math.sqrt(d))
+            i = np.arange(T)[:, None]
+            j = np.arange(T)[None, :]
+            mask = np.concatenate([(j <= i) & ((i - j) >= w), (j <= i) & ((i - j) < w)], axis=1)
+            ref = torch.logsumexp(S.masked_fill(~torch.from_numpy(mask), float("-inf")), dim=-1)
+            np.testing.assert_allclose(lse, ref.numpy(), rtol=0, atol=1e-12)
+
+
 # ---------------------------------------------------------------- backward
 
 def torch_dual_store(q, k, v, wd, wu, w):
@@ -432,6 +450,7 @@ ALL_CHECKS = [
     check_first_row,
     check_gqa_is_repeated_mha,
     check_rows_match_prefill,
+    check_log_sum_exp,
     check_backward_finite_differences,
     check_backward_dual_store_autograd,
     check_backward_vanilla_no_bottleneck_gradient,

@@ -82,10 +82,10 @@ FAKE = ctypes.c_void_p(1 << 20)       # aligned, never dereferenced
 MISALIGNED = ctypes.c_void_p((1 << 20) + 2)
 
 
-def call_prefill(shape, T=16, q=FAKE, k=FAKE, v=FAKE, wd=FAKE, wu=None, o=FAKE, ws=FAKE,
-                 ws_bytes=1 << 30):
-    return dar.lib.dar_attn_prefill(ctypes.byref(shape), T, q, k, v, wd, wu, o, ws, ws_bytes,
-                                    None)
+def call_prefill(shape, T=16, q=FAKE, k=FAKE, v=FAKE, wd=FAKE, wu=None, o=FAKE, lse=None,
+                 ws=FAKE, ws_bytes=1 << 30):
+    return dar.lib.dar_attn_prefill(ctypes.byref(shape), T, q, k, v, wd, wu, o, lse, ws,
+                                    ws_bytes, None)
 
 
 @no_gpu
@@ -99,6 +99,7 @@ def call_prefill(shape, T=16, q=FAKE, k=FAKE, v=FAKE, wd=FAKE, wu=None, o=FAKE, 
     ({"q": None}, {}, dar.DAR_E_ARG),
     ({"k": MISALIGNED}, {}, dar.DAR_E_ARG),
     ({"wu": MISALIGNED}, {}, dar.DAR_E_ARG),
+    ({"lse": MISALIGNED}, {}, dar.DAR_E_ARG),
     ({"ws": None, "ws_bytes": 0}, {}, dar.DAR_E_WORKSPACE),
     ({"ws_bytes": 16}, {}, dar.DAR_E_WORKSPACE),
 ])
@@ -164,13 +165,14 @@ def expected_backward_ws(B, Hq, Hkv, T, d, dd):
     """fp32 (rows padded to a multiple of 32): log-sum-exp and delta per row,
     four d_down-wide row arrays (q W_up^T,
     dO W_up^T and the two distant sums), four d_down-wide key arrays (latents
-    and the two distant sums), weight partials over min(128, ceil(rows/256))
-    chunks; every part 256-byte aligned."""
+    and the two distant sums), weight partials over the larger chunk count of
+    the two kernel families; every part 256-byte aligned."""
     al = lambda x: (x + 255) // 256 * 256
     Tr = (T + 31) // 32 * 32          # token counts padded to whole 32-token blocks
     rows, toks = B * Hq * Tr, B * Hkv * Tr
     nch = lambda r: min(128, max(1, (r + 255) // 256))
-    nchunk = max(nch(B * T), nch(B * (Hq // Hkv) * T))
+    nblk = (T + 127) // 128                # matrix-core path: one share per 128-row workgroup
+    nchunk = max(nch(B * T), nch(B * (Hq // Hkv) * T), B * nblk, B * (Hq // Hkv) * nblk)
     return (2 * al(rows * 4) + 4 * al(rows * dd * 4) + 4 * al(toks * dd * 4)
             + al(2 * Hkv * nchunk * d * dd * 4))
 
@@ -185,12 +187,13 @@ def test_backward_workspace_size():
 
 
 def call_backward(shape, T=16, wu=None, dwu=None, ws=FAKE, ws_bytes=1 << 30, **kw):
-    args = dict(q=FAKE, k=FAKE, v=FAKE, wd=FAKE, o=FAKE, dout=FAKE, dq=FAKE, dk=FAKE, dv=FAKE,
-                dwd=FAKE)
+    args = dict(q=FAKE, k=FAKE, v=FAKE, wd=FAKE, o=FAKE, lse=FAKE, dout=FAKE, dq=FAKE, dk=FAKE,
+                dv=FAKE, dwd=FAKE)
     args.update(kw)
     return dar.lib.dar_attn_prefill_backward(
         ctypes.byref(shape), T, args["q"], args["k"], args["v"], args["wd"], wu, args["o"],
-        args["dout"], args["dq"], args["dk"], args["dv"], args["dwd"], dwu, ws, ws_bytes, None)
+        args["lse"], args["dout"], args["dq"], args["dk"], args["dv"], args["dwd"], dwu, ws,
+        ws_bytes, None)
 
 
 @no_gpu
@@ -198,6 +201,7 @@ def call_backward(shape, T=16, wu=None, dwu=None, ws=FAKE, ws_bytes=1 << 30, **k
     ({}, {"Hq": 3}, dar.DAR_E_ARG),
     ({"T": 0}, {}, dar.DAR_E_ARG),
     ({"dout": None}, {}, dar.DAR_E_ARG),
+    ({"lse": None}, {}, dar.DAR_E_ARG),
     ({"o": MISALIGNED}, {}, dar.DAR_E_ARG),
     ({"dwd": None}, {}, dar.DAR_E_ARG),
     ({"wu": FAKE}, {}, dar.DAR_E_ARG),             # untied needs dw_up

@@ -29,8 +29,8 @@ def run_gpu(inp, w):
     q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
     wd, wu = to_dev(inp["wd"]), to_dev(inp["wu"])
     dout = to_dev(inp["dout"])
-    o = dar.dar_attn_prefill(q, k, v, wd, wu, w)
-    grads = dar.dar_attn_prefill_backward(q, k, v, wd, wu, w, o, dout)
+    o, lse = dar.dar_attn_prefill(q, k, v, wd, wu, w, return_lse=True)
+    grads = dar.dar_attn_prefill_backward(q, k, v, wd, wu, w, o, lse, dout)
     torch.cuda.synchronize()
     return [None if g is None else to_host64(g) for g in grads]
 

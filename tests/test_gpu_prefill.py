@@ -135,3 +135,29 @@ def test_full_size_sampled_rows(name):
     # properties at every row: finite, and a convex combination bound
     of = o.float()
     assert torch.isfinite(of).all()
+
+
+@pytest.mark.parametrize("wl,untied", [
+    (di.WORKLOADS["tiny"], False),
+    (di.WORKLOADS["tiny"].with_(w=0, T=100), True),
+    (BF16_SMALL.with_(w=64), False),
+    (BF16_SMALL.with_(w=0), True),
+    (BF16_SMALL.with_(w=1000), False),
+    (di.Workload("bf16_d128", 11, 1, 8, 2, 400, 128, 32, 100, "bf16"), True),
+    (di.Workload("generic", 14, 1, 2, 1, 50, 256, 64, 7, "bf16"), False),
+])
+def test_log_sum_exp_output(wl, untied):
+    """The optional lse output (log of each row's softmax denominator) against
+    the oracle's, max abs error within the path's tolerance."""
+    inp = di.make_prefill_inputs(wl, untied=untied)
+    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
+    wd, wu = to_dev(inp["wd"]), to_dev(inp["wu"])
+    o, lse = dar.dar_attn_prefill(q, k, v, wd, wu, wl.w, return_lse=True)
+    o2 = dar.dar_attn_prefill(q, k, v, wd, wu, wl.w)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o2)  # asking for lse changes nothing else
+    ref_o, ref_lse = oracle.prefill(inp["q"].f64, inp["k"].f64, inp["v"].f64, inp["wd"].f64,
+                                    None if inp["wu"] is None else inp["wu"].f64, wl.w,
+                                    want_lse=True)
+    err = np.abs(lse.cpu().numpy().astype(np.float64) - ref_lse)
+    assert err.max() <= tol(wl.dtype), "lse max abs err %.3g" % err.max()

@@ -28,6 +28,7 @@ MUTANTS = [
     ("lift_only_keys", "double* vl = lift_all(T, d, dd, v, wd, wu);",
      "double* vl = lift_all(T, d, dd, k, wd, wu);"),
     ("max_not_subtracted_sign", "s[j] = exp(s[j] - m);", "s[j] = exp(m - s[j]);"),
+    ("lse_drops_max", "if (lse) *lse = m + log(sum);", "if (lse) *lse = log(sum);"),
     # backward
     ("bwd_softmax_jacobian_drops_delta", "const double ds = p[j] * (dp[j] - delta);",
      "const double ds = p[j] * dp[j];"),
