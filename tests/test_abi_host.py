@@ -162,19 +162,33 @@ def test_python_binding_names_match_abi():
 
 
 def expected_backward_ws(B, Hq, Hkv, T, d, dd):
-    """fp32 (rows padded to a multiple of 32): log-sum-exp and delta per row,
-    four d_down-wide row arrays (q W_up^T,
-    dO W_up^T and the two distant sums), four d_down-wide key arrays (latents
-    and the two distant sums), weight partials over the larger chunk count of
-    the two kernel families; every part 256-byte aligned."""
+    """The larger of the two kernel families' layouts (every part 256-byte
+    aligned, token counts padded to a multiple of 32):
+      lse and delta per row (fp32);
+      two per-row operand arrays (q W_up^T, dO W_up^T) and two per-key ones
+      (the latents): fp32 [dd] each for the vector-ALU kernels; bf16 [dd] plus
+      a transposed 32-row block padded to 32 latent rows for the matrix-core
+      kernels, which also keep 16 bf16 row constants per row;
+      two d_down-wide fp32 sums per row and two per key;
+      weight partials: over min(128, ceil(rows/256)) row chunks (vector ALU) or
+      one per 128-row workgroup (matrix core)."""
     al = lambda x: (x + 255) // 256 * 256
-    Tr = (T + 31) // 32 * 32          # token counts padded to whole 32-token blocks
+    Tr = (T + 31) // 32 * 32
     rows, toks = B * Hq * Tr, B * Hkv * Tr
-    nch = lambda r: min(128, max(1, (r + 255) // 256))
-    nblk = (T + 127) // 128                # matrix-core path: one share per 128-row workgroup
-    nchunk = max(nch(B * T), nch(B * (Hq // Hkv) * T), B * nblk, B * (Hq // Hkv) * nblk)
-    return (2 * al(rows * 4) + 4 * al(rows * dd * 4) + 4 * al(toks * dd * 4)
-            + al(2 * Hkv * nchunk * d * dd * 4))
+    G = Hq // Hkv
+
+    def layout(mfma):
+        opw = (dd + 32) * 2 if mfma else dd * 4
+        if mfma:
+            nblk = (T + 127) // 128
+            nchunk = max(B * nblk, B * G * nblk)
+        else:
+            nch = lambda r: min(128, max(1, (r + 255) // 256))
+            nchunk = max(nch(B * T), nch(B * G * T))
+        return (2 * al(rows * 4) + 2 * al(rows * opw) + (al(rows * 32) if mfma else 0)
+                + 2 * al(rows * dd * 4) + 2 * al(toks * opw) + 2 * al(toks * dd * 4)
+                + al(2 * Hkv * nchunk * d * dd * 4))
+    return max(layout(False), layout(True))
 
 
 def test_backward_workspace_size():
