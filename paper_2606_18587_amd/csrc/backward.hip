@@ -460,32 +460,57 @@ __global__ __launch_bounds__(256) void bwd_wpart_kernel(
 }
 
 // Sum of the chunk partials; tied: dw_down = dW_down + dW_up^T. A workgroup
-// takes 64 outputs of one KV head; its 4 wavefronts each sum every 4th chunk
-// in chunk order, and the 4 sums are added in wavefront order, so the result
-// is the same on every run. Grid: (ceil(d * dd / 64), Hkv).
+// takes 16 outputs of one KV head; its 16 thread groups each sum every 16th
+// chunk in chunk order, and the 16 sums are added in group order, so the
+// result is the same on every run. Grid: (ceil(d * dd / 16), Hkv).
 __global__ __launch_bounds__(256) void bwd_wreduce_kernel(const float* __restrict__ part,
                                                           float* __restrict__ dwd,
                                                           float* __restrict__ dwu, int Hkv,
                                                           int d, int dd, int nchunk_d,
                                                           int nchunk_u, int nchunk) {
-    __shared__ float red[2][4][64];
+    __shared__ float red[2][16][16];
     const int g = wg_id_y();
-    const int ol = lane_id_x() & 63, grp = lane_id_x() >> 6;
-    const int o = wg_id_x() * 64 + ol;
+    const int ol = lane_id_x() & 15, grp = lane_id_x() >> 4;
+    const int o = wg_id_x() * 16 + ol;
     const int n_out = d * dd;
     float sd = 0.f, su = 0.f;
     if (o < n_out) {
         const float* pd = part + ((size_t)g * nchunk) * n_out + o;
         const float* pu = part + ((size_t)(Hkv + g) * nchunk) * n_out + o;
-        for (int c = grp; c < nchunk_d; c += 4) sd += pd[(size_t)c * n_out];
-        for (int c = grp; c < nchunk_u; c += 4) su += pu[(size_t)c * n_out];
+        // independent loads first, then the sums in chunk order
+        constexpr int U = 8;
+        for (int c0 = grp; c0 < nchunk_d; c0 += 16 * U) {
+            float x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int c = c0 + 16 * u;
+                x[u] = c < nchunk_d ? pd[(size_t)c * n_out] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) sd += x[u];
+        }
+        for (int c0 = grp; c0 < nchunk_u; c0 += 16 * U) {
+            float x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int c = c0 + 16 * u;
+                x[u] = c < nchunk_u ? pu[(size_t)c * n_out] : 0.f;
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) su += x[u];
+        }
     }
     red[0][grp][ol] = sd;
     red[1][grp][ol] = su;
     __syncthreads();
     if (grp != 0 || o >= n_out) return;
-    sd = ((red[0][0][ol] + red[0][1][ol]) + red[0][2][ol]) + red[0][3][ol];
-    su = ((red[1][0][ol] + red[1][1][ol]) + red[1][2][ol]) + red[1][3][ol];
+    sd = 0.f;
+    su = 0.f;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+        sd += red[0][k][ol];
+        su += red[1][k][ol];
+    }
     const int e = o / dd, c = o % dd;
     if (dwu) {
         dwd[(size_t)g * n_out + o] = sd;
@@ -497,7 +522,7 @@ __global__ __launch_bounds__(256) void bwd_wreduce_kernel(const float* __restric
 
 hipError_t launch_bwd_wreduce(const float* part, float* dwd, float* dwu, int Hkv, int d, int dd,
                               const BwdWs& L, hipStream_t st) {
-    hipLaunchKernelGGL(bwd_wreduce_kernel, dim3((d * dd + 63) / 64, Hkv), dim3(256), 0, st, part,
+    hipLaunchKernelGGL(bwd_wreduce_kernel, dim3((d * dd + 15) / 16, Hkv), dim3(256), 0, st, part,
                        dwd, dwu, Hkv, d, dd, L.nchunk_d, L.nchunk_u, L.nchunk);
     return hipGetLastError();
 }

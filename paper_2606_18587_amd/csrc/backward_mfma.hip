@@ -134,142 +134,143 @@ __device__ __forceinline__ void wg_share(const f32x16_t (&acc)[D / 32], float* p
 
 // ---------------------------------------------------------------- preparation
 
-// Per query row i (padded rows get zeros): q~s = (q W_up^T) log2(e)/sqrt(d),
-// dO~ = dO W_up^T (bf16, row-major and in transposed 32-row blocks), and
-// -delta = -dO . O and -lse (the forward's, in log2 units), both in fp32 and
-// as bf16 hi + mid + lo row constants. One thread per row.
-// Grid: (ceil(Tr / 256), B * Hq).
-template <int D, int DD>
-__global__ __launch_bounds__(256) void bwd_prep_rows_kernel(
+// Per query row i (padded rows get zeros): q~s = (q W_up^T) log2(e)/sqrt(d)
+// and dO~ = dO W_up^T in bf16, row-major and in transposed 32-row blocks, and
+// -delta = -dO . O and -lse (the forward's, in log2 units), in fp32 and as
+// bf16 hi + mid + lo row constants. One wavefront per 32 rows on the matrix
+// cores: U W^T with U = W_up gives one latent row per lane column (the
+// row-major store), Q U^T one token per lane column (the transposed store);
+// latent rows past d_down come out zero from U's zero rows.
+// Grid: (Tr / (32 NW), B * Hq).
+template <int D, int DD, int NW>
+__global__ __launch_bounds__(NW * 64) void bwd_prep_rows_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ o, const bf16_t* __restrict__ dout,
     const float* __restrict__ lse, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
     bf16_t* __restrict__ qts, bf16_t* __restrict__ qtT, bf16_t* __restrict__ dts,
     bf16_t* __restrict__ dtT, bf16_t* __restrict__ rc, float* __restrict__ nd,
     float* __restrict__ nl2, int Hq, int Hkv, int T, int Tr, float qscale) {
-    __shared__ float U[DD * D];  // U[c][e] = W_up[c][e]
+    constexpr int KS = D / 16, DS = DD / 16, LDU = D + 8;
+    __shared__ __attribute__((aligned(16))) bf16_t U[32 * LDU];  // U[c][e] = W_up[c][e]
+    const int tid = lane_id_x(), lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int bh = wg_id_y();
     const int g = (bh % Hq) / (Hq / Hkv);
     const bf16_t* wdg = wd + (size_t)g * D * DD;
     const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
-    for (int idx = lane_id_x(); idx < DD * D; idx += 256) {
+    for (int idx = tid; idx < 32 * D; idx += NW * 64) {
         const int c = idx / D, e = idx % D;
-        U[idx] = wug ? bf16_to_f32(wug[(size_t)c * D + e]) : bf16_to_f32(wdg[(size_t)e * DD + c]);
+        U[c * LDU + e] = c < DD ? (wug ? wug[(size_t)c * D + e] : wdg[(size_t)e * DD + c]) : (bf16_t)0;
     }
     __syncthreads();
-    const int i = wg_id_x() * 256 + lane_id_x();
-    if (i >= Tr) return;
-    float aq[DD], ad[DD];
+    const int r0 = wg_id_x() * NW * 32 + wave * 32;
+    if (r0 >= Tr) return;
+    const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
+    const int rb = r0 + qc, ra = r0 + prow;  // B-layout row, A-layout row
+    const bf16_t* qh = q + (size_t)bh * T * D;
+    const bf16_t* dh = dout + (size_t)bh * T * D;
+    const bf16_t* oh = o + (size_t)bh * T * D;
+    bf16x8_t qB[KS], dB[KS], oB[KS], qA[KS], dA[KS];
 #pragma unroll
-    for (int c = 0; c < DD; ++c) { aq[c] = 0.f; ad[c] = 0.f; }
+    for (int s = 0; s < KS; ++s) {
+        const int e = s * 16 + hg * 8;
+        qB[s] = rb < T ? load_bf16x8(qh + (size_t)rb * D + e) : zero_bf16x8();
+        dB[s] = rb < T ? load_bf16x8(dh + (size_t)rb * D + e) : zero_bf16x8();
+        oB[s] = rb < T ? load_bf16x8(oh + (size_t)rb * D + e) : zero_bf16x8();
+        qA[s] = ra < T ? load_bf16x8(qh + (size_t)ra * D + e) : zero_bf16x8();
+        dA[s] = ra < T ? load_bf16x8(dh + (size_t)ra * D + e) : zero_bf16x8();
+    }
+    // latent rows of row rb: U Q^T, A rows = latent columns in perm_row order
+    f32x16_t qt = splat16(0.f), dt = splat16(0.f), qn = splat16(0.f), dn = splat16(0.f);
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        const bf16x8_t ua = load_bf16x8(U + prow * LDU + s * 16 + hg * 8);
+        const bf16x8_t ub = load_bf16x8(U + qc * LDU + s * 16 + hg * 8);
+        qt = mfma(ua, qB[s], qt);
+        dt = mfma(ua, dB[s], dt);
+        qn = mfma(qA[s], ub, qn);
+        dn = mfma(dA[s], ub, dn);
+    }
+    const size_t prw = (size_t)bh * Tr + rb;
+#pragma unroll
+    for (int s = 0; s < DS; ++s) {
+        *reinterpret_cast<bf16x8_t*>(qts + prw * DD + s * 16 + hg * 8) = pack8(qt, 8 * s, qscale);
+        *reinterpret_cast<bf16x8_t*>(dts + prw * DD + s * 16 + hg * 8) = pack8(dt, 8 * s);
+    }
+    // transposed block: lane column = latent c, registers = tokens 8 hg + r, 16 + 8 hg + r
+    const size_t blk = (((size_t)bh * (Tr / 32) + r0 / 32) * 32 + qc) * 32;
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+        *reinterpret_cast<bf16x8_t*>(qtT + blk + 16 * h2 + 8 * hg) = pack8(qn, 8 * h2, qscale);
+        *reinterpret_cast<bf16x8_t*>(dtT + blk + 16 * h2 + 8 * hg) = pack8(dn, 8 * h2);
+    }
     float dl = 0.f;
-    if (i < T) {
-        const size_t row = (size_t)bh * T + i;
 #pragma unroll
-        for (int e8 = 0; e8 < D; e8 += 8) {
-            const uint4 uq = *reinterpret_cast<const uint4*>(q + row * D + e8);
-            const uint4 ud = *reinterpret_cast<const uint4*>(dout + row * D + e8);
-            const uint4 uo = *reinterpret_cast<const uint4*>(o + row * D + e8);
-            const uint32_t wq[4] = {uq.x, uq.y, uq.z, uq.w};
-            const uint32_t wdd[4] = {ud.x, ud.y, ud.z, ud.w};
-            const uint32_t wo[4] = {uo.x, uo.y, uo.z, uo.w};
-#pragma unroll
-            for (int h2 = 0; h2 < 8; ++h2) {
-                const int sh = (h2 & 1) ? 0 : 16;
-                const float xq = __uint_as_float((wq[h2 >> 1] << sh) & 0xffff0000u);
-                const float xd = __uint_as_float((wdd[h2 >> 1] << sh) & 0xffff0000u);
-                const float xo = __uint_as_float((wo[h2 >> 1] << sh) & 0xffff0000u);
-                dl = __builtin_fmaf(xd, xo, dl);
-#pragma unroll
-                for (int c = 0; c < DD; ++c) {
-                    aq[c] = __builtin_fmaf(xq, U[c * D + e8 + h2], aq[c]);
-                    ad[c] = __builtin_fmaf(xd, U[c * D + e8 + h2], ad[c]);
-                }
-            }
-        }
+    for (int s = 0; s < KS; ++s) dl = dot8(dB[s], oB[s], dl);
+    dl = pair_sum(dl);
+    if (hg == 0) {
+        const float L2 = rb < T ? lse[(size_t)bh * T + rb] * kLog2eB : 0.f;
+        nd[prw] = -dl;
+        nl2[prw] = -L2;
+        *reinterpret_cast<uint4*>(rc + prw * 16) = neg_split3(L2);
+        *reinterpret_cast<uint4*>(rc + prw * 16 + 8) = neg_split3(dl);
     }
-    const size_t prow = (size_t)bh * Tr + i;
-    bf16_t* qr = qts + prow * DD;
-    bf16_t* dr = dts + prow * DD;
-#pragma unroll
-    for (int c8 = 0; c8 < DD; c8 += 8) {
-        *reinterpret_cast<uint4*>(qr + c8) =
-            make_uint4(pack2(aq[c8] * qscale, aq[c8 + 1] * qscale), pack2(aq[c8 + 2] * qscale, aq[c8 + 3] * qscale),
-                       pack2(aq[c8 + 4] * qscale, aq[c8 + 5] * qscale), pack2(aq[c8 + 6] * qscale, aq[c8 + 7] * qscale));
-        *reinterpret_cast<uint4*>(dr + c8) =
-            make_uint4(pack2(ad[c8], ad[c8 + 1]), pack2(ad[c8 + 2], ad[c8 + 3]),
-                       pack2(ad[c8 + 4], ad[c8 + 5]), pack2(ad[c8 + 6], ad[c8 + 7]));
-    }
-    bf16_t* qb = qtT + ((size_t)bh * (Tr / 32) + i / 32) * 32 * 32 + (i & 31);
-    bf16_t* db = dtT + ((size_t)bh * (Tr / 32) + i / 32) * 32 * 32 + (i & 31);
-#pragma unroll
-    for (int c = 0; c < 32; ++c) {
-        qb[c * 32] = c < DD ? f32_to_bf16(aq[c < DD ? c : 0] * qscale) : (bf16_t)0;
-        db[c * 32] = c < DD ? f32_to_bf16(ad[c < DD ? c : 0]) : (bf16_t)0;
-    }
-    const float L2 = i < T ? lse[(size_t)bh * T + i] * kLog2eB : 0.f;
-    nd[prow] = -dl;
-    nl2[prow] = -L2;
-    const uint4 cl = neg_split3(L2), cd = neg_split3(dl);
-    *reinterpret_cast<uint4*>(rc + prow * 16) = cl;
-    *reinterpret_cast<uint4*>(rc + prow * 16 + 8) = cd;
 }
 
 // Per key token j (padded rows get zeros): c^K = k W_down, c^V = v W_down
-// (Eq. 1) in bf16, row-major and in transposed 32-token blocks. One thread per
-// token. Grid: (ceil(Tr / 256), B * Hkv).
-template <int D, int DD>
-__global__ __launch_bounds__(256) void bwd_prep_keys_kernel(
+// (Eq. 1) in bf16, row-major and in transposed 32-token blocks, computed as
+// in bwd_prep_rows_kernel with U = W_down^T. Grid: (Tr / (32 NW), B * Hkv).
+template <int D, int DD, int NW>
+__global__ __launch_bounds__(NW * 64) void bwd_prep_keys_kernel(
     const bf16_t* __restrict__ k, const bf16_t* __restrict__ v, const bf16_t* __restrict__ wd,
     bf16_t* __restrict__ ckb, bf16_t* __restrict__ ckT, bf16_t* __restrict__ cvb,
     bf16_t* __restrict__ cvT, int Hkv, int T, int Tr) {
-    __shared__ float W[D * DD];  // W[e][c] = W_down[e][c]
+    constexpr int KS = D / 16, DS = DD / 16, LDU = D + 8;
+    __shared__ __attribute__((aligned(16))) bf16_t U[32 * LDU];  // U[c][e] = W_down[e][c]
+    const int tid = lane_id_x(), lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int bg = wg_id_y();
-    const int g = bg % Hkv;
-    const bf16_t* wdg = wd + (size_t)g * D * DD;
-    for (int idx = lane_id_x(); idx < D * DD; idx += 256) W[idx] = bf16_to_f32(wdg[idx]);
+    const bf16_t* wdg = wd + (size_t)(bg % Hkv) * D * DD;
+    for (int idx = tid; idx < 32 * D; idx += NW * 64) {
+        const int c = idx / D, e = idx % D;
+        U[c * LDU + e] = c < DD ? wdg[(size_t)e * DD + c] : (bf16_t)0;
+    }
     __syncthreads();
-    const int j = wg_id_x() * 256 + lane_id_x();
-    if (j >= Tr) return;
-    float ak[DD], av[DD];
+    const int r0 = wg_id_x() * NW * 32 + wave * 32;
+    if (r0 >= Tr) return;
+    const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
+    const int rb = r0 + qc, ra = r0 + prow;
+    const bf16_t* kh = k + (size_t)bg * T * D;
+    const bf16_t* vh = v + (size_t)bg * T * D;
+    bf16x8_t kB[KS], vB[KS], kA[KS], vA[KS];
 #pragma unroll
-    for (int c = 0; c < DD; ++c) { ak[c] = 0.f; av[c] = 0.f; }
-    if (j < T) {
-        const size_t row = (size_t)bg * T + j;
-#pragma unroll
-        for (int e8 = 0; e8 < D; e8 += 8) {
-            const uint4 uk = *reinterpret_cast<const uint4*>(k + row * D + e8);
-            const uint4 uv = *reinterpret_cast<const uint4*>(v + row * D + e8);
-            const uint32_t wk[4] = {uk.x, uk.y, uk.z, uk.w};
-            const uint32_t wv[4] = {uv.x, uv.y, uv.z, uv.w};
-#pragma unroll
-            for (int h2 = 0; h2 < 8; ++h2) {
-                const int sh = (h2 & 1) ? 0 : 16;
-                const float xk = __uint_as_float((wk[h2 >> 1] << sh) & 0xffff0000u);
-                const float xv = __uint_as_float((wv[h2 >> 1] << sh) & 0xffff0000u);
-#pragma unroll
-                for (int c = 0; c < DD; ++c) {
-                    ak[c] = __builtin_fmaf(xk, W[(e8 + h2) * DD + c], ak[c]);
-                    av[c] = __builtin_fmaf(xv, W[(e8 + h2) * DD + c], av[c]);
-                }
-            }
-        }
+    for (int s = 0; s < KS; ++s) {
+        const int e = s * 16 + hg * 8;
+        kB[s] = rb < T ? load_bf16x8(kh + (size_t)rb * D + e) : zero_bf16x8();
+        vB[s] = rb < T ? load_bf16x8(vh + (size_t)rb * D + e) : zero_bf16x8();
+        kA[s] = ra < T ? load_bf16x8(kh + (size_t)ra * D + e) : zero_bf16x8();
+        vA[s] = ra < T ? load_bf16x8(vh + (size_t)ra * D + e) : zero_bf16x8();
     }
-    const size_t prow = (size_t)bg * Tr + j;
+    f32x16_t kt = splat16(0.f), vt = splat16(0.f), kn = splat16(0.f), vn = splat16(0.f);
 #pragma unroll
-    for (int c8 = 0; c8 < DD; c8 += 8) {
-        *reinterpret_cast<uint4*>(ckb + prow * DD + c8) =
-            make_uint4(pack2(ak[c8], ak[c8 + 1]), pack2(ak[c8 + 2], ak[c8 + 3]),
-                       pack2(ak[c8 + 4], ak[c8 + 5]), pack2(ak[c8 + 6], ak[c8 + 7]));
-        *reinterpret_cast<uint4*>(cvb + prow * DD + c8) =
-            make_uint4(pack2(av[c8], av[c8 + 1]), pack2(av[c8 + 2], av[c8 + 3]),
-                       pack2(av[c8 + 4], av[c8 + 5]), pack2(av[c8 + 6], av[c8 + 7]));
+    for (int s = 0; s < KS; ++s) {
+        const bf16x8_t ua = load_bf16x8(U + prow * LDU + s * 16 + hg * 8);
+        const bf16x8_t ub = load_bf16x8(U + qc * LDU + s * 16 + hg * 8);
+        kt = mfma(ua, kB[s], kt);
+        vt = mfma(ua, vB[s], vt);
+        kn = mfma(kA[s], ub, kn);
+        vn = mfma(vA[s], ub, vn);
     }
-    bf16_t* kb = ckT + ((size_t)bg * (Tr / 32) + j / 32) * 32 * 32 + (j & 31);
-    bf16_t* vb = cvT + ((size_t)bg * (Tr / 32) + j / 32) * 32 * 32 + (j & 31);
+    const size_t prw = (size_t)bg * Tr + rb;
 #pragma unroll
-    for (int c = 0; c < 32; ++c) {
-        kb[c * 32] = c < DD ? f32_to_bf16(ak[c < DD ? c : 0]) : (bf16_t)0;
-        vb[c * 32] = c < DD ? f32_to_bf16(av[c < DD ? c : 0]) : (bf16_t)0;
+    for (int s = 0; s < DS; ++s) {
+        *reinterpret_cast<bf16x8_t*>(ckb + prw * DD + s * 16 + hg * 8) = pack8(kt, 8 * s);
+        *reinterpret_cast<bf16x8_t*>(cvb + prw * DD + s * 16 + hg * 8) = pack8(vt, 8 * s);
+    }
+    const size_t blk = (((size_t)bg * (Tr / 32) + r0 / 32) * 32 + qc) * 32;
+#pragma unroll
+    for (int h2 = 0; h2 < 2; ++h2) {
+        *reinterpret_cast<bf16x8_t*>(ckT + blk + 16 * h2 + 8 * hg) = pack8(kn, 8 * h2);
+        *reinterpret_cast<bf16x8_t*>(cvT + blk + 16 * h2 + 8 * hg) = pack8(vn, 8 * h2);
     }
 }
 
@@ -918,11 +919,12 @@ static hipError_t launch_bwd_mfma_t(const bf16_t* q, const bf16_t* k, const bf16
     const float qscale = scale * kLog2eB;
     const int nblk = (T + NW * 32 - 1) / (NW * 32);
 
-    hipLaunchKernelGGL((bwd_prep_rows_kernel<D, DD>), dim3((Tr + 255) / 256, B * Hq), dim3(256), 0,
+    const int nprep = (Tr + NW * 32 - 1) / (NW * 32);
+    hipLaunchKernelGGL((bwd_prep_rows_kernel<D, DD, NW>), dim3(nprep, B * Hq), dim3(NW * 64), 0,
                        st, q, o, dout, lse, wd, wu, qts, qtT, dts, dtT, rc, nd, nl2, Hq, Hkv, T, Tr,
                        qscale);
-    hipLaunchKernelGGL((bwd_prep_keys_kernel<D, DD>), dim3((Tr + 255) / 256, B * Hkv), dim3(256),
-                       0, st, k, v, wd, ckb, ckT, cvb, cvT, Hkv, T, Tr);
+    hipLaunchKernelGGL((bwd_prep_keys_kernel<D, DD, NW>), dim3(nprep, B * Hkv), dim3(NW * 64), 0,
+                       st, k, v, wd, ckb, ckT, cvb, cvT, Hkv, T, Tr);
     hipLaunchKernelGGL((bwd_rows_dist_kernel<DD, NW>), dim3(nblk, B * Hq), dim3(NW * 64), 0, st,
                        (const bf16_t*)ckb, (const bf16_t*)ckT, (const bf16_t*)cvb,
                        (const bf16_t*)cvT, (const bf16_t*)qts, (const bf16_t*)dts,
