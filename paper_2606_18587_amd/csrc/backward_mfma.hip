@@ -280,8 +280,8 @@ __global__ __launch_bounds__(NW * 64) void bwd_prep_keys_kernel(
 // j <= i - w only. No LDS and no barriers: the d_down-wide operands are read
 // straight from L2, one 32-key subtile ahead (two register sets used in
 // turn). Writes h = sum dS c^K and ol = sum P c^V (fp32) of every real row
-// (zero without distant keys). Grid: (ceil(T / (32 NW)), B * Hq); row blocks
-// with the most keys first.
+// (zero without distant keys). Grid: ceil(T / (32 NW)) * B * Hq workgroups,
+// dealt XCD by XCD (xcd_block_head); row blocks with the most keys first.
 template <int DD>
 struct RowDistOps {
     bf16x8_t ck[DD / 16], cv[DD / 16], kt[2], vt[2];
@@ -293,13 +293,14 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_dist_kernel(
     const bf16_t* __restrict__ cvb, const bf16_t* __restrict__ cvT,
     const bf16_t* __restrict__ qts, const bf16_t* __restrict__ dts,
     const float* __restrict__ nl2, const float* __restrict__ nd, float* __restrict__ hk,
-    float* __restrict__ ol, int Hq, int Hkv, int T, int Tr, int w) {
+    float* __restrict__ ol, int Hq, int Hkv, int T, int Tr, int w, int BH) {
     constexpr int DS = DD / 16, BM = NW * 32;
     const int lane = lane_id_x() & 63;
     const int wave = __builtin_amdgcn_readfirstlane(lane_id_x() >> 6);
     const int nblk = (T + BM - 1) / BM;
-    const int rb = nblk - 1 - wg_id_x();
-    const int bh = wg_id_y();
+    int rbi, bh;
+    xcd_block_head(wg_id_x(), BH, rbi, bh);
+    const int rb = nblk - 1 - rbi;  // row blocks with the most keys first
     const int b = bh / Hq, h = bh % Hq;
     const int bg = b * Hkv + h / (Hq / Hkv);
     const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
@@ -366,13 +367,13 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_dist_kernel(
             olT = mfma(c.vt[0], pack8(p, 0), olT);
             olT = mfma(c.vt[1], pack8(p, 8), olT);
         };
-        RowDistOps<DD> ca = load(0), cb;
+        RowDistOps<DD> bufa = load(0), bufb;
         for (int js = 0;; js += 64) {
-            cb = load(js + 32);
-            step(ca, js);
+            bufb = load(js + 32);
+            step(bufa, js);
             if (js + 32 > jd_end) break;
-            ca = load(js + 64);
-            step(cb, js + 32);
+            bufa = load(js + 64);
+            step(bufb, js + 32);
             if (js + 64 > jd_end) break;
         }
     }
@@ -397,7 +398,8 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_dist_kernel(
 // used in turn). Each row's -lse and -delta enter through one more product
 // each, with the row-constant operand (hi + mid + lo) against ones3. Writes
 // gK = sum dS q~ (q~ unscaled) and gV = sum P dO~ (fp32) of every real key.
-// Grid: (ceil(T / (32 NW)), B * Hkv); key block 0 (most rows) first.
+// Grid: ceil(T / (32 NW)) * B * Hkv workgroups (xcd_block_head); key block 0
+// (most rows) first.
 template <int DD>
 struct ColDistOps {
     bf16x8_t q[DD / 16], d[DD / 16], qt[2], dt[2], cst;
@@ -409,15 +411,16 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_dist_kernel(
     const bf16_t* __restrict__ qts, const bf16_t* __restrict__ qtT,
     const bf16_t* __restrict__ dts, const bf16_t* __restrict__ dtT,
     const bf16_t* __restrict__ rc, float* __restrict__ gk, float* __restrict__ gv, int Hq,
-    int Hkv, int T, int Tr, int w, float gscale) {
+    int Hkv, int T, int Tr, int w, float gscale, int BKV) {
     constexpr int DS = DD / 16, BK = NW * 32;
     const int lane = lane_id_x() & 63;
     const int wave = __builtin_amdgcn_readfirstlane(lane_id_x() >> 6);
-    const int bg = wg_id_y();
+    int cb, bg;
+    xcd_block_head(wg_id_x(), BKV, cb, bg);  // key block 0 (most rows) first
     const int b = bg / Hkv, g = bg % Hkv;
     const int G = Hq / Hkv;
     const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
-    const int c0 = wg_id_x() * BK + wave * 32, j = c0 + qc;
+    const int c0 = cb * BK + wave * 32, j = c0 + qc;
     if (c0 >= T) return;  // no barriers in this kernel
     const int jj = imin(j, T - 1);
     const int T32 = Tr / 32;
@@ -483,13 +486,13 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_dist_kernel(
             gvT = mfma(c.dt[0], pack8(p, 0), gvT);
             gvT = mfma(c.dt[1], pack8(p, 8), gvT);
         };
-        ColDistOps<DD> ca = load(is0), cb;
+        ColDistOps<DD> bufa = load(is0), bufb;
         for (int is = is0;; is += 64) {
-            cb = load(is + 32);
-            step(ca, is);
+            bufb = load(is + 32);
+            step(bufa, is);
             if (is + 32 >= T) break;
-            ca = load(is + 64);
-            step(cb, is + 32);
+            bufa = load(is + 64);
+            step(bufb, is + 32);
             if (is + 64 >= T) break;
         }
     }
@@ -513,14 +516,15 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_dist_kernel(
 // One wavefront per 32 query rows, window keys i - w < j <= i through 64-key
 // K/V tiles in LDS. Epilogue: dq = s (dq_win + h W_up) and the workgroup's
 // share of dW_up^T = sum_i q_i^T (s h_i) + dO_i^T ol_i (chunk
-// (b * G + h % G) * nblk + row block). Grid: (ceil(T / (32 NW)), B * Hq).
+// (b * G + h % G) * nblk + row block). Grid: ceil(T / (32 NW)) * B * Hq
+// workgroups (xcd_block_head).
 template <int D, int DD, int NW>
 __global__ __launch_bounds__(NW * 64) void bwd_rows_local_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
     const bf16_t* __restrict__ dout, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
     const float* __restrict__ hk, const float* __restrict__ ol, const float* __restrict__ nl2,
     const float* __restrict__ nd, bf16_t* __restrict__ dq, float* __restrict__ wpart, int Hq,
-    int Hkv, int T, int Tr, int w, float qscale, float scale, int nchunk) {
+    int Hkv, int T, int Tr, int w, float qscale, float scale, int nchunk, int BH) {
     constexpr int KS = D / 16, NT = D / 32, DS = DD / 16, BN = 64, LDK = D + 8, LDH = 40;
     constexpr int BM = NW * 32;
     __shared__ __attribute__((aligned(16))) bf16_t lds_kv[2 * BN * LDK];  // K tile, V tile
@@ -532,8 +536,9 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_local_kernel(
     const int tid = lane_id_x(), lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nblk = (T + BM - 1) / BM;
-    const int rb = nblk - 1 - wg_id_x();
-    const int bh = wg_id_y();
+    int rbi, bh;
+    xcd_block_head(wg_id_x(), BH, rbi, bh);
+    const int rb = nblk - 1 - rbi;
     const int b = bh / Hq, h = bh % Hq;
     const int G = Hq / Hkv;
     const int g = h / G;
@@ -695,7 +700,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_local_kernel(
 // of the group through 64-row Q / dO tiles in LDS. Epilogue: the distant part
 // gK W_down^T, gV W_down^T (hi + lo bf16), and the workgroup's share of
 // dW_down = sum_j k_j^T s gK_j + v_j^T gV_j (chunk b * nkb + key block).
-// Grid: (ceil(T / (32 NW)), B * Hkv).
+// Grid: ceil(T / (32 NW)) * B * Hkv workgroups (xcd_block_head).
 template <int D, int DD, int NW>
 __global__ __launch_bounds__(NW * 64) void bwd_cols_local_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
@@ -703,7 +708,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_local_kernel(
     const float* __restrict__ gk, const float* __restrict__ gv, const float* __restrict__ nl2,
     const float* __restrict__ nd, bf16_t* __restrict__ dk, bf16_t* __restrict__ dv,
     float* __restrict__ wpart, int Hq, int Hkv, int T, int Tr, int w, float qscale, float scale,
-    int nchunk) {
+    int nchunk, int BKV) {
     constexpr int KS = D / 16, NT = D / 32, DS = DD / 16, BN = 64, LDK = D + 8, LDH = 40;
     constexpr int BK = NW * 32;
     __shared__ __attribute__((aligned(16))) bf16_t lds_qd[2 * BN * LDK];  // Q tile, dO tile
@@ -716,9 +721,9 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_local_kernel(
 
     const int tid = lane_id_x(), lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int cb = wg_id_x();
+    int cb, bg;
+    xcd_block_head(wg_id_x(), BKV, cb, bg);
     const int nkb = (T + BK - 1) / BK;
-    const int bg = wg_id_y();
     const int b = bg / Hkv, g = bg % Hkv;
     const int G = Hq / Hkv;
     const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
@@ -925,22 +930,22 @@ static hipError_t launch_bwd_mfma_t(const bf16_t* q, const bf16_t* k, const bf16
                        qscale);
     hipLaunchKernelGGL((bwd_prep_keys_kernel<D, DD, NW>), dim3(nprep, B * Hkv), dim3(NW * 64), 0,
                        st, k, v, wd, ckb, ckT, cvb, cvT, Hkv, T, Tr);
-    hipLaunchKernelGGL((bwd_rows_dist_kernel<DD, NW>), dim3(nblk, B * Hq), dim3(NW * 64), 0, st,
+    hipLaunchKernelGGL((bwd_rows_dist_kernel<DD, NW>), dim3(nblk * B * Hq), dim3(NW * 64), 0, st,
                        (const bf16_t*)ckb, (const bf16_t*)ckT, (const bf16_t*)cvb,
                        (const bf16_t*)cvT, (const bf16_t*)qts, (const bf16_t*)dts,
-                       (const float*)nl2, (const float*)nd, hk, ol, Hq, Hkv, T, Tr, w);
-    hipLaunchKernelGGL((bwd_cols_dist_kernel<DD, NW>), dim3(nblk, B * Hkv), dim3(NW * 64), 0, st,
+                       (const float*)nl2, (const float*)nd, hk, ol, Hq, Hkv, T, Tr, w, B * Hq);
+    hipLaunchKernelGGL((bwd_cols_dist_kernel<DD, NW>), dim3(nblk * B * Hkv), dim3(NW * 64), 0, st,
                        (const bf16_t*)ckb, (const bf16_t*)cvb, (const bf16_t*)qts,
                        (const bf16_t*)qtT, (const bf16_t*)dts, (const bf16_t*)dtT,
-                       (const bf16_t*)rc, gk, gv, Hq, Hkv, T, Tr, w, 1.f / qscale);
-    hipLaunchKernelGGL((bwd_rows_local_kernel<D, DD, NW>), dim3(nblk, B * Hq), dim3(NW * 64), 0,
+                       (const bf16_t*)rc, gk, gv, Hq, Hkv, T, Tr, w, 1.f / qscale, B * Hkv);
+    hipLaunchKernelGGL((bwd_rows_local_kernel<D, DD, NW>), dim3(nblk * B * Hq), dim3(NW * 64), 0,
                        st, q, k, v, dout, wd, wu, (const float*)hk, (const float*)ol,
                        (const float*)nl2, (const float*)nd, dq, part, Hq, Hkv, T, Tr, w,
-                       qscale, scale, L.nchunk);
-    hipLaunchKernelGGL((bwd_cols_local_kernel<D, DD, NW>), dim3(nblk, B * Hkv), dim3(NW * 64), 0,
+                       qscale, scale, L.nchunk, B * Hq);
+    hipLaunchKernelGGL((bwd_cols_local_kernel<D, DD, NW>), dim3(nblk * B * Hkv), dim3(NW * 64), 0,
                        st, q, k, v, dout, wd, (const float*)gk, (const float*)gv,
                        (const float*)nl2, (const float*)nd, dk, dv, part, Hq, Hkv, T, Tr, w,
-                       qscale, scale, L.nchunk);
+                       qscale, scale, L.nchunk, B * Hkv);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_bwd_wreduce(part, dwd, dwu, Hkv, D, DD, L, st);

@@ -71,6 +71,21 @@ __device__ __forceinline__ f32x16_t splat16(float x) {
     return r;
 }
 
+// Workgroup -> (block, head) for a 1-D grid of nblk * BH workgroups, block 0
+// first. Workgroups are dealt to the 8 XCDs round-robin; when BH % 8 == 0 all
+// blocks of a head go to one XCD, so an XCD's L2 holds the operands of BH/8
+// heads instead of all of them.
+__device__ __forceinline__ void xcd_block_head(int L, int BH, int& blk, int& head) {
+    if ((BH & 7) == 0) {
+        const int xcd = L & 7, local = L >> 3, hpx = BH >> 3;
+        blk = local / hpx;
+        head = (local - blk * hpx) * 8 + xcd;
+    } else {
+        blk = L / BH;
+        head = L - blk * BH;
+    }
+}
+
 // Dot product of two 8-element bf16 operands, fp32 accumulation.
 __device__ __forceinline__ float dot8(bf16x8_t a, bf16x8_t b, float acc) {
     const uint4 ua = __builtin_bit_cast(uint4, a), ub = __builtin_bit_cast(uint4, b);
