@@ -8,7 +8,9 @@ One step = the whole hot path once:
     token (window exit projected to its latent) + split-KV decode.
 Inputs are seeded synthetic N(0,1) tensors of those shapes, resident in HBM
 before timing starts. `value` is the prefill's algorithmic TFLOP/s; the decode
-KV GB/s is reported beside it.
+KV GB/s is reported beside it. After the timed steps, the backward of the same
+prefill (the training step's attention part, given the forward's output and
+log-sum-exp) is timed on its own and reported under "backward".
 
 Prints ONE JSON line (rank 0). Only one GPU is used: --gpus above 1 exits.
 """
@@ -37,10 +39,13 @@ CSRC = os.path.join(ROOT, "paper_2606_18587_amd", "csrc")
 MEASURED_TRAFFIC = {
     "prefill": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "latent.hip",
                           "prefill_mfma.hip"],
-                "sha256_16": "e198041d0833cae5", "bytes": 130073991},
+                "sha256_16": "90d0482f3f5ed5e6", "bytes": 130236768},
     "decode": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "decode.hip",
                          "decode_mfma.hip"],
-               "sha256_16": "11223b6b26fe7967", "bytes": 581715433},
+               "sha256_16": "8c83ffdc9fa769b7", "bytes": 579741696},
+    "backward": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "mfma_common.hpp",
+                           "backward.hip", "backward_mfma.hip"],
+                 "sha256_16": "6ae715f1a0e503fb", "bytes": 504779744},
 }
 
 
@@ -65,6 +70,18 @@ def prefill_flops(B, Hq, T, d, dd, w):
     return float(B * Hq * (4 * d * n_loc + 4 * dd * n_dist))
 
 
+def backward_flops(B, Hq, T, d, dd, w):
+    """Algorithmic flops of the prefill backward at 2 flop/MAC: per window pair
+    the five d-wide products (S, dP recomputed; dV, dK, dQ), per distant pair
+    the six d_down-wide ones (S, dP; gK, gV to the keys; h and the latent
+    output to the queries). The O(T d d_down) projections and lifts are not
+    counted."""
+    i = np.arange(T, dtype=np.int64)
+    n_loc = np.minimum(i + 1, w).sum()
+    n_dist = (i + 1).sum() - n_loc
+    return float(B * Hq * (10 * d * n_loc + 12 * dd * n_dist))
+
+
 def decode_bytes(B, Hq, Hkv, d, dd, w, L, esize=2):
     """Algorithmic HBM bytes of one decode step at cache length L: ring and
     latents (keys and values) once, plus query, output and W_down."""
@@ -80,6 +97,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip the separately timed prefill backward")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter calibration)")
@@ -180,6 +199,33 @@ def main():
                       for L in range(L_first, L_last + 1)])
     gbs = dbytes / (dec_us * 1e-6) / 1e9
 
+    # ---------------- prefill backward (the training step's attention part),
+    # timed on its own after the steps above
+    bwd = None
+    if not args.no_backward:
+        dgrad = up(di.make_backward_inputs(pw)["dout"])
+        o_f, lse_f = dar.dar_attn_prefill(q, k, v, wd, None, pw.w, ws=ws, return_lse=True)
+        bws = torch.empty(dar.dar_prefill_backward_workspace_bytes(shape, pw.T), dtype=torch.uint8,
+                          device=dev)
+        for _ in range(args.warmup):
+            dar.dar_attn_prefill_backward(q, k, v, wd, None, pw.w, o_f, lse_f, dgrad, ws=bws,
+                                          check=False)
+        torch.cuda.synchronize()
+        bev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
+        for i in range(args.steps):
+            bev[i][0].record()
+            dar.dar_attn_prefill_backward(q, k, v, wd, None, pw.w, o_f, lse_f, dgrad, ws=bws,
+                                          check=False)
+            bev[i][1].record()
+        torch.cuda.synchronize()
+        bwd_ms = np.array([e[0].elapsed_time(e[1]) for e in bev])
+        bflops = backward_flops(pw.B, pw.Hq, pw.T, pw.d, pw.dd, pw.w)
+        bwd_us = float(bwd_ms.mean() * 1e3)
+        btf = bflops / (bwd_us * 1e-6) / 1e12
+        bwd = {"us": round(bwd_us, 2), "us_median": round(float(np.median(bwd_ms) * 1e3), 2),
+               "tflops": round(btf, 2), "frac_bf16_peak": round(btf / PEAK_BF16_TFLOPS, 4),
+               "alg_flop": bflops}
+
     result = {
         "metric": "DAR prefill TFLOP/s + decode KV GB/s, as fraction of MI355X peak, 1 GPU",
         "value": round(tflops, 3),
@@ -217,6 +263,13 @@ def main():
                             "traffic": measured_traffic("decode")},
         "setup_s": round(setup_s, 1),
     }
+    if bwd is not None:
+        result["backward"] = bwd
+        result["roofline_backward"] = {
+            "kernel": "dar_attn_prefill_backward (preparation, distant and window kernels for "
+                      "dq and for dk/dv, weight-share reduction)", "bound": "mfma",
+            "achieved": bwd["tflops"], "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+            "frac": bwd["frac_bf16_peak"], "traffic": measured_traffic("backward")}
 
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(pw, pin, args.cpu_seconds)

@@ -130,6 +130,40 @@ __device__ __forceinline__ void wg_share(const f32x16_t (&acc)[D / 32], float* p
     for (int idx = tid; idx < D * DD; idx += NW * 64) out[idx] = pbuf[idx];
 }
 
+// Cooperative staging of a 64-row tile of two row-major [rows][D] bf16 arrays
+// through registers into LDS (rows at or past `n` read as zero): fetch() for
+// the next tile is issued before the current one is computed on, so its
+// global latency hides behind that work.
+template <int D, int NW>
+struct TilePair {
+    static constexpr int C8 = D / 8, PER = 64 * C8 / (NW * 64);  // 16-byte chunks per thread
+    uint4 a[PER], b[PER];
+    __device__ __forceinline__ void fetch(const bf16_t* ga, const bf16_t* gb, int t, int n,
+                                          int tid) {
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int idx = tid + u * NW * 64;
+            const int row = t + idx / C8, c8 = idx % C8;
+            const size_t off = (size_t)imin(row, n - 1) * D + c8 * 8;  // clamped: no branch
+            a[u] = *reinterpret_cast<const uint4*>(ga + off);
+            b[u] = *reinterpret_cast<const uint4*>(gb + off);
+            if (row >= n) {
+                a[u] = make_uint4(0, 0, 0, 0);
+                b[u] = make_uint4(0, 0, 0, 0);
+            }
+        }
+    }
+    __device__ __forceinline__ void store(bf16_t* la, bf16_t* lb, int ld, int tid) const {
+#pragma unroll
+        for (int u = 0; u < PER; ++u) {
+            const int idx = tid + u * NW * 64;
+            const int r = idx / C8, c8 = idx % C8;
+            *reinterpret_cast<uint4*>(la + r * ld + c8 * 8) = a[u];
+            *reinterpret_cast<uint4*>(lb + r * ld + c8 * 8) = b[u];
+        }
+    }
+};
+
 }  // namespace
 
 // ---------------------------------------------------------------- preparation
@@ -568,22 +602,14 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_local_kernel(
     const bf16_t* kg = k + (size_t)bg * T * D;
     const bf16_t* vg = v + (size_t)bg * T * D;
     if (w > 0) {
-        const int jlo = imax(0, i0 - w + 1);
-        for (int t = jlo & ~(BN - 1); t <= iwg_hi; t += BN) {
+        const int t_first = imax(0, i0 - w + 1) & ~(BN - 1);
+        TilePair<D, NW> tp;
+        tp.fetch(kg, vg, t_first, T, tid);
+        for (int t = t_first; t <= iwg_hi; t += BN) {
+            __syncthreads();  // the previous tile is no longer read
+            tp.store(lds_k, lds_v, LDK, tid);
             __syncthreads();
-            constexpr int C8 = D / 8;
-            for (int idx = tid; idx < BN * C8; idx += NW * 64) {
-                const int r = idx / C8, c8 = idx % C8;
-                const int key = t + r;
-                uint4 uk = make_uint4(0, 0, 0, 0), uv = make_uint4(0, 0, 0, 0);
-                if (key < T) {
-                    uk = *reinterpret_cast<const uint4*>(kg + (size_t)key * D + c8 * 8);
-                    uv = *reinterpret_cast<const uint4*>(vg + (size_t)key * D + c8 * 8);
-                }
-                *reinterpret_cast<uint4*>(lds_k + r * LDK + c8 * 8) = uk;
-                *reinterpret_cast<uint4*>(lds_v + r * LDK + c8 * 8) = uv;
-            }
-            __syncthreads();
+            if (t + BN <= iwg_hi) tp.fetch(kg, vg, t + BN, T, tid);
             if (!live) continue;
 #pragma unroll
             for (int sub = 0; sub < BN / 32; ++sub) {
@@ -747,32 +773,31 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_local_kernel(
     for (int t = 0; t < NT; ++t) { dkT[t] = splat16(0.f); dvT[t] = splat16(0.f); }
     const int loc_hi = w > 0 ? imin(T - 1, cwg_hi + w - 1) : -1;  // last row with a window pair
 
-    for (int hh = 0; hh < G; ++hh) {
-        const int bh = b * Hq + g * G + hh;
-        const bf16_t* qh = q + (size_t)bh * T * D;
-        const bf16_t* dh = dout + (size_t)bh * T * D;
-        const float* lh = nl2 + (size_t)bh * Tr;
-        const float* dlh = nd + (size_t)bh * Tr;
-        for (int t = cwg_lo; t <= loc_hi; t += BN) {
+    // (head, 64-row tile) pairs in order, the next one fetched during the
+    // current one's work
+    const int ntile = loc_hi >= cwg_lo ? (loc_hi - cwg_lo) / BN + 1 : 0;
+    TilePair<D, NW> tp;
+    float sv = 0.f;  // -lse (threads 0..63) or -delta (64..127) of one tile row
+    auto fetch = [&](int n) {
+        const int hh = n / ntile, t = cwg_lo + (n - hh * ntile) * BN;
+        const size_t bh = (size_t)b * Hq + g * G + hh;
+        tp.fetch(q + bh * T * D, dout + bh * T * D, t, T, tid);
+        if (tid < 2 * BN) {
+            const int r = tid & (BN - 1);
+            const float* src = (tid < BN ? nl2 : nd) + bh * Tr;
+            sv = t + r < Tr ? src[imin(t + r, Tr - 1)] : 0.f;
+        }
+    };
+    if (ntile > 0) fetch(0);
+    for (int n = 0; n < G * ntile; ++n) {
+        const int t = cwg_lo + (n % ntile) * BN;
+        {
+            __syncthreads();  // the previous tile is no longer read
+            tp.store(lds_q, lds_do, LDK, tid);
+            if (tid < BN) lds_lse[tid] = sv;
+            else if (tid < 2 * BN) lds_del[tid - BN] = sv;
             __syncthreads();
-            constexpr int C8 = D / 8;
-            for (int idx = tid; idx < BN * C8; idx += NW * 64) {
-                const int r = idx / C8, c8 = idx % C8;
-                const int row = t + r;
-                uint4 uq = make_uint4(0, 0, 0, 0), ud = make_uint4(0, 0, 0, 0);
-                if (row < T) {
-                    uq = *reinterpret_cast<const uint4*>(qh + (size_t)row * D + c8 * 8);
-                    ud = *reinterpret_cast<const uint4*>(dh + (size_t)row * D + c8 * 8);
-                }
-                *reinterpret_cast<uint4*>(lds_q + r * LDK + c8 * 8) = uq;
-                *reinterpret_cast<uint4*>(lds_do + r * LDK + c8 * 8) = ud;
-            }
-            for (int r = tid; r < BN; r += NW * 64) {
-                const bool in = t + r < Tr;
-                lds_lse[r] = in ? lh[t + r] : 0.f;
-                lds_del[r] = in ? dlh[t + r] : 0.f;
-            }
-            __syncthreads();
+            if (n + 1 < G * ntile) fetch(n + 1);
             if (!live) continue;
 #pragma unroll
             for (int sub = 0; sub < BN / 32; ++sub) {
