@@ -42,9 +42,9 @@ constexpr float kLog2e = 1.4426950408889634f;
 BwdWs bwd_ws_layout(int B, int Hq, int Hkv, int T, int d, int dd, bool mfma) {
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     BwdWs L{};
-    // token counts padded to a multiple of 32 (the matrix-core path reads whole
-    // 32-token blocks and keeps two bf16 arrays where this path keeps one fp32)
-    const size_t Tr = (size_t)round_up(T, 32);
+    // token counts padded to a multiple of 64 (the matrix-core path reads whole
+    // 64-token tiles and keeps two bf16 arrays where this path keeps one fp32)
+    const size_t Tr = (size_t)round_up(T, 64);
     const size_t rows = (size_t)B * Hq * Tr;
     const size_t toks = (size_t)B * Hkv * Tr;
     // operand arrays: fp32 [n][dd] here; on the matrix-core path bf16 [n][dd]

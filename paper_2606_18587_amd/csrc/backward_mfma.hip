@@ -308,19 +308,72 @@ __global__ __launch_bounds__(NW * 64) void bwd_prep_keys_kernel(
     }
 }
 
-// ---------------------------------------------------------------- distant: h, ol
+// ---------------------------------------------------------------- distant tiles
 
-// One wavefront per 32 query rows of one (batch, query head), distant keys
-// j <= i - w only. No LDS and no barriers: the d_down-wide operands are read
-// straight from L2, one 32-key subtile ahead (two register sets used in
-// turn). Writes h = sum dS c^K and ol = sum P c^V (fp32) of every real row
-// (zero without distant keys). Grid: ceil(T / (32 NW)) * B * Hq workgroups,
-// dealt XCD by XCD (xcd_block_head); row blocks with the most keys first.
-template <int DD>
-struct RowDistOps {
-    bf16x8_t ck[DD / 16], cv[DD / 16], kt[2], vt[2];
+// Cooperative copy of a 64-token operand tile through registers into LDS.
+// The tile is up to five contiguous global segments of n_k 16-byte chunks
+// (each a multiple of 64), laid out in LDS in the same order. Load u of
+// wavefront `wave` moves the 64 chunks of group wave + NW u, so every load's
+// segment is the same for the whole wavefront (no divergent address choice).
+// seg_fetch() for the next tile is issued before the current one is computed
+// on; the registers travel by value (a struct updated through a reference
+// would be kept in scratch memory).
+template <int NW, int NCH>
+struct SegRegs {
+    static_assert(NCH % 64 == 0, "tile segments are whole 64-chunk groups");
+    static constexpr int NGRP = NCH / 64;
+    static constexpr int PER = (NGRP + NW - 1) / NW;
+    uint4 r[PER];
 };
 
+struct Segs {
+    const uint4 *s0, *s1, *s2, *s3, *s4;
+    int n0, n1, n2, n3;
+};
+
+template <int NW, int NCH>
+__device__ __forceinline__ SegRegs<NW, NCH> seg_fetch(const Segs& g, int wave, int lane) {
+    using R = SegRegs<NW, NCH>;
+    R o;
+#pragma unroll
+    for (int u = 0; u < R::PER; ++u) {
+        int grp = wave + NW * u;  // wave-uniform
+        if (R::NGRP % NW != 0 && grp >= R::NGRP) grp = R::NGRP - 1;  // spare loads repeat a group
+        const int c = grp * 64, b1 = g.n0, b2 = b1 + g.n1, b3 = b2 + g.n2, b4 = b3 + g.n3;
+        const uint4* src = c < b1 ? g.s0 + c
+                         : c < b2 ? g.s1 + (c - b1)
+                         : c < b3 ? g.s2 + (c - b2)
+                         : c < b4 ? g.s3 + (c - b3)
+                                  : g.s4 + (c - b4);
+        o.r[u] = src[lane];
+    }
+    return o;
+}
+
+// (lds points at the tile's first chunk, or at a later segment's)
+template <int NW, int NCH>
+__device__ __forceinline__ void seg_store(const SegRegs<NW, NCH> st, uint4* lds, int wave,
+                                          int lane) {
+    using R = SegRegs<NW, NCH>;
+#pragma unroll
+    for (int u = 0; u < R::PER; ++u) {
+        const int grp = wave + NW * u;
+        if (R::NGRP % NW == 0 || grp < R::NGRP) lds[grp * 64 + lane] = st.r[u];
+    }
+}
+
+// ---------------------------------------------------------------- distant: h, ol
+
+// One workgroup of NW wavefronts = 32 NW query rows of one (batch, query
+// head); distant keys j <= i - w only. The d_down-wide key operands of each
+// 64-key tile (c^K and c^V rows, their transposed blocks) are copied once into
+// LDS for the workgroup, the next tile's loads in flight meanwhile. Tiles
+// whose keys are distant for every row of the workgroup are computed without
+// masks, both 32-key subtiles in one straight-line block so that the products
+// of one overlap the exponentials of the other. Writes h = sum dS c^K and
+// ol = sum P c^V (fp32) of every real row (zero without distant keys).
+// Grid: ceil(T / (32 NW)) * B * Hq workgroups (xcd_block_head); row blocks
+// with the most keys first.
 template <int DD, int NW>
 __global__ __launch_bounds__(NW * 64) void bwd_rows_dist_kernel(
     const bf16_t* __restrict__ ckb, const bf16_t* __restrict__ ckT,
@@ -329,17 +382,25 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_dist_kernel(
     const float* __restrict__ nl2, const float* __restrict__ nd, float* __restrict__ hk,
     float* __restrict__ ol, int Hq, int Hkv, int T, int Tr, int w, int BH) {
     constexpr int DS = DD / 16, BM = NW * 32;
-    const int lane = lane_id_x() & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(lane_id_x() >> 6);
+    constexpr int NK = 8 * DD, NT = 256;       // 16-byte chunks: 64 latent rows, 2 blocks
+    constexpr int NCH = 2 * NK + 2 * NT;
+    __shared__ __attribute__((aligned(16))) uint4 tile[NCH];
+    const bf16_t* lck = reinterpret_cast<const bf16_t*>(tile);
+    const bf16_t* lcv = lck + 64 * DD;
+    const bf16_t* lkt = lcv + 64 * DD;
+    const bf16_t* lvt = lkt + 2 * 1024;
+
+    const int tid = lane_id_x(), lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int nblk = (T + BM - 1) / BM;
     int rbi, bh;
     xcd_block_head(wg_id_x(), BH, rbi, bh);
     const int rb = nblk - 1 - rbi;  // row blocks with the most keys first
     const int b = bh / Hq, h = bh % Hq;
     const int bg = b * Hkv + h / (Hq / Hkv);
-    const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
-    const int r0 = rb * BM + wave * 32, i = r0 + qc;
-    if (r0 >= T) return;  // no barriers in this kernel
+    const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc), lrow = perm_row(qc);
+    const int i0 = rb * BM, r0 = i0 + wave * 32, i = r0 + qc;
+    const bool live = r0 < T;
     const int i_hi = imin(r0 + 31, T - 1);
     const int ii = imin(i, T - 1);
     const int T32 = Tr / 32;
@@ -354,64 +415,65 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_dist_kernel(
     const f32x16_t negL = splat16(nl2[prw]), negd = splat16(nd[prw]);
     f32x16_t hT = splat16(0.f), olT = splat16(0.f);
 
-    const int jd_end = i_hi - w;  // last distant key of any row here
-    if (jd_end >= 0) {
-        const bf16_t* ckg = ckb + (size_t)bg * Tr * DD + (size_t)prow * DD + hg * 8;
-        const bf16_t* cvg = cvb + (size_t)bg * Tr * DD + (size_t)prow * DD + hg * 8;
-        const bf16_t* ckTg = ckT + (size_t)bg * T32 * 32 * 32;
-        const bf16_t* cvTg = cvT + (size_t)bg * T32 * 32 * 32;
-        const int js_last = jd_end & ~31;
-        auto load = [&](int js) {
-            js = imin(js, js_last);  // loads past the last subtile repeat it
-            RowDistOps<DD> o;
+    // one 32-key subtile at offset `sub` of the LDS tile (keys js..js+31)
+    auto step = [&](int sub, int js, bool masked) {
+        const bf16_t* ckr = lck + (sub * 32 + prow) * DD + hg * 8;
+        const bf16_t* cvr = lcv + (sub * 32 + prow) * DD + hg * 8;
+        f32x16_t x = mfma(load_bf16x8(ckr), qtop[0], negL);
+        f32x16_t dp = mfma(load_bf16x8(cvr), dtop[0], negd);
+        if (DS == 2) {
+            x = mfma(load_bf16x8(ckr + 16), qtop[DS - 1], x);
+            dp = mfma(load_bf16x8(cvr + 16), dtop[DS - 1], dp);
+        }
+        if (masked) {
 #pragma unroll
-            for (int s = 0; s < DS; ++s) {
-                o.ck[s] = load_bf16x8(ckg + (size_t)js * DD + s * 16);
-                o.cv[s] = load_bf16x8(cvg + (size_t)js * DD + s * 16);
-            }
-            const bf16_t* kb = ckTg + (size_t)(js >> 5) * 32 * 32;
-            const bf16_t* vb = cvTg + (size_t)(js >> 5) * 32 * 32;
+            for (int r = 0; r < 16; ++r)
+                if (js + acc_row(r, hg) > i - w) x[r] = -INFINITY;
+        }
+        f32x16_t p, ds;
 #pragma unroll
-            for (int hf = 0; hf < 2; ++hf) {
-                o.kt[hf] = latT_operand(kb, qc, hg, hf);
-                o.vt[hf] = latT_operand(vb, qc, hg, hf);
-            }
-            return o;
+        for (int r = 0; r < 16; ++r) {
+            p[r] = __builtin_amdgcn_exp2f(x[r]);
+            ds[r] = p[r] * dp[r];
+        }
+        const bf16_t* kt = lkt + sub * 1024 + lrow * 32 + hg * 8;
+        const bf16_t* vt = lvt + sub * 1024 + lrow * 32 + hg * 8;
+        hT = mfma(load_bf16x8(kt), pack8(ds, 0), hT);
+        hT = mfma(load_bf16x8(kt + 16), pack8(ds, 8), hT);
+        olT = mfma(load_bf16x8(vt), pack8(p, 0), olT);
+        olT = mfma(load_bf16x8(vt + 16), pack8(p, 8), olT);
+    };
+
+    const int jd_wg = imin(i0 + BM - 1, T - 1) - w;  // last distant key of the workgroup
+    const int jd_end = live ? i_hi - w : -1;         // ... of this wavefront
+    if (jd_wg >= 0) {
+        const uint4* g_ck = reinterpret_cast<const uint4*>(ckb + (size_t)bg * Tr * DD);
+        const uint4* g_cv = reinterpret_cast<const uint4*>(cvb + (size_t)bg * Tr * DD);
+        const uint4* g_kt = reinterpret_cast<const uint4*>(ckT + (size_t)bg * T32 * 1024);
+        const uint4* g_vt = reinterpret_cast<const uint4*>(cvT + (size_t)bg * T32 * 1024);
+        auto segs = [&](int t) {
+            // rows t..t+63 (DD / 8 chunks each); transposed blocks t/32, t/32 + 1 (128 each)
+            const size_t tb = (size_t)(t / 32) * 128;
+            // four segments: the fifth is never read
+            return Segs{g_ck + (size_t)t * DD / 8, g_cv + (size_t)t * DD / 8, g_kt + tb, g_vt + tb,
+                        g_vt + tb, NK, NK, NT, NT};
         };
-        auto step = [&](const RowDistOps<DD>& c, int js) {
-            f32x16_t x = mfma(c.ck[0], qtop[0], negL);
-            f32x16_t dp = mfma(c.cv[0], dtop[0], negd);
-            if (DS == 2) {
-                x = mfma(c.ck[DS - 1], qtop[DS - 1], x);
-                dp = mfma(c.cv[DS - 1], dtop[DS - 1], dp);
+        SegRegs<NW, NCH> st = seg_fetch<NW, NCH>(segs(0), wave, lane);
+        for (int t = 0; t <= jd_wg; t += 64) {
+            __syncthreads();  // the previous tile is no longer read
+            seg_store<NW, NCH>(st, tile, wave, lane);
+            __syncthreads();
+            if (t + 64 <= jd_wg) st = seg_fetch<NW, NCH>(segs(t + 64), wave, lane);
+            const bool interior = t + 63 <= r0 - w;  // every key distant for every row
+            if (live && interior) {
+                step(0, t, false);
+                step(1, t + 32, false);
             }
-            if (js + 31 > r0 - w) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (js + acc_row(r, hg) > i - w) x[r] = -INFINITY;
-            }
-            f32x16_t p, ds;
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                p[r] = __builtin_amdgcn_exp2f(x[r]);
-                ds[r] = p[r] * dp[r];
-            }
-            hT = mfma(c.kt[0], pack8(ds, 0), hT);
-            hT = mfma(c.kt[1], pack8(ds, 8), hT);
-            olT = mfma(c.vt[0], pack8(p, 0), olT);
-            olT = mfma(c.vt[1], pack8(p, 8), olT);
-        };
-        RowDistOps<DD> bufa = load(0), bufb;
-        for (int js = 0;; js += 64) {
-            bufb = load(js + 32);
-            step(bufa, js);
-            if (js + 32 > jd_end) break;
-            bufa = load(js + 64);
-            step(bufb, js + 32);
-            if (js + 64 > jd_end) break;
+            if (live && !interior && t <= jd_end) step(0, t, t + 31 > r0 - w);
+            if (live && !interior && t + 32 <= jd_end) step(1, t + 32, t + 63 > r0 - w);
         }
     }
-    if (i >= T) return;
+    if (!live || i >= T) return;
     float* hr = hk + ((size_t)bh * T + i) * DD;
     float* orr = ol + ((size_t)bh * T + i) * DD;
 #pragma unroll
@@ -426,19 +488,15 @@ __global__ __launch_bounds__(NW * 64) void bwd_rows_dist_kernel(
 
 // ---------------------------------------------------------------- distant: gK, gV
 
-// One wavefront per 32 keys of one (batch, KV head), the distant rows
-// i >= j + w of every query head of the group. No LDS and no barriers; the
-// row operands are read from L2 one 32-row subtile ahead (two register sets
-// used in turn). Each row's -lse and -delta enter through one more product
-// each, with the row-constant operand (hi + mid + lo) against ones3. Writes
+// One workgroup of NW wavefronts = 32 NW keys of one (batch, KV head); the
+// distant rows i >= j + w of every query head of the group. The row operands
+// of each 64-row tile (q~ and dO~ rows, their transposed blocks, the row
+// constants) are copied once into LDS for the workgroup, as in the query-side
+// kernel. Each row's -lse and -delta enter through one more product each,
+// the row-constant operand (hi + mid + lo) against ones3. Writes
 // gK = sum dS q~ (q~ unscaled) and gV = sum P dO~ (fp32) of every real key.
 // Grid: ceil(T / (32 NW)) * B * Hkv workgroups (xcd_block_head); key block 0
 // (most rows) first.
-template <int DD>
-struct ColDistOps {
-    bf16x8_t q[DD / 16], d[DD / 16], qt[2], dt[2], cst;
-};
-
 template <int DD, int NW>
 __global__ __launch_bounds__(NW * 64) void bwd_cols_dist_kernel(
     const bf16_t* __restrict__ ckb, const bf16_t* __restrict__ cvb,
@@ -447,15 +505,25 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_dist_kernel(
     const bf16_t* __restrict__ rc, float* __restrict__ gk, float* __restrict__ gv, int Hq,
     int Hkv, int T, int Tr, int w, float gscale, int BKV) {
     constexpr int DS = DD / 16, BK = NW * 32;
-    const int lane = lane_id_x() & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(lane_id_x() >> 6);
+    constexpr int NQ = 8 * DD, NT = 256, NC = 128;  // 16-byte chunks per 64-row tile
+    constexpr int NCH = 2 * NQ + 2 * NT + NC;
+    __shared__ __attribute__((aligned(16))) uint4 tile[NCH];
+    const bf16_t* lq = reinterpret_cast<const bf16_t*>(tile);
+    const bf16_t* ld = lq + 64 * DD;
+    const bf16_t* lqt = ld + 64 * DD;
+    const bf16_t* ldt = lqt + 2 * 1024;
+    const bf16_t* lrc = ldt + 2 * 1024;
+
+    const int tid = lane_id_x(), lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     int cb, bg;
-    xcd_block_head(wg_id_x(), BKV, cb, bg);  // key block 0 (most rows) first
+    xcd_block_head(wg_id_x(), BKV, cb, bg);
     const int b = bg / Hkv, g = bg % Hkv;
     const int G = Hq / Hkv;
     const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
-    const int c0 = cb * BK + wave * 32, j = c0 + qc;
-    if (c0 >= T) return;  // no barriers in this kernel
+    const int cwg = cb * BK;
+    const int c0 = cwg + wave * 32, j = c0 + qc;
+    const bool live = c0 < T;
     const int jj = imin(j, T - 1);
     const int T32 = Tr / 32;
 
@@ -467,70 +535,78 @@ __global__ __launch_bounds__(NW * 64) void bwd_cols_dist_kernel(
     }
     const bf16x8_t b_lse = ones3(hg, 0), b_del = ones3(hg, 1);
     f32x16_t gkT = splat16(0.f), gvT = splat16(0.f);
-    const int is0 = (c0 + w) & ~31;  // first row block with a distant pair
-    const int is_last = (T - 1) & ~31;
-    for (int hh = 0; hh < G && is0 < T; ++hh) {
-        const int bh = b * Hq + g * G + hh;
-        const bf16_t* qth = qts + (size_t)bh * Tr * DD + (size_t)prow * DD + hg * 8;
-        const bf16_t* dth = dts + (size_t)bh * Tr * DD + (size_t)prow * DD + hg * 8;
-        const bf16_t* rch = rc + (size_t)bh * Tr * 16 + (size_t)prow * 16 + hg * 8;
-        const bf16_t* qtTh = qtT + (size_t)bh * T32 * 32 * 32;
-        const bf16_t* dtTh = dtT + (size_t)bh * T32 * 32 * 32;
-        auto load = [&](int is) {
-            is = imin(is, is_last);  // loads past the last subtile repeat it
-            ColDistOps<DD> o;
+
+    auto step = [&](int sub, int is, bool masked) {
+        const bf16_t* qr = lq + (sub * 32 + prow) * DD + hg * 8;
+        const bf16_t* dr = ld + (sub * 32 + prow) * DD + hg * 8;
+        const bf16x8_t cst = load_bf16x8(lrc + (sub * 32 + prow) * 16 + hg * 8);
+        f32x16_t x = mfma(cst, b_lse, splat16(0.f));
+        f32x16_t dp = mfma(cst, b_del, splat16(0.f));
 #pragma unroll
-            for (int s = 0; s < DS; ++s) {
-                o.q[s] = load_bf16x8(qth + (size_t)is * DD + s * 16);
-                o.d[s] = load_bf16x8(dth + (size_t)is * DD + s * 16);
-            }
-            o.cst = load_bf16x8(rch + (size_t)is * 16);
-            const bf16_t* qb = qtTh + (size_t)(is >> 5) * 32 * 32;
-            const bf16_t* db = dtTh + (size_t)(is >> 5) * 32 * 32;
-#pragma unroll
-            for (int hf = 0; hf < 2; ++hf) {
-                o.qt[hf] = latT_operand(qb, qc, hg, hf);
-                o.dt[hf] = latT_operand(db, qc, hg, hf);
-            }
-            return o;
-        };
-        auto step = [&](const ColDistOps<DD>& c, int is) {
-            f32x16_t x = mfma(c.cst, b_lse, splat16(0.f));
-            f32x16_t dp = mfma(c.cst, b_del, splat16(0.f));
-#pragma unroll
-            for (int s = 0; s < DS; ++s) {
-                x = mfma(c.q[s], ckop[s], x);
-                dp = mfma(c.d[s], cvop[s], dp);
-            }
-            if (!(is >= c0 + 31 + w && is + 31 < T)) {
-#pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int i = is + acc_row(r, hg);
-                    if (i - j < w || i >= T) x[r] = -INFINITY;
-                }
-            }
-            f32x16_t p, ds;
+        for (int s = 0; s < DS; ++s) {
+            x = mfma(load_bf16x8(qr + s * 16), ckop[s], x);
+            dp = mfma(load_bf16x8(dr + s * 16), cvop[s], dp);
+        }
+        if (masked) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                p[r] = __builtin_amdgcn_exp2f(x[r]);
-                ds[r] = p[r] * dp[r];
+                const int i = is + acc_row(r, hg);
+                if (i - j < w || i >= T) x[r] = -INFINITY;
             }
-            gkT = mfma(c.qt[0], pack8(ds, 0), gkT);
-            gkT = mfma(c.qt[1], pack8(ds, 8), gkT);
-            gvT = mfma(c.dt[0], pack8(p, 0), gvT);
-            gvT = mfma(c.dt[1], pack8(p, 8), gvT);
-        };
-        ColDistOps<DD> bufa = load(is0), bufb;
-        for (int is = is0;; is += 64) {
-            bufb = load(is + 32);
-            step(bufa, is);
-            if (is + 32 >= T) break;
-            bufa = load(is + 64);
-            step(bufb, is + 32);
-            if (is + 64 >= T) break;
         }
+        f32x16_t p, ds;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+            p[r] = __builtin_amdgcn_exp2f(x[r]);
+            ds[r] = p[r] * dp[r];
+        }
+        const bf16_t* qt = lqt + sub * 1024 + prow * 32 + hg * 8;
+        const bf16_t* dt = ldt + sub * 1024 + prow * 32 + hg * 8;
+        gkT = mfma(load_bf16x8(qt), pack8(ds, 0), gkT);
+        gkT = mfma(load_bf16x8(qt + 16), pack8(ds, 8), gkT);
+        gvT = mfma(load_bf16x8(dt), pack8(p, 0), gvT);
+        gvT = mfma(load_bf16x8(dt + 16), pack8(p, 8), gvT);
+    };
+
+    const int t0 = (cwg + w) & ~63;  // first row tile with a distant pair in the workgroup
+    const int ntile = t0 < T ? (T - 1 - t0) / 64 + 1 : 0;
+    const int ntot = G * ntile;
+    // two copies per tile (the operand rows and blocks, then the row constants):
+    // each keeps at most four loads per thread in registers
+    constexpr int NA = NCH - NC;
+    auto segs = [&](int n, bool consts) {
+        const int hh = n / ntile, t = t0 + (n - hh * ntile) * 64;
+        const size_t bh = (size_t)b * Hq + g * G + hh;
+        const uint4* rcs = reinterpret_cast<const uint4*>(rc + (bh * Tr + t) * 16);
+        if (consts) return Segs{rcs, rcs, rcs, rcs, rcs, NC, 0, 0, 0};
+        return Segs{reinterpret_cast<const uint4*>(qts + (bh * Tr + t) * DD),
+                    reinterpret_cast<const uint4*>(dts + (bh * Tr + t) * DD),
+                    reinterpret_cast<const uint4*>(qtT + (bh * T32 + t / 32) * 1024),
+                    reinterpret_cast<const uint4*>(dtT + (bh * T32 + t / 32) * 1024),
+                    rcs, NQ, NQ, NT, NT};
+    };
+    if (ntot > 0) {  // workgroup-uniform
+    SegRegs<NW, NA> sa = seg_fetch<NW, NA>(segs(0, false), wave, lane);
+    SegRegs<NW, NC> sc = seg_fetch<NW, NC>(segs(0, true), wave, lane);
+    for (int n = 0; n < ntot; ++n) {
+        const int t = t0 + (n % ntile) * 64;
+        __syncthreads();  // the previous tile is no longer read
+        seg_store<NW, NA>(sa, tile, wave, lane);
+        seg_store<NW, NC>(sc, tile + NA, wave, lane);
+        __syncthreads();
+        const int nn = imin(n + 1, ntot - 1);  // the last fetch repeats
+        sa = seg_fetch<NW, NA>(segs(nn, false), wave, lane);
+        sc = seg_fetch<NW, NC>(segs(nn, true), wave, lane);
+        const bool interior = t >= c0 + 31 + w && t + 63 < T;  // every pair distant and real
+        if (live && interior) {
+            step(0, t, false);
+            step(1, t + 32, false);
+        }
+        if (live && !interior && t + 31 >= c0 + w) step(0, t, true);
+        if (live && !interior && t + 63 >= c0 + w && t + 32 < T) step(1, t + 32, true);
     }
-    if (j >= T) return;
+    }
+    if (!live || j >= T) return;
     float* gkr = gk + ((size_t)bg * T + j) * DD;
     float* gvr = gv + ((size_t)bg * T + j) * DD;
 #pragma unroll
@@ -927,7 +1003,7 @@ static hipError_t launch_bwd_mfma_t(const bf16_t* q, const bf16_t* k, const bf16
                                     bf16_t* dv, float* dwd, float* dwu, char* ws, const BwdWs& L,
                                     int B, int Hq, int Hkv, int T, int w, hipStream_t st) {
     constexpr int NW = 4;
-    const int Tr = round_up(T, 32);
+    const int Tr = round_up(T, 64);
     const size_t nrow = (size_t)B * Hq * Tr * DD, ntok = (size_t)B * Hkv * Tr * DD;  // bf16
     float* nl2 = (float*)(ws + L.lse_off);
     float* nd = (float*)(ws + L.delta_off);

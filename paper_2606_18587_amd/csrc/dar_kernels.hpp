@@ -76,7 +76,7 @@ hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, c
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
                          int d, int dd, int w, int cap, int len, hipStream_t st);
 
-// Prefill backward workspace (256-byte aligned parts; Tr = round_up(T, 32)):
+// Prefill backward workspace (256-byte aligned parts; Tr = round_up(T, 64)):
 //   lse, delta        [B*Hq][Tr] fp32     dO . O per row (matrix-core path: -lse in
 //                                         log2 units and -delta)
 //   qt, dot           [B*Hq][Tr]          q W_up^T, dO W_up^T: fp32 [dd] per row, or

@@ -163,7 +163,7 @@ def test_python_binding_names_match_abi():
 
 def expected_backward_ws(B, Hq, Hkv, T, d, dd):
     """The larger of the two kernel families' layouts (every part 256-byte
-    aligned, token counts padded to a multiple of 32):
+    aligned, token counts padded to a multiple of 64):
       lse and delta per row (fp32);
       two per-row operand arrays (q W_up^T, dO W_up^T) and two per-key ones
       (the latents): fp32 [dd] each for the vector-ALU kernels; bf16 [dd] plus
@@ -173,7 +173,7 @@ def expected_backward_ws(B, Hq, Hkv, T, d, dd):
       weight partials: over min(128, ceil(rows/256)) row chunks (vector ALU) or
       one per 128-row workgroup (matrix core)."""
     al = lambda x: (x + 255) // 256 * 256
-    Tr = (T + 31) // 32 * 32
+    Tr = (T + 63) // 64 * 64
     rows, toks = B * Hq * Tr, B * Hkv * Tr
     G = Hq // Hkv
 
