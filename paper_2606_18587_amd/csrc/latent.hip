@@ -173,6 +173,15 @@ __device__ __forceinline__ lbf16x8 lload8(const bf16_t* p) {
     return __builtin_bit_cast(lbf16x8, *reinterpret_cast<const uint4*>(p));
 }
 
+// Two fp32 values rounded to bf16 (nearest even, one v_cvt_pk_bf16_f32) and
+// packed, a in the low half. Equal to f32_to_bf16 on every non-NaN input.
+__device__ __forceinline__ uint32_t rne_pack2(float a, float b) {
+    typedef float lf32x2 __attribute__((ext_vector_type(2)));
+    typedef __bf16 lbf16x2 __attribute__((ext_vector_type(2)));
+    const lf32x2 v = {a, b};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, lbf16x2));
+}
+
 template <int D>
 __device__ __forceinline__ void load_wd_operand(const bf16_t* __restrict__ wdg, int dd, int lane,
                                                 lbf16x8 (&wa)[D / 16]) {
@@ -251,14 +260,25 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
     };
 
     // W_down^T into LDS: row c (latent column, zero for c >= dd), k = e.
-    // Requested before any key or value row (loads return in order).
+    // This thread's elements are requested together, before any key or value
+    // row (loads return in order, so the LDS stores wait for W only and the
+    // rows stay in flight through the barrier). Column indices are clamped so
+    // that no load sits under a branch.
+    constexpr int WPT = D * 32 / 256;  // W elements per thread
     const bf16_t* wdg = wd + (size_t)g * D * dd;
-    for (int idx = tid; idx < D * 32; idx += 256) {
-        const int e = idx >> 5, c = idx & 31;
-        wsh[c * LDW + e] = c < dd ? wdg[(size_t)e * dd + c] : (bf16_t)0;
+    bf16_t wv[WPT];
+#pragma unroll
+    for (int j = 0; j < WPT; ++j) {
+        const int idx = tid + 256 * j, e = idx >> 5, c = idx & 31;
+        wv[j] = wdg[(size_t)e * dd + imin(c, dd - 1)];
     }
     const int chunk = wg_id_x();
     const Rows cur = load(chunk);
+#pragma unroll
+    for (int j = 0; j < WPT; ++j) {
+        const int idx = tid + 256 * j, e = idx >> 5, c = idx & 31;
+        wsh[c * LDW + e] = c < dd ? wv[j] : (bf16_t)0;
+    }
     __syncthreads();
     lbf16x8 wa[KS];
 #pragma unroll
@@ -295,13 +315,18 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
             // key latents: token-major, columns in latent_pos order, plus the norm
             {
                 const lf32x16 acc = project_mfma<D>(wa, xk);
+                // squared norm of the stored (bf16-rounded) row; columns past
+                // d_down are zero (W^T rows past d_down are zero)
                 float n2 = 0.f;
+                uint32_t pk[8];  // the row's bf16 values, pairs of registers
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    if (acc_col(r, hg) < dd) {
-                        const float cr = bf16_to_f32(f32_to_bf16(acc[r]));
-                        n2 = __builtin_fmaf(cr, cr, n2);
-                    }
+                for (int r = 0; r < 16; r += 2) {
+                    const uint32_t u = rne_pack2(acc[r], acc[r + 1]);
+                    pk[r >> 1] = u;
+                    const float c0 = __uint_as_float(u << 16), c1 = __uint_as_float(u & 0xffff0000u);
+                    n2 = __builtin_fmaf(c0, c0, n2);
+                    n2 = __builtin_fmaf(c1, c1, n2);
+                }
                 n2 += __shfl_xor(n2, 32, 64);
                 const float nmax = wave_max_dpp(n2);
                 if (lane == 0) cnorm[(size_t)bg * (Tp / 32) + (ts >> 5)] = sqrtf(nmax);
@@ -309,23 +334,20 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
                 // latent_pos order: positions 16s + 8hg + j hold registers 8s + j
 #pragma unroll
                 for (int s = 0; s < 2; ++s)
-                    if (16 * s < dd) {
-                        uint4 u;
-                        u.x = (uint32_t)f32_to_bf16(acc[8 * s + 0]) | ((uint32_t)f32_to_bf16(acc[8 * s + 1]) << 16);
-                        u.y = (uint32_t)f32_to_bf16(acc[8 * s + 2]) | ((uint32_t)f32_to_bf16(acc[8 * s + 3]) << 16);
-                        u.z = (uint32_t)f32_to_bf16(acc[8 * s + 4]) | ((uint32_t)f32_to_bf16(acc[8 * s + 5]) << 16);
-                        u.w = (uint32_t)f32_to_bf16(acc[8 * s + 6]) | ((uint32_t)f32_to_bf16(acc[8 * s + 7]) << 16);
-                        *reinterpret_cast<uint4*>(out + 16 * s + 8 * hg) = u;
-                    }
+                    if (16 * s < dd)
+                        *reinterpret_cast<uint4*>(out + 16 * s + 8 * hg) =
+                            make_uint4(pk[4 * s], pk[4 * s + 1], pk[4 * s + 2], pk[4 * s + 3]);
             }
             // value latents, transposed per 32-token block: [c][token], via LDS
             {
                 const lf32x16 acc = project_mfma<D>(wa, xv);
                 bf16_t* tb = vtr[wave];
+                // all 32 rows of the block (rows past d_down are zero and not read)
 #pragma unroll
-                for (int r = 0; r < 16; ++r) {
-                    const int c = acc_col(r, hg);
-                    if (c < dd) tb[c * LDT + tl] = f32_to_bf16(acc[r]);
+                for (int r = 0; r < 16; r += 2) {
+                    const uint32_t u = rne_pack2(acc[r], acc[r + 1]);
+                    tb[acc_col(r, hg) * LDT + tl] = (bf16_t)(u & 0xffffu);
+                    tb[acc_col(r + 1, hg) * LDT + tl] = (bf16_t)(u >> 16);
                 }
                 // same wavefront: its LDS writes complete before its reads
                 const int rb = cvt_rows(dd);  // block rows: dd, plus a ones row when dd == 16
