@@ -7,10 +7,13 @@ One step = the whole hot path once:
     Hkv8 d64 d_down16 w512, 32768 cached tokens): cache append of the new
     token (window exit projected to its latent) + split-KV decode.
 Inputs are seeded synthetic N(0,1) tensors of those shapes, resident in HBM
-before timing starts. `value` is the prefill's algorithmic TFLOP/s; the decode
-KV GB/s is reported beside it. After the timed steps, the backward of the same
-prefill (the training step's attention part, given the forward's output and
-log-sum-exp) is timed on its own and reported under "backward".
+before timing starts. `ms_per_step` times whole steps back to back; then each
+operation is timed on its own over the same number of back-to-back calls (the
+decode at the final cache length, which it does not change), with one event
+pair around each run. `value` is the prefill's algorithmic TFLOP/s; the decode
+KV GB/s is reported beside it. The backward of the same prefill (the training
+step's attention part, given the forward's output and log-sum-exp) is timed
+the same way and reported under "backward".
 
 Prints ONE JSON line (rank 0). Only one GPU is used: --gpus above 1 exits.
 """
@@ -59,6 +62,15 @@ def measured_traffic(which):
         with open(os.path.join(CSRC, f), "rb") as fh:
             m.update(fh.read())
     return rec["bytes"] if m.hexdigest()[:16] == rec["sha256_16"] else None
+
+
+def head_start(torch, steps):
+    """Keep the GPU busy (a spin kernel on the current stream, ahead of the
+    first timed event) while the host enqueues every timed step, so that the
+    per-call events measure GPU execution and not the Python launch path
+    (about 50 us per step of ctypes marshalling, more than a prefill lasts).
+    The spin is outside the timed region; 1 ms of head start per step."""
+    torch.cuda._sleep(int(2.4e9 * 1e-3 * steps))
 
 
 def prefill_flops(B, Hq, T, d, dd, w):
@@ -140,7 +152,7 @@ def main():
     dw = di.WORKLOADS["decode1b"]
     t0 = time.time()
     pre = di.make_decode_prefix(dw, dw.T)
-    cap = dw.T + args.warmup + args.steps + 1
+    cap = dw.T + args.warmup + 2 * args.steps + 1
     cache = dar.DarCache(dw.B, dw.Hkv, dw.d, dw.dd, dw.w, cap, torch.bfloat16, device=dev)
     dwd = up(pre["wd"])
     kpre, vpre = up(pre["k"]), up(pre["v"])
@@ -158,45 +170,48 @@ def main():
     torch.cuda.synchronize()
     setup_s = time.time() - t0
 
-    def one_step(idx, evs=None):
+    def one_step(idx):
         qd, kd, vd = step_in[idx]
-        if evs:
-            evs[0].record()
         dar.dar_attn_prefill(q, k, v, wd, None, pw.w, o=o, ws=ws, check=False)
-        if evs:
-            evs[1].record()
         dar.dar_cache_append(cache, kd, vd, dwd, Hq=dw.Hq)
-        if evs:
-            evs[2].record()
         dar.dar_attn_decode(cache, qd, dwd, None, o=dout, ws=dws)
-        if evs:
-            evs[3].record()
+
+    def timed(fn, n):
+        """Mean GPU time (ms) of n back-to-back calls of fn(i): one event pair
+        around the whole run (an event marker between two kernels costs the
+        stream several microseconds of idle time, more than a cache append)."""
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        head_start(torch, n)
+        e0.record()
+        for i in range(n):
+            fn(i)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
 
     for i in range(args.warmup):
         one_step(i)
     torch.cuda.synchronize()
 
+    # whole steps (prefill + append + decode), then each operation on its own
     L_first = cache.len + 1
-    events = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
-    start = torch.cuda.Event(enable_timing=True)
-    stop = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    start.record()
-    for i in range(args.steps):
-        one_step(args.warmup + i, events[i])
-    stop.record()
-    torch.cuda.synchronize()
-    total_ms = start.elapsed_time(stop)
-    pre_ms = np.array([e[0].elapsed_time(e[1]) for e in events])
-    app_ms = np.array([e[1].elapsed_time(e[2]) for e in events])
-    dec_ms = np.array([e[2].elapsed_time(e[3]) for e in events])
+    step_ms = timed(lambda i: one_step(args.warmup + i), args.steps)
     L_last = cache.len
+    total_ms = step_ms * args.steps
+    pre_ms = timed(lambda i: dar.dar_attn_prefill(q, k, v, wd, None, pw.w, o=o, ws=ws, check=False),
+                   args.steps)
+    qd_last = step_in[-1][0]
+    dec_ms = timed(lambda i: dar.dar_attn_decode(cache, qd_last, dwd, None, o=dout, ws=dws),
+                   args.steps)
+    app_ms = timed(lambda i: dar.dar_cache_append(cache, step_in[i][1], step_in[i][2], dwd,
+                                                  Hq=dw.Hq), args.steps)
 
-    pre_us = float(pre_ms.mean() * 1e3)
-    dec_us = float(dec_ms.mean() * 1e3)
+    pre_us = float(pre_ms * 1e3)
+    dec_us = float(dec_ms * 1e3)
     tflops = flops / (pre_us * 1e-6) / 1e12
-    dbytes = np.mean([decode_bytes(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, L)
-                      for L in range(L_first, L_last + 1)])
+    dbytes = decode_bytes(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, L_last)
     gbs = dbytes / (dec_us * 1e-6) / 1e9
 
     # ---------------- prefill backward (the training step's attention part),
@@ -211,20 +226,14 @@ def main():
             dar.dar_attn_prefill_backward(q, k, v, wd, None, pw.w, o_f, lse_f, dgrad, ws=bws,
                                           check=False)
         torch.cuda.synchronize()
-        bev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(args.steps)]
-        for i in range(args.steps):
-            bev[i][0].record()
-            dar.dar_attn_prefill_backward(q, k, v, wd, None, pw.w, o_f, lse_f, dgrad, ws=bws,
-                                          check=False)
-            bev[i][1].record()
-        torch.cuda.synchronize()
-        bwd_ms = np.array([e[0].elapsed_time(e[1]) for e in bev])
+        bwd_ms = timed(lambda i: dar.dar_attn_prefill_backward(q, k, v, wd, None, pw.w, o_f, lse_f,
+                                                               dgrad, ws=bws, check=False),
+                       args.steps)
         bflops = backward_flops(pw.B, pw.Hq, pw.T, pw.d, pw.dd, pw.w)
-        bwd_us = float(bwd_ms.mean() * 1e3)
+        bwd_us = float(bwd_ms * 1e3)
         btf = bflops / (bwd_us * 1e-6) / 1e12
-        bwd = {"us": round(bwd_us, 2), "us_median": round(float(np.median(bwd_ms) * 1e3), 2),
-               "tflops": round(btf, 2), "frac_bf16_peak": round(btf / PEAK_BF16_TFLOPS, 4),
-               "alg_flop": bflops}
+        bwd = {"us": round(bwd_us, 2), "tflops": round(btf, 2),
+               "frac_bf16_peak": round(btf / PEAK_BF16_TFLOPS, 4), "alg_flop": bflops}
 
     result = {
         "metric": "DAR prefill TFLOP/s + decode KV GB/s, as fraction of MI355X peak, 1 GPU",
@@ -244,13 +253,12 @@ def main():
                         "1B-shaped B32 Hq32 Hkv8 d64 d_down16 w512 L32768",
             "global_batch": pw.B, "seq_len": pw.T, "parallelism": "none (1 GPU)",
         },
-        "prefill": {"us": round(pre_us, 2), "us_median": round(float(np.median(pre_ms) * 1e3), 2),
-                    "tflops": round(tflops, 2), "frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
-                    "alg_flop": flops},
-        "decode": {"us": round(dec_us, 2), "us_median": round(float(np.median(dec_ms) * 1e3), 2),
-                   "gbs": round(gbs, 1), "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4),
-                   "alg_bytes": dbytes, "cache_len": [L_first, L_last],
-                   "append_us": round(float(app_ms.mean() * 1e3), 2)},
+        "prefill": {"us": round(pre_us, 2), "tflops": round(tflops, 2),
+                    "frac_bf16_peak": round(tflops / PEAK_BF16_TFLOPS, 4), "alg_flop": flops},
+        "decode": {"us": round(dec_us, 2), "gbs": round(gbs, 1),
+                   "frac_hbm_peak": round(gbs / PEAK_HBM_GBS, 4), "alg_bytes": dbytes,
+                   "cache_len": L_last, "step_cache_len": [L_first, L_last],
+                   "append_us": round(float(app_ms * 1e3), 2)},
         "roofline": {"kernel": "dar_attn_prefill (latent pre-pass + attention kernel)",
                      "bound": "mfma", "achieved": round(tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(tflops / PEAK_BF16_TFLOPS, 4),

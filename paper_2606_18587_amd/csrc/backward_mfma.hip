@@ -191,9 +191,19 @@ __global__ __launch_bounds__(NW * 64) void bwd_prep_rows_kernel(
     const int g = (bh % Hq) / (Hq / Hkv);
     const bf16_t* wdg = wd + (size_t)g * D * DD;
     const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
-    for (int idx = tid; idx < 32 * D; idx += NW * 64) {
-        const int c = idx / D, e = idx % D;
-        U[c * LDU + e] = c < DD ? (wug ? wug[(size_t)c * D + e] : wdg[(size_t)e * DD + c]) : (bf16_t)0;
+    // (all of this thread's elements requested at once, indices clamped, no
+    // load under a branch: one memory round trip before the barrier)
+    constexpr int UPT = 32 * D / (NW * 64);
+    bf16_t uv[UPT];
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+        const int idx = tid + j * NW * 64, c = imin(idx / D, DD - 1), e = idx % D;
+        uv[j] = *(wug ? wug + (size_t)c * D + e : wdg + (size_t)e * DD + c);
+    }
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+        const int idx = tid + j * NW * 64, c = idx / D, e = idx % D;
+        U[c * LDU + e] = c < DD ? uv[j] : (bf16_t)0;
     }
     __syncthreads();
     const int r0 = wg_id_x() * NW * 32 + wave * 32;
@@ -264,9 +274,19 @@ __global__ __launch_bounds__(NW * 64) void bwd_prep_keys_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int bg = wg_id_y();
     const bf16_t* wdg = wd + (size_t)(bg % Hkv) * D * DD;
-    for (int idx = tid; idx < 32 * D; idx += NW * 64) {
-        const int c = idx / D, e = idx % D;
-        U[c * LDU + e] = c < DD ? wdg[(size_t)e * DD + c] : (bf16_t)0;
+    // (all of this thread's elements requested at once, indices clamped, no
+    // load under a branch: one memory round trip before the barrier)
+    constexpr int UPT = 32 * D / (NW * 64);
+    bf16_t uv[UPT];
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+        const int idx = tid + j * NW * 64, c = imin(idx / D, DD - 1), e = idx % D;
+        uv[j] = wdg[(size_t)e * DD + c];
+    }
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+        const int idx = tid + j * NW * 64, c = idx / D, e = idx % D;
+        U[c * LDU + e] = c < DD ? uv[j] : (bf16_t)0;
     }
     __syncthreads();
     const int r0 = wg_id_x() * NW * 32 + wave * 32;

@@ -269,9 +269,20 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     if (fuse) {
         const bf16_t* wdg = wd + (size_t)g * D * DD;
         const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
-        for (int idx = tid; idx < DD * D; idx += NW * 64) {
+        // (all of this thread's elements requested at once, no load under a
+        // branch: the cache stream below is not held up by them)
+        constexpr int UPT = (DD * D + NW * 64 - 1) / (NW * 64);
+        bf16_t uv[UPT];
+#pragma unroll
+        for (int j = 0; j < UPT; ++j) {
+            const int idx = imin(tid + j * NW * 64, DD * D - 1);
             const int c = idx / D, e = idx - (idx / D) * D;
-            wsh[c][e] = bf16_to_f32(wug ? wug[(size_t)c * D + e] : wdg[(size_t)e * DD + c]);
+            uv[j] = *(wug ? wug + (size_t)c * D + e : wdg + (size_t)e * DD + c);
+        }
+#pragma unroll
+        for (int j = 0; j < UPT; ++j) {
+            const int idx = tid + j * NW * 64;
+            if (idx < DD * D) wsh[idx / D][idx - (idx / D) * D] = bf16_to_f32(uv[j]);
         }
     }
     const WaveRun run = decode_wave_run(len, w, D, DD, P * NW, s * NW + wave);

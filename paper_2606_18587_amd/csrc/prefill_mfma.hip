@@ -588,9 +588,20 @@ void prefill_mfma_kernel(
     // U = W_up (W_down^T when tied), once per workgroup: its rows are the A
     // operand of q~ = q W_up^T, its columns that of the lift
     // O^T += W_up^T O_lat^T.
-    for (int idx = tid; idx < DD * D; idx += NW * 64) {
-        const int cc = idx / D, e = idx - (idx / D) * D;
-        wU[cc * LDU + e] = wug ? wug[(size_t)cc * D + e] : wdg[(size_t)e * DD + cc];
+    // (all of this thread's elements requested at once, no load under a
+    // branch: one memory round trip before the barrier)
+    constexpr int UPT = DD * D / (NW * 64);
+    static_assert(DD * D % (NW * 64) == 0, "whole W_up elements per thread");
+    bf16_t uv[UPT];
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+        const int idx = tid + j * NW * 64, cc = idx / D, e = idx - (idx / D) * D;
+        uv[j] = *(wug ? wug + (size_t)cc * D + e : wdg + (size_t)e * DD + cc);
+    }
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+        const int idx = tid + j * NW * 64, cc = idx / D, e = idx - (idx / D) * D;
+        wU[cc * LDU + e] = uv[j];
     }
     __syncthreads();
 
