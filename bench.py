@@ -111,6 +111,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the separately timed prefill backward")
+    ap.add_argument("--no-other-prefill", action="store_true",
+                    help="skip the prefill workloads reported beside the main one")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter calibration)")
@@ -214,6 +216,32 @@ def main():
     dbytes = decode_bytes(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, L_last)
     gbs = dbytes / (dec_us * 1e-6) / 1e9
 
+    # ---------------- the other prefill workloads (parity-test shapes of the
+    # survey's configurations), each timed the same way; not part of `value`
+    other = {}
+    if not args.no_other_prefill:
+        for name in ("pythia410m_w128", "pythia410m_w512", "long16k"):
+            ow_ = di.WORKLOADS[name]
+            oin = di.make_prefill_inputs(ow_)
+            oq, ok_, ov, owd = (up(oin[x]) for x in ("q", "k", "v", "wd"))
+            del oin
+            oo = torch.empty_like(oq)
+            osh = dar.make_shape(ow_.B, ow_.Hq, ow_.Hkv, ow_.d, ow_.dd, ow_.w, torch.bfloat16)
+            ows = torch.empty(max(1, dar.dar_prefill_workspace_bytes(osh, ow_.T)),
+                              dtype=torch.uint8, device=dev)
+            run = lambda i: dar.dar_attn_prefill(oq, ok_, ov, owd, None, ow_.w, o=oo, ws=ows,
+                                                 check=False)
+            for i in range(args.warmup):
+                run(i)
+            oms = timed(run, args.steps)
+            ofl = prefill_flops(ow_.B, ow_.Hq, ow_.T, ow_.d, ow_.dd, ow_.w)
+            otf = ofl / (oms * 1e-3) / 1e12
+            other[name] = {"shape": "B%d Hq%d Hkv%d T%d d%d d_down%d w%d" % (
+                               ow_.B, ow_.Hq, ow_.Hkv, ow_.T, ow_.d, ow_.dd, ow_.w),
+                           "us": round(oms * 1e3, 2), "tflops": round(otf, 2),
+                           "frac_bf16_peak": round(otf / PEAK_BF16_TFLOPS, 4)}
+            del oq, ok_, ov, owd, oo, ows
+
     # ---------------- prefill backward (the training step's attention part),
     # timed on its own after the steps above
     bwd = None
@@ -271,6 +299,8 @@ def main():
                             "traffic": measured_traffic("decode")},
         "setup_s": round(setup_s, 1),
     }
+    if other:
+        result["prefill_other"] = other
     if bwd is not None:
         result["backward"] = bwd
         result["roofline_backward"] = {
