@@ -107,6 +107,30 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
 dar_status dar_cache_append(const dar_shape* s, dar_cache* c, const void* k_new,
                             const void* v_new, int n, const void* w_down, hipStream_t stream);
 
+/* Chunked prefill into a split cache (serving: a prompt arriving in pieces, or
+ * a batch of new tokens appended at once). The n >= 1 new tokens sit at
+ * positions len..len+n-1 (len = c->len) with queries q [B][Hq][n][d] and keys
+ * and values k_new, v_new [B][Hkv][n][d]. Every new row i attends to the
+ * positions 0..i under Eq. 3-4 exactly as row i of dar_attn_prefill over the
+ * whole sequence 0..len+n-1 would: the window tokens come from the cache's
+ * ring and from k_new/v_new at full dimension, older tokens from the cache's
+ * latents (Eq. 1, absorbed as in dar_attn_prefill). The cache is then
+ * extended by the n tokens exactly as dar_cache_append(s, c, k_new, v_new, n,
+ * w_down) extends it (bit-identical ring and latents; c->len += n at enqueue
+ * time).
+ *   o [B][Hq][n][d] (output); lse: NULL or fp32 [B][Hq][n] (output, as for
+ *   dar_attn_prefill); w_up: [Hkv][d_down][d] or NULL (tied).
+ *   ws: device workspace of at least dar_prefill_chunk_workspace_bytes(s, len,
+ *   n) bytes (caller-owned, overwritten): a copy of the ring's tokens and the
+ *   new ones, and a prefill workspace of len + n positions (the cache's latents
+ *   are re-laid out into it).
+ * Fails with DAR_E_CAPACITY if len + n > cap (nothing is enqueued). Supported:
+ * as dar_attn_prefill, with d * (element size) a multiple of 4 bytes. */
+dar_status dar_attn_prefill_chunk(const dar_shape* s, dar_cache* c, int n, const void* q,
+                                  const void* k_new, const void* v_new, const void* w_down,
+                                  const void* w_up, void* o, float* lse, void* ws,
+                                  size_t ws_bytes, hipStream_t stream);
+
 /* One decode step for the query q [B][Hq][d] at position c->len - 1, whose own
  * key and value must already have been appended. o [B][Hq][d] (output).
  * ws: device workspace of at least dar_decode_workspace_bytes(s, c->cap)
@@ -144,6 +168,7 @@ dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, c
 size_t dar_prefill_workspace_bytes(const dar_shape* s, int T);
 size_t dar_decode_workspace_bytes(const dar_shape* s, int cap);
 size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T);
+size_t dar_prefill_chunk_workspace_bytes(const dar_shape* s, int len, int n);
 
 /* Static English text for a status code. */
 const char* dar_status_string(dar_status st);

@@ -28,7 +28,7 @@ PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize) 
 // Both fast paths (matrix-core prefill) and the generic kernels live in this
 // library; the generic path handles everything the fast one does not.
 bool prefill_mfma_supported(const dar_shape* s);
-hipError_t launch_prefill_mfma(const dar_shape* s, int T, const void* q, const void* k,
+hipError_t launch_prefill_mfma(const dar_shape* s, const PrefillGeo& geo, const void* q, const void* k,
                                const void* v, const void* wd, const void* wu, void* o, float* lse,
                                const void* cK, const void* cVt, const float* cnorm,
                                const float* knorm, const void* consts, hipStream_t st);
@@ -82,6 +82,67 @@ bool group_supported(const dar_shape* s) {
 
 void clear_hip_error() { (void)hipGetLastError(); }
 
+// Pre-pass and attention kernels of one prefill (whole sequence or chunk):
+// k and v hold the positions geo describes, ws the prefill workspace laid out
+// as L for geo.total() positions.
+hipError_t run_prefill(const dar_shape* s, const PrefillGeo& geo, const void* q, const void* k,
+                       const void* v, const void* w_down, const void* w_up, void* o, float* lse,
+                       void* ws, const PrefillWs& L, bool fast, hipStream_t stream) {
+    char* wsb = (char*)ws;
+    void* cK = wsb + L.ck_off;
+    void* cV = wsb + L.cv_off;
+    void* consts = wsb + L.const_off;
+    float* cnorm = (float*)(wsb + L.norm_off);
+    float* knorm = (float*)(wsb + L.knorm_off);
+    hipError_t e;
+    if (s->dtype == DAR_BF16) {
+        e = launch_prefill_latent<bf16_t>((const bf16_t*)k, (const bf16_t*)v,
+                                          (const bf16_t*)w_down, (bf16_t*)cK, (bf16_t*)cV, cnorm,
+                                          knorm, (bf16_t*)consts, s->B, s->Hkv, geo, s->d,
+                                          s->d_down, s->w, fast, stream);
+        if (e != hipSuccess) return e;
+        if (fast)
+            return launch_prefill_mfma(s, geo, q, k, v, w_down, w_up, o, lse, cK, cV, cnorm, knorm,
+                                       consts, stream);
+        return launch_prefill_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v,
+                                           (const bf16_t*)w_down, (const bf16_t*)w_up,
+                                           (const bf16_t*)cK, (const bf16_t*)cV, (bf16_t*)o, lse,
+                                           s->B, s->Hq, s->Hkv, geo, s->d, s->d_down, s->w,
+                                           stream);
+    }
+    e = launch_prefill_latent<float>((const float*)k, (const float*)v, (const float*)w_down,
+                                     (float*)cK, (float*)cV, cnorm, knorm, (float*)consts, s->B,
+                                     s->Hkv, geo, s->d, s->d_down, s->w, false, stream);
+    if (e != hipSuccess) return e;
+    return launch_prefill_valu<float>((const float*)q, (const float*)k, (const float*)v,
+                                      (const float*)w_down, (const float*)w_up, (const float*)cK,
+                                      (const float*)cV, (float*)o, lse, s->B, s->Hq, s->Hkv, geo,
+                                      s->d, s->d_down, s->w, stream);
+}
+
+// Chunked prefill workspace: the context rows (the ring's tokens from kv0 on,
+// then the new ones) for K and V, then the prefill workspace of len + n
+// positions; every part 256-byte aligned.
+struct ChunkWs {
+    size_t ctx_k_off, ctx_v_off, pre_off, bytes;
+    PrefillWs pre;
+    int kv0, Tc;
+};
+
+ChunkWs chunk_ws_layout(const dar_shape* s, int len, int n) {
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    ChunkWs L{};
+    L.kv0 = len - s->w > 0 ? len - s->w : 0;
+    L.Tc = len + n - L.kv0;
+    const size_t ctx = al((size_t)s->B * s->Hkv * L.Tc * s->d * esize_of(s->dtype));
+    L.ctx_k_off = 0;
+    L.ctx_v_off = ctx;
+    L.pre_off = 2 * ctx;
+    L.pre = prefill_ws_layout(s->B, s->Hkv, len + n, s->d_down, s->w, esize_of(s->dtype));
+    L.bytes = L.pre_off + L.pre.bytes;
+    return L;
+}
+
 }  // namespace
 
 extern "C" {
@@ -109,6 +170,12 @@ size_t dar_decode_workspace_bytes(const dar_shape* s, int cap) {
     return (size_t)s->B * s->Hq * S * (2 + s->d_down + s->d) * sizeof(float);
 }
 
+size_t dar_prefill_chunk_workspace_bytes(const dar_shape* s, int len, int n) {
+    if (check_shape(s) != DAR_OK || len < 0 || n < 1) return 0;
+    if ((long long)len + n > 0x7fffffffLL) return 0;
+    return chunk_ws_layout(s, len, n).bytes;
+}
+
 size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T) {
     if (check_shape(s) != DAR_OK || T < 1) return 0;
     // enough for either kernel family (DAR_BWD_VALU may pick the generic one)
@@ -131,12 +198,6 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
     if (!aligned16(ws)) return DAR_E_ARG;
 
     clear_hip_error();
-    char* wsb = (char*)ws;
-    const void* cK = wsb + L.ck_off;
-    const void* cV = wsb + L.cv_off;
-    void* consts = wsb + L.const_off;
-    float* cnorm = (float*)(wsb + L.norm_off);
-    float* knorm = (float*)(wsb + L.knorm_off);
     hipError_t e = hipSuccess;
     const bool fast = prefill_mfma_supported(s);
     if (log_enabled())
@@ -144,30 +205,9 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
                 s->Hq, s->Hkv, T, s->d, s->d_down, s->w, s->dtype == DAR_BF16 ? "bf16" : "f32",
                 fast ? "mfma" : "valu");
     if (s->dtype == DAR_BF16) {
-        e = launch_prefill_latent<bf16_t>((const bf16_t*)k, (const bf16_t*)v,
-                                          (const bf16_t*)w_down, (bf16_t*)cK, (bf16_t*)cV, cnorm,
-                                          knorm, (bf16_t*)consts, s->B, s->Hkv, T, s->d,
-                                          s->d_down, s->w, fast, stream);
-        if (e == hipSuccess) {
-            if (fast)
-                e = launch_prefill_mfma(s, T, q, k, v, w_down, w_up, o, lse, cK, cV, cnorm, knorm,
-                                        consts, stream);
-            else
-                e = launch_prefill_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k,
-                                                (const bf16_t*)v, (const bf16_t*)w_down,
-                                                (const bf16_t*)w_up, (const bf16_t*)cK,
-                                                (const bf16_t*)cV, (bf16_t*)o, lse, s->B,
-                                                s->Hq, s->Hkv, T, s->d, s->d_down, s->w, stream);
-        }
+        e = run_prefill(s, whole_sequence(T), q, k, v, w_down, w_up, o, lse, ws, L, fast, stream);
     } else {
-        e = launch_prefill_latent<float>((const float*)k, (const float*)v, (const float*)w_down,
-                                         (float*)cK, (float*)cV, cnorm, knorm, (float*)consts,
-                                         s->B, s->Hkv, T, s->d, s->d_down, s->w, false, stream);
-        if (e == hipSuccess)
-            e = launch_prefill_valu<float>((const float*)q, (const float*)k, (const float*)v,
-                                           (const float*)w_down, (const float*)w_up,
-                                           (const float*)cK, (const float*)cV, (float*)o, lse,
-                                           s->B, s->Hq, s->Hkv, T, s->d, s->d_down, s->w, stream);
+        e = run_prefill(s, whole_sequence(T), q, k, v, w_down, w_up, o, lse, ws, L, false, stream);
     }
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
@@ -220,6 +260,71 @@ dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, c
                                    dw_down, dw_up, (char*)ws, L, s->B, s->Hq, s->Hkv, T, s->d,
                                    s->d_down, s->w, stream);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+dar_status dar_attn_prefill_chunk(const dar_shape* s, dar_cache* c, int n, const void* q,
+                                  const void* k_new, const void* v_new, const void* w_down,
+                                  const void* w_up, void* o, float* lse, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (!c || n < 1 || c->cap < 1 || c->len < 0 || c->len > c->cap) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(k_new) || !dev_ok(v_new) || !dev_ok(w_down) || !dev_ok(o))
+        return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if (lse && !aligned16(lse)) return DAR_E_ARG;
+    if (!dev_ok(c->k_lat) || !dev_ok(c->v_lat)) return DAR_E_ARG;
+    if (s->w > 0 && (!dev_ok(c->k_win) || !dev_ok(c->v_win))) return DAR_E_ARG;
+    if ((long long)c->len + n > (long long)c->cap) return DAR_E_CAPACITY;
+    if ((long long)s->B * s->Hkv > 65535 || (long long)s->B * s->Hq > 65535)
+        return DAR_E_UNSUPPORTED;
+    // the context copy moves 4-byte words of whole rows
+    if ((s->d * (int)esize_of(s->dtype)) % 4 != 0) return DAR_E_UNSUPPORTED;
+    const ChunkWs L = chunk_ws_layout(s, c->len, n);
+    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+
+    clear_hip_error();
+    char* wsb = (char*)ws;
+    void* ctx_k = wsb + L.ctx_k_off;
+    void* ctx_v = wsb + L.ctx_v_off;
+    const int len = c->len;
+    // rows len..len+n-1; keys/values from the context rows; latents of the
+    // tokens that left the window before this chunk from the cache
+    const PrefillGeo geo{len, n, L.kv0, L.Tc, L.kv0, c->cap, c->k_lat, c->v_lat};
+    const bool fast = prefill_mfma_supported(s);
+    hipError_t e;
+    if (s->dtype == DAR_BF16)
+        e = launch_chunk_gather<bf16_t>((const bf16_t*)c->k_win, (const bf16_t*)c->v_win,
+                                        (const bf16_t*)k_new, (const bf16_t*)v_new,
+                                        (bf16_t*)ctx_k, (bf16_t*)ctx_v, s->B, s->Hkv, s->d, s->w,
+                                        len, n, L.kv0, stream);
+    else
+        e = launch_chunk_gather<float>((const float*)c->k_win, (const float*)c->v_win,
+                                       (const float*)k_new, (const float*)v_new, (float*)ctx_k,
+                                       (float*)ctx_v, s->B, s->Hkv, s->d, s->w, len, n, L.kv0,
+                                       stream);
+    if (e == hipSuccess)
+        e = run_prefill(s, geo, q, ctx_k, ctx_v, w_down, w_up, o, lse, wsb + L.pre_off, L.pre,
+                        fast, stream);
+    // the cache update is the append of the same tokens (the attention above
+    // reads only the context copy and the workspace)
+    if (e == hipSuccess) {
+        if (s->dtype == DAR_BF16)
+            e = launch_append<bf16_t>((const bf16_t*)k_new, (const bf16_t*)v_new,
+                                      (const bf16_t*)w_down, (bf16_t*)c->k_win,
+                                      (bf16_t*)c->v_win, (bf16_t*)c->k_lat, (bf16_t*)c->v_lat,
+                                      s->B, s->Hkv, s->d, s->d_down, s->w, c->cap, len, n,
+                                      stream);
+        else
+            e = launch_append<float>((const float*)k_new, (const float*)v_new,
+                                     (const float*)w_down, (float*)c->k_win, (float*)c->v_win,
+                                     (float*)c->k_lat, (float*)c->v_lat, s->B, s->Hkv, s->d,
+                                     s->d_down, s->w, c->cap, len, n, stream);
+    }
+    if (e != hipSuccess) return DAR_E_HIP;
+    c->len += n;
+    return DAR_OK;
 }
 
 dar_status dar_cache_append(const dar_shape* s, dar_cache* c, const void* k_new,

@@ -32,6 +32,24 @@ static inline int prefill_tp(int T, int w) {
     return Tl > 0 ? round_up(Tl, 32) + 64 : 0;
 }
 PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize);
+
+// Where the rows, keys/values and latents of a prefill come from. Rows
+// r = 0..n_rows-1 are the queries at positions q0 + r (T = q0 + n_rows
+// positions in all); k and v row t holds position kv0 + t (t < Tkv); the
+// latent of a position below lat0 is read from a split cache (k_lat, v_lat,
+// [B*Hkv][cap][dd]) instead of being projected from k and v. A whole-sequence
+// prefill has q0 = kv0 = lat0 = 0 and n_rows = Tkv = T; a chunk appended to a
+// cache of len tokens has q0 = len, kv0 = max(0, len - w) (the ring's oldest
+// token), lat0 = len - w.
+struct PrefillGeo {
+    int q0, n_rows, kv0, Tkv, lat0, cap;
+    const void* k_lat;
+    const void* v_lat;
+    int total() const { return q0 + n_rows; }
+};
+static inline PrefillGeo whole_sequence(int T) {
+    return PrefillGeo{0, T, 0, T, 0, 0, nullptr, nullptr};
+}
 // Rows of a 32-token block of the transposed value latents written by the
 // matrix-core pre-pass: d_down, plus a row of ones when d_down == 16 (the
 // padding row of the 32-row MFMA operand, which then yields the row sums).
@@ -49,8 +67,16 @@ int decode_max_partials(int B, int Hkv, int cap, int w, int d, int dd, int G);
 
 template <typename T>
 hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt,
-                                 float* cnorm, float* knorm, T* consts, int B, int Hkv, int T_,
-                                 int d, int dd, int w, bool perm, hipStream_t st);
+                                 float* cnorm, float* knorm, T* consts, int B, int Hkv,
+                                 const PrefillGeo& geo, int d, int dd, int w, bool perm,
+                                 hipStream_t st);
+
+// Copies the ring's tokens [kv0, len) and the n new tokens into one row range
+// ctx [B*Hkv][len + n - kv0][d] (positions kv0..len+n-1).
+template <typename T>
+hipError_t launch_chunk_gather(const T* k_win, const T* v_win, const T* k_new, const T* v_new,
+                               T* ctx_k, T* ctx_v, int B, int Hkv, int d, int w, int len, int n,
+                               int kv0, hipStream_t st);
 
 template <typename T>
 hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, T* v_win,
@@ -60,7 +86,8 @@ hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, 
 template <typename T>
 hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, const T* wu,
                                const T* cK, const T* cVt, T* o, float* lse, int B, int Hq,
-                               int Hkv, int T_, int d, int dd, int w, hipStream_t st);
+                               int Hkv, const PrefillGeo& geo, int d, int dd, int w,
+                               hipStream_t st);
 
 // Matrix-core decode (bf16, d in {64,128}, d_down in {16,32}, <= 8 query heads
 // per KV head); shares decode_combine_kernel with the vector-ALU path.

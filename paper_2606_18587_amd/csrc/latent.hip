@@ -22,20 +22,24 @@ namespace dar {
 template <typename T>
 __global__ __launch_bounds__(256) void prefill_latent_kernel(
     const T* __restrict__ k, const T* __restrict__ v, const T* __restrict__ wd,
-    T* __restrict__ cK, T* __restrict__ cVt, int Hkv, int T_, int d, int dd, int Tl, int Tp,
-    int perm) {
+    T* __restrict__ cK, T* __restrict__ cVt, int Hkv, int d, int dd, int Tl, int Tp, int perm,
+    int kv0, int Tkv, int lat0, const T* __restrict__ k_lat, const T* __restrict__ v_lat,
+    int cap) {
     extern __shared__ float xs[];  // [2][64][d+1]
     const int bg = wg_id_y();
     const int g = bg % Hkv;
     const int t0 = wg_id_x() * 64;
     const int ld = d + 1;
     const T* wdg = wd + (size_t)g * d * dd;
+    // rows of the positions whose latent is projected here (k/v row = position - kv0)
     for (int which = 0; which < 2; ++which) {
-        const T* x = (which ? v : k) + (size_t)bg * T_ * d;
+        const T* x = (which ? v : k) + (size_t)bg * Tkv * d;
         float* dst = xs + which * 64 * ld;
         for (int idx = lane_id_x(); idx < 64 * d; idx += 256) {
             const int t = idx / d, e = idx - (idx / d) * d;
-            dst[t * ld + e] = (t0 + t < Tl) ? elem<T>::load(x + (size_t)(t0 + t) * d + e) : 0.f;
+            const int p = t0 + t;
+            dst[t * ld + e] = (p < Tl && p >= lat0 && p >= kv0 && p - kv0 < Tkv)
+                                  ? elem<T>::load(x + (size_t)(p - kv0) * d + e) : 0.f;
         }
     }
     __syncthreads();
@@ -58,17 +62,23 @@ __global__ __launch_bounds__(256) void prefill_latent_kernel(
                     acc[j] = __builtin_fmaf(xv, elem<T>::load(wdg + (size_t)e * dd + c0 + j), acc[j]);
         }
         if (t < Tp) {
+            // positions below lat0: the cache's latent, copied
+            const bool fromc = t < lat0;
+            const T* cached = (which ? v_lat : k_lat) + ((size_t)bg * cap + imin(t, imax(lat0 - 1, 0))) * dd;
             if (which == 0) {
                 T* out = cK + ((size_t)bg * Tp + t) * dd;
 #pragma unroll
                 for (int j = 0; j < 8; ++j)
                     if (c0 + j < dd)
-                        out[perm ? latent_pos(c0 + j) : c0 + j] = elem<T>::from_f32(acc[j]);
+                        out[perm ? latent_pos(c0 + j) : c0 + j] =
+                            fromc ? cached[c0 + j] : elem<T>::from_f32(acc[j]);
             } else {
                 T* out = cVt + ((size_t)bg * Tp + (size_t)(t >> 5) * 32) * dd;
 #pragma unroll
                 for (int j = 0; j < 8; ++j)
-                    if (c0 + j < dd) out[(size_t)(c0 + j) * 32 + (t & 31)] = elem<T>::from_f32(acc[j]);
+                    if (c0 + j < dd)
+                        out[(size_t)(c0 + j) * 32 + (t & 31)] =
+                            fromc ? cached[c0 + j] : elem<T>::from_f32(acc[j]);
             }
         }
     }
@@ -207,11 +217,14 @@ __device__ __forceinline__ lf32x16 project_mfma(const lbf16x8 (&wa)[D / 16], con
 
 __device__ __forceinline__ int acc_col(int r, int hg) { return 8 * (r >> 2) + 4 * hg + (r & 3); }
 
-// Prefill pre-pass. Block (x, y) serves 128-token chunk x of (batch, KV
-// head) y; wavefront w takes tokens [32w, 32w + 32) of it. Also writes, per
-// 32-token block, the largest L2 norm of the stored c^K rows (over tokens
-// [0, T - w)) and of the key rows (over all tokens [0, T)); the matrix-core
-// prefill bounds its scores with them.
+// Prefill pre-pass. Block (x, y) serves positions [128x, 128x + 128) of
+// (batch, KV head) y; wavefront w takes positions [32w, 32w + 32) of them.
+// Writes the latents of positions [0, T - w), and per 32-position block the
+// largest L2 norm of the stored c^K rows and of the key rows that k holds
+// (positions [kv0, T)); the matrix-core prefill bounds its scores with them.
+// k and v row t holds position kv0 + t; positions below lat0 take their
+// latents from the cache arrays k_lat / v_lat (row stride cap) instead of a
+// projection (chunked prefill: the tokens that left the window earlier).
 //
 // Latency layout: W_down is requested first and brought into LDS (stored
 // transposed as the A operand rows); the key and value rows are in flight
@@ -222,7 +235,8 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
     const bf16_t* __restrict__ k, const bf16_t* __restrict__ v, const bf16_t* __restrict__ wd,
     bf16_t* __restrict__ cK, bf16_t* __restrict__ cVt, float* __restrict__ cnorm,
     float* __restrict__ knorm, bf16_t* __restrict__ consts, int Hkv, int T_, int dd, int Tl,
-    int Tp) {
+    int Tp, int kv0, int Tkv, int lat0, const bf16_t* __restrict__ k_lat,
+    const bf16_t* __restrict__ v_lat, int cap) {
     constexpr int KS = D / 16;
     constexpr int LDW = D + 8;   // W^T row in LDS (bf16 elements)
     constexpr int LDT = 32 + 8;  // transposed value-latent row in LDS
@@ -237,20 +251,20 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int tl = lane & 31, hg = lane >> 5;
     const int Tk = (T_ + 31) & ~31;
-    const bf16_t* kbase = k + (size_t)bg * T_ * D;
-    const bf16_t* vbase = v + (size_t)bg * T_ * D;
-    const int vlast = imax(Tl, 1) - 1;
+    const bf16_t* kbase = k + (size_t)bg * Tkv * D;
+    const bf16_t* vbase = v + (size_t)bg * Tkv * D;
 
-    // key and value rows of a wavefront's 32 tokens (indices clamped; rows
-    // out of range are zeroed before use)
+    // key and value rows of a wavefront's 32 positions (row indices clamped;
+    // rows of positions k does not hold are zeroed before use)
     struct Rows {
         lbf16x8 k[KS], v[KS];
     };
     auto load = [&](int chunk) {
         Rows r;
         const int t = chunk * 128 + wave * 32 + tl;
-        const bf16_t* kr = kbase + (size_t)imin(t, T_ - 1) * D;
-        const bf16_t* vr = vbase + (size_t)imin(t, vlast) * D;
+        const int row = imax(imin(t - kv0, Tkv - 1), 0);
+        const bf16_t* kr = kbase + (size_t)row * D;
+        const bf16_t* vr = vbase + (size_t)row * D;
 #pragma unroll
         for (int s = 0; s < KS; ++s) {
             r.k[s] = lload8(kr + s * 16 + hg * 8);
@@ -292,7 +306,7 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
             float n2 = 0.f;
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
-                const uint4 u = __builtin_bit_cast(uint4, t < T_ ? cur.k[s] : zero8);
+                const uint4 u = __builtin_bit_cast(uint4, t < T_ && t >= kv0 ? cur.k[s] : zero8);
                 const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
@@ -312,6 +326,23 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
                 xk[s] = t < Tl ? cur.k[s] : zero8;
                 xv[s] = t < Tl ? cur.v[s] : zero8;
             }
+            // Latents read from the cache for positions below lat0: per lane
+            // the columns 8q + 4hg + 0..3 of its token, i.e. the register
+            // pairs (4q, 4q + 1) and (4q + 2, 4q + 3) of the projection.
+            const bool fromc = t < lat0;
+            uint2 ck[4], cv[4];
+#pragma unroll
+            for (int q4 = 0; q4 < 4; ++q4) ck[q4] = cv[q4] = make_uint2(0, 0);
+            if (ts < lat0) {  // wave-uniform
+                const size_t rowc = ((size_t)bg * cap + imin(t, lat0 - 1)) * dd;
+#pragma unroll
+                for (int q4 = 0; q4 < 4; ++q4)
+                    if (8 * q4 < dd) {
+                        ck[q4] = *reinterpret_cast<const uint2*>(k_lat + rowc + 8 * q4 + 4 * hg);
+                        cv[q4] = *reinterpret_cast<const uint2*>(v_lat + rowc + 8 * q4 + 4 * hg);
+                    }
+            }
+            auto cpair = [&](const uint2 (&c)[4], int m) { return (m & 1) ? c[m >> 1].y : c[m >> 1].x; };
             // key latents: token-major, columns in latent_pos order, plus the norm
             {
                 const lf32x16 acc = project_mfma<D>(wa, xk);
@@ -321,7 +352,7 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
                 uint32_t pk[8];  // the row's bf16 values, pairs of registers
 #pragma unroll
                 for (int r = 0; r < 16; r += 2) {
-                    const uint32_t u = rne_pack2(acc[r], acc[r + 1]);
+                    const uint32_t u = fromc ? cpair(ck, r >> 1) : rne_pack2(acc[r], acc[r + 1]);
                     pk[r >> 1] = u;
                     const float c0 = __uint_as_float(u << 16), c1 = __uint_as_float(u & 0xffff0000u);
                     n2 = __builtin_fmaf(c0, c0, n2);
@@ -345,7 +376,7 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
                 // all 32 rows of the block (rows past d_down are zero and not read)
 #pragma unroll
                 for (int r = 0; r < 16; r += 2) {
-                    const uint32_t u = rne_pack2(acc[r], acc[r + 1]);
+                    const uint32_t u = fromc ? cpair(cv, r >> 1) : rne_pack2(acc[r], acc[r + 1]);
                     tb[acc_col(r, hg) * LDT + tl] = (bf16_t)(u & 0xffffu);
                     tb[acc_col(r + 1, hg) * LDT + tl] = (bf16_t)(u >> 16);
                 }
@@ -422,8 +453,9 @@ static bool mfma_projection(int d, int dd) { return (d == 64 || d == 128) && dd 
 
 template <typename T>
 static hipError_t launch_prefill_latent_valu(const T* k, const T* v, const T* wd, T* cK, T* cVt,
-                                             int B, int Hkv, int T_, int d, int dd, int w,
-                                             bool perm, hipStream_t st) {
+                                             int B, int Hkv, const PrefillGeo& geo, int d, int dd,
+                                             int w, bool perm, hipStream_t st) {
+    const int T_ = geo.total();
     const int Tl = T_ - w;
     if (Tl <= 0) return hipSuccess;
     const int Tp = prefill_tp(T_, w);
@@ -435,7 +467,8 @@ static hipError_t launch_prefill_latent_valu(const T* k, const T* v, const T* wd
         if (e != hipSuccess) return e;
     }
     hipLaunchKernelGGL(prefill_latent_kernel<T>, grid, dim3(256), lds, st, k, v, wd, cK, cVt, Hkv,
-                       T_, d, dd, Tl, Tp, perm ? 1 : 0);
+                       d, dd, Tl, Tp, perm ? 1 : 0, geo.kv0, geo.Tkv, geo.lat0,
+                       (const T*)geo.k_lat, (const T*)geo.v_lat, geo.cap);
     return hipGetLastError();
 }
 
@@ -469,21 +502,22 @@ static hipError_t launch_append_valu(const T* k_new, const T* v_new, const T* wd
 template <>
 hipError_t launch_prefill_latent<bf16_t>(const bf16_t* k, const bf16_t* v, const bf16_t* wd,
                                          bf16_t* cK, bf16_t* cVt, float* cnorm, float* knorm,
-                                         bf16_t* consts, int B, int Hkv, int T_, int d, int dd,
-                                         int w, bool perm, hipStream_t st) {
+                                         bf16_t* consts, int B, int Hkv, const PrefillGeo& geo,
+                                         int d, int dd, int w, bool perm, hipStream_t st) {
+    const int T_ = geo.total();
     const int Tl = T_ - w;
     const int Tp = prefill_tp(T_, w);
     if (!perm || !mfma_projection(d, dd)) {
         if (Tl <= 0) return hipSuccess;
-        return launch_prefill_latent_valu<bf16_t>(k, v, wd, cK, cVt, B, Hkv, T_, d, dd, w, perm, st);
+        return launch_prefill_latent_valu<bf16_t>(k, v, wd, cK, cVt, B, Hkv, geo, d, dd, w, perm, st);
     }
     const int Tk = (T_ + 31) & ~31;
     const int ntok = Tp > Tk ? Tp : Tk;
     dim3 grid((ntok + 127) / 128, B * Hkv);
-    if (d == 64)
-        hipLaunchKernelGGL(prefill_latent_mfma_kernel<64>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv, T_, dd, Tl, Tp);
-    else
-        hipLaunchKernelGGL(prefill_latent_mfma_kernel<128>, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv, T_, dd, Tl, Tp);
+    auto kern = d == 64 ? prefill_latent_mfma_kernel<64> : prefill_latent_mfma_kernel<128>;
+    hipLaunchKernelGGL(kern, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv,
+                       T_, dd, Tl, Tp, geo.kv0, geo.Tkv, geo.lat0, (const bf16_t*)geo.k_lat,
+                       (const bf16_t*)geo.v_lat, geo.cap);
     return hipGetLastError();
 }
 
@@ -509,14 +543,55 @@ hipError_t launch_append<bf16_t>(const bf16_t* k_new, const bf16_t* v_new, const
 
 template <typename T>
 hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt,
-                                 float* cnorm, float* knorm, T* consts, int B, int Hkv, int T_,
-                                 int d, int dd, int w, bool perm, hipStream_t st) {
+                                 float* cnorm, float* knorm, T* consts, int B, int Hkv,
+                                 const PrefillGeo& geo, int d, int dd, int w, bool perm,
+                                 hipStream_t st) {
     (void)cnorm;   // only the matrix-core prefill reads the norms
     (void)knorm;
     (void)consts;  // and the constant rows
-    if (T_ - w <= 0) return hipSuccess;
-    return launch_prefill_latent_valu<T>(k, v, wd, cK, cVt, B, Hkv, T_, d, dd, w, perm, st);
+    if (geo.total() - w <= 0) return hipSuccess;
+    return launch_prefill_latent_valu<T>(k, v, wd, cK, cVt, B, Hkv, geo, d, dd, w, perm, st);
 }
+
+// One thread per 4-byte word of a context row; positions below len come from
+// the ring (slot p % w), the others from the new tokens.
+template <typename T>
+__global__ __launch_bounds__(256) void chunk_gather_kernel(
+    const T* __restrict__ k_win, const T* __restrict__ v_win, const T* __restrict__ k_new,
+    const T* __restrict__ v_new, T* __restrict__ ctx_k, T* __restrict__ ctx_v, int d, int w,
+    int len, int n, int kv0, int Tc) {
+    const int bg = wg_id_y();
+    const int words = d * (int)sizeof(T) / 4;  // d * esize is a multiple of 4
+    const long long idx = (long long)wg_id_x() * 256 + lane_id_x();
+    if (idx >= (long long)Tc * words) return;
+    const int r = (int)(idx / words), wd4 = (int)(idx - (long long)r * words);
+    const int p = kv0 + r;
+    const size_t src_row = p < len ? (size_t)bg * w + p % w : (size_t)bg * n + (p - len);
+    const uint32_t* sk = reinterpret_cast<const uint32_t*>(p < len ? k_win : k_new) + src_row * words;
+    const uint32_t* sv = reinterpret_cast<const uint32_t*>(p < len ? v_win : v_new) + src_row * words;
+    const size_t dst = ((size_t)bg * Tc + r) * words + wd4;
+    reinterpret_cast<uint32_t*>(ctx_k)[dst] = sk[wd4];
+    reinterpret_cast<uint32_t*>(ctx_v)[dst] = sv[wd4];
+}
+
+template <typename T>
+hipError_t launch_chunk_gather(const T* k_win, const T* v_win, const T* k_new, const T* v_new,
+                               T* ctx_k, T* ctx_v, int B, int Hkv, int d, int w, int len, int n,
+                               int kv0, hipStream_t st) {
+    const int Tc = len + n - kv0;
+    const long long words = (long long)Tc * d * (long long)sizeof(T) / 4;
+    dim3 grid((unsigned)((words + 255) / 256), B * Hkv);
+    hipLaunchKernelGGL(chunk_gather_kernel<T>, grid, dim3(256), 0, st, k_win, v_win, k_new, v_new,
+                       ctx_k, ctx_v, d, w, len, n, kv0, Tc);
+    return hipGetLastError();
+}
+
+template hipError_t launch_chunk_gather<float>(const float*, const float*, const float*,
+                                               const float*, float*, float*, int, int, int, int,
+                                               int, int, int, hipStream_t);
+template hipError_t launch_chunk_gather<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
+                                                const bf16_t*, bf16_t*, bf16_t*, int, int, int,
+                                                int, int, int, int, hipStream_t);
 
 template <typename T>
 hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, T* v_win,
@@ -526,8 +601,9 @@ hipError_t launch_append(const T* k_new, const T* v_new, const T* wd, T* k_win, 
 }
 
 template hipError_t launch_prefill_latent<float>(const float*, const float*, const float*, float*,
-                                                 float*, float*, float*, float*, int, int, int, int,
-                                                 int, int, bool, hipStream_t);
+                                                 float*, float*, float*, float*, int, int,
+                                                 const PrefillGeo&, int, int, int, bool,
+                                                 hipStream_t);
 template hipError_t launch_append<float>(const float*, const float*, const float*, float*, float*,
                                          float*, float*, int, int, int, int, int, int, int, int,
                                          hipStream_t);

@@ -185,9 +185,11 @@ __device__ __forceinline__ float dot8(bf16x8_t a, bf16x8_t b, float acc) {
     return acc;
 }
 
-// Everything a wavefront needs to walk one row block.
+// Everything a wavefront needs to walk one row block. Row indices are
+// positions (r0, i, i_hi < T); key/value row t of k and v holds position
+// kv0 + t (t < Tkv).
 struct RowCtx {
-    int T, w, Tp, r0, i, i_hi, qc, hg, prow, bg, tid;
+    int T, w, Tp, r0, i, i_hi, qc, hg, prow, bg, tid, kv0, Tkv;
     float c_scale;
 };
 
@@ -341,18 +343,18 @@ __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t
     const int jb_lo = imax(0, i0 - w + 1);
     const int t_first = jb_lo & ~(BN - 1);
     const int ntile = (iwg_hi - t_first) / BN + 1;
-    const bf16_t* kb = k + (size_t)c.bg * T * D;
-    const bf16_t* vb = v + (size_t)c.bg * T * D;
+    const bf16_t* kb = k + (size_t)c.bg * c.Tkv * D;
+    const bf16_t* vb = v + (size_t)c.bg * c.Tkv * D;
     uint4 pk[CH], pv[CH];
     auto gload = [&](int t0) {
 #pragma unroll
         for (int q = 0; q < CH; ++q) {
             const int chunk = c.tid + q * NW * 64;
             const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
-            const int key = t0 + row;
-            if (key < T) {
-                pk[q] = *reinterpret_cast<const uint4*>(kb + (size_t)key * D + col);
-                pv[q] = *reinterpret_cast<const uint4*>(vb + (size_t)key * D + col);
+            const int key = t0 + row;  // (keys below kv0 are never local: masked)
+            if (key < T && key >= c.kv0) {
+                pk[q] = *reinterpret_cast<const uint4*>(kb + (size_t)(key - c.kv0) * D + col);
+                pv[q] = *reinterpret_cast<const uint4*>(vb + (size_t)(key - c.kv0) * D + col);
             } else {
                 pk[q] = make_uint4(0, 0, 0, 0);
                 pv[q] = make_uint4(0, 0, 0, 0);
@@ -439,8 +441,8 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
     const int jb_lo = imax(0, i0 - w + 1);
     const int t_first = jb_lo & ~(BN - 1);
     const int ntile = (iwg_hi - t_first) / BN + 1;
-    const bf16_t* kb = k + (size_t)c.bg * T * D;
-    const bf16_t* vb = v + (size_t)c.bg * T * D;
+    const bf16_t* kb = k + (size_t)c.bg * c.Tkv * D;
+    const bf16_t* vb = v + (size_t)c.bg * c.Tkv * D;
     // d = 64: two register sets; the loads of tile n+2 are issued when tile n
     // starts and reach LDS when tile n+1 ends, so two tiles of work cover
     // their latency.
@@ -456,8 +458,10 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
             const int chunk = c.tid + q * NW * 64;
             const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
             // keys past the sequence repeat its last key: their scores are
-            // masked (j > i) and their weights are zero
-            const int key = imin(t0 + row, T - 1);
+            // masked (j > i) and their weights are zero; keys below kv0 (the
+            // first rows a tile start rounded down may cover) are never local
+            // and read row 0
+            const int key = imax(imin(t0 + row, T - 1) - c.kv0, 0);
             r.k[q] = *reinterpret_cast<const uint4*>(kb + (size_t)key * D + col);
             r.v[q] = *reinterpret_cast<const uint4*>(vb + (size_t)key * D + col);
         }
@@ -548,7 +552,7 @@ void prefill_mfma_kernel(
     const bf16_t* __restrict__ cVt, const float* __restrict__ cnorm,
     const float* __restrict__ knorm, const bf16_t* __restrict__ consts, bf16_t* __restrict__ o,
     float* __restrict__ lse, int Hq, int Hkv, int T, int w, int Tp, int nblk, int BH,
-    float c_scale) {
+    float c_scale, int q0, int n_rows, int kv0, int Tkv) {
     constexpr int BM = NW * 32;
     constexpr int KS = D / 16;   // 16-wide k slabs of q . k
     constexpr int DS = DD / 16;  // 16-wide k slabs of q~ . c^K
@@ -624,7 +628,9 @@ void prefill_mfma_kernel(
         c.bg = bg;
         c.tid = tid;
         c.c_scale = c_scale;
-        const int i0 = rb * BM;
+        c.kv0 = kv0;
+        c.Tkv = Tkv;
+        const int i0 = q0 + rb * BM;  // position of the block's first row
         c.r0 = i0 + wave * 32;
         c.i = c.r0 + c.qc;
         c.i_hi = imin(c.r0 + 31, T - 1);  // last real row of this wavefront (< r0 if none)
@@ -639,13 +645,13 @@ void prefill_mfma_kernel(
         // Every global load of the setup is issued here, before any of its
         // results is used: the query row, the row's own key or latent (the
         // witness), and the first norm maxima of both regions.
-        const bf16_t* qrow = q + ((size_t)bh * T + ii) * D;
+        const bf16_t* qrow = q + ((size_t)bh * n_rows + (ii - q0)) * D;
         bf16x8_t qop[KS];  // B operand of S^T = K Q^T: q[i][s*16 + hg*8 + 0..7]
 #pragma unroll
         for (int s = 0; s < KS; ++s) qop[s] = load_bf16x8(qrow + s * 16 + hg * 8);
         bf16x8_t wit[KS];  // own key (w >= 1) or own latent key (w = 0)
         if (w >= 1) {
-            const bf16_t* krow = k + ((size_t)bg * T + ii) * D;
+            const bf16_t* krow = k + ((size_t)bg * Tkv + (ii - kv0)) * D;
 #pragma unroll
             for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(krow + s * 16 + hg * 8);
         } else {
@@ -785,9 +791,9 @@ void prefill_mfma_kernel(
 
         if (i < T) {
             // log of the row's softmax denominator (natural log), for a backward pass
-            if (lse && hg == 0) lse[(size_t)bh * T + i] = (st.m + log2f(lt)) * 0.6931471805599453f;
+            if (lse && hg == 0) lse[(size_t)bh * n_rows + (i - q0)] = (st.m + log2f(lt)) * 0.6931471805599453f;
             const float inv = 1.f / lt;
-            bf16_t* orow = o + ((size_t)bh * T + i) * D;
+            bf16_t* orow = o + ((size_t)bh * n_rows + (i - q0)) * D;
 #pragma unroll
             for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -810,13 +816,14 @@ bool prefill_mfma_supported(const dar_shape* s) {
 }
 
 template <int D, int DD>
-static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q, const void* k,
+static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w, const void* q, const void* k,
                             const void* v, const void* wd, const void* wu, void* o, float* lse,
                             const void* cK, const void* cVt, const float* cnorm,
                             const float* knorm, const void* consts, hipStream_t st) {
     constexpr int NW = 4;
     constexpr int BM = NW * 32;
-    const int nblk = (T + BM - 1) / BM;
+    const int T = geo.total();
+    const int nblk = (geo.n_rows + BM - 1) / BM;
     const int npair = (nblk + 1) / 2;
     const int BH = B * Hq;
     const int Tp = prefill_tp(T, w);
@@ -830,19 +837,20 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, int T, int w, const void* q,
     hipLaunchKernelGGL(kern, dim3(npair * BH), dim3(NW * 64), lds, st, (const bf16_t*)q,
                        (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)wd, (const bf16_t*)wu,
                        (const bf16_t*)cK, (const bf16_t*)cVt, cnorm, knorm, (const bf16_t*)consts,
-                       (bf16_t*)o, lse, Hq, Hkv, T, w, Tp, nblk, BH, c_scale);
+                       (bf16_t*)o, lse, Hq, Hkv, T, w, Tp, nblk, BH, c_scale, geo.q0,
+                       geo.n_rows, geo.kv0, geo.Tkv);
     return hipGetLastError();
 }
 
-hipError_t launch_prefill_mfma(const dar_shape* s, int T, const void* q, const void* k,
+hipError_t launch_prefill_mfma(const dar_shape* s, const PrefillGeo& geo, const void* q, const void* k,
                                const void* v, const void* wd, const void* wu, void* o, float* lse,
                                const void* cK, const void* cVt, const float* cnorm,
                                const float* knorm, const void* consts, hipStream_t st) {
     const int B = s->B, Hq = s->Hq, Hkv = s->Hkv, w = s->w;
-    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
-    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
-    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
-    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, T, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
     return hipErrorNotSupported;
 }
 

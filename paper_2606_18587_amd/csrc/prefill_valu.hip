@@ -1,7 +1,9 @@
 // Generic causal DAR prefill on the vector ALUs (fp32 path, and the fallback
 // for bf16 head sizes the matrix-core kernel does not cover).
 //
-// One wavefront per (query row i, batch * query head). For row i the keys
+// One wavefront per (query row, batch * query head); row r is the query at
+// position i = q0 + r (q0 = 0 for a whole sequence, the cache length for a
+// chunk appended to a cache), and k/v row t holds position kv0 + t. For row i the keys
 // j <= i - w are distant: their score is q~ . c^K_j with q~ = q W_up^T, their
 // value contribution is accumulated in d_down space and lifted once at the
 // end, (sum_j p_j c^V_j) W_up (Eq. 2 absorbed, Limitations section). The keys
@@ -19,13 +21,14 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ wd, const T* __restrict__ wu, const T* __restrict__ cK,
     const T* __restrict__ cVt, T* __restrict__ o, float* __restrict__ lse, int Hq, int Hkv,
-    int T_, int d, int dd, int w, int Tp, float qscale) {
+    int q0, int n_rows, int kv0, int Tkv, int d, int dd, int w, int Tp, float qscale) {
     __shared__ float qs[256];
     __shared__ float qts[256];
     __shared__ float ps[64];
     __shared__ float lat[256];
     const int lane = lane_id_x();
-    const int i = (T_ - 1) - wg_id_x();  // longest rows are launched first
+    const int row = (n_rows - 1) - wg_id_x();  // longest rows are launched first
+    const int i = q0 + row;                    // its position
     const int bh = wg_id_y();
     const int b = bh / Hq, h = bh - (bh / Hq) * Hq;
     const int g = h / (Hq / Hkv);
@@ -33,7 +36,7 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
     const T* wdg = wd + (size_t)g * d * dd;
     const T* wug = wu ? wu + (size_t)g * dd * d : nullptr;
 
-    const T* qrow = q + ((size_t)bh * T_ + i) * d;
+    const T* qrow = q + ((size_t)bh * n_rows + row) * d;
     for (int e = lane; e < d; e += 64) qs[e] = elem<T>::load(qrow + e) * qscale;
     __syncthreads();
 
@@ -92,13 +95,13 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
 
     // local region (the window, including the query's own token), d wide
     const int j_lo = imax(0, i - w + 1);
-    const T* kg = k + (size_t)bg * T_ * d;
-    const T* vg = v + (size_t)bg * T_ * d;
+    const T* kg = k + (size_t)bg * Tkv * d;  // row of position j: j - kv0
+    const T* vg = v + (size_t)bg * Tkv * d;
     for (int j0 = j_lo; j0 <= i; j0 += 64) {
         const int j = j0 + lane;
         float s = -INFINITY;
         if (j <= i) {
-            const T* kr = kg + (size_t)j * d;
+            const T* kr = kg + (size_t)(j - kv0) * d;
             float acc = 0.f;
             for (int e = 0; e < d; ++e) acc = __builtin_fmaf(qs[e], elem<T>::load(kr + e), acc);
             s = acc;
@@ -115,7 +118,7 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
         const int cnt = imin(64, i + 1 - j0);
         for (int jj = 0; jj < cnt; ++jj) {
             const float pj = ps[jj];
-            const T* vr = vg + (size_t)(j0 + jj) * d;
+            const T* vr = vg + (size_t)(j0 + jj - kv0) * d;
 #pragma unroll
             for (int r = 0; r < 4; ++r) {
                 const int e = lane + 64 * r;
@@ -132,10 +135,10 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
         if (c < dd) lat[c] = al[r];
     }
     __syncthreads();
-    T* orow = o + ((size_t)bh * T_ + i) * d;
+    T* orow = o + ((size_t)bh * n_rows + row) * d;
     const float inv_l = 1.f / l;
     // log of the row's softmax denominator (natural log), for a backward pass
-    if (lse && lane == 0) lse[(size_t)bh * T_ + i] = (m + log2f(l)) * 0.6931471805599453f;
+    if (lse && lane == 0) lse[(size_t)bh * n_rows + row] = (m + log2f(l)) * 0.6931471805599453f;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
         const int e = lane + 64 * r;
@@ -155,22 +158,23 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
 template <typename T>
 hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, const T* wu,
                                const T* cK, const T* cVt, T* o, float* lse, int B, int Hq,
-                               int Hkv, int T_, int d, int dd, int w, hipStream_t st) {
-    const int Tp = prefill_tp(T_, w);
+                               int Hkv, const PrefillGeo& geo, int d, int dd, int w,
+                               hipStream_t st) {
+    const int Tp = prefill_tp(geo.total(), w);
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
-    dim3 grid(T_, B * Hq);
+    dim3 grid(geo.n_rows, B * Hq);
     hipLaunchKernelGGL(prefill_valu_kernel<T>, grid, dim3(64), 0, st, q, k, v, wd, wu, cK, cVt, o,
-                       lse, Hq, Hkv, T_, d, dd, w, Tp, qscale);
+                       lse, Hq, Hkv, geo.q0, geo.n_rows, geo.kv0, geo.Tkv, d, dd, w, Tp, qscale);
     return hipGetLastError();
 }
 
 template hipError_t launch_prefill_valu<float>(const float*, const float*, const float*,
                                                const float*, const float*, const float*,
-                                               const float*, float*, float*, int, int, int, int,
-                                               int, int, int, hipStream_t);
+                                               const float*, float*, float*, int, int, int,
+                                               const PrefillGeo&, int, int, int, hipStream_t);
 template hipError_t launch_prefill_valu<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
                                                 const bf16_t*, const bf16_t*, const bf16_t*,
-                                                const bf16_t*, bf16_t*, float*, int, int, int, int,
-                                                int, int, int, hipStream_t);
+                                                const bf16_t*, bf16_t*, float*, int, int, int,
+                                                const PrefillGeo&, int, int, int, hipStream_t);
 
 }  // namespace dar

@@ -32,6 +32,7 @@ def test_exports_every_declared_symbol():
     assert set(names) == {"dar_attn_prefill", "dar_cache_append", "dar_attn_decode",
                           "dar_attn_prefill_backward", "dar_prefill_workspace_bytes",
                           "dar_decode_workspace_bytes", "dar_prefill_backward_workspace_bytes",
+                          "dar_attn_prefill_chunk", "dar_prefill_chunk_workspace_bytes",
                           "dar_status_string"}
     raw = ctypes.CDLL(dar.LIB_PATH)
     for n in names:
@@ -228,3 +229,46 @@ def call_backward(shape, T=16, wu=None, dwu=None, ws=FAKE, ws_bytes=1 << 30, **k
 def test_backward_rejects(kw, shape_kw, expect):
     assert call_backward(S(**shape_kw), **kw) == expect
 
+
+
+def test_chunk_workspace_size():
+    """Context copy of K and V (ring tokens from max(0, len - w), then the n new
+    ones) followed by the prefill workspace of len + n positions."""
+    al = lambda x: (x + 255) // 256 * 256
+    for (B, Hq, Hkv, d, dd, w, dt, es), (L, n) in [((2, 4, 2, 64, 16, 8, torch.bfloat16, 2), (100, 7)),
+                                                   ((2, 4, 2, 64, 16, 8, torch.bfloat16, 2), (3, 50)),
+                                                   ((1, 2, 2, 16, 4, 0, torch.float32, 4), (40, 9))]:
+        s = dar.make_shape(B, Hq, Hkv, d, dd, w, dt)
+        kv0 = max(0, L - w)
+        ctx = al(B * Hkv * (L + n - kv0) * d * es)
+        want = 2 * ctx + expected_prefill_ws(B, Hkv, L + n, dd, w, es)
+        assert dar.dar_prefill_chunk_workspace_bytes(s, L, n) == want
+    s = S()
+    assert dar.dar_prefill_chunk_workspace_bytes(s, 10, 0) == 0    # n >= 1
+    assert dar.dar_prefill_chunk_workspace_bytes(s, -1, 4) == 0    # len >= 0
+    assert dar.dar_prefill_chunk_workspace_bytes(S(Hq=3), 4, 4) == 0
+
+
+def call_chunk(shape, c, n=5, q=FAKE, k=FAKE, v=FAKE, wd=FAKE, wu=None, o=FAKE, lse=None,
+               ws=FAKE, ws_bytes=1 << 30):
+    return dar.lib.dar_attn_prefill_chunk(ctypes.byref(shape), ctypes.byref(c), n, q, k, v, wd,
+                                          wu, o, lse, ws, ws_bytes, None)
+
+
+@no_gpu
+def test_chunk_rejects_before_any_launch():
+    s = S()
+    c = cache_struct(cap=64, length=60)
+    assert call_chunk(s, c, n=5) == dar.DAR_E_CAPACITY and c.len == 60
+    assert call_chunk(s, c, n=0) == dar.DAR_E_ARG and c.len == 60
+    assert call_chunk(s, c, n=2, q=None) == dar.DAR_E_ARG and c.len == 60
+    assert call_chunk(s, c, n=2, k=MISALIGNED) == dar.DAR_E_ARG and c.len == 60
+    assert call_chunk(s, c, n=2, wu=MISALIGNED) == dar.DAR_E_ARG and c.len == 60
+    assert call_chunk(s, c, n=2, lse=MISALIGNED) == dar.DAR_E_ARG and c.len == 60
+    assert call_chunk(s, c, n=2, ws_bytes=64) == dar.DAR_E_WORKSPACE and c.len == 60
+    assert call_chunk(s, c, n=2, ws=None, ws_bytes=0) == dar.DAR_E_WORKSPACE and c.len == 60
+    assert call_chunk(S(Hq=3), c, n=2) == dar.DAR_E_ARG and c.len == 60
+    c2 = cache_struct(win=None)  # a ring is required when w > 0
+    assert call_chunk(s, c2, n=2) == dar.DAR_E_ARG and c2.len == 0
+    # bf16 rows of an odd number of elements cannot be copied in 4-byte words
+    assert call_chunk(S(d=63, dd=16), cache_struct(), n=2) == dar.DAR_E_UNSUPPORTED
