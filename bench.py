@@ -73,6 +73,19 @@ def head_start(torch, steps):
     torch.cuda._sleep(int(2.4e9 * 1e-3 * steps))
 
 
+CHUNK_N = 256       # new tokens per chunked-prefill call
+CHUNK_CALLS = 5     # timed chunked-prefill calls
+
+
+def chunk_flops(B, Hq, L, n, d, dd, w):
+    """Rows L..L+n-1 of a causal prefill: 4 d flop per window pair, 4 d_down
+    per distant pair."""
+    i = np.arange(L, L + n, dtype=np.int64)
+    nl = np.minimum(i + 1, w).sum()
+    nd = (i + 1).sum() - nl
+    return float(B * Hq * (4 * d * nl + 4 * dd * nd))
+
+
 def prefill_flops(B, Hq, T, d, dd, w):
     """Algorithmic flops: QK^T and PV at 2 flop/MAC, d wide inside the window,
     d_down wide beyond it; masked and skipped work is not counted."""
@@ -111,6 +124,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the separately timed prefill backward")
+    ap.add_argument("--no-chunk", action="store_true",
+                    help="skip the chunked prefill into the decode cache")
     ap.add_argument("--no-other-prefill", action="store_true",
                     help="skip the prefill workloads reported beside the main one")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -154,7 +169,7 @@ def main():
     dw = di.WORKLOADS["decode1b"]
     t0 = time.time()
     pre = di.make_decode_prefix(dw, dw.T)
-    cap = dw.T + args.warmup + 2 * args.steps + 1
+    cap = dw.T + args.warmup + 2 * args.steps + 1 + (CHUNK_CALLS + 1) * CHUNK_N
     cache = dar.DarCache(dw.B, dw.Hkv, dw.d, dw.dd, dw.w, cap, torch.bfloat16, device=dev)
     dwd = up(pre["wd"])
     kpre, vpre = up(pre["k"]), up(pre["v"])
@@ -209,6 +224,34 @@ def main():
                    args.steps)
     app_ms = timed(lambda i: dar.dar_cache_append(cache, step_in[i][1], step_in[i][2], dwd,
                                                   Hq=dw.Hq), args.steps)
+
+    # chunked prefill into the same decode cache: chunks of CHUNK_N new tokens
+    # (seeded N(0,1) queries, keys and values; the same tensors each call, at
+    # advancing positions) attend to the ring, the latents and each other
+    chunk = None
+    if not args.no_chunk:
+        gc = torch.Generator(device=dev).manual_seed(260618587)
+        cq = torch.randn(dw.B, dw.Hq, CHUNK_N, dw.d, device=dev, generator=gc).bfloat16()
+        ck = torch.randn(dw.B, dw.Hkv, CHUNK_N, dw.d, device=dev, generator=gc).bfloat16()
+        cv = torch.randn(dw.B, dw.Hkv, CHUNK_N, dw.d, device=dev, generator=gc).bfloat16()
+        co = torch.empty_like(cq)
+        n_chunk = CHUNK_CALLS
+        cws = torch.empty(dar.dar_prefill_chunk_workspace_bytes(
+            dshape, cache.len + (n_chunk + 1) * CHUNK_N, CHUNK_N), dtype=torch.uint8, device=dev)
+        run_chunk = lambda i: dar.dar_attn_prefill_chunk(cache, cq, ck, cv, dwd, None, o=co, ws=cws,
+                                                         check=False)
+        run_chunk(0)  # warm-up
+        L0 = cache.len
+        ch_ms = timed(run_chunk, n_chunk)
+        cfl = np.mean([chunk_flops(dw.B, dw.Hq, L0 + c * CHUNK_N, CHUNK_N, dw.d, dw.dd, dw.w)
+                       for c in range(n_chunk)])
+        ctf = cfl / (ch_ms * 1e-3) / 1e12
+        chunk = {"shape": "B%d Hq%d Hkv%d d%d d_down%d w%d, %d new tokens per call" % (
+                     dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, CHUNK_N),
+                 "cache_len": [L0, cache.len], "us": round(ch_ms * 1e3, 1),
+                 "tflops": round(ctf, 2), "frac_bf16_peak": round(ctf / PEAK_BF16_TFLOPS, 4),
+                 "alg_flop": cfl}
+        del cws, cq, ck, cv, co
 
     pre_us = float(pre_ms * 1e3)
     dec_us = float(dec_ms * 1e3)
@@ -301,6 +344,8 @@ def main():
     }
     if other:
         result["prefill_other"] = other
+    if chunk is not None:
+        result["prefill_chunk"] = chunk
     if bwd is not None:
         result["backward"] = bwd
         result["roofline_backward"] = {
