@@ -42,13 +42,13 @@ CSRC = os.path.join(ROOT, "paper_2606_18587_amd", "csrc")
 MEASURED_TRAFFIC = {
     "prefill": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "latent.hip",
                           "prefill_mfma.hip"],
-                "sha256_16": "90d0482f3f5ed5e6", "bytes": 130236768},
+                "sha256_16": "496d0f0d231a78c4", "bytes": 133232730},
     "decode": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "decode.hip",
                          "decode_mfma.hip"],
-               "sha256_16": "8c83ffdc9fa769b7", "bytes": 579741696},
+               "sha256_16": "fbe8dff6aaceaf56", "bytes": 574064716},
     "backward": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "mfma_common.hpp",
                            "backward.hip", "backward_mfma.hip"],
-                 "sha256_16": "6ae715f1a0e503fb", "bytes": 504779744},
+                 "sha256_16": "20943a1f92990983", "bytes": 500968430},
 }
 
 
