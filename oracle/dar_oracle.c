@@ -18,8 +18,10 @@
  *           both regions, since the lifted key has dimension d.
  *
  * The method's readings taken here (bottleneck per KV head acting on k and v,
- * no rotary embedding inside the boundary, 0-based positions) are listed in
- * the design notes of the repository.
+ * 0-based positions) are listed in the design notes of the repository. The
+ * functions without "rope" in their name leave rotary position embedding to
+ * the caller; dar_oracle_rows_rope / dar_oracle_prefill_rope put it where
+ * Eq. 3 does (after the lift on the distant path).
  *
  * Parallelism: OpenMP over independent query rows only; every row is the
  * plain sequential definition above.
@@ -337,4 +339,135 @@ int dar_oracle_backward(int B, int Hq, int Hkv, int T, int d, int dd, int w, con
     free(pwd);
     free(pwu);
     return bad ? -1 : 0;
+}
+
+/*
+ * Rotary position embedding inside Eq. 3 (the paper applies RoPE to the key
+ * of both paths: to the token's own key in the window, and to the key
+ * computed from the lifted representation beyond it; values are not
+ * rotated, and the query is rotated at its own position as usual).
+ *
+ * Pairing: rotate-half (the GPT-NeoX convention of the Pythia models the
+ * paper trains): for m < r/2 the pair (x[m], x[m + r/2]) of a row at
+ * position p is turned by the angle p * base^(-2m/r); elements r..d-1 are
+ * left unchanged (a partial rotary dimension, r < d, is allowed).
+ *
+ * out[t][.] = RoPE(x[t][.], pos[t]) for t < n. r even, 0 <= r <= d.
+ */
+void dar_oracle_rope(int n, int d, int r, double base, const int* pos, const double* x,
+                     double* out)
+{
+    const int half = r / 2;
+    for (int t = 0; t < n; ++t) {
+        const double* xr = x + (size_t)t * d;
+        double* yr = out + (size_t)t * d;
+        for (int e = 0; e < d; ++e) yr[e] = xr[e];
+        for (int m = 0; m < half; ++m) {
+            const double ang = (double)pos[t] * pow(base, -2.0 * m / r);
+            const double c = cos(ang), s = sin(ang);
+            yr[m] = xr[m] * c - xr[m + half] * s;
+            yr[m + half] = xr[m + half] * c + xr[m] * s;
+        }
+    }
+}
+
+/* The angle table: tab[p][m] = cos(p * base^(-2m/r)), tab[p][r/2 + m] = the
+ * sine, for p < n_pos and m < r/2. */
+void dar_oracle_rope_table(int r, double base, int n_pos, double* tab)
+{
+    const int half = r / 2;
+    for (int p = 0; p < n_pos; ++p)
+        for (int m = 0; m < half; ++m) {
+            const double ang = (double)p * pow(base, -2.0 * m / r);
+            tab[(size_t)p * r + m] = cos(ang);
+            tab[(size_t)p * r + half + m] = sin(ang);
+        }
+}
+
+/*
+ * Query rows of one head with RoPE inside Eq. 3. Token j sits at position
+ * pos0 + j; the query of row r at position pos0 + pos[r].
+ *   window key    RoPE(k_j)                    value v_j
+ *   distant key   RoPE((k_j W_down) W_up)      value (v_j W_down) W_up
+ * Other arguments as for dar_oracle_rows (k, v, qr are un-rotated).
+ */
+int dar_oracle_rows_rope(int T, int d, int dd, int w, int r, double base, int pos0,
+                         const double* k, const double* v, const double* wd, const double* wu,
+                         int n_rows, const int* pos, const double* qr, double* o, double* lse)
+{
+    if (T < 1 || d < 1 || dd < 1 || w < 0 || n_rows < 0 || r < 0 || r > d || (r & 1) ||
+        pos0 < 0 || !(base > 0.0))
+        return -1;
+    for (int i = 0; i < n_rows; ++i)
+        if (pos[i] < 0 || pos[i] >= T) return -1;
+    int* tpos = (int*)malloc(sizeof(int) * (size_t)T);
+    int* qpos = (int*)malloc(sizeof(int) * (size_t)(n_rows > 0 ? n_rows : 1));
+    double* kr = (double*)malloc(sizeof(double) * (size_t)T * d);
+    double* klr = (double*)malloc(sizeof(double) * (size_t)T * d);
+    double* qrr = (double*)malloc(sizeof(double) * (size_t)(n_rows > 0 ? n_rows : 1) * d);
+    double* kl = lift_all(T, d, dd, k, wd, wu);
+    double* vl = lift_all(T, d, dd, v, wd, wu);
+    int bad = !tpos || !qpos || !kr || !klr || !qrr || !kl || !vl;
+    if (!bad) {
+        for (int j = 0; j < T; ++j) tpos[j] = pos0 + j;
+        for (int i = 0; i < n_rows; ++i) qpos[i] = pos0 + pos[i];
+        dar_oracle_rope(T, d, r, base, tpos, k, kr);      /* window keys */
+        dar_oracle_rope(T, d, r, base, tpos, kl, klr);    /* distant keys, after the lift */
+        dar_oracle_rope(n_rows, d, r, base, qpos, qr, qrr);
+#pragma omp parallel
+        {
+            double* s = (double*)malloc(sizeof(double) * (size_t)T);
+            if (!s) {
+#pragma omp atomic write
+                bad = 1;
+            } else {
+#pragma omp for schedule(dynamic, 4)
+                for (int i = 0; i < n_rows; ++i)
+                    one_row(d, w, pos[i], qrr + (size_t)i * d, kr, v, klr, vl, s,
+                            o + (size_t)i * d, NULL, lse ? lse + i : NULL);
+                free(s);
+            }
+        }
+    }
+    free(tpos);
+    free(qpos);
+    free(kr);
+    free(klr);
+    free(qrr);
+    free(kl);
+    free(vl);
+    return bad ? -1 : 0;
+}
+
+/* Causal prefill with RoPE inside Eq. 3: positions pos0 .. pos0+T-1.
+ * Shapes as for dar_oracle_prefill. */
+int dar_oracle_prefill_rope(int B, int Hq, int Hkv, int T, int d, int dd, int w, int r,
+                            double base, int pos0, const double* q, const double* k,
+                            const double* v, const double* wd, const double* wu, double* o,
+                            double* lse, int nthreads)
+{
+    if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || T < 1 || d < 1 || dd < 1 || w < 0)
+        return -1;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    const int group = Hq / Hkv;
+    int* pos = (int*)malloc(sizeof(int) * (size_t)T);
+    if (!pos) return -1;
+    for (int i = 0; i < T; ++i) pos[i] = i;
+    int rc = 0;
+    for (int b = 0; b < B && rc == 0; ++b)
+        for (int h = 0; h < Hq && rc == 0; ++h) {
+            const int g = h / group;
+            const size_t kv_off = ((size_t)b * Hkv + g) * (size_t)T * d;
+            const size_t q_off = ((size_t)b * Hq + h) * (size_t)T * d;
+            rc = dar_oracle_rows_rope(T, d, dd, w, r, base, pos0, k + kv_off, v + kv_off,
+                                      wd + (size_t)g * d * dd, wu ? wu + (size_t)g * dd * d : NULL,
+                                      T, pos, q + q_off, o + q_off,
+                                      lse ? lse + ((size_t)b * Hq + h) * T : NULL);
+        }
+    free(pos);
+    return rc;
 }

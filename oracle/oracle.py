@@ -11,6 +11,10 @@ Functions follow the paper's method section:
               the log of each row's softmax denominator
   backward()  gradients of sum(dO * O) of the prefill (Section 2.3, the
               training setting) with respect to Q, K, V, W_down, W_up
+  rope()      the rotary position embedding of Eq. 3 (rotate-half pairing)
+  rope_table()   its cos/sin per position and pair
+  rows_rope(), prefill_rope()   Eq. 3-4 with RoPE where Eq. 3 applies it:
+              on the window key, and on the distant key after the lift
   cache_model()  where the split cache keeps each token after n appends
                  (the efficient cache of the Limitations section: full K/V for
                  the last w tokens, the d_down latent for older ones)
@@ -71,6 +75,16 @@ class Oracle:
         lib.dar_oracle_up.restype = None
         lib.dar_oracle_up.argtypes = [ctypes.c_int] * 3 + [_dp, _dp, _dp, _dp]
         lib.dar_oracle_num_threads.restype = ctypes.c_int
+        lib.dar_oracle_rope.restype = None
+        lib.dar_oracle_rope.argtypes = [ctypes.c_int] * 3 + [ctypes.c_double, _ip, _dp, _dp]
+        lib.dar_oracle_rope_table.restype = None
+        lib.dar_oracle_rope_table.argtypes = [ctypes.c_int, ctypes.c_double, ctypes.c_int, _dp]
+        lib.dar_oracle_rows_rope.restype = ctypes.c_int
+        lib.dar_oracle_rows_rope.argtypes = ([ctypes.c_int] * 5 + [ctypes.c_double, ctypes.c_int]
+                                             + [_dp] * 4 + [ctypes.c_int, _ip, _dp, _dp, _dp])
+        lib.dar_oracle_prefill_rope.restype = ctypes.c_int
+        lib.dar_oracle_prefill_rope.argtypes = ([ctypes.c_int] * 8 + [ctypes.c_double, ctypes.c_int]
+                                                + [_dp] * 7 + [ctypes.c_int])
         lib.dar_oracle_backward.restype = ctypes.c_int
         lib.dar_oracle_backward.argtypes = [ctypes.c_int] * 7 + [_dp] * 11 + [ctypes.c_int]
         self.lib = lib
@@ -142,6 +156,63 @@ class Oracle:
             raise ValueError("dar_oracle_prefill rejected its arguments")
         return (o, lse) if want_lse else o
 
+    def rope(self, x, pos, r, base):
+        """RoPE of each row x [n, d] at positions pos [n] (Eq. 3)."""
+        x = _c64(x)
+        n, d = x.shape
+        pos = np.ascontiguousarray(pos, dtype=np.int32)
+        assert pos.shape == (n,) and 0 <= r <= d and r % 2 == 0
+        out = np.empty_like(x)
+        self.lib.dar_oracle_rope(n, d, int(r), float(base), pos.ctypes.data_as(_ip), _ptr(x),
+                                 _ptr(out))
+        return out
+
+    def rope_table(self, r, base, n_pos):
+        """[n_pos, r]: cos of the r/2 angles of each position, then their sin."""
+        tab = np.empty((n_pos, r), np.float64)
+        self.lib.dar_oracle_rope_table(int(r), float(base), int(n_pos), _ptr(tab))
+        return tab
+
+    def rows_rope(self, k, v, wd, wu, w, r, base, pos0, pos, qr):
+        """Eq. 3-4 with RoPE for query vectors qr [n, d] (un-rotated) at row
+        indices pos of one head whose tokens k, v [T, d] (un-rotated) sit at
+        positions pos0 .. pos0+T-1."""
+        k = _c64(k)
+        v = _c64(v)
+        wd = _c64(wd)
+        wu_c = None if wu is None else _c64(wu)
+        qr = _c64(qr)
+        T, d = k.shape
+        dd = wd.shape[1]
+        pos = np.ascontiguousarray(pos, dtype=np.int32)
+        n = pos.shape[0]
+        o = np.empty((n, d), np.float64)
+        rc = self.lib.dar_oracle_rows_rope(T, d, dd, int(w), int(r), float(base), int(pos0),
+                                           _ptr(k), _ptr(v), _ptr(wd), _ptr(wu_c), n,
+                                           pos.ctypes.data_as(_ip), _ptr(qr), _ptr(o), None)
+        if rc != 0:
+            raise ValueError("dar_oracle_rows_rope rejected its arguments")
+        return o
+
+    def prefill_rope(self, q, k, v, wd, wu, w, r, base, pos0=0, threads=0, want_lse=False):
+        """Causal prefill with RoPE inside Eq. 3 over positions pos0..pos0+T-1
+        (q, k, v un-rotated; shapes as for prefill)."""
+        q = _c64(q)
+        k = _c64(k)
+        v = _c64(v)
+        wd = _c64(wd)
+        wu_c = None if wu is None else _c64(wu)
+        B, Hq, T, d = q.shape
+        Hkv = k.shape[1]
+        dd = wd.shape[2]
+        o = np.empty_like(q)
+        lse = np.empty((B, Hq, T), np.float64) if want_lse else None
+        rc = self.lib.dar_oracle_prefill_rope(B, Hq, Hkv, T, d, dd, int(w), int(r), float(base),
+                                              int(pos0), _ptr(q), _ptr(k), _ptr(v), _ptr(wd),
+                                              _ptr(wu_c), _ptr(o), _ptr(lse), int(threads))
+        if rc != 0:
+            raise ValueError("dar_oracle_prefill_rope rejected its arguments")
+        return (o, lse) if want_lse else o
 
     def backward(self, q, k, v, wd, wu, w, dout, threads=0):
         """Gradients of sum(dout * O) of the causal prefill (Section 2.3's
@@ -201,6 +272,22 @@ def prefill(q, k, v, wd, wu, w, threads=0, want_lse=False):
 
 def backward(q, k, v, wd, wu, w, dout, threads=0):
     return default().backward(q, k, v, wd, wu, w, dout, threads)
+
+
+def rope(x, pos, r, base):
+    return default().rope(x, pos, r, base)
+
+
+def rope_table(r, base, n_pos):
+    return default().rope_table(r, base, n_pos)
+
+
+def rows_rope(k, v, wd, wu, w, r, base, pos0, pos, qr):
+    return default().rows_rope(k, v, wd, wu, w, r, base, pos0, pos, qr)
+
+
+def prefill_rope(q, k, v, wd, wu, w, r, base, pos0=0, threads=0, want_lse=False):
+    return default().prefill_rope(q, k, v, wd, wu, w, r, base, pos0, threads, want_lse)
 
 
 def cache_model(n_tokens: int, w: int, cap: int):

@@ -19,6 +19,19 @@ References for what is pinned:
   * Hand-derived closed forms (tests/golden/hand_examples.json).
   * Pure-Python brute force (oracle/brute.py) on tiny inputs.
 
+RoPE inside Eq. 3 (rotate-half pairing, window keys rotated as they are,
+distant keys rotated after the lift, values never):
+  * the rotation against its complex-number form (each pair as one complex
+    number multiplied by exp(i * angle)) and against cos/sin of 1 and 3
+    radians written out;
+  * r = 0 is the plain prefill;
+  * every score depends on positions only through i - j (the defining
+    property of rotary embeddings), so shifting all positions leaves the
+    output unchanged; a rotation skipped, misplaced or applied before the
+    lift breaks this;
+  * general w: the dual-store masked attention above with the keys rotated
+    in complex form (w >= T: causal attention over rotated queries and keys).
+
 Backward (gradients of sum(dO * O), the training setting of Section 2.3):
   * central finite differences of the forward prefill (itself pinned above);
   * torch fp64 autograd of the dual-store masked attention, written here with
@@ -435,6 +448,86 @@ def check_backward_identities(orc, seed=25):
         np.testing.assert_allclose(lhs, rhs, rtol=0, atol=1e-10)
 
 
+# ---------------------------------------------------------------- RoPE
+
+def rope_complex(x, pos, r, base):
+    """RoPE in complex form: the pair (x[m], x[m + r/2]) is the complex number
+    x[m] + i x[m + r/2], multiplied by exp(i pos base^(-2m/r)); pos broadcasts
+    over the rows (second-to-last axis) of x."""
+    x = np.asarray(x, np.float64)
+    out = x.copy()
+    h = r // 2
+    if h == 0:
+        return out
+    ang = np.asarray(pos, np.float64)[:, None] * float(base) ** (-2.0 * np.arange(h) / r)
+    z = (x[..., :h] + 1j * x[..., h:r]) * np.exp(1j * ang)
+    out[..., :h] = z.real
+    out[..., h:r] = z.imag
+    return out
+
+
+def check_rope_rotation(orc, seed=31):
+    # cos and sin of 1 and 3 radians: with r = 2 the only angle is the position
+    got = orc.rope(np.array([[1.0, 0.0], [0.0, 1.0]]), [1, 3], 2, 10000.0)
+    want = np.array([[0.5403023058681398, 0.8414709848078965],
+                     [-0.1411200080598672, -0.9899924966004454]])
+    np.testing.assert_allclose(got, want, rtol=0, atol=1e-15)
+    g = rng(seed)
+    for d, r, base in ((8, 8, 10000.0), (8, 4, 10000.0), (12, 6, 500000.0), (6, 0, 10.0)):
+        x = g.standard_normal((40, d))
+        pos = g.integers(0, 40000, 40)
+        np.testing.assert_allclose(orc.rope(x, pos, r, base), rope_complex(x, pos, r, base),
+                                   rtol=0, atol=1e-9)
+        if r:
+            ang = np.arange(50)[:, None] * base ** (-2.0 * np.arange(r // 2) / r)
+            tab = orc.rope_table(r, base, 50)
+            np.testing.assert_allclose(tab[:, : r // 2], np.exp(1j * ang).real, rtol=0, atol=1e-12)
+            np.testing.assert_allclose(tab[:, r // 2:], np.exp(1j * ang).imag, rtol=0, atol=1e-12)
+
+
+def check_rope_zero_dim_is_plain(orc, seed=32):
+    q, k, v, wd, wu = rand_case(seed)
+    for w in (0, 4, 100):
+        np.testing.assert_allclose(orc.prefill_rope(q, k, v, wd, wu, w, 0, 10000.0, pos0=9),
+                                   orc.prefill(q, k, v, wd, wu, w), rtol=0, atol=1e-15)
+
+
+def check_rope_shift_invariance(orc, seed=33):
+    q, k, v, wd, wu = rand_case(seed, d=8, dd=3)
+    for w, r in ((5, 8), (1, 4), (0, 8), (30, 6)):
+        a = orc.prefill_rope(q, k, v, wd, wu, w, r, 100.0, pos0=0)
+        b = orc.prefill_rope(q, k, v, wd, wu, w, r, 100.0, pos0=1237)
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-10)
+    # and the rotation does change the output
+    assert np.abs(a - orc.prefill(q, k, v, wd, wu, 30)).max() > 1e-3
+
+
+def check_rope_dual_store(orc, seed=34):
+    q, k, v, wd, wu = rand_case(seed, d=8, dd=3)
+    B, Hq, T, d = q.shape
+    for w, r, pos0, base in ((5, 6, 3, 50.0), (0, 8, 0, 10000.0), (T, 8, 11, 10.0),
+                             (9, 4, 2000, 10000.0)):
+        pos = pos0 + np.arange(T)
+        kl = lifted(k, wd, wu)
+        vl = lifted(v, wd, wu)
+        K2 = np.concatenate([expand_kv(rope_complex(kl, pos, r, base), Hq),
+                             expand_kv(rope_complex(k, pos, r, base), Hq)], axis=2)
+        V2 = np.concatenate([expand_kv(vl, Hq), expand_kv(v, Hq)], axis=2)
+        i = np.arange(T)[:, None]
+        j = np.arange(T)[None, :]
+        causal = j <= i
+        near = (i - j) < w
+        mask = np.concatenate([causal & ~near, causal & near], axis=1)
+        ref = sdpa(rope_complex(q, pos, r, base), K2, V2, mask=mask)
+        got = orc.prefill_rope(q, k, v, wd, wu, w, r, base, pos0=pos0)
+        np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12)
+        # the per-row entry point gives the same rows
+        rows = np.array([0, 3, T - 1])
+        o = orc.rows_rope(k[1, 0], v[1, 0], wd[0], None if wu is None else wu[0], w, r, base, pos0,
+                          rows, q[1, 1, rows])
+        np.testing.assert_allclose(o, got[1, 1, rows], rtol=0, atol=1e-12)
+
+
 ALL_CHECKS = [
     check_vanilla_when_window_covers,
     check_rows_inside_window_are_vanilla,
@@ -456,4 +549,8 @@ ALL_CHECKS = [
     check_backward_vanilla_no_bottleneck_gradient,
     check_backward_single_token,
     check_backward_identities,
+    check_rope_rotation,
+    check_rope_zero_dim_is_plain,
+    check_rope_shift_invariance,
+    check_rope_dual_store,
 ]

@@ -44,6 +44,19 @@ MUTANTS = [
     ("bwd_delta_from_key", "delta += p[j] * acc;", "delta += p[j] * acc * (j > 0);"),
     ("bwd_dwu_from_gradient_of_key_only", "const double* dxl = which ? dvl : dkl;",
      "const double* dxl = dkl;"),
+    # RoPE inside Eq. 3
+    ("rope_sin_sign", "yr[m] = xr[m] * c - xr[m + half] * s;", "yr[m] = xr[m] * c + xr[m + half] * s;"),
+    ("rope_pairs_adjacent",
+     "yr[m] = xr[m] * c - xr[m + half] * s;\n            yr[m + half] = xr[m + half] * c + xr[m] * s;",
+     "yr[2 * m] = xr[2 * m] * c - xr[2 * m + 1] * s;\n            yr[2 * m + 1] = xr[2 * m + 1] * c + xr[2 * m] * s;"),
+    ("rope_frequency_over_d", "(double)pos[t] * pow(base, -2.0 * m / r)",
+     "(double)pos[t] * pow(base, -2.0 * m / d)"),
+    ("rope_distant_key_unrotated", "qrr + (size_t)i * d, kr, v, klr, vl,", "qrr + (size_t)i * d, kr, v, kl, vl,"),
+    ("rope_window_key_unrotated", "qrr + (size_t)i * d, kr, v, klr, vl,", "qrr + (size_t)i * d, k, v, klr, vl,"),
+    ("rope_query_unrotated", "qrr + (size_t)i * d, kr, v, klr, vl,", "qr + (size_t)i * d, kr, v, klr, vl,"),
+    ("rope_query_position_shifted", "qpos[i] = pos0 + pos[i];", "qpos[i] = pos0 + pos[i] + 1;"),
+    ("rope_before_lift", "dar_oracle_rope(T, d, r, base, tpos, kl, klr);",
+     "{ double* t_ = lift_all(T, d, dd, kr, wd, wu); memcpy(klr, t_, sizeof(double) * (size_t)T * d); free(t_); }"),
 ]
 
 
