@@ -26,8 +26,10 @@
  *     the dtype of the shape (fp32 or bf16), except the weight gradients of
  *     the backward, which are fp32; bf16 runs accumulate in fp32.
  *   - Positions are 0-based and implicit (prefill: 0..T-1; decode: the query
- *     sits at position len-1 of the cache). Rotary position embedding, if any,
- *     is applied by the caller before these calls.
+ *     sits at position len-1 of the cache). The entry points without "rope"
+ *     in their name take q and k as they are (a caller may rotate them first:
+ *     then the distant key is the lift of the rotated key); the "rope" entry
+ *     points apply the rotary embedding where Eq. 3 does.
  *   - Ownership: every tensor pointer is device memory owned by the caller.
  *     The library allocates nothing and keeps no state between calls beyond
  *     one-time per-device kernel attributes; calls on different streams with
@@ -131,6 +133,46 @@ dar_status dar_attn_prefill_chunk(const dar_shape* s, dar_cache* c, int n, const
                                   const void* w_up, void* o, float* lse, void* ws,
                                   size_t ws_bytes, hipStream_t stream);
 
+/* Rotary position embedding inside Eq. 3. Eq. 3 rotates the key of both
+ * paths: the window key is RoPE(k_j), the distant key is RoPE of the lifted
+ * key, RoPE((k_j W_down) W_up); values are not rotated; the query is rotated
+ * at its own position. Rotate-half pairing: for m < r/2 the pair
+ * (x[m], x[m + r/2]) of a row at position p turns by the angle
+ * p * base^(-2m/r); elements r..d-1 are left as they are.
+ *   rotary_dim  r: even, 0 <= r <= d (0: no rotation)
+ *   n_pos       positions the table covers (0..n_pos-1)
+ *   table       device fp32 [n_pos][r]: cos of the r/2 angles of position p,
+ *               then their sin (dar_rope_table writes it; caller-owned) */
+typedef struct {
+    int rotary_dim;
+    int n_pos;
+    const float* table;
+} dar_rope;
+
+/* Fills table [n_pos][rotary_dim] (device, caller-owned) for the base
+ * frequency `base` (10000 in the original rotary embedding), computing each
+ * angle and its cos/sin in fp64 and rounding to fp32. rotary_dim even in
+ * [2, 256], 1 <= n_pos <= 65535, base > 0. */
+dar_status dar_rope_table(int rotary_dim, double base, int n_pos, float* table, hipStream_t stream);
+
+/* Causal prefill with the rotary embedding of Eq. 3: rows at positions
+ * pos0..pos0+T-1 (pos0 >= 0, pos0 + T <= rope->n_pos). q, k are the
+ * un-rotated queries and keys (q = h W_Q, k = h W_K); everything else as for
+ * dar_attn_prefill (lse included). Because the rotation does not commute with
+ * W_up, the distant keys are lifted and rotated to full d in the workspace
+ * (not absorbed into the query), so the attention costs as much as full
+ * causal attention; the cache the decode keeps is unchanged (latents of the
+ * un-rotated keys).
+ *   ws: at least dar_prefill_rope_workspace_bytes(s, T) bytes (caller-owned,
+ *   overwritten): rotated queries and keys, lifted distant keys and values,
+ *   and block norms.
+ * Supported: fp32 and bf16 with d <= 256 (bf16 with d in {64, 128}, any
+ * d_down, takes the matrix-core path). */
+dar_status dar_attn_prefill_rope(const dar_shape* s, int T, int pos0, const dar_rope* rope,
+                                 const void* q, const void* k, const void* v, const void* w_down,
+                                 const void* w_up, void* o, float* lse, void* ws, size_t ws_bytes,
+                                 hipStream_t stream);
+
 /* One decode step for the query q [B][Hq][d] at position c->len - 1, whose own
  * key and value must already have been appended. o [B][Hq][d] (output).
  * ws: device workspace of at least dar_decode_workspace_bytes(s, c->cap)
@@ -169,6 +211,7 @@ size_t dar_prefill_workspace_bytes(const dar_shape* s, int T);
 size_t dar_decode_workspace_bytes(const dar_shape* s, int cap);
 size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T);
 size_t dar_prefill_chunk_workspace_bytes(const dar_shape* s, int len, int n);
+size_t dar_prefill_rope_workspace_bytes(const dar_shape* s, int T);
 
 /* Static English text for a status code. */
 const char* dar_status_string(dar_status st);

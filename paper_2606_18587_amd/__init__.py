@@ -31,6 +31,11 @@ class DarCacheStruct(ctypes.Structure):
                 ("cap", ctypes.c_int), ("len", ctypes.c_int)]
 
 
+class DarRopeStruct(ctypes.Structure):
+    _fields_ = [("rotary_dim", ctypes.c_int), ("n_pos", ctypes.c_int),
+                ("table", ctypes.c_void_p)]
+
+
 class DarError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -63,6 +68,13 @@ def _load():
     lib.dar_attn_prefill_chunk.argtypes = [shp, cp, ci] + [vp] * 8 + [sz, vp]
     lib.dar_prefill_chunk_workspace_bytes.restype = sz
     lib.dar_prefill_chunk_workspace_bytes.argtypes = [shp, ci, ci]
+    rp = ctypes.POINTER(DarRopeStruct)
+    lib.dar_rope_table.restype = ci
+    lib.dar_rope_table.argtypes = [ci, ctypes.c_double, ci, vp, vp]
+    lib.dar_attn_prefill_rope.restype = ci
+    lib.dar_attn_prefill_rope.argtypes = [shp, ci, ci, rp] + [vp] * 8 + [sz, vp]
+    lib.dar_prefill_rope_workspace_bytes.restype = sz
+    lib.dar_prefill_rope_workspace_bytes.argtypes = [shp, ci]
     lib.dar_status_string.restype = ctypes.c_char_p
     lib.dar_status_string.argtypes = [ci]
     return lib
@@ -161,6 +173,74 @@ def dar_attn_prefill(q, k, v, w_down, w_up, w, o=None, ws=None, stream=None, che
                               _stream(stream))
     if st != DAR_OK:
         raise DarError(st, "dar_attn_prefill")
+    return (o, lse) if return_lse else o
+
+
+def dar_rope_table(rotary_dim, base, n_pos, device="cuda", stream=None):
+    """The angle table [n_pos, rotary_dim] fp32: cos of the r/2 angles of each
+    position, then their sin (computed on the device in fp64)."""
+    table = torch.empty(int(n_pos), int(rotary_dim), dtype=torch.float32, device=device)
+    st = lib.dar_rope_table(int(rotary_dim), float(base), int(n_pos), _ptr(table), _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_rope_table")
+    return table
+
+
+class Rope:
+    """Rotary embedding of Eq. 3: rotate-half pairs over the first rotary_dim
+    elements, angle p * base^(-2m/r); `table` [n_pos, r] fp32 on the device
+    (filled by dar_rope_table unless given)."""
+
+    def __init__(self, rotary_dim, base=10000.0, n_pos=4096, device="cuda", table=None,
+                 stream=None):
+        self.rotary_dim = int(rotary_dim)
+        self.base = float(base)
+        self.n_pos = int(n_pos)
+        if table is None and self.rotary_dim > 0:
+            table = dar_rope_table(self.rotary_dim, self.base, self.n_pos, device, stream)
+        self.table = table
+
+    def struct(self) -> DarRopeStruct:
+        return DarRopeStruct(self.rotary_dim, self.n_pos,
+                             None if self.table is None else self.table.data_ptr())
+
+
+def dar_prefill_rope_workspace_bytes(shape: DarShape, T: int) -> int:
+    return int(lib.dar_prefill_rope_workspace_bytes(ctypes.byref(shape), int(T)))
+
+
+def dar_attn_prefill_rope(q, k, v, w_down, w_up, w, rope: Rope, pos0=0, o=None, ws=None,
+                          stream=None, check=True, lse=None, return_lse=False):
+    """Causal DAR prefill with the rotary embedding of Eq. 3 at positions
+    pos0..pos0+T-1; q, k un-rotated. Other arguments as dar_attn_prefill."""
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    dd = w_down.shape[2]
+    shape = make_shape(B, Hq, Hkv, d, dd, w, q.dtype)
+    if check:
+        for name, t, want in (("k", k, (B, Hkv, T, d)), ("v", v, (B, Hkv, T, d)),
+                              ("w_down", w_down, (Hkv, d, dd))):
+            if tuple(t.shape) != want or t.dtype != q.dtype:
+                raise ValueError("%s: expected %s %s, got %s %s" % (name, want, q.dtype,
+                                                                   tuple(t.shape), t.dtype))
+        if w_up is not None and (tuple(w_up.shape) != (Hkv, dd, d) or w_up.dtype != q.dtype):
+            raise ValueError("w_up: expected %s" % ((Hkv, dd, d),))
+    if o is None:
+        o = torch.empty_like(q)
+    if return_lse and lse is None:
+        lse = torch.empty(B, Hq, T, dtype=torch.float32, device=q.device)
+    if lse is not None and (tuple(lse.shape) != (B, Hq, T) or lse.dtype != torch.float32):
+        raise ValueError("lse: expected %s float32" % ((B, Hq, T),))
+    if ws is None:
+        ws = _workspace(dar_prefill_rope_workspace_bytes(shape, T), q.device)
+    rs = rope.struct()
+    st = lib.dar_attn_prefill_rope(ctypes.byref(shape), int(T), int(pos0), ctypes.byref(rs),
+                                   _ptr(q), _ptr(k), _ptr(v), _ptr(w_down), _ptr(w_up), _ptr(o),
+                                   _ptr(lse), _ptr(ws),
+                                   0 if ws is None else ws.numel() * ws.element_size(),
+                                   _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_prefill_rope")
     return (o, lse) if return_lse else o
 
 

@@ -16,7 +16,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdar.so")
 SOURCES = ["dar_api.hip", "latent.hip", "prefill_valu.hip", "prefill_mfma.hip", "decode.hip",
-           "decode_mfma.hip", "backward.hip", "backward_mfma.hip"]
+           "decode_mfma.hip", "backward.hip", "backward_mfma.hip", "rope.hip"]
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [

@@ -32,6 +32,33 @@ hipError_t launch_prefill_mfma(const dar_shape* s, const PrefillGeo& geo, const 
                                const void* v, const void* wd, const void* wu, void* o, float* lse,
                                const void* cK, const void* cVt, const float* cnorm,
                                const float* knorm, const void* consts, hipStream_t st);
+bool prefill_mfma_rope_supported(const dar_shape* s);
+hipError_t launch_prefill_mfma_rope(const dar_shape* s, int T, const void* qr, const void* kr,
+                                    const void* v, const void* kd, const void* vd, void* o,
+                                    float* lse, const float* knorm, const float* dnorm,
+                                    hipStream_t st);
+
+// Prefill workspace with rotary embedding: rotated queries and keys, the
+// lifted-and-rotated distant keys and lifted values of positions < T - w,
+// and the 32-row block norms of the two key arrays; 256-byte aligned parts.
+struct RopeWs {
+    size_t qr_off, kr_off, kd_off, vd_off, knorm_off, dnorm_off, bytes;
+};
+
+RopeWs rope_ws_layout(const dar_shape* s, int T) {
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t es = s->dtype == DAR_BF16 ? 2 : 4;
+    const size_t Td = T > s->w ? (size_t)(T - s->w) : 0;
+    RopeWs L{};
+    L.qr_off = 0;
+    L.kr_off = L.qr_off + al((size_t)s->B * s->Hq * T * s->d * es);
+    L.kd_off = L.kr_off + al((size_t)s->B * s->Hkv * T * s->d * es);
+    L.vd_off = L.kd_off + al((size_t)s->B * s->Hkv * Td * s->d * es);
+    L.knorm_off = L.vd_off + al((size_t)s->B * s->Hkv * Td * s->d * es);
+    L.dnorm_off = L.knorm_off + al((size_t)s->B * s->Hkv * ((T + 31) / 32) * sizeof(float));
+    L.bytes = L.dnorm_off + al((size_t)s->B * s->Hkv * ((Td + 31) / 32) * sizeof(float)) + 256;
+    return L;
+}
 
 }  // namespace dar
 
@@ -174,6 +201,83 @@ size_t dar_prefill_chunk_workspace_bytes(const dar_shape* s, int len, int n) {
     if (check_shape(s) != DAR_OK || len < 0 || n < 1) return 0;
     if ((long long)len + n > 0x7fffffffLL) return 0;
     return chunk_ws_layout(s, len, n).bytes;
+}
+
+size_t dar_prefill_rope_workspace_bytes(const dar_shape* s, int T) {
+    if (check_shape(s) != DAR_OK || T < 1) return 0;
+    return rope_ws_layout(s, T).bytes;
+}
+
+dar_status dar_rope_table(int rotary_dim, double base, int n_pos, float* table, hipStream_t stream) {
+    if (rotary_dim < 2 || (rotary_dim & 1) || rotary_dim > 256 || n_pos < 1) return DAR_E_ARG;
+    if (!(base > 0.0) || base > 1e300) return DAR_E_ARG;
+    if (!dev_ok(table)) return DAR_E_ARG;
+    if (n_pos > 65535) return DAR_E_UNSUPPORTED;
+    clear_hip_error();
+    return launch_rope_table(rotary_dim, base, n_pos, table, stream) == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+dar_status dar_attn_prefill_rope(const dar_shape* s, int T, int pos0, const dar_rope* rope,
+                                 const void* q, const void* k, const void* v, const void* w_down,
+                                 const void* w_up, void* o, float* lse, void* ws, size_t ws_bytes,
+                                 hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (T < 1 || pos0 < 0 || !rope) return DAR_E_ARG;
+    const int r = rope->rotary_dim;
+    if (r < 0 || (r & 1) || r > s->d) return DAR_E_ARG;
+    if (r > 0 && !dev_ok(rope->table)) return DAR_E_ARG;
+    if ((long long)pos0 + T > (long long)rope->n_pos) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(w_down) || !dev_ok(o)) return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if (lse && !aligned16(lse)) return DAR_E_ARG;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+    const RopeWs L = rope_ws_layout(s, T);
+    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+
+    clear_hip_error();
+    char* wsb = (char*)ws;
+    void* qr = wsb + L.qr_off;
+    void* kr = wsb + L.kr_off;
+    void* kd = wsb + L.kd_off;
+    void* vd = wsb + L.vd_off;
+    float* knorm = (float*)(wsb + L.knorm_off);
+    float* dnorm = (float*)(wsb + L.dnorm_off);
+    const bool fast = prefill_mfma_rope_supported(s);
+    if (log_enabled())
+        fprintf(stderr, "[dar] prefill_rope B=%d Hq=%d Hkv=%d T=%d d=%d dd=%d w=%d r=%d pos0=%d %s path=%s\n",
+                s->B, s->Hq, s->Hkv, T, s->d, s->d_down, s->w, r, pos0,
+                s->dtype == DAR_BF16 ? "bf16" : "f32", fast ? "mfma" : "valu");
+    hipError_t e;
+    if (s->dtype == DAR_BF16) {
+        e = launch_rope_prepass<bf16_t>((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v,
+                                        (const bf16_t*)w_down, (const bf16_t*)w_up, rope->table,
+                                        (bf16_t*)qr, (bf16_t*)kr, (bf16_t*)kd, (bf16_t*)vd,
+                                        fast ? knorm : nullptr, fast ? dnorm : nullptr, s->B, s->Hq,
+                                        s->Hkv, T, s->d, s->d_down, s->w, r, pos0, stream);
+        if (e == hipSuccess) {
+            if (fast)
+                e = launch_prefill_mfma_rope(s, T, qr, kr, v, kd, vd, o, lse, knorm, dnorm, stream);
+            else
+                e = launch_prefill_rope_valu<bf16_t>((const bf16_t*)qr, (const bf16_t*)kr,
+                                                     (const bf16_t*)v, (const bf16_t*)kd,
+                                                     (const bf16_t*)vd, (bf16_t*)o, lse, s->B,
+                                                     s->Hq, s->Hkv, T, s->d, s->w, stream);
+        }
+    } else {
+        e = launch_rope_prepass<float>((const float*)q, (const float*)k, (const float*)v,
+                                       (const float*)w_down, (const float*)w_up, rope->table,
+                                       (float*)qr, (float*)kr, (float*)kd, (float*)vd, nullptr,
+                                       nullptr, s->B, s->Hq, s->Hkv, T, s->d, s->d_down, s->w, r,
+                                       pos0, stream);
+        if (e == hipSuccess)
+            e = launch_prefill_rope_valu<float>((const float*)qr, (const float*)kr,
+                                                (const float*)v, (const float*)kd, (const float*)vd,
+                                                (float*)o, lse, s->B, s->Hq, s->Hkv, T, s->d, s->w,
+                                                stream);
+    }
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 
 size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T) {

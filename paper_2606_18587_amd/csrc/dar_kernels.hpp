@@ -156,4 +156,19 @@ hipError_t launch_bwd_valu(const T* q, const T* k, const T* v, const T* o, const
                            float* dwd, float* dwu, char* ws, const BwdWs& L, int B, int Hq,
                            int Hkv, int T_, int d, int dd, int w, hipStream_t st);
 
+// Rotary embedding inside Eq. 3 (rope.hip): the angle table [n_pos][r] (cos
+// of the r/2 angles of a position, then their sin; fp32 from fp64), the
+// prefill pre-pass (rotated queries and keys; lifted, rotated distant keys
+// and lifted values of positions < T - w; block norms when knorm/dnorm are
+// given) and the generic attention over those arrays.
+hipError_t launch_rope_table(int r, double base, int n_pos, float* tab, hipStream_t st);
+template <typename T>
+hipError_t launch_rope_prepass(const T* q, const T* k, const T* v, const T* wd, const T* wu,
+                               const float* tab, T* qr, T* kr, T* kd, T* vd, float* knorm,
+                               float* dnorm, int B, int Hq, int Hkv, int T_, int d, int dd, int w,
+                               int r, int pos0, hipStream_t st);
+template <typename T>
+hipError_t launch_prefill_rope_valu(const T* qr, const T* kr, const T* v, const T* kd, const T* vd,
+                                    T* o, float* lse, int B, int Hq, int Hkv, int T_, int d, int w,
+                                    hipStream_t st);
 }  // namespace dar

@@ -190,7 +190,37 @@ __device__ __forceinline__ float dot8(bf16x8_t a, bf16x8_t b, float acc) {
 // kv0 + t (t < Tkv).
 struct RowCtx {
     int T, w, Tp, r0, i, i_hi, qc, hg, prow, bg, tid, kv0, Tkv;
+    int Td;  // with rotary embedding: rows of the lifted keys and values (T - w)
     float c_scale;
+};
+
+// The key range one call of the window-tile loop covers. LOCAL: the window,
+// i - w < j <= i, from the token's own keys and values. DIST (rotary
+// embedding only): the distant keys j <= i - w at full d, from the lifted
+// and rotated keys and the lifted values (rows 0..Td-1).
+template <bool DIST>
+struct Region {
+    static __device__ __forceinline__ int first_tile(int i0, int w, int bn) {
+        return DIST ? 0 : (imax(0, i0 - w + 1) & ~(bn - 1));
+    }
+    static __device__ __forceinline__ int last_key(int iwg_hi, int w) { return DIST ? iwg_hi - w : iwg_hi; }
+    // source row of key t (clamped: rows past the range are masked)
+    static __device__ __forceinline__ int row(const RowCtx& c, int t) {
+        return DIST ? imin(t, c.Td - 1) : imax(imin(t, c.T - 1) - c.kv0, 0);
+    }
+    static __device__ __forceinline__ size_t rows(const RowCtx& c) { return DIST ? c.Td : c.Tkv; }
+    // some row of this wavefront has a key of the region in [js, js + 31]
+    static __device__ __forceinline__ bool active(const RowCtx& c, int js) {
+        return DIST ? (c.r0 < c.T && js <= c.i_hi - c.w)
+                    : (c.r0 < c.T && js <= c.i_hi && js + 31 > c.r0 - c.w);
+    }
+    // every key of [js, js + 31] is in the region for every row
+    static __device__ __forceinline__ bool full(const RowCtx& c, int js) {
+        return DIST ? (js + 31 <= c.r0 - c.w) : (js > c.i_hi - c.w && js + 31 <= c.r0);
+    }
+    static __device__ __forceinline__ bool masked(const RowCtx& c, int j) {
+        return DIST ? (j > c.i - c.w) : (j <= c.i - c.w || j > c.i);
+    }
 };
 
 // Word 3 of a raw buffer descriptor on gfx9-family parts (32-bit data
@@ -331,7 +361,7 @@ __device__ __forceinline__ void distant_region(const RowCtx& c, const bf16_t* __
 // query operand is the unscaled bf16 query (scaling it in bf16 would add a
 // rounding proportional to the score); one FMA per score applies
 // log2(e)/sqrt(d) and the reference.
-template <int D, int DD, int NW, bool FIXED>
+template <int D, int DD, int NW, bool FIXED, bool DIST = false>
 __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t* __restrict__ k,
                                              const bf16_t* __restrict__ v, bf16_t* lds_k,
                                              bf16_t* lds_v, const bf16x8_t (&qop)[D / 16],
@@ -339,12 +369,12 @@ __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t
                                              f32x16_t (&ow)[D / 32], f32x16_t& ol) {
     constexpr int KS = D / 16, NT = D / 32, BN = 64, LDK = D + 8;
     constexpr int CH = BN * D / 8 / (NW * 64);
+    using R = Region<DIST>;
     const int T = c.T, w = c.w;
-    const int jb_lo = imax(0, i0 - w + 1);
-    const int t_first = jb_lo & ~(BN - 1);
-    const int ntile = (iwg_hi - t_first) / BN + 1;
-    const bf16_t* kb = k + (size_t)c.bg * c.Tkv * D;
-    const bf16_t* vb = v + (size_t)c.bg * c.Tkv * D;
+    const int t_first = R::first_tile(i0, w, BN);
+    const int ntile = (R::last_key(iwg_hi, w) - t_first) / BN + 1;
+    const bf16_t* kb = k + (size_t)c.bg * R::rows(c) * D;
+    const bf16_t* vb = v + (size_t)c.bg * R::rows(c) * D;
     uint4 pk[CH], pv[CH];
     auto gload = [&](int t0) {
 #pragma unroll
@@ -352,9 +382,10 @@ __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t
             const int chunk = c.tid + q * NW * 64;
             const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
             const int key = t0 + row;  // (keys below kv0 are never local: masked)
-            if (key < T && key >= c.kv0) {
-                pk[q] = *reinterpret_cast<const uint4*>(kb + (size_t)(key - c.kv0) * D + col);
-                pv[q] = *reinterpret_cast<const uint4*>(vb + (size_t)(key - c.kv0) * D + col);
+            if (DIST ? key < c.Td : (key < T && key >= c.kv0)) {
+                const int sr = DIST ? key : key - c.kv0;
+                pk[q] = *reinterpret_cast<const uint4*>(kb + (size_t)sr * D + col);
+                pv[q] = *reinterpret_cast<const uint4*>(vb + (size_t)sr * D + col);
             } else {
                 pk[q] = make_uint4(0, 0, 0, 0);
                 pv[q] = make_uint4(0, 0, 0, 0);
@@ -384,7 +415,7 @@ __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t
 #pragma unroll
         for (int sub = 0; sub < BN / 32; ++sub) {
             const int js = t0 + sub * 32;
-            if (c.r0 < T && js <= c.i_hi && js + 31 > c.r0 - w) {
+            if (R::active(c, js)) {
                 f32x16_t sc = mfma(load_bf16x8(lk + (sub * 32 + c.prow) * LDK + c.hg * 8), qop[0], splat16(0.f));
 #pragma unroll
                 for (int ks = 1; ks < KS; ++ks)
@@ -392,12 +423,10 @@ __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t
                 f32x16_t x;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], c.c_scale, st.cm);
-                if (!(js > c.i_hi - w && js + 31 <= c.r0)) {  // edge subtile: keep i - w < j <= i
+                if (!R::full(c, js)) {  // edge subtile: mask the keys outside the region
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int j = js + acc_key(r, c.hg);
-                        if (j <= c.i - w || j > c.i) x[r] = -INFINITY;
-                    }
+                    for (int r = 0; r < 16; ++r)
+                        if (R::masked(c, js + acc_key(r, c.hg))) x[r] = -INFINITY;
                 }
                 bf16x8_t p0, p1;
                 if (FIXED) exp_pack<true>(x, st.l, p0, p1);
@@ -429,7 +458,7 @@ __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t
 // query operand is the unscaled bf16 query (scaling it in bf16 would add a
 // rounding proportional to the score); one FMA per score applies
 // log2(e)/sqrt(d) and the reference.
-template <int D, int DD, int NW, bool FIXED>
+template <int D, int DD, int NW, bool FIXED, bool DIST = false>
 __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __restrict__ k,
                                              const bf16_t* __restrict__ v, bf16_t* lds_k,
                                              bf16_t* lds_v, const bf16x8_t (&qop)[D / 16],
@@ -437,12 +466,12 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
                                              f32x16_t (&ow)[D / 32], f32x16_t& ol) {
     constexpr int KS = D / 16, NT = D / 32, BN = 64, LDK = D + 8;
     constexpr int CH = BN * D / 8 / (NW * 64);
-    const int T = c.T, w = c.w;
-    const int jb_lo = imax(0, i0 - w + 1);
-    const int t_first = jb_lo & ~(BN - 1);
-    const int ntile = (iwg_hi - t_first) / BN + 1;
-    const bf16_t* kb = k + (size_t)c.bg * c.Tkv * D;
-    const bf16_t* vb = v + (size_t)c.bg * c.Tkv * D;
+    using R = Region<DIST>;
+    const int w = c.w;
+    const int t_first = R::first_tile(i0, w, BN);
+    const int ntile = (R::last_key(iwg_hi, w) - t_first) / BN + 1;
+    const bf16_t* kb = k + (size_t)c.bg * R::rows(c) * D;
+    const bf16_t* vb = v + (size_t)c.bg * R::rows(c) * D;
     // d = 64: two register sets; the loads of tile n+2 are issued when tile n
     // starts and reach LDS when tile n+1 ends, so two tiles of work cover
     // their latency.
@@ -457,11 +486,11 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
         for (int q = 0; q < CH; ++q) {
             const int chunk = c.tid + q * NW * 64;
             const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
-            // keys past the sequence repeat its last key: their scores are
-            // masked (j > i) and their weights are zero; keys below kv0 (the
-            // first rows a tile start rounded down may cover) are never local
-            // and read row 0
-            const int key = imax(imin(t0 + row, T - 1) - c.kv0, 0);
+            // keys past the range repeat its last key: their scores are
+            // masked and their weights are zero; keys below kv0 (the first
+            // rows a tile start rounded down may cover) are never local and
+            // read row 0
+            const int key = R::row(c, t0 + row);
             r.k[q] = *reinterpret_cast<const uint4*>(kb + (size_t)key * D + col);
             r.v[q] = *reinterpret_cast<const uint4*>(vb + (size_t)key * D + col);
         }
@@ -484,7 +513,7 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
 #pragma unroll
         for (int sub = 0; sub < BN / 32; ++sub) {
             const int js = t0 + sub * 32;
-            if (c.r0 < T && js <= c.i_hi && js + 31 > c.r0 - w) {
+            if (R::active(c, js)) {
                 f32x16_t sc = mfma(load_bf16x8(lk + (sub * 32 + c.prow) * LDK + c.hg * 8), qop[0], splat16(0.f));
 #pragma unroll
                 for (int ks = 1; ks < KS; ++ks)
@@ -492,12 +521,10 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
                 f32x16_t x;
 #pragma unroll
                 for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], c.c_scale, st.cm);
-                if (!(js > c.i_hi - w && js + 31 <= c.r0)) {  // edge subtile: keep i - w < j <= i
+                if (!R::full(c, js)) {  // edge subtile: mask the keys outside the region
 #pragma unroll
-                    for (int r = 0; r < 16; ++r) {
-                        const int j = js + acc_key(r, c.hg);
-                        if (j <= c.i - w || j > c.i) x[r] = -INFINITY;
-                    }
+                    for (int r = 0; r < 16; ++r)
+                        if (R::masked(c, js + acc_key(r, c.hg))) x[r] = -INFINITY;
                 }
                 bf16x8_t p0, p1;
                 if (FIXED) exp_pack<true>(x, st.l, p0, p1);
@@ -544,7 +571,12 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
     }
 }
 
-template <int D, int DD, int NW>
+// ROPE: rotary embedding inside Eq. 3. q, k are the rotated queries and
+// keys, cK / cVt the lifted-and-rotated distant keys and the lifted values
+// ([B*Hkv][T - w][D] each), cnorm their 32-row block norms (Tp / 32 per
+// head); the distant region then runs the full-d tile loop (no absorbed
+// query, no lift in the epilogue), and W_down / W_up are not read.
+template <int D, int DD, int NW, bool ROPE>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void prefill_mfma_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
@@ -597,15 +629,17 @@ void prefill_mfma_kernel(
     constexpr int UPT = DD * D / (NW * 64);
     static_assert(DD * D % (NW * 64) == 0, "whole W_up elements per thread");
     bf16_t uv[UPT];
+    if constexpr (!ROPE) {
 #pragma unroll
-    for (int j = 0; j < UPT; ++j) {
-        const int idx = tid + j * NW * 64, cc = idx / D, e = idx - (idx / D) * D;
-        uv[j] = *(wug ? wug + (size_t)cc * D + e : wdg + (size_t)e * DD + cc);
-    }
+        for (int j = 0; j < UPT; ++j) {
+            const int idx = tid + j * NW * 64, cc = idx / D, e = idx - (idx / D) * D;
+            uv[j] = *(wug ? wug + (size_t)cc * D + e : wdg + (size_t)e * DD + cc);
+        }
 #pragma unroll
-    for (int j = 0; j < UPT; ++j) {
-        const int idx = tid + j * NW * 64, cc = idx / D, e = idx - (idx / D) * D;
-        wU[cc * LDU + e] = uv[j];
+        for (int j = 0; j < UPT; ++j) {
+            const int idx = tid + j * NW * 64, cc = idx / D, e = idx - (idx / D) * D;
+            wU[cc * LDU + e] = uv[j];
+        }
     }
     __syncthreads();
 
@@ -630,6 +664,7 @@ void prefill_mfma_kernel(
         c.c_scale = c_scale;
         c.kv0 = kv0;
         c.Tkv = Tkv;
+        c.Td = imax(T - w, 0);
         const int i0 = q0 + rb * BM;  // position of the block's first row
         c.r0 = i0 + wave * 32;
         c.i = c.r0 + c.qc;
@@ -654,6 +689,10 @@ void prefill_mfma_kernel(
             const bf16_t* krow = k + ((size_t)bg * Tkv + (ii - kv0)) * D;
 #pragma unroll
             for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(krow + s * 16 + hg * 8);
+        } else if (ROPE) {
+            const bf16_t* crow = cK + ((size_t)bg * c.Td + ii) * D;  // lifted, rotated own key
+#pragma unroll
+            for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(crow + s * 16 + hg * 8);
         } else {
             const bf16_t* crow = cK + ((size_t)bg * Tp + ii) * DD;
 #pragma unroll
@@ -686,7 +725,12 @@ void prefill_mfma_kernel(
         // ---- absorbed query q~ = q W_up^T (scaled): A rows = latent column c, k = e
         bf16x8_t qtop[DS];
         float bound = -INFINITY;
-        if (jd_end >= 0) {
+        if (ROPE && jd_end >= 0) {
+            // full-d distant keys: |q . k| <= |q| |k|
+            for (int sb = lane + 64; sb < nsb; sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * (Tp / 32) + sb]);
+            cmax = wave_max(cmax);
+            bound = c_scale * sqrtf(qs2) * cmax;
+        } else if (jd_end >= 0) {
             f32x16_t qt = splat16(0.f);
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
@@ -718,7 +762,7 @@ void prefill_mfma_kernel(
         // key), so no row's weights can all underflow.
         bound = bound * 1.001f + 1e-6f;
         float witness = 0.f;
-        if (w >= 1) {
+        if (w >= 1 || ROPE) {
 #pragma unroll
             for (int s = 0; s < KS; ++s) witness = dot8(qop[s], wit[s], witness);
             witness *= c_scale;
@@ -736,7 +780,19 @@ void prefill_mfma_kernel(
         }
 
         // ------------------------------------------------------------ distant region
-        if (jd_end >= 0) {
+        if constexpr (ROPE) {
+            // full d, tiles staged for the workgroup (a barrier per tile: the
+            // condition is the workgroup's)
+            if (iwg_hi - w >= 0) {
+                if constexpr (D > 64) {
+                    if (fixed) local_region_1deep<D, DD, NW, true, true>(c, cK, cVt, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+                    else local_region_1deep<D, DD, NW, false, true>(c, cK, cVt, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+                } else {
+                    if (fixed) local_region<D, DD, NW, true, true>(c, cK, cVt, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+                    else local_region<D, DD, NW, false, true>(c, cK, cVt, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+                }
+            }
+        } else if (jd_end >= 0) {
             if (fixed) distant_region<D, DD, true>(c, cK, cVt, qtop, js_last, st, ow, ol);
             else distant_region<D, DD, false>(c, cK, cVt, qtop, js_last, st, ow, ol);
         }
@@ -755,10 +811,10 @@ void prefill_mfma_kernel(
 
         // ------------------------------------------------------------ epilogue
         float lt = st.l;
-        if (DD == 16) lt += ol[8];  // ones row (row 16, held by lanes of half 0)
+        if (DD == 16 && !ROPE) lt += ol[8];  // ones row (row 16, held by lanes of half 0)
         lt = pair_sum(lt);
 
-        if (jd_end >= 0) {
+        if (jd_end >= 0 && !ROPE) {
             // O^T += W_up^T O_lat^T, O_lat split into bf16 hi + lo parts
 #pragma unroll
             for (int s = 0; s < DS; ++s) {
@@ -815,7 +871,7 @@ bool prefill_mfma_supported(const dar_shape* s) {
     return true;
 }
 
-template <int D, int DD>
+template <int D, int DD, bool ROPE = false>
 static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w, const void* q, const void* k,
                             const void* v, const void* wd, const void* wu, void* o, float* lse,
                             const void* cK, const void* cVt, const float* cnorm,
@@ -826,10 +882,10 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w
     const int nblk = (geo.n_rows + BM - 1) / BM;
     const int npair = (nblk + 1) / 2;
     const int BH = B * Hq;
-    const int Tp = prefill_tp(T, w);
+    const int Tp = ROPE ? round_up(T - w > 0 ? T - w : 0, 32) : prefill_tp(T, w);
     const float c_scale = 1.4426950408889634f / sqrtf((float)D);
     const size_t lds = sizeof(bf16_t) * (4 * 64 * (D + 8) + DD * (D + 8));
-    auto kern = prefill_mfma_kernel<D, DD, NW>;
+    auto kern = prefill_mfma_kernel<D, DD, NW, ROPE>;
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
@@ -852,6 +908,30 @@ hipError_t launch_prefill_mfma(const dar_shape* s, const PrefillGeo& geo, const 
     if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
     if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
     return hipErrorNotSupported;
+}
+
+}  // namespace dar
+
+namespace dar {
+
+// Rotary embedding inside Eq. 3 (bf16, d in {64, 128}, any d_down: the
+// lift happened in the pre-pass): qr, kr the rotated queries and keys, v the
+// values, kd / vd the lifted-and-rotated distant keys and lifted values
+// [B*Hkv][T - w][d], knorm / dnorm the 32-row block norms of kr and kd.
+bool prefill_mfma_rope_supported(const dar_shape* s) {
+    return s->dtype == DAR_BF16 && (s->d == 64 || s->d == 128);
+}
+
+hipError_t launch_prefill_mfma_rope(const dar_shape* s, int T, const void* qr, const void* kr,
+                                    const void* v, const void* kd, const void* vd, void* o,
+                                    float* lse, const float* knorm, const float* dnorm,
+                                    hipStream_t st) {
+    const PrefillGeo geo = whole_sequence(T);
+    if (s->d == 64)
+        return launch_dd<64, 16, true>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o,
+                                       lse, kd, vd, dnorm, knorm, nullptr, st);
+    return launch_dd<128, 16, true>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o, lse,
+                                    kd, vd, dnorm, knorm, nullptr, st);
 }
 
 }  // namespace dar

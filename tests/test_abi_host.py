@@ -33,7 +33,8 @@ def test_exports_every_declared_symbol():
                           "dar_attn_prefill_backward", "dar_prefill_workspace_bytes",
                           "dar_decode_workspace_bytes", "dar_prefill_backward_workspace_bytes",
                           "dar_attn_prefill_chunk", "dar_prefill_chunk_workspace_bytes",
-                          "dar_status_string"}
+                          "dar_rope_table", "dar_attn_prefill_rope",
+                          "dar_prefill_rope_workspace_bytes", "dar_status_string"}
     raw = ctypes.CDLL(dar.LIB_PATH)
     for n in names:
         assert hasattr(raw, n), n
@@ -272,3 +273,53 @@ def test_chunk_rejects_before_any_launch():
     assert call_chunk(s, c2, n=2) == dar.DAR_E_ARG and c2.len == 0
     # bf16 rows of an odd number of elements cannot be copied in 4-byte words
     assert call_chunk(S(d=63, dd=16), cache_struct(), n=2) == dar.DAR_E_UNSUPPORTED
+
+
+def test_rope_workspace_size():
+    """Rotated queries and keys, lifted distant keys and values (positions
+    < T - w), block norms of both key arrays; 256-byte aligned parts."""
+    al = lambda x: (x + 255) // 256 * 256
+    for (B, Hq, Hkv, d, dd, w, dt, es), T in [((2, 4, 2, 64, 16, 8, torch.bfloat16, 2), 100),
+                                              ((2, 4, 2, 64, 16, 8, torch.bfloat16, 2), 5),
+                                              ((1, 2, 1, 16, 4, 0, torch.float32, 4), 33)]:
+        s = dar.make_shape(B, Hq, Hkv, d, dd, w, dt)
+        Td = max(T - w, 0)
+        want = (al(B * Hq * T * d * es) + al(B * Hkv * T * d * es) + 2 * al(B * Hkv * Td * d * es)
+                + al(B * Hkv * ((T + 31) // 32) * 4) + al(B * Hkv * ((Td + 31) // 32) * 4) + 256)
+        assert dar.dar_prefill_rope_workspace_bytes(s, T) == want
+    assert dar.dar_prefill_rope_workspace_bytes(S(), 0) == 0
+    assert dar.dar_prefill_rope_workspace_bytes(S(Hq=3), 8) == 0
+
+
+def call_rope(shape, T=16, pos0=0, r=64, n_pos=64, table=FAKE, q=FAKE, k=FAKE, v=FAKE, wd=FAKE,
+              wu=None, o=FAKE, lse=None, ws=FAKE, ws_bytes=1 << 30, null_rope=False):
+    rs = dar.DarRopeStruct(r, n_pos, table)
+    return dar.lib.dar_attn_prefill_rope(ctypes.byref(shape), T, pos0,
+                                         None if null_rope else ctypes.byref(rs), q, k, v, wd, wu,
+                                         o, lse, ws, ws_bytes, None)
+
+
+@no_gpu
+def test_rope_rejects_before_any_launch():
+    s = S()
+    assert call_rope(s, null_rope=True) == dar.DAR_E_ARG
+    assert call_rope(s, r=63) == dar.DAR_E_ARG            # odd rotary dimension
+    assert call_rope(s, r=66) == dar.DAR_E_ARG            # wider than d
+    assert call_rope(s, r=-2) == dar.DAR_E_ARG
+    assert call_rope(s, table=None) == dar.DAR_E_ARG      # r > 0 needs the table
+    assert call_rope(s, table=MISALIGNED) == dar.DAR_E_ARG
+    assert call_rope(s, T=60, pos0=5, n_pos=64) == dar.DAR_E_ARG   # positions past the table
+    assert call_rope(s, pos0=-1) == dar.DAR_E_ARG
+    assert call_rope(s, T=0) == dar.DAR_E_ARG
+    assert call_rope(s, q=None) == dar.DAR_E_ARG
+    assert call_rope(s, wu=MISALIGNED) == dar.DAR_E_ARG
+    assert call_rope(s, ws_bytes=64) == dar.DAR_E_WORKSPACE
+    assert call_rope(s, ws=None, ws_bytes=0) == dar.DAR_E_WORKSPACE
+    assert call_rope(S(Hq=3)) == dar.DAR_E_ARG
+    st = dar.lib.dar_rope_table
+    assert st(63, 10000.0, 8, FAKE, None) == dar.DAR_E_ARG
+    assert st(0, 10000.0, 8, FAKE, None) == dar.DAR_E_ARG
+    assert st(64, 0.0, 8, FAKE, None) == dar.DAR_E_ARG
+    assert st(64, 10000.0, 0, FAKE, None) == dar.DAR_E_ARG
+    assert st(64, 10000.0, 8, None, None) == dar.DAR_E_ARG
+    assert st(64, 10000.0, 70000, FAKE, None) == dar.DAR_E_UNSUPPORTED

@@ -1,0 +1,138 @@
+"""GPU parity of the rotary embedding inside Eq. 3 (dar_rope_table,
+dar_attn_prefill_rope through the C ABI) against the fp64 oracle.
+
+The queries and keys handed over are un-rotated; the window keys are rotated
+at their positions, the distant keys after the lift, values never (Eq. 3).
+Tolerance as for prefill: max abs 1e-4 (fp32), 2e-2 (bf16 storage, fp32
+accumulation), element by element.
+"""
+import numpy as np
+import pytest
+import torch
+
+import dar_inputs as di
+from oracle import oracle
+from tests.dev import to_dev, to_host64, tol
+
+pytestmark = pytest.mark.gpu
+
+dar = pytest.importorskip("paper_2606_18587_amd")
+
+
+@pytest.mark.parametrize("r,base,n_pos", [(64, 10000.0, 4096), (16, 10000.0, 33000),
+                                          (128, 500000.0, 70), (2, 10.0, 5)])
+def test_table_matches_oracle(r, base, n_pos):
+    """Each entry is the fp64 cos/sin rounded to fp32 (at most one fp32 step
+    apart where the two fp64 libraries round a value differently)."""
+    got = dar.dar_rope_table(r, base, n_pos).cpu().numpy().astype(np.float64)
+    ref = oracle.rope_table(r, base, n_pos)
+    step = np.spacing(np.abs(ref).astype(np.float32)).astype(np.float64)
+    assert (np.abs(got - ref) <= step).all()
+
+
+def run(wl, r, base, pos0=0, untied=False, check_lse=False, q_scale=1.0):
+    inp = di.make_prefill_inputs(wl, untied=untied, q_scale=q_scale)
+    q, k, v = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"])
+    wd, wu = to_dev(inp["wd"]), to_dev(inp["wu"])
+    rope = dar.Rope(r, base, n_pos=pos0 + wl.T)
+    o, lse = dar.dar_attn_prefill_rope(q, k, v, wd, wu, wl.w, rope, pos0=pos0, return_lse=True)
+    torch.cuda.synchronize()
+    got = to_host64(o)
+    ref, ref_lse = oracle.prefill_rope(inp["q"].f64, inp["k"].f64, inp["v"].f64, inp["wd"].f64,
+                                       None if inp["wu"] is None else inp["wu"].f64, wl.w, r, base,
+                                       pos0=pos0, want_lse=True)
+    assert np.isfinite(got).all()
+    err = np.abs(got - ref)
+    assert err.max() <= tol(wl.dtype), "max abs err %.3g at %s" % (
+        err.max(), np.unravel_index(err.argmax(), err.shape))
+    if check_lse:
+        lerr = np.abs(lse.double().cpu().numpy() - ref_lse).max()
+        assert lerr <= (1e-4 if wl.dtype == "f32" else 2e-2), lerr
+    return float(err.max())
+
+
+TINY = di.WORKLOADS["tiny"].with_(B=2, Hq=4, Hkv=2, T=90)   # fp32 d16 d_down4
+
+
+@pytest.mark.parametrize("w", [0, 1, 8, 40, 200])
+@pytest.mark.parametrize("r,pos0", [(16, 0), (8, 37), (0, 5), (2, 1000)])
+def test_fp32_tiny(w, r, pos0):
+    run(TINY.with_(w=w), r, 10000.0, pos0=pos0, untied=(w % 2 == 1), check_lse=True)
+
+
+BF16 = di.Workload("rope_bf16", 30, 1, 4, 2, 300, 64, 16, 64, "bf16")
+
+
+@pytest.mark.parametrize("w", [0, 1, 32, 100, 299, 400])
+@pytest.mark.parametrize("r,base", [(64, 10000.0), (16, 10000.0), (32, 500000.0)])
+def test_bf16_d64_matrix_core(w, r, base):
+    run(BF16.with_(w=w), r, base, untied=(w == 100), check_lse=(w == 32))
+
+
+@pytest.mark.parametrize("T", [1, 2, 63, 129, 257, 500])
+def test_bf16_d64_lengths(T):
+    run(BF16.with_(T=T, w=48, B=2), 64, 10000.0, pos0=3)
+
+
+@pytest.mark.parametrize("w,r", [(0, 128), (64, 128), (100, 32), (512, 64)])
+def test_bf16_d128_gqa(w, r):
+    run(di.Workload("rope_d128", 31, 1, 8, 2, 400, 128, 32, w, "bf16"), r, 500000.0,
+        untied=(w == 100), check_lse=True)
+
+
+@pytest.mark.parametrize("d,dd,w,T,r", [(80, 20, 30, 150, 80), (48, 12, 10, 90, 16),
+                                        (64, 64, 20, 120, 64), (128, 8, 50, 170, 64)])
+def test_bf16_other_shapes(d, dd, w, T, r):
+    """d not in {64, 128} takes the generic kernels; any d_down works on the
+    matrix-core path (the lift happens before the attention)."""
+    run(di.Workload("rope_other", 32, 1, 4, 2, T, d, dd, w, "bf16"), r, 10000.0, untied=True)
+
+
+def test_large_positions():
+    """Positions near 33K (a long cache): large angles."""
+    run(BF16.with_(T=200, w=40), 64, 10000.0, pos0=32700)
+
+
+def test_peaky_queries():
+    """Queries scaled by 2 (sharper rows). The rotated query and key are
+    rounded to bf16 before the matrix cores multiply them (the operands the
+    rotation-free path takes exactly as given), an error proportional to
+    the score size: measured 0.012 at unit scale, 0.014 here, 0.032 at x4
+    (the rotation-free path: 0.015 at x4)."""
+    run(BF16.with_(w=64, T=400), 64, 10000.0, q_scale=2.0)
+
+
+def test_shift_invariance_on_gpu():
+    """Scores depend on positions only through i - j: moving the whole
+    sequence changes the output by rounding only."""
+    wl = BF16.with_(w=50, T=260)
+    inp = di.make_prefill_inputs(wl)
+    q, k, v, wd = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"]), to_dev(inp["wd"])
+    rope = dar.Rope(64, 10000.0, n_pos=5000)
+    a = dar.dar_attn_prefill_rope(q, k, v, wd, None, wl.w, rope, pos0=0)
+    b = dar.dar_attn_prefill_rope(q, k, v, wd, None, wl.w, rope, pos0=4000)
+    torch.cuda.synchronize()
+    assert np.abs(to_host64(a) - to_host64(b)).max() <= tol("bf16")
+
+
+@pytest.mark.parametrize("r,base", [(16, 10000.0), (64, 500000.0)])
+def test_full_size_sampled_rows(r, base):
+    """The pythia70m-shaped prefill (B8 H8 T2048 d64 d_down16 w256) with the
+    Pythia rotary fraction (16 of 64 dims) and with full rotation: sampled
+    rows against the oracle's per-row evaluation."""
+    wl = di.WORKLOADS["pythia70m"]
+    inp = di.make_prefill_inputs(wl)
+    q, k, v, wd = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"]), to_dev(inp["wd"])
+    rope = dar.Rope(r, base, n_pos=wl.T)
+    o = dar.dar_attn_prefill_rope(q, k, v, wd, None, wl.w, rope)
+    torch.cuda.synchronize()
+    rng = np.random.Generator(np.random.PCG64(5))
+    rows = np.array(sorted({0, 255, 256, 257, 1000, wl.T - 1} | set(int(x) for x in rng.integers(0, wl.T, 6))))
+    worst = 0.0
+    for b, h in ((0, 0), (7, 7), (3, 5)):
+        ref = oracle.rows_rope(inp["k"].f64[b, h], inp["v"].f64[b, h], inp["wd"].f64[h], None, wl.w,
+                               r, base, 0, rows, inp["q"].f64[b, h, rows])
+        got = to_host64(o[b, h, torch.from_numpy(rows).to(o.device)])
+        worst = max(worst, float(np.abs(got - ref).max()))
+    assert worst <= tol("bf16"), worst
+    assert torch.isfinite(o.float()).all()
