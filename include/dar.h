@@ -181,6 +181,19 @@ dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q
                            const void* w_down, const void* w_up, void* o, void* ws,
                            size_t ws_bytes, hipStream_t stream);
 
+/* One decode step with the rotary embedding of Eq. 3: the query q [B][Hq][d]
+ * (un-rotated) sits at position c->len - 1 and cache token e at position e
+ * (c->len <= rope->n_pos). The cache is the one dar_cache_append keeps (ring
+ * of un-rotated keys and values, latents of the un-rotated keys): each ring
+ * key is rotated at its position, each distant key is lifted from its latent
+ * to full d and rotated (Eq. 3; the rotation does not commute with W_up, so
+ * W_up cannot be absorbed into the query for the keys); the distant values
+ * are summed in d_down space and lifted once. ws, o and the other arguments
+ * as for dar_attn_decode (same workspace size). */
+dar_status dar_attn_decode_rope(const dar_shape* s, const dar_cache* c, const dar_rope* rope,
+                                const void* q, const void* w_down, const void* w_up, void* o,
+                                void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* Backward of dar_attn_prefill: the gradients of L = sum(dout * o) with
  * respect to q, k, v, W_down and W_up (the training setting of Section 2.3,
  * whose objective is Eq. 5; the bottleneck weights receive gradient only

@@ -73,6 +73,8 @@ def _load():
     lib.dar_rope_table.argtypes = [ci, ctypes.c_double, ci, vp, vp]
     lib.dar_attn_prefill_rope.restype = ci
     lib.dar_attn_prefill_rope.argtypes = [shp, ci, ci, rp] + [vp] * 8 + [sz, vp]
+    lib.dar_attn_decode_rope.restype = ci
+    lib.dar_attn_decode_rope.argtypes = [shp, cp, rp] + [vp] * 5 + [sz, vp]
     lib.dar_prefill_rope_workspace_bytes.restype = sz
     lib.dar_prefill_rope_workspace_bytes.argtypes = [shp, ci]
     lib.dar_status_string.restype = ctypes.c_char_p
@@ -367,4 +369,24 @@ def dar_attn_decode(cache: DarCache, q, w_down, w_up=None, o=None, ws=None, stre
                              _stream(stream))
     if st != DAR_OK:
         raise DarError(st, "dar_attn_decode")
+    return o
+
+
+def dar_attn_decode_rope(cache: "DarCache", q, w_down, rope: Rope, w_up=None, o=None, ws=None,
+                         stream=None):
+    """One decode step with the rotary embedding of Eq. 3; q [B,Hq,d] un-rotated,
+    at position cache.len - 1. Returns o [B,Hq,d]."""
+    B, Hq, d = q.shape
+    shape = make_shape(B, Hq, cache.Hkv, d, cache.d_down, cache.w, q.dtype)
+    if o is None:
+        o = torch.empty_like(q)
+    if ws is None:
+        ws = _workspace(dar_decode_workspace_bytes(shape, cache.cap), q.device)
+    rs = rope.struct()
+    st = lib.dar_attn_decode_rope(ctypes.byref(shape), ctypes.byref(cache.struct), ctypes.byref(rs), _ptr(q),
+                                  _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(ws),
+                                  0 if ws is None else ws.numel() * ws.element_size(),
+                                  _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_decode_rope")
     return o

@@ -495,4 +495,49 @@ dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 
+dar_status dar_attn_decode_rope(const dar_shape* s, const dar_cache* c, const dar_rope* rope,
+                                const void* q, const void* w_down, const void* w_up, void* o,
+                                void* ws, size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (!c || c->cap < 1 || c->len < 1 || c->len > c->cap || !rope) return DAR_E_ARG;
+    const int r = rope->rotary_dim;
+    if (r < 0 || (r & 1) || r > s->d) return DAR_E_ARG;
+    if (r > 0 && !dev_ok(rope->table)) return DAR_E_ARG;
+    if (c->len > rope->n_pos) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(w_down) || !dev_ok(o)) return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if (!dev_ok(c->k_lat) || !dev_ok(c->v_lat)) return DAR_E_ARG;
+    if (s->w > 0 && (!dev_ok(c->k_win) || !dev_ok(c->v_win))) return DAR_E_ARG;
+    if (!group_supported(s)) return DAR_E_UNSUPPORTED;
+    const int G = s->Hq / s->Hkv;
+    if (decode_max_partials(s->B, s->Hkv, c->cap, s->w, s->d, s->d_down, G) > 1024)
+        return DAR_E_UNSUPPORTED;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+    const size_t need = dar_decode_workspace_bytes(s, c->cap);
+    if (ws == nullptr || ws_bytes < need) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+
+    clear_hip_error();
+    if (log_enabled())
+        fprintf(stderr, "[dar] decode_rope B=%d Hq=%d Hkv=%d d=%d dd=%d w=%d r=%d len=%d %s\n", s->B,
+                s->Hq, s->Hkv, s->d, s->d_down, s->w, r, c->len,
+                s->dtype == DAR_BF16 ? "bf16" : "f32");
+    hipError_t e;
+    if (s->dtype == DAR_BF16)
+        e = launch_decode_rope<bf16_t>((const bf16_t*)q, (const bf16_t*)w_down,
+                                       (const bf16_t*)w_up, (const bf16_t*)c->k_win,
+                                       (const bf16_t*)c->v_win, (const bf16_t*)c->k_lat,
+                                       (const bf16_t*)c->v_lat, rope->table, (bf16_t*)o,
+                                       (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w,
+                                       c->cap, c->len, r, stream);
+    else
+        e = launch_decode_rope<float>((const float*)q, (const float*)w_down, (const float*)w_up,
+                                      (const float*)c->k_win, (const float*)c->v_win,
+                                      (const float*)c->k_lat, (const float*)c->v_lat, rope->table,
+                                      (float*)o, (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down,
+                                      s->w, c->cap, c->len, r, stream);
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
 }  // extern "C"

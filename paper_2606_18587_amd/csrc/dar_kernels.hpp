@@ -167,6 +167,18 @@ hipError_t launch_rope_prepass(const T* q, const T* k, const T* v, const T* wd, 
                                const float* tab, T* qr, T* kr, T* kd, T* vd, float* knorm,
                                float* dnorm, int B, int Hq, int Hkv, int T_, int d, int dd, int w,
                                int r, int pos0, hipStream_t st);
+// Second stage of the split decodes: merges the S partial records of each
+// (batch, query head) and lifts the latent part (decode_combine_kernel).
+template <typename T>
+hipError_t launch_decode_combine(const float* part, const T* wd, const T* wu, T* o, int B, int Hq,
+                                 int Hkv, int d, int dd, int S, hipStream_t st);
+// Decode with the rotary embedding of Eq. 3 (query at position len - 1, cache
+// token e at position e; positions < len index the table).
+template <typename T>
+hipError_t launch_decode_rope(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
+                              const T* k_lat, const T* v_lat, const float* tab, T* o, float* part,
+                              int B, int Hq, int Hkv, int d, int dd, int w, int cap, int len, int r,
+                              hipStream_t st);
 template <typename T>
 hipError_t launch_prefill_rope_valu(const T* qr, const T* kr, const T* v, const T* kd, const T* vd,
                                     T* o, float* lse, int B, int Hq, int Hkv, int T_, int d, int w,

@@ -340,6 +340,19 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
     }
 }
 
+template <typename T>
+hipError_t launch_decode_combine(const float* part, const T* wd, const T* wu, T* o, int B, int Hq,
+                                 int Hkv, int d, int dd, int S, hipStream_t st) {
+    hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu, o, Hq,
+                       Hkv, d, dd, S);
+    return hipGetLastError();
+}
+template hipError_t launch_decode_combine<float>(const float*, const float*, const float*, float*,
+                                                 int, int, int, int, int, int, hipStream_t);
+template hipError_t launch_decode_combine<bf16_t>(const float*, const bf16_t*, const bf16_t*,
+                                                  bf16_t*, int, int, int, int, int, int,
+                                                  hipStream_t);
+
 static int group_chunk(int G) { return kDecScoreSlots / G; }
 
 DecodeSplits decode_splits(int len, int w, int d, int dd, int G) {

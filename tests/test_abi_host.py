@@ -33,7 +33,7 @@ def test_exports_every_declared_symbol():
                           "dar_attn_prefill_backward", "dar_prefill_workspace_bytes",
                           "dar_decode_workspace_bytes", "dar_prefill_backward_workspace_bytes",
                           "dar_attn_prefill_chunk", "dar_prefill_chunk_workspace_bytes",
-                          "dar_rope_table", "dar_attn_prefill_rope",
+                          "dar_rope_table", "dar_attn_prefill_rope", "dar_attn_decode_rope",
                           "dar_prefill_rope_workspace_bytes", "dar_status_string"}
     raw = ctypes.CDLL(dar.LIB_PATH)
     for n in names:
@@ -323,3 +323,20 @@ def test_rope_rejects_before_any_launch():
     assert st(64, 10000.0, 0, FAKE, None) == dar.DAR_E_ARG
     assert st(64, 10000.0, 8, None, None) == dar.DAR_E_ARG
     assert st(64, 10000.0, 70000, FAKE, None) == dar.DAR_E_UNSUPPORTED
+
+
+@no_gpu
+def test_decode_rope_rejects_before_any_launch():
+    s = S()
+    def call(c, r=64, n_pos=64, table=FAKE, q=FAKE, ws_bytes=1 << 30, null_rope=False):
+        rs = dar.DarRopeStruct(r, n_pos, table)
+        return dar.lib.dar_attn_decode_rope(ctypes.byref(s), ctypes.byref(c),
+                                            None if null_rope else ctypes.byref(rs), q, FAKE, None,
+                                            FAKE, FAKE, ws_bytes, None)
+    assert call(cache_struct(cap=64, length=10), null_rope=True) == dar.DAR_E_ARG
+    assert call(cache_struct(cap=64, length=0)) == dar.DAR_E_ARG        # empty cache
+    assert call(cache_struct(cap=100, length=70), n_pos=64) == dar.DAR_E_ARG  # past the table
+    assert call(cache_struct(cap=64, length=10), r=5) == dar.DAR_E_ARG
+    assert call(cache_struct(cap=64, length=10), table=None) == dar.DAR_E_ARG
+    assert call(cache_struct(cap=64, length=10), q=MISALIGNED) == dar.DAR_E_ARG
+    assert call(cache_struct(cap=64, length=10), ws_bytes=8) == dar.DAR_E_WORKSPACE

@@ -136,3 +136,111 @@ def test_full_size_sampled_rows(r, base):
         worst = max(worst, float(np.abs(got - ref).max()))
     assert worst <= tol("bf16"), worst
     assert torch.isfinite(o.float()).all()
+
+
+# ---------------------------------------------------------------- decode
+
+TDT = {"bf16": torch.bfloat16, "f32": torch.float32}
+
+
+def run_decode_rope(wl, L0, steps, r, base=10000.0, untied=False, check_heads=None):
+    """Append L0 tokens, then `steps` x {append one, decode with RoPE}; each
+    decode against the oracle's row at position len - 1 (RoPE inside Eq. 3
+    over the full-dimension history, tokens at positions 0..len-1)."""
+    pre = di.make_decode_prefix(wl, L0)
+    wd = pre["wd"]
+    wu = None
+    if untied:
+        g = np.random.Generator(np.random.PCG64(78))
+        wu = di.Tensor(g.standard_normal((wl.Hkv, wl.dd, wl.d), dtype=np.float32) /
+                       np.sqrt(wl.dd), wl.dtype)
+    cap = L0 + steps
+    c = dar.DarCache(wl.B, wl.Hkv, wl.d, wl.dd, wl.w, cap, TDT[wl.dtype])
+    wdd, wud = to_dev(wd), to_dev(wu)
+    if L0 > 0:
+        dar.dar_cache_append(c, to_dev(pre["k"]), to_dev(pre["v"]), wdd, Hq=wl.Hq)
+    rope = dar.Rope(r, base, n_pos=cap)
+    grp = wl.Hq // wl.Hkv
+    heads = check_heads or [(b, h) for b in range(wl.B) for h in range(wl.Hq)]
+    hist_k, hist_v = {}, {}
+    for (b, h) in heads:
+        key = (b, h // grp)
+        if key not in hist_k:
+            hist_k[key] = [pre["k"].f64_slice(key)]
+            hist_v[key] = [pre["v"].f64_slice(key)]
+    worst = 0.0
+    for t in range(steps):
+        st = di.make_decode_step(wl, t)
+        dar.dar_cache_append(c, to_dev(st["k"]), to_dev(st["v"]), wdd, Hq=wl.Hq)
+        o = dar.dar_attn_decode_rope(c, to_dev(st["q"]), wdd, rope, w_up=wud)
+        torch.cuda.synchronize()
+        got = to_host64(o)
+        assert np.isfinite(got).all()
+        L = L0 + t + 1
+        for key in hist_k:
+            hist_k[key].append(st["k"].f64[key[0], key[1]])
+            hist_v[key].append(st["v"].f64[key[0], key[1]])
+        for (b, h) in heads:
+            g = h // grp
+            K = np.concatenate(hist_k[(b, g)])
+            V = np.concatenate(hist_v[(b, g)])
+            ref = oracle.rows_rope(K, V, wd.f64[g], None if wu is None else wu.f64[g], wl.w, r,
+                                   base, 0, [L - 1], st["q"].f64[b, h][None])
+            worst = max(worst, float(np.abs(got[b, h] - ref[0]).max()))
+    assert worst <= tol(wl.dtype), worst
+    return worst
+
+
+DEC = di.Workload("dec_rope", 33, 2, 8, 2, 0, 64, 16, 32, "bf16", kind="decode")
+
+
+@pytest.mark.parametrize("w", [0, 1, 32, 600])
+@pytest.mark.parametrize("r", [64, 16])
+def test_decode_rope_bf16(w, r):
+    run_decode_rope(DEC.with_(w=w), 300, 2, r, untied=(w == 1))
+
+
+def test_decode_rope_fp32_tiny():
+    run_decode_rope(di.Workload("dec_rope_tiny", 34, 1, 2, 2, 0, 16, 4, 8, "f32", kind="decode"),
+                    50, 3, 16)
+
+
+@pytest.mark.parametrize("G", [1, 2, 8])
+def test_decode_rope_group_sizes(G):
+    run_decode_rope(DEC.with_(Hq=2 * G, Hkv=2), 130, 2, 32, base=500000.0)
+
+
+def test_decode_rope_d128_long():
+    run_decode_rope(di.Workload("dec_rope_d128", 35, 1, 8, 2, 0, 128, 32, 100, "bf16",
+                                kind="decode"), 3000, 2, 128, base=500000.0)
+
+
+def test_decode_rope_starts_from_empty_cache():
+    run_decode_rope(DEC.with_(w=4), 0, 7, 64)
+
+
+def test_decode_rope_matches_prefill_rope_rows():
+    """Decoding token p after appending tokens 0..p gives row p of the
+    prefill with the same rotary embedding."""
+    wl = di.Workload("dec_vs_prefill_rope", 36, 1, 4, 2, 160, 64, 16, 24, "bf16")
+    inp = di.make_prefill_inputs(wl)
+    q, k, v, wd = (to_dev(inp[x]) for x in ("q", "k", "v", "wd"))
+    rope = dar.Rope(64, 10000.0, n_pos=wl.T)
+    o_pre = dar.dar_attn_prefill_rope(q, k, v, wd, None, wl.w, rope)
+    c = dar.DarCache(wl.B, wl.Hkv, wl.d, wl.dd, wl.w, wl.T, torch.bfloat16)
+    worst = 0.0
+    for p in range(wl.T):
+        dar.dar_cache_append(c, k[:, :, p:p + 1].contiguous(), v[:, :, p:p + 1].contiguous(), wd,
+                             Hq=wl.Hq)
+        if p % 13 == 0 or p in (wl.w - 1, wl.w, wl.T - 1):
+            o = dar.dar_attn_decode_rope(c, q[:, :, p].contiguous(), wd, rope)
+            worst = max(worst, (o.float() - o_pre[:, :, p].float()).abs().max().item())
+    torch.cuda.synchronize()
+    assert worst <= 2e-2, worst
+
+
+def test_decode_rope_full_size_sampled_heads():
+    """The decode1b cache (B32 Hq32 Hkv8 d64 d_down16 w512, 32768 tokens) with
+    full rotation: sampled heads against the oracle."""
+    wl = di.WORKLOADS["decode1b"]
+    run_decode_rope(wl, wl.T, 1, 64, check_heads=[(0, 0), (5, 9), (31, 31)])
