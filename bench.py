@@ -15,6 +15,13 @@ KV GB/s is reported beside it. The backward of the same prefill (the training
 step's attention part, given the forward's output and log-sum-exp) is timed
 the same way and reported under "backward".
 
+Also reported, each timed the same way: the prefill and the decode with a
+cold cache hierarchy (a 1 GiB buffer written between calls evicts L2 and
+the Infinity Cache; the time of the writes alone is subtracted), the prefill
+and the decode with the rotary embedding inside Eq. 3 (prefill: rotary
+dimension 16 of 64, base 10000, as in the Pythia models; decode: full
+rotation), the chunked prefill and the other prefill workloads.
+
 Prints ONE JSON line (rank 0). Only one GPU is used: --gpus above 1 exits.
 """
 from __future__ import annotations
@@ -32,6 +39,12 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+# Measured exponential rate of one CU (v_exp_f32: 8.4 cycles per wave
+# instruction, 27.6 lanes per clock per CU): 256 CUs at 2.4 GHz.
+EXP_CEILING_PER_S = 27.6 * 256 * 2.4e9
+ROPE_PREFILL_DIM = 16       # rotary dimension of the prefill line (Pythia: 25% of 64)
+ROPE_DECODE_DIM = 64        # full rotation on the decode line
+ROPE_BASE = 10000.0
 
 # HBM bytes per entry-point launch from two rocprofv3 counter runs (FETCH_SIZE,
 # then WRITE_SIZE), each scaled by what the counter reads for a plain 256 MiB
@@ -107,6 +120,12 @@ def backward_flops(B, Hq, T, d, dd, w):
     return float(B * Hq * (10 * d * n_loc + 12 * dd * n_dist))
 
 
+def full_flops(B, Hq, T, d):
+    """Causal attention at d for every pair (the rotary path: distant keys are
+    lifted to full d, Eq. 3): 4 d flop per pair."""
+    return float(B * Hq * 4 * d * (T * (T + 1) // 2))
+
+
 def decode_bytes(B, Hq, Hkv, d, dd, w, L, esize=2):
     """Algorithmic HBM bytes of one decode step at cache length L: ring and
     latents (keys and values) once, plus query, output and W_down."""
@@ -128,6 +147,10 @@ def main():
                     help="skip the chunked prefill into the decode cache")
     ap.add_argument("--no-other-prefill", action="store_true",
                     help="skip the prefill workloads reported beside the main one")
+    ap.add_argument("--no-rope", action="store_true",
+                    help="skip the prefill and decode with the rotary embedding")
+    ap.add_argument("--no-cold", action="store_true",
+                    help="skip the cold-cache timings")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter calibration)")
@@ -224,6 +247,43 @@ def main():
                    args.steps)
     app_ms = timed(lambda i: dar.dar_cache_append(cache, step_in[i][1], step_in[i][2], dwd,
                                                   Hq=dw.Hq), args.steps)
+
+    # cold cache hierarchy: a 1 GiB write between calls; the writes alone are
+    # timed the same way and subtracted
+    cold = {}
+    if not args.no_cold:
+        flushbuf = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+
+        def timed_cold(fn, n):
+            both = timed(lambda i: (flushbuf.fill_(i & 0xff), fn(i)), n)
+            alone = timed(lambda i: flushbuf.fill_(i & 0xff), n)
+            return both - alone
+
+        cold["prefill_ms"] = timed_cold(
+            lambda i: dar.dar_attn_prefill(q, k, v, wd, None, pw.w, o=o, ws=ws, check=False),
+            args.steps)
+        cold["decode_ms"] = timed_cold(
+            lambda i: dar.dar_attn_decode(cache, qd_last, dwd, None, o=dout, ws=dws), args.steps)
+        del flushbuf
+
+    # the rotary embedding inside Eq. 3: the same prefill batch (un-rotated
+    # queries and keys) and the same decode cache
+    rope = {}
+    if not args.no_rope:
+        rp = dar.Rope(ROPE_PREFILL_DIM, ROPE_BASE, n_pos=pw.T, device=dev)
+        rws = torch.empty(dar.dar_prefill_rope_workspace_bytes(shape, pw.T), dtype=torch.uint8,
+                          device=dev)
+        run_rp = lambda i: dar.dar_attn_prefill_rope(q, k, v, wd, None, pw.w, rp, o=o, ws=rws,
+                                                     check=False)
+        for i in range(args.warmup):
+            run_rp(i)
+        rope["prefill_ms"] = timed(run_rp, args.steps)
+        del rws
+        rd = dar.Rope(ROPE_DECODE_DIM, ROPE_BASE, n_pos=cap, device=dev)
+        run_rd = lambda i: dar.dar_attn_decode_rope(cache, qd_last, dwd, rd, o=dout, ws=dws)
+        for i in range(args.warmup):
+            run_rd(i)
+        rope["decode_ms"] = timed(run_rd, args.steps)
 
     # chunked prefill into the same decode cache: chunks of CHUNK_N new tokens
     # (seeded N(0,1) queries, keys and values; the same tensors each call, at
@@ -342,6 +402,30 @@ def main():
                             "traffic": measured_traffic("decode")},
         "setup_s": round(setup_s, 1),
     }
+    # one exponential per causal pair: the distant region's bound
+    n_exp = float(pw.B * pw.Hq * (pw.T * (pw.T + 1) // 2))
+    result["prefill"]["score_elems_per_s"] = n_exp / (pre_us * 1e-6)
+    result["prefill"]["frac_exp_ceiling"] = round(n_exp / (pre_us * 1e-6) / EXP_CEILING_PER_S, 4)
+    if cold:
+        cu = float(cold["prefill_ms"] * 1e3)
+        result["prefill"]["cold_us"] = round(cu, 2)
+        result["prefill"]["cold_tflops"] = round(flops / (cu * 1e-6) / 1e12, 2)
+        du = float(cold["decode_ms"] * 1e3)
+        result["decode"]["cold_us"] = round(du, 2)
+        result["decode"]["cold_gbs"] = round(dbytes / (du * 1e-6) / 1e9, 1)
+    if rope:
+        ru = float(rope["prefill_ms"] * 1e3)
+        rfl = full_flops(pw.B, pw.Hq, pw.T, pw.d)
+        result["prefill_rope"] = {
+            "shape": "pythia70m batch, rotary dim %d of %d, base %g" % (ROPE_PREFILL_DIM, pw.d,
+                                                                      ROPE_BASE),
+            "us": round(ru, 2), "alg_flop": rfl, "tflops": round(rfl / (ru * 1e-6) / 1e12, 2),
+            "frac_bf16_peak": round(rfl / (ru * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        rdu = float(rope["decode_ms"] * 1e3)
+        result["decode_rope"] = {
+            "shape": "decode1b cache, rotary dim %d, base %g" % (ROPE_DECODE_DIM, ROPE_BASE),
+            "us": round(rdu, 2), "gbs": round(dbytes / (rdu * 1e-6) / 1e9, 1),
+            "frac_hbm_peak": round(dbytes / (rdu * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     if other:
         result["prefill_other"] = other
     if chunk is not None:
