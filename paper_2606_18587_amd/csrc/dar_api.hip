@@ -528,14 +528,14 @@ dar_status dar_attn_decode_rope(const dar_shape* s, const dar_cache* c, const da
         e = launch_decode_rope<bf16_t>((const bf16_t*)q, (const bf16_t*)w_down,
                                        (const bf16_t*)w_up, (const bf16_t*)c->k_win,
                                        (const bf16_t*)c->v_win, (const bf16_t*)c->k_lat,
-                                       (const bf16_t*)c->v_lat, rope->table, (bf16_t*)o,
+                                       (const bf16_t*)c->v_lat, rope->table, rope->n_pos, (bf16_t*)o,
                                        (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w,
                                        c->cap, c->len, r, stream);
     else
         e = launch_decode_rope<float>((const float*)q, (const float*)w_down, (const float*)w_up,
                                       (const float*)c->k_win, (const float*)c->v_win,
                                       (const float*)c->k_lat, (const float*)c->v_lat, rope->table,
-                                      (float*)o, (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down,
+                                      rope->n_pos, (float*)o, (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down,
                                       s->w, c->cap, c->len, r, stream);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }

@@ -98,6 +98,14 @@ hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* w
                               const bf16_t* v_lat, float* part, bf16_t* o, int B, int Hq, int Hkv,
                               int d, int dd, int w, int cap, int len, int& P, hipStream_t st);
 
+// The same kernel with the rotary embedding of Eq. 3 (d = 64, rotary
+// dimension 16, 32 or 64); tab [n_pos][r].
+bool decode_mfma_rope_supported(int d, int dd, int G, int r, bool bf16);
+hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
+                                   const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_lat,
+                                   const bf16_t* v_lat, const float* tab, int n_pos, float* part,
+                                   bf16_t* o, int B, int Hq, int Hkv, int dd, int w, int cap,
+                                   int len, int r, int& P, hipStream_t st);
 template <typename T>
 hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
@@ -176,9 +184,9 @@ hipError_t launch_decode_combine(const float* part, const T* wd, const T* wu, T*
 // token e at position e; positions < len index the table).
 template <typename T>
 hipError_t launch_decode_rope(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
-                              const T* k_lat, const T* v_lat, const float* tab, T* o, float* part,
-                              int B, int Hq, int Hkv, int d, int dd, int w, int cap, int len, int r,
-                              hipStream_t st);
+                              const T* k_lat, const T* v_lat, const float* tab, int n_pos, T* o,
+                              float* part, int B, int Hq, int Hkv, int d, int dd, int w, int cap,
+                              int len, int r, hipStream_t st);
 template <typename T>
 hipError_t launch_prefill_rope_valu(const T* qr, const T* kr, const T* v, const T* kd, const T* vd,
                                     T* o, float* lse, int B, int Hq, int Hkv, int T_, int d, int w,

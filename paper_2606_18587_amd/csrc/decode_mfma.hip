@@ -78,6 +78,52 @@ __device__ __forceinline__ int dperm(int R) {
     return 16 * (a >> 1) + 8 * gg + 4 * (a & 1) + b;
 }
 
+// RoPE (rotate-half, rotary dimension R) of a row held as KS slabs of 8
+// elements in the operand layout (lane half hg holds elements 16k + 8hg + j),
+// at the position whose table row is cs (cos of the R/2 angles, then sin).
+// With R a multiple of 32 the partner of element e (e + R/2) is in this
+// lane (slab k + R/32); with R = 16 it is in the other half (one swap).
+template <int KS, int R>
+__device__ __forceinline__ void rotate_slabs(float (&x)[KS][8], const float* cs, int hg) {
+    if constexpr (R % 32 == 0) {
+#pragma unroll
+        for (int k = 0; k < R / 32; ++k) {
+            const int m0 = 16 * k + 8 * hg;
+            const float4 c0 = *reinterpret_cast<const float4*>(cs + m0);
+            const float4 c1 = *reinterpret_cast<const float4*>(cs + m0 + 4);
+            const float4 s0 = *reinterpret_cast<const float4*>(cs + R / 2 + m0);
+            const float4 s1 = *reinterpret_cast<const float4*>(cs + R / 2 + m0 + 4);
+            const float c8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+            const float s8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                const float a = x[k][j], b = x[k + R / 32][j];
+                x[k][j] = __builtin_fmaf(a, c8[j], -(b * s8[j]));
+                x[k + R / 32][j] = __builtin_fmaf(b, c8[j], a * s8[j]);
+            }
+        }
+    } else {
+        static_assert(R == 16, "rotary dimension 16 or a multiple of 32");
+        // slab 0: half 0 holds elements 0..7 (first of their pairs), half 1
+        // elements 8..15 (the partners); both use angles m = j
+        const float4 c0 = *reinterpret_cast<const float4*>(cs);
+        const float4 c1 = *reinterpret_cast<const float4*>(cs + 4);
+        const float4 s0 = *reinterpret_cast<const float4*>(cs + 8);
+        const float4 s1 = *reinterpret_cast<const float4*>(cs + 12);
+        const float c8[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+        const float s8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const float own = x[0][j];
+            auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(own), __float_as_uint(own), false, false);
+            // the partner's value: lanes of half 0 find it in r[1], half 1 in r[0]
+            const float other = __uint_as_float(hg == 0 ? r[1] : r[0]);
+            x[0][j] = hg == 0 ? __builtin_fmaf(own, c8[j], -(other * s8[j]))
+                              : __builtin_fmaf(own, c8[j], other * s8[j]);
+        }
+    }
+}
+
 // The reference m is kept exactly representable in bf16 (rounded up when it
 // moves), so that the latent scores can subtract it inside the MFMA: a rank-1
 // product of a constant operand (1 in contraction slot 0 of every key row)
@@ -235,17 +281,33 @@ struct DecWaves {
     static constexpr int value = 8;
 };
 // Latent subtiles in flight per wavefront (register budget of 2 waves/SIMD).
-template <int D, int DD>
+template <int D, int DD, int R = 0>
 struct DecStages {
-    static constexpr int value = D <= 64 ? (DD <= 16 ? 12 : 7) : (DD <= 16 ? 10 : 5);
+    static constexpr int value = R > 0 ? (DD <= 16 ? 6 : 4)
+                                       : (D <= 64 ? (DD <= 16 ? 12 : 7) : (DD <= 16 ? 10 : 5));
 };
 
-template <int D, int DD, int NW>
+// R > 0: the rotary embedding of Eq. 3 with rotary dimension R (rotate-half
+// pairs; d = 64). The query is rotated at position len - 1, each ring key at
+// its position as it is loaded. A distant key has to be lifted to full d
+// before its rotation: per 32-token subtile the latent keys are lifted on
+// the matrix cores, K'^T = W_up^T C^T (the latent rows as loaded are the B
+// operand), and each lane rotates its token's elements in registers. Token
+// p = t0 + delta of a subtile starting at t0 takes cos/sin(p f) from the
+// angle-addition formula, with the subtile's table row (t0) read per subtile
+// and the lane's offset row (delta) held in registers for the whole run.
+// The rotated K' is the A operand of the scores as it stands (its element
+// order is matched by a permuted query operand). Values are not rotated:
+// the distant ones stay in d_down space and are lifted once, as without
+// rotation. tab: [n_pos][R] (cos of the R/2 angles, then their sin).
+template <int D, int DD, int NW, int R = 0>
 __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
     const bf16_t* __restrict__ k_win, const bf16_t* __restrict__ v_win,
     const bf16_t* __restrict__ k_lat, const bf16_t* __restrict__ v_lat, float* __restrict__ part,
-    bf16_t* __restrict__ o, int Hq, int Hkv, int w, int cap, int len, int P, float qscale) {
+    bf16_t* __restrict__ o, int Hq, int Hkv, int w, int cap, int len, int P, float qscale,
+    const float* __restrict__ tab, int n_pos) {
+    static_assert(R == 0 || (D == 64 && R % 16 == 0 && R <= D), "rotary: d = 64, R a multiple of 16");
     constexpr int KS = D / 16, DS = DD / 16, NT = D / 32;
     constexpr int LDW = D + 8;                      // padded ring row in LDS (bf16)
     constexpr int VBUF = 32 * LDW;                  // per-wave V staging (bf16 elements)
@@ -301,8 +363,40 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const bool hval = col < G;
     const bf16_t* qrow = q + ((size_t)b * Hq + (size_t)g * G + (hval ? col : 0)) * D;
     dbf16x8 qop[KS];
+    // with rotation: the query rotated at len - 1 (fp32 until packed); qopr is
+    // its scaled operand in the element order of the lifted keys' registers
+    dbf16x8 qopr[R > 0 ? KS : 1];
+    if constexpr (R == 0) {
 #pragma unroll
-    for (int k = 0; k < KS; ++k) qop[k] = hval ? ld8(qrow + k * 16 + hg * 8) : zero8();
+        for (int k = 0; k < KS; ++k) qop[k] = hval ? ld8(qrow + k * 16 + hg * 8) : zero8();
+    } else {
+        float qf[KS][8];
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+            const uint4 u = hval ? *reinterpret_cast<const uint4*>(qrow + k * 16 + hg * 8) : make_uint4(0, 0, 0, 0);
+            const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                qf[k][2 * j] = __uint_as_float(w4[j] << 16);
+                qf[k][2 * j + 1] = __uint_as_float(w4[j] & 0xffff0000u);
+            }
+        }
+        rotate_slabs<KS, R>(qf, tab + (size_t)(len - 1) * R, hg);
+#pragma unroll
+        for (int k = 0; k < KS; ++k) {
+            qop[k] = pk8(qf[k]);
+            // element order 16k + (j < 4 ? 4hg + j : 8 + 4hg + j - 4): swap
+            // the middle quads across the lane halves
+            float v8[8];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(qf[k][j]), __float_as_uint(qf[k][4 + j]), false, false);
+                v8[j] = __uint_as_float(r[0]) * qscale;
+                v8[4 + j] = __uint_as_float(r[1]) * qscale;
+            }
+            qopr[k] = pk8(v8);
+        }
+    }
 
     DecState st{-INFINITY, 0.f, -INFINITY, 0.f, zero8()};
     const int quad = lane >> 4, sl = lane & 15;
@@ -338,7 +432,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         // NST subtiles in flight per wavefront (the stream is latency bound:
         // the depth, not the arithmetic, sets its rate), issued before the
         // query absorption below so that its latency overlaps theirs
-        constexpr int NST = DecStages<D, DD>::value;
+        constexpr int NST = DecStages<D, DD, R>::value;
         dbf16x8 aks[NST][DS];
         uint4 vs[NST][DS];
 #pragma unroll
@@ -347,11 +441,12 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         // ---- q~^T = W_up q^T, scaled; rearranged from the accumulator layout
         // (lane half g holds columns 4g..4g+3, 8+4g..8+4g+3 of each 16) to the
         // B-operand layout (half g holds 8g..8g+7) with one swap across halves.
+        // (Not with rotation: the keys are lifted instead.)
         const bf16_t* wdg = wd + (size_t)g * D * DD;
         const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
         df32x16 qt = fill16(0.f);
 #pragma unroll
-        for (int k = 0; k < KS; ++k) {
+        for (int k = 0; k < (R > 0 ? 0 : KS); ++k) {
             dbf16x8 a = zero8();
             if (col < DD) {
                 if (wug) {
@@ -379,12 +474,82 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             qtop[k] = pk8(v8);
         }
 
+        // rotation: W_up^T rows (A operand of the lift; contraction slot
+        // 8 hg + j = latent column 16 s2 + 8 hg + j) and the lane's offset
+        // angles (token prow of the subtile) for its rotated pairs
+        constexpr int NP = R / 4;  // rotated pairs per lane
+        dbf16x8 aU[R > 0 ? NT : 1][R > 0 ? DS : 1];
+        float co[NP > 0 ? NP : 1], so[NP > 0 ? NP : 1];
+        if constexpr (R > 0) {
+#pragma unroll
+            for (int t = 0; t < NT; ++t)
+#pragma unroll
+                for (int s2 = 0; s2 < DS; ++s2) {
+                    uint16_t e8[8];
+                    const int e = 32 * t + col;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) {
+                        const int c = 16 * s2 + 8 * hg + j;
+                        e8[j] = wug ? wug[(size_t)c * D + e] : wdg[(size_t)e * DD + c];
+                    }
+                    aU[t][s2] = __builtin_bit_cast(dbf16x8, e8);
+                }
+            // (an offset row past the table belongs to a token past the run: masked)
+            const float* orow = tab + (size_t)imin(prow, n_pos - 1) * R;
+#pragma unroll
+            for (int f = 0; f < R / 16; ++f) {
+                const float4 c4 = *reinterpret_cast<const float4*>(orow + 8 * f + 4 * hg);
+                const float4 s4 = *reinterpret_cast<const float4*>(orow + R / 2 + 8 * f + 4 * hg);
+                co[4 * f] = c4.x; co[4 * f + 1] = c4.y; co[4 * f + 2] = c4.z; co[4 * f + 3] = c4.w;
+                so[4 * f] = s4.x; so[4 * f + 1] = s4.y; so[4 * f + 2] = s4.z; so[4 * f + 3] = s4.w;
+            }
+        }
+
         // Software pipelined: the scores of subtile n+1 are on the matrix
         // cores while the exponentials of subtile n run.
         auto scores = [&](int t0, const dbf16x8 (&ak)[DS]) {
-            df32x16 x = mma(ak[0], qtop[0], mma(ones_a, st.negm, fill16(0.f)));
+            df32x16 x;
+            if constexpr (R == 0) {
+                x = mma(ak[0], qtop[0], mma(ones_a, st.negm, fill16(0.f)));
 #pragma unroll
-            for (int k = 1; k < DS; ++k) x = mma(ak[k], qtop[k], x);
+                for (int k = 1; k < DS; ++k) x = mma(ak[k], qtop[k], x);
+            } else {
+                // K'^T tiles: lane = token prow, register 4 mm + i of tile t =
+                // element 32 t + 8 mm + 4 hg + i
+                df32x16 kx[NT];
+#pragma unroll
+                for (int t = 0; t < NT; ++t) {
+                    kx[t] = mma(aU[t][0], ak[0], fill16(0.f));
+#pragma unroll
+                    for (int s2 = 1; s2 < DS; ++s2) kx[t] = mma(aU[t][s2], ak[s2], kx[t]);
+                }
+                // the subtile's base angles (row t0; t0 <= last < n_pos)
+                const float* brow = tab + (size_t)t0 * R;
+#pragma unroll
+                for (int f = 0; f < R / 16; ++f) {
+                    const float4 c4 = *reinterpret_cast<const float4*>(brow + 8 * f + 4 * hg);
+                    const float4 s4 = *reinterpret_cast<const float4*>(brow + R / 2 + 8 * f + 4 * hg);
+                    const float cb[4] = {c4.x, c4.y, c4.z, c4.w}, sb[4] = {s4.x, s4.y, s4.z, s4.w};
+                    constexpr int q8 = R / 16;  // partner: 8 q8 elements on
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        const float c = __builtin_fmaf(cb[i], co[4 * f + i], -(sb[i] * so[4 * f + i]));
+                        const float sn = __builtin_fmaf(sb[i], co[4 * f + i], cb[i] * so[4 * f + i]);
+                        const int F2 = f + q8;
+                        const float av = kx[f / 4][4 * (f % 4) + i], bv = kx[F2 / 4][4 * (F2 % 4) + i];
+                        kx[f / 4][4 * (f % 4) + i] = __builtin_fmaf(av, c, -(bv * sn));
+                        kx[F2 / 4][4 * (F2 % 4) + i] = __builtin_fmaf(bv, c, av * sn);
+                    }
+                }
+                x = mma(ones_a, st.negm, fill16(0.f));
+#pragma unroll
+                for (int k = 0; k < KS; ++k) {
+                    float a8[8];
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) a8[j] = kx[k / 2][8 * (k % 2) + j];
+                    x = mma(pk8(a8), qopr[k], x);
+                }
+            }
             if (t0 + 31 > last) {
                 keep_branch();
 #pragma unroll
@@ -463,9 +628,26 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         const int last = t_end - 1;
         constexpr int CPT = 32 * D / 8 / 64;  // 16-byte chunks per lane per subtile
         auto load = [&](int t0, dbf16x8 (&ak)[KS], uint4 (&vv)[CPT]) {
-            const int kr = imin(t0 + prow, last) % w;
+            const int kpos = imin(t0 + prow, last);
+            const int kr = kpos % w;
 #pragma unroll
             for (int k = 0; k < KS; ++k) ak[k] = __builtin_bit_cast(dbf16x8, ld_stream(kw + (size_t)kr * D + k * 16 + hg * 8));
+            if constexpr (R > 0) {  // the key rotated at its position
+                float kf[KS][8];
+#pragma unroll
+                for (int k = 0; k < KS; ++k) {
+                    const uint4 u = __builtin_bit_cast(uint4, ak[k]);
+                    const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        kf[k][2 * j] = __uint_as_float(w4[j] << 16);
+                        kf[k][2 * j + 1] = __uint_as_float(w4[j] & 0xffff0000u);
+                    }
+                }
+                rotate_slabs<KS, R>(kf, tab + (size_t)kpos * R, hg);
+#pragma unroll
+                for (int k = 0; k < KS; ++k) ak[k] = pk8(kf[k]);
+            }
 #pragma unroll
             for (int k = 0; k < CPT; ++k) {
                 const int chunk = lane + 64 * k;
@@ -599,12 +781,42 @@ hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* w
 #define DAR_DEC_LAUNCH(D_, DD_)                                                                     \
     hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value>), grid,                    \
                        dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
-                       part, o, Hq, Hkv, w, cap, len, P, qscale)
+                       part, o, Hq, Hkv, w, cap, len, P, qscale, (const float*)nullptr, 0)
     if (d == 64 && dd == 16) DAR_DEC_LAUNCH(64, 16);
     else if (d == 64 && dd == 32) DAR_DEC_LAUNCH(64, 32);
     else if (d == 128 && dd == 16) DAR_DEC_LAUNCH(128, 16);
     else DAR_DEC_LAUNCH(128, 32);
 #undef DAR_DEC_LAUNCH
+    return hipGetLastError();
+}
+
+bool decode_mfma_rope_supported(int d, int dd, int G, int r, bool bf16) {
+    return bf16 && d == 64 && (dd == 16 || dd == 32) && G >= 1 && G <= kDecMaxGroup &&
+           (r == 16 || r == 32 || r == 64);
+}
+
+hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
+                                   const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_lat,
+                                   const bf16_t* v_lat, const float* tab, int n_pos, float* part,
+                                   bf16_t* o, int B, int Hq, int Hkv, int dd, int w, int cap,
+                                   int len, int r, int& P, hipStream_t st) {
+    P = decode_mfma_parts(B, Hkv, len, w, 64);
+    const float qscale = 1.4426950408889634f / sqrtf(64.f);
+    dim3 grid(P, B * Hkv);
+#define DAR_DEC_ROPE(DD_, R_)                                                                        \
+    hipLaunchKernelGGL((decode_mfma_kernel<64, DD_, DecWaves<64>::value, R_>), grid,                 \
+                       dim3(64 * DecWaves<64>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
+                       part, o, Hq, Hkv, w, cap, len, P, qscale, tab, n_pos)
+    if (dd == 16) {
+        if (r == 16) DAR_DEC_ROPE(16, 16);
+        else if (r == 32) DAR_DEC_ROPE(16, 32);
+        else DAR_DEC_ROPE(16, 64);
+    } else {
+        if (r == 16) DAR_DEC_ROPE(32, 16);
+        else if (r == 32) DAR_DEC_ROPE(32, 32);
+        else DAR_DEC_ROPE(32, 64);
+    }
+#undef DAR_DEC_ROPE
     return hipGetLastError();
 }
 

@@ -886,9 +886,18 @@ static hipError_t launch_decode_rope_g(const T* q, const T* wd, const T* wu, con
 
 template <typename T>
 hipError_t launch_decode_rope(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
-                              const T* k_lat, const T* v_lat, const float* tab, T* o, float* part,
-                              int B, int Hq, int Hkv, int d, int dd, int w, int cap, int len, int r,
-                              hipStream_t st) {
+                              const T* k_lat, const T* v_lat, const float* tab, int n_pos, T* o,
+                              float* part, int B, int Hq, int Hkv, int d, int dd, int w, int cap,
+                              int len, int r, hipStream_t st) {
+    if (decode_mfma_rope_supported(d, dd, Hq / Hkv, r, sizeof(T) == 2)) {
+        int P = 0;
+        hipError_t e = launch_decode_mfma_rope((const bf16_t*)q, (const bf16_t*)wd, (const bf16_t*)wu,
+                                               (const bf16_t*)k_win, (const bf16_t*)v_win,
+                                               (const bf16_t*)k_lat, (const bf16_t*)v_lat, tab, n_pos,
+                                               part, (bf16_t*)o, B, Hq, Hkv, dd, w, cap, len, r, P, st);
+        if (e != hipSuccess || P == 1) return e;
+        return launch_decode_combine<T>(part, wd, wu, o, B, Hq, Hkv, d, dd, P, st);
+    }
     switch (Hq / Hkv) {
         case 1: return launch_decode_rope_g<T, 1>(q, wd, wu, k_win, v_win, k_lat, v_lat, tab, o, part, B, Hq, Hkv, d, dd, w, cap, len, r, st);
         case 2: return launch_decode_rope_g<T, 2>(q, wd, wu, k_win, v_win, k_lat, v_lat, tab, o, part, B, Hq, Hkv, d, dd, w, cap, len, r, st);
@@ -900,11 +909,11 @@ hipError_t launch_decode_rope(const T* q, const T* wd, const T* wu, const T* k_w
 
 template hipError_t launch_decode_rope<float>(const float*, const float*, const float*, const float*,
                                               const float*, const float*, const float*, const float*,
-                                              float*, float*, int, int, int, int, int, int, int, int,
-                                              int, hipStream_t);
+                                              int, float*, float*, int, int, int, int, int, int, int,
+                                              int, int, hipStream_t);
 template hipError_t launch_decode_rope<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
                                                const bf16_t*, const bf16_t*, const bf16_t*,
-                                               const bf16_t*, const float*, bf16_t*, float*, int, int,
-                                               int, int, int, int, int, int, int, hipStream_t);
+                                               const bf16_t*, const float*, int, bf16_t*, float*, int,
+                                               int, int, int, int, int, int, int, int, hipStream_t);
 
 }  // namespace dar

@@ -244,3 +244,12 @@ def test_decode_rope_full_size_sampled_heads():
     full rotation: sampled heads against the oracle."""
     wl = di.WORKLOADS["decode1b"]
     run_decode_rope(wl, wl.T, 1, 64, check_heads=[(0, 0), (5, 9), (31, 31)])
+
+
+@pytest.mark.parametrize("L0,dd,r,untied", [(20000, 16, 64, False), (9000, 32, 32, True),
+                                            (5000, 32, 16, False), (700, 32, 64, True)])
+def test_decode_rope_matrix_core_shapes(L0, dd, r, untied):
+    """d_down 32 and long caches over few (batch, KV head) pairs: each pair is
+    split over several workgroups whose partial records the combine kernel
+    merges."""
+    run_decode_rope(DEC.with_(B=1, dd=dd, w=256), L0, 2, r, base=500000.0, untied=untied)
