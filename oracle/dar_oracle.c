@@ -471,3 +471,93 @@ int dar_oracle_prefill_rope(int B, int Hq, int Hkv, int T, int d, int dd, int w,
     free(pos);
     return rc;
 }
+
+/*
+ * Single shared latent (the cache the Limitations section proposes: one
+ * d_down vector per token, from which both the key and the value of the
+ * distant path are computed). With the latent c_j = h_j W_down of Eq. 1 and
+ * the lift of Eq. 2 followed by the key and value projections, the distant
+ * key is c_j (W_up W_K) and the distant value c_j (W_up W_V); per KV head
+ * these products are the matrices U_K, U_V [d_down][d]. The latent is an
+ * input here (a projection of the hidden state, like q, k, v).
+ *
+ * Query rows of one head:
+ *   window (i - j < w)   key k_j,        value v_j
+ *   distant              key c_j U_K,    value c_j U_V
+ * c [T][dd], uk, uv [dd][d]; other arguments as for dar_oracle_rows.
+ */
+int dar_oracle_rows_shared(int T, int d, int dd, int w, const double* k, const double* v,
+                           const double* c, const double* uk, const double* uv, int n_rows,
+                           const int* pos, const double* qr, double* o, double* lse)
+{
+    if (T < 1 || d < 1 || dd < 1 || w < 0 || n_rows < 0) return -1;
+    for (int i = 0; i < n_rows; ++i)
+        if (pos[i] < 0 || pos[i] >= T) return -1;
+    double* kl = (double*)malloc(sizeof(double) * (size_t)T * d);
+    double* vl = (double*)malloc(sizeof(double) * (size_t)T * d);
+    int bad = !kl || !vl;
+    if (!bad) {
+        /* Eq. 2 with the key / value projection folded in: x'_j = c_j U */
+        for (int j = 0; j < T; ++j)
+            for (int e = 0; e < d; ++e) {
+                double ak = 0.0, av = 0.0;
+                for (int cc = 0; cc < dd; ++cc) {
+                    ak += c[(size_t)j * dd + cc] * uk[(size_t)cc * d + e];
+                    av += c[(size_t)j * dd + cc] * uv[(size_t)cc * d + e];
+                }
+                kl[(size_t)j * d + e] = ak;
+                vl[(size_t)j * d + e] = av;
+            }
+#pragma omp parallel
+        {
+            double* s = (double*)malloc(sizeof(double) * (size_t)T);
+            if (!s) {
+#pragma omp atomic write
+                bad = 1;
+            } else {
+#pragma omp for schedule(dynamic, 4)
+                for (int i = 0; i < n_rows; ++i)
+                    one_row(d, w, pos[i], qr + (size_t)i * d, k, v, kl, vl, s, o + (size_t)i * d,
+                            NULL, lse ? lse + i : NULL);
+                free(s);
+            }
+        }
+    }
+    free(kl);
+    free(vl);
+    return bad ? -1 : 0;
+}
+
+/* Causal prefill with the shared latent: q [B][Hq][T][d], k, v [B][Hkv][T][d],
+ * c [B][Hkv][T][dd], uk, uv [Hkv][dd][d], o [B][Hq][T][d], lse optional. */
+int dar_oracle_prefill_shared(int B, int Hq, int Hkv, int T, int d, int dd, int w,
+                              const double* q, const double* k, const double* v, const double* c,
+                              const double* uk, const double* uv, double* o, double* lse,
+                              int nthreads)
+{
+    if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || T < 1 || d < 1 || dd < 1 || w < 0)
+        return -1;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    const int group = Hq / Hkv;
+    int* pos = (int*)malloc(sizeof(int) * (size_t)T);
+    if (!pos) return -1;
+    for (int i = 0; i < T; ++i) pos[i] = i;
+    int rc = 0;
+    for (int b = 0; b < B && rc == 0; ++b)
+        for (int h = 0; h < Hq && rc == 0; ++h) {
+            const int g = h / group;
+            const size_t kv_off = ((size_t)b * Hkv + g) * (size_t)T * d;
+            const size_t c_off = ((size_t)b * Hkv + g) * (size_t)T * dd;
+            const size_t q_off = ((size_t)b * Hq + h) * (size_t)T * d;
+            rc = dar_oracle_rows_shared(T, d, dd, w, k + kv_off, v + kv_off, c + c_off,
+                                        uk + (size_t)g * dd * d, uv + (size_t)g * dd * d, T, pos,
+                                        q + q_off, o + q_off,
+                                        lse ? lse + ((size_t)b * Hq + h) * T : NULL);
+        }
+    free(pos);
+    return rc;
+}

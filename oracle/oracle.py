@@ -15,6 +15,9 @@ Functions follow the paper's method section:
   rope_table()   its cos/sin per position and pair
   rows_rope(), prefill_rope()   Eq. 3-4 with RoPE where Eq. 3 applies it:
               on the window key, and on the distant key after the lift
+  rows_shared(), prefill_shared()   Eq. 3-4 with one shared latent per token
+              (distant key c U_K, distant value c U_V; the Limitations
+              section's h^D cache)
   cache_model()  where the split cache keeps each token after n appends
                  (the efficient cache of the Limitations section: full K/V for
                  the last w tokens, the d_down latent for older ones)
@@ -85,6 +88,11 @@ class Oracle:
         lib.dar_oracle_prefill_rope.restype = ctypes.c_int
         lib.dar_oracle_prefill_rope.argtypes = ([ctypes.c_int] * 8 + [ctypes.c_double, ctypes.c_int]
                                                 + [_dp] * 7 + [ctypes.c_int])
+        lib.dar_oracle_rows_shared.restype = ctypes.c_int
+        lib.dar_oracle_rows_shared.argtypes = ([ctypes.c_int] * 4 + [_dp] * 5
+                                               + [ctypes.c_int, _ip, _dp, _dp, _dp])
+        lib.dar_oracle_prefill_shared.restype = ctypes.c_int
+        lib.dar_oracle_prefill_shared.argtypes = [ctypes.c_int] * 7 + [_dp] * 8 + [ctypes.c_int]
         lib.dar_oracle_backward.restype = ctypes.c_int
         lib.dar_oracle_backward.argtypes = [ctypes.c_int] * 7 + [_dp] * 11 + [ctypes.c_int]
         self.lib = lib
@@ -214,6 +222,38 @@ class Oracle:
             raise ValueError("dar_oracle_prefill_rope rejected its arguments")
         return (o, lse) if want_lse else o
 
+    def rows_shared(self, k, v, c, uk, uv, w, pos, qr):
+        """Eq. 3-4 with a shared latent for query vectors qr [n, d] at positions
+        pos: window keys/values k, v [T, d], distant key c U_K and value c U_V
+        (c [T, dd], uk, uv [dd, d])."""
+        k, v, c, uk, uv, qr = (_c64(x) for x in (k, v, c, uk, uv, qr))
+        T, d = k.shape
+        dd = c.shape[1]
+        pos = np.ascontiguousarray(pos, dtype=np.int32)
+        n = pos.shape[0]
+        o = np.empty((n, d), np.float64)
+        rc = self.lib.dar_oracle_rows_shared(T, d, dd, int(w), _ptr(k), _ptr(v), _ptr(c), _ptr(uk),
+                                             _ptr(uv), n, pos.ctypes.data_as(_ip), _ptr(qr),
+                                             _ptr(o), None)
+        if rc != 0:
+            raise ValueError("dar_oracle_rows_shared rejected its arguments")
+        return o
+
+    def prefill_shared(self, q, k, v, c, uk, uv, w, threads=0, want_lse=False):
+        """Causal prefill with the shared latent: c [B,Hkv,T,dd], uk, uv [Hkv,dd,d]."""
+        q, k, v, c, uk, uv = (_c64(x) for x in (q, k, v, c, uk, uv))
+        B, Hq, T, d = q.shape
+        Hkv = k.shape[1]
+        dd = c.shape[3]
+        o = np.empty_like(q)
+        lse = np.empty((B, Hq, T), np.float64) if want_lse else None
+        rc = self.lib.dar_oracle_prefill_shared(B, Hq, Hkv, T, d, dd, int(w), _ptr(q), _ptr(k),
+                                                _ptr(v), _ptr(c), _ptr(uk), _ptr(uv), _ptr(o),
+                                                _ptr(lse), int(threads))
+        if rc != 0:
+            raise ValueError("dar_oracle_prefill_shared rejected its arguments")
+        return (o, lse) if want_lse else o
+
     def backward(self, q, k, v, wd, wu, w, dout, threads=0):
         """Gradients of sum(dout * O) of the causal prefill (Section 2.3's
         training setting): returns dq, dk, dv, dwd, dwu (dwu is None when
@@ -276,6 +316,14 @@ def backward(q, k, v, wd, wu, w, dout, threads=0):
 
 def rope(x, pos, r, base):
     return default().rope(x, pos, r, base)
+
+
+def rows_shared(k, v, c, uk, uv, w, pos, qr):
+    return default().rows_shared(k, v, c, uk, uv, w, pos, qr)
+
+
+def prefill_shared(q, k, v, c, uk, uv, w, threads=0, want_lse=False):
+    return default().prefill_shared(q, k, v, c, uk, uv, w, threads, want_lse)
 
 
 def rope_table(r, base, n_pos):

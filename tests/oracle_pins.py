@@ -32,6 +32,15 @@ distant keys rotated after the lift, values never):
   * general w: the dual-store masked attention above with the keys rotated
     in complex form (w >= T: causal attention over rotated queries and keys).
 
+Single shared latent (one d_down vector c_j per token and KV head, distant
+key c_j U_K, distant value c_j U_V; the Limitations section's cache):
+  * with v = k, c = k W_down and U_K = U_V = W_down^T it is the two-latent
+    oracle above (pinned);
+  * general w: the dual-store masked attention with keys [c U_K ; k] and
+    values [c U_V ; v], written with numpy products and library SDPA;
+  * w >= T: causal attention over k, v alone (no latent is read);
+  * w = 0: attention over (c U_K, c U_V) alone, the row's own token included.
+
 Backward (gradients of sum(dO * O), the training setting of Section 2.3):
   * central finite differences of the forward prefill (itself pinned above);
   * torch fp64 autograd of the dual-store masked attention, written here with
@@ -528,6 +537,55 @@ def check_rope_dual_store(orc, seed=34):
         np.testing.assert_allclose(o, got[1, 1, rows], rtol=0, atol=1e-12)
 
 
+# ---------------------------------------------------------------- shared latent
+
+def shared_case(seed, B=2, Hq=4, Hkv=2, T=23, d=8, dd=3):
+    g = rng(seed)
+    q = g.standard_normal((B, Hq, T, d))
+    k = g.standard_normal((B, Hkv, T, d))
+    v = g.standard_normal((B, Hkv, T, d))
+    c = g.standard_normal((B, Hkv, T, dd))
+    uk = g.standard_normal((Hkv, dd, d)) / math.sqrt(dd)
+    uv = g.standard_normal((Hkv, dd, d)) / math.sqrt(dd)
+    return q, k, v, c, uk, uv
+
+
+def check_shared_reduces_to_two_latents(orc, seed=41):
+    q, k, v, wd, wu = rand_case(seed, untied=False)
+    c = np.einsum("bgtd,gde->bgte", k, wd)
+    wdt = np.ascontiguousarray(np.swapaxes(wd, 1, 2))
+    for w in (0, 3, 9):
+        np.testing.assert_allclose(orc.prefill_shared(q, k, k, c, wdt, wdt, w),
+                                   orc.prefill(q, k, k, wd, None, w), rtol=0, atol=1e-12)
+
+
+def check_shared_dual_store(orc, seed=42):
+    q, k, v, c, uk, uv = shared_case(seed)
+    B, Hq, T, d = q.shape
+    i = np.arange(T)[:, None]
+    j = np.arange(T)[None, :]
+    for w in (0, 1, 6, T, T + 5):
+        kl = np.einsum("bgtc,gcd->bgtd", c, uk)
+        vl = np.einsum("bgtc,gcd->bgtd", c, uv)
+        K2 = np.concatenate([expand_kv(kl, Hq), expand_kv(k, Hq)], axis=2)
+        V2 = np.concatenate([expand_kv(vl, Hq), expand_kv(v, Hq)], axis=2)
+        causal = j <= i
+        near = (i - j) < w
+        mask = np.concatenate([causal & ~near, causal & near], axis=1)
+        got = orc.prefill_shared(q, k, v, c, uk, uv, w)
+        np.testing.assert_allclose(got, sdpa(q, K2, V2, mask=mask), rtol=0, atol=1e-12)
+        if w >= T:   # no latent is read
+            ref = sdpa(q, expand_kv(k, Hq), expand_kv(v, Hq), causal=True)
+            np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12)
+        if w == 0:   # every token through the latent, its own included
+            ref = sdpa(q, expand_kv(kl, Hq), expand_kv(vl, Hq), causal=True)
+            np.testing.assert_allclose(got, ref, rtol=0, atol=1e-12)
+    rows = np.array([0, 5, T - 1])
+    o = orc.rows_shared(k[1, 1], v[1, 1], c[1, 1], uk[1], uv[1], 6, rows, q[1, 3, rows])
+    np.testing.assert_allclose(o, orc.prefill_shared(q, k, v, c, uk, uv, 6)[1, 3, rows], rtol=0,
+                               atol=1e-12)
+
+
 ALL_CHECKS = [
     check_vanilla_when_window_covers,
     check_rows_inside_window_are_vanilla,
@@ -553,4 +611,6 @@ ALL_CHECKS = [
     check_rope_zero_dim_is_plain,
     check_rope_shift_invariance,
     check_rope_dual_store,
+    check_shared_reduces_to_two_latents,
+    check_shared_dual_store,
 ]

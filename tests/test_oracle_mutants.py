@@ -55,6 +55,14 @@ MUTANTS = [
     ("rope_window_key_unrotated", "qrr + (size_t)i * d, kr, v, klr, vl,", "qrr + (size_t)i * d, k, v, klr, vl,"),
     ("rope_query_unrotated", "qrr + (size_t)i * d, kr, v, klr, vl,", "qr + (size_t)i * d, kr, v, klr, vl,"),
     ("rope_query_position_shifted", "qpos[i] = pos0 + pos[i];", "qpos[i] = pos0 + pos[i] + 1;"),
+    # single shared latent
+    ("shared_value_lifted_with_key_matrix", "av += c[(size_t)j * dd + cc] * uv[(size_t)cc * d + e];",
+     "av += c[(size_t)j * dd + cc] * uk[(size_t)cc * d + e];"),
+    ("shared_key_lifted_with_value_matrix", "ak += c[(size_t)j * dd + cc] * uk[(size_t)cc * d + e];",
+     "ak += c[(size_t)j * dd + cc] * uv[(size_t)cc * d + e];"),
+    ("shared_matrix_transposed", "uk[(size_t)cc * d + e]", "uk[(size_t)e * dd + cc % dd]"),
+    ("shared_distant_uses_full_value", "one_row(d, w, pos[i], qr + (size_t)i * d, k, v, kl, vl, s, o + (size_t)i * d,\n                            NULL, lse ? lse + i : NULL);",
+     "one_row(d, w, pos[i], qr + (size_t)i * d, k, v, kl, v, s, o + (size_t)i * d,\n                            NULL, lse ? lse + i : NULL);"),
     ("rope_before_lift", "dar_oracle_rope(T, d, r, base, tpos, kl, klr);",
      "{ double* t_ = lift_all(T, d, dd, kr, wd, wu); memcpy(klr, t_, sizeof(double) * (size_t)T * d); free(t_); }"),
 ]
