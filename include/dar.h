@@ -194,6 +194,33 @@ dar_status dar_attn_decode_rope(const dar_shape* s, const dar_cache* c, const da
                                 const void* q, const void* w_down, const void* w_up, void* o,
                                 void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Single shared latent (the Limitations section's cache): one d_down latent
+ * per token and KV head, c_j = h_j W_down of Eq. 1, from which both the
+ * distant key and the distant value are computed. With the lift of Eq. 2
+ * followed by the key and value projections, distant key = c_j U_K and
+ * distant value = c_j U_V, where U_K = W_up W_K and U_V = W_up W_V per KV head
+ * ([Hkv][d_down][d] each). The latent is an input, projected from the hidden
+ * state by the caller like q, k and v; window keys and values are k, v (Eq. 3).
+ * The distant cache is one latent array instead of two.
+ *   Prefill: c [B][Hkv][T][d_down]; other arguments as dar_attn_prefill (same
+ *   workspace size, dar_prefill_workspace_bytes). Supported as dar_attn_prefill.
+ *   Append: the latent slot of each of the n new tokens (positions
+ *   len..len+n-1) takes c_new [B][Hkv][n][d_down] as given (every token, the
+ *   window's included); the ring takes the newest min(n, w) tokens of k_new,
+ *   v_new. c->k_lat holds the latents; c->v_lat is not used (may be NULL).
+ *   Fails with DAR_E_CAPACITY if len + n > cap.
+ *   Decode: as dar_attn_decode over such a cache (same workspace size). */
+dar_status dar_attn_prefill_shared(const dar_shape* s, int T, const void* q, const void* k,
+                                   const void* v, const void* c, const void* u_k, const void* u_v,
+                                   void* o, float* lse, void* ws, size_t ws_bytes,
+                                   hipStream_t stream);
+dar_status dar_cache_append_shared(const dar_shape* s, dar_cache* cache, const void* k_new,
+                                   const void* v_new, const void* c_new, int n,
+                                   hipStream_t stream);
+dar_status dar_attn_decode_shared(const dar_shape* s, const dar_cache* cache, const void* q,
+                                  const void* u_k, const void* u_v, void* o, void* ws,
+                                  size_t ws_bytes, hipStream_t stream);
+
 /* Backward of dar_attn_prefill: the gradients of L = sum(dout * o) with
  * respect to q, k, v, W_down and W_up (the training setting of Section 2.3,
  * whose objective is Eq. 5; the bottleneck weights receive gradient only

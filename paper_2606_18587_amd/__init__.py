@@ -75,6 +75,12 @@ def _load():
     lib.dar_attn_prefill_rope.argtypes = [shp, ci, ci, rp] + [vp] * 8 + [sz, vp]
     lib.dar_attn_decode_rope.restype = ci
     lib.dar_attn_decode_rope.argtypes = [shp, cp, rp] + [vp] * 5 + [sz, vp]
+    lib.dar_attn_prefill_shared.restype = ci
+    lib.dar_attn_prefill_shared.argtypes = [shp, ci] + [vp] * 9 + [sz, vp]
+    lib.dar_cache_append_shared.restype = ci
+    lib.dar_cache_append_shared.argtypes = [shp, cp, vp, vp, vp, ci, vp]
+    lib.dar_attn_decode_shared.restype = ci
+    lib.dar_attn_decode_shared.argtypes = [shp, cp] + [vp] * 5 + [sz, vp]
     lib.dar_prefill_rope_workspace_bytes.restype = sz
     lib.dar_prefill_rope_workspace_bytes.argtypes = [shp, ci]
     lib.dar_status_string.restype = ctypes.c_char_p
@@ -290,14 +296,18 @@ class DarCache:
     """Split KV cache owned by torch: ring [B,Hkv,w,d] for the window and
     latents [B,Hkv,cap,dd] for older tokens (see dar_cache in include/dar.h)."""
 
-    def __init__(self, B, Hkv, d, d_down, w, cap, dtype, device="cuda"):
+    def __init__(self, B, Hkv, d, d_down, w, cap, dtype, device="cuda", shared=False):
+        """shared: one latent array (the single shared latent per token; used
+        with the *_shared entry points), else separate key and value latents."""
         self.B, self.Hkv, self.d, self.d_down, self.w, self.cap = B, Hkv, d, d_down, w, cap
         self.dtype = dtype
+        self.shared = shared
         wl = max(w, 1)  # keep valid pointers for w = 0 (the ring is never touched then)
         self.k_win = torch.zeros(B, Hkv, wl, d, dtype=dtype, device=device)
         self.v_win = torch.zeros(B, Hkv, wl, d, dtype=dtype, device=device)
         self.k_lat = torch.zeros(B, Hkv, cap, d_down, dtype=dtype, device=device)
-        self.v_lat = torch.zeros(B, Hkv, cap, d_down, dtype=dtype, device=device)
+        self.v_lat = self.k_lat if shared else torch.zeros(B, Hkv, cap, d_down, dtype=dtype,
+                                                           device=device)
         self.struct = DarCacheStruct(self.k_win.data_ptr(), self.v_win.data_ptr(),
                                      self.k_lat.data_ptr(), self.v_lat.data_ptr(), int(cap), 0)
 
@@ -389,4 +399,61 @@ def dar_attn_decode_rope(cache: "DarCache", q, w_down, rope: Rope, w_up=None, o=
                                   _stream(stream))
     if st != DAR_OK:
         raise DarError(st, "dar_attn_decode_rope")
+    return o
+
+
+def dar_attn_prefill_shared(q, k, v, c, u_k, u_v, w, o=None, ws=None, stream=None, lse=None,
+                            return_lse=False):
+    """Causal prefill with one shared latent per token: c [B,Hkv,T,dd]; distant
+    key c U_K, distant value c U_V (u_k, u_v [Hkv,dd,d])."""
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    dd = c.shape[3]
+    shape = make_shape(B, Hq, Hkv, d, dd, w, q.dtype)
+    for name, t, want in (("k", k, (B, Hkv, T, d)), ("v", v, (B, Hkv, T, d)),
+                          ("c", c, (B, Hkv, T, dd)), ("u_k", u_k, (Hkv, dd, d)),
+                          ("u_v", u_v, (Hkv, dd, d))):
+        if tuple(t.shape) != want or t.dtype != q.dtype:
+            raise ValueError("%s: expected %s %s" % (name, want, q.dtype))
+    if o is None:
+        o = torch.empty_like(q)
+    if return_lse and lse is None:
+        lse = torch.empty(B, Hq, T, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = _workspace(dar_prefill_workspace_bytes(shape, T), q.device)
+    st = lib.dar_attn_prefill_shared(ctypes.byref(shape), int(T), _ptr(q), _ptr(k), _ptr(v), _ptr(c),
+                                     _ptr(u_k), _ptr(u_v), _ptr(o), _ptr(lse), _ptr(ws),
+                                     0 if ws is None else ws.numel() * ws.element_size(),
+                                     _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_prefill_shared")
+    return (o, lse) if return_lse else o
+
+
+def dar_cache_append_shared(cache: DarCache, k_new, v_new, c_new, Hq=None, stream=None):
+    """Append n tokens with their shared latents c_new [B,Hkv,n,dd]."""
+    assert cache.shared, "a cache made with shared=True"
+    B, Hkv, n, d = k_new.shape
+    shape = make_shape(B, Hq or Hkv, Hkv, d, cache.d_down, cache.w, k_new.dtype)
+    st = lib.dar_cache_append_shared(ctypes.byref(shape), ctypes.byref(cache.struct), _ptr(k_new),
+                                     _ptr(v_new), _ptr(c_new), int(n), _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_cache_append_shared")
+
+
+def dar_attn_decode_shared(cache: DarCache, q, u_k, u_v, o=None, ws=None, stream=None):
+    """One decode step over a shared-latent cache; q [B,Hq,d] at position len-1."""
+    assert cache.shared, "a cache made with shared=True"
+    B, Hq, d = q.shape
+    shape = make_shape(B, Hq, cache.Hkv, d, cache.d_down, cache.w, q.dtype)
+    if o is None:
+        o = torch.empty_like(q)
+    if ws is None:
+        ws = _workspace(dar_decode_workspace_bytes(shape, cache.cap), q.device)
+    st = lib.dar_attn_decode_shared(ctypes.byref(shape), ctypes.byref(cache.struct), _ptr(q),
+                                    _ptr(u_k), _ptr(u_v), _ptr(o), _ptr(ws),
+                                    0 if ws is None else ws.numel() * ws.element_size(),
+                                    _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_decode_shared")
     return o

@@ -31,7 +31,8 @@ bool prefill_mfma_supported(const dar_shape* s);
 hipError_t launch_prefill_mfma(const dar_shape* s, const PrefillGeo& geo, const void* q, const void* k,
                                const void* v, const void* wd, const void* wu, void* o, float* lse,
                                const void* cK, const void* cVt, const float* cnorm,
-                               const float* knorm, const void* consts, hipStream_t st);
+                               const float* knorm, const void* consts, hipStream_t st,
+                               const void* wv = nullptr);
 bool prefill_mfma_rope_supported(const dar_shape* s);
 hipError_t launch_prefill_mfma_rope(const dar_shape* s, int T, const void* qr, const void* kr,
                                     const void* v, const void* kd, const void* vd, void* o,
@@ -114,7 +115,8 @@ void clear_hip_error() { (void)hipGetLastError(); }
 // as L for geo.total() positions.
 hipError_t run_prefill(const dar_shape* s, const PrefillGeo& geo, const void* q, const void* k,
                        const void* v, const void* w_down, const void* w_up, void* o, float* lse,
-                       void* ws, const PrefillWs& L, bool fast, hipStream_t stream) {
+                       void* ws, const PrefillWs& L, bool fast, hipStream_t stream,
+                       const void* w_val = nullptr) {
     char* wsb = (char*)ws;
     void* cK = wsb + L.ck_off;
     void* cV = wsb + L.cv_off;
@@ -130,12 +132,12 @@ hipError_t run_prefill(const dar_shape* s, const PrefillGeo& geo, const void* q,
         if (e != hipSuccess) return e;
         if (fast)
             return launch_prefill_mfma(s, geo, q, k, v, w_down, w_up, o, lse, cK, cV, cnorm, knorm,
-                                       consts, stream);
+                                       consts, stream, w_val);
         return launch_prefill_valu<bf16_t>((const bf16_t*)q, (const bf16_t*)k, (const bf16_t*)v,
                                            (const bf16_t*)w_down, (const bf16_t*)w_up,
                                            (const bf16_t*)cK, (const bf16_t*)cV, (bf16_t*)o, lse,
                                            s->B, s->Hq, s->Hkv, geo, s->d, s->d_down, s->w,
-                                           stream);
+                                           stream, (const bf16_t*)w_val);
     }
     e = launch_prefill_latent<float>((const float*)k, (const float*)v, (const float*)w_down,
                                      (float*)cK, (float*)cV, cnorm, knorm, (float*)consts, s->B,
@@ -144,7 +146,7 @@ hipError_t run_prefill(const dar_shape* s, const PrefillGeo& geo, const void* q,
     return launch_prefill_valu<float>((const float*)q, (const float*)k, (const float*)v,
                                       (const float*)w_down, (const float*)w_up, (const float*)cK,
                                       (const float*)cV, (float*)o, lse, s->B, s->Hq, s->Hkv, geo,
-                                      s->d, s->d_down, s->w, stream);
+                                      s->d, s->d_down, s->w, stream, (const float*)w_val);
 }
 
 // Chunked prefill workspace: the context rows (the ring's tokens from kv0 on,
@@ -537,6 +539,105 @@ dar_status dar_attn_decode_rope(const dar_shape* s, const dar_cache* c, const da
                                       (const float*)c->k_lat, (const float*)c->v_lat, rope->table,
                                       rope->n_pos, (float*)o, (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down,
                                       s->w, c->cap, c->len, r, stream);
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+dar_status dar_attn_prefill_shared(const dar_shape* s, int T, const void* q, const void* k,
+                                   const void* v, const void* c, const void* u_k, const void* u_v,
+                                   void* o, float* lse, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (T < 1) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(c) || !dev_ok(u_k) || !dev_ok(u_v) ||
+        !dev_ok(o))
+        return DAR_E_ARG;
+    if (lse && !aligned16(lse)) return DAR_E_ARG;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+    const PrefillWs L = prefill_ws_layout(s->B, s->Hkv, T, s->d_down, s->w, esize_of(s->dtype));
+    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+
+    clear_hip_error();
+    // every position's latent is given: the pre-pass reads them (as a chunk
+    // reads a cache's) instead of projecting; U_K takes the place of W_up in
+    // the query absorption, U_V in the lift of the output. The pre-pass's
+    // W_down operand is never used for a projection here (U_K, of the same
+    // size, is passed so that its loads stay in bounds).
+    const PrefillGeo geo{0, T, 0, T, T, T, c, c};
+    const bool fast = s->dtype == DAR_BF16 && prefill_mfma_supported(s);
+    if (log_enabled())
+        fprintf(stderr, "[dar] prefill_shared B=%d Hq=%d Hkv=%d T=%d d=%d dd=%d w=%d %s path=%s\n",
+                s->B, s->Hq, s->Hkv, T, s->d, s->d_down, s->w, s->dtype == DAR_BF16 ? "bf16" : "f32",
+                fast ? "mfma" : "valu");
+    const hipError_t e = run_prefill(s, geo, q, k, v, u_k, u_k, o, lse, ws, L, fast, stream, u_v);
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+dar_status dar_cache_append_shared(const dar_shape* s, dar_cache* cache, const void* k_new,
+                                   const void* v_new, const void* c_new, int n,
+                                   hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (!cache || n < 1 || cache->cap < 1 || cache->len < 0 || cache->len > cache->cap)
+        return DAR_E_ARG;
+    if (!dev_ok(k_new) || !dev_ok(v_new) || !dev_ok(c_new) || !dev_ok(cache->k_lat))
+        return DAR_E_ARG;
+    if (s->w > 0 && (!dev_ok(cache->k_win) || !dev_ok(cache->v_win))) return DAR_E_ARG;
+    if ((long long)cache->len + n > (long long)cache->cap) return DAR_E_CAPACITY;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+
+    clear_hip_error();
+    hipError_t e;
+    if (s->dtype == DAR_BF16)
+        e = launch_append_shared<bf16_t>((const bf16_t*)k_new, (const bf16_t*)v_new,
+                                         (const bf16_t*)c_new, (bf16_t*)cache->k_win,
+                                         (bf16_t*)cache->v_win, (bf16_t*)cache->k_lat, s->B, s->Hkv,
+                                         s->d, s->d_down, s->w, cache->cap, cache->len, n, stream);
+    else
+        e = launch_append_shared<float>((const float*)k_new, (const float*)v_new,
+                                        (const float*)c_new, (float*)cache->k_win,
+                                        (float*)cache->v_win, (float*)cache->k_lat, s->B, s->Hkv,
+                                        s->d, s->d_down, s->w, cache->cap, cache->len, n, stream);
+    if (e != hipSuccess) return DAR_E_HIP;
+    cache->len += n;
+    return DAR_OK;
+}
+
+dar_status dar_attn_decode_shared(const dar_shape* s, const dar_cache* cache, const void* q,
+                                  const void* u_k, const void* u_v, void* o, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (!cache || cache->cap < 1 || cache->len < 1 || cache->len > cache->cap) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(u_k) || !dev_ok(u_v) || !dev_ok(o) || !dev_ok(cache->k_lat))
+        return DAR_E_ARG;
+    if (s->w > 0 && (!dev_ok(cache->k_win) || !dev_ok(cache->v_win))) return DAR_E_ARG;
+    if (!group_supported(s)) return DAR_E_UNSUPPORTED;
+    const int G = s->Hq / s->Hkv;
+    if (decode_max_partials(s->B, s->Hkv, cache->cap, s->w, s->d, s->d_down, G) > 1024)
+        return DAR_E_UNSUPPORTED;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+    const size_t need = dar_decode_workspace_bytes(s, cache->cap);
+    if (ws == nullptr || ws_bytes < need) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+
+    clear_hip_error();
+    // keys and values of the distant region read the same latents; U_K is
+    // absorbed into the query, U_V lifts the output
+    hipError_t e;
+    if (s->dtype == DAR_BF16)
+        e = launch_decode<bf16_t>((const bf16_t*)q, (const bf16_t*)u_k, (const bf16_t*)u_k,
+                                  (const bf16_t*)cache->k_win, (const bf16_t*)cache->v_win,
+                                  (const bf16_t*)cache->k_lat, (const bf16_t*)cache->k_lat,
+                                  (bf16_t*)o, (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down,
+                                  s->w, cache->cap, cache->len, stream, (const bf16_t*)u_v);
+    else
+        e = launch_decode<float>((const float*)q, (const float*)u_k, (const float*)u_k,
+                                 (const float*)cache->k_win, (const float*)cache->v_win,
+                                 (const float*)cache->k_lat, (const float*)cache->k_lat, (float*)o,
+                                 (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w,
+                                 cache->cap, cache->len, stream, (const float*)u_v);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 

@@ -87,7 +87,7 @@ template <typename T>
 hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, const T* wu,
                                const T* cK, const T* cVt, T* o, float* lse, int B, int Hq,
                                int Hkv, const PrefillGeo& geo, int d, int dd, int w,
-                               hipStream_t st);
+                               hipStream_t st, const T* wv = nullptr);
 
 // Matrix-core decode (bf16, d in {64,128}, d_down in {16,32}, <= 8 query heads
 // per KV head); shares decode_combine_kernel with the vector-ALU path.
@@ -96,7 +96,8 @@ bool decode_mfma_supported(int d, int dd, int G, bool bf16);
 hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
                               const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_lat,
                               const bf16_t* v_lat, float* part, bf16_t* o, int B, int Hq, int Hkv,
-                              int d, int dd, int w, int cap, int len, int& P, hipStream_t st);
+                              int d, int dd, int w, int cap, int len, int& P, hipStream_t st,
+                              const bf16_t* wv = nullptr);
 
 // The same kernel with the rotary embedding of Eq. 3 (d = 64, rotary
 // dimension 16, 32 or 64); tab [n_pos][r].
@@ -109,7 +110,15 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
 template <typename T>
 hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
-                         int d, int dd, int w, int cap, int len, hipStream_t st);
+                         int d, int dd, int w, int cap, int len, hipStream_t st,
+                         const T* wv = nullptr);
+// Single shared latent: the cache's latent slot of every new token takes its
+// given latent (c_new [B][Hkv][n][dd]); the ring takes the newest min(n, w)
+// tokens' keys and values. No projection.
+template <typename T>
+hipError_t launch_append_shared(const T* k_new, const T* v_new, const T* c_new, T* k_win, T* v_win,
+                                T* lat, int B, int Hkv, int d, int dd, int w, int cap, int len,
+                                int n, hipStream_t st);
 
 // Prefill backward workspace (256-byte aligned parts; Tr = round_up(T, 64)):
 //   lse, delta        [B*Hq][Tr] fp32     dO . O per row (matrix-core path: -lse in
@@ -179,7 +188,8 @@ hipError_t launch_rope_prepass(const T* q, const T* k, const T* v, const T* wd, 
 // (batch, query head) and lifts the latent part (decode_combine_kernel).
 template <typename T>
 hipError_t launch_decode_combine(const float* part, const T* wd, const T* wu, T* o, int B, int Hq,
-                                 int Hkv, int d, int dd, int S, hipStream_t st);
+                                 int Hkv, int d, int dd, int S, hipStream_t st,
+                                 const T* wv = nullptr);
 // Decode with the rotary embedding of Eq. 3 (query at position len - 1, cache
 // token e at position e; positions < len index the table).
 template <typename T>

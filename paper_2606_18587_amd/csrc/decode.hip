@@ -248,7 +248,7 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
 template <typename T>
 __global__ __launch_bounds__(64) void decode_combine_kernel(
     const float* __restrict__ part, const T* __restrict__ wd, const T* __restrict__ wu,
-    T* __restrict__ o, int Hq, int Hkv, int d, int dd, int S) {
+    T* __restrict__ o, int Hq, int Hkv, int d, int dd, int S, const T* __restrict__ wv) {
     constexpr int kLiftCols = 32;  // W_up rows held in registers (d_down <= 32, d <= 64)
     const int bh = wg_id_x();
     const int h = bh % Hq;
@@ -257,7 +257,9 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
     const int stride = 2 + dd + d;
     const float* pp = part + (size_t)bh * S * stride;
     const T* wdg = wd + (size_t)g * d * dd;
-    const T* wug = wu ? wu + (size_t)g * dd * d : nullptr;
+    // the lift's matrix: W_up (W_down^T when tied), or (shared latent) the
+    // value matrix
+    const T* wug = wv ? wv + (size_t)g * dd * d : (wu ? wu + (size_t)g * dd * d : nullptr);
     const bool lift_regs = dd <= kLiftCols && d <= 64;
 
     const T* wp = wug ? wug + imin(lane, d - 1) : wdg + (size_t)imin(lane, d - 1) * dd;
@@ -342,16 +344,17 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
 
 template <typename T>
 hipError_t launch_decode_combine(const float* part, const T* wd, const T* wu, T* o, int B, int Hq,
-                                 int Hkv, int d, int dd, int S, hipStream_t st) {
+                                 int Hkv, int d, int dd, int S, hipStream_t st, const T* wv) {
     hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu, o, Hq,
-                       Hkv, d, dd, S);
+                       Hkv, d, dd, S, wv);
     return hipGetLastError();
 }
 template hipError_t launch_decode_combine<float>(const float*, const float*, const float*, float*,
-                                                 int, int, int, int, int, int, hipStream_t);
+                                                 int, int, int, int, int, int, hipStream_t,
+                                                 const float*);
 template hipError_t launch_decode_combine<bf16_t>(const float*, const bf16_t*, const bf16_t*,
                                                   bf16_t*, int, int, int, int, int, int,
-                                                  hipStream_t);
+                                                  hipStream_t, const bf16_t*);
 
 static int group_chunk(int G) { return kDecScoreSlots / G; }
 
@@ -386,7 +389,7 @@ template <typename T, int G>
 static hipError_t launch_decode_g(const T* q, const T* wd, const T* wu, const T* k_win,
                                   const T* v_win, const T* k_lat, const T* v_lat, T* o,
                                   float* part, int B, int Hq, int Hkv, int d, int dd, int w,
-                                  int cap, int len, hipStream_t st) {
+                                  int cap, int len, hipStream_t st, const T* wv) {
     DecodeSplits sp = decode_splits(len, w, d, dd, G);
     const int S = sp.n_lat_split + sp.n_win_split;
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
@@ -396,40 +399,42 @@ static hipError_t launch_decode_g(const T* q, const T* wd, const T* wu, const T*
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu, o,
-                       Hq, Hkv, d, dd, S);
+                       Hq, Hkv, d, dd, S, wv);
     return hipGetLastError();
 }
 
 template <typename T>
 hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,
-                         int d, int dd, int w, int cap, int len, hipStream_t st) {
+                         int d, int dd, int w, int cap, int len, hipStream_t st, const T* wv) {
     if (decode_mfma_supported(d, dd, Hq / Hkv, sizeof(T) == 2)) {
         int P = 0;
         hipError_t e = launch_decode_mfma((const bf16_t*)q, (const bf16_t*)wd, (const bf16_t*)wu,
                                           (const bf16_t*)k_win, (const bf16_t*)v_win,
                                           (const bf16_t*)k_lat, (const bf16_t*)v_lat, part,
-                                          (bf16_t*)o, B, Hq, Hkv, d, dd, w, cap, len, P, st);
+                                          (bf16_t*)o, B, Hq, Hkv, d, dd, w, cap, len, P, st,
+                                          (const bf16_t*)wv);
         if (e != hipSuccess || P == 1) return e;
         hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu,
-                           o, Hq, Hkv, d, dd, P);
+                           o, Hq, Hkv, d, dd, P, wv);
         return hipGetLastError();
     }
     switch (Hq / Hkv) {
-        case 1: return launch_decode_g<T, 1>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
-        case 2: return launch_decode_g<T, 2>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
-        case 4: return launch_decode_g<T, 4>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
-        case 8: return launch_decode_g<T, 8>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st);
+        case 1: return launch_decode_g<T, 1>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st, wv);
+        case 2: return launch_decode_g<T, 2>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st, wv);
+        case 4: return launch_decode_g<T, 4>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st, wv);
+        case 8: return launch_decode_g<T, 8>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st, wv);
         default: return hipErrorInvalidValue;
     }
 }
 
 template hipError_t launch_decode<float>(const float*, const float*, const float*, const float*,
                                          const float*, const float*, const float*, float*, float*,
-                                         int, int, int, int, int, int, int, int, hipStream_t);
+                                         int, int, int, int, int, int, int, int, hipStream_t,
+                                         const float*);
 template hipError_t launch_decode<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
                                           const bf16_t*, const bf16_t*, const bf16_t*,
                                           const bf16_t*, bf16_t*, float*, int, int, int, int, int,
-                                          int, int, int, hipStream_t);
+                                          int, int, int, hipStream_t, const bf16_t*);
 
 }  // namespace dar

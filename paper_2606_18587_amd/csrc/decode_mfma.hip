@@ -306,7 +306,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const bf16_t* __restrict__ k_win, const bf16_t* __restrict__ v_win,
     const bf16_t* __restrict__ k_lat, const bf16_t* __restrict__ v_lat, float* __restrict__ part,
     bf16_t* __restrict__ o, int Hq, int Hkv, int w, int cap, int len, int P, float qscale,
-    const float* __restrict__ tab, int n_pos) {
+    const float* __restrict__ tab, int n_pos, const bf16_t* __restrict__ wv) {
     static_assert(R == 0 || (D == 64 && R % 16 == 0 && R <= D), "rotary: d = 64, R a multiple of 16");
     constexpr int KS = D / 16, DS = DD / 16, NT = D / 32;
     constexpr int LDW = D + 8;                      // padded ring row in LDS (bf16)
@@ -331,6 +331,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     if (fuse) {
         const bf16_t* wdg = wd + (size_t)g * D * DD;
         const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
+        // the lift's matrix: W_up, or (shared latent) the value matrix
+        const bf16_t* wlift = wv ? wv + (size_t)g * DD * D : wug;
         // (all of this thread's elements requested at once, no load under a
         // branch: the cache stream below is not held up by them)
         constexpr int UPT = (DD * D + NW * 64 - 1) / (NW * 64);
@@ -339,7 +341,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         for (int j = 0; j < UPT; ++j) {
             const int idx = imin(tid + j * NW * 64, DD * D - 1);
             const int c = idx / D, e = idx - (idx / D) * D;
-            uv[j] = *(wug ? wug + (size_t)c * D + e : wdg + (size_t)e * DD + c);
+            uv[j] = *(wlift ? wlift + (size_t)c * D + e : wdg + (size_t)e * DD + c);
         }
 #pragma unroll
         for (int j = 0; j < UPT; ++j) {
@@ -774,14 +776,15 @@ int decode_mfma_parts(int B, int Hkv, int len, int w, int d) {
 hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
                               const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_lat,
                               const bf16_t* v_lat, float* part, bf16_t* o, int B, int Hq, int Hkv,
-                              int d, int dd, int w, int cap, int len, int& P, hipStream_t st) {
+                              int d, int dd, int w, int cap, int len, int& P, hipStream_t st,
+                              const bf16_t* wv) {
     P = decode_mfma_parts(B, Hkv, len, w, d);
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
     dim3 grid(P, B * Hkv);
 #define DAR_DEC_LAUNCH(D_, DD_)                                                                     \
     hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value>), grid,                    \
                        dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
-                       part, o, Hq, Hkv, w, cap, len, P, qscale, (const float*)nullptr, 0)
+                       part, o, Hq, Hkv, w, cap, len, P, qscale, (const float*)nullptr, 0, wv)
     if (d == 64 && dd == 16) DAR_DEC_LAUNCH(64, 16);
     else if (d == 64 && dd == 32) DAR_DEC_LAUNCH(64, 32);
     else if (d == 128 && dd == 16) DAR_DEC_LAUNCH(128, 16);
@@ -806,7 +809,7 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
 #define DAR_DEC_ROPE(DD_, R_)                                                                        \
     hipLaunchKernelGGL((decode_mfma_kernel<64, DD_, DecWaves<64>::value, R_>), grid,                 \
                        dim3(64 * DecWaves<64>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
-                       part, o, Hq, Hkv, w, cap, len, P, qscale, tab, n_pos)
+                       part, o, Hq, Hkv, w, cap, len, P, qscale, tab, n_pos, (const bf16_t*)nullptr)
     if (dd == 16) {
         if (r == 16) DAR_DEC_ROPE(16, 16);
         else if (r == 32) DAR_DEC_ROPE(16, 32);

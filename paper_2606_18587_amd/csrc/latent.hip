@@ -609,3 +609,51 @@ template hipError_t launch_append<float>(const float*, const float*, const float
                                          hipStream_t);
 
 }  // namespace dar
+
+namespace dar {
+
+// Append with a single shared latent per token (its latent is given, one
+// per token and KV head): grid (n, B*Hkv), 64 threads; token t (position
+// len + t) goes to latent slot len + t, and to ring slot (len + t) % w when
+// it is one of the newest min(n, w). Plain copies, so the cache holds the
+// given bits.
+template <typename T>
+__global__ __launch_bounds__(64) void append_shared_kernel(const T* __restrict__ k_new,
+                                                           const T* __restrict__ v_new,
+                                                           const T* __restrict__ c_new,
+                                                           T* __restrict__ k_win, T* __restrict__ v_win,
+                                                           T* __restrict__ lat, int d, int dd, int w,
+                                                           int cap, int len, int n) {
+    const int t = wg_id_x(), bg = wg_id_y();
+    const int lane = lane_id_x();
+    const int pos = len + t;
+    const T* cs = c_new + ((size_t)bg * n + t) * dd;
+    T* cd = lat + ((size_t)bg * cap + pos) * dd;
+    for (int c = lane; c < dd; c += 64) cd[c] = cs[c];
+    if (w > 0 && t >= n - imin(n, w)) {
+        const size_t src = ((size_t)bg * n + t) * d;
+        const size_t dst = ((size_t)bg * w + pos % w) * d;
+        for (int e = lane; e < d; e += 64) {
+            k_win[dst + e] = k_new[src + e];
+            v_win[dst + e] = v_new[src + e];
+        }
+    }
+}
+
+template <typename T>
+hipError_t launch_append_shared(const T* k_new, const T* v_new, const T* c_new, T* k_win, T* v_win,
+                                T* lat, int B, int Hkv, int d, int dd, int w, int cap, int len,
+                                int n, hipStream_t st) {
+    hipLaunchKernelGGL(append_shared_kernel<T>, dim3(n, B * Hkv), dim3(64), 0, st, k_new, v_new,
+                       c_new, k_win, v_win, lat, d, dd, w, cap, len, n);
+    return hipGetLastError();
+}
+
+template hipError_t launch_append_shared<float>(const float*, const float*, const float*, float*,
+                                                float*, float*, int, int, int, int, int, int, int,
+                                                int, hipStream_t);
+template hipError_t launch_append_shared<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
+                                                 bf16_t*, bf16_t*, bf16_t*, int, int, int, int, int,
+                                                 int, int, int, hipStream_t);
+
+}  // namespace dar

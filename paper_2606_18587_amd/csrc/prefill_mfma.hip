@@ -584,7 +584,7 @@ void prefill_mfma_kernel(
     const bf16_t* __restrict__ cVt, const float* __restrict__ cnorm,
     const float* __restrict__ knorm, const bf16_t* __restrict__ consts, bf16_t* __restrict__ o,
     float* __restrict__ lse, int Hq, int Hkv, int T, int w, int Tp, int nblk, int BH,
-    float c_scale, int q0, int n_rows, int kv0, int Tkv) {
+    float c_scale, int q0, int n_rows, int kv0, int Tkv, const bf16_t* __restrict__ wv) {
     constexpr int BM = NW * 32;
     constexpr int KS = D / 16;   // 16-wide k slabs of q . k
     constexpr int DS = DD / 16;  // 16-wide k slabs of q~ . c^K
@@ -596,6 +596,9 @@ void prefill_mfma_kernel(
     bf16_t* lds_k = smem;                    // [2][BN][LDK]
     bf16_t* lds_v = smem + 2 * BN * LDK;     // [2][BN][LDK]
     bf16_t* wU = smem + 4 * BN * LDK;        // [DD][LDU]: U[c][e] = W_up[c][e]
+    // the value lift's matrix: W_up itself, or (shared latent) a second one
+    // [Hkv][DD][D] staged after it
+    bf16_t* wV = wv ? wU + DD * LDU : wU;
 
     // Each workgroup takes row blocks p and nblk-1-p of one (batch, head): a
     // short and a long causal row block, so every workgroup has the same work.
@@ -639,6 +642,19 @@ void prefill_mfma_kernel(
         for (int j = 0; j < UPT; ++j) {
             const int idx = tid + j * NW * 64, cc = idx / D, e = idx - (idx / D) * D;
             wU[cc * LDU + e] = uv[j];
+        }
+        if (wv) {
+            const bf16_t* wvg = wv + (size_t)g * DD * D;
+#pragma unroll
+            for (int j = 0; j < UPT; ++j) {
+                const int idx = tid + j * NW * 64;
+                uv[j] = wvg[idx];
+            }
+#pragma unroll
+            for (int j = 0; j < UPT; ++j) {
+                const int idx = tid + j * NW * 64, cc = idx / D, e = idx - (idx / D) * D;
+                wV[cc * LDU + e] = uv[j];
+            }
         }
     }
     __syncthreads();
@@ -831,7 +847,7 @@ void prefill_mfma_kernel(
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
                     // A row e = t*32 + qc, k = latent columns s*16 + {4hg..4hg+3, 8+4hg..8+4hg+3}
-                    const bf16_t* ur = wU + (s * 16 + 4 * hg) * LDU + t * 32 + qc;
+                    const bf16_t* ur = wV + (s * 16 + 4 * hg) * LDU + t * 32 + qc;
                     uint16_t a8[8];
 #pragma unroll
                     for (int j = 0; j < 4; ++j) {
@@ -875,7 +891,8 @@ template <int D, int DD, bool ROPE = false>
 static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w, const void* q, const void* k,
                             const void* v, const void* wd, const void* wu, void* o, float* lse,
                             const void* cK, const void* cVt, const float* cnorm,
-                            const float* knorm, const void* consts, hipStream_t st) {
+                            const float* knorm, const void* consts, hipStream_t st,
+                            const void* wv = nullptr) {
     constexpr int NW = 4;
     constexpr int BM = NW * 32;
     const int T = geo.total();
@@ -884,7 +901,7 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w
     const int BH = B * Hq;
     const int Tp = ROPE ? round_up(T - w > 0 ? T - w : 0, 32) : prefill_tp(T, w);
     const float c_scale = 1.4426950408889634f / sqrtf((float)D);
-    const size_t lds = sizeof(bf16_t) * (4 * 64 * (D + 8) + DD * (D + 8));
+    const size_t lds = sizeof(bf16_t) * (4 * 64 * (D + 8) + (wv ? 2 : 1) * DD * (D + 8));
     auto kern = prefill_mfma_kernel<D, DD, NW, ROPE>;
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -894,19 +911,20 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w
                        (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)wd, (const bf16_t*)wu,
                        (const bf16_t*)cK, (const bf16_t*)cVt, cnorm, knorm, (const bf16_t*)consts,
                        (bf16_t*)o, lse, Hq, Hkv, T, w, Tp, nblk, BH, c_scale, geo.q0,
-                       geo.n_rows, geo.kv0, geo.Tkv);
+                       geo.n_rows, geo.kv0, geo.Tkv, (const bf16_t*)wv);
     return hipGetLastError();
 }
 
 hipError_t launch_prefill_mfma(const dar_shape* s, const PrefillGeo& geo, const void* q, const void* k,
                                const void* v, const void* wd, const void* wu, void* o, float* lse,
                                const void* cK, const void* cVt, const float* cnorm,
-                               const float* knorm, const void* consts, hipStream_t st) {
+                               const float* knorm, const void* consts, hipStream_t st,
+                               const void* wv) {
     const int B = s->B, Hq = s->Hq, Hkv = s->Hkv, w = s->w;
-    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
-    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
-    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
-    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st);
+    if (s->d == 64 && s->d_down == 16) return launch_dd<64, 16>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st, wv);
+    if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st, wv);
+    if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st, wv);
+    if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st, wv);
     return hipErrorNotSupported;
 }
 

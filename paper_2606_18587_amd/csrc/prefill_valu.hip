@@ -21,7 +21,8 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
     const T* __restrict__ q, const T* __restrict__ k, const T* __restrict__ v,
     const T* __restrict__ wd, const T* __restrict__ wu, const T* __restrict__ cK,
     const T* __restrict__ cVt, T* __restrict__ o, float* __restrict__ lse, int Hq, int Hkv,
-    int q0, int n_rows, int kv0, int Tkv, int d, int dd, int w, int Tp, float qscale) {
+    int q0, int n_rows, int kv0, int Tkv, int d, int dd, int w, int Tp, float qscale,
+    const T* __restrict__ wv) {
     __shared__ float qs[256];
     __shared__ float qts[256];
     __shared__ float ps[64];
@@ -35,6 +36,7 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
     const int bg = b * Hkv + g;
     const T* wdg = wd + (size_t)g * d * dd;
     const T* wug = wu ? wu + (size_t)g * dd * d : nullptr;
+    const T* wvg = wv ? wv + (size_t)g * dd * d : nullptr;  // value lift (shared latent), else W_up
 
     const T* qrow = q + ((size_t)bh * n_rows + row) * d;
     for (int e = lane; e < d; e += 64) qs[e] = elem<T>::load(qrow + e) * qscale;
@@ -146,7 +148,8 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
             float acc = aw[r];
             if (n_dist > 0)
                 for (int c = 0; c < dd; ++c) {
-                    const float u = wug ? elem<T>::load(wug + (size_t)c * d + e)
+                    const float u = wvg ? elem<T>::load(wvg + (size_t)c * d + e)
+                                  : wug ? elem<T>::load(wug + (size_t)c * d + e)
                                         : elem<T>::load(wdg + (size_t)e * dd + c);
                     acc = __builtin_fmaf(lat[c], u, acc);
                 }
@@ -159,22 +162,24 @@ template <typename T>
 hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, const T* wu,
                                const T* cK, const T* cVt, T* o, float* lse, int B, int Hq,
                                int Hkv, const PrefillGeo& geo, int d, int dd, int w,
-                               hipStream_t st) {
+                               hipStream_t st, const T* wv) {
     const int Tp = prefill_tp(geo.total(), w);
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
     dim3 grid(geo.n_rows, B * Hq);
     hipLaunchKernelGGL(prefill_valu_kernel<T>, grid, dim3(64), 0, st, q, k, v, wd, wu, cK, cVt, o,
-                       lse, Hq, Hkv, geo.q0, geo.n_rows, geo.kv0, geo.Tkv, d, dd, w, Tp, qscale);
+                       lse, Hq, Hkv, geo.q0, geo.n_rows, geo.kv0, geo.Tkv, d, dd, w, Tp, qscale, wv);
     return hipGetLastError();
 }
 
 template hipError_t launch_prefill_valu<float>(const float*, const float*, const float*,
                                                const float*, const float*, const float*,
                                                const float*, float*, float*, int, int, int,
-                                               const PrefillGeo&, int, int, int, hipStream_t);
+                                               const PrefillGeo&, int, int, int, hipStream_t,
+                                               const float*);
 template hipError_t launch_prefill_valu<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
                                                 const bf16_t*, const bf16_t*, const bf16_t*,
                                                 const bf16_t*, bf16_t*, float*, int, int, int,
-                                                const PrefillGeo&, int, int, int, hipStream_t);
+                                                const PrefillGeo&, int, int, int, hipStream_t,
+                                                const bf16_t*);
 
 }  // namespace dar

@@ -34,6 +34,8 @@ def test_exports_every_declared_symbol():
                           "dar_decode_workspace_bytes", "dar_prefill_backward_workspace_bytes",
                           "dar_attn_prefill_chunk", "dar_prefill_chunk_workspace_bytes",
                           "dar_rope_table", "dar_attn_prefill_rope", "dar_attn_decode_rope",
+                          "dar_attn_prefill_shared", "dar_cache_append_shared",
+                          "dar_attn_decode_shared",
                           "dar_prefill_rope_workspace_bytes", "dar_status_string"}
     raw = ctypes.CDLL(dar.LIB_PATH)
     for n in names:
@@ -340,3 +342,25 @@ def test_decode_rope_rejects_before_any_launch():
     assert call(cache_struct(cap=64, length=10), table=None) == dar.DAR_E_ARG
     assert call(cache_struct(cap=64, length=10), q=MISALIGNED) == dar.DAR_E_ARG
     assert call(cache_struct(cap=64, length=10), ws_bytes=8) == dar.DAR_E_WORKSPACE
+
+
+@no_gpu
+def test_shared_latent_rejects_before_any_launch():
+    s = S()
+    pf = lambda T=16, c=FAKE, uv=FAKE, ws_bytes=1 << 30: dar.lib.dar_attn_prefill_shared(
+        ctypes.byref(s), T, FAKE, FAKE, FAKE, c, FAKE, uv, FAKE, None, FAKE, ws_bytes, None)
+    assert pf(c=None) == dar.DAR_E_ARG
+    assert pf(uv=MISALIGNED) == dar.DAR_E_ARG
+    assert pf(T=0) == dar.DAR_E_ARG
+    assert pf(ws_bytes=16) == dar.DAR_E_WORKSPACE
+    c = cache_struct(cap=64, length=60)
+    ap = lambda n=2, cn=FAKE: dar.lib.dar_cache_append_shared(ctypes.byref(s), ctypes.byref(c),
+                                                             FAKE, FAKE, cn, n, None)
+    assert ap(n=5) == dar.DAR_E_CAPACITY and c.len == 60
+    assert ap(cn=None) == dar.DAR_E_ARG and c.len == 60
+    assert ap(n=0) == dar.DAR_E_ARG and c.len == 60
+    dc = lambda cc, uk=FAKE, ws_bytes=1 << 30: dar.lib.dar_attn_decode_shared(
+        ctypes.byref(s), ctypes.byref(cc), FAKE, uk, FAKE, FAKE, FAKE, ws_bytes, None)
+    assert dc(cache_struct(cap=64, length=0)) == dar.DAR_E_ARG
+    assert dc(cache_struct(cap=64, length=10), uk=None) == dar.DAR_E_ARG
+    assert dc(cache_struct(cap=64, length=10), ws_bytes=8) == dar.DAR_E_WORKSPACE
