@@ -20,7 +20,10 @@ cold cache hierarchy (a 1 GiB buffer written between calls evicts L2 and
 the Infinity Cache; the time of the writes alone is subtracted), the prefill
 and the decode with the rotary embedding inside Eq. 3 (prefill: rotary
 dimension 16 of 64, base 10000, as in the Pythia models; decode: full
-rotation), the chunked prefill and the other prefill workloads.
+rotation), the prefill and the decode with a single shared latent per token
+(the same batches, with seeded N(0,1) latents and N(0, 1/d_down) U_K, U_V:
+the decode streams one latent array instead of two), the chunked prefill and
+the other prefill workloads.
 
 Prints ONE JSON line (rank 0). Only one GPU is used: --gpus above 1 exits.
 """
@@ -120,6 +123,15 @@ def backward_flops(B, Hq, T, d, dd, w):
     return float(B * Hq * (10 * d * n_loc + 12 * dd * n_dist))
 
 
+def decode_bytes_shared(B, Hq, Hkv, d, dd, w, L, esize=2):
+    """As decode_bytes with one shared latent per token (one latent stream
+    for keys and values), plus the two U matrices."""
+    n_win = min(L, w)
+    n_lat = L - n_win
+    kv = B * Hkv * (2 * n_win * d + n_lat * dd) * esize
+    return float(kv + 2 * B * Hq * d * esize + 2 * Hkv * d * dd * esize)
+
+
 def full_flops(B, Hq, T, d):
     """Causal attention at d for every pair (the rotary path: distant keys are
     lifted to full d, Eq. 3): 4 d flop per pair."""
@@ -149,6 +161,8 @@ def main():
                     help="skip the prefill workloads reported beside the main one")
     ap.add_argument("--no-rope", action="store_true",
                     help="skip the prefill and decode with the rotary embedding")
+    ap.add_argument("--no-shared", action="store_true",
+                    help="skip the prefill and decode with a single shared latent")
     ap.add_argument("--no-cold", action="store_true",
                     help="skip the cold-cache timings")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
@@ -198,6 +212,17 @@ def main():
     kpre, vpre = up(pre["k"]), up(pre["v"])
     del pre
     dar.dar_cache_append(cache, kpre, vpre, dwd, Hq=dw.Hq)
+    # the same tokens in a single-shared-latent cache, with seeded latents
+    scache = None
+    if not args.no_shared:
+        gs = torch.Generator(device=dev).manual_seed(260618588)
+        scache = dar.DarCache(dw.B, dw.Hkv, dw.d, dw.dd, dw.w, dw.T, torch.bfloat16, device=dev,
+                              shared=True)
+        clat = torch.randn(dw.B, dw.Hkv, dw.T, dw.dd, device=dev, generator=gs).bfloat16()
+        dar.dar_cache_append_shared(scache, kpre, vpre, clat, Hq=dw.Hq)
+        s_uk = (torch.randn(dw.Hkv, dw.dd, dw.d, device=dev, generator=gs) / dw.dd ** 0.5).bfloat16()
+        s_uv = (torch.randn(dw.Hkv, dw.dd, dw.d, device=dev, generator=gs) / dw.dd ** 0.5).bfloat16()
+        del clat
     del kpre, vpre
     dshape = dar.make_shape(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, torch.bfloat16)
     dws = torch.empty(dar.dar_decode_workspace_bytes(dshape, cap), dtype=torch.uint8, device=dev)
@@ -265,6 +290,26 @@ def main():
         cold["decode_ms"] = timed_cold(
             lambda i: dar.dar_attn_decode(cache, qd_last, dwd, None, o=dout, ws=dws), args.steps)
         del flushbuf
+
+    # single shared latent: the prefill batch with seeded latents, and the
+    # decode over the shared cache (query at its last position)
+    shared = {}
+    if scache is not None:
+        gp = torch.Generator(device=dev).manual_seed(260618589)
+        pc = torch.randn(pw.B, pw.Hkv, pw.T, pw.dd, device=dev, generator=gp).bfloat16()
+        p_uk = (torch.randn(pw.Hkv, pw.dd, pw.d, device=dev, generator=gp) / pw.dd ** 0.5).bfloat16()
+        p_uv = (torch.randn(pw.Hkv, pw.dd, pw.d, device=dev, generator=gp) / pw.dd ** 0.5).bfloat16()
+        run_sp = lambda i: dar.dar_attn_prefill_shared(q, k, v, pc, p_uk, p_uv, pw.w, o=o, ws=ws)
+        for i in range(args.warmup):
+            run_sp(i)
+        shared["prefill_ms"] = timed(run_sp, args.steps)
+        del pc
+        run_sd = lambda i: dar.dar_attn_decode_shared(scache, qd_last, s_uk, s_uv, o=dout, ws=dws)
+        for i in range(args.warmup):
+            run_sd(i)
+        shared["decode_ms"] = timed(run_sd, args.steps)
+        shared["decode_len"] = scache.len
+        del scache
 
     # the rotary embedding inside Eq. 3: the same prefill batch (un-rotated
     # queries and keys) and the same decode cache
@@ -413,6 +458,21 @@ def main():
         du = float(cold["decode_ms"] * 1e3)
         result["decode"]["cold_us"] = round(du, 2)
         result["decode"]["cold_gbs"] = round(dbytes / (du * 1e-6) / 1e9, 1)
+    if shared:
+        su = float(shared["prefill_ms"] * 1e3)
+        result["prefill_shared"] = {
+            "shape": "pythia70m batch, one shared latent per token",
+            "us": round(su, 2), "alg_flop": flops, "tflops": round(flops / (su * 1e-6) / 1e12, 2),
+            "frac_bf16_peak": round(flops / (su * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        sdu = float(shared["decode_ms"] * 1e3)
+        sb = decode_bytes_shared(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, shared["decode_len"])
+        result["decode_shared"] = {
+            "shape": "decode1b batch, one shared latent per token, %d cached tokens"
+                     % shared["decode_len"],
+            "us": round(sdu, 2), "alg_bytes": sb, "gbs": round(sb / (sdu * 1e-6) / 1e9, 1),
+            "frac_hbm_peak": round(sb / (sdu * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+            "bytes_vs_two_latents": round(sb / decode_bytes(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w,
+                                                            shared["decode_len"]), 4)}
     if rope:
         ru = float(rope["prefill_ms"] * 1e3)
         rfl = full_flops(pw.B, pw.Hq, pw.T, pw.d)
