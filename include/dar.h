@@ -83,6 +83,29 @@ typedef struct {
     int len;
 } dar_cache;
 
+/* Paged split cache with one length per sequence (serving: sequences of
+ * different lengths in one batch, memory handed out in pages). Device
+ * buffers owned by the caller, this struct on the host.
+ *   k_win, v_win  [B][Hkv][w][d]      ring per sequence, token p in slot p % w
+ *                                     while p >= lens[b] - w
+ *   k_pool, v_pool [n_pages][Hkv][page_size][d_down]  latent pages: token e
+ *                 of sequence b (e < lens[b] - w) in page
+ *                 block_table[b * max_blocks + e / page_size], row
+ *                 e % page_size (every KV head of the token in that page)
+ *   block_table   device int [B][max_blocks] (caller-managed; an entry
+ *                 outside [0, n_pages) is never read or written through:
+ *                 such tokens are not stored and read as zeros)
+ *   lens          device int [B], tokens held per sequence (the append
+ *                 advances it on the device; the host never reads it)
+ *   page_size     a multiple of 32; capacity max_blocks * page_size tokens
+ *                 per sequence */
+typedef struct {
+    void *k_win, *v_win, *k_pool, *v_pool;
+    const int* block_table;
+    int* lens;
+    int page_size, max_blocks, n_pages;
+} dar_paged_cache;
+
 /* Causal prefill over positions 0..T-1 (Eq. 3-4 for every row).
  *   q [B][Hq][T][d], k, v [B][Hkv][T][d], w_down [Hkv][d][d_down],
  *   w_up [Hkv][d_down][d] or NULL (tied), o [B][Hq][T][d] (output).
@@ -193,6 +216,26 @@ dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q
 dar_status dar_attn_decode_rope(const dar_shape* s, const dar_cache* c, const dar_rope* rope,
                                 const void* q, const void* w_down, const void* w_up, void* o,
                                 void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* One token per sequence appended to a paged cache: k_new, v_new
+ * [B][Hkv][d] at position lens[b] of each sequence. The token leaving the
+ * window (position lens[b] - w) is projected with W_down (Eq. 1, the same
+ * arithmetic as dar_cache_append, bit-identical latents) into its page slot;
+ * the new token goes to the ring; then lens[b] += 1 on the device (stream
+ * order). A sequence at capacity stores nothing and keeps its length. The
+ * pages of the blocks being written must be mapped in block_table. */
+dar_status dar_cache_append_paged(const dar_shape* s, const dar_paged_cache* c, const void* k_new,
+                                  const void* v_new, const void* w_down, hipStream_t stream);
+
+/* One decode step over a paged cache: the query q [B][Hq][d] of sequence b
+ * sits at position lens[b] - 1 (its own key and value already appended;
+ * lens[b] >= 1). As dar_attn_decode otherwise; ws: at least
+ * dar_decode_workspace_bytes(s, max_blocks * page_size) bytes. Supported:
+ * the matrix-core shapes (bf16, d in {64, 128}, d_down in {16, 32},
+ * Hq / Hkv in {1, 2, 4, 8}). */
+dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, const void* q,
+                                 const void* w_down, const void* w_up, void* o, void* ws,
+                                 size_t ws_bytes, hipStream_t stream);
 
 /* Single shared latent (the Limitations section's cache): one d_down latent
  * per token and KV head, c_j = h_j W_down of Eq. 1, from which both the

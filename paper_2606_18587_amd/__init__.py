@@ -36,6 +36,13 @@ class DarRopeStruct(ctypes.Structure):
                 ("table", ctypes.c_void_p)]
 
 
+class DarPagedCacheStruct(ctypes.Structure):
+    _fields_ = [("k_win", ctypes.c_void_p), ("v_win", ctypes.c_void_p),
+                ("k_pool", ctypes.c_void_p), ("v_pool", ctypes.c_void_p),
+                ("block_table", ctypes.c_void_p), ("lens", ctypes.c_void_p),
+                ("page_size", ctypes.c_int), ("max_blocks", ctypes.c_int), ("n_pages", ctypes.c_int)]
+
+
 class DarError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
@@ -81,6 +88,11 @@ def _load():
     lib.dar_cache_append_shared.argtypes = [shp, cp, vp, vp, vp, ci, vp]
     lib.dar_attn_decode_shared.restype = ci
     lib.dar_attn_decode_shared.argtypes = [shp, cp] + [vp] * 5 + [sz, vp]
+    pcp = ctypes.POINTER(DarPagedCacheStruct)
+    lib.dar_cache_append_paged.restype = ci
+    lib.dar_cache_append_paged.argtypes = [shp, pcp, vp, vp, vp, vp]
+    lib.dar_attn_decode_paged.restype = ci
+    lib.dar_attn_decode_paged.argtypes = [shp, pcp] + [vp] * 5 + [sz, vp]
     lib.dar_prefill_rope_workspace_bytes.restype = sz
     lib.dar_prefill_rope_workspace_bytes.argtypes = [shp, ci]
     lib.dar_status_string.restype = ctypes.c_char_p
@@ -456,4 +468,62 @@ def dar_attn_decode_shared(cache: DarCache, q, u_k, u_v, o=None, ws=None, stream
                                     _stream(stream))
     if st != DAR_OK:
         raise DarError(st, "dar_attn_decode_shared")
+    return o
+
+
+class DarPagedCache:
+    """Paged split cache (include/dar.h, dar_paged_cache): rings [B,Hkv,w,d],
+    latent pages [n_pages,Hkv,page_size,dd] for keys and values, a block table
+    [B,max_blocks] (int32, device) and per-sequence lengths [B] (int32,
+    device). block_table and lens are plain torch tensors the caller fills."""
+
+    def __init__(self, B, Hkv, d, d_down, w, page_size, max_blocks, n_pages, dtype,
+                 device="cuda"):
+        self.B, self.Hkv, self.d, self.d_down, self.w = B, Hkv, d, d_down, w
+        self.page_size, self.max_blocks, self.n_pages = page_size, max_blocks, n_pages
+        wl = max(w, 1)
+        self.k_win = torch.zeros(B, Hkv, wl, d, dtype=dtype, device=device)
+        self.v_win = torch.zeros(B, Hkv, wl, d, dtype=dtype, device=device)
+        self.k_pool = torch.zeros(n_pages, Hkv, page_size, d_down, dtype=dtype, device=device)
+        self.v_pool = torch.zeros(n_pages, Hkv, page_size, d_down, dtype=dtype, device=device)
+        self.block_table = torch.full((B, max_blocks), -1, dtype=torch.int32, device=device)
+        self.lens = torch.zeros(B, dtype=torch.int32, device=device)
+
+    @property
+    def cap(self):
+        return self.page_size * self.max_blocks
+
+    def struct(self) -> DarPagedCacheStruct:
+        return DarPagedCacheStruct(self.k_win.data_ptr(), self.v_win.data_ptr(),
+                                   self.k_pool.data_ptr(), self.v_pool.data_ptr(),
+                                   self.block_table.data_ptr(), self.lens.data_ptr(),
+                                   self.page_size, self.max_blocks, self.n_pages)
+
+
+def dar_cache_append_paged(cache: DarPagedCache, k_new, v_new, w_down, Hq=None, stream=None):
+    """One token per sequence: k_new, v_new [B,Hkv,d]; lens advance on the device."""
+    B, Hkv, d = k_new.shape
+    shape = make_shape(B, Hq or Hkv, Hkv, d, cache.d_down, cache.w, k_new.dtype)
+    cs = cache.struct()
+    st = lib.dar_cache_append_paged(ctypes.byref(shape), ctypes.byref(cs), _ptr(k_new), _ptr(v_new),
+                                    _ptr(w_down), _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_cache_append_paged")
+
+
+def dar_attn_decode_paged(cache: DarPagedCache, q, w_down, w_up=None, o=None, ws=None, stream=None):
+    """One decode step per sequence (query at position lens[b] - 1)."""
+    B, Hq, d = q.shape
+    shape = make_shape(B, Hq, cache.Hkv, d, cache.d_down, cache.w, q.dtype)
+    if o is None:
+        o = torch.empty_like(q)
+    if ws is None:
+        ws = _workspace(dar_decode_workspace_bytes(shape, cache.cap), q.device)
+    cs = cache.struct()
+    st = lib.dar_attn_decode_paged(ctypes.byref(shape), ctypes.byref(cs), _ptr(q), _ptr(w_down),
+                                   _ptr(w_up), _ptr(o), _ptr(ws),
+                                   0 if ws is None else ws.numel() * ws.element_size(),
+                                   _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_decode_paged")
     return o

@@ -641,4 +641,69 @@ dar_status dar_attn_decode_shared(const dar_shape* s, const dar_cache* cache, co
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 
+static dar_status check_paged(const dar_shape* s, const dar_paged_cache* c) {
+    if (!c || c->page_size < 32 || c->page_size % 32 != 0 || c->max_blocks < 1 || c->n_pages < 1)
+        return DAR_E_ARG;
+    if ((long long)c->page_size * c->max_blocks > 0x7fffffffLL) return DAR_E_ARG;
+    if (!dev_ok(c->k_pool) || !dev_ok(c->v_pool) || !c->block_table || !c->lens) return DAR_E_ARG;
+    if (((uintptr_t)c->block_table & 3u) || ((uintptr_t)c->lens & 3u)) return DAR_E_ARG;
+    if (s->w > 0 && (!dev_ok(c->k_win) || !dev_ok(c->v_win))) return DAR_E_ARG;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+    return DAR_OK;
+}
+
+dar_status dar_cache_append_paged(const dar_shape* s, const dar_paged_cache* c, const void* k_new,
+                                  const void* v_new, const void* w_down, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    st = check_paged(s, c);
+    if (st != DAR_OK) return st;
+    if (!dev_ok(k_new) || !dev_ok(v_new) || !dev_ok(w_down)) return DAR_E_ARG;
+    clear_hip_error();
+    const PagedArgs pg{c->lens, c->block_table, c->page_size, c->max_blocks, c->n_pages};
+    hipError_t e;
+    if (s->dtype == DAR_BF16)
+        e = launch_append_paged<bf16_t>((const bf16_t*)k_new, (const bf16_t*)v_new,
+                                        (const bf16_t*)w_down, (bf16_t*)c->k_win, (bf16_t*)c->v_win,
+                                        (bf16_t*)c->k_pool, (bf16_t*)c->v_pool, pg, c->lens, s->B,
+                                        s->Hkv, s->d, s->d_down, s->w, stream);
+    else
+        e = launch_append_paged<float>((const float*)k_new, (const float*)v_new,
+                                       (const float*)w_down, (float*)c->k_win, (float*)c->v_win,
+                                       (float*)c->k_pool, (float*)c->v_pool, pg, c->lens, s->B,
+                                       s->Hkv, s->d, s->d_down, s->w, stream);
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, const void* q,
+                                 const void* w_down, const void* w_up, void* o, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    st = check_paged(s, c);
+    if (st != DAR_OK) return st;
+    if (!dev_ok(q) || !dev_ok(w_down) || !dev_ok(o)) return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if (!decode_mfma_supported(s->d, s->d_down, s->Hq / s->Hkv, s->dtype == DAR_BF16) ||
+        !group_supported(s))
+        return DAR_E_UNSUPPORTED;
+    const int cap = c->page_size * c->max_blocks;
+    const size_t need = dar_decode_workspace_bytes(s, cap);
+    if (ws == nullptr || ws_bytes < need) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+    clear_hip_error();
+    const PagedArgs pg{c->lens, c->block_table, c->page_size, c->max_blocks, c->n_pages};
+    int P = 0;
+    hipError_t e = launch_decode_mfma_paged((const bf16_t*)q, (const bf16_t*)w_down,
+                                            (const bf16_t*)w_up, (const bf16_t*)c->k_win,
+                                            (const bf16_t*)c->v_win, (const bf16_t*)c->k_pool,
+                                            (const bf16_t*)c->v_pool, pg, (float*)ws, (bf16_t*)o,
+                                            s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, P, stream);
+    if (e == hipSuccess && P > 1)
+        e = launch_decode_combine<bf16_t>((const float*)ws, (const bf16_t*)w_down,
+                                          (const bf16_t*)w_up, (bf16_t*)o, s->B, s->Hq, s->Hkv,
+                                          s->d, s->d_down, P, stream);
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
 }  // extern "C"

@@ -33,6 +33,17 @@ static inline int prefill_tp(int T, int w) {
 }
 PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize);
 
+// Paged split cache (serving): rings [B][Hkv][w][d] per sequence; latents in
+// pages [n_pages][Hkv][ps][dd] (ps tokens of every KV head per page), token e
+// of sequence b in page bt[b * maxb + e / ps], row e % ps; lens[b] tokens per
+// sequence (device). Page indices outside [0, n_pages) are never read or
+// written (such tokens read as zeros and are not stored).
+struct PagedArgs {
+    const int* lens;
+    const int* bt;
+    int ps, maxb, n_pages;
+};
+
 // Where the rows, keys/values and latents of a prefill come from. Rows
 // r = 0..n_rows-1 are the queries at positions q0 + r (T = q0 + n_rows
 // positions in all); k and v row t holds position kv0 + t (t < Tkv); the
@@ -107,6 +118,20 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
                                    const bf16_t* v_lat, const float* tab, int n_pos, float* part,
                                    bf16_t* o, int B, int Hq, int Hkv, int dd, int w, int cap,
                                    int len, int r, int& P, hipStream_t st);
+// The same kernel over a paged cache with per-sequence lengths (bf16 shapes
+// of decode_mfma_supported); P from the largest possible length.
+hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
+                                    const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_pool,
+                                    const bf16_t* v_pool, const PagedArgs& pg, float* part,
+                                    bf16_t* o, int B, int Hq, int Hkv, int d, int dd, int w, int& P,
+                                    hipStream_t st);
+// One token per sequence into a paged cache at position lens[b]; the token
+// leaving the window is projected (as launch_append projects it) into its
+// page slot; lens[b] += 1 for every sequence below capacity.
+template <typename T>
+hipError_t launch_append_paged(const T* k_new, const T* v_new, const T* wd, T* k_win, T* v_win,
+                               T* k_pool, T* v_pool, const PagedArgs& pg, int* lens, int B, int Hkv,
+                               int d, int dd, int w, hipStream_t st);
 template <typename T>
 hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, const T* v_win,
                          const T* k_lat, const T* v_lat, T* o, float* part, int B, int Hq, int Hkv,

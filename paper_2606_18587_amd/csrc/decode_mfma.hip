@@ -300,13 +300,16 @@ struct DecStages {
 // order is matched by a permuted query operand). Values are not rotated:
 // the distant ones stay in d_down space and are lifted once, as without
 // rotation. tab: [n_pos][R] (cos of the R/2 angles, then their sin).
-template <int D, int DD, int NW, int R = 0>
+// PAGED: the latents come from the pages of a paged cache and the cache
+// length of each sequence from pg.lens; each 32-token subtile lies inside one
+// page (ps is a multiple of 32), whose descriptor is built per subtile.
+template <int D, int DD, int NW, int R = 0, bool PAGED = false>
 __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
     const bf16_t* __restrict__ k_win, const bf16_t* __restrict__ v_win,
     const bf16_t* __restrict__ k_lat, const bf16_t* __restrict__ v_lat, float* __restrict__ part,
-    bf16_t* __restrict__ o, int Hq, int Hkv, int w, int cap, int len, int P, float qscale,
-    const float* __restrict__ tab, int n_pos, const bf16_t* __restrict__ wv) {
+    bf16_t* __restrict__ o, int Hq, int Hkv, int w, int cap, int len_arg, int P, float qscale,
+    const float* __restrict__ tab, int n_pos, const bf16_t* __restrict__ wv, PagedArgs pg) {
     static_assert(R == 0 || (D == 64 && R % 16 == 0 && R <= D), "rotary: d = 64, R a multiple of 16");
     constexpr int KS = D / 16, DS = DD / 16, NT = D / 32;
     constexpr int LDW = D + 8;                      // padded ring row in LDS (bf16)
@@ -322,6 +325,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const int s = wg_id_x();  // part of this (batch, KV head), < P
     const int bg = wg_id_y();
     const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
+    const int len = PAGED ? pg.lens[b] : len_arg;  // tokens in this sequence's cache
     const int G = Hq / Hkv;
     const int tid = lane_id_x();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -422,13 +426,34 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         // A operand of the rank-1 reference product: 1 at contraction slot 0
         const dbf16x8 ones_a = __builtin_bit_cast(dbf16x8, make_uint4(hg == 0 ? 0x3f80u : 0u, 0u, 0u, 0u));
         auto load = [&](int t0, dbf16x8 (&ak)[DS], uint4 (&vv)[DS]) {
-            const int o = (t0 - t_begin) * DD * 2;
+            if constexpr (PAGED) {
+                // this subtile's page: rows past the run (or of an unmapped
+                // page) are outside the descriptor's size and read as zeros
+                const int blk = imin(t0 / pg.ps, pg.maxb - 1);
+                const int page = pg.bt[(size_t)b * pg.maxb + blk];
+                const int pstart = blk * pg.ps;
+                const bool ok = t0 < t_end && page >= 0 && page < pg.n_pages;
+                const int nrow = ok ? imin(pg.ps, t_end - pstart) : 0;
+                const size_t poff = ((size_t)(ok ? page : 0) * Hkv + g) * pg.ps * DD;
+                const int nb = __builtin_amdgcn_readfirstlane(nrow * DD * 2);
+                const __amdgpu_buffer_rsrc_t rkp = __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(k_lat + poff), (short)0, nb, kBufWord3);
+                const __amdgpu_buffer_rsrc_t rvp = __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(v_lat + poff), (short)0, nb, kBufWord3);
+                const int r0 = t0 - pstart;
 #pragma unroll
-            for (int k = 0; k < DS; ++k)
-                ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + o + k * 32, 0, kStream));
+                for (int k = 0; k < DS; ++k)
+                    ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rkp, (r0 + prow) * DD * 2 + hg * 16 + k * 32, 0, kStream));
 #pragma unroll
-            for (int k = 0; k < DS; ++k)
-                vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + o + k * 1024, 0, kStream));
+                for (int k = 0; k < DS; ++k)
+                    vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rvp, r0 * DD * 2 + lane * 16 + k * 1024, 0, kStream));
+            } else {
+                const int o = (t0 - t_begin) * DD * 2;
+#pragma unroll
+                for (int k = 0; k < DS; ++k)
+                    ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + o + k * 32, 0, kStream));
+#pragma unroll
+                for (int k = 0; k < DS; ++k)
+                    vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + o + k * 1024, 0, kStream));
+            }
         };
         static_assert(kSubBytes == 1024 * DS, "one V chunk of 16 bytes per lane per 16 latent columns");
         // NST subtiles in flight per wavefront (the stream is latency bound:
@@ -784,7 +809,7 @@ hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* w
 #define DAR_DEC_LAUNCH(D_, DD_)                                                                     \
     hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value>), grid,                    \
                        dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
-                       part, o, Hq, Hkv, w, cap, len, P, qscale, (const float*)nullptr, 0, wv)
+                       part, o, Hq, Hkv, w, cap, len, P, qscale, (const float*)nullptr, 0, wv, PagedArgs{})
     if (d == 64 && dd == 16) DAR_DEC_LAUNCH(64, 16);
     else if (d == 64 && dd == 32) DAR_DEC_LAUNCH(64, 32);
     else if (d == 128 && dd == 16) DAR_DEC_LAUNCH(128, 16);
@@ -809,7 +834,7 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
 #define DAR_DEC_ROPE(DD_, R_)                                                                        \
     hipLaunchKernelGGL((decode_mfma_kernel<64, DD_, DecWaves<64>::value, R_>), grid,                 \
                        dim3(64 * DecWaves<64>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
-                       part, o, Hq, Hkv, w, cap, len, P, qscale, tab, n_pos, (const bf16_t*)nullptr)
+                       part, o, Hq, Hkv, w, cap, len, P, qscale, tab, n_pos, (const bf16_t*)nullptr, PagedArgs{})
     if (dd == 16) {
         if (r == 16) DAR_DEC_ROPE(16, 16);
         else if (r == 32) DAR_DEC_ROPE(16, 32);
@@ -820,6 +845,28 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
         else DAR_DEC_ROPE(32, 64);
     }
 #undef DAR_DEC_ROPE
+    return hipGetLastError();
+}
+
+hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
+                                    const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_pool,
+                                    const bf16_t* v_pool, const PagedArgs& pg, float* part,
+                                    bf16_t* o, int B, int Hq, int Hkv, int d, int dd, int w, int& P,
+                                    hipStream_t st) {
+    const int cap = pg.maxb * pg.ps;
+    P = decode_mfma_parts(B, Hkv, cap, w, d);
+    const float qscale = 1.4426950408889634f / sqrtf((float)d);
+    dim3 grid(P, B * Hkv);
+#define DAR_DEC_PAGED(D_, DD_)                                                                       \
+    hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value, 0, true>), grid,            \
+                       dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_pool, v_pool, \
+                       part, o, Hq, Hkv, w, cap, 0, P, qscale, (const float*)nullptr, 0,              \
+                       (const bf16_t*)nullptr, pg)
+    if (d == 64 && dd == 16) DAR_DEC_PAGED(64, 16);
+    else if (d == 64 && dd == 32) DAR_DEC_PAGED(64, 32);
+    else if (d == 128 && dd == 16) DAR_DEC_PAGED(128, 16);
+    else DAR_DEC_PAGED(128, 32);
+#undef DAR_DEC_PAGED
     return hipGetLastError();
 }
 

@@ -657,3 +657,123 @@ template hipError_t launch_append_shared<bf16_t>(const bf16_t*, const bf16_t*, c
                                                  int, int, int, hipStream_t);
 
 }  // namespace dar
+
+namespace dar {
+
+// Paged append, one token per sequence (grid B*Hkv, one wavefront each): the
+// new token of sequence b sits at position len = lens[b]; the token leaving
+// the window, ex = len - w (the new token itself when w = 0), is projected
+// into its page slot with the same instruction sequence as the dense append
+// (matrix cores: token in column 0), then the new token goes to ring slot
+// len % w (after the read of the same slot). A sequence at capacity, or whose
+// page is not mapped, stores nothing.
+template <int D>
+__global__ __launch_bounds__(64) void append_paged_mfma_kernel(
+    const bf16_t* __restrict__ k_new, const bf16_t* __restrict__ v_new, const bf16_t* __restrict__ wd,
+    bf16_t* k_win, bf16_t* v_win, bf16_t* __restrict__ k_pool, bf16_t* __restrict__ v_pool,
+    PagedArgs pg, int Hkv, int dd, int w) {
+    constexpr int KS = D / 16;
+    const int bg = wg_id_x();
+    const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
+    const int lane = lane_id_x();
+    const int tl = lane & 31, hg = lane >> 5;
+    const int len = pg.lens[b];
+    if (len >= pg.maxb * pg.ps) return;
+    const int ex = len - w;
+    int page = -1;
+    if (ex >= 0) page = pg.bt[(size_t)b * pg.maxb + ex / pg.ps];
+    const bool project = ex >= 0 && page >= 0 && page < pg.n_pages;
+    lbf16x8 wa[KS];
+    load_wd_operand<D>(wd + (size_t)g * D * dd, dd, lane, wa);
+    for (int which = 0; which < 2; ++which) {
+        const bf16_t* src_new = (which ? v_new : k_new) + (size_t)bg * D;
+        bf16_t* ring = (which ? v_win : k_win) + (size_t)bg * w * D;
+        const bf16_t* row = w > 0 ? ring + (size_t)(imax(ex, 0) % w) * D : src_new;
+        lbf16x8 x[KS];
+#pragma unroll
+        for (int s = 0; s < KS; ++s)
+            x[s] = (project && tl == 0) ? lload8(row + s * 16 + hg * 8)
+                                        : __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
+        const lf32x16 acc = project_mfma<D>(wa, x);
+        if (project && tl == 0) {
+            bf16_t* out = (which ? v_pool : k_pool) + (((size_t)page * Hkv + g) * pg.ps + ex % pg.ps) * dd;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int c = acc_col(r, hg);
+                if (c < dd) out[c] = f32_to_bf16(acc[r]);
+            }
+        }
+        if (w > 0 && tl == 0) {
+            bf16_t* dst = ring + (size_t)(len % w) * D;
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                *reinterpret_cast<uint4*>(dst + s * 16 + hg * 8) = *reinterpret_cast<const uint4*>(src_new + s * 16 + hg * 8);
+        }
+    }
+}
+
+// The same for every dtype and head size, on the vector ALUs (project_col:
+// the dense append's arithmetic). One workgroup of 64 per (batch, KV head).
+template <typename T>
+__global__ __launch_bounds__(64) void append_paged_kernel(
+    const T* __restrict__ k_new, const T* __restrict__ v_new, const T* __restrict__ wd, T* k_win,
+    T* v_win, T* __restrict__ k_pool, T* __restrict__ v_pool, PagedArgs pg, int Hkv, int d, int dd,
+    int w) {
+    const int bg = wg_id_x();
+    const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
+    const int lane = lane_id_x();
+    const int len = pg.lens[b];
+    if (len >= pg.maxb * pg.ps) return;
+    const int ex = len - w;
+    int page = -1;
+    if (ex >= 0) page = pg.bt[(size_t)b * pg.maxb + ex / pg.ps];
+    const bool project = ex >= 0 && page >= 0 && page < pg.n_pages;
+    const T* wdg = wd + (size_t)g * d * dd;
+    for (int which = 0; which < 2; ++which) {
+        const T* src_new = (which ? v_new : k_new) + (size_t)bg * d;
+        T* ring = (which ? v_win : k_win) + (size_t)bg * w * d;
+        const T* row = w > 0 ? ring + (size_t)(imax(ex, 0) % w) * d : src_new;
+        if (project) {
+            T* out = (which ? v_pool : k_pool) + (((size_t)page * Hkv + g) * pg.ps + ex % pg.ps) * dd;
+            for (int c = lane; c < dd; c += 64) out[c] = elem<T>::from_f32(project_col<T>(row, wdg, d, dd, c));
+        }
+        __syncthreads();  // every read of the ring slot before it is overwritten
+        if (w > 0)
+            for (int e = lane; e < d; e += 64) ring[(size_t)(len % w) * d + e] = src_new[e];
+    }
+}
+
+__global__ __launch_bounds__(64) void lens_advance_kernel(int* __restrict__ lens, int B, int cap) {
+    const int b = wg_id_x() * 64 + lane_id_x();
+    if (b < B && lens[b] < cap) lens[b] += 1;
+}
+
+template <typename T>
+hipError_t launch_append_paged(const T* k_new, const T* v_new, const T* wd, T* k_win, T* v_win,
+                               T* k_pool, T* v_pool, const PagedArgs& pg, int* lens, int B, int Hkv,
+                               int d, int dd, int w, hipStream_t st) {
+    if (sizeof(T) == 2 && mfma_projection(d, dd)) {
+        auto kern = d == 64 ? append_paged_mfma_kernel<64> : append_paged_mfma_kernel<128>;
+        hipLaunchKernelGGL(kern, dim3(B * Hkv), dim3(64), 0, st, (const bf16_t*)k_new,
+                           (const bf16_t*)v_new, (const bf16_t*)wd, (bf16_t*)k_win, (bf16_t*)v_win,
+                           (bf16_t*)k_pool, (bf16_t*)v_pool, pg, Hkv, dd, w);
+    } else {
+        hipLaunchKernelGGL(append_paged_kernel<T>, dim3(B * Hkv), dim3(64), 0, st, k_new, v_new, wd,
+                           k_win, v_win, k_pool, v_pool, pg, Hkv, d, dd, w);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    // after every workgroup above has read lens (stream order)
+    hipLaunchKernelGGL(lens_advance_kernel, dim3((B + 63) / 64), dim3(64), 0, st, lens, B,
+                       pg.maxb * pg.ps);
+    return hipGetLastError();
+}
+
+template hipError_t launch_append_paged<float>(const float*, const float*, const float*, float*,
+                                               float*, float*, float*, const PagedArgs&, int*, int,
+                                               int, int, int, int, hipStream_t);
+template hipError_t launch_append_paged<bf16_t>(const bf16_t*, const bf16_t*, const bf16_t*,
+                                                bf16_t*, bf16_t*, bf16_t*, bf16_t*, const PagedArgs&,
+                                                int*, int, int, int, int, int, hipStream_t);
+
+}  // namespace dar

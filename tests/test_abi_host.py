@@ -35,7 +35,8 @@ def test_exports_every_declared_symbol():
                           "dar_attn_prefill_chunk", "dar_prefill_chunk_workspace_bytes",
                           "dar_rope_table", "dar_attn_prefill_rope", "dar_attn_decode_rope",
                           "dar_attn_prefill_shared", "dar_cache_append_shared",
-                          "dar_attn_decode_shared",
+                          "dar_attn_decode_shared", "dar_cache_append_paged",
+                          "dar_attn_decode_paged",
                           "dar_prefill_rope_workspace_bytes", "dar_status_string"}
     raw = ctypes.CDLL(dar.LIB_PATH)
     for n in names:
@@ -364,3 +365,30 @@ def test_shared_latent_rejects_before_any_launch():
     assert dc(cache_struct(cap=64, length=0)) == dar.DAR_E_ARG
     assert dc(cache_struct(cap=64, length=10), uk=None) == dar.DAR_E_ARG
     assert dc(cache_struct(cap=64, length=10), ws_bytes=8) == dar.DAR_E_WORKSPACE
+
+
+@no_gpu
+def test_paged_rejects_before_any_launch():
+    s = S()
+    def pc(ps=64, maxb=4, n_pages=8, pool=FAKE, bt=FAKE, lens=FAKE, win=FAKE):
+        return dar.DarPagedCacheStruct(win.value if win else None, win.value if win else None,
+                                       pool.value if pool else None, FAKE.value,
+                                       bt.value if bt else None, lens.value if lens else None,
+                                       ps, maxb, n_pages)
+    ap = lambda c, k=FAKE: dar.lib.dar_cache_append_paged(ctypes.byref(s), ctypes.byref(c), k, FAKE,
+                                                          FAKE, None)
+    dc = lambda c, ws_bytes=1 << 30, shape=s: dar.lib.dar_attn_decode_paged(
+        ctypes.byref(shape), ctypes.byref(c), FAKE, FAKE, None, FAKE, FAKE, ws_bytes, None)
+    assert ap(pc(ps=48)) == dar.DAR_E_ARG          # page size not a multiple of 32
+    assert ap(pc(ps=0)) == dar.DAR_E_ARG
+    assert ap(pc(maxb=0)) == dar.DAR_E_ARG
+    assert ap(pc(n_pages=0)) == dar.DAR_E_ARG
+    assert ap(pc(pool=None)) == dar.DAR_E_ARG
+    assert ap(pc(bt=None)) == dar.DAR_E_ARG
+    assert ap(pc(lens=None)) == dar.DAR_E_ARG
+    assert ap(pc(lens=ctypes.c_void_p((1 << 20) + 2))) == dar.DAR_E_ARG   # int array misaligned
+    assert ap(pc(win=None)) == dar.DAR_E_ARG       # a ring is required when w > 0
+    assert ap(pc(), k=MISALIGNED) == dar.DAR_E_ARG
+    assert dc(pc(), ws_bytes=8) == dar.DAR_E_WORKSPACE
+    assert dc(pc(), shape=S(dtype=torch.float32)) == dar.DAR_E_UNSUPPORTED   # matrix-core shapes only
+    assert dc(pc(), shape=S(d=80, dd=16)) == dar.DAR_E_UNSUPPORTED
