@@ -22,8 +22,10 @@ and the decode with the rotary embedding inside Eq. 3 (prefill: rotary
 dimension 16 of 64, base 10000, as in the Pythia models; decode: full
 rotation), the prefill and the decode with a single shared latent per token
 (the same batches, with seeded N(0,1) latents and N(0, 1/d_down) U_K, U_V:
-the decode streams one latent array instead of two), the chunked prefill and
-the other prefill workloads.
+the decode streams one latent array instead of two), the decode over a
+paged cache (256-token pages in shuffled order; every sequence at the decode
+length, then lengths spread from 1K to 32K tokens: a ragged batch), the
+chunked prefill and the other prefill workloads.
 
 Prints ONE JSON line (rank 0). Only one GPU is used: --gpus above 1 exits.
 """
@@ -161,6 +163,8 @@ def main():
                     help="skip the prefill workloads reported beside the main one")
     ap.add_argument("--no-rope", action="store_true",
                     help="skip the prefill and decode with the rotary embedding")
+    ap.add_argument("--no-paged", action="store_true",
+                    help="skip the decode over a paged cache")
     ap.add_argument("--no-shared", action="store_true",
                     help="skip the prefill and decode with a single shared latent")
     ap.add_argument("--no-cold", action="store_true",
@@ -311,6 +315,45 @@ def main():
         shared["decode_len"] = scache.len
         del scache
 
+    # paged cache: the decode cache's contents copied into 256-token pages
+    # handed out in a seeded random order; then the same pages with ragged
+    # lengths (the sequences' first tokens only)
+    paged = {}
+    if not args.no_paged:
+        PS = 256
+        L = cache.len
+        nblk = (L + 1 + PS - 1) // PS
+        n_pages = dw.B * nblk
+        pcache = dar.DarPagedCache(dw.B, dw.Hkv, dw.d, dw.dd, dw.w, PS, nblk, n_pages,
+                                   torch.bfloat16, device=dev)
+        perm = torch.randperm(n_pages, generator=torch.Generator().manual_seed(260618590))
+        bt = perm.view(dw.B, nblk).to(torch.int32)
+        pcache.block_table.copy_(bt)
+        pcache.k_win.copy_(cache.k_win)
+        pcache.v_win.copy_(cache.v_win)
+        n_lat = L - dw.w
+        for blk in range(nblk):
+            e0, e1 = blk * PS, min((blk + 1) * PS, n_lat)
+            if e1 <= e0:
+                break
+            pages = bt[:, blk].long().to(dev)
+            pcache.k_pool[pages, :, : e1 - e0] = cache.k_lat[:, :, e0:e1]
+            pcache.v_pool[pages, :, : e1 - e0] = cache.v_lat[:, :, e0:e1]
+        pcache.lens.fill_(L)
+        run_pd = lambda i: dar.dar_attn_decode_paged(pcache, qd_last, dwd, o=dout, ws=dws)
+        for i in range(args.warmup):
+            run_pd(i)
+        paged["uniform_ms"] = timed(run_pd, args.steps)
+        paged["uniform_len"] = L
+        lens_r = torch.linspace(1024, L, dw.B).round().to(torch.int32)
+        lens_r = lens_r[torch.randperm(dw.B, generator=torch.Generator().manual_seed(260618591))]
+        pcache.lens.copy_(lens_r)
+        for i in range(args.warmup):
+            run_pd(i)
+        paged["ragged_ms"] = timed(run_pd, args.steps)
+        paged["ragged_lens"] = [int(x) for x in lens_r.tolist()]
+        del pcache
+
     # the rotary embedding inside Eq. 3: the same prefill batch (un-rotated
     # queries and keys) and the same decode cache
     rope = {}
@@ -458,6 +501,21 @@ def main():
         du = float(cold["decode_ms"] * 1e3)
         result["decode"]["cold_us"] = round(du, 2)
         result["decode"]["cold_gbs"] = round(dbytes / (du * 1e-6) / 1e9, 1)
+    if paged:
+        pu = float(paged["uniform_ms"] * 1e3)
+        pb = decode_bytes(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, paged["uniform_len"])
+        rlu = float(paged["ragged_ms"] * 1e3)
+        rb = sum(decode_bytes(1, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, n) for n in paged["ragged_lens"])
+        result["decode_paged"] = {
+            "shape": "decode1b batch, 256-token pages, every sequence at %d tokens"
+                     % paged["uniform_len"],
+            "us": round(pu, 2), "alg_bytes": pb, "gbs": round(pb / (pu * 1e-6) / 1e9, 1),
+            "frac_hbm_peak": round(pb / (pu * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        result["decode_ragged"] = {
+            "shape": "decode1b batch, 256-token pages, lengths %d..%d (ragged)"
+                     % (min(paged["ragged_lens"]), max(paged["ragged_lens"])),
+            "us": round(rlu, 2), "alg_bytes": rb, "gbs": round(rb / (rlu * 1e-6) / 1e9, 1),
+            "frac_hbm_peak": round(rb / (rlu * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     if shared:
         su = float(shared["prefill_ms"] * 1e3)
         result["prefill_shared"] = {

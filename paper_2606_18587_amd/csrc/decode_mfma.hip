@@ -425,12 +425,19 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         constexpr int kSubBytes = 32 * DD * 2;
         // A operand of the rank-1 reference product: 1 at contraction slot 0
         const dbf16x8 ones_a = __builtin_bit_cast(dbf16x8, make_uint4(hg == 0 ? 0x3f80u : 0u, 0u, 0u, 0u));
+        // paged: lane i holds the page of block blk0 + i of this run (read once;
+        // a subtile then takes its page from a lane instead of from memory)
+        const int blk0 = PAGED ? t_begin / pg.ps : 0;
+        int pagev = 0;
+        if constexpr (PAGED) pagev = pg.bt[(size_t)b * pg.maxb + imin(blk0 + lane, pg.maxb - 1)];
         auto load = [&](int t0, dbf16x8 (&ak)[DS], uint4 (&vv)[DS]) {
             if constexpr (PAGED) {
                 // this subtile's page: rows past the run (or of an unmapped
                 // page) are outside the descriptor's size and read as zeros
                 const int blk = imin(t0 / pg.ps, pg.maxb - 1);
-                const int page = pg.bt[(size_t)b * pg.maxb + blk];
+                const int rel = blk - blk0;
+                const int page = rel < 64 ? __builtin_amdgcn_readlane(pagev, rel)
+                                          : pg.bt[(size_t)b * pg.maxb + blk];
                 const int pstart = blk * pg.ps;
                 const bool ok = t0 < t_end && page >= 0 && page < pg.n_pages;
                 const int nrow = ok ? imin(pg.ps, t_end - pstart) : 0;
