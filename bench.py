@@ -60,13 +60,13 @@ CSRC = os.path.join(ROOT, "paper_2606_18587_amd", "csrc")
 MEASURED_TRAFFIC = {
     "prefill": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "latent.hip",
                           "prefill_mfma.hip"],
-                "sha256_16": "496d0f0d231a78c4", "bytes": 133232730},
+                "sha256_16": "e28479b4c4e44586", "bytes": 132674892},
     "decode": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "decode.hip",
                          "decode_mfma.hip"],
-               "sha256_16": "fbe8dff6aaceaf56", "bytes": 574064716},
+               "sha256_16": "92e318e4d2b1a58b", "bytes": 574067915},
     "backward": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "mfma_common.hpp",
                            "backward.hip", "backward_mfma.hip"],
-                 "sha256_16": "20943a1f92990983", "bytes": 500968430},
+                 "sha256_16": "9dc7ebc5630c6fb7", "bytes": 500446639},
 }
 
 
