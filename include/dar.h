@@ -97,8 +97,8 @@ typedef struct {
  *                 such tokens are not stored and read as zeros)
  *   lens          device int [B], tokens held per sequence (the append
  *                 advances it on the device; the host never reads it)
- *   page_size     a multiple of 32; capacity max_blocks * page_size tokens
- *                 per sequence */
+ *   page_size     a power of two, at least 32; capacity max_blocks *
+ *                 page_size tokens per sequence */
 typedef struct {
     void *k_win, *v_win, *k_pool, *v_pool;
     const int* block_table;

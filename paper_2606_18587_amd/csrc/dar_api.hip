@@ -642,7 +642,8 @@ dar_status dar_attn_decode_shared(const dar_shape* s, const dar_cache* cache, co
 }
 
 static dar_status check_paged(const dar_shape* s, const dar_paged_cache* c) {
-    if (!c || c->page_size < 32 || c->page_size % 32 != 0 || c->max_blocks < 1 || c->n_pages < 1)
+    if (!c || c->page_size < 32 || (c->page_size & (c->page_size - 1)) || c->max_blocks < 1 ||
+        c->n_pages < 1)
         return DAR_E_ARG;
     if ((long long)c->page_size * c->max_blocks > 0x7fffffffLL) return DAR_E_ARG;
     if (!dev_ok(c->k_pool) || !dev_ok(c->v_pool) || !c->block_table || !c->lens) return DAR_E_ARG;
@@ -660,7 +661,8 @@ dar_status dar_cache_append_paged(const dar_shape* s, const dar_paged_cache* c, 
     if (st != DAR_OK) return st;
     if (!dev_ok(k_new) || !dev_ok(v_new) || !dev_ok(w_down)) return DAR_E_ARG;
     clear_hip_error();
-    const PagedArgs pg{c->lens, c->block_table, c->page_size, c->max_blocks, c->n_pages};
+    const PagedArgs pg{c->lens, c->block_table, c->page_size, c->max_blocks, c->n_pages,
+                       __builtin_ctz((unsigned)c->page_size)};
     hipError_t e;
     if (s->dtype == DAR_BF16)
         e = launch_append_paged<bf16_t>((const bf16_t*)k_new, (const bf16_t*)v_new,
@@ -692,7 +694,8 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
     if (ws == nullptr || ws_bytes < need) return DAR_E_WORKSPACE;
     if (!aligned16(ws)) return DAR_E_ARG;
     clear_hip_error();
-    const PagedArgs pg{c->lens, c->block_table, c->page_size, c->max_blocks, c->n_pages};
+    const PagedArgs pg{c->lens, c->block_table, c->page_size, c->max_blocks, c->n_pages,
+                       __builtin_ctz((unsigned)c->page_size)};
     int P = 0;
     hipError_t e = launch_decode_mfma_paged((const bf16_t*)q, (const bf16_t*)w_down,
                                             (const bf16_t*)w_up, (const bf16_t*)c->k_win,

@@ -42,6 +42,7 @@ struct PagedArgs {
     const int* lens;
     const int* bt;
     int ps, maxb, n_pages;
+    int ps_shift;  // log2(ps): page sizes are powers of two
 };
 
 // Where the rows, keys/values and latents of a prefill come from. Rows

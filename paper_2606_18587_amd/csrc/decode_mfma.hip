@@ -309,7 +309,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const bf16_t* __restrict__ k_win, const bf16_t* __restrict__ v_win,
     const bf16_t* __restrict__ k_lat, const bf16_t* __restrict__ v_lat, float* __restrict__ part,
     bf16_t* __restrict__ o, int Hq, int Hkv, int w, int cap, int len_arg, int P, float qscale,
-    const float* __restrict__ tab, int n_pos, const bf16_t* __restrict__ wv, PagedArgs pg) {
+    const float* __restrict__ tab, int n_pos, const bf16_t* __restrict__ wv, PagedArgs pg,
+    const int* __restrict__ block_table) {
     static_assert(R == 0 || (D == 64 && R % 16 == 0 && R <= D), "rotary: d = 64, R a multiple of 16");
     constexpr int KS = D / 16, DS = DD / 16, NT = D / 32;
     constexpr int LDW = D + 8;                      // padded ring row in LDS (bf16)
@@ -425,19 +426,16 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         constexpr int kSubBytes = 32 * DD * 2;
         // A operand of the rank-1 reference product: 1 at contraction slot 0
         const dbf16x8 ones_a = __builtin_bit_cast(dbf16x8, make_uint4(hg == 0 ? 0x3f80u : 0u, 0u, 0u, 0u));
-        // paged: lane i holds the page of block blk0 + i of this run (read once;
-        // a subtile then takes its page from a lane instead of from memory)
-        const int blk0 = PAGED ? t_begin / pg.ps : 0;
-        int pagev = 0;
-        if constexpr (PAGED) pagev = pg.bt[(size_t)b * pg.maxb + imin(blk0 + lane, pg.maxb - 1)];
+        // paged: this sequence's row of the block table (the index of a
+        // subtile's block is wave-uniform: a scalar load, kept apart from the
+        // vector loads in flight)
+        const int* btb = PAGED ? block_table + (size_t)b * pg.maxb : nullptr;
         auto load = [&](int t0, dbf16x8 (&ak)[DS], uint4 (&vv)[DS]) {
             if constexpr (PAGED) {
                 // this subtile's page: rows past the run (or of an unmapped
                 // page) are outside the descriptor's size and read as zeros
-                const int blk = imin(t0 / pg.ps, pg.maxb - 1);
-                const int rel = blk - blk0;
-                const int page = rel < 64 ? __builtin_amdgcn_readlane(pagev, rel)
-                                          : pg.bt[(size_t)b * pg.maxb + blk];
+                const int blk = imin(t0 >> pg.ps_shift, pg.maxb - 1);
+                const int page = btb[blk];
                 const int pstart = blk * pg.ps;
                 const bool ok = t0 < t_end && page >= 0 && page < pg.n_pages;
                 const int nrow = ok ? imin(pg.ps, t_end - pstart) : 0;
@@ -816,7 +814,8 @@ hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* w
 #define DAR_DEC_LAUNCH(D_, DD_)                                                                     \
     hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value>), grid,                    \
                        dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
-                       part, o, Hq, Hkv, w, cap, len, P, qscale, (const float*)nullptr, 0, wv, PagedArgs{})
+                       part, o, Hq, Hkv, w, cap, len, P, qscale, (const float*)nullptr, 0, wv, PagedArgs{}, \
+                       (const int*)nullptr)
     if (d == 64 && dd == 16) DAR_DEC_LAUNCH(64, 16);
     else if (d == 64 && dd == 32) DAR_DEC_LAUNCH(64, 32);
     else if (d == 128 && dd == 16) DAR_DEC_LAUNCH(128, 16);
@@ -841,7 +840,8 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
 #define DAR_DEC_ROPE(DD_, R_)                                                                        \
     hipLaunchKernelGGL((decode_mfma_kernel<64, DD_, DecWaves<64>::value, R_>), grid,                 \
                        dim3(64 * DecWaves<64>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
-                       part, o, Hq, Hkv, w, cap, len, P, qscale, tab, n_pos, (const bf16_t*)nullptr, PagedArgs{})
+                       part, o, Hq, Hkv, w, cap, len, P, qscale, tab, n_pos, (const bf16_t*)nullptr, PagedArgs{}, \
+                       (const int*)nullptr)
     if (dd == 16) {
         if (r == 16) DAR_DEC_ROPE(16, 16);
         else if (r == 32) DAR_DEC_ROPE(16, 32);
@@ -868,7 +868,7 @@ hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf1
     hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value, 0, true>), grid,            \
                        dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_pool, v_pool, \
                        part, o, Hq, Hkv, w, cap, 0, P, qscale, (const float*)nullptr, 0,              \
-                       (const bf16_t*)nullptr, pg)
+                       (const bf16_t*)nullptr, pg, pg.bt)
     if (d == 64 && dd == 16) DAR_DEC_PAGED(64, 16);
     else if (d == 64 && dd == 32) DAR_DEC_PAGED(64, 32);
     else if (d == 128 && dd == 16) DAR_DEC_PAGED(128, 16);

@@ -379,7 +379,8 @@ def test_paged_rejects_before_any_launch():
                                                           FAKE, None)
     dc = lambda c, ws_bytes=1 << 30, shape=s: dar.lib.dar_attn_decode_paged(
         ctypes.byref(shape), ctypes.byref(c), FAKE, FAKE, None, FAKE, FAKE, ws_bytes, None)
-    assert ap(pc(ps=48)) == dar.DAR_E_ARG          # page size not a multiple of 32
+    assert ap(pc(ps=48)) == dar.DAR_E_ARG          # page size not a power of two
+    assert ap(pc(ps=96)) == dar.DAR_E_ARG
     assert ap(pc(ps=0)) == dar.DAR_E_ARG
     assert ap(pc(maxb=0)) == dar.DAR_E_ARG
     assert ap(pc(n_pages=0)) == dar.DAR_E_ARG
