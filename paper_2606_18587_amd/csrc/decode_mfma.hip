@@ -281,6 +281,8 @@ struct DecWaves {
     static constexpr int value = 8;
 };
 // Latent subtiles in flight per wavefront (register budget of 2 waves/SIMD).
+// (A shared latent array would have room for more subtiles in flight, its
+// key operand coming from LDS; 20 instead of 12 measured slower.)
 template <int D, int DD, int R = 0>
 struct DecStages {
     static constexpr int value = R > 0 ? (DD <= 16 ? 6 : 4)
@@ -303,7 +305,10 @@ struct DecStages {
 // PAGED: the latents come from the pages of a paged cache and the cache
 // length of each sequence from pg.lens; each 32-token subtile lies inside one
 // page (ps is a multiple of 32), whose descriptor is built per subtile.
-template <int D, int DD, int NW, int R = 0, bool PAGED = false>
+// SHARED: one latent array for keys and values (v_lat == k_lat): each
+// latent subtile is loaded once, in the value chunks' order, into one of two
+// LDS buffers of the wavefront; the key operand rows are read back from there.
+template <int D, int DD, int NW, int R = 0, bool PAGED = false, bool SHARED = false>
 __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
     const bf16_t* __restrict__ k_win, const bf16_t* __restrict__ v_win,
@@ -452,9 +457,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
                     vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rvp, r0 * DD * 2 + lane * 16 + k * 1024, 0, kStream));
             } else {
                 const int o = (t0 - t_begin) * DD * 2;
+                if constexpr (!SHARED) {
 #pragma unroll
-                for (int k = 0; k < DS; ++k)
-                    ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + o + k * 32, 0, kStream));
+                    for (int k = 0; k < DS; ++k)
+                        ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + o + k * 32, 0, kStream));
+                }
 #pragma unroll
                 for (int k = 0; k < DS; ++k)
                     vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + o + k * 1024, 0, kStream));
@@ -539,8 +546,20 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
 
         // Software pipelined: the scores of subtile n+1 are on the matrix
         // cores while the exponentials of subtile n run.
-        auto scores = [&](int t0, const dbf16x8 (&ak)[DS]) {
+        auto scores = [&](int t0, const dbf16x8 (&ak_in)[DS], const uint4 (&vv)[DS]) {
             df32x16 x;
+            dbf16x8 ak[DS];
+            if constexpr (SHARED) {
+                // the subtile into its LDS buffer, the key rows back out
+                bf16_t* vbs = vb + (((t0 - t_begin) >> 5) & 1) * 32 * DD;
+#pragma unroll
+                for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vbs + (lane + 64 * k) * 8) = vv[k];
+#pragma unroll
+                for (int k = 0; k < DS; ++k) ak[k] = ld8(vbs + prow * DD + k * 16 + hg * 8);
+            } else {
+#pragma unroll
+                for (int k = 0; k < DS; ++k) ak[k] = ak_in[k];
+            }
             if constexpr (R == 0) {
                 x = mma(ak[0], qtop[0], mma(ones_a, st.negm, fill16(0.f)));
 #pragma unroll
@@ -590,9 +609,13 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             }
             return x;
         };
-        auto finish = [&](df32x16& x, const uint4 (&vv)[DS], df32x16* xnext) {
+        auto finish = [&](int t0, df32x16& x, const uint4 (&vv)[DS], df32x16* xnext) {
+            // shared: this subtile is already in its LDS buffer (scores put it there)
+            bf16_t* vbs = SHARED ? vb + (((t0 - t_begin) >> 5) & 1) * 32 * DD : vb;
+            if constexpr (!SHARED) {
 #pragma unroll
-            for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vb + (lane + 64 * k) * 8) = vv[k];
+                for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vb + (lane + 64 * k) * 8) = vv[k];
+            }
             dbf16x8 p0, p1;
             dstep<1, DD != 16>(x, st, acc, p0, p1, hg, xnext);
             // V^T operand: rows c = lane%32 of the DD-wide tile
@@ -606,8 +629,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
                     plo = vb + VBUF;
                     phi = vb + VBUF;
                 } else {
-                    plo = vb + key * DD + c;
-                    phi = vb + (key + 4) * DD + c;
+                    plo = vbs + key * DD + c;
+                    phi = vbs + (key + 4) * DD + c;
                 }
                 const ds16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_ds16x4*)plo);
                 const ds16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_ds16x4*)phi);
@@ -617,13 +640,13 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             }
         };
         int t0 = t_begin;
-        df32x16 x = scores(t_begin, aks[0]);
+        df32x16 x = scores(t_begin, aks[0], vs[0]);
         for (; t0 + 32 * (NST - 1) < t_end; t0 += 32 * NST) {
 #pragma unroll
             for (int j = 0; j < NST; ++j) {
                 const int tj = t0 + 32 * j;
-                df32x16 xn = scores(tj + 32, aks[(j + 1) % NST]);
-                finish(x, vs[j], &xn);
+                df32x16 xn = scores(tj + 32, aks[(j + 1) % NST], vs[(j + 1) % NST]);
+                finish(tj, x, vs[j], &xn);
                 load(tj + 32 * NST, aks[j], vs[j]);
                 x = xn;
             }
@@ -633,11 +656,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             const int tj = t0 + 32 * j;
             if (tj < t_end) {
                 if (tj + 32 < t_end) {
-                    df32x16 xn = scores(tj + 32, aks[j + 1]);
-                    finish(x, vs[j], &xn);
+                    df32x16 xn = scores(tj + 32, aks[j + 1], vs[j + 1]);
+                    finish(tj, x, vs[j], &xn);
                     x = xn;
                 } else {
-                    finish(x, vs[j], nullptr);
+                    finish(tj, x, vs[j], nullptr);
                 }
             }
         }
@@ -811,6 +834,19 @@ hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* w
     P = decode_mfma_parts(B, Hkv, len, w, d);
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
     dim3 grid(P, B * Hkv);
+    if (k_lat == v_lat) {  // one shared latent array: each subtile loaded once
+#define DAR_DEC_SHARED(D_, DD_)                                                                     \
+    hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value, 0, false, true>), grid,    \
+                       dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
+                       part, o, Hq, Hkv, w, cap, len, P, qscale, (const float*)nullptr, 0, wv, PagedArgs{}, \
+                       (const int*)nullptr)
+        if (d == 64 && dd == 16) DAR_DEC_SHARED(64, 16);
+        else if (d == 64 && dd == 32) DAR_DEC_SHARED(64, 32);
+        else if (d == 128 && dd == 16) DAR_DEC_SHARED(128, 16);
+        else DAR_DEC_SHARED(128, 32);
+#undef DAR_DEC_SHARED
+        return hipGetLastError();
+    }
 #define DAR_DEC_LAUNCH(D_, DD_)                                                                     \
     hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value>), grid,                    \
                        dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
