@@ -613,29 +613,32 @@ template hipError_t launch_append<float>(const float*, const float*, const float
 namespace dar {
 
 // Append with a single shared latent per token (its latent is given, one
-// per token and KV head): grid (n, B*Hkv), 64 threads; token t (position
-// len + t) goes to latent slot len + t, and to ring slot (len + t) % w when
-// it is one of the newest min(n, w). Plain copies, so the cache holds the
-// given bits.
+// per token and KV head): grid (ceil(n / 64), B*Hkv), 256 threads; a block
+// copies the latents of 64 consecutive tokens (positions len + t) into their
+// slots (one contiguous run in both arrays), and the rows of those among the
+// newest min(n, w) tokens into ring slots (len + t) % w. Plain copies, so the
+// cache holds the given bits.
 template <typename T>
-__global__ __launch_bounds__(64) void append_shared_kernel(const T* __restrict__ k_new,
-                                                           const T* __restrict__ v_new,
-                                                           const T* __restrict__ c_new,
-                                                           T* __restrict__ k_win, T* __restrict__ v_win,
-                                                           T* __restrict__ lat, int d, int dd, int w,
-                                                           int cap, int len, int n) {
-    const int t = wg_id_x(), bg = wg_id_y();
-    const int lane = lane_id_x();
-    const int pos = len + t;
-    const T* cs = c_new + ((size_t)bg * n + t) * dd;
-    T* cd = lat + ((size_t)bg * cap + pos) * dd;
-    for (int c = lane; c < dd; c += 64) cd[c] = cs[c];
-    if (w > 0 && t >= n - imin(n, w)) {
-        const size_t src = ((size_t)bg * n + t) * d;
-        const size_t dst = ((size_t)bg * w + pos % w) * d;
-        for (int e = lane; e < d; e += 64) {
-            k_win[dst + e] = k_new[src + e];
-            v_win[dst + e] = v_new[src + e];
+__global__ __launch_bounds__(256) void append_shared_kernel(const T* __restrict__ k_new,
+                                                            const T* __restrict__ v_new,
+                                                            const T* __restrict__ c_new,
+                                                            T* __restrict__ k_win, T* __restrict__ v_win,
+                                                            T* __restrict__ lat, int d, int dd, int w,
+                                                            int cap, int len, int n) {
+    const int t0 = wg_id_x() * 64, bg = wg_id_y();
+    const int tid = lane_id_x();
+    const int nt = imin(64, n - t0);
+    const T* cs = c_new + ((size_t)bg * n + t0) * dd;
+    T* cd = lat + ((size_t)bg * cap + len + t0) * dd;
+    for (int i = tid; i < nt * dd; i += 256) cd[i] = cs[i];
+    if (w > 0) {
+        const int first = imax(t0, n - imin(n, w));  // first token of this block bound for the ring
+        for (int i = tid; i < (t0 + nt - first) * d; i += 256) {
+            const int t = first + i / d, e = i - (i / d) * d;
+            const size_t src = ((size_t)bg * n + t) * d + e;
+            const size_t dst = ((size_t)bg * w + (len + t) % w) * d + e;
+            k_win[dst] = k_new[src];
+            v_win[dst] = v_new[src];
         }
     }
 }
@@ -644,8 +647,8 @@ template <typename T>
 hipError_t launch_append_shared(const T* k_new, const T* v_new, const T* c_new, T* k_win, T* v_win,
                                 T* lat, int B, int Hkv, int d, int dd, int w, int cap, int len,
                                 int n, hipStream_t st) {
-    hipLaunchKernelGGL(append_shared_kernel<T>, dim3(n, B * Hkv), dim3(64), 0, st, k_new, v_new,
-                       c_new, k_win, v_win, lat, d, dd, w, cap, len, n);
+    hipLaunchKernelGGL(append_shared_kernel<T>, dim3((n + 63) / 64, B * Hkv), dim3(256), 0, st, k_new,
+                       v_new, c_new, k_win, v_win, lat, d, dd, w, cap, len, n);
     return hipGetLastError();
 }
 
