@@ -163,6 +163,8 @@ def main():
                     help="skip the prefill workloads reported beside the main one")
     ap.add_argument("--no-rope", action="store_true",
                     help="skip the prefill and decode with the rotary embedding")
+    ap.add_argument("--no-ragged", action="store_true",
+                    help="skip the ragged-batch prefill line")
     ap.add_argument("--no-paged", action="store_true",
                     help="skip the decode over a paged cache")
     ap.add_argument("--no-shared", action="store_true",
@@ -314,6 +316,19 @@ def main():
         shared["decode_ms"] = timed(run_sd, args.steps)
         shared["decode_len"] = scache.len
         del scache
+
+    # ragged prefill: the same padded batch, sequence lengths spread evenly
+    # over 256..T in a seeded order
+    ragged = {}
+    if not args.no_ragged:
+        lens_p = torch.linspace(256, pw.T, pw.B).round().to(torch.int32)
+        lens_p = lens_p[torch.randperm(pw.B, generator=torch.Generator().manual_seed(260618592))]
+        sl_dev = lens_p.to(dev)
+        run_rg = lambda i: dar.dar_attn_prefill_ragged(q, k, v, wd, None, pw.w, sl_dev, o=o, ws=ws)
+        for i in range(args.warmup):
+            run_rg(i)
+        ragged["ms"] = timed(run_rg, args.steps)
+        ragged["lens"] = [int(x) for x in lens_p.tolist()]
 
     # paged cache: the decode cache's contents copied into 256-token pages
     # handed out in a seeded random order; then the same pages with ragged
@@ -516,6 +531,14 @@ def main():
                      % (min(paged["ragged_lens"]), max(paged["ragged_lens"])),
             "us": round(rlu, 2), "alg_bytes": rb, "gbs": round(rb / (rlu * 1e-6) / 1e9, 1),
             "frac_hbm_peak": round(rb / (rlu * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+    if ragged:
+        gu = float(ragged["ms"] * 1e3)
+        gfl = sum(prefill_flops(1, pw.Hq, n, pw.d, pw.dd, pw.w) for n in ragged["lens"])
+        result["prefill_ragged"] = {
+            "shape": "pythia70m batch padded to %d, lengths %d..%d (ragged)"
+                     % (pw.T, min(ragged["lens"]), max(ragged["lens"])),
+            "us": round(gu, 2), "alg_flop": gfl, "tflops": round(gfl / (gu * 1e-6) / 1e12, 2),
+            "frac_bf16_peak": round(gfl / (gu * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)}
     if shared:
         su = float(shared["prefill_ms"] * 1e3)
         result["prefill_shared"] = {

@@ -122,6 +122,18 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
                             const void* v, const void* w_down, const void* w_up, void* o,
                             float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
 
+/* Causal prefill of a ragged batch: sequence b of the padded batch holds
+ * seq_lens[b] tokens (device int [B], each in [0, T]); q, k, v, o, lse are laid
+ * out as for dar_attn_prefill with T the padded length. Row i of sequence b,
+ * i < seq_lens[b], is Eq. 3-4 over that sequence's positions 0..i; positions
+ * at or past seq_lens[b] are never read (their contents do not matter) and
+ * those rows of o and lse are not written. Workspace and support as for
+ * dar_attn_prefill. */
+dar_status dar_attn_prefill_ragged(const dar_shape* s, int T, const int* seq_lens, const void* q,
+                                   const void* k, const void* v, const void* w_down,
+                                   const void* w_up, void* o, float* lse, void* ws,
+                                   size_t ws_bytes, hipStream_t stream);
+
 /* Append n >= 1 tokens k_new, v_new [B][Hkv][n][d] at positions len..len+n-1.
  * Every token that leaves the window (position len+t-w for t < n) is
  * down-projected with W_down (Eq. 1, fp32 accumulation, rounded to the cache

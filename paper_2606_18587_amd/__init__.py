@@ -93,6 +93,8 @@ def _load():
     lib.dar_cache_append_paged.argtypes = [shp, pcp, vp, vp, vp, vp]
     lib.dar_attn_decode_paged.restype = ci
     lib.dar_attn_decode_paged.argtypes = [shp, pcp] + [vp] * 5 + [sz, vp]
+    lib.dar_attn_prefill_ragged.restype = ci
+    lib.dar_attn_prefill_ragged.argtypes = [shp, ci] + [vp] * 9 + [sz, vp]
     lib.dar_prefill_rope_workspace_bytes.restype = sz
     lib.dar_prefill_rope_workspace_bytes.argtypes = [shp, ci]
     lib.dar_status_string.restype = ctypes.c_char_p
@@ -527,3 +529,29 @@ def dar_attn_decode_paged(cache: DarPagedCache, q, w_down, w_up=None, o=None, ws
     if st != DAR_OK:
         raise DarError(st, "dar_attn_decode_paged")
     return o
+
+
+def dar_attn_prefill_ragged(q, k, v, w_down, w_up, w, seq_lens, o=None, ws=None, stream=None,
+                            lse=None, return_lse=False):
+    """Causal prefill of a padded batch whose sequence b holds seq_lens[b]
+    tokens (int32 device tensor [B]); rows past a sequence's length are left
+    unwritten. Other arguments as dar_attn_prefill."""
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    dd = w_down.shape[2]
+    shape = make_shape(B, Hq, Hkv, d, dd, w, q.dtype)
+    if seq_lens.dtype != torch.int32 or tuple(seq_lens.shape) != (B,) or not seq_lens.is_cuda:
+        raise ValueError("seq_lens: expected an int32 device tensor of shape (%d,)" % B)
+    if o is None:
+        o = torch.empty_like(q)
+    if return_lse and lse is None:
+        lse = torch.empty(B, Hq, T, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = _workspace(dar_prefill_workspace_bytes(shape, T), q.device)
+    st = lib.dar_attn_prefill_ragged(ctypes.byref(shape), int(T), _ptr(seq_lens), _ptr(q), _ptr(k),
+                                     _ptr(v), _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(lse), _ptr(ws),
+                                     0 if ws is None else ws.numel() * ws.element_size(),
+                                     _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_prefill_ragged")
+    return (o, lse) if return_lse else o

@@ -318,6 +318,27 @@ dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 
+dar_status dar_attn_prefill_ragged(const dar_shape* s, int T, const int* seq_lens, const void* q,
+                                   const void* k, const void* v, const void* w_down,
+                                   const void* w_up, void* o, float* lse, void* ws,
+                                   size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (T < 1 || !seq_lens || ((uintptr_t)seq_lens & 3u)) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(w_down) || !dev_ok(o)) return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if (lse && !aligned16(lse)) return DAR_E_ARG;
+    const PrefillWs L = prefill_ws_layout(s->B, s->Hkv, T, s->d_down, s->w, esize_of(s->dtype));
+    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+    clear_hip_error();
+    PrefillGeo geo = whole_sequence(T);
+    geo.seq_lens = seq_lens;
+    const bool fast = s->dtype == DAR_BF16 && prefill_mfma_supported(s);
+    const hipError_t e = run_prefill(s, geo, q, k, v, w_down, w_up, o, lse, ws, L, fast, stream);
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
 dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, const void* k,
                                      const void* v, const void* w_down, const void* w_up,
                                      const void* o, const float* lse, const void* dout, void* dq,

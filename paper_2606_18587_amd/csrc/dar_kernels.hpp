@@ -53,14 +53,18 @@ struct PagedArgs {
 // prefill has q0 = kv0 = lat0 = 0 and n_rows = Tkv = T; a chunk appended to a
 // cache of len tokens has q0 = len, kv0 = max(0, len - w) (the ring's oldest
 // token), lat0 = len - w.
+// seq_lens (whole-sequence prefill of a ragged batch only): device int [B],
+// the length of each sequence of the padded batch; positions at or past a
+// sequence's length are neither read nor written (NULL: every sequence is T).
 struct PrefillGeo {
     int q0, n_rows, kv0, Tkv, lat0, cap;
     const void* k_lat;
     const void* v_lat;
+    const int* seq_lens = nullptr;
     int total() const { return q0 + n_rows; }
 };
 static inline PrefillGeo whole_sequence(int T) {
-    return PrefillGeo{0, T, 0, T, 0, 0, nullptr, nullptr};
+    return PrefillGeo{0, T, 0, T, 0, 0, nullptr, nullptr, nullptr};
 }
 // Rows of a 32-token block of the transposed value latents written by the
 // matrix-core pre-pass: d_down, plus a row of ones when d_down == 16 (the

@@ -236,7 +236,7 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
     bf16_t* __restrict__ cK, bf16_t* __restrict__ cVt, float* __restrict__ cnorm,
     float* __restrict__ knorm, bf16_t* __restrict__ consts, int Hkv, int T_, int dd, int Tl,
     int Tp, int kv0, int Tkv, int lat0, const bf16_t* __restrict__ k_lat,
-    const bf16_t* __restrict__ v_lat, int cap) {
+    const bf16_t* __restrict__ v_lat, int cap, const int* __restrict__ seq_lens) {
     constexpr int KS = D / 16;
     constexpr int LDW = D + 8;   // W^T row in LDS (bf16 elements)
     constexpr int LDT = 32 + 8;  // transposed value-latent row in LDS
@@ -246,6 +246,10 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
         consts[lane_id_x()] = lane_id_x() < 8 ? (bf16_t)0x3f80 : (bf16_t)0;
     const int bg = wg_id_y();
     const int g = bg % Hkv;
+    // a ragged batch: this sequence's length Tv (positions at or past it are
+    // padding: no norm, zero latents), its latent count Tlv
+    const int Tv = seq_lens ? imin(imax(seq_lens[bg / Hkv], 0), T_) : T_;
+    const int Tlv = Tl - (T_ - Tv);
     const int tid = lane_id_x();
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -306,7 +310,7 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
             float n2 = 0.f;
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
-                const uint4 u = __builtin_bit_cast(uint4, t < T_ && t >= kv0 ? cur.k[s] : zero8);
+                const uint4 u = __builtin_bit_cast(uint4, t < Tv && t >= kv0 ? cur.k[s] : zero8);
                 const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
 #pragma unroll
                 for (int j = 0; j < 4; ++j) {
@@ -323,8 +327,8 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
             lbf16x8 xk[KS], xv[KS];
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
-                xk[s] = t < Tl ? cur.k[s] : zero8;
-                xv[s] = t < Tl ? cur.v[s] : zero8;
+                xk[s] = t < Tlv ? cur.k[s] : zero8;
+                xv[s] = t < Tlv ? cur.v[s] : zero8;
             }
             // Latents read from the cache for positions below lat0: per lane
             // the columns 8q + 4hg + 0..3 of its token, i.e. the register
@@ -517,7 +521,7 @@ hipError_t launch_prefill_latent<bf16_t>(const bf16_t* k, const bf16_t* v, const
     auto kern = d == 64 ? prefill_latent_mfma_kernel<64> : prefill_latent_mfma_kernel<128>;
     hipLaunchKernelGGL(kern, grid, dim3(256), 0, st, k, v, wd, cK, cVt, cnorm, knorm, consts, Hkv,
                        T_, dd, Tl, Tp, geo.kv0, geo.Tkv, geo.lat0, (const bf16_t*)geo.k_lat,
-                       (const bf16_t*)geo.v_lat, geo.cap);
+                       (const bf16_t*)geo.v_lat, geo.cap, geo.seq_lens);
     return hipGetLastError();
 }
 

@@ -584,7 +584,8 @@ void prefill_mfma_kernel(
     const bf16_t* __restrict__ cVt, const float* __restrict__ cnorm,
     const float* __restrict__ knorm, const bf16_t* __restrict__ consts, bf16_t* __restrict__ o,
     float* __restrict__ lse, int Hq, int Hkv, int T, int w, int Tp, int nblk, int BH,
-    float c_scale, int q0, int n_rows, int kv0, int Tkv, const bf16_t* __restrict__ wv) {
+    float c_scale, int q0, int n_rows, int kv0, int Tkv, const bf16_t* __restrict__ wv,
+    const int* __restrict__ seq_lens) {
     constexpr int BM = NW * 32;
     constexpr int KS = D / 16;   // 16-wide k slabs of q . k
     constexpr int DS = DD / 16;  // 16-wide k slabs of q~ . c^K
@@ -618,6 +619,9 @@ void prefill_mfma_kernel(
     const int b = bh / Hq, h = bh - (bh / Hq) * Hq;
     const int g = h / (Hq / Hkv);
     const int bg = b * Hkv + g;
+    // this sequence's length (a ragged batch; T, the padded length, stays the
+    // layout of every array)
+    const int Tb = seq_lens ? imin(imax(seq_lens[b], 0), T) : T;
     const int tid = lane_id_x();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const bf16_t* wdg = wd + (size_t)g * D * DD;
@@ -668,8 +672,9 @@ void prefill_mfma_kernel(
         __asm__ volatile("" : "+v"(lane));
         const int rb = part == 0 ? nblk - 1 - pair : pair;
         if (part == 1 && rb >= nblk - 1 - pair) break;  // odd block count: middle block once
+        if (q0 + rb * BM >= Tb) continue;  // past this sequence's end (workgroup-uniform)
         RowCtx c;
-        c.T = T;
+        c.T = Tb;
         c.w = w;
         c.Tp = Tp;
         c.qc = lane & 31;
@@ -684,14 +689,14 @@ void prefill_mfma_kernel(
         const int i0 = q0 + rb * BM;  // position of the block's first row
         c.r0 = i0 + wave * 32;
         c.i = c.r0 + c.qc;
-        c.i_hi = imin(c.r0 + 31, T - 1);  // last real row of this wavefront (< r0 if none)
+        c.i_hi = imin(c.r0 + 31, Tb - 1);  // last real row of this wavefront (< r0 if none)
         const int qc = c.qc, hg = c.hg, i = c.i;
 
-        const int jd_end = (c.r0 < T) ? c.i_hi - w : -1;  // last distant key of any row here
+        const int jd_end = (c.r0 < Tb) ? c.i_hi - w : -1;  // last distant key of any row here
         const int js_last = jd_end & ~31;
-        const int iwg_hi = imin(i0 + BM - 1, T - 1);
+        const int iwg_hi = imin(i0 + BM - 1, Tb - 1);
         const bool has_local = w > 0 && imax(0, i0 - w + 1) <= iwg_hi;
-        const int ii = imin(i, T - 1);
+        const int ii = imin(i, Tb - 1);
 
         // Every global load of the setup is issued here, before any of its
         // results is used: the query row, the row's own key or latent (the
@@ -718,7 +723,7 @@ void prefill_mfma_kernel(
         const int kb_lo = imax(0, c.r0 - w + 1) >> 5, kb_hi = imax(0, c.i_hi) >> 5;
         float cmax = lane < nsb ? cnorm[(size_t)bg * (Tp / 32) + lane] : 0.f;
         float kmax = (has_local && kb_lo + lane <= kb_hi) ? knorm[(size_t)bg * nkb + kb_lo + lane] : 0.f;
-        if (i >= T) {
+        if (i >= Tb) {
 #pragma unroll
             for (int s = 0; s < KS; ++s) qop[s] = zero_bf16x8();
         }
@@ -787,7 +792,7 @@ void prefill_mfma_kernel(
             for (int s = 0; s < DS; ++s) witness = dot8(qtop[s], wit[s], witness);
         }
         witness = pair_sum(witness);
-        const bool fixed = c.r0 < T && !__builtin_amdgcn_ballot_w64(i < T && bound - witness > 100.f);
+        const bool fixed = c.r0 < Tb && !__builtin_amdgcn_ballot_w64(i < Tb && bound - witness > 100.f);
         if (fixed) {
             st.m = bound;
             st.cm = -bound;
@@ -823,7 +828,7 @@ void prefill_mfma_kernel(
             }
         }
 
-        if (c.r0 >= T) continue;
+        if (c.r0 >= Tb) continue;
 
         // ------------------------------------------------------------ epilogue
         float lt = st.l;
@@ -861,7 +866,7 @@ void prefill_mfma_kernel(
             }
         }
 
-        if (i < T) {
+        if (i < Tb) {
             // log of the row's softmax denominator (natural log), for a backward pass
             if (lse && hg == 0) lse[(size_t)bh * n_rows + (i - q0)] = (st.m + log2f(lt)) * 0.6931471805599453f;
             const float inv = 1.f / lt;
@@ -911,7 +916,7 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w
                        (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)wd, (const bf16_t*)wu,
                        (const bf16_t*)cK, (const bf16_t*)cVt, cnorm, knorm, (const bf16_t*)consts,
                        (bf16_t*)o, lse, Hq, Hkv, T, w, Tp, nblk, BH, c_scale, geo.q0,
-                       geo.n_rows, geo.kv0, geo.Tkv, (const bf16_t*)wv);
+                       geo.n_rows, geo.kv0, geo.Tkv, (const bf16_t*)wv, geo.seq_lens);
     return hipGetLastError();
 }
 

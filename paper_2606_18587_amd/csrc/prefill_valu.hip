@@ -22,7 +22,7 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
     const T* __restrict__ wd, const T* __restrict__ wu, const T* __restrict__ cK,
     const T* __restrict__ cVt, T* __restrict__ o, float* __restrict__ lse, int Hq, int Hkv,
     int q0, int n_rows, int kv0, int Tkv, int d, int dd, int w, int Tp, float qscale,
-    const T* __restrict__ wv) {
+    const T* __restrict__ wv, const int* __restrict__ seq_lens) {
     __shared__ float qs[256];
     __shared__ float qts[256];
     __shared__ float ps[64];
@@ -34,6 +34,8 @@ __global__ __launch_bounds__(64) void prefill_valu_kernel(
     const int b = bh / Hq, h = bh - (bh / Hq) * Hq;
     const int g = h / (Hq / Hkv);
     const int bg = b * Hkv + g;
+    // a ragged batch: rows at or past this sequence's length are not computed
+    if (seq_lens && i >= seq_lens[b]) return;
     const T* wdg = wd + (size_t)g * d * dd;
     const T* wug = wu ? wu + (size_t)g * dd * d : nullptr;
     const T* wvg = wv ? wv + (size_t)g * dd * d : nullptr;  // value lift (shared latent), else W_up
@@ -167,7 +169,8 @@ hipError_t launch_prefill_valu(const T* q, const T* k, const T* v, const T* wd, 
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
     dim3 grid(geo.n_rows, B * Hq);
     hipLaunchKernelGGL(prefill_valu_kernel<T>, grid, dim3(64), 0, st, q, k, v, wd, wu, cK, cVt, o,
-                       lse, Hq, Hkv, geo.q0, geo.n_rows, geo.kv0, geo.Tkv, d, dd, w, Tp, qscale, wv);
+                       lse, Hq, Hkv, geo.q0, geo.n_rows, geo.kv0, geo.Tkv, d, dd, w, Tp, qscale, wv,
+                       geo.seq_lens);
     return hipGetLastError();
 }
 

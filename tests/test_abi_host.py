@@ -36,7 +36,7 @@ def test_exports_every_declared_symbol():
                           "dar_rope_table", "dar_attn_prefill_rope", "dar_attn_decode_rope",
                           "dar_attn_prefill_shared", "dar_cache_append_shared",
                           "dar_attn_decode_shared", "dar_cache_append_paged",
-                          "dar_attn_decode_paged",
+                          "dar_attn_decode_paged", "dar_attn_prefill_ragged",
                           "dar_prefill_rope_workspace_bytes", "dar_status_string"}
     raw = ctypes.CDLL(dar.LIB_PATH)
     for n in names:
@@ -393,3 +393,15 @@ def test_paged_rejects_before_any_launch():
     assert dc(pc(), ws_bytes=8) == dar.DAR_E_WORKSPACE
     assert dc(pc(), shape=S(dtype=torch.float32)) == dar.DAR_E_UNSUPPORTED   # matrix-core shapes only
     assert dc(pc(), shape=S(d=80, dd=16)) == dar.DAR_E_UNSUPPORTED
+
+
+@no_gpu
+def test_ragged_prefill_rejects_before_any_launch():
+    s = S()
+    call = lambda T=16, lens=FAKE, q=FAKE, ws_bytes=1 << 30: dar.lib.dar_attn_prefill_ragged(
+        ctypes.byref(s), T, lens, q, FAKE, FAKE, FAKE, None, FAKE, None, FAKE, ws_bytes, None)
+    assert call(lens=None) == dar.DAR_E_ARG
+    assert call(lens=ctypes.c_void_p((1 << 20) + 2)) == dar.DAR_E_ARG
+    assert call(T=0) == dar.DAR_E_ARG
+    assert call(q=MISALIGNED) == dar.DAR_E_ARG
+    assert call(ws_bytes=16) == dar.DAR_E_WORKSPACE
