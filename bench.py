@@ -60,13 +60,13 @@ CSRC = os.path.join(ROOT, "paper_2606_18587_amd", "csrc")
 MEASURED_TRAFFIC = {
     "prefill": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "latent.hip",
                           "prefill_mfma.hip"],
-                "sha256_16": "e28479b4c4e44586", "bytes": 132674892},
+                "sha256_16": "c8c26149d800ab81", "bytes": 132222963},
     "decode": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "decode.hip",
                          "decode_mfma.hip"],
-               "sha256_16": "92e318e4d2b1a58b", "bytes": 574067915},
+               "sha256_16": "b74104da949ca313", "bytes": 574224062},
     "backward": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "mfma_common.hpp",
                            "backward.hip", "backward_mfma.hip"],
-                 "sha256_16": "9dc7ebc5630c6fb7", "bytes": 500446639},
+                 "sha256_16": "0c77ba9ba9d9d3eb", "bytes": 500385874},
 }
 
 

@@ -717,16 +717,17 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
     clear_hip_error();
     const PagedArgs pg{c->lens, c->block_table, c->page_size, c->max_blocks, c->n_pages,
                        __builtin_ctz((unsigned)c->page_size)};
-    int P = 0;
+    int P = 0, chunk = 0;
     hipError_t e = launch_decode_mfma_paged((const bf16_t*)q, (const bf16_t*)w_down,
                                             (const bf16_t*)w_up, (const bf16_t*)c->k_win,
                                             (const bf16_t*)c->v_win, (const bf16_t*)c->k_pool,
                                             (const bf16_t*)c->v_pool, pg, (float*)ws, (bf16_t*)o,
-                                            s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, P, stream);
+                                            s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, P, chunk,
+                                            stream);
     if (e == hipSuccess && P > 1)
         e = launch_decode_combine<bf16_t>((const float*)ws, (const bf16_t*)w_down,
                                           (const bf16_t*)w_up, (bf16_t*)o, s->B, s->Hq, s->Hkv,
-                                          s->d, s->d_down, P, stream);
+                                          s->d, s->d_down, P, stream, nullptr, c->lens, chunk);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 

@@ -43,6 +43,7 @@ struct PagedArgs {
     const int* bt;
     int ps, maxb, n_pages;
     int ps_shift;  // log2(ps): page sizes are powers of two
+    int chunk;     // most tokens one part (workgroup) of a sequence takes
 };
 
 // Where the rows, keys/values and latents of a prefill come from. Rows
@@ -129,7 +130,7 @@ hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf1
                                     const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_pool,
                                     const bf16_t* v_pool, const PagedArgs& pg, float* part,
                                     bf16_t* o, int B, int Hq, int Hkv, int d, int dd, int w, int& P,
-                                    hipStream_t st);
+                                    int& chunk, hipStream_t st);
 // One token per sequence into a paged cache at position lens[b]; the token
 // leaving the window is projected (as launch_append projects it) into its
 // page slot; lens[b] += 1 for every sequence below capacity.
@@ -219,7 +220,7 @@ hipError_t launch_rope_prepass(const T* q, const T* k, const T* v, const T* wd, 
 template <typename T>
 hipError_t launch_decode_combine(const float* part, const T* wd, const T* wu, T* o, int B, int Hq,
                                  int Hkv, int d, int dd, int S, hipStream_t st,
-                                 const T* wv = nullptr);
+                                 const T* wv = nullptr, const int* lens = nullptr, int chunk = 0);
 // Decode with the rotary embedding of Eq. 3 (query at position len - 1, cache
 // token e at position e; positions < len index the table).
 template <typename T>

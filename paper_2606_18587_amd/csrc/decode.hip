@@ -248,14 +248,18 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
 template <typename T>
 __global__ __launch_bounds__(64) void decode_combine_kernel(
     const float* __restrict__ part, const T* __restrict__ wd, const T* __restrict__ wu,
-    T* __restrict__ o, int Hq, int Hkv, int d, int dd, int S, const T* __restrict__ wv) {
+    T* __restrict__ o, int Hq, int Hkv, int d, int dd, int S_all, const T* __restrict__ wv,
+    const int* __restrict__ lens, int chunk) {
     constexpr int kLiftCols = 32;  // W_up rows held in registers (d_down <= 32, d <= 64)
     const int bh = wg_id_x();
+    // records per head: S_all, or (a paged batch) the parts this sequence's
+    // length used, one per chunk tokens
+    const int S = lens ? imin(S_all, imax(1, (lens[bh / Hq] + chunk - 1) / chunk)) : S_all;
     const int h = bh % Hq;
     const int g = h / (Hq / Hkv);
     const int lane = lane_id_x();
     const int stride = 2 + dd + d;
-    const float* pp = part + (size_t)bh * S * stride;
+    const float* pp = part + (size_t)bh * S_all * stride;
     const T* wdg = wd + (size_t)g * d * dd;
     // the lift's matrix: W_up (W_down^T when tied), or (shared latent) the
     // value matrix
@@ -344,17 +348,18 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
 
 template <typename T>
 hipError_t launch_decode_combine(const float* part, const T* wd, const T* wu, T* o, int B, int Hq,
-                                 int Hkv, int d, int dd, int S, hipStream_t st, const T* wv) {
+                                 int Hkv, int d, int dd, int S, hipStream_t st, const T* wv,
+                                 const int* lens, int chunk) {
     hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu, o, Hq,
-                       Hkv, d, dd, S, wv);
+                       Hkv, d, dd, S, wv, lens, chunk);
     return hipGetLastError();
 }
 template hipError_t launch_decode_combine<float>(const float*, const float*, const float*, float*,
                                                  int, int, int, int, int, int, hipStream_t,
-                                                 const float*);
+                                                 const float*, const int*, int);
 template hipError_t launch_decode_combine<bf16_t>(const float*, const bf16_t*, const bf16_t*,
                                                   bf16_t*, int, int, int, int, int, int,
-                                                  hipStream_t, const bf16_t*);
+                                                  hipStream_t, const bf16_t*, const int*, int);
 
 static int group_chunk(int G) { return kDecScoreSlots / G; }
 
@@ -399,7 +404,7 @@ static hipError_t launch_decode_g(const T* q, const T* wd, const T* wu, const T*
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu, o,
-                       Hq, Hkv, d, dd, S, wv);
+                       Hq, Hkv, d, dd, S, wv, (const int*)nullptr, 0);
     return hipGetLastError();
 }
 
@@ -416,7 +421,7 @@ hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, c
                                           (const bf16_t*)wv);
         if (e != hipSuccess || P == 1) return e;
         hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu,
-                           o, Hq, Hkv, d, dd, P, wv);
+                           o, Hq, Hkv, d, dd, P, wv, (const int*)nullptr, 0);
         return hipGetLastError();
     }
     switch (Hq / Hkv) {

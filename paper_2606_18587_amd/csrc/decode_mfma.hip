@@ -332,6 +332,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const int bg = wg_id_y();
     const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
     const int len = PAGED ? pg.lens[b] : len_arg;  // tokens in this sequence's cache
+    // a paged (ragged) batch: this sequence uses one part per chunk tokens of
+    // its own length, so a long sequence is spread over more workgroups than
+    // a short one; the other parts have nothing to do (workgroup-uniform)
+    const int Pb = PAGED ? imin(P, imax(1, (len + pg.chunk - 1) / pg.chunk)) : P;
+    if (s >= Pb) return;
     const int G = Hq / Hkv;
     const int tid = lane_id_x();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -359,7 +364,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             if (idx < DD * D) wsh[idx / D][idx - (idx / D) * D] = bf16_to_f32(uv[j]);
         }
     }
-    const WaveRun run = decode_wave_run(len, w, D, DD, P * NW, s * NW + wave);
+    const WaveRun run = decode_wave_run(len, w, D, DD, Pb * NW, s * NW + wave);
     const bool latent = run.latent != 0;
     const int t_begin = run.t_begin, t_end = run.t_end;  // this wavefront's tokens
     bf16_t* vb = vbuf[wave];
@@ -893,11 +898,20 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
 
 hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
                                     const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_pool,
-                                    const bf16_t* v_pool, const PagedArgs& pg, float* part,
+                                    const bf16_t* v_pool, const PagedArgs& pg_in, float* part,
                                     bf16_t* o, int B, int Hq, int Hkv, int d, int dd, int w, int& P,
-                                    hipStream_t st) {
-    const int cap = pg.maxb * pg.ps;
+                                    int& chunk, hipStream_t st) {
+    const int cap = pg_in.maxb * pg_in.ps;
+    // Parts per (sequence, KV head) as for a dense cache at full capacity;
+    // lengths differ per sequence and live on the device, so each sequence
+    // takes one part per chunk tokens of its own length and the rest return
+    // at once. (More parts than that, so that a long sequence of a full batch
+    // is spread wider, measured slower: every extra generation of workgroups
+    // pays its own pipeline fill and drain, and the merge kernel runs.)
     P = decode_mfma_parts(B, Hkv, cap, w, d);
+    chunk = (cap + P - 1) / P;
+    PagedArgs pg = pg_in;
+    pg.chunk = chunk;
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
     dim3 grid(P, B * Hkv);
 #define DAR_DEC_PAGED(D_, DD_)                                                                       \
