@@ -699,26 +699,12 @@ void prefill_mfma_kernel(
         const int ii = imin(i, Tb - 1);
 
         // Every global load of the setup is issued here, before any of its
-        // results is used: the query row, the row's own key or latent (the
-        // witness), and the first norm maxima of both regions.
+        // results is used: the query row and the first norm maxima of both
+        // regions.
         const bf16_t* qrow = q + ((size_t)bh * n_rows + (ii - q0)) * D;
         bf16x8_t qop[KS];  // B operand of S^T = K Q^T: q[i][s*16 + hg*8 + 0..7]
 #pragma unroll
         for (int s = 0; s < KS; ++s) qop[s] = load_bf16x8(qrow + s * 16 + hg * 8);
-        bf16x8_t wit[KS];  // own key (w >= 1) or own latent key (w = 0)
-        if (w >= 1) {
-            const bf16_t* krow = k + ((size_t)bg * Tkv + (ii - kv0)) * D;
-#pragma unroll
-            for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(krow + s * 16 + hg * 8);
-        } else if (ROPE) {
-            const bf16_t* crow = cK + ((size_t)bg * c.Td + ii) * D;  // lifted, rotated own key
-#pragma unroll
-            for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(crow + s * 16 + hg * 8);
-        } else {
-            const bf16_t* crow = cK + ((size_t)bg * Tp + ii) * DD;
-#pragma unroll
-            for (int s = 0; s < KS; ++s) wit[s] = s < DS ? load_bf16x8(crow + s * 16 + hg * 8) : zero_bf16x8();
-        }
         const int nsb = jd_end >= 0 ? (js_last >> 5) + 1 : 0;  // latent blocks with a norm
         const int kb_lo = imax(0, c.r0 - w + 1) >> 5, kb_hi = imax(0, c.i_hi) >> 5;
         float cmax = lane < nsb ? cnorm[(size_t)bg * (Tp / 32) + lane] : 0.f;
@@ -778,21 +764,41 @@ void prefill_mfma_kernel(
             kmax = wave_max(kmax);
             bound = fmaxf(bound, c_scale * sqrtf(qs2) * kmax);
         }
-        // Fixed reference: the bound (inflated for fp32 rounding) is used when,
-        // for every row, it is within 2^100 of a real score of that row (its own
-        // key), so no row's weights can all underflow.
+        // Fixed reference: the bound (inflated for fp32 rounding) bounds |s|
+        // for every real score s of the row (Cauchy-Schwarz), so when it is at
+        // most 50 every weight 2^(s - bound) is at least 2^-100. A row with a
+        // larger bound needs a witness: a real score of that row (its own key
+        // or latent) within 100 of the bound, so that its largest weight
+        // cannot underflow. Only a wavefront with such a row loads it.
         bound = bound * 1.001f + 1e-6f;
-        float witness = 0.f;
-        if (w >= 1 || ROPE) {
+        bool fixed = c.r0 < Tb;
+        if (fixed && __builtin_amdgcn_ballot_w64(i < Tb && bound > 50.f)) {
+            bf16x8_t wit[KS];  // own key (w >= 1) or own latent key (w = 0)
+            if (w >= 1) {
+                const bf16_t* krow = k + ((size_t)bg * Tkv + (ii - kv0)) * D;
 #pragma unroll
-            for (int s = 0; s < KS; ++s) witness = dot8(qop[s], wit[s], witness);
-            witness *= c_scale;
-        } else {
+                for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(krow + s * 16 + hg * 8);
+            } else if (ROPE) {
+                const bf16_t* crow = cK + ((size_t)bg * c.Td + ii) * D;  // lifted, rotated own key
 #pragma unroll
-            for (int s = 0; s < DS; ++s) witness = dot8(qtop[s], wit[s], witness);
+                for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(crow + s * 16 + hg * 8);
+            } else {
+                const bf16_t* crow = cK + ((size_t)bg * Tp + ii) * DD;
+#pragma unroll
+                for (int s = 0; s < KS; ++s) wit[s] = s < DS ? load_bf16x8(crow + s * 16 + hg * 8) : zero_bf16x8();
+            }
+            float witness = 0.f;
+            if (w >= 1 || ROPE) {
+#pragma unroll
+                for (int s = 0; s < KS; ++s) witness = dot8(qop[s], wit[s], witness);
+                witness *= c_scale;
+            } else {
+#pragma unroll
+                for (int s = 0; s < DS; ++s) witness = dot8(qtop[s], wit[s], witness);
+            }
+            witness = pair_sum(witness);
+            fixed = !__builtin_amdgcn_ballot_w64(i < Tb && bound - witness > 100.f);
         }
-        witness = pair_sum(witness);
-        const bool fixed = c.r0 < Tb && !__builtin_amdgcn_ballot_w64(i < Tb && bound - witness > 100.f);
         if (fixed) {
             st.m = bound;
             st.cm = -bound;
