@@ -282,26 +282,38 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
     // row (loads return in order, so the LDS stores wait for W only and the
     // rows stay in flight through the barrier). Column indices are clamped so
     // that no load sits under a branch.
+    // A workgroup whose 128 positions all take their latents from the cache
+    // and lie below the first key row (chunked prefill: no key norm either)
+    // projects nothing: it only copies the cached latents into this kernel's
+    // layouts with their norms (workgroup-uniform, so the barrier below is
+    // skipped by every thread of it or by none).
+    const int chunk = wg_id_x();
+    const bool cached = chunk * 128 + 127 < imin(lat0, kv0);
+    const lbf16x8 zero8 = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
     constexpr int WPT = D * 32 / 256;  // W elements per thread
     const bf16_t* wdg = wd + (size_t)g * D * dd;
-    bf16_t wv[WPT];
-#pragma unroll
-    for (int j = 0; j < WPT; ++j) {
-        const int idx = tid + 256 * j, e = idx >> 5, c = idx & 31;
-        wv[j] = wdg[(size_t)e * dd + imin(c, dd - 1)];
-    }
-    const int chunk = wg_id_x();
-    const Rows cur = load(chunk);
-#pragma unroll
-    for (int j = 0; j < WPT; ++j) {
-        const int idx = tid + 256 * j, e = idx >> 5, c = idx & 31;
-        wsh[c * LDW + e] = c < dd ? wv[j] : (bf16_t)0;
-    }
-    __syncthreads();
+    Rows cur;
     lbf16x8 wa[KS];
+    if (!cached) {
+        bf16_t wv[WPT];
 #pragma unroll
-    for (int s = 0; s < KS; ++s) wa[s] = *reinterpret_cast<const lbf16x8*>(wsh + tl * LDW + s * 16 + hg * 8);
-    const lbf16x8 zero8 = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
+        for (int j = 0; j < WPT; ++j) {
+            const int idx = tid + 256 * j, e = idx >> 5, c = idx & 31;
+            wv[j] = wdg[(size_t)e * dd + imin(c, dd - 1)];
+        }
+        cur = load(chunk);
+#pragma unroll
+        for (int j = 0; j < WPT; ++j) {
+            const int idx = tid + 256 * j, e = idx >> 5, c = idx & 31;
+            wsh[c * LDW + e] = c < dd ? wv[j] : (bf16_t)0;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int s = 0; s < KS; ++s) wa[s] = *reinterpret_cast<const lbf16x8*>(wsh + tl * LDW + s * 16 + hg * 8);
+    } else {
+#pragma unroll
+        for (int s = 0; s < KS; ++s) cur.k[s] = cur.v[s] = wa[s] = zero8;
+    }
 
     {
         const int ts = chunk * 128 + wave * 32;  // first token of this wavefront
@@ -347,9 +359,10 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
                     }
             }
             auto cpair = [&](const uint2 (&c)[4], int m) { return (m & 1) ? c[m >> 1].y : c[m >> 1].x; };
+            const lf32x16 zacc = {};
             // key latents: token-major, columns in latent_pos order, plus the norm
             {
-                const lf32x16 acc = project_mfma<D>(wa, xk);
+                const lf32x16 acc = cached ? zacc : project_mfma<D>(wa, xk);
                 // squared norm of the stored (bf16-rounded) row; columns past
                 // d_down are zero (W^T rows past d_down are zero)
                 float n2 = 0.f;
@@ -375,7 +388,7 @@ __global__ __launch_bounds__(256) void prefill_latent_mfma_kernel(
             }
             // value latents, transposed per 32-token block: [c][token], via LDS
             {
-                const lf32x16 acc = project_mfma<D>(wa, xv);
+                const lf32x16 acc = cached ? zacc : project_mfma<D>(wa, xv);
                 bf16_t* tb = vtr[wave];
                 // all 32 rows of the block (rows past d_down are zero and not read)
 #pragma unroll
