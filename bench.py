@@ -176,7 +176,7 @@ def main():
                     help="only run a plain device copy of known size (HBM counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py measures one GPU only; this build has no multi-GPU path "
+        print("bench.py measures one GPU only; the library has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
 
@@ -422,8 +422,8 @@ def main():
     dbytes = decode_bytes(dw.B, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, L_last)
     gbs = dbytes / (dec_us * 1e-6) / 1e9
 
-    # ---------------- the other prefill workloads (parity-test shapes of the
-    # survey's configurations), each timed the same way; not part of `value`
+    # ---------------- the other prefill workloads (the parity-test shapes of
+    # the other prefill configurations), each timed the same way; not part of `value`
     other = {}
     if not args.no_other_prefill:
         for name in ("pythia410m_w128", "pythia410m_w512", "long16k"):
