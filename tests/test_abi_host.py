@@ -405,3 +405,26 @@ def test_ragged_prefill_rejects_before_any_launch():
     assert call(T=0) == dar.DAR_E_ARG
     assert call(q=MISALIGNED) == dar.DAR_E_ARG
     assert call(ws_bytes=16) == dar.DAR_E_WORKSPACE
+
+
+def test_ragged_prefill_binding_checks_lengths():
+    """The binding rejects lengths that are not an int32 tensor of shape (B,)
+    on the device, before any call into the library."""
+    q = torch.zeros(2, 2, 8, 64, dtype=torch.bfloat16)
+    k = torch.zeros(2, 1, 8, 64, dtype=torch.bfloat16)
+    wd = torch.zeros(1, 64, 16, dtype=torch.bfloat16)
+    for lens in (torch.tensor([8, 3], dtype=torch.int64), torch.tensor([8], dtype=torch.int32),
+                 torch.tensor([8, 3], dtype=torch.int32)):   # the last one is on the host
+        with pytest.raises(ValueError):
+            dar.dar_attn_prefill_ragged(q, k, k, wd, None, 4, lens)
+
+
+def test_bench_refuses_several_gpus():
+    """bench.py measures one GPU: --gpus 2 exits with status 2 and says so."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode == 2
+    assert "one GPU" in r.stderr
