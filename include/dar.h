@@ -109,9 +109,6 @@ typedef struct {
 /* Causal prefill over positions 0..T-1 (Eq. 3-4 for every row).
  *   q [B][Hq][T][d], k, v [B][Hkv][T][d], w_down [Hkv][d][d_down],
  *   w_up [Hkv][d_down][d] or NULL (tied), o [B][Hq][T][d] (output).
- *   lse: NULL, or fp32 [B][Hq][T] (output): the natural log of each row's
- *   softmax denominator, log sum_j exp(S_ij) with S_ij the scaled score of
- *   Eq. 4; dar_attn_prefill_backward takes it.
  *   ws: device workspace of at least dar_prefill_workspace_bytes(s, T) bytes
  *   (never NULL; caller-owned, overwritten by the call): latents of the
  *   tokens that are distant for some row (Eq. 1), per-32-token norm maxima
@@ -120,7 +117,19 @@ typedef struct {
  * d_down in {16, 32} take the matrix-core path). */
 dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void* k,
                             const void* v, const void* w_down, const void* w_up, void* o,
-                            float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
+                            void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* dar_attn_prefill that also writes each row's softmax statistics for a
+ * backward pass (Section 2.3 trains through this attention):
+ *   lse: NULL (then identical to dar_attn_prefill), or fp32 [B][Hq][T]
+ *   (output): the natural log of each row's softmax denominator,
+ *   log sum_j exp(S_ij) with S_ij the scaled score of Eq. 4;
+ *   dar_attn_prefill_backward takes it.
+ * Every other argument, the output o and the support are those of
+ * dar_attn_prefill; asking for lse changes no bit of o. */
+dar_status dar_attn_prefill_lse(const dar_shape* s, int T, const void* q, const void* k,
+                                const void* v, const void* w_down, const void* w_up, void* o,
+                                float* lse, void* ws, size_t ws_bytes, hipStream_t stream);
 
 /* Causal prefill of a ragged batch: sequence b of the padded batch holds
  * seq_lens[b] tokens (device int [B], each in [0, T]); q, k, v, o, lse are laid

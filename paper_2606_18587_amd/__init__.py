@@ -58,7 +58,9 @@ def _load():
     shp = ctypes.POINTER(DarShape)
     cp = ctypes.POINTER(DarCacheStruct)
     lib.dar_attn_prefill.restype = ci
-    lib.dar_attn_prefill.argtypes = [shp, ci, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.dar_attn_prefill.argtypes = [shp, ci, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.dar_attn_prefill_lse.restype = ci
+    lib.dar_attn_prefill_lse.argtypes = [shp, ci, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.dar_cache_append.restype = ci
     lib.dar_cache_append.argtypes = [shp, cp, vp, vp, ci, vp, vp]
     lib.dar_attn_decode.restype = ci
@@ -167,7 +169,8 @@ def dar_attn_prefill(q, k, v, w_down, w_up, w, o=None, ws=None, stream=None, che
     """Causal DAR prefill. q [B,Hq,T,d]; k, v [B,Hkv,T,d]; w_down [Hkv,d,dd];
     w_up [Hkv,dd,d] or None (tied). Returns o [B,Hq,T,d], or (o, lse) with
     return_lse (lse [B,Hq,T] fp32, the log of each row's softmax denominator,
-    written into `lse` when given)."""
+    written into `lse` when given). Calls dar_attn_prefill, or
+    dar_attn_prefill_lse when the log-sum-exp is asked for."""
     B, Hq, T, d = q.shape
     Hkv = k.shape[1]
     dd = w_down.shape[2]
@@ -189,13 +192,28 @@ def dar_attn_prefill(q, k, v, w_down, w_up, w, o=None, ws=None, stream=None, che
     need = dar_prefill_workspace_bytes(shape, T)
     if ws is None:
         ws = _workspace(need, q.device)
-    st = lib.dar_attn_prefill(ctypes.byref(shape), int(T), _ptr(q), _ptr(k), _ptr(v),
-                              _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(lse), _ptr(ws),
-                              0 if ws is None else ws.numel() * ws.element_size(),
-                              _stream(stream))
+    wsb = 0 if ws is None else ws.numel() * ws.element_size()
+    if lse is None:
+        st = lib.dar_attn_prefill(ctypes.byref(shape), int(T), _ptr(q), _ptr(k), _ptr(v),
+                                  _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(ws), wsb,
+                                  _stream(stream))
+        where = "dar_attn_prefill"
+    else:
+        st = lib.dar_attn_prefill_lse(ctypes.byref(shape), int(T), _ptr(q), _ptr(k), _ptr(v),
+                                      _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(lse), _ptr(ws),
+                                      wsb, _stream(stream))
+        where = "dar_attn_prefill_lse"
     if st != DAR_OK:
-        raise DarError(st, "dar_attn_prefill")
+        raise DarError(st, where)
     return (o, lse) if return_lse else o
+
+
+def dar_attn_prefill_lse(q, k, v, w_down, w_up, w, o=None, lse=None, ws=None, stream=None,
+                         check=True):
+    """dar_attn_prefill that also returns each row's log-sum-exp: (o, lse),
+    lse [B,Hq,T] fp32 (written into `lse` when given)."""
+    return dar_attn_prefill(q, k, v, w_down, w_up, w, o=o, ws=ws, stream=stream, check=check,
+                            lse=lse, return_lse=True)
 
 
 def dar_rope_table(rotary_dim, base, n_pos, device="cuda", stream=None):

@@ -292,7 +292,13 @@ size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T) {
 
 dar_status dar_attn_prefill(const dar_shape* s, int T, const void* q, const void* k,
                             const void* v, const void* w_down, const void* w_up, void* o,
-                            float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
+                            void* ws, size_t ws_bytes, hipStream_t stream) {
+    return dar_attn_prefill_lse(s, T, q, k, v, w_down, w_up, o, nullptr, ws, ws_bytes, stream);
+}
+
+dar_status dar_attn_prefill_lse(const dar_shape* s, int T, const void* q, const void* k,
+                                const void* v, const void* w_down, const void* w_up, void* o,
+                                float* lse, void* ws, size_t ws_bytes, hipStream_t stream) {
     dar_status st = check_shape(s);
     if (st != DAR_OK) return st;
     if (T < 1) return DAR_E_ARG;

@@ -29,7 +29,7 @@ def declared_functions():
 
 def test_exports_every_declared_symbol():
     names = declared_functions()
-    assert set(names) == {"dar_attn_prefill", "dar_cache_append", "dar_attn_decode",
+    assert set(names) == {"dar_attn_prefill", "dar_attn_prefill_lse", "dar_cache_append", "dar_attn_decode",
                           "dar_attn_prefill_backward", "dar_prefill_workspace_bytes",
                           "dar_decode_workspace_bytes", "dar_prefill_backward_workspace_bytes",
                           "dar_attn_prefill_chunk", "dar_prefill_chunk_workspace_bytes",
@@ -89,8 +89,15 @@ MISALIGNED = ctypes.c_void_p((1 << 20) + 2)
 
 def call_prefill(shape, T=16, q=FAKE, k=FAKE, v=FAKE, wd=FAKE, wu=None, o=FAKE, lse=None,
                  ws=FAKE, ws_bytes=1 << 30):
-    return dar.lib.dar_attn_prefill(ctypes.byref(shape), T, q, k, v, wd, wu, o, lse, ws,
-                                    ws_bytes, None)
+    if lse is None:
+        st = dar.lib.dar_attn_prefill(ctypes.byref(shape), T, q, k, v, wd, wu, o, ws, ws_bytes,
+                                      None)
+        # the lse entry point with lse = NULL validates the same way
+        assert dar.lib.dar_attn_prefill_lse(ctypes.byref(shape), T, q, k, v, wd, wu, o, None, ws,
+                                            ws_bytes, None) == st
+        return st
+    return dar.lib.dar_attn_prefill_lse(ctypes.byref(shape), T, q, k, v, wd, wu, o, lse, ws,
+                                        ws_bytes, None)
 
 
 @no_gpu

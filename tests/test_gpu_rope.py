@@ -116,26 +116,25 @@ def test_shift_invariance_on_gpu():
 
 
 @pytest.mark.parametrize("r,base", [(16, 10000.0), (64, 500000.0)])
-def test_full_size_sampled_rows(r, base):
+def test_full_size_every_row(r, base):
     """The pythia70m-shaped prefill (B8 H8 T2048 d64 d_down16 w256) with the
-    Pythia rotary fraction (16 of 64 dims) and with full rotation: sampled
-    rows against the oracle's per-row evaluation."""
+    Pythia rotary fraction (16 of 64 dims) and with full rotation: every row
+    of every head against the oracle (output NaN-filled first)."""
     wl = di.WORKLOADS["pythia70m"]
     inp = di.make_prefill_inputs(wl)
     q, k, v, wd = to_dev(inp["q"]), to_dev(inp["k"]), to_dev(inp["v"]), to_dev(inp["wd"])
     rope = dar.Rope(r, base, n_pos=wl.T)
-    o = dar.dar_attn_prefill_rope(q, k, v, wd, None, wl.w, rope)
+    o = torch.full_like(q, float("nan"))
+    dar.dar_attn_prefill_rope(q, k, v, wd, None, wl.w, rope, o=o)
     torch.cuda.synchronize()
-    rng = np.random.Generator(np.random.PCG64(5))
-    rows = np.array(sorted({0, 255, 256, 257, 1000, wl.T - 1} | set(int(x) for x in rng.integers(0, wl.T, 6))))
-    worst = 0.0
-    for b, h in ((0, 0), (7, 7), (3, 5)):
-        ref = oracle.rows_rope(inp["k"].f64[b, h], inp["v"].f64[b, h], inp["wd"].f64[h], None, wl.w,
-                               r, base, 0, rows, inp["q"].f64[b, h, rows])
-        got = to_host64(o[b, h, torch.from_numpy(rows).to(o.device)])
-        worst = max(worst, float(np.abs(got - ref).max()))
-    assert worst <= tol("bf16"), worst
-    assert torch.isfinite(o.float()).all()
+    got = to_host64(o)
+    del q, k, v, o
+    ref = oracle.prefill_rope(inp["q"].f64, inp["k"].f64, inp["v"].f64, inp["wd"].f64, None, wl.w,
+                              r, base)
+    assert np.isfinite(got).all()
+    err = np.abs(got - ref).max()
+    print("[rope r=%d] every row: max abs err %.4g" % (r, err), flush=True)
+    assert err <= tol("bf16"), err
 
 
 # ---------------------------------------------------------------- decode
