@@ -44,9 +44,10 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
-# Measured exponential rate of one CU (v_exp_f32: 8.4 cycles per wave
-# instruction, 27.6 lanes per clock per CU): 256 CUs at 2.4 GHz.
-EXP_CEILING_PER_S = 27.6 * 256 * 2.4e9
+# The exponential ceiling (v_exp_f32 results per second for the whole device,
+# at the clock the device holds under that load) is measured at the start of
+# every run by the machine microbenchmarks (paper_2606_18587_amd/k0.py,
+# include/dar_k0.h) and reported under "k0".
 ROPE_PREFILL_DIM = 16       # rotary dimension of the prefill line (Pythia: 25% of 64)
 ROPE_DECODE_DIM = 64        # full rotation on the decode line
 ROPE_BASE = 10000.0
@@ -190,6 +191,9 @@ def main():
     if args.copy_calibration:
         copy_calibration(torch, dev)
         return
+    from paper_2606_18587_amd import k0 as k0_bench
+
+    k0 = k0_bench.measure(dev)
 
     def up(t):
         if t is None:
@@ -505,10 +509,12 @@ def main():
                             "traffic": measured_traffic("decode")},
         "setup_s": round(setup_s, 1),
     }
-    # one exponential per causal pair: the distant region's bound
+    # one exponential per causal pair: the distant region's bound, against the
+    # exponential rate measured above at its own clock
     n_exp = float(pw.B * pw.Hq * (pw.T * (pw.T + 1) // 2))
     result["prefill"]["score_elems_per_s"] = n_exp / (pre_us * 1e-6)
-    result["prefill"]["frac_exp_ceiling"] = round(n_exp / (pre_us * 1e-6) / EXP_CEILING_PER_S, 4)
+    result["prefill"]["frac_exp_ceiling"] = round(n_exp / (pre_us * 1e-6) / k0["exp_per_s"], 4)
+    result["k0"] = k0
     if cold:
         cu = float(cold["prefill_ms"] * 1e3)
         result["prefill"]["cold_us"] = round(cu, 2)
@@ -585,16 +591,30 @@ def main():
     print(json.dumps(result), flush=True)
 
 
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(pw, pin, budget_s):
-    """The fp64 oracle on the host cores, on whole (batch, head) slices of the
+    """The fp64 oracle on the host cores: on whole (batch, head) slices of the
     same prefill workload, cycling over the slices until the time budget is
-    used (at least one slice)."""
+    used (at least one slice), with every OpenMP thread; then with one thread
+    on the tiny workload (whole) and on single pythia70m slices."""
+    import dar_inputs as di
     from oracle import oracle
 
     grp = pw.Hq // pw.Hkv
     pos = np.arange(pw.T)
     per_head = prefill_flops(1, 1, pw.T, pw.d, pw.dd, pw.w)
     n_slices = pw.B * pw.Hq
+    threads = oracle.num_threads()
     done = 0
     t0 = time.time()
     while done == 0 or time.time() - t0 < budget_s:
@@ -604,10 +624,29 @@ def cpu_baseline(pw, pin, budget_s):
                     pin["q"].f64[b, h])
         done += 1
     el = time.time() - t0
-    return {"value": round(done * per_head / el / 1e12, 6), "unit": "TFLOP/s",
-            "cores": oracle.num_threads(), "kind": "oracle",
-            "sample": "%d (batch, head) slices (cycling over the %d of the pythia70m prefill), "
-                      "all %d rows each, %.1f s" % (done, n_slices, pw.T, el)}
+    out = {"value": round(done * per_head / el / 1e12, 6), "unit": "TFLOP/s",
+           "cores": threads, "kind": "oracle", "cpu_model": cpu_model(),
+           "sample": "%d (batch, head) slices (cycling over the %d of the pythia70m prefill), "
+                     "all %d rows each, %.1f s, %d threads" % (done, n_slices, pw.T, el, threads)}
+
+    # one thread (the oracle's OpenMP count is left at 1 afterwards: this runs last)
+    def one_thread(inp, wl, budget):
+        sl = lambda t: t.f64[0:1, 0:1]
+        fl = prefill_flops(1, 1, wl.T, wl.d, wl.dd, wl.w)
+        n = 0
+        t1 = time.time()
+        while n == 0 or time.time() - t1 < budget:
+            oracle.prefill(sl(inp["q"]), sl(inp["k"]), sl(inp["v"]), inp["wd"].f64[0:1], None, wl.w,
+                           threads=1)
+            n += 1
+        e = time.time() - t1
+        return {"value": round(n * fl / e / 1e12, 6), "unit": "TFLOP/s", "cores": 1,
+                "sample": "%d prefills of one (batch, head) slice, %.2f s" % (n, e)}
+
+    tw = di.WORKLOADS["tiny"]
+    out["single_thread"] = {"tiny": one_thread(di.make_prefill_inputs(tw), tw, 0.5),
+                            "pythia70m": one_thread(pin, pw, 3.0)}
+    return out
 
 
 def copy_calibration(torch, dev, nbytes=1 << 28, reps=5):

@@ -15,6 +15,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libdar.so")
+K0_LIB = os.path.join(PKG, "libdar_k0.so")
+K0_SOURCE = "k0_microbench.hip"
 SOURCES = ["dar_api.hip", "latent.hip", "prefill_valu.hip", "prefill_mfma.hip", "decode.hip",
            "decode_mfma.hip", "backward.hip", "backward_mfma.hip", "rope.hip"]
 ARCH = "gfx950"
@@ -69,7 +71,25 @@ def build(verbose: bool = False) -> str:
     cmd = [_hipcc(), "--offload-arch=" + ARCH, "-shared", "-fPIC", *objs, "-o", tmp]
     subprocess.check_call(cmd)
     os.replace(tmp, LIB)
+    build_k0(verbose)
     return LIB
+
+
+def build_k0(verbose: bool = False) -> str:
+    """The machine microbenchmarks (include/dar_k0.h) as their own library:
+    they are measurement code, not part of the attention path."""
+    tmp = K0_LIB + ".tmp%d" % os.getpid()
+    cmd = [_hipcc(), *HIPCC_FLAGS, "-shared", os.path.join(CSRC, K0_SOURCE), "-o", tmp]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    p = subprocess.run(cmd, stdout=subprocess.PIPE, stderr=subprocess.STDOUT)
+    text = "\n".join(l for l in p.stdout.decode(errors="replace").splitlines()
+                     if "packed-fp32-ops" not in l)
+    if p.returncode != 0:
+        print(text, file=sys.stderr)
+        raise RuntimeError("hipcc failed for " + K0_SOURCE)
+    os.replace(tmp, K0_LIB)
+    return K0_LIB
 
 
 if __name__ == "__main__":

@@ -43,6 +43,29 @@ def test_exports_every_declared_symbol():
         assert hasattr(raw, n), n
 
 
+def test_k0_library_exports_its_header():
+    """The microbenchmark library (include/dar_k0.h) loads without a GPU and
+    exports what its header declares."""
+    text = open(os.path.join(ROOT, "include", "dar_k0.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = sorted(set(re.findall(r"\b(dar_[a-z0-9_]+)\s*\(", text)))
+    assert names == ["dar_k0_measure"]
+    from paper_2606_18587_amd import k0
+    raw = ctypes.CDLL(k0.K0_LIB_PATH)
+    for n in names:
+        assert hasattr(raw, n), n
+
+
+@no_gpu
+def test_k0_rejects_small_buffer():
+    from paper_2606_18587_amd import k0
+    lib = k0._load()
+    r = k0.DarK0Result()
+    assert lib.dar_k0_measure(FAKE, 1 << 20, ctypes.byref(r), None) == 1
+    assert lib.dar_k0_measure(None, 1 << 31, ctypes.byref(r), None) == 1
+    assert lib.dar_k0_measure(MISALIGNED, 1 << 31, ctypes.byref(r), None) == 1
+
+
 def test_status_strings():
     for st in range(6):
         assert dar.status_string(st)
