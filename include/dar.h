@@ -225,6 +225,28 @@ dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q
                            const void* w_down, const void* w_up, void* o, void* ws,
                            size_t ws_bytes, hipStream_t stream);
 
+/* dar_attn_decode for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, hosts that forbid allocation): no
+ * workspace argument. The partial records a call may need live in a
+ * fixed device array inside the library, dar_decode_noalloc_max_bytes()
+ * bytes (16 MiB) per GPU, created when the library is loaded on that GPU and
+ * held until the process ends; the call allocates nothing.
+ *   dar_decode_noalloc_bytes(s, len): bytes of that array a call at cache
+ *   length len uses (0 when one workgroup per (batch, KV head) finishes the
+ *   output itself, as at B32 Hkv8); 0 also on an invalid shape.
+ * Arguments, output and support as dar_attn_decode. Fails with
+ * DAR_E_WORKSPACE, before anything is enqueued, when the call would need
+ * more than dar_decode_noalloc_max_bytes(). Every call on one GPU shares
+ * that GPU's array: calls that overlap in time on one GPU (different streams
+ * without ordering between them) race and must not be issued; calls in one
+ * stream are ordered and safe. Nothing in the array needs to start at zero
+ * (every record a call reads, that call writes first). */
+dar_status dar_attn_decode_noalloc(const dar_shape* s, const dar_cache* c, const void* q,
+                                   const void* w_down, const void* w_up, void* o,
+                                   hipStream_t stream);
+size_t dar_decode_noalloc_bytes(const dar_shape* s, int len);
+size_t dar_decode_noalloc_max_bytes(void);
+
 /* One decode step with the rotary embedding of Eq. 3: the query q [B][Hq][d]
  * (un-rotated) sits at position c->len - 1 and cache token e at position e
  * (c->len <= rope->n_pos). The cache is the one dar_cache_append keeps (ring

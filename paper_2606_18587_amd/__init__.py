@@ -99,6 +99,12 @@ def _load():
     lib.dar_attn_prefill_ragged.argtypes = [shp, ci] + [vp] * 9 + [sz, vp]
     lib.dar_prefill_rope_workspace_bytes.restype = sz
     lib.dar_prefill_rope_workspace_bytes.argtypes = [shp, ci]
+    lib.dar_attn_decode_noalloc.restype = ci
+    lib.dar_attn_decode_noalloc.argtypes = [shp, cp, vp, vp, vp, vp, vp]
+    lib.dar_decode_noalloc_bytes.restype = sz
+    lib.dar_decode_noalloc_bytes.argtypes = [shp, ci]
+    lib.dar_decode_noalloc_max_bytes.restype = sz
+    lib.dar_decode_noalloc_max_bytes.argtypes = []
     lib.dar_status_string.restype = ctypes.c_char_p
     lib.dar_status_string.argtypes = [ci]
     return lib
@@ -412,6 +418,29 @@ def dar_attn_decode(cache: DarCache, q, w_down, w_up=None, o=None, ws=None, stre
     if st != DAR_OK:
         raise DarError(st, "dar_attn_decode")
     return o
+
+
+def dar_attn_decode_noalloc(cache: "DarCache", q, w_down, w_up=None, o=None, stream=None):
+    """One decode step as dar_attn_decode, through the entry point that takes
+    no workspace (its partial records live in a fixed array inside the
+    library). Pass `o` to keep the call free of allocation."""
+    B, Hq, d = q.shape
+    shape = make_shape(B, Hq, cache.Hkv, d, cache.d_down, cache.w, q.dtype)
+    if o is None:
+        o = torch.empty_like(q)
+    st = lib.dar_attn_decode_noalloc(ctypes.byref(shape), ctypes.byref(cache.struct), _ptr(q),
+                                     _ptr(w_down), _ptr(w_up), _ptr(o), _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_decode_noalloc")
+    return o
+
+
+def dar_decode_noalloc_bytes(shape: DarShape, length: int) -> int:
+    return int(lib.dar_decode_noalloc_bytes(ctypes.byref(shape), int(length)))
+
+
+def dar_decode_noalloc_max_bytes() -> int:
+    return int(lib.dar_decode_noalloc_max_bytes())
 
 
 def dar_attn_decode_rope(cache: "DarCache", q, w_down, rope: Rope, w_up=None, o=None, ws=None,

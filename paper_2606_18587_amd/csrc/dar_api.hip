@@ -7,6 +7,8 @@
 #include <stdio.h>
 #include <stdlib.h>
 
+#include <mutex>
+
 namespace dar {
 
 PrefillWs prefill_ws_layout(int B, int Hkv, int T, int dd, int w, size_t esize) {
@@ -488,9 +490,14 @@ dar_status dar_cache_append(const dar_shape* s, dar_cache* c, const void* k_new,
     return DAR_OK;
 }
 
-dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q,
-                           const void* w_down, const void* w_up, void* o, void* ws,
-                           size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// Arguments of one decode step over a dense split cache, apart from the
+// workspace.
+dar_status check_decode(const dar_shape* s, const dar_cache* c, const void* q, const void* w_down,
+                        const void* w_up, const void* o) {
     dar_status st = check_shape(s);
     if (st != DAR_OK) return st;
     if (!c || c->cap < 1 || c->len < 1 || c->len > c->cap) return DAR_E_ARG;
@@ -503,25 +510,90 @@ dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q
     if (decode_max_partials(s->B, s->Hkv, c->cap, s->w, s->d, s->d_down, G) > 1024)
         return DAR_E_UNSUPPORTED;
     if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
-    const size_t need = dar_decode_workspace_bytes(s, c->cap);
-    if (ws == nullptr || ws_bytes < need) return DAR_E_WORKSPACE;
-    if (!aligned16(ws)) return DAR_E_ARG;
+    return DAR_OK;
+}
 
+dar_status run_decode(const dar_shape* s, const dar_cache* c, const void* q, const void* w_down,
+                      const void* w_up, void* o, float* part, hipStream_t stream) {
     clear_hip_error();
     hipError_t e;
     if (s->dtype == DAR_BF16)
         e = launch_decode<bf16_t>((const bf16_t*)q, (const bf16_t*)w_down, (const bf16_t*)w_up,
                                   (const bf16_t*)c->k_win, (const bf16_t*)c->v_win,
                                   (const bf16_t*)c->k_lat, (const bf16_t*)c->v_lat, (bf16_t*)o,
-                                  (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, c->cap,
+                                  part, s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, c->cap,
                                   c->len, stream);
     else
         e = launch_decode<float>((const float*)q, (const float*)w_down, (const float*)w_up,
                                  (const float*)c->k_win, (const float*)c->v_win,
-                                 (const float*)c->k_lat, (const float*)c->v_lat, (float*)o,
-                                 (float*)ws, s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, c->cap,
-                                 c->len, stream);
+                                 (const float*)c->k_lat, (const float*)c->v_lat, (float*)o, part,
+                                 s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, c->cap, c->len,
+                                 stream);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+// Workspace of dar_attn_decode_noalloc: the partial records of one decode
+// call live in this file-scope device array instead of caller memory. Each
+// GPU the library runs on holds its own copy until the process ends. In host
+// code `scratch` only names the symbol: its device address on the current
+// GPU comes from hipGetSymbolAddress, looked up once per device.
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_on_device[kMaxDevices];  // null until looked up on that device
+
+hipError_t scratch_address(void** out) {
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    if (scratch_on_device[dev] == nullptr) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        scratch_on_device[dev] = p;
+    }
+    *out = scratch_on_device[dev];
+    return hipSuccess;
+}
+
+}  // namespace
+
+extern "C" {
+
+dar_status dar_attn_decode(const dar_shape* s, const dar_cache* c, const void* q,
+                           const void* w_down, const void* w_up, void* o, void* ws,
+                           size_t ws_bytes, hipStream_t stream) {
+    const dar_status st = check_decode(s, c, q, w_down, w_up, o);
+    if (st != DAR_OK) return st;
+    const size_t need = dar_decode_workspace_bytes(s, c->cap);
+    if (ws == nullptr || ws_bytes < need) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+    return run_decode(s, c, q, w_down, w_up, o, (float*)ws, stream);
+}
+
+size_t dar_decode_noalloc_max_bytes(void) { return kNoAllocScratchBytes; }
+
+size_t dar_decode_noalloc_bytes(const dar_shape* s, int len) {
+    if (check_shape(s) != DAR_OK || len < 1 || !group_supported(s)) return 0;
+    const int parts = decode_partials_at(s->B, s->Hkv, len, s->w, s->d, s->d_down, s->Hq / s->Hkv,
+                                         s->dtype == DAR_BF16);
+    return (size_t)s->B * s->Hq * parts * (2 + s->d_down + s->d) * sizeof(float);
+}
+
+dar_status dar_attn_decode_noalloc(const dar_shape* s, const dar_cache* c, const void* q,
+                                   const void* w_down, const void* w_up, void* o,
+                                   hipStream_t stream) {
+    const dar_status st = check_decode(s, c, q, w_down, w_up, o);
+    if (st != DAR_OK) return st;
+    if (dar_decode_noalloc_bytes(s, c->len) > kNoAllocScratchBytes) return DAR_E_WORKSPACE;
+    void* ws = nullptr;
+    if (scratch_address(&ws) != hipSuccess) return DAR_E_HIP;
+    return run_decode(s, c, q, w_down, w_up, o, (float*)ws, stream);
 }
 
 dar_status dar_attn_decode_rope(const dar_shape* s, const dar_cache* c, const dar_rope* rope,

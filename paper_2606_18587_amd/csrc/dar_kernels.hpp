@@ -81,6 +81,10 @@ struct DecodeSplits {
 DecodeSplits decode_splits(int len, int w, int d, int dd, int G);
 int decode_mfma_parts(int B, int Hkv, int len, int w, int d);
 int decode_max_partials(int B, int Hkv, int cap, int w, int d, int dd, int G);
+// Partial records (each 2 + d_down + d floats per query head) that one
+// launch_decode call at cache length len writes: 0 when one workgroup per
+// (batch, KV head) finishes the output itself.
+int decode_partials_at(int B, int Hkv, int len, int w, int d, int dd, int G, bool bf16);
 
 template <typename T>
 hipError_t launch_prefill_latent(const T* k, const T* v, const T* wd, T* cK, T* cVt,

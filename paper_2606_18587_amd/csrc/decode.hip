@@ -390,6 +390,16 @@ int decode_max_partials(int B, int Hkv, int cap, int w, int d, int dd, int G) {
     return m > p ? m : p;
 }
 
+int decode_partials_at(int B, int Hkv, int len, int w, int d, int dd, int G, bool bf16) {
+    // the same choice of path and split count as launch_decode below
+    if (decode_mfma_supported(d, dd, G, bf16)) {
+        const int P = decode_mfma_parts(B, Hkv, len, w, d);
+        return P > 1 ? P : 0;
+    }
+    const DecodeSplits sp = decode_splits(len, w, d, dd, G);
+    return sp.n_lat_split + sp.n_win_split;
+}
+
 template <typename T, int G>
 static hipError_t launch_decode_g(const T* q, const T* wd, const T* wu, const T* k_win,
                                   const T* v_win, const T* k_lat, const T* v_lat, T* o,

@@ -37,7 +37,9 @@ def test_exports_every_declared_symbol():
                           "dar_attn_prefill_shared", "dar_cache_append_shared",
                           "dar_attn_decode_shared", "dar_cache_append_paged",
                           "dar_attn_decode_paged", "dar_attn_prefill_ragged",
-                          "dar_prefill_rope_workspace_bytes", "dar_status_string"}
+                          "dar_prefill_rope_workspace_bytes", "dar_status_string",
+                          "dar_attn_decode_noalloc", "dar_decode_noalloc_bytes",
+                          "dar_decode_noalloc_max_bytes"}
     raw = ctypes.CDLL(dar.LIB_PATH)
     for n in names:
         assert hasattr(raw, n), n
@@ -189,6 +191,36 @@ def test_decode_rejects():
     st = dar.lib.dar_attn_decode(ctypes.byref(s3), ctypes.byref(c), FAKE, FAKE, None, FAKE, FAKE,
                                  1 << 30, None)
     assert st == dar.DAR_E_UNSUPPORTED
+
+
+def test_noalloc_decode_sizes():
+    assert dar.dar_decode_noalloc_max_bytes() == 16 << 20
+    # decode1b: one workgroup per (batch, KV head) finishes the output, no records
+    s = dar.make_shape(32, 32, 8, 64, 16, 512, torch.bfloat16)
+    assert dar.dar_decode_noalloc_bytes(s, 32768) == 0
+    # few heads and a long cache: P parts, one record of 2 + d_down + d floats per head
+    s = dar.make_shape(1, 8, 2, 64, 16, 32, torch.bfloat16)
+    n = dar.dar_decode_noalloc_bytes(s, 20000)
+    assert n > 0 and n % (8 * (2 + 16 + 64) * 4) == 0
+    assert n <= dar.dar_decode_workspace_bytes(s, 20000)
+    assert dar.dar_decode_noalloc_bytes(S(Hq=12, Hkv=4), 100) == 0  # group of 3: unsupported
+
+
+@no_gpu
+def test_noalloc_decode_rejects_beyond_its_array():
+    """A call that would need more partial records than the fixed array holds
+    is refused before anything touches HIP."""
+    s = dar.make_shape(8, 64, 8, 256, 64, 16, torch.float32)
+    need = dar.dar_decode_noalloc_bytes(s, 100000)
+    assert need > dar.dar_decode_noalloc_max_bytes()
+    c = cache_struct(cap=100000, length=100000)
+    st = dar.lib.dar_attn_decode_noalloc(ctypes.byref(s), ctypes.byref(c), FAKE, FAKE, None, FAKE,
+                                         None)
+    assert st == dar.DAR_E_WORKSPACE
+    c0 = cache_struct(cap=64, length=0)  # nothing cached yet
+    st = dar.lib.dar_attn_decode_noalloc(ctypes.byref(S()), ctypes.byref(c0), FAKE, FAKE, None,
+                                         FAKE, None)
+    assert st == dar.DAR_E_ARG
 
 
 def test_python_binding_names_match_abi():
