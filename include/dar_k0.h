@@ -14,7 +14,8 @@
  *   - v_exp_f32 rate (independent chains), in lanes per clock per compute
  *     unit at the clock measured during the same kernel;
  *   - both in one wavefront's instruction stream (8 matrix ops and 16
- *     exponentials per iteration), to see how far the two pipes overlap;
+ *     exponentials per iteration), to see how far the two pipes overlap,
+ *     and the same with 16 plain fp32 FMAs in place of the exponentials;
  *   - streaming HBM reads (16-byte loads, grid-stride) and writes over a
  *     caller-provided buffer larger than the caches;
  *   - the shader clock under load: the ratio of the shader cycle counter to
@@ -45,6 +46,8 @@ typedef struct {
     double mix_cycles_per_iter;    /* SIMD cycles per wave-iteration of 8 MFMA + 16 exp, 2 waves/SIMD */
     double mfma_only_cycles_per_iter;  /* the 8 MFMA alone, same shape       */
     double exp_only_cycles_per_iter;   /* the 16 exp alone, same shape       */
+    double fma_only_cycles_per_iter;   /* 16 v_fma_f32 alone, same shape     */
+    double mix_fma_cycles_per_iter;    /* 8 MFMA + 16 v_fma_f32 in one stream */
     double hbm_read_gbs;           /* best of the grid sizes tried           */
     double hbm_write_gbs;
 } dar_k0_result;

@@ -34,9 +34,10 @@ __device__ __forceinline__ bf16x8_t operand(float base) {
     return r;
 }
 
-// NM matrix ops and NE exponentials per loop iteration, on 4 independent
-// accumulators and 16 independent exponential chains per lane.
-template <int NM, int NE>
+// NM matrix ops and NE vector ops per loop iteration, on 4 independent
+// accumulators and 16 independent chains per lane. OP selects the vector op:
+// 0 v_exp_f32, 1 v_fma_f32.
+template <int NM, int NE, int OP = 0>
 __global__ __launch_bounds__(kThreads) void k0_pipes(float* sink, unsigned long long* clk, int iters,
                                                      float seed) {
     stamp(clk, 0);
@@ -58,7 +59,13 @@ __global__ __launch_bounds__(kThreads) void k0_pipes(float* sink, unsigned long 
         // x = 2^-x keeps every chain inside [0.5, 1]: one v_exp_f32 each
         // (the negation is a source modifier)
 #pragma unroll
-        for (int e = 0; e < NE; ++e) x[e & 15] = __builtin_amdgcn_exp2f(-x[e & 15]);
+        for (int e = 0; e < NE; ++e) {
+            if (OP == 0) {
+                x[e & 15] = __builtin_amdgcn_exp2f(-x[e & 15]);
+            } else {
+                x[e & 15] = __builtin_fmaf(x[e & 15], 0.999f, 0.0005f);
+            }
+        }
     }
     float s = 0.f;
 #pragma unroll
@@ -189,6 +196,22 @@ extern "C" int dar_k0_measure(void* buf, size_t buf_bytes, dar_k0_result* out, h
         // each SIMD runs 2 wavefronts of mix_iters iterations
         cyc[c] = ms * 1e-3 * mhz * 1e6 / (2.0 * mix_iters);
     }
+    // the same with plain fp32 FMAs instead of exponentials
+    double cf[2];
+    for (int c = 0; c < 2; ++c) {
+        const double ms = time_ms(tm, st, 3, [&] {
+            if (c == 0)
+                hipLaunchKernelGGL((k0_pipes<0, 16, 1>), dim3(n_cu * 2), dim3(kThreads), 0, st, sink,
+                                   clk, mix_iters, 1.f);
+            else
+                hipLaunchKernelGGL((k0_pipes<8, 16, 1>), dim3(n_cu * 2), dim3(kThreads), 0, st, sink,
+                                   clk, mix_iters, 1.f);
+        });
+        if (ms <= 0) return 5;
+        cf[c] = ms * 1e-3 * clock_mhz(clk, st) * 1e6 / (2.0 * mix_iters);
+    }
+    out->fma_only_cycles_per_iter = cf[0];
+    out->mix_fma_cycles_per_iter = cf[1];
     out->mix_cycles_per_iter = cyc[0];
     out->mfma_only_cycles_per_iter = cyc[1];
     out->exp_only_cycles_per_iter = cyc[2];

@@ -23,6 +23,8 @@ class DarK0Result(ctypes.Structure):
                 ("mix_cycles_per_iter", ctypes.c_double),
                 ("mfma_only_cycles_per_iter", ctypes.c_double),
                 ("exp_only_cycles_per_iter", ctypes.c_double),
+                ("fma_only_cycles_per_iter", ctypes.c_double),
+                ("mix_fma_cycles_per_iter", ctypes.c_double),
                 ("hbm_read_gbs", ctypes.c_double),
                 ("hbm_write_gbs", ctypes.c_double)]
 
@@ -60,6 +62,8 @@ def measure(device="cuda", buf_bytes=2 << 30) -> dict:
         "mix_8mfma_16exp_cycles": round(r.mix_cycles_per_iter, 1),
         "mfma8_only_cycles": round(r.mfma_only_cycles_per_iter, 1),
         "exp16_only_cycles": round(r.exp_only_cycles_per_iter, 1),
+        "fma16_only_cycles": round(r.fma_only_cycles_per_iter, 1),
+        "mix_8mfma_16fma_cycles": round(r.mix_fma_cycles_per_iter, 1),
         "hbm_read_gbs": round(r.hbm_read_gbs, 1),
         "hbm_write_gbs": round(r.hbm_write_gbs, 1),
     }
