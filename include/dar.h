@@ -96,7 +96,10 @@ typedef struct {
  *                 outside [0, n_pages) is never read or written through:
  *                 such tokens are not stored and read as zeros)
  *   lens          device int [B], tokens held per sequence (the append
- *                 advances it on the device; the host never reads it)
+ *                 advances it on the device; the library never reads it on
+ *                 the host). A negative entry -1 - n marks a sequence that
+ *                 held n tokens when an append found it at capacity
+ *                 (overflowed: not appended to or attended any more)
  *   page_size     a power of two, at least 32; capacity max_blocks *
  *                 page_size tokens per sequence */
 typedef struct {
@@ -265,14 +268,19 @@ dar_status dar_attn_decode_rope(const dar_shape* s, const dar_cache* c, const da
  * window (position lens[b] - w) is projected with W_down (Eq. 1, the same
  * arithmetic as dar_cache_append, bit-identical latents) into its page slot;
  * the new token goes to the ring; then lens[b] += 1 on the device (stream
- * order). A sequence at capacity stores nothing and keeps its length. The
- * pages of the blocks being written must be mapped in block_table. */
+ * order). A sequence found at capacity (lens[b] == max_blocks * page_size)
+ * stores nothing and is marked overflowed: lens[b] becomes -1 - lens[b]
+ * (the caller may read it back to detect the overflow); an overflowed
+ * sequence stays as it is under later appends. The pages of the blocks being
+ * written must be mapped in block_table. */
 dar_status dar_cache_append_paged(const dar_shape* s, const dar_paged_cache* c, const void* k_new,
                                   const void* v_new, const void* w_down, hipStream_t stream);
 
 /* One decode step over a paged cache: the query q [B][Hq][d] of sequence b
  * sits at position lens[b] - 1 (its own key and value already appended;
- * lens[b] >= 1). As dar_attn_decode otherwise; ws: at least
+ * lens[b] >= 1). A sequence with lens[b] < 1 (empty, or marked overflowed by
+ * the append) has no query position: its rows of o are written as NaN, the
+ * other sequences' are unaffected. As dar_attn_decode otherwise; ws: at least
  * dar_decode_workspace_bytes(s, max_blocks * page_size) bytes. Supported:
  * the matrix-core shapes (bf16, d in {64, 128}, d_down in {16, 32},
  * Hq / Hkv in {1, 2, 4, 8}). */

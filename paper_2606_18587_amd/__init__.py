@@ -542,6 +542,11 @@ class DarPagedCache:
     def cap(self):
         return self.page_size * self.max_blocks
 
+    def overflowed(self):
+        """Sequences the append found at capacity (lens marked -1 - n); reads
+        lens back to the host (synchronises with the current stream)."""
+        return [b for b, n in enumerate(self.lens.cpu().tolist()) if n < 0]
+
     def struct(self) -> DarPagedCacheStruct:
         return DarPagedCacheStruct(self.k_win.data_ptr(), self.v_win.data_ptr(),
                                    self.k_pool.data_ptr(), self.v_pool.data_ptr(),

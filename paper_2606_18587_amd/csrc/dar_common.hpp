@@ -36,9 +36,12 @@ template <> struct elem<bf16_t> {
 };
 
 // Eq. 1 for one output column: c = sum_e x[e] * W_down[e][col], fp32 fused
-// multiply-adds in increasing e. Every kernel that produces a latent goes
-// through this function, so prefill latents, bulk appends and single-token
-// appends are bit-identical.
+// multiply-adds in increasing e. The vector-ALU kernels that produce a latent
+// go through this function; on the matrix-core shapes (bf16, d 64/128,
+// d_down 16/32) every latent comes from the MFMA projection instead (a fixed
+// order too). Either way all latent producers of one shape share the same
+// arithmetic, so prefill latents, bulk appends and single-token appends are
+// bit-identical.
 template <typename T>
 __device__ __forceinline__ float project_col(const T* __restrict__ x, const T* __restrict__ wd,
                                              int d, int dd, int col) {

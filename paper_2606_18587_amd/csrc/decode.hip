@@ -255,6 +255,14 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
     // records per head: S_all, or (a paged batch) the parts this sequence's
     // length used, one per chunk tokens
     const int S = lens ? imin(S_all, imax(1, (lens[bh / Hq] + chunk - 1) / chunk)) : S_all;
+    if (lens && lens[bh / Hq] < 1) {
+        // an empty or overflowed sequence (paged batch): no query position, NaN
+        for (int e = lane_id_x(); e < d; e += 64) {
+            if (sizeof(T) == 2) reinterpret_cast<uint16_t*>(o)[(size_t)bh * d + e] = 0x7fc0;
+            else reinterpret_cast<uint32_t*>(o)[(size_t)bh * d + e] = 0x7fc00000u;
+        }
+        return;
+    }
     const int h = bh % Hq;
     const int g = h / (Hq / Hkv);
     const int lane = lane_id_x();

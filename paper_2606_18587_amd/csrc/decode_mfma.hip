@@ -331,7 +331,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     const int s = wg_id_x();  // part of this (batch, KV head), < P
     const int bg = wg_id_y();
     const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
-    const int len = PAGED ? pg.lens[b] : len_arg;  // tokens in this sequence's cache
+    const int len_raw = PAGED ? pg.lens[b] : len_arg;  // tokens in this sequence's cache
+    // (paged) an empty sequence, or one marked overflowed by the append
+    // (negative length), has no query position: its output is NaN
+    const bool dead = PAGED && len_raw < 1;
+    const int len = imax(len_raw, 0);
     // a paged (ragged) batch: this sequence uses one part per chunk tokens of
     // its own length, so a long sequence is spread over more workgroups than
     // a short one; the other parts have nothing to do (workgroup-uniform)
@@ -807,7 +811,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         float acc = mrg[h][2 + DD + e];
 #pragma unroll
         for (int c = 0; c < DD; ++c) acc = __builtin_fmaf(mrg[h][2 + c], wsh[c][e], acc);
-        o[((size_t)b * Hq + (size_t)g * G + h) * D + e] = f32_to_bf16(acc / mrg[h][1]);
+        o[((size_t)b * Hq + (size_t)g * G + h) * D + e] = dead ? (bf16_t)0x7fc0 : f32_to_bf16(acc / mrg[h][1]);
     }
 }
 

@@ -5,9 +5,12 @@
 //  * cache append: each token that leaves the window is projected into its
 //    latent slot, the newest tokens go to the ring.
 //
-// Both accumulate c[col] = sum_e x[e] * W_down[e][col] with fp32 fused
-// multiply-adds in increasing e (the order of dar::project_col), so the two
-// produce identical bits for identical inputs, however tokens are batched.
+// Both accumulate c[col] = sum_e x[e] * W_down[e][col] in fp32 in a fixed
+// order: on the vector ALUs with fused multiply-adds in increasing e
+// (dar::project_col), on the matrix cores (bf16, d 64/128, d_down 16/32) with
+// the MFMA sequence of project_mfma. Each shape takes the same one of the two
+// in the pre-pass and in every append kernel, so they produce identical bits
+// for identical inputs, however tokens are batched.
 #include "dar_common.hpp"
 #include "dar_kernels.hpp"
 
@@ -466,7 +469,11 @@ __global__ __launch_bounds__(64) void append_mfma_kernel(
     }
 }
 
-static bool mfma_projection(int d, int dd) { return (d == 64 || d == 128) && dd <= 32; }
+// The matrix-core projection is used exactly on the shapes the matrix-core
+// prefill takes (bf16, d 64/128, d_down 16/32), by the pre-pass and by every
+// append kernel alike: one projection per shape, so the latents a chunked
+// prefill attends with are the bits the cache keeps.
+static bool mfma_projection(int d, int dd) { return (d == 64 || d == 128) && (dd == 16 || dd == 32); }
 
 template <typename T>
 static hipError_t launch_prefill_latent_valu(const T* k, const T* v, const T* wd, T* cK, T* cVt,
@@ -698,7 +705,7 @@ __global__ __launch_bounds__(64) void append_paged_mfma_kernel(
     const int lane = lane_id_x();
     const int tl = lane & 31, hg = lane >> 5;
     const int len = pg.lens[b];
-    if (len >= pg.maxb * pg.ps) return;
+    if (len < 0 || len >= pg.maxb * pg.ps) return;  // overflowed, or at capacity: nothing stored
     const int ex = len - w;
     int page = -1;
     if (ex >= 0) page = pg.bt[(size_t)b * pg.maxb + ex / pg.ps];
@@ -743,7 +750,7 @@ __global__ __launch_bounds__(64) void append_paged_kernel(
     const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
     const int lane = lane_id_x();
     const int len = pg.lens[b];
-    if (len >= pg.maxb * pg.ps) return;
+    if (len < 0 || len >= pg.maxb * pg.ps) return;  // overflowed, or at capacity: nothing stored
     const int ex = len - w;
     int page = -1;
     if (ex >= 0) page = pg.bt[(size_t)b * pg.maxb + ex / pg.ps];
@@ -763,9 +770,16 @@ __global__ __launch_bounds__(64) void append_paged_kernel(
     }
 }
 
+// A sequence whose token could not be stored (at capacity) is marked as
+// overflowed: its length becomes -1 - len (the held length stays readable),
+// later appends leave it alone and the decode writes NaN for it.
 __global__ __launch_bounds__(64) void lens_advance_kernel(int* __restrict__ lens, int B, int cap) {
     const int b = wg_id_x() * 64 + lane_id_x();
-    if (b < B && lens[b] < cap) lens[b] += 1;
+    if (b < B) {
+        const int len = lens[b];
+        if (len >= 0 && len < cap) lens[b] = len + 1;
+        else if (len >= cap) lens[b] = -1 - len;
+    }
 }
 
 template <typename T>

@@ -35,6 +35,22 @@ def run_gpu(inp, w):
     return [None if g is None else to_host64(g) for g in grads]
 
 
+# Elementwise check beside the normwise one: max over elements of
+# |got - ref| / (tol * max(1, |ref|)), asserted against ELEM_BOUND[tensor].
+# dq, dk, dv: the bf16 rounding points of the matrix-core backward (q~, dO~,
+# c^K, c^V, P, dS, delta from the bf16 o), modelled in numpy without the GPU,
+# give 0.94 on the hardest case; the kernels measured at most 1.24 over every
+# case here (dk, untied W_up, w = 0); 1.4 leaves ~13 % for drift.
+# dW_down, dW_up: every entry is a sum over all B*T rows whose small entries
+# come from cancellation (the exact value is the difference of terms hundreds
+# of times larger), so their elementwise ratio measures the rounding of the
+# summands rather than the entry: measured at most 9.4 (w = 0); the normwise
+# check (<= 0.26 measured) is the meaningful one there, and 12 still catches
+# a lost or doubled term.
+ELEM_BOUND = {"dq": 1.4, "dk": 1.4, "dv": 1.4, "dwd": 12.0, "dwu": 12.0}
+ELEM_WORST = {}
+
+
 def compare(got, ref, dtype, what="", scale=1.0):
     t = tol(dtype) * scale
     names = ("dq", "dk", "dv", "dwd", "dwu")
@@ -47,9 +63,13 @@ def compare(got, ref, dtype, what="", scale=1.0):
         assert np.isfinite(a).all(), what + " " + n + " not finite"
         err = np.abs(a - b)
         ratio = err.max() / (t * max(1.0, np.abs(b).max()))
+        elem = (err / (t * np.maximum(1.0, np.abs(b)))).max()
         worst[n] = ratio
-        assert ratio <= 1.0, "%s %s: error %.3g of the bound (max abs err %.3g)" % (
+        worst[n + "_elem"] = elem
+        ELEM_WORST[n] = max(ELEM_WORST.get(n, 0.0), float(elem))
+        assert ratio <= 1.0, "%s %s: error %.3g of the normwise bound (max abs err %.3g)" % (
             what, n, ratio, err.max())
+        assert elem <= ELEM_BOUND[n], "%s %s: elementwise error %.3g of the bound" % (what, n, elem)
     return worst
 
 

@@ -109,6 +109,9 @@ def test_bf16_d64_chunk_after_prefix(w, L, n):
     (di.Workload("chunk_d128", 21, 1, 8, 2, 0, 128, 32, 64, "bf16"), 257, 190, True),
     (di.Workload("chunk_d64_32", 22, 1, 4, 4, 0, 64, 32, 48, "bf16"), 130, 70, False),
     (di.Workload("chunk_generic", 23, 1, 2, 1, 0, 80, 20, 24, "bf16"), 90, 41, False),
+    # d 64 with d_down 8: the pre-pass and the appends must take the same
+    # (vector-ALU) projection for the cache to be byte-equal to appends
+    (di.Workload("chunk_d64_dd8", 25, 1, 4, 2, 0, 64, 8, 40, "bf16"), 150, 60, False),
 ])
 def test_other_shapes(wl, L, n, untied):
     run_chunks(wl.with_(T=L + n), [n], untied=untied, prefix=[L], check_lse=True)

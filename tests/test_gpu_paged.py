@@ -166,10 +166,12 @@ def test_long_sequences_several_workgroups():
     r.check_decode(1, heads_per_seq=[0, 5])
 
 
-def test_sequence_at_capacity_stores_nothing():
-    """A sequence whose blocks are all used keeps its length and its cache."""
+def test_sequence_at_capacity_is_marked_overflowed():
+    """A sequence whose blocks are all used stores nothing, is marked
+    overflowed (lens = -1 - cap), stays so under a later append, and decodes
+    to NaN; the other sequence appends and decodes as usual (oracle row)."""
     wl = WL.with_(w=16)
-    r = Ragged(wl, [64, 10], 32, extra_blocks=0, steps=1)
+    r = Ragged(wl, [64, 10], 32, extra_blocks=0, steps=2)
     # sequence 0 holds exactly max_blocks * page_size tokens: fill it to capacity
     cap = r.pc.cap
     r.pc.lens[0] = cap
@@ -177,11 +179,40 @@ def test_sequence_at_capacity_stores_nothing():
     k, v = r.step_tokens(0)
     dar.dar_cache_append_paged(r.pc, k, v, r.wdd, Hq=wl.Hq)
     torch.cuda.synchronize()
-    assert r.pc.lens.cpu().tolist() == [cap, 11]
+    assert r.pc.lens.cpu().tolist() == [-1 - cap, 11]
+    assert r.pc.overflowed() == [0]
     # only sequence 1's page rows may have changed
     after = raw(r.pc.k_pool)
     changed = np.unique(np.nonzero((before != after).any(axis=(1, 2, 3)))[0])
     assert set(changed.tolist()) <= set(int(p) for p in r.bt[1] if p >= 0)
+    k, v = r.step_tokens(1)
+    dar.dar_cache_append_paged(r.pc, k, v, r.wdd, Hq=wl.Hq)
+    torch.cuda.synchronize()
+    assert r.pc.lens.cpu().tolist() == [-1 - cap, 12]
+    assert np.array_equal(raw(r.pc.k_pool)[[p for p in r.bt[0] if p >= 0]],
+                          before[[p for p in r.bt[0] if p >= 0]])
+    g = np.random.Generator(np.random.PCG64(71))
+    q = di.Tensor(g.standard_normal((2, wl.Hq, wl.d), dtype=np.float32), "bf16")
+    o = to_host64(dar.dar_attn_decode_paged(r.pc, to_dev(q), r.wdd))
+    assert np.isnan(o[0]).all()
+    grp = wl.Hq // wl.Hkv
+    for h in range(wl.Hq):
+        gg = h // grp
+        ref = oracle.rows(r.k[1].f64_slice(gg)[:12], r.v[1].f64_slice(gg)[:12], r.wd.f64[gg], None,
+                          wl.w, [11], q.f64[1, h][None])
+        assert np.abs(o[1, h] - ref[0]).max() <= tol("bf16")
+
+
+@pytest.mark.parametrize("long_len", [100, 20000])
+def test_empty_sequence_decodes_to_nan(long_len):
+    """lens[b] = 0 (no query position): NaN rows for that sequence only, with
+    one workgroup per (sequence, KV head) and with split records merged."""
+    r = Ragged(WL, [long_len, 0, 37], 64, steps=1)
+    g = np.random.Generator(np.random.PCG64(72))
+    q = di.Tensor(g.standard_normal((3, WL.Hq, WL.d), dtype=np.float32), "bf16")
+    o = to_host64(dar.dar_attn_decode_paged(r.pc, to_dev(q), r.wdd))
+    assert np.isnan(o[1]).all()
+    assert np.isfinite(o[0]).all() and np.isfinite(o[2]).all()
 
 
 def test_full_size_ragged_decode1b():
