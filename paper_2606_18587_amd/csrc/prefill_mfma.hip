@@ -138,7 +138,9 @@ struct SoftmaxState {
 
 // One 32-key subtile of the online softmax on x[16] (already relative to the
 // reference). Returns P^T as two bf16x8 operands; rescales ow/ol if needed.
-template <int NT, bool SUM_VALU>
+// OL: the latent accumulator ol is still separate (distant region); after
+// it has been lifted into ow (window region) only ow is rescaled.
+template <int NT, bool SUM_VALU, bool OL = true>
 __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x16_t (&ow)[NT],
                                              f32x16_t& ol, bf16x8_t& p0, bf16x8_t& p1,
                                              f32x16_t* xnext = nullptr) {
@@ -158,8 +160,10 @@ __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x
         for (int t = 0; t < NT; ++t)
 #pragma unroll
             for (int r = 0; r < 16; ++r) ow[t][r] *= fac;
+        if (OL) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) ol[r] *= fac;
+            for (int r = 0; r < 16; ++r) ol[r] *= fac;
+        }
         st.l *= fac;
         if (need) st.m = fresh ? mx : st.m + delta;
         st.cm = (st.m == -INFINITY) ? 0.f : -st.m;
@@ -236,7 +240,7 @@ __device__ __forceinline__ const bf16_t* uniform_ptr(const bf16_t* p) {
 }
 
 // Distant region: subtiles of 32 keys [0, js_last] against the latents of
-// the pre-pass. With d = 64, d_down = 16 it is software pipelined: the scores of subtile n+1 are on the
+// the pre-pass, software pipelined: the scores of subtile n+1 are on the
 // matrix cores while the exponentials of subtile n run, so neither unit
 // waits for the other. Latent keys are loaded three subtiles ahead, values
 // three ahead of their use, through buffer loads whose subtile offset is a
@@ -302,28 +306,6 @@ __device__ __forceinline__ void distant_region(const RowCtx& c, const bf16_t* __
         ol = mfma(vt.v[0], p0, ol);
         ol = mfma(vt.v[1], p1, ol);
     };
-    if constexpr (D != 64 || DD != 16) {
-        // wider heads: no room for the pipeline's registers; two subtiles of
-        // loads in flight, scores and exponentials in sequence
-        KT ka = loadK(0), kb = loadK(1);
-        VT va = loadV(0), vb = loadV(1);
-        int n = 0;
-        for (; n + 1 < n_sub; n += 2) {
-            f32x16_t x = scores(n, ka);
-            ka = loadK(n + 2);
-            finish(x, va, nullptr);
-            va = loadV(n + 2);
-            x = scores(n + 1, kb);
-            kb = loadK(n + 3);
-            finish(x, vb, nullptr);
-            vb = loadV(n + 3);
-        }
-        if (n < n_sub) {
-            f32x16_t x = scores(n, ka);
-            finish(x, va, nullptr);
-        }
-        return;
-    }
     KT ka = loadK(0), kb = loadK(1), kc = loadK(2);
     VT va = loadV(0), vb = loadV(1), vc = loadV(2);
     f32x16_t x = scores(0, ka);
@@ -430,7 +412,7 @@ __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t
                 }
                 bf16x8_t p0, p1;
                 if (FIXED) exp_pack<true>(x, st.l, p0, p1);
-                else softmax_step<NT, true>(x, st, ow, ol, p0, p1);
+                else softmax_step<NT, true, false>(x, st, ow, ol, p0, p1);
                 // O_win^T += V^T P^T; V^T operand via transposing LDS reads
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
@@ -528,7 +510,7 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
                 }
                 bf16x8_t p0, p1;
                 if (FIXED) exp_pack<true>(x, st.l, p0, p1);
-                else softmax_step<NT, true>(x, st, ow, ol, p0, p1);
+                else softmax_step<NT, true, false>(x, st, ow, ol, p0, p1);
                 // O_win^T += V^T P^T; V^T operand via transposing LDS reads
 #pragma unroll
                 for (int t = 0; t < NT; ++t) {
@@ -607,11 +589,15 @@ void prefill_mfma_kernel(
     // workgroups of a head are placed on one XCD so its L2 holds only the
     // K/V/latents of BH/8 heads.
     int pair, bh;
-    if ((BH & 7) == 0) {
+    const int G = Hq / Hkv;
+    const int BG = BH / G;  // (batch, KV head) groups
+    if ((BG & 7) == 0) {
+        // the G query heads of a KV head share its XCD (and its L2)
         const int xcd = wg_id_x() & 7, local = wg_id_x() >> 3;
-        const int hpx = BH >> 3;  // heads per XCD
+        const int hpx = BH >> 3;  // query heads per XCD
         pair = local / hpx;
-        bh = (local - pair * hpx) * 8 + xcd;
+        const int rem = local - pair * hpx;
+        bh = ((rem / G) * 8 + xcd) * G + rem % G;
     } else {
         pair = wg_id_x() / BH;
         bh = wg_id_x() - pair * BH;
@@ -823,24 +809,9 @@ void prefill_mfma_kernel(
             if (fixed) distant_region<D, DD, true>(c, cK, cVt, qtop, js_last, st, ow, ol);
             else distant_region<D, DD, false>(c, cK, cVt, qtop, js_last, st, ow, ol);
         }
-        // ------------------------------------------------------------ local region
-        if (has_local) {
-            if constexpr (D > 64) {
-                if (fixed) local_region_1deep<D, DD, NW, true>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
-                else local_region_1deep<D, DD, NW, false>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
-            } else {
-                if (fixed) local_region<D, DD, NW, true>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
-                else local_region<D, DD, NW, false>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
-            }
-        }
-
-        if (c.r0 >= Tb) continue;
-
-        // ------------------------------------------------------------ epilogue
-        float lt = st.l;
-        if (DD == 16 && !ROPE) lt += ol[8];  // ones row (row 16, held by lanes of half 0)
-        lt = pair_sum(lt);
-
+        // The latent part is complete: lift it now (Eq. 2 by linearity), so the
+        // window region below carries ow only.
+        if (DD == 16 && !ROPE) st.l += ol[8];  // ones row (row 16, held by lanes of half 0)
         if (jd_end >= 0 && !ROPE) {
             // O^T += W_up^T O_lat^T, O_lat split into bf16 hi + lo parts
 #pragma unroll
@@ -871,6 +842,23 @@ void prefill_mfma_kernel(
                 }
             }
         }
+
+
+        // ------------------------------------------------------------ local region
+        if (has_local) {
+            if constexpr (D > 64) {
+                if (fixed) local_region_1deep<D, DD, NW, true>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+                else local_region_1deep<D, DD, NW, false>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+            } else {
+                if (fixed) local_region<D, DD, NW, true>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+                else local_region<D, DD, NW, false>(c, k, v, lds_k, lds_v, qop, i0, iwg_hi, st, ow, ol);
+            }
+        }
+
+        if (c.r0 >= Tb) continue;
+
+        // ------------------------------------------------------------ epilogue
+        const float lt = pair_sum(st.l);
 
         if (i < Tb) {
             // log of the row's softmax denominator (natural log), for a backward pass
