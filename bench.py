@@ -172,6 +172,8 @@ def main():
                     help="skip the prefill and decode with a single shared latent")
     ap.add_argument("--no-cold", action="store_true",
                     help="skip the cold-cache timings")
+    ap.add_argument("--no-launch", action="store_true",
+                    help="skip the host launch-cost and graph-replay measurement")
     ap.add_argument("--cpu-seconds", type=float, default=12.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a plain device copy of known size (HBM counter calibration)")
@@ -430,8 +432,14 @@ def main():
     # the other prefill configurations), each timed the same way; not part of `value`
     other = {}
     if not args.no_other_prefill:
-        for name in ("pythia410m_w128", "pythia410m_w512", "long16k"):
-            ow_ = di.WORKLOADS[name]
+        # pythia70m_dd32: the same batch with d_down 32, the distant width of the
+        # decoupled-rotary cache the paper's Limitations section names (latent
+        # 16 + an uncompressed rotary key part of 16, the Pythia rotary width):
+        # the cost of absorbing W_up with a rotary model, against the rotary
+        # line below that lifts the distant keys to full d
+        for name in ("pythia410m_w128", "pythia410m_w512", "long16k", "pythia70m_dd32"):
+            ow_ = (di.WORKLOADS["pythia70m"].with_(name=name, dd=32) if name == "pythia70m_dd32"
+                   else di.WORKLOADS[name])
             oin = di.make_prefill_inputs(ow_)
             oq, ok_, ov, owd = (up(oin[x]) for x in ("q", "k", "v", "wd"))
             del oin
@@ -472,6 +480,10 @@ def main():
         btf = bflops / (bwd_us * 1e-6) / 1e12
         bwd = {"us": round(bwd_us, 2), "tflops": round(btf, 2),
                "frac_bf16_peak": round(btf / PEAK_BF16_TFLOPS, 4), "alg_flop": bflops}
+
+    launch = None
+    if not args.no_launch:
+        launch = launch_cost(torch, dar, q, k, v, wd, o, ws, shape, pw, args.steps)
 
     result = {
         "metric": "DAR prefill TFLOP/s + decode KV GB/s, as fraction of MI355X peak, 1 GPU",
@@ -577,6 +589,8 @@ def main():
         result["prefill_other"] = other
     if chunk is not None:
         result["prefill_chunk"] = chunk
+    if launch is not None:
+        result["launch"] = launch
     if bwd is not None:
         result["backward"] = bwd
         result["roofline_backward"] = {
@@ -589,6 +603,73 @@ def main():
         result["cpu_baseline"] = cpu_baseline(pw, pin, args.cpu_seconds)
 
     print(json.dumps(result), flush=True)
+
+
+def launch_cost(torch, dar, q, k, v, wd, o, ws, shape, pw, n):
+    """Host cost of one prefill call and the GPU time of a graph replay.
+    host_us_binding: the Python binding (argument checks off) per call;
+    host_us_c_abi: the bare C ABI call (ctypes, arguments prepared once):
+    validation and two kernel launches; both measured with the GPU kept busy
+    so no call waits for it. graph_us: GPU time per replay of a HIP graph
+    holding one prefill (pre-pass and attention kernel), back to back, beside
+    eager_us, the same calls enqueued eagerly."""
+    import ctypes
+
+    n = max(n, 20)
+    st = torch.cuda.current_stream()
+    wsb = ws.numel()
+    args_c = (ctypes.byref(shape), pw.T, ctypes.c_void_p(q.data_ptr()), ctypes.c_void_p(k.data_ptr()),
+              ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(wd.data_ptr()), None,
+              ctypes.c_void_p(o.data_ptr()), ctypes.c_void_p(ws.data_ptr()), wsb,
+              ctypes.c_void_p(st.cuda_stream))
+    torch.cuda.synchronize()
+    torch.cuda._sleep(int(2.4e9 * 2e-3 * n))
+    t0 = time.perf_counter()
+    for _ in range(n):
+        dar.dar_attn_prefill(q, k, v, wd, None, pw.w, o=o, ws=ws, check=False)
+    t1 = time.perf_counter()
+    for _ in range(n):
+        rc = dar.lib.dar_attn_prefill(*args_c)
+    t2 = time.perf_counter()
+    assert rc == 0, rc
+    torch.cuda.synchronize()
+    # one prefill captured into a graph (no memset or allocation inside)
+    g = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    cs.wait_stream(st)
+    with torch.cuda.stream(cs):
+        dar.dar_attn_prefill(q, k, v, wd, None, pw.w, o=o, ws=ws, check=False)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=cs):
+            dar.dar_attn_prefill(q, k, v, wd, None, pw.w, o=o, ws=ws, check=False)
+    st.wait_stream(cs)
+    torch.cuda.synchronize()
+
+    def gpu_time(fn):
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(2.4e9 * 1e-3 * n))
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n * 1e3
+
+    graph_us = gpu_time(g.replay)
+    eager_us = gpu_time(lambda: dar.dar_attn_prefill(q, k, v, wd, None, pw.w, o=o, ws=ws,
+                                                     check=False))
+    t3 = time.perf_counter()
+    for _ in range(n):
+        g.replay()
+    t4 = time.perf_counter()
+    torch.cuda.synchronize()
+    del g
+    return {"host_us_binding": round((t1 - t0) / n * 1e6, 2),
+            "host_us_c_abi": round((t2 - t1) / n * 1e6, 2),
+            "host_us_graph_replay": round((t4 - t3) / n * 1e6, 2),
+            "graph_us": round(graph_us, 2), "eager_us": round(eager_us, 2), "calls": n}
 
 
 def cpu_model():

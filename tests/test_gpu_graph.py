@@ -1,0 +1,71 @@
+"""The prefill and the decode captured into a HIP graph (through torch's graph
+capture on the current stream) and replayed: every replay, with eager work
+and synchronisations in between, must give the eager call's bits. Nothing in
+these entry points allocates, memsets or synchronises, so they can be
+captured."""
+import numpy as np
+import pytest
+import torch
+
+import dar_inputs as di
+from tests.dev import to_dev
+
+pytestmark = pytest.mark.gpu
+
+dar = pytest.importorskip("paper_2606_18587_amd")
+
+
+def bits(x):
+    return x.detach().cpu().view(torch.int16).numpy().copy()
+
+
+def replay_matches(run, out):
+    """Capture run() (which writes `out`), replay it three times with eager
+    work between the replays; each replay must reproduce the eager bits."""
+    run()
+    torch.cuda.synchronize()
+    ref = bits(out)
+    g = torch.cuda.CUDAGraph()
+    cs = torch.cuda.Stream()
+    cs.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(cs):
+        with torch.cuda.graph(g, stream=cs):
+            run()
+    torch.cuda.current_stream().wait_stream(cs)
+    torch.cuda.synchronize()
+    scratch = torch.zeros(1 << 20, device="cuda")
+    for rep in range(3):
+        out.fill_(float("nan"))        # eager work between replays
+        scratch.add_(1.0)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(bits(out), ref), "replay %d differs" % rep
+
+
+@pytest.mark.parametrize("w", [0, 64])
+def test_prefill_graph_replay(w):
+    wl = di.Workload("graph_pf", 70, 2, 4, 2, 700, 64, 16, w, "bf16")
+    inp = di.make_prefill_inputs(wl)
+    q, k, v, wd = (to_dev(inp[x]) for x in ("q", "k", "v", "wd"))
+    o = torch.empty_like(q)
+    shape = dar.make_shape(wl.B, wl.Hq, wl.Hkv, wl.d, wl.dd, wl.w, torch.bfloat16)
+    ws = torch.empty(dar.dar_prefill_workspace_bytes(shape, wl.T), dtype=torch.uint8, device="cuda")
+    replay_matches(lambda: dar.dar_attn_prefill(q, k, v, wd, None, wl.w, o=o, ws=ws), o)
+
+
+@pytest.mark.parametrize("L0", [300, 20000])
+def test_decode_graph_replay(L0):
+    """Decode over a fixed cache (one workgroup per (batch, KV head) at the
+    short length; split records and the combine kernel at the long one)."""
+    wl = di.Workload("graph_dec", 71, 1, 8, 2, 0, 64, 16, 32, "bf16", kind="decode")
+    pre = di.make_decode_prefix(wl, L0)
+    c = dar.DarCache(wl.B, wl.Hkv, wl.d, wl.dd, wl.w, L0, torch.bfloat16)
+    wd = to_dev(pre["wd"])
+    dar.dar_cache_append(c, to_dev(pre["k"]), to_dev(pre["v"]), wd, Hq=wl.Hq)
+    q = to_dev(di.make_decode_step(wl, 0)["q"])
+    o = torch.empty_like(q)
+    shape = dar.make_shape(wl.B, wl.Hq, wl.Hkv, wl.d, wl.dd, wl.w, torch.bfloat16)
+    ws = torch.empty(dar.dar_decode_workspace_bytes(shape, c.cap), dtype=torch.uint8, device="cuda")
+    replay_matches(lambda: dar.dar_attn_decode(c, q, wd, o=o, ws=ws), o)
+    replay_matches(lambda: dar.dar_attn_decode_noalloc(c, q, wd, o=o), o)
