@@ -393,6 +393,29 @@ def main():
         for i in range(args.warmup):
             run_rd(i)
         rope["decode_ms"] = timed(run_rd, args.steps)
+        # d = 128 heads: a cache of the long16k shape (batch 8) filled with
+        # seeded N(0,1) ring entries and latents, the plain decode beside it
+        B8, H8, K8, D8, DD8, W8, L8 = 8, 32, 8, 128, 32, 1024, 16384
+        g8 = torch.Generator(device=dev).manual_seed(260618593)
+        c8 = dar.DarCache(B8, K8, D8, DD8, W8, L8, torch.bfloat16, device=dev)
+        for t in (c8.k_win, c8.v_win, c8.k_lat, c8.v_lat):
+            t.copy_(torch.randn(t.shape, device=dev, generator=g8))
+        c8.struct.len = L8
+        q8 = torch.randn(B8, H8, D8, device=dev, generator=g8).bfloat16()
+        wd8 = (torch.randn(K8, D8, DD8, device=dev, generator=g8) / D8 ** 0.5).bfloat16()
+        o8 = torch.empty_like(q8)
+        sh8 = dar.make_shape(B8, H8, K8, D8, DD8, W8, torch.bfloat16)
+        ws8 = torch.empty(dar.dar_decode_workspace_bytes(sh8, L8), dtype=torch.uint8, device=dev)
+        rd8 = dar.Rope(ROPE_DECODE_DIM, ROPE_BASE, n_pos=L8, device=dev)
+        run_r8 = lambda i: dar.dar_attn_decode_rope(c8, q8, wd8, rd8, o=o8, ws=ws8)
+        run_p8 = lambda i: dar.dar_attn_decode(c8, q8, wd8, None, o=o8, ws=ws8)
+        for i in range(args.warmup):
+            run_r8(i)
+            run_p8(i)
+        rope["d128_decode_ms"] = timed(run_r8, args.steps)
+        rope["d128_plain_ms"] = timed(run_p8, args.steps)
+        rope["d128_bytes"] = decode_bytes(B8, H8, K8, D8, DD8, W8, L8)
+        del c8, ws8
 
     # chunked prefill into the same decode cache: chunks of CHUNK_N new tokens
     # (seeded N(0,1) queries, keys and values; the same tensors each call, at
@@ -585,6 +608,15 @@ def main():
             "shape": "decode1b cache, rotary dim %d, base %g" % (ROPE_DECODE_DIM, ROPE_BASE),
             "us": round(rdu, 2), "gbs": round(dbytes / (rdu * 1e-6) / 1e9, 1),
             "frac_hbm_peak": round(dbytes / (rdu * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        b8 = rope["d128_bytes"]
+        r8, p8 = float(rope["d128_decode_ms"] * 1e3), float(rope["d128_plain_ms"] * 1e3)
+        result["decode_rope_d128"] = {
+            "shape": "B8 Hq32 Hkv8 d128 d_down32 w1024, 16384 cached tokens, rotary dim %d, "
+                     "base %g" % (ROPE_DECODE_DIM, ROPE_BASE),
+            "us": round(r8, 2), "alg_bytes": b8, "gbs": round(b8 / (r8 * 1e-6) / 1e9, 1),
+            "frac_hbm_peak": round(b8 / (r8 * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+            "plain_decode_us": round(p8, 2),
+            "plain_frac_hbm_peak": round(b8 / (p8 * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     if other:
         result["prefill_other"] = other
     if chunk is not None:

@@ -120,14 +120,14 @@ hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* w
                               int d, int dd, int w, int cap, int len, int& P, hipStream_t st,
                               const bf16_t* wv = nullptr);
 
-// The same kernel with the rotary embedding of Eq. 3 (d = 64, rotary
+// The same kernel with the rotary embedding of Eq. 3 (d 64 or 128, rotary
 // dimension 16, 32 or 64); tab [n_pos][r].
 bool decode_mfma_rope_supported(int d, int dd, int G, int r, bool bf16);
 hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
                                    const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_lat,
                                    const bf16_t* v_lat, const float* tab, int n_pos, float* part,
                                    bf16_t* o, int B, int Hq, int Hkv, int dd, int w, int cap,
-                                   int len, int r, int& P, hipStream_t st);
+                                   int len, int r, int& P, hipStream_t st, int d);
 // The same kernel over a paged cache with per-sequence lengths (bf16 shapes
 // of decode_mfma_supported); P from the largest possible length.
 hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,

@@ -316,8 +316,16 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     bf16_t* __restrict__ o, int Hq, int Hkv, int w, int cap, int len_arg, int P, float qscale,
     const float* __restrict__ tab, int n_pos, const bf16_t* __restrict__ wv, PagedArgs pg,
     const int* __restrict__ block_table) {
-    static_assert(R == 0 || (D == 64 && R % 16 == 0 && R <= D), "rotary: d = 64, R a multiple of 16");
+    static_assert(R == 0 || ((D == 64 || D == 128) && R % 16 == 0 && R <= 64),
+                  "rotary: d 64 or 128, R a multiple of 16 up to 64");
     constexpr int KS = D / 16, DS = DD / 16, NT = D / 32;
+    // With rotation only elements [0, R) of a lifted distant key turn, R <= 64:
+    // the first 64 elements are lifted and rotated per subtile (NL tiles of
+    // 32, KL query slabs against them); with D = 128 elements [64, 128) are
+    // not rotated, so their part of the score stays absorbed in the query,
+    // (q_hi W_up,hi^T) . c, one more MFMA on the latent rows as loaded.
+    constexpr int NL = R > 0 ? 2 : NT, KL = R > 0 ? 4 : KS;
+    constexpr int QK0 = R > 0 ? (D > 64 ? 4 : KS) : 0;  // first query slab absorbed
     constexpr int LDW = D + 8;                      // padded ring row in LDS (bf16)
     constexpr int VBUF = 32 * LDW;                  // per-wave V staging (bf16 elements)
     constexpr int stride = 2 + DD + D;              // partial record {m, l, acc_lat, acc_win}
@@ -386,7 +394,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     dbf16x8 qop[KS];
     // with rotation: the query rotated at len - 1 (fp32 until packed); qopr is
     // its scaled operand in the element order of the lifted keys' registers
-    dbf16x8 qopr[R > 0 ? KS : 1];
+    dbf16x8 qopr[R > 0 ? KL : 1];
     if constexpr (R == 0) {
 #pragma unroll
         for (int k = 0; k < KS; ++k) qop[k] = hval ? ld8(qrow + k * 16 + hg * 8) : zero8();
@@ -404,8 +412,9 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         }
         rotate_slabs<KS, R>(qf, tab + (size_t)(len - 1) * R, hg);
 #pragma unroll
-        for (int k = 0; k < KS; ++k) {
-            qop[k] = pk8(qf[k]);
+        for (int k = 0; k < KS; ++k) qop[k] = pk8(qf[k]);
+#pragma unroll
+        for (int k = 0; k < KL; ++k) {
             // element order 16k + (j < 4 ? 4hg + j : 8 + 4hg + j - 4): swap
             // the middle quads across the lane halves
             float v8[8];
@@ -489,12 +498,13 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         // ---- q~^T = W_up q^T, scaled; rearranged from the accumulator layout
         // (lane half g holds columns 4g..4g+3, 8+4g..8+4g+3 of each 16) to the
         // B-operand layout (half g holds 8g..8g+7) with one swap across halves.
-        // (Not with rotation: the keys are lifted instead.)
+        // (With rotation only slabs QK0.. not touched by it: the keys are lifted
+        // instead for the rotated ones.)
         const bf16_t* wdg = wd + (size_t)g * D * DD;
         const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
         df32x16 qt = fill16(0.f);
 #pragma unroll
-        for (int k = 0; k < (R > 0 ? 0 : KS); ++k) {
+        for (int k = QK0; k < KS; ++k) {
             dbf16x8 a = zero8();
             if (col < DD) {
                 if (wug) {
@@ -526,11 +536,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         // 8 hg + j = latent column 16 s2 + 8 hg + j) and the lane's offset
         // angles (token prow of the subtile) for its rotated pairs
         constexpr int NP = R / 4;  // rotated pairs per lane
-        dbf16x8 aU[R > 0 ? NT : 1][R > 0 ? DS : 1];
+        dbf16x8 aU[R > 0 ? NL : 1][R > 0 ? DS : 1];
         float co[NP > 0 ? NP : 1], so[NP > 0 ? NP : 1];
         if constexpr (R > 0) {
 #pragma unroll
-            for (int t = 0; t < NT; ++t)
+            for (int t = 0; t < NL; ++t)
 #pragma unroll
                 for (int s2 = 0; s2 < DS; ++s2) {
                     uint16_t e8[8];
@@ -576,9 +586,9 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             } else {
                 // K'^T tiles: lane = token prow, register 4 mm + i of tile t =
                 // element 32 t + 8 mm + 4 hg + i
-                df32x16 kx[NT];
+                df32x16 kx[NL];
 #pragma unroll
-                for (int t = 0; t < NT; ++t) {
+                for (int t = 0; t < NL; ++t) {
                     kx[t] = mma(aU[t][0], ak[0], fill16(0.f));
 #pragma unroll
                     for (int s2 = 1; s2 < DS; ++s2) kx[t] = mma(aU[t][s2], ak[s2], kx[t]);
@@ -603,11 +613,15 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
                 }
                 x = mma(ones_a, st.negm, fill16(0.f));
 #pragma unroll
-                for (int k = 0; k < KS; ++k) {
+                for (int k = 0; k < KL; ++k) {
                     float a8[8];
 #pragma unroll
                     for (int j = 0; j < 8; ++j) a8[j] = kx[k / 2][8 * (k % 2) + j];
                     x = mma(pk8(a8), qopr[k], x);
+                }
+                if constexpr (D > 64) {  // the unrotated half, absorbed
+#pragma unroll
+                    for (int k = 0; k < DS; ++k) x = mma(ak[k], qtop[k], x);
                 }
             }
             if (t0 + 31 > last) {
@@ -870,7 +884,7 @@ hipError_t launch_decode_mfma(const bf16_t* q, const bf16_t* wd, const bf16_t* w
 }
 
 bool decode_mfma_rope_supported(int d, int dd, int G, int r, bool bf16) {
-    return bf16 && d == 64 && (dd == 16 || dd == 32) && G >= 1 && G <= kDecMaxGroup &&
+    return bf16 && (d == 64 || d == 128) && (dd == 16 || dd == 32) && G >= 1 && G <= kDecMaxGroup &&
            (r == 16 || r == 32 || r == 64);
 }
 
@@ -878,24 +892,31 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
                                    const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_lat,
                                    const bf16_t* v_lat, const float* tab, int n_pos, float* part,
                                    bf16_t* o, int B, int Hq, int Hkv, int dd, int w, int cap,
-                                   int len, int r, int& P, hipStream_t st) {
-    P = decode_mfma_parts(B, Hkv, len, w, 64);
-    const float qscale = 1.4426950408889634f / sqrtf(64.f);
+                                   int len, int r, int& P, hipStream_t st, int d) {
+    P = decode_mfma_parts(B, Hkv, len, w, d);
+    const float qscale = 1.4426950408889634f / sqrtf((float)d);
     dim3 grid(P, B * Hkv);
-#define DAR_DEC_ROPE(DD_, R_)                                                                        \
-    hipLaunchKernelGGL((decode_mfma_kernel<64, DD_, DecWaves<64>::value, R_>), grid,                 \
-                       dim3(64 * DecWaves<64>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
+#define DAR_DEC_ROPE(D_, DD_, R_)                                                                    \
+    hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value, R_>), grid,                 \
+                       dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_lat, v_lat, \
                        part, o, Hq, Hkv, w, cap, len, P, qscale, tab, n_pos, (const bf16_t*)nullptr, PagedArgs{}, \
                        (const int*)nullptr)
-    if (dd == 16) {
-        if (r == 16) DAR_DEC_ROPE(16, 16);
-        else if (r == 32) DAR_DEC_ROPE(16, 32);
-        else DAR_DEC_ROPE(16, 64);
-    } else {
-        if (r == 16) DAR_DEC_ROPE(32, 16);
-        else if (r == 32) DAR_DEC_ROPE(32, 32);
-        else DAR_DEC_ROPE(32, 64);
+#define DAR_DEC_ROPE_D(D_)                                    \
+    if (dd == 16) {                                           \
+        if (r == 16) DAR_DEC_ROPE(D_, 16, 16);                \
+        else if (r == 32) DAR_DEC_ROPE(D_, 16, 32);           \
+        else DAR_DEC_ROPE(D_, 16, 64);                        \
+    } else {                                                  \
+        if (r == 16) DAR_DEC_ROPE(D_, 32, 16);                \
+        else if (r == 32) DAR_DEC_ROPE(D_, 32, 32);           \
+        else DAR_DEC_ROPE(D_, 32, 64);                        \
     }
+    if (d == 64) {
+        DAR_DEC_ROPE_D(64)
+    } else {
+        DAR_DEC_ROPE_D(128)
+    }
+#undef DAR_DEC_ROPE_D
 #undef DAR_DEC_ROPE
     return hipGetLastError();
 }

@@ -894,7 +894,8 @@ hipError_t launch_decode_rope(const T* q, const T* wd, const T* wu, const T* k_w
         hipError_t e = launch_decode_mfma_rope((const bf16_t*)q, (const bf16_t*)wd, (const bf16_t*)wu,
                                                (const bf16_t*)k_win, (const bf16_t*)v_win,
                                                (const bf16_t*)k_lat, (const bf16_t*)v_lat, tab, n_pos,
-                                               part, (bf16_t*)o, B, Hq, Hkv, dd, w, cap, len, r, P, st);
+                                               part, (bf16_t*)o, B, Hq, Hkv, dd, w, cap, len, r, P, st,
+                                               d);
         if (e != hipSuccess || P == 1) return e;
         return launch_decode_combine<T>(part, wd, wu, o, B, Hq, Hkv, d, dd, P, st);
     }

@@ -214,6 +214,18 @@ def test_decode_rope_d128_long():
                                 kind="decode"), 3000, 2, 128, base=500000.0)
 
 
+@pytest.mark.parametrize("dd,r,w,L0,untied", [
+    (32, 32, 64, 700, False), (16, 64, 100, 300, True), (32, 16, 0, 400, False),
+    (32, 64, 512, 600, True),
+    # few (batch, KV head) pairs and long caches: split records and the combine
+    (32, 32, 256, 20000, False), (16, 16, 1024, 9000, True),
+])
+def test_decode_rope_d128_matrix_core(dd, r, w, L0, untied):
+    """d = 128 on the matrix cores: the first 64 elements of each distant key
+    lifted and rotated, the unrotated upper half absorbed in the query."""
+    run_decode_rope(DEC.with_(B=1, d=128, dd=dd, w=w), L0, 2, r, untied=untied)
+
+
 def test_decode_rope_starts_from_empty_cache():
     run_decode_rope(DEC.with_(w=4), 0, 7, 64)
 
