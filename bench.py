@@ -373,6 +373,13 @@ def main():
             run_pd(i)
         paged["ragged_ms"] = timed(run_pd, args.steps)
         paged["ragged_lens"] = [int(x) for x in lens_r.tolist()]
+        # skewed: one sequence at full length, the others at 600 tokens
+        lens_s = [L] + [600] * (dw.B - 1)
+        pcache.lens.copy_(torch.tensor(lens_s, dtype=torch.int32))
+        for i in range(args.warmup):
+            run_pd(i)
+        paged["skewed_ms"] = timed(run_pd, args.steps)
+        paged["skewed_lens"] = lens_s
         del pcache
 
     # the rotary embedding inside Eq. 3: the same prefill batch (un-rotated
@@ -572,6 +579,13 @@ def main():
                      % (min(paged["ragged_lens"]), max(paged["ragged_lens"])),
             "us": round(rlu, 2), "alg_bytes": rb, "gbs": round(rb / (rlu * 1e-6) / 1e9, 1),
             "frac_hbm_peak": round(rb / (rlu * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        sku = float(paged["skewed_ms"] * 1e3)
+        sb = sum(decode_bytes(1, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, n) for n in paged["skewed_lens"])
+        result["decode_skewed"] = {
+            "shape": "decode1b batch, 256-token pages, one sequence at %d tokens, %d at 600"
+                     % (paged["skewed_lens"][0], dw.B - 1),
+            "us": round(sku, 2), "alg_bytes": sb, "gbs": round(sb / (sku * 1e-6) / 1e9, 1),
+            "frac_hbm_peak": round(sb / (sku * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
     if ragged:
         gu = float(ragged["ms"] * 1e3)
         gfl = sum(prefill_flops(1, pw.Hq, n, pw.d, pw.dd, pw.w) for n in ragged["lens"])

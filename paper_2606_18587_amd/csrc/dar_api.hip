@@ -198,7 +198,9 @@ size_t dar_prefill_workspace_bytes(const dar_shape* s, int T) {
 size_t dar_decode_workspace_bytes(const dar_shape* s, int cap) {
     if (check_shape(s) != DAR_OK || cap < 1 || !group_supported(s)) return 0;
     const int S = decode_max_partials(s->B, s->Hkv, cap, s->w, s->d, s->d_down, s->Hq / s->Hkv);
-    return (size_t)s->B * s->Hq * S * (2 + s->d_down + s->d) * sizeof(float);
+    // records, then (paged decode) one piece count per (sequence, KV head)
+    return (size_t)s->B * s->Hq * S * (2 + s->d_down + s->d) * sizeof(float) +
+           (size_t)s->B * s->Hkv * sizeof(int);
 }
 
 size_t dar_prefill_chunk_workspace_bytes(const dar_shape* s, int len, int n) {
@@ -795,17 +797,20 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
     clear_hip_error();
     const PagedArgs pg{c->lens, c->block_table, c->page_size, c->max_blocks, c->n_pages,
                        __builtin_ctz((unsigned)c->page_size)};
-    int P = 0, chunk = 0;
+    int P = 0;
+    int* counts = nullptr;
     hipError_t e = launch_decode_mfma_paged((const bf16_t*)q, (const bf16_t*)w_down,
                                             (const bf16_t*)w_up, (const bf16_t*)c->k_win,
                                             (const bf16_t*)c->v_win, (const bf16_t*)c->k_pool,
                                             (const bf16_t*)c->v_pool, pg, (float*)ws, (bf16_t*)o,
-                                            s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, P, chunk,
+                                            s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, P, counts,
                                             stream);
-    if (e == hipSuccess && P > 1)
+    // the pairs split over several workgroups, and the empty or overflowed
+    // sequences (NaN rows)
+    if (e == hipSuccess)
         e = launch_decode_combine<bf16_t>((const float*)ws, (const bf16_t*)w_down,
                                           (const bf16_t*)w_up, (bf16_t*)o, s->B, s->Hq, s->Hkv,
-                                          s->d, s->d_down, P, stream, nullptr, c->lens, chunk);
+                                          s->d, s->d_down, P, stream, nullptr, c->lens, counts);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 

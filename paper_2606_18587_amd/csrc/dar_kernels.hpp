@@ -43,7 +43,8 @@ struct PagedArgs {
     const int* bt;
     int ps, maxb, n_pages;
     int ps_shift;  // log2(ps): page sizes are powers of two
-    int chunk;     // most tokens one part (workgroup) of a sequence takes
+    int nseq;      // sequences in the batch (B)
+    int* counts;   // [B * Hkv]: partial records of each (sequence, KV head) (decode)
 };
 
 // Where the rows, keys/values and latents of a prefill come from. Rows
@@ -129,12 +130,19 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
                                    bf16_t* o, int B, int Hq, int Hkv, int dd, int w, int cap,
                                    int len, int r, int& P, hipStream_t st, int d);
 // The same kernel over a paged cache with per-sequence lengths (bf16 shapes
-// of decode_mfma_supported); P from the largest possible length.
+// of decode_mfma_supported), as a persistent grid: the batch's cache bytes
+// are dealt out in equal shares, one per workgroup. A (sequence, KV head)
+// pair that one workgroup covers whole is finished there; the others get one
+// partial record per piece (P records per head at most) and their piece
+// count in pg.counts, and launch_decode_combine (with lens and counts)
+// finishes them. part: P * B * Hq records, then B * Hkv ints (counts).
 hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
                                     const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_pool,
                                     const bf16_t* v_pool, const PagedArgs& pg, float* part,
                                     bf16_t* o, int B, int Hq, int Hkv, int d, int dd, int w, int& P,
-                                    int& chunk, hipStream_t st);
+                                    int*& counts, hipStream_t st);
+// Partial records per head of a paged decode (bound over all length mixes).
+int decode_paged_slots(int Hkv, int cap, int w, int d, int dd);
 // One token per sequence into a paged cache at position lens[b]; the token
 // leaving the window is projected (as launch_append projects it) into its
 // page slot; lens[b] += 1 for every sequence below capacity.
@@ -224,7 +232,8 @@ hipError_t launch_rope_prepass(const T* q, const T* k, const T* v, const T* wd, 
 template <typename T>
 hipError_t launch_decode_combine(const float* part, const T* wd, const T* wu, T* o, int B, int Hq,
                                  int Hkv, int d, int dd, int S, hipStream_t st,
-                                 const T* wv = nullptr, const int* lens = nullptr, int chunk = 0);
+                                 const T* wv = nullptr, const int* lens = nullptr,
+                                 const int* counts = nullptr);
 // Decode with the rotary embedding of Eq. 3 (query at position len - 1, cache
 // token e at position e; positions < len index the table).
 template <typename T>

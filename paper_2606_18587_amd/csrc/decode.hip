@@ -245,16 +245,19 @@ __global__ __launch_bounds__(kDecThreads) void decode_split_kernel(
 // independent of the others, so each phase costs one memory round trip: the
 // W_up column of the lane is fetched first, split weights are broadcast from
 // the lane that owns the split, and partial rows are read eight at a time.
-template <typename T>
+// NR: output columns per lane (lane + 64 r, r < NR; d <= 64 NR).
+template <typename T, int NR>
 __global__ __launch_bounds__(64) void decode_combine_kernel(
     const float* __restrict__ part, const T* __restrict__ wd, const T* __restrict__ wu,
     T* __restrict__ o, int Hq, int Hkv, int d, int dd, int S_all, const T* __restrict__ wv,
-    const int* __restrict__ lens, int chunk) {
-    constexpr int kLiftCols = 32;  // W_up rows held in registers (d_down <= 32, d <= 64)
+    const int* __restrict__ lens, const int* __restrict__ counts) {
+    constexpr int kLiftCols = 32;  // W_up rows held in registers (d_down <= 32)
     const int bh = wg_id_x();
-    // records per head: S_all, or (a paged batch) the parts this sequence's
-    // length used, one per chunk tokens
-    const int S = lens ? imin(S_all, imax(1, (lens[bh / Hq] + chunk - 1) / chunk)) : S_all;
+    const int h = bh % Hq;
+    const int g = h / (Hq / Hkv);
+    // records per head: S_all, or (a paged batch) the records the decode
+    // kernel wrote for this (sequence, KV head)
+    const int S = lens ? imin(S_all, counts[(bh / Hq) * Hkv + g]) : S_all;
     if (lens && lens[bh / Hq] < 1) {
         // an empty or overflowed sequence (paged batch): no query position, NaN
         for (int e = lane_id_x(); e < d; e += 64) {
@@ -263,8 +266,7 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
         }
         return;
     }
-    const int h = bh % Hq;
-    const int g = h / (Hq / Hkv);
+    if (lens && S <= 1) return;
     const int lane = lane_id_x();
     const int stride = 2 + dd + d;
     const float* pp = part + (size_t)bh * S_all * stride;
@@ -272,21 +274,52 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
     // the lift's matrix: W_up (W_down^T when tied), or (shared latent) the
     // value matrix
     const T* wug = wv ? wv + (size_t)g * dd * d : (wu ? wu + (size_t)g * dd * d : nullptr);
-    const bool lift_regs = dd <= kLiftCols && d <= 64;
+    const bool lift_regs = dd <= kLiftCols;
 
-    const T* wp = wug ? wug + imin(lane, d - 1) : wdg + (size_t)imin(lane, d - 1) * dd;
+    // the lane's W_up columns: every load issued before any is used, none
+    // under a branch (clamped addresses; the values past d_down are zeroed)
     const int wstep = wug ? d : 1;  // distance between consecutive latent columns c
-    float wcol[kLiftCols];
+    const int cmax = imin(dd, kLiftCols) - 1;
+    float wcol[NR][kLiftCols];
 #pragma unroll
-    for (int c = 0; c < kLiftCols; ++c)
-        wcol[c] = (lift_regs && c < dd) ? elem<T>::load(wp + (size_t)c * wstep) : 0.f;
+    for (int r = 0; r < NR; ++r) {
+        const int e = imin(lane + 64 * r, d - 1);
+        const T* wp = wug ? wug + e : wdg + (size_t)e * dd;
+#pragma unroll
+        for (int c = 0; c < kLiftCols; ++c) wcol[r][c] = elem<T>::load(wp + (size_t)imin(c, cmax) * wstep);
+    }
+#pragma unroll
+    for (int r = 0; r < NR; ++r)
+#pragma unroll
+        for (int c = 0; c < kLiftCols; ++c)
+            if (c >= dd) wcol[r][c] = 0.f;
+
+    // (d_down <= d <= 64 NR: the lane's columns are lane + 64 r, r < NR.)
+    // The first kFirst records' rows and the first 64 records' {m, l},
+    // requested together (clamped addresses, no load under a branch), so that
+    // a merge of few records costs one memory round trip after W_up.
+    constexpr int kFirst = 8;
+    const int n0 = imin(S, kFirst);
+    float al0[kFirst][NR], aw0[kFirst][NR];
+#pragma unroll
+    for (int j = 0; j < kFirst; ++j) {
+        const float* row = pp + (size_t)imin(j, n0 - 1) * stride + 2;
+#pragma unroll
+        for (int r = 0; r < NR; ++r) {
+            const int e = lane + 64 * r;
+            al0[j][r] = row[imin(e, dd - 1)];
+            aw0[j][r] = row[dd + imin(e, d - 1)];
+        }
+    }
+    const int s_ml = imin(lane, S - 1);
+    const float m_l = pp[(size_t)s_ml * stride], l_l = pp[(size_t)s_ml * stride + 1];
 
     // split weights: w_s = 2^(m_s - M), L = sum_s w_s l_s
-    float M = -INFINITY;
-    for (int s = lane; s < S; s += 64) M = fmaxf(M, pp[(size_t)s * stride]);
+    float M = lane < S ? m_l : -INFINITY;
+    for (int s = lane + 64; s < S; s += 64) M = fmaxf(M, pp[(size_t)s * stride]);
     M = wave_max(M);
-    float L = 0.f;
-    for (int s = lane; s < S; s += 64) {
+    float L = lane < S && m_l != -INFINITY ? exp2f(m_l - M) * l_l : 0.f;
+    for (int s = lane + 64; s < S; s += 64) {
         const float ms = pp[(size_t)s * stride];
         if (ms != -INFINITY) L += exp2f(ms - M) * pp[(size_t)s * stride + 1];
     }
@@ -296,6 +329,20 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
     // lane owns latent columns lane + 64 r (< dd) and window columns lane + 64 r (< d)
     float lat[4] = {0.f, 0.f, 0.f, 0.f};
     float win[4] = {0.f, 0.f, 0.f, 0.f};
+    {
+        const float w0 = lane < S && m_l != -INFINITY ? exp2f(m_l - M) : 0.f;
+#pragma unroll
+        for (int j = 0; j < kFirst; ++j) {
+            const float ws = j < n0 ? __shfl(w0, j, 64) : 0.f;
+#pragma unroll
+            for (int r = 0; r < NR; ++r) {
+                const int e = lane + 64 * r;
+                lat[r] = __builtin_fmaf(ws, e < dd ? al0[j][r] : 0.f, lat[r]);
+                win[r] = __builtin_fmaf(ws, e < d ? aw0[j][r] : 0.f, win[r]);
+            }
+        }
+    }
+    // the records past the first kFirst
     for (int s0 = 0; s0 < S; s0 += 64) {
         float wl = 0.f;  // weight of split s0 + lane, broadcast below
         if (s0 + lane < S) {
@@ -303,7 +350,7 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
             wl = ms == -INFINITY ? 0.f : exp2f(ms - M);
         }
         const int ns = imin(64, S - s0);
-        for (int j0 = 0; j0 < ns; j0 += 8) {
+        for (int j0 = s0 == 0 ? kFirst : 0; j0 < ns; j0 += 8) {
             float al[8][4], aw[8][4];
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
@@ -327,22 +374,28 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
         }
     }
     if (lift_regs) {
-        float acc = win[0];
+        float acc[NR];
+#pragma unroll
+        for (int r = 0; r < NR; ++r) acc[r] = win[r];
+        // (columns past d_down add zero: their W_up values are zeroed)
 #pragma unroll
         for (int c = 0; c < kLiftCols; ++c) {
-            if (c >= dd) break;
-            acc = __builtin_fmaf(__shfl(lat[0], c, 64), wcol[c], acc);
+            const float lc = __shfl(lat[0], c, 64);
+#pragma unroll
+            for (int r = 0; r < NR; ++r) acc[r] = __builtin_fmaf(lc, wcol[r][c], acc[r]);
         }
-        if (lane < d) o[(size_t)bh * d + lane] = elem<T>::from_f32(acc * inv);
+#pragma unroll
+        for (int r = 0; r < NR; ++r)
+            if (lane + 64 * r < d) o[(size_t)bh * d + lane + 64 * r] = elem<T>::from_f32(acc[r] * inv);
         return;
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
+    for (int r = 0; r < NR; ++r) {
         const int e = lane + 64 * r;
         float acc = win[r];
 #pragma unroll
         for (int r2 = 0; r2 < 4; ++r2)
-#pragma unroll 1
+#pragma unroll 8
             for (int c2 = 0; c2 < 64 && 64 * r2 + c2 < dd; ++c2) {
                 const int c = 64 * r2 + c2;
                 const float lc = __shfl(lat[r2], c2, 64);
@@ -357,17 +410,23 @@ __global__ __launch_bounds__(64) void decode_combine_kernel(
 template <typename T>
 hipError_t launch_decode_combine(const float* part, const T* wd, const T* wu, T* o, int B, int Hq,
                                  int Hkv, int d, int dd, int S, hipStream_t st, const T* wv,
-                                 const int* lens, int chunk) {
-    hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu, o, Hq,
-                       Hkv, d, dd, S, wv, lens, chunk);
+                                 const int* lens, const int* counts) {
+#define DAR_COMBINE(NR_)                                                                          \
+    hipLaunchKernelGGL((decode_combine_kernel<T, NR_>), dim3(B * Hq), dim3(64), 0, st, part, wd, wu, \
+                       o, Hq, Hkv, d, dd, S, wv, lens, counts)
+    if (d <= 64) DAR_COMBINE(1);
+    else if (d <= 128) DAR_COMBINE(2);
+    else DAR_COMBINE(4);
+#undef DAR_COMBINE
     return hipGetLastError();
 }
 template hipError_t launch_decode_combine<float>(const float*, const float*, const float*, float*,
                                                  int, int, int, int, int, int, hipStream_t,
-                                                 const float*, const int*, int);
+                                                 const float*, const int*, const int*);
 template hipError_t launch_decode_combine<bf16_t>(const float*, const bf16_t*, const bf16_t*,
                                                   bf16_t*, int, int, int, int, int, int,
-                                                  hipStream_t, const bf16_t*, const int*, int);
+                                                  hipStream_t, const bf16_t*, const int*,
+                                                  const int*);
 
 static int group_chunk(int G) { return kDecScoreSlots / G; }
 
@@ -394,7 +453,11 @@ int decode_max_partials(int B, int Hkv, int cap, int w, int d, int dd, int G) {
     DecodeSplits b = decode_splits(cap, 0, d, dd, G);
     int m = a.n_lat_split + a.n_win_split;
     m = m > b.n_lat_split + b.n_win_split ? m : b.n_lat_split + b.n_win_split;
-    const int p = decode_mfma_parts(B, Hkv, cap, w, d);
+    int p = decode_mfma_parts(B, Hkv, cap, w, d);
+    if (dd == 16 || dd == 32) {  // a paged decode of this shape
+        const int ps = decode_paged_slots(Hkv, cap, w, d, dd);
+        p = p > ps ? p : ps;
+    }
     return m > p ? m : p;
 }
 
@@ -421,9 +484,7 @@ static hipError_t launch_decode_g(const T* q, const T* wd, const T* wu, const T*
                        sp.chunk_lat, sp.chunk_win, sp.n_lat_split, S, qscale);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu, o,
-                       Hq, Hkv, d, dd, S, wv, (const int*)nullptr, 0);
-    return hipGetLastError();
+    return launch_decode_combine<T>(part, wd, wu, o, B, Hq, Hkv, d, dd, S, st, wv, nullptr, 0);
 }
 
 template <typename T>
@@ -438,9 +499,7 @@ hipError_t launch_decode(const T* q, const T* wd, const T* wu, const T* k_win, c
                                           (bf16_t*)o, B, Hq, Hkv, d, dd, w, cap, len, P, st,
                                           (const bf16_t*)wv);
         if (e != hipSuccess || P == 1) return e;
-        hipLaunchKernelGGL(decode_combine_kernel<T>, dim3(B * Hq), dim3(64), 0, st, part, wd, wu,
-                           o, Hq, Hkv, d, dd, P, wv, (const int*)nullptr, 0);
-        return hipGetLastError();
+        return launch_decode_combine<T>(part, wd, wu, o, B, Hq, Hkv, d, dd, P, st, wv, nullptr, 0);
     }
     switch (Hq / Hkv) {
         case 1: return launch_decode_g<T, 1>(q, wd, wu, k_win, v_win, k_lat, v_lat, o, part, B, Hq, Hkv, d, dd, w, cap, len, st, wv);

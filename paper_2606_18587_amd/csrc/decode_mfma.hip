@@ -243,10 +243,14 @@ struct WaveRun {
     int t_begin, t_end;  // token positions [t_begin, t_end)
 };
 
-__host__ __device__ inline WaveRun decode_wave_run(int len, int w, int D, int DD, int nwave, int idx) {
+// Subtile run of wavefront idx (of nwave) over latent subtiles [ls0, ls1)
+// and ring subtiles [ws0, ws1) of a cache of len tokens.
+__host__ __device__ inline WaveRun decode_wave_run_range(int len, int w, int D, int DD, int ls0,
+                                                         int ls1, int ws0, int ws1, int nwave,
+                                                         int idx) {
     const int n_lat = len - w > 0 ? len - w : 0;
     const int n_win = len - n_lat;
-    const long long nls = (n_lat + 31) / 32, nws = (n_win + 31) / 32;
+    const long long nls = ls1 - ls0, nws = ws1 - ws0;
     int nwr = 0;  // wavefronts on the ring
     if (nws > 0) {
         if (nls == 0) {
@@ -260,18 +264,24 @@ __host__ __device__ inline WaveRun decode_wave_run(int len, int w, int D, int DD
     const int nwl = nwave - nwr;
     WaveRun r;
     if (idx < nwl) {
-        const long long s0 = nls * idx / nwl, s1 = nls * (idx + 1) / nwl;
+        const long long s0 = ls0 + nls * idx / nwl, s1 = ls0 + nls * (idx + 1) / nwl;
         r.latent = 1;
         r.t_begin = (int)(32 * s0);
         r.t_end = (int)(32 * s1 < n_lat ? 32 * s1 : n_lat);
     } else {
         const int j = idx - nwl;
-        const long long s0 = nws * j / nwr, s1 = nws * (j + 1) / nwr;
+        const long long s0 = ws0 + nws * j / nwr, s1 = ws0 + nws * (j + 1) / nwr;
         r.latent = 0;
         r.t_begin = n_lat + (int)(32 * s0);
         r.t_end = n_lat + (int)(32 * s1 < n_win ? 32 * s1 : n_win);
     }
     return r;
+}
+
+__host__ __device__ inline WaveRun decode_wave_run(int len, int w, int D, int DD, int nwave, int idx) {
+    const int n_lat = len - w > 0 ? len - w : 0;
+    return decode_wave_run_range(len, w, D, DD, 0, (n_lat + 31) / 32, 0, (len - n_lat + 31) / 32,
+                                 nwave, idx);
 }
 
 // NW = 8 wavefronts per workgroup: one workgroup per compute unit, 2 waves
@@ -281,16 +291,42 @@ struct DecWaves {
     static constexpr int value = 8;
 };
 // Latent subtiles in flight per wavefront (register budget of 2 waves/SIMD).
-// (A shared latent array would have room for more subtiles in flight, its
-// key operand coming from LDS; 20 instead of 12 measured slower.)
 template <int D, int DD, int R = 0>
 struct DecStages {
     static constexpr int value = R > 0 ? (DD <= 16 ? 6 : 4)
                                        : (D <= 64 ? (DD <= 16 ? 12 : 7) : (DD <= 16 ? 10 : 5));
 };
 
+// Jobs of a paged batch. The work of a (sequence, KV head) pair is counted
+// in units of one latent subtile's bytes (a ring subtile is D / DD units). A
+// pair of U units is cut into n = ceil(U / cu) parts of cu units (the last one
+// the remainder), cu = max(ceil(total / kPagedGroups), kPagedMinPart,
+// ceil(U(cap) / kPagedMaxParts)): about one compute unit's share of the
+// batch. One workgroup per part; the full parts of all pairs come first in
+// the grid, then the remainders from the largest down (longest processing
+// time first), so that the last workgroups to start are the shortest. A pair
+// of one part is finished by its workgroup; the others' parts leave partial
+// records (slot = part index, count n in pg.counts) for the combine kernel.
+constexpr int kPagedGroups = 256;   // compute units
+constexpr long kPagedMinPart = 32;  // units
+constexpr int kPagedMaxParts = 16;  // parts of one pair, at most
+constexpr int kPagedRankMax = 512;  // sequences ranked by remainder (more: in batch order)
+__host__ __device__ inline long paged_units(int len, int w, int cap, int D, int DD) {
+    len = len < 0 ? 0 : (len > cap ? cap : len);  // empty or overflowed: no work
+    const int n_lat = len - w > 0 ? len - w : 0;
+    return (long)((n_lat + 31) / 32) + (long)((len - n_lat + 31) / 32) * (D / DD);
+}
+// the part size for a batch of `total` units
+__host__ __device__ inline long paged_part(long total, int cap, int w, int D, int DD) {
+    long cu = (total * 3 + kPagedGroups * 2 - 1) / (kPagedGroups * 2);
+    const long cmin = (paged_units(cap, w, cap, D, DD) + kPagedMaxParts - 1) / kPagedMaxParts;
+    cu = cu > cmin ? cu : cmin;
+    return cu > kPagedMinPart ? cu : kPagedMinPart;
+}
+
+
 // R > 0: the rotary embedding of Eq. 3 with rotary dimension R (rotate-half
-// pairs; d = 64). The query is rotated at position len - 1, each ring key at
+// pairs; d 64 or 128, R <= 64). The query is rotated at position len - 1, each ring key at
 // its position as it is loaded. A distant key has to be lifted to full d
 // before its rotation: per 32-token subtile the latent keys are lifted on
 // the matrix cores, K'^T = W_up^T C^T (the latent rows as loaded are the B
@@ -304,18 +340,42 @@ struct DecStages {
 // rotation. tab: [n_pos][R] (cos of the R/2 angles, then their sin).
 // PAGED: the latents come from the pages of a paged cache and the cache
 // length of each sequence from pg.lens; each 32-token subtile lies inside one
-// page (ps is a multiple of 32), whose descriptor is built per subtile.
+// page (ps is a multiple of 32), whose descriptor is built per subtile. The
+// grid is one workgroup per job (part of a pair; see kPagedGroups).
 // SHARED: one latent array for keys and values (v_lat == k_lat): each
-// latent subtile is loaded once, in the value chunks' order, into one of two
-// LDS buffers of the wavefront; the key operand rows are read back from there.
+// latent subtile is loaded once, in the key operand's layout; the scores use
+// it as loaded, and the same registers, stored at their token rows, are the
+// LDS tile the value operand is read from.
+// The kernel's arguments, as one piece of work reads them.
+struct DecArgs {
+    const bf16_t *q, *wd, *wu, *k_win, *v_win, *k_lat, *v_lat;
+    float* part;
+    bf16_t* o;
+    const float* tab;
+    const bf16_t* wv;
+    const int* block_table;
+    PagedArgs pg;
+    int Hq, Hkv, w, cap, P, n_pos;
+    float qscale;
+};
+static_assert(sizeof(DecArgs) % 4 == 0, "copied as 32-bit words");
+
+// A wave-uniform load through the scalar cache (the data is not written
+// while the kernel runs): a vector load here would be waited for behind the
+// cache stream's loads in flight, which retire in order.
+__device__ __forceinline__ int scalar_load(const int* p) {
+    return *(const __attribute__((address_space(4))) int*)p;
+}
+
+
 template <int D, int DD, int NW, int R = 0, bool PAGED = false, bool SHARED = false>
 __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
-    const bf16_t* __restrict__ q, const bf16_t* __restrict__ wd, const bf16_t* __restrict__ wu,
-    const bf16_t* __restrict__ k_win, const bf16_t* __restrict__ v_win,
-    const bf16_t* __restrict__ k_lat, const bf16_t* __restrict__ v_lat, float* __restrict__ part,
-    bf16_t* __restrict__ o, int Hq, int Hkv, int w, int cap, int len_arg, int P, float qscale,
-    const float* __restrict__ tab, int n_pos, const bf16_t* __restrict__ wv, PagedArgs pg,
-    const int* __restrict__ block_table) {
+    const bf16_t* __restrict__ q_, const bf16_t* __restrict__ wd_, const bf16_t* __restrict__ wu_,
+    const bf16_t* __restrict__ k_win_, const bf16_t* __restrict__ v_win_,
+    const bf16_t* __restrict__ k_lat_, const bf16_t* __restrict__ v_lat_, float* __restrict__ part_,
+    bf16_t* __restrict__ o_, int Hq_, int Hkv_, int w_, int cap_, int len_arg, int P_, float qscale_,
+    const float* __restrict__ tab_, int n_pos_, const bf16_t* __restrict__ wv_, PagedArgs pg_,
+    const int* __restrict__ block_table_) {
     static_assert(R == 0 || ((D == 64 || D == 128) && R % 16 == 0 && R <= 64),
                   "rotary: d 64 or 128, R a multiple of 16 up to 64");
     constexpr int KS = D / 16, DS = DD / 16, NT = D / 32;
@@ -335,26 +395,41 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     __shared__ int red_lat[NW];
     __shared__ float wsh[DD][D];                    // W_up (fp32), used when P == 1
     __shared__ float mrg[kDecMaxGroup][stride];     // merged record, used when P == 1
+    const DecArgs args_in{q_, wd_, wu_, k_win_, v_win_, k_lat_, v_lat_, part_, o_, tab_, wv_,
+                          block_table_, pg_, Hq_, Hkv_, w_, cap_, P_, n_pos_, qscale_};
 
-    const int s = wg_id_x();  // part of this (batch, KV head), < P
-    const int bg = wg_id_y();
-    const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
-    const int len_raw = PAGED ? pg.lens[b] : len_arg;  // tokens in this sequence's cache
-    // (paged) an empty sequence, or one marked overflowed by the append
-    // (negative length), has no query position: its output is NaN
-    const bool dead = PAGED && len_raw < 1;
-    const int len = imax(len_raw, 0);
-    // a paged (ragged) batch: this sequence uses one part per chunk tokens of
-    // its own length, so a long sequence is spread over more workgroups than
-    // a short one; the other parts have nothing to do (workgroup-uniform)
-    const int Pb = PAGED ? imin(P, imax(1, (len + pg.chunk - 1) / pg.chunk)) : P;
-    if (s >= Pb) return;
+    // One piece of work: latent subtiles [ls0, ls1) and ring subtiles
+    // [ws0, ws1) of (sequence b, KV head g), whose cache holds len tokens,
+    // shared by nwave wavefronts of which this one is number widx. fuse: the
+    // workgroup has the whole pair and writes the output; else it writes
+    // partial record srec of each head.
+    auto piece = [&](const int b, const int g, const int len, const bool fuse, const int srec,
+                     const int ls0, const int ls1, const int ws0, const int ws1, const int nwave,
+                     const int widx) {
+    const DecArgs A = args_in;
+    const bf16_t* __restrict__ const q = A.q;
+    const bf16_t* __restrict__ const wd = A.wd;
+    const bf16_t* __restrict__ const wu = A.wu;
+    const bf16_t* __restrict__ const k_win = A.k_win;
+    const bf16_t* __restrict__ const v_win = A.v_win;
+    const bf16_t* __restrict__ const k_lat = A.k_lat;
+    const bf16_t* __restrict__ const v_lat = A.v_lat;
+    float* __restrict__ const part = A.part;
+    bf16_t* __restrict__ const o = A.o;
+    const float* __restrict__ const tab = A.tab;
+    const bf16_t* __restrict__ const wv = A.wv;
+    const int* __restrict__ const block_table = A.block_table;
+    const PagedArgs pg = A.pg;
+    const int Hq = A.Hq, Hkv = A.Hkv, w = A.w, cap = A.cap, P = A.P, n_pos = A.n_pos;
+    const float qscale = A.qscale;
     const int G = Hq / Hkv;
+    // (the thread's indices are computed here, not captured: captured, they
+    // cost the loops below registers)
     const int tid = lane_id_x();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int lane = tid & 63;
     const int col = lane & 31, hg = lane >> 5;
-    const bool fuse = P == 1;  // one workgroup per (batch, KV head): finish here
+    const int bg = b * Hkv + g;
     if (fuse) {
         const bf16_t* wdg = wd + (size_t)g * D * DD;
         const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
@@ -376,7 +451,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             if (idx < DD * D) wsh[idx / D][idx - (idx / D) * D] = bf16_to_f32(uv[j]);
         }
     }
-    const WaveRun run = decode_wave_run(len, w, D, DD, Pb * NW, s * NW + wave);
+    // (computed after the W_up loads are issued: earlier costs registers)
+    const WaveRun run = decode_wave_run_range(len, w, D, DD, ls0, ls1, ws0, ws1, nwave, widx);
     const bool latent = run.latent != 0;
     const int t_begin = run.t_begin, t_end = run.t_end;  // this wavefront's tokens
     bf16_t* vb = vbuf[wave];
@@ -458,7 +534,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
                 // this subtile's page: rows past the run (or of an unmapped
                 // page) are outside the descriptor's size and read as zeros
                 const int blk = imin(t0 >> pg.ps_shift, pg.maxb - 1);
-                const int page = btb[blk];
+                const int page = scalar_load(btb + blk);
                 const int pstart = blk * pg.ps;
                 const bool ok = t0 < t_end && page >= 0 && page < pg.n_pages;
                 const int nrow = ok ? imin(pg.ps, t_end - pstart) : 0;
@@ -475,14 +551,14 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
                     vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rvp, r0 * DD * 2 + lane * 16 + k * 1024, 0, kStream));
             } else {
                 const int o = (t0 - t_begin) * DD * 2;
+#pragma unroll
+                for (int k = 0; k < DS; ++k)
+                    ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + o + k * 32, 0, kStream));
                 if constexpr (!SHARED) {
 #pragma unroll
                     for (int k = 0; k < DS; ++k)
-                        ak[k] = __builtin_bit_cast(dbf16x8, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + o + k * 32, 0, kStream));
+                        vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + o + k * 1024, 0, kStream));
                 }
-#pragma unroll
-                for (int k = 0; k < DS; ++k)
-                    vv[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + o + k * 1024, 0, kStream));
             }
         };
         static_assert(kSubBytes == 1024 * DS, "one V chunk of 16 bytes per lane per 16 latent columns");
@@ -565,20 +641,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
 
         // Software pipelined: the scores of subtile n+1 are on the matrix
         // cores while the exponentials of subtile n run.
-        auto scores = [&](int t0, const dbf16x8 (&ak_in)[DS], const uint4 (&vv)[DS]) {
+        auto scores = [&](int t0, const dbf16x8 (&ak)[DS]) {
             df32x16 x;
-            dbf16x8 ak[DS];
-            if constexpr (SHARED) {
-                // the subtile into its LDS buffer, the key rows back out
-                bf16_t* vbs = vb + (((t0 - t_begin) >> 5) & 1) * 32 * DD;
-#pragma unroll
-                for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vbs + (lane + 64 * k) * 8) = vv[k];
-#pragma unroll
-                for (int k = 0; k < DS; ++k) ak[k] = ld8(vbs + prow * DD + k * 16 + hg * 8);
-            } else {
-#pragma unroll
-                for (int k = 0; k < DS; ++k) ak[k] = ak_in[k];
-            }
             if constexpr (R == 0) {
                 x = mma(ak[0], qtop[0], mma(ones_a, st.negm, fill16(0.f)));
 #pragma unroll
@@ -632,10 +696,16 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             }
             return x;
         };
-        auto finish = [&](int t0, df32x16& x, const uint4 (&vv)[DS], df32x16* xnext) {
-            // shared: this subtile is already in its LDS buffer (scores put it there)
-            bf16_t* vbs = SHARED ? vb + (((t0 - t_begin) >> 5) & 1) * 32 * DD : vb;
-            if constexpr (!SHARED) {
+        auto finish = [&](int t0, df32x16& x, const dbf16x8 (&ak)[DS], const uint4 (&vv)[DS],
+                          df32x16* xnext) {
+            const bf16_t* vbs = vb;
+            if constexpr (SHARED) {
+                // the key operand as loaded holds token prow's latent row:
+                // stored at that row it is the value tile
+#pragma unroll
+                for (int k = 0; k < DS; ++k)
+                    *reinterpret_cast<dbf16x8*>(vb + prow * DD + k * 16 + hg * 8) = ak[k];
+            } else {
 #pragma unroll
                 for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vb + (lane + 64 * k) * 8) = vv[k];
             }
@@ -663,13 +733,13 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             }
         };
         int t0 = t_begin;
-        df32x16 x = scores(t_begin, aks[0], vs[0]);
+        df32x16 x = scores(t_begin, aks[0]);
         for (; t0 + 32 * (NST - 1) < t_end; t0 += 32 * NST) {
 #pragma unroll
             for (int j = 0; j < NST; ++j) {
                 const int tj = t0 + 32 * j;
-                df32x16 xn = scores(tj + 32, aks[(j + 1) % NST], vs[(j + 1) % NST]);
-                finish(tj, x, vs[j], &xn);
+                df32x16 xn = scores(tj + 32, aks[(j + 1) % NST]);
+                finish(tj, x, aks[j], vs[j], &xn);
                 load(tj + 32 * NST, aks[j], vs[j]);
                 x = xn;
             }
@@ -679,11 +749,11 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             const int tj = t0 + 32 * j;
             if (tj < t_end) {
                 if (tj + 32 < t_end) {
-                    df32x16 xn = scores(tj + 32, aks[j + 1], vs[j + 1]);
-                    finish(tj, x, vs[j], &xn);
+                    df32x16 xn = scores(tj + 32, aks[j + 1]);
+                    finish(tj, x, aks[j], vs[j], &xn);
                     x = xn;
                 } else {
-                    finish(tj, x, vs[j], nullptr);
+                    finish(tj, x, aks[j], vs[j], nullptr);
                 }
             }
         }
@@ -766,12 +836,24 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
                     acc[t] = mma(a, half ? p1 : p0, acc[t]);
                 }
         };
-        dbf16x8 akA[KS];
-        uint4 vA[CPT];
-        for (int t0 = t_begin; t0 < t_end; t0 += 32) {
-            load(t0, akA, vA);
-            body(t0, akA, vA);
+        // NSW subtiles in flight (positions past the run are clamped to its
+        // last token, so the prefetches need no branch)
+        constexpr int NSW = D > 64 ? 1 : (R > 0 ? 2 : 3);
+        dbf16x8 akw[NSW][KS];
+        uint4 vw4[NSW][CPT];
+#pragma unroll
+        for (int j = 0; j < NSW; ++j) load(t_begin + 32 * j, akw[j], vw4[j]);
+        int t0 = t_begin;
+        for (; t0 + 32 * (NSW - 1) < t_end; t0 += 32 * NSW) {
+#pragma unroll
+            for (int j = 0; j < NSW; ++j) {
+                body(t0 + 32 * j, akw[j], vw4[j]);
+                load(t0 + 32 * (j + NSW), akw[j], vw4[j]);
+            }
         }
+#pragma unroll
+        for (int j = 0; j < NSW - 1; ++j)
+            if (t0 + 32 * j < t_end) body(t0 + 32 * j, akw[j], vw4[j]);
         st.l = psum(st.l);
         if (col < G) {
 #pragma unroll
@@ -814,7 +896,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             mrg[h][f] = val;
         } else {
             const size_t bh = (size_t)b * Hq + (size_t)g * G + h;
-            part[(bh * P + s) * stride + f] = val;
+            part[(bh * P + srec) * stride + f] = val;
         }
     }
     if (!fuse) return;
@@ -825,7 +907,154 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         float acc = mrg[h][2 + DD + e];
 #pragma unroll
         for (int c = 0; c < DD; ++c) acc = __builtin_fmaf(mrg[h][2 + c], wsh[c][e], acc);
-        o[((size_t)b * Hq + (size_t)g * G + h) * D + e] = dead ? (bf16_t)0x7fc0 : f32_to_bf16(acc / mrg[h][1]);
+        o[((size_t)b * Hq + (size_t)g * G + h) * D + e] = f32_to_bf16(acc / mrg[h][1]);
+    }
+    };  // piece
+
+    const int tid = lane_id_x();
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int lane = tid & 63;
+    if constexpr (!PAGED) {
+        // P workgroups per (sequence, KV head): this one is part s
+        const int s = wg_id_x(), bg = wg_id_y();
+        const int b = bg / Hkv_, g = bg - (bg / Hkv_) * Hkv_;
+        const int n_lat = imax(len_arg - w_, 0);
+        piece(b, g, len_arg, P_ == 1, s, 0, (n_lat + 31) / 32, 0, (len_arg - n_lat + 31) / 32, P_ * NW,
+              s * NW + wave);
+    } else {
+        // ---- this workgroup's job (every workgroup derives the same plan
+        // from the lengths). Block-wide sums and exclusive prefixes:
+        __shared__ long red[NW];
+        __shared__ int job[3];  // sequence, KV head, part
+        auto block_scan = [&](long v, long& excl, long& tot) {
+            long inc = v;
+#pragma unroll
+            for (int off = 1; off < 64; off <<= 1) {
+                const long t = __shfl_up(inc, off, 64);
+                if (lane >= off) inc += t;
+            }
+            if (lane == 63) red[wave] = inc;
+            __syncthreads();
+            long before = 0;
+            tot = 0;
+#pragma unroll
+            for (int v2 = 0; v2 < NW; ++v2) {
+                const long t = red[v2];
+                tot += t;
+                if (v2 < wave) before += t;
+            }
+            excl = before + inc - v;
+            __syncthreads();  // red is reused
+        };
+        const int B = pg_.nseq;
+        const int per = (B + NW * 64 - 1) / (NW * 64);
+        const int b0 = tid * per;  // this thread's sequences: [b0, b0 + per)
+        // units of this thread's sequences (the first kKeep kept in registers)
+        constexpr int kKeep = 2;
+        long uk[kKeep];
+        auto units_of = [&](int i) -> long {
+            if (i < kKeep) {
+                long u = 0;
+#pragma unroll
+                for (int t = 0; t < kKeep; ++t) u = t == i ? uk[t] : u;
+                return u;
+            }
+            return b0 + i < B ? paged_units(pg_.lens[b0 + i], w_, cap_, D, DD) : 0;
+        };
+#pragma unroll
+        for (int t = 0; t < kKeep; ++t)
+            uk[t] = t < per && b0 + t < B ? paged_units(pg_.lens[b0 + t], w_, cap_, D, DD) : 0;
+        long myU = 0, myLive = 0;
+        for (int i = 0; i < per; ++i) {
+            const long u = units_of(i);
+            myU += u;
+            myLive += u > 0;
+        }
+        long ex, totU, totLive;
+        block_scan(myU, ex, totU);
+        block_scan(myLive, ex, totLive);
+        const long liveBefore = ex;
+        const long cu = paged_part(totU * Hkv_, cap_, w_, D, DD);
+        auto nparts = [&](long u) { return (u + cu - 1) / cu; };
+        long myFull = 0;  // full parts (all but the last) of this thread's pairs
+        for (int i = 0; i < per; ++i) {
+            const long u = units_of(i);
+            if (u > 0) myFull += (nparts(u) - 1) * Hkv_;
+        }
+        long fullBefore, F;
+        block_scan(myFull, fullBefore, F);
+        const long i0 = wg_id_x();
+        if (i0 >= F + totLive * Hkv_) return;  // no job (uniform)
+        if (i0 < F) {
+            // a full part: the thread whose pairs hold full part i0
+            long pos = fullBefore;
+            for (int i = 0; i < per; ++i) {
+                const long u = units_of(i);
+                const long nf = u > 0 ? nparts(u) - 1 : 0;  // full parts per pair
+                if (nf > 0 && pos <= i0 && i0 < pos + nf * Hkv_) {
+                    job[0] = b0 + i;
+                    job[1] = (int)((i0 - pos) / nf);
+                    job[2] = (int)((i0 - pos) % nf);
+                }
+                pos += nf * Hkv_;
+            }
+        } else {
+            // a last part: the sequence of rank (i0 - F) / Hkv among the live
+            // ones, ranked by remainder (largest first, then batch order)
+            const long j = i0 - F, target = j / Hkv_;
+            __shared__ int rem[kPagedRankMax];
+            if (B <= kPagedRankMax) {
+                // (per == 1 here)
+                long u = 0, r = -1;
+                if (tid < B) {
+                    u = uk[0];
+                    r = u > 0 ? u - (nparts(u) - 1) * cu : -1;
+                    rem[tid] = (int)r;
+                }
+                __syncthreads();
+                if (tid < B && r >= 0) {
+                    int rank = 0;
+                    for (int b2 = 0; b2 < B; ++b2) {
+                        const int r2 = rem[b2];
+                        rank += (r2 > r || (r2 == r && b2 < tid)) ? 1 : 0;
+                    }
+                    if (rank == target) {
+                        job[0] = tid;
+                        job[1] = (int)(j % Hkv_);
+                        job[2] = (int)(nparts(u) - 1);
+                    }
+                }
+            } else {
+                long pos = liveBefore;
+                for (int i = 0; i < per; ++i) {
+                    const long u = units_of(i);
+                    if (u > 0) {
+                        if (pos == target) {
+                            job[0] = b0 + i;
+                            job[1] = (int)(j % Hkv_);
+                            job[2] = (int)(nparts(u) - 1);
+                        }
+                        ++pos;
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        const int b = __builtin_amdgcn_readfirstlane(job[0]);
+        const int g = __builtin_amdgcn_readfirstlane(job[1]);
+        const int p = __builtin_amdgcn_readfirstlane(job[2]);
+        const int len = imin(imax(scalar_load(pg_.lens + b), 0), cap_);
+        const long U = paged_units(len, w_, cap_, D, DD);
+        const int n = (int)nparts(U);
+        const long u0 = p * cu, u1 = u0 + cu < U ? u0 + cu : U;  // this part's units
+        constexpr int RU = D / DD;
+        const int n_lat = imax(len - w_, 0);
+        const int nls = (n_lat + 31) / 32, nws = (len - n_lat + 31) / 32;
+        const int ls0 = (int)(u0 < nls ? u0 : nls), ls1 = (int)(u1 < nls ? u1 : nls);
+        const int ws0 = imin((int)(u0 > nls ? (u0 - nls + RU - 1) / RU : 0), nws);
+        const int ws1 = imin((int)(u1 > nls ? (u1 - nls + RU - 1) / RU : 0), nws);
+        if (p == 0 && tid == 0) pg_.counts[b * Hkv_ + g] = n;
+        piece(b, g, len, n == 1, p, ls0, ls1, ws0, ws1, NW, wave);
     }
 }
 
@@ -921,24 +1150,27 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
     return hipGetLastError();
 }
 
+int decode_paged_slots(int Hkv, int cap, int w, int d, int dd) {
+    // cu >= ceil(U(cap) / kPagedMaxParts): a pair has at most that many parts
+    (void)Hkv; (void)cap; (void)w; (void)d; (void)dd;
+    return kPagedMaxParts;
+}
+
 hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
                                     const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_pool,
                                     const bf16_t* v_pool, const PagedArgs& pg_in, float* part,
                                     bf16_t* o, int B, int Hq, int Hkv, int d, int dd, int w, int& P,
-                                    int& chunk, hipStream_t st) {
+                                    int*& counts, hipStream_t st) {
     const int cap = pg_in.maxb * pg_in.ps;
-    // Parts per (sequence, KV head) as for a dense cache at full capacity;
-    // lengths differ per sequence and live on the device, so each sequence
-    // takes one part per chunk tokens of its own length and the rest return
-    // at once. (More parts than that, so that a long sequence of a full batch
-    // is spread wider, measured slower: every extra generation of workgroups
-    // pays its own pipeline fill and drain, and the merge kernel runs.)
-    P = decode_mfma_parts(B, Hkv, cap, w, d);
-    chunk = (cap + P - 1) / P;
+    P = decode_paged_slots(Hkv, cap, w, d, dd);
+    counts = reinterpret_cast<int*>(part + (size_t)B * Hq * P * (2 + dd + d));
     PagedArgs pg = pg_in;
-    pg.chunk = chunk;
+    pg.nseq = B;
+    pg.counts = counts;
     const float qscale = 1.4426950408889634f / sqrtf((float)d);
-    dim3 grid(P, B * Hkv);
+    // jobs: at most kPagedGroups full parts (cu >= total / kPagedGroups) and
+    // one last part per pair
+    dim3 grid(kPagedGroups + B * Hkv);
 #define DAR_DEC_PAGED(D_, DD_)                                                                       \
     hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value, 0, true>), grid,            \
                        dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_pool, v_pool, \

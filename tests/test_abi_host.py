@@ -104,7 +104,11 @@ def test_decode_workspace_size_grows_with_capacity():
     a = dar.dar_decode_workspace_bytes(s, 1000)
     b = dar.dar_decode_workspace_bytes(s, 100000)
     assert 0 < a < b
-    assert a % (s.B * s.Hq * (2 + s.d_down + s.d) * 4) == 0
+    # whole partial records {m, l, acc_lat, acc_win} per (batch, query head),
+    # then one int per (batch, KV head): the paged decode's record count
+    rec = s.B * s.Hq * (2 + s.d_down + s.d) * 4
+    for x in (a, b):
+        assert (x - s.B * s.Hkv * 4) % rec == 0
     assert dar.dar_decode_workspace_bytes(S(Hq=12, Hkv=4), 100) == 0  # group of 3: unsupported
 
 

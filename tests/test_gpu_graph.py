@@ -69,3 +69,29 @@ def test_decode_graph_replay(L0):
     ws = torch.empty(dar.dar_decode_workspace_bytes(shape, c.cap), dtype=torch.uint8, device="cuda")
     replay_matches(lambda: dar.dar_attn_decode(c, q, wd, o=o, ws=ws), o)
     replay_matches(lambda: dar.dar_attn_decode_noalloc(c, q, wd, o=o), o)
+
+
+def test_paged_decode_graph_replay():
+    """Paged decode over a batch of mixed lengths: a long sequence split into
+    parts (their records merged by the combine kernel, which reads the record
+    counts the decode kernel wrote), short ones finished whole, an empty one
+    written as NaN."""
+    B, Hq, Hkv, d, dd, w, ps = 6, 8, 2, 64, 16, 32, 64
+    lens = [9000, 5, 0, 300, 64, 1]
+    nblk = max(lens) // ps + 2
+    n_pages = B * nblk
+    pc = dar.DarPagedCache(B, Hkv, d, dd, w, ps, nblk, n_pages, torch.bfloat16)
+    gen = torch.Generator(device="cuda").manual_seed(73)
+    for t in (pc.k_win, pc.v_win, pc.k_pool, pc.v_pool):
+        t.copy_(torch.randn(t.shape, device="cuda", generator=gen))
+    perm = torch.randperm(n_pages, generator=torch.Generator().manual_seed(74))
+    pc.block_table.copy_(perm.view(B, nblk).to(torch.int32))
+    pc.lens.copy_(torch.tensor(lens, dtype=torch.int32))
+    q = torch.randn(B, Hq, d, device="cuda", generator=gen).bfloat16()
+    wd = (torch.randn(Hkv, d, dd, device="cuda", generator=gen) / d ** 0.5).bfloat16()
+    o = torch.empty_like(q)
+    shape = dar.make_shape(B, Hq, Hkv, d, dd, w, torch.bfloat16)
+    ws = torch.empty(dar.dar_decode_workspace_bytes(shape, pc.cap), dtype=torch.uint8, device="cuda")
+    replay_matches(lambda: dar.dar_attn_decode_paged(pc, q, wd, o=o, ws=ws), o)
+    got = o.float().cpu()
+    assert torch.isnan(got[2]).all() and torch.isfinite(got[[0, 1, 3, 4, 5]]).all()

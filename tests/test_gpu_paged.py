@@ -98,11 +98,14 @@ class Ragged:
         o = dar.dar_attn_decode_paged(self.pc, to_dev(q), self.wdd)
         torch.cuda.synchronize()
         got = to_host64(o)
-        assert np.isfinite(got).all()
         grp = wl.Hq // wl.Hkv
         worst = 0.0
         for b in range(self.B):
             L = self.lens[b] + t
+            if L < 1:  # empty sequence: no query position
+                assert np.isnan(got[b]).all()
+                continue
+            assert np.isfinite(got[b]).all()
             heads = range(wl.Hq) if heads_per_seq is None else heads_per_seq
             for h in heads:
                 gg = h // grp
@@ -164,6 +167,25 @@ def test_long_sequences_several_workgroups():
     r.check_decode(0, heads_per_seq=[0, 3, 7])
     r.append_step(0)
     r.check_decode(1, heads_per_seq=[0, 5])
+
+
+@pytest.mark.parametrize("d,dd,w,Hq,Hkv,lens", [
+    (64, 16, 600, 8, 2, [30000, 1, 2, 0, 33, 700, 64, 100]),
+    (128, 16, 100, 4, 2, [5, 9000, 0, 0, 1, 4000]),
+    (64, 32, 48, 8, 2, [12000] + [3] * 20),
+    (64, 16, 32, 4, 1, [7000, 10, 0, 2500]),
+    (128, 32, 256, 8, 1, [1, 300, 6000]),
+])
+def test_mixed_lengths_equal_shares(d, dd, w, Hq, Hkv, lens):
+    """The batch's cache bytes are dealt out in equal shares, one per
+    workgroup: a long sequence beside tiny and empty ones is cut into many
+    pieces (some boundaries fall inside a ring subtile), whose records the
+    combine kernel merges; pairs a workgroup holds whole are finished there;
+    empty sequences decode to NaN."""
+    r = Ragged(WL.with_(d=d, dd=dd, w=w, Hq=Hq, Hkv=Hkv), lens, 64, steps=1)
+    r.check_decode(0)
+    r.append_step(0)
+    r.check_decode(1)
 
 
 def test_sequence_at_capacity_is_marked_overflowed():
