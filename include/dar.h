@@ -220,6 +220,28 @@ dar_status dar_attn_prefill_rope(const dar_shape* s, int T, int pos0, const dar_
                                  const void* w_up, void* o, float* lse, void* ws, size_t ws_bytes,
                                  hipStream_t stream);
 
+/* Chunked prefill (as dar_attn_prefill_chunk) with the rotary embedding of
+ * Eq. 3 (as dar_attn_prefill_rope): the n new tokens at positions
+ * len..len+n-1 (len = c->len, len + n <= rope->n_pos) with un-rotated q,
+ * k_new, v_new; window keys are rotated at their positions, distant keys are
+ * lifted and then rotated: those below len - w from the cache's latents
+ * (c^K W_up), the others projected from the ring or the chunk
+ * ((k W_down) W_up), as the decode with rotation treats them. The cache is
+ * extended by the un-rotated tokens exactly as dar_cache_append extends it
+ * (c->len += n at enqueue time).
+ *   o [B][Hq][n][d] (output); lse: NULL or fp32 [B][Hq][n].
+ *   ws: at least dar_prefill_chunk_rope_workspace_bytes(s, len, n) bytes
+ *   (caller-owned, overwritten): the window's and the chunk's rows, rotated
+ *   queries and keys, lifted distant keys and values of positions below
+ *   len + n - w (full d), and block norms.
+ * Fails with DAR_E_CAPACITY if len + n > cap. Supported: the matrix-core
+ * shapes (bf16, d in {64, 128}, any d_down) with rotary_dim a multiple of
+ * 16; other shapes return DAR_E_UNSUPPORTED. */
+dar_status dar_attn_prefill_chunk_rope(const dar_shape* s, dar_cache* c, const dar_rope* rope,
+                                       int n, const void* q, const void* k_new, const void* v_new,
+                                       const void* w_down, const void* w_up, void* o, float* lse,
+                                       void* ws, size_t ws_bytes, hipStream_t stream);
+
 /* One decode step for the query q [B][Hq][d] at position c->len - 1, whose own
  * key and value must already have been appended. o [B][Hq][d] (output).
  * ws: device workspace of at least dar_decode_workspace_bytes(s, c->cap)
@@ -346,6 +368,7 @@ size_t dar_decode_workspace_bytes(const dar_shape* s, int cap);
 size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T);
 size_t dar_prefill_chunk_workspace_bytes(const dar_shape* s, int len, int n);
 size_t dar_prefill_rope_workspace_bytes(const dar_shape* s, int T);
+size_t dar_prefill_chunk_rope_workspace_bytes(const dar_shape* s, int len, int n);
 
 /* Static English text for a status code. */
 const char* dar_status_string(dar_status st);

@@ -99,6 +99,10 @@ def _load():
     lib.dar_attn_prefill_ragged.argtypes = [shp, ci] + [vp] * 9 + [sz, vp]
     lib.dar_prefill_rope_workspace_bytes.restype = sz
     lib.dar_prefill_rope_workspace_bytes.argtypes = [shp, ci]
+    lib.dar_attn_prefill_chunk_rope.restype = ci
+    lib.dar_attn_prefill_chunk_rope.argtypes = [shp, cp, rp, ci] + [vp] * 8 + [sz, vp]
+    lib.dar_prefill_chunk_rope_workspace_bytes.restype = sz
+    lib.dar_prefill_chunk_rope_workspace_bytes.argtypes = [shp, ci, ci]
     lib.dar_attn_decode_noalloc.restype = ci
     lib.dar_attn_decode_noalloc.argtypes = [shp, cp, vp, vp, vp, vp, vp]
     lib.dar_decode_noalloc_bytes.restype = sz
@@ -400,6 +404,44 @@ def dar_attn_prefill_chunk(cache: DarCache, q, k_new, v_new, w_down, w_up=None, 
                                     _stream(stream))
     if st != DAR_OK:
         raise DarError(st, "dar_attn_prefill_chunk")
+    return (o, lse) if return_lse else o
+
+
+def dar_prefill_chunk_rope_workspace_bytes(shape, len_, n) -> int:
+    return int(lib.dar_prefill_chunk_rope_workspace_bytes(ctypes.byref(shape), int(len_), int(n)))
+
+
+def dar_attn_prefill_chunk_rope(cache: DarCache, q, k_new, v_new, w_down, rope: "Rope", w_up=None,
+                                o=None, lse=None, return_lse=False, ws=None, stream=None,
+                                check=True):
+    """Chunked prefill with the rotary embedding of Eq. 3: n new tokens at
+    positions cache.len.. (q, k_new, v_new un-rotated, shapes as
+    dar_attn_prefill_chunk); the cache is extended by the un-rotated tokens.
+    Returns o [B,Hq,n,d], or (o, lse) with return_lse."""
+    B, Hq, n, d = q.shape
+    Hkv = cache.Hkv
+    shape = make_shape(B, Hq, Hkv, d, cache.d_down, cache.w, q.dtype)
+    if check:
+        for name, t in (("k_new", k_new), ("v_new", v_new)):
+            if tuple(t.shape) != (B, Hkv, n, d) or t.dtype != q.dtype:
+                raise ValueError("%s: expected %s %s" % (name, (B, Hkv, n, d), q.dtype))
+        if (B, d) != (cache.B, cache.d) or q.dtype != cache.dtype:
+            raise ValueError("q does not match the cache")
+    if o is None:
+        o = torch.empty_like(q)
+    if return_lse and lse is None:
+        lse = torch.empty(B, Hq, n, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = _workspace(dar_prefill_chunk_rope_workspace_bytes(shape, cache.len, n), q.device)
+    rs = rope.struct()
+    st = lib.dar_attn_prefill_chunk_rope(ctypes.byref(shape), ctypes.byref(cache.struct),
+                                         ctypes.byref(rs), int(n), _ptr(q), _ptr(k_new),
+                                         _ptr(v_new), _ptr(w_down), _ptr(w_up), _ptr(o),
+                                         _ptr(lse), _ptr(ws),
+                                         0 if ws is None else ws.numel() * ws.element_size(),
+                                         _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_prefill_chunk_rope")
     return (o, lse) if return_lse else o
 
 

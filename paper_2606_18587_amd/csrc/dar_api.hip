@@ -36,6 +36,13 @@ hipError_t launch_prefill_mfma(const dar_shape* s, const PrefillGeo& geo, const 
                                const float* knorm, const void* consts, hipStream_t st,
                                const void* wv = nullptr);
 bool prefill_mfma_rope_supported(const dar_shape* s);
+// The matrix-core rotary attention over a chunk geometry (see PrefillGeo):
+// qr the rotated chunk queries, kr / v the rotated keys and the values of the
+// context rows (from geo.kv0), kd / vd the distant rows (positions 0..).
+hipError_t launch_prefill_mfma_rope_geo(const dar_shape* s, const PrefillGeo& geo, const void* qr,
+                                        const void* kr, const void* v, const void* kd,
+                                        const void* vd, void* o, float* lse, const float* knorm,
+                                        const float* dnorm, hipStream_t st);
 hipError_t launch_prefill_mfma_rope(const dar_shape* s, int T, const void* qr, const void* kr,
                                     const void* v, const void* kd, const void* vd, void* o,
                                     float* lse, const float* knorm, const float* dnorm,
@@ -160,6 +167,38 @@ struct ChunkWs {
     int kv0, Tc;
 };
 
+// Chunked prefill with the rotary embedding: the context rows (from kv0, the
+// window's oldest position rounded down to 32 so that key blocks of 32 rows
+// are position blocks; with w = 0 there is no window and kv0 = len), the
+// rotated queries and context keys, the lifted rotated distant keys and
+// lifted values (positions < len + n - w), and the two block-norm arrays.
+struct ChunkRopeWs {
+    size_t ctx_k_off, ctx_v_off, qr_off, kr_off, kd_off, vd_off, knorm_off, dnorm_off, bytes;
+    int kv0, Tc, Td;
+};
+
+ChunkRopeWs chunk_rope_ws_layout(const dar_shape* s, int len, int n) {
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const size_t es = esize_of(s->dtype);
+    ChunkRopeWs L{};
+    L.kv0 = s->w > 0 ? (len - s->w > 0 ? len - s->w : 0) & ~31 : len;
+    L.Tc = len + n - L.kv0;
+    const int T = len + n;
+    L.Td = T - s->w > 0 ? T - s->w : 0;
+    const size_t ctx = al((size_t)s->B * s->Hkv * L.Tc * s->d * es);
+    const size_t dist = al((size_t)s->B * s->Hkv * L.Td * s->d * es);
+    L.ctx_k_off = 0;
+    L.ctx_v_off = ctx;
+    L.qr_off = 2 * ctx;
+    L.kr_off = L.qr_off + al((size_t)s->B * s->Hq * n * s->d * es);
+    L.kd_off = L.kr_off + ctx;
+    L.vd_off = L.kd_off + dist;
+    L.knorm_off = L.vd_off + dist;
+    L.dnorm_off = L.knorm_off + al((size_t)s->B * s->Hkv * ((T + 31) / 32) * sizeof(float));
+    L.bytes = L.dnorm_off + al((size_t)s->B * s->Hkv * ((L.Td + 31) / 32 + 1) * sizeof(float));
+    return L;
+}
+
 ChunkWs chunk_ws_layout(const dar_shape* s, int len, int n) {
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     ChunkWs L{};
@@ -207,6 +246,12 @@ size_t dar_prefill_chunk_workspace_bytes(const dar_shape* s, int len, int n) {
     if (check_shape(s) != DAR_OK || len < 0 || n < 1) return 0;
     if ((long long)len + n > 0x7fffffffLL) return 0;
     return chunk_ws_layout(s, len, n).bytes;
+}
+
+size_t dar_prefill_chunk_rope_workspace_bytes(const dar_shape* s, int len, int n) {
+    if (check_shape(s) != DAR_OK || len < 0 || n < 1) return 0;
+    if ((long long)len + n > 0x7fffffffLL) return 0;
+    return chunk_rope_ws_layout(s, len, n).bytes;
 }
 
 size_t dar_prefill_rope_workspace_bytes(const dar_shape* s, int T) {
@@ -459,6 +504,67 @@ dar_status dar_attn_prefill_chunk(const dar_shape* s, dar_cache* c, int n, const
                                      (float*)c->k_lat, (float*)c->v_lat, s->B, s->Hkv, s->d,
                                      s->d_down, s->w, c->cap, len, n, stream);
     }
+    if (e != hipSuccess) return DAR_E_HIP;
+    c->len += n;
+    return DAR_OK;
+}
+
+dar_status dar_attn_prefill_chunk_rope(const dar_shape* s, dar_cache* c, const dar_rope* rope,
+                                       int n, const void* q, const void* k_new, const void* v_new,
+                                       const void* w_down, const void* w_up, void* o, float* lse,
+                                       void* ws, size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (!c || !rope || n < 1 || c->cap < 1 || c->len < 0 || c->len > c->cap) return DAR_E_ARG;
+    const int r = rope->rotary_dim;
+    if (r < 0 || (r & 1) || r > s->d) return DAR_E_ARG;
+    if (r > 0 && !dev_ok(rope->table)) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(k_new) || !dev_ok(v_new) || !dev_ok(w_down) || !dev_ok(o))
+        return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if (lse && !aligned16(lse)) return DAR_E_ARG;
+    if (!dev_ok(c->k_lat) || !dev_ok(c->v_lat)) return DAR_E_ARG;
+    if (s->w > 0 && (!dev_ok(c->k_win) || !dev_ok(c->v_win))) return DAR_E_ARG;
+    if ((long long)c->len + n > (long long)c->cap) return DAR_E_CAPACITY;
+    if ((long long)c->len + n > (long long)rope->n_pos) return DAR_E_ARG;
+    if ((long long)s->B * s->Hkv > 65535 || (long long)s->B * s->Hq > 65535)
+        return DAR_E_UNSUPPORTED;
+    // the matrix-core shapes, rotated in 8-element chunks
+    if (!prefill_mfma_rope_supported(s) || r % 16 != 0) return DAR_E_UNSUPPORTED;
+    const ChunkRopeWs L = chunk_rope_ws_layout(s, c->len, n);
+    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+
+    clear_hip_error();
+    char* wsb = (char*)ws;
+    const int len = c->len;
+    bf16_t* ctx_k = (bf16_t*)(wsb + L.ctx_k_off);
+    bf16_t* ctx_v = (bf16_t*)(wsb + L.ctx_v_off);
+    bf16_t* qr = (bf16_t*)(wsb + L.qr_off);
+    bf16_t* kr = (bf16_t*)(wsb + L.kr_off);
+    bf16_t* kd = (bf16_t*)(wsb + L.kd_off);
+    bf16_t* vd = (bf16_t*)(wsb + L.vd_off);
+    float* knorm = (float*)(wsb + L.knorm_off);
+    float* dnorm = (float*)(wsb + L.dnorm_off);
+    hipError_t e = launch_chunk_gather<bf16_t>((const bf16_t*)c->k_win, (const bf16_t*)c->v_win,
+                                               (const bf16_t*)k_new, (const bf16_t*)v_new, ctx_k,
+                                               ctx_v, s->B, s->Hkv, s->d, s->w, len, n, L.kv0,
+                                               stream);
+    if (e == hipSuccess)
+        e = launch_rope_chunk_prepass<bf16_t>(
+            (const bf16_t*)q, ctx_k, ctx_v, (const bf16_t*)c->k_lat, (const bf16_t*)c->v_lat,
+            c->cap, (const bf16_t*)w_down, (const bf16_t*)w_up, rope->table, qr, kr, kd, vd, knorm,
+            dnorm, s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, r, len, n, L.kv0, stream);
+    // rows len..len+n-1 against the context rows from kv0 and the distant rows
+    const PrefillGeo geo{len, n, L.kv0, L.Tc, 0, 0, nullptr, nullptr};
+    if (e == hipSuccess)
+        e = launch_prefill_mfma_rope_geo(s, geo, qr, kr, ctx_v, kd, vd, o, lse, knorm, dnorm, stream);
+    // the cache update: the append of the same (un-rotated) tokens
+    if (e == hipSuccess)
+        e = launch_append<bf16_t>((const bf16_t*)k_new, (const bf16_t*)v_new, (const bf16_t*)w_down,
+                                  (bf16_t*)c->k_win, (bf16_t*)c->v_win, (bf16_t*)c->k_lat,
+                                  (bf16_t*)c->v_lat, s->B, s->Hkv, s->d, s->d_down, s->w, c->cap,
+                                  len, n, stream);
     if (e != hipSuccess) return DAR_E_HIP;
     c->len += n;
     return DAR_OK;

@@ -227,6 +227,19 @@ hipError_t launch_rope_prepass(const T* q, const T* k, const T* v, const T* wd, 
                                const float* tab, T* qr, T* kr, T* kd, T* vd, float* knorm,
                                float* dnorm, int B, int Hq, int Hkv, int T_, int d, int dd, int w,
                                int r, int pos0, hipStream_t st);
+// Pre-pass of a chunked prefill with the rotary embedding (n new tokens at
+// positions len.., context rows ctx_k / ctx_v of positions kv0..len+n-1, kv0
+// a multiple of 32): the rotated queries and context keys, the lifted and
+// rotated distant keys and lifted values of positions < len + n - w (below
+// len - w from the cache's latents, k_lat / v_lat with cap rows a head, the
+// rest projected from the context rows), and the block norms of both key
+// arrays in the matrix-core kernel's position-block layout.
+template <typename T>
+hipError_t launch_rope_chunk_prepass(const T* q, const T* ctx_k, const T* ctx_v, const T* k_lat,
+                                     const T* v_lat, int cap, const T* wd, const T* wu,
+                                     const float* tab, T* qr, T* kr, T* kd, T* vd, float* knorm,
+                                     float* dnorm, int B, int Hq, int Hkv, int d, int dd, int w,
+                                     int r, int len, int n, int kv0, hipStream_t st);
 // Second stage of the split decodes: merges the S partial records of each
 // (batch, query head) and lifts the latent part (decode_combine_kernel).
 template <typename T>

@@ -939,6 +939,17 @@ bool prefill_mfma_rope_supported(const dar_shape* s) {
     return s->dtype == DAR_BF16 && (s->d == 64 || s->d == 128);
 }
 
+hipError_t launch_prefill_mfma_rope_geo(const dar_shape* s, const PrefillGeo& geo, const void* qr,
+                                        const void* kr, const void* v, const void* kd,
+                                        const void* vd, void* o, float* lse, const float* knorm,
+                                        const float* dnorm, hipStream_t st) {
+    if (s->d == 64)
+        return launch_dd<64, 16, true>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o,
+                                       lse, kd, vd, dnorm, knorm, nullptr, st);
+    return launch_dd<128, 16, true>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o, lse,
+                                    kd, vd, dnorm, knorm, nullptr, st);
+}
+
 hipError_t launch_prefill_mfma_rope(const dar_shape* s, int T, const void* qr, const void* kr,
                                     const void* v, const void* kd, const void* vd, void* o,
                                     float* lse, const float* knorm, const float* dnorm,

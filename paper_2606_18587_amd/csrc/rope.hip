@@ -640,13 +640,180 @@ hipError_t launch_prefill_rope_valu(const T* qr, const T* kr, const T* v, const 
     return hipGetLastError();
 }
 
+// ---- chunked prefill into a split cache with the rotary embedding
+
+// Kd / Vd rows [out_row0, out_row0 + nrows) of each (batch, KV head), row =
+// position, either from full-d rows (in_k / in_v row in_row0 + t, in_stride
+// rows a head: the latent is projected as in rope_lift_lds_kernel) or, when
+// lat_k is given, from the cache's latents (lat_k / lat_v row out_row0 + t,
+// lat_stride rows a head); then lifted with W_up by fp32 FMAs in increasing
+// latent column, and the keys rotated at their positions. Grid
+// (ceil(nrows / 32), B*Hkv), 256 threads, dynamic LDS (2 d dd + 32 d +
+// 32 dd) floats.
+template <typename T>
+__global__ __launch_bounds__(256) void rope_lift_span_kernel(
+    const T* __restrict__ in_k, const T* __restrict__ in_v, int in_stride, int in_row0,
+    const T* __restrict__ lat_k, const T* __restrict__ lat_v, int lat_stride,
+    const T* __restrict__ wd, const T* __restrict__ wu, T* __restrict__ kd, T* __restrict__ vd,
+    int out_stride, int out_row0, int nrows, const float* __restrict__ tab, int Hkv, int d, int dd,
+    int r) {
+    extern __shared__ float lsh[];
+    float* wD = lsh;              // [d][dd]
+    float* wU = wD + d * dd;      // [dd][d]
+    float* xs = wU + dd * d;      // [32][d]: input rows, then lifted rows
+    float* cs = xs + 32 * d;      // [32][dd]
+    const int tid = lane_id_x();
+    const int blk = wg_id_x(), bg = wg_id_y();
+    const int g = bg % Hkv;
+    const T* wdg = wd + (size_t)g * d * dd;
+    const T* wug = wu ? wu + (size_t)g * dd * d : nullptr;
+    for (int idx = tid; idx < d * dd; idx += 256) {
+        wD[idx] = elem<T>::load(wdg + idx);
+        const int c = idx / d, e = idx - (idx / d) * d;  // wU[c][e]
+        wU[idx] = wug ? elem<T>::load(wug + idx) : elem<T>::load(wdg + (size_t)e * dd + c);
+    }
+    const int t0 = blk * 32;
+    const int nrow = imin(32, nrows - t0);
+    const int nch = d >> 3;
+    for (int which = 0; which < 2; ++which) {
+        T* dst = (which == 0 ? kd : vd) + ((size_t)bg * out_stride + out_row0 + t0) * d;
+        if (lat_k) {
+            const T* lat = (which == 0 ? lat_k : lat_v) + ((size_t)bg * lat_stride + out_row0 + t0) * dd;
+            for (int idx = tid; idx < nrow * dd; idx += 256) cs[idx] = elem<T>::load(lat + idx);
+            __syncthreads();
+        } else {
+            const T* src = (which == 0 ? in_k : in_v) + ((size_t)bg * in_stride + in_row0 + t0) * d;
+            for (int idx = tid; idx < nrow * nch; idx += 256) {
+                float a[8];
+                vec8<T>::load(src + (size_t)idx * 8, a);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) xs[idx * 8 + j] = a[j];
+            }
+            __syncthreads();
+            // Eq. 1
+            for (int idx = tid; idx < nrow * dd; idx += 256) {
+                const int tt = idx / dd, c = idx - (idx / dd) * dd;
+                float acc = 0.f;
+                for (int e = 0; e < d; ++e) acc = __builtin_fmaf(xs[tt * d + e], wD[e * dd + c], acc);
+                cs[idx] = elem<T>::to_f32(elem<T>::from_f32(acc));
+            }
+            __syncthreads();
+        }
+        // Eq. 2
+        for (int idx = tid; idx < nrow * d; idx += 256) {
+            const int tt = idx / d, e = idx - (idx / d) * d;
+            float acc = 0.f;
+            for (int c = 0; c < dd; ++c) acc = __builtin_fmaf(cs[tt * dd + c], wU[c * d + e], acc);
+            xs[idx] = acc;
+        }
+        __syncthreads();
+        // rotate (keys) and store
+        for (int idx = tid; idx < nrow * nch; idx += 256) {
+            const int row = idx / nch, ch = idx - (idx / nch) * nch;
+            float a[8], b[8], y[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) a[j] = xs[row * d + ch * 8 + j];
+            if (which == 0) {
+                const int hc = r >> 4;
+                if (ch < 2 * hc) {
+                    const int pc = ch < hc ? ch + hc : ch - hc;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) b[j] = xs[row * d + pc * 8 + j];
+                }
+                rotate_chunk(ch, r, a, b, tab + (size_t)(out_row0 + t0 + row) * r, y);
+            } else {
+#pragma unroll
+                for (int j = 0; j < 8; ++j) y[j] = a[j];
+            }
+            vec8<T>::store(dst + (size_t)row * d + ch * 8, y);
+        }
+        __syncthreads();
+    }
+}
+
+// Largest L2 norm of the stored rows of each 32-position block (the
+// matrix-core kernel's fixed softmax reference): row t of x (stride rows a
+// head) holds position row_pos0 + t, t < nrows; block b covers positions
+// [32 b, 32 b + 32) and lands in out[bg * out_blocks + b]. Grid
+// (blocks met by the rows, B*Hkv), 256 threads = 32 rows x 8.
+template <typename T>
+__global__ __launch_bounds__(256) void block_norm_kernel(const T* __restrict__ x, int stride,
+                                                         int row_pos0, int nrows, int d,
+                                                         float* __restrict__ out, int out_blocks) {
+    __shared__ float rsq[32];
+    const int tid = lane_id_x();
+    const int row = tid >> 3, sub = tid & 7;
+    const int bg = wg_id_y();
+    const int b = (row_pos0 >> 5) + wg_id_x();
+    const int pos = 32 * b + row;
+    float sq = 0.f;
+    if (pos >= row_pos0 && pos < row_pos0 + nrows) {
+        const T* xr = x + ((size_t)bg * stride + (pos - row_pos0)) * d;
+        for (int e = sub; e < d; e += 8) {
+            const float v = elem<T>::load(xr + e);
+            sq = __builtin_fmaf(v, v, sq);
+        }
+    }
+    sq += __shfl_xor(sq, 1, 64);
+    sq += __shfl_xor(sq, 2, 64);
+    sq += __shfl_xor(sq, 4, 64);
+    if (sub == 0) rsq[row] = sq;
+    __syncthreads();
+    if (tid == 0) {
+        float m = 0.f;
+        for (int i = 0; i < 32; ++i) m = fmaxf(m, rsq[i]);
+        out[(size_t)bg * out_blocks + b] = sqrtf(m);
+    }
+}
+
+template <typename T>
+hipError_t launch_rope_chunk_prepass(const T* q, const T* ctx_k, const T* ctx_v, const T* k_lat,
+                                     const T* v_lat, int cap, const T* wd, const T* wu,
+                                     const float* tab, T* qr, T* kr, T* kd, T* vd, float* knorm,
+                                     float* dnorm, int B, int Hq, int Hkv, int d, int dd, int w,
+                                     int r, int len, int n, int kv0, hipStream_t st) {
+    if (!rope_vec_ok(d, r)) return hipErrorNotSupported;
+    const int Tc = len + n - kv0, T_ = len + n, Td = T_ - w > 0 ? T_ - w : 0;
+    const int lat0 = len - w > 0 ? len - w : 0;  // cached latents: positions < lat0
+    const int nt = 32 * (d / 8);
+    hipLaunchKernelGGL(rope_rows_vec_kernel<T>, dim3((n + 31) / 32, B * Hq), dim3(nt), 0, st, q, qr,
+                       (float*)nullptr, tab, n, d, r, len);
+    hipLaunchKernelGGL(rope_rows_vec_kernel<T>, dim3((Tc + 31) / 32, B * Hkv), dim3(nt), 0, st, ctx_k,
+                       kr, (float*)nullptr, tab, Tc, d, r, kv0);
+    const int nkb = (T_ + 31) / 32;
+    hipLaunchKernelGGL(block_norm_kernel<T>, dim3(nkb - (kv0 >> 5), B * Hkv), dim3(256), 0, st,
+                       (const T*)kr, Tc, kv0, Tc, d, knorm, nkb);
+    if (Td > 0) {
+        const size_t lds = sizeof(float) * (2 * (size_t)d * dd + 32 * (size_t)d + 32 * (size_t)dd);
+        if (lds > 65536) return hipErrorNotSupported;
+        const int ncache = lat0 < Td ? lat0 : Td;
+        if (ncache > 0)
+            hipLaunchKernelGGL(rope_lift_span_kernel<T>, dim3((ncache + 31) / 32, B * Hkv), dim3(256),
+                               lds, st, (const T*)nullptr, (const T*)nullptr, 0, 0, k_lat, v_lat, cap,
+                               wd, wu, kd, vd, Td, 0, ncache, tab, Hkv, d, dd, r);
+        if (Td > lat0)
+            hipLaunchKernelGGL(rope_lift_span_kernel<T>, dim3((Td - lat0 + 31) / 32, B * Hkv),
+                               dim3(256), lds, st, ctx_k, ctx_v, Tc, lat0 - kv0, (const T*)nullptr,
+                               (const T*)nullptr, 0, wd, wu, kd, vd, Td, lat0, Td - lat0, tab, Hkv,
+                               d, dd, r);
+        hipLaunchKernelGGL(block_norm_kernel<T>, dim3((Td + 31) / 32, B * Hkv), dim3(256), 0, st,
+                           (const T*)kd, Td, 0, Td, d, dnorm, (Td + 31) / 32);
+    }
+    return hipGetLastError();
+}
+
 #define DAR_ROPE_INST(T)                                                                            \
     template hipError_t launch_rope_prepass<T>(const T*, const T*, const T*, const T*, const T*,   \
                                                const float*, T*, T*, T*, T*, float*, float*, int,  \
                                                int, int, int, int, int, int, int, int, hipStream_t); \
     template hipError_t launch_prefill_rope_valu<T>(const T*, const T*, const T*, const T*,        \
                                                     const T*, T*, float*, int, int, int, int, int, \
-                                                    int, hipStream_t);
+                                                    int, hipStream_t);                             \
+    template hipError_t launch_rope_chunk_prepass<T>(const T*, const T*, const T*, const T*,       \
+                                                     const T*, int, const T*, const T*,           \
+                                                     const float*, T*, T*, T*, T*, float*, float*, \
+                                                     int, int, int, int, int, int, int, int, int,  \
+                                                     int, hipStream_t);
 DAR_ROPE_INST(float)
 DAR_ROPE_INST(bf16_t)
 #undef DAR_ROPE_INST

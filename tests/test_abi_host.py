@@ -33,6 +33,7 @@ def test_exports_every_declared_symbol():
                           "dar_attn_prefill_backward", "dar_prefill_workspace_bytes",
                           "dar_decode_workspace_bytes", "dar_prefill_backward_workspace_bytes",
                           "dar_attn_prefill_chunk", "dar_prefill_chunk_workspace_bytes",
+                          "dar_attn_prefill_chunk_rope", "dar_prefill_chunk_rope_workspace_bytes",
                           "dar_rope_table", "dar_attn_prefill_rope", "dar_attn_decode_rope",
                           "dar_attn_prefill_shared", "dar_cache_append_shared",
                           "dar_attn_decode_shared", "dar_cache_append_paged",
@@ -342,6 +343,47 @@ def test_chunk_rejects_before_any_launch():
     assert call_chunk(s, c2, n=2) == dar.DAR_E_ARG and c2.len == 0
     # bf16 rows of an odd number of elements cannot be copied in 4-byte words
     assert call_chunk(S(d=63, dd=16), cache_struct(), n=2) == dar.DAR_E_UNSUPPORTED
+
+
+def test_chunk_rope_workspace_size():
+    """Context rows from the window's oldest position rounded down to 32 (len
+    with w = 0), rotated chunk queries, rotated context keys, lifted distant
+    keys and values (positions < len + n - w), block norms; 256-byte aligned."""
+    al = lambda x: (x + 255) // 256 * 256
+    for (B, Hq, Hkv, d, dd, w), (L, n) in [((2, 4, 2, 64, 16, 40), (100, 7)),
+                                           ((2, 4, 2, 64, 16, 40), (3, 50)),
+                                           ((1, 8, 2, 128, 32, 0), (70, 9))]:
+        s = dar.make_shape(B, Hq, Hkv, d, dd, w, torch.bfloat16)
+        kv0 = (max(0, L - w) // 32) * 32 if w > 0 else L
+        Tc, T = L + n - kv0, L + n
+        Td = max(T - w, 0)
+        ctx = al(B * Hkv * Tc * d * 2)
+        want = (3 * ctx + al(B * Hq * n * d * 2) + 2 * al(B * Hkv * Td * d * 2)
+                + al(B * Hkv * ((T + 31) // 32) * 4) + al(B * Hkv * ((Td + 31) // 32 + 1) * 4))
+        assert dar.dar_prefill_chunk_rope_workspace_bytes(s, L, n) == want
+    assert dar.dar_prefill_chunk_rope_workspace_bytes(S(), 10, 0) == 0
+    assert dar.dar_prefill_chunk_rope_workspace_bytes(S(), -1, 4) == 0
+
+
+@no_gpu
+def test_chunk_rope_rejects_before_any_launch():
+    def call(shape, c, n=2, r=16, n_pos=128, table=FAKE, q=FAKE, ws_bytes=1 << 30, null_rope=False):
+        rs = dar.DarRopeStruct(r, n_pos, table)
+        return dar.lib.dar_attn_prefill_chunk_rope(
+            ctypes.byref(shape), ctypes.byref(c), None if null_rope else ctypes.byref(rs), n, q, FAKE,
+            FAKE, FAKE, None, FAKE, None, FAKE, ws_bytes, None)
+    s = S()
+    c = cache_struct(cap=64, length=60)
+    assert call(s, c, n=5) == dar.DAR_E_CAPACITY and c.len == 60
+    assert call(s, c, null_rope=True) == dar.DAR_E_ARG and c.len == 60
+    assert call(s, c, n_pos=61) == dar.DAR_E_ARG and c.len == 60          # past the table
+    assert call(s, c, r=5) == dar.DAR_E_ARG and c.len == 60
+    assert call(s, c, table=None) == dar.DAR_E_ARG and c.len == 60
+    assert call(s, c, q=MISALIGNED) == dar.DAR_E_ARG and c.len == 60
+    assert call(s, c, ws_bytes=64) == dar.DAR_E_WORKSPACE and c.len == 60
+    assert call(s, c, r=8) == dar.DAR_E_UNSUPPORTED and c.len == 60       # r % 16
+    assert call(S(dtype=torch.float32), c) == dar.DAR_E_UNSUPPORTED and c.len == 60
+    assert call(S(d=80, dd=20), c) == dar.DAR_E_UNSUPPORTED and c.len == 60
 
 
 def test_rope_workspace_size():
