@@ -450,7 +450,37 @@ def main():
                  "cache_len": [L0, cache.len], "us": round(ch_ms * 1e3, 1),
                  "tflops": round(ctf, 2), "frac_bf16_peak": round(ctf / PEAK_BF16_TFLOPS, 4),
                  "alg_flop": cfl}
-        del cws, cq, ck, cv, co
+        # the same chunks through the paged cache: a paged copy of the cache as
+        # the dense calls left it (64-token pages, identity block table), each
+        # sequence taking CHUNK_N tokens per call
+        ps = 64
+        maxb = (cache.cap + ps - 1) // ps
+        pcache = dar.DarPagedCache(dw.B, dw.Hkv, dw.d, dw.dd, dw.w, ps, maxb, dw.B * maxb,
+                                   torch.bfloat16)
+        for src, dst in ((cache.k_lat, pcache.k_pool), (cache.v_lat, pcache.v_pool)):
+            full = torch.zeros(dw.B, dw.Hkv, maxb * ps, dw.dd, dtype=torch.bfloat16, device=dev)
+            full[:, :, :cache.cap] = src
+            dst.copy_(full.view(dw.B, dw.Hkv, maxb, ps, dw.dd).permute(0, 2, 1, 3, 4)
+                      .reshape(dw.B * maxb, dw.Hkv, ps, dw.dd))
+            del full
+        pcache.k_win.copy_(cache.k_win)
+        pcache.v_win.copy_(cache.v_win)
+        pcache.block_table.copy_(torch.arange(dw.B * maxb, dtype=torch.int32, device=dev)
+                                 .view(dw.B, maxb))
+        Lp = max(0, cache.cap - (n_chunk + 1) * CHUNK_N)
+        Lp = min(Lp, cache.len)
+        pcache.lens.fill_(Lp)
+        pws = torch.empty(dar.dar_prefill_chunk_paged_workspace_bytes(dshape, pcache.cap, CHUNK_N),
+                          dtype=torch.uint8, device=dev)
+        run_pchunk = lambda i: dar.dar_attn_prefill_chunk_paged(pcache, cq, ck, cv, dwd, o=co, ws=pws)
+        run_pchunk(0)  # warm-up
+        pch_ms = timed(run_pchunk, n_chunk)
+        pfl = np.mean([chunk_flops(dw.B, dw.Hq, Lp + (c + 1) * CHUNK_N, CHUNK_N, dw.d, dw.dd, dw.w)
+                       for c in range(n_chunk)])
+        chunk["paged"] = {"page_size": ps, "cache_len": [Lp + CHUNK_N, Lp + (n_chunk + 1) * CHUNK_N],
+                          "us": round(pch_ms * 1e3, 1),
+                          "tflops": round(pfl / (pch_ms * 1e-3) / 1e12, 2)}
+        del pcache, pws, cws, cq, ck, cv, co
 
     pre_us = float(pre_ms * 1e3)
     dec_us = float(dec_ms * 1e3)

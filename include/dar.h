@@ -171,8 +171,10 @@ dar_status dar_cache_append(const dar_shape* s, dar_cache* c, const void* k_new,
  *   dar_attn_prefill); w_up: [Hkv][d_down][d] or NULL (tied).
  *   ws: device workspace of at least dar_prefill_chunk_workspace_bytes(s, len,
  *   n) bytes (caller-owned, overwritten): a copy of the ring's tokens and the
- *   new ones, and a prefill workspace of len + n positions (the cache's latents
- *   are re-laid out into it).
+ *   new ones, and, on the matrix-core shapes (bf16, d in {64, 128}, d_down in
+ *   {16, 32}), the block norms of the keys (the cache's latents are read in
+ *   place), else a prefill workspace of len + n positions (the cache's
+ *   latents are re-laid out into it).
  * Fails with DAR_E_CAPACITY if len + n > cap (nothing is enqueued). Supported:
  * as dar_attn_prefill, with d * (element size) a multiple of 4 bytes. */
 dar_status dar_attn_prefill_chunk(const dar_shape* s, dar_cache* c, int n, const void* q,
@@ -310,6 +312,36 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
                                  const void* w_down, const void* w_up, void* o, void* ws,
                                  size_t ws_bytes, hipStream_t stream);
 
+/* Chunked prefill over a paged cache (serving: several sequences of different
+ * lengths taking their next prompt tokens in one call). Sequence b takes
+ * n_b = n_new[b] new tokens (n_new: device int [B], each clamped to [0, n];
+ * NULL: every sequence takes n) at positions lens[b]..lens[b]+n_b-1, with
+ * queries q [B][Hq][n][d] and keys and values k_new, v_new [B][Hkv][n][d]
+ * (rows at or past n_b are never read). Every new row of sequence b attends
+ * to that sequence's positions 0..i under Eq. 3-4 exactly as row i of
+ * dar_attn_prefill over its whole sequence would (window tokens from its
+ * ring and the chunk at full dimension, older ones from its latent pages,
+ * Eq. 1, absorbed). The cache is extended as n_b single-token
+ * dar_cache_append_paged calls would extend it (bit-identical ring and
+ * latent pages), then lens[b] += n_b on the device.
+ *   o [B][Hq][n][d] (output; rows at or past n_b are not written); lse: NULL
+ *   or fp32 [B][Hq][n] (output, as for dar_attn_prefill).
+ *   A sequence with n_b > 0 whose chunk does not fit (lens[b] < 0, or
+ *   lens[b] + n_b > max_blocks * page_size) stores nothing, gets NaN rows
+ *   and is marked overflowed (lens[b] = -1 - lens[b] if it was >= 0).
+ *   The pages of every block written must be mapped in block_table.
+ *   ws: at least dar_prefill_chunk_paged_workspace_bytes(s, max_blocks *
+ *   page_size, n) bytes (caller-owned, overwritten): the window's and the
+ *   chunk's rows of every sequence and the block norms.
+ * The latent pages are read in place (nothing is copied out of them).
+ * Supported: the matrix-core shapes (bf16, d in {64, 128}, d_down in {16,
+ * 32}); others return DAR_E_UNSUPPORTED. */
+dar_status dar_attn_prefill_chunk_paged(const dar_shape* s, const dar_paged_cache* c, int n,
+                                        const int* n_new, const void* q, const void* k_new,
+                                        const void* v_new, const void* w_down, const void* w_up,
+                                        void* o, float* lse, void* ws, size_t ws_bytes,
+                                        hipStream_t stream);
+
 /* Single shared latent (the Limitations section's cache): one d_down latent
  * per token and KV head, c_j = h_j W_down of Eq. 1, from which both the
  * distant key and the distant value are computed. With the lift of Eq. 2
@@ -369,6 +401,7 @@ size_t dar_prefill_backward_workspace_bytes(const dar_shape* s, int T);
 size_t dar_prefill_chunk_workspace_bytes(const dar_shape* s, int len, int n);
 size_t dar_prefill_rope_workspace_bytes(const dar_shape* s, int T);
 size_t dar_prefill_chunk_rope_workspace_bytes(const dar_shape* s, int len, int n);
+size_t dar_prefill_chunk_paged_workspace_bytes(const dar_shape* s, int cap, int n);
 
 /* Static English text for a status code. */
 const char* dar_status_string(dar_status st);

@@ -95,6 +95,10 @@ def _load():
     lib.dar_cache_append_paged.argtypes = [shp, pcp, vp, vp, vp, vp]
     lib.dar_attn_decode_paged.restype = ci
     lib.dar_attn_decode_paged.argtypes = [shp, pcp] + [vp] * 5 + [sz, vp]
+    lib.dar_attn_prefill_chunk_paged.restype = ci
+    lib.dar_attn_prefill_chunk_paged.argtypes = [shp, pcp, ci] + [vp] * 9 + [sz, vp]
+    lib.dar_prefill_chunk_paged_workspace_bytes.restype = sz
+    lib.dar_prefill_chunk_paged_workspace_bytes.argtypes = [shp, ci, ci]
     lib.dar_attn_prefill_ragged.restype = ci
     lib.dar_attn_prefill_ragged.argtypes = [shp, ci] + [vp] * 9 + [sz, vp]
     lib.dar_prefill_rope_workspace_bytes.restype = sz
@@ -623,6 +627,44 @@ def dar_attn_decode_paged(cache: DarPagedCache, q, w_down, w_up=None, o=None, ws
     if st != DAR_OK:
         raise DarError(st, "dar_attn_decode_paged")
     return o
+
+
+def dar_prefill_chunk_paged_workspace_bytes(shape, cap, n) -> int:
+    return int(lib.dar_prefill_chunk_paged_workspace_bytes(ctypes.byref(shape), int(cap), int(n)))
+
+
+def dar_attn_prefill_chunk_paged(cache: DarPagedCache, q, k_new, v_new, w_down, w_up=None,
+                                 n_new=None, o=None, lse=None, return_lse=False, ws=None,
+                                 stream=None):
+    """Chunked prefill over a paged cache: sequence b takes n_new[b] (device
+    int32 [B], each <= n; None: all n) new tokens at positions lens[b]..,
+    q [B,Hq,n,d], k_new/v_new [B,Hkv,n,d]; lens advance on the device.
+    Returns o [B,Hq,n,d] (rows past n_new[b] not written), or (o, lse)."""
+    B, Hq, n, d = q.shape
+    Hkv = cache.Hkv
+    shape = make_shape(B, Hq, Hkv, d, cache.d_down, cache.w, q.dtype)
+    for name, t in (("k_new", k_new), ("v_new", v_new)):
+        if tuple(t.shape) != (B, Hkv, n, d) or t.dtype != q.dtype:
+            raise ValueError("%s: expected %s %s" % (name, (B, Hkv, n, d), q.dtype))
+    if (B, d) != (cache.B, cache.d):
+        raise ValueError("q does not match the cache")
+    if n_new is not None and (n_new.dtype != torch.int32 or tuple(n_new.shape) != (B,)):
+        raise ValueError("n_new: expected int32 [%d]" % B)
+    if o is None:
+        o = torch.empty_like(q)
+    if return_lse and lse is None:
+        lse = torch.empty(B, Hq, n, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = _workspace(dar_prefill_chunk_paged_workspace_bytes(shape, cache.cap, n), q.device)
+    cs = cache.struct()
+    st = lib.dar_attn_prefill_chunk_paged(ctypes.byref(shape), ctypes.byref(cs), int(n),
+                                          _ptr(n_new), _ptr(q), _ptr(k_new), _ptr(v_new),
+                                          _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(lse), _ptr(ws),
+                                          0 if ws is None else ws.numel() * ws.element_size(),
+                                          _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_prefill_chunk_paged")
+    return (o, lse) if return_lse else o
 
 
 def dar_attn_prefill_ragged(q, k, v, w_down, w_up, w, seq_lens, o=None, ws=None, stream=None,

@@ -36,6 +36,14 @@ hipError_t launch_prefill_mfma(const dar_shape* s, const PrefillGeo& geo, const 
                                const float* knorm, const void* consts, hipStream_t st,
                                const void* wv = nullptr);
 bool prefill_mfma_rope_supported(const dar_shape* s);
+// The attention kernel on a chunk (rows q0.., geo as for launch_prefill_mfma
+// with k / v the context rows) with the distant latents read from lc; for a
+// paged lc the per-sequence geometry comes from lc.lens / lc.n_new and geo.Tkv
+// is the context rows' stride (w + n).
+hipError_t launch_prefill_mfma_cache(const dar_shape* s, const PrefillGeo& geo, const LatCache& lc,
+                                     const void* q, const void* ctx_k, const void* ctx_v,
+                                     const void* wd, const void* wu, void* o, float* lse,
+                                     const float* cnorm, const float* knorm, hipStream_t st);
 // The matrix-core rotary attention over a chunk geometry (see PrefillGeo):
 // qr the rotated chunk queries, kr / v the rotated keys and the values of the
 // context rows (from geo.kv0), kd / vd the distant rows (positions 0..).
@@ -159,12 +167,15 @@ hipError_t run_prefill(const dar_shape* s, const PrefillGeo& geo, const void* q,
 }
 
 // Chunked prefill workspace: the context rows (the ring's tokens from kv0 on,
-// then the new ones) for K and V, then the prefill workspace of len + n
-// positions; every part 256-byte aligned.
+// then the new ones) for K and V, then either (matrix-core shapes, latents
+// read in place from the cache) the two block-norm arrays of nblk blocks a
+// head, or the prefill workspace of len + n positions; every part 256-byte
+// aligned.
 struct ChunkWs {
-    size_t ctx_k_off, ctx_v_off, pre_off, bytes;
+    size_t ctx_k_off, ctx_v_off, pre_off, cnorm_off, knorm_off, bytes;
     PrefillWs pre;
-    int kv0, Tc;
+    int kv0, Tc, nblk;
+    bool in_place;
 };
 
 // Chunked prefill with the rotary embedding: the context rows (from kv0, the
@@ -207,9 +218,40 @@ ChunkWs chunk_ws_layout(const dar_shape* s, int len, int n) {
     const size_t ctx = al((size_t)s->B * s->Hkv * L.Tc * s->d * esize_of(s->dtype));
     L.ctx_k_off = 0;
     L.ctx_v_off = ctx;
+    L.in_place = prefill_mfma_supported(s);
+    if (L.in_place) {
+        L.nblk = (len + n + 31) / 32;
+        const size_t norms = al((size_t)s->B * s->Hkv * L.nblk * sizeof(float));
+        L.cnorm_off = 2 * ctx;
+        L.knorm_off = L.cnorm_off + norms;
+        L.bytes = L.knorm_off + norms;
+        return L;
+    }
     L.pre_off = 2 * ctx;
     L.pre = prefill_ws_layout(s->B, s->Hkv, len + n, s->d_down, s->w, esize_of(s->dtype));
     L.bytes = L.pre_off + L.pre.bytes;
+    return L;
+}
+
+// Paged chunked prefill workspace: the context rows of every sequence (w + n
+// rows a head), then the two block-norm arrays (a whole sequence's capacity
+// of 32-position blocks a head).
+struct ChunkPagedWs {
+    size_t ctx_k_off, ctx_v_off, cnorm_off, knorm_off, bytes;
+    int nblk;
+};
+
+ChunkPagedWs chunk_paged_ws_layout(const dar_shape* s, int cap, int n) {
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    ChunkPagedWs L{};
+    const size_t ctx = al((size_t)s->B * s->Hkv * (s->w + n) * s->d * esize_of(s->dtype));
+    L.nblk = (int)(((long long)cap + 31) / 32);
+    const size_t norms = al((size_t)s->B * s->Hkv * L.nblk * sizeof(float));
+    L.ctx_k_off = 0;
+    L.ctx_v_off = ctx;
+    L.cnorm_off = 2 * ctx;
+    L.knorm_off = L.cnorm_off + norms;
+    L.bytes = L.knorm_off + norms;
     return L;
 }
 
@@ -471,6 +513,35 @@ dar_status dar_attn_prefill_chunk(const dar_shape* s, dar_cache* c, int n, const
     void* ctx_k = wsb + L.ctx_k_off;
     void* ctx_v = wsb + L.ctx_v_off;
     const int len = c->len;
+    if (L.in_place) {
+        // context rows first (the append below rewrites ring slots), then the
+        // append (every distant latent of the chunk's rows is then in the
+        // cache), the norms, and the attention reading the latents in place
+        const bf16_t* wd = (const bf16_t*)w_down;
+        hipError_t e = launch_chunk_gather<bf16_t>((const bf16_t*)c->k_win, (const bf16_t*)c->v_win,
+                                                   (const bf16_t*)k_new, (const bf16_t*)v_new,
+                                                   (bf16_t*)ctx_k, (bf16_t*)ctx_v, s->B, s->Hkv,
+                                                   s->d, s->w, len, n, L.kv0, stream);
+        if (e == hipSuccess)
+            e = launch_append<bf16_t>((const bf16_t*)k_new, (const bf16_t*)v_new, wd,
+                                      (bf16_t*)c->k_win, (bf16_t*)c->v_win, (bf16_t*)c->k_lat,
+                                      (bf16_t*)c->v_lat, s->B, s->Hkv, s->d, s->d_down, s->w,
+                                      c->cap, len, n, stream);
+        const LatCache lc{(const bf16_t*)c->k_lat, (const bf16_t*)c->v_lat, nullptr, nullptr, nullptr,
+                          c->cap, 0, 0, 0, L.nblk, L.nblk};
+        float* cnorm = (float*)(wsb + L.cnorm_off);
+        float* knorm = (float*)(wsb + L.knorm_off);
+        if (e == hipSuccess)
+            e = launch_chunk_norms(lc, (const bf16_t*)ctx_k, L.Tc, cnorm, knorm, s->B, s->Hkv, s->d,
+                                   s->d_down, s->w, len, n, L.nblk, stream);
+        const PrefillGeo geo{len, n, L.kv0, L.Tc, 0, 0, nullptr, nullptr};
+        if (e == hipSuccess)
+            e = launch_prefill_mfma_cache(s, geo, lc, q, ctx_k, ctx_v, w_down, w_up, o, lse, cnorm,
+                                          knorm, stream);
+        if (e != hipSuccess) return DAR_E_HIP;
+        c->len += n;
+        return DAR_OK;
+    }
     // rows len..len+n-1; keys/values from the context rows; latents of the
     // tokens that left the window before this chunk from the cache
     const PrefillGeo geo{len, n, L.kv0, L.Tc, L.kv0, c->cap, c->k_lat, c->v_lat};
@@ -917,6 +988,62 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
         e = launch_decode_combine<bf16_t>((const float*)ws, (const bf16_t*)w_down,
                                           (const bf16_t*)w_up, (bf16_t*)o, s->B, s->Hq, s->Hkv,
                                           s->d, s->d_down, P, stream, nullptr, c->lens, counts);
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+size_t dar_prefill_chunk_paged_workspace_bytes(const dar_shape* s, int cap, int n) {
+    if (check_shape(s) != DAR_OK || cap < 1 || n < 1) return 0;
+    return chunk_paged_ws_layout(s, cap, n).bytes;
+}
+
+dar_status dar_attn_prefill_chunk_paged(const dar_shape* s, const dar_paged_cache* c, int n,
+                                        const int* n_new, const void* q, const void* k_new,
+                                        const void* v_new, const void* w_down, const void* w_up,
+                                        void* o, float* lse, void* ws, size_t ws_bytes,
+                                        hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    st = check_paged(s, c);
+    if (st != DAR_OK) return st;
+    if (n < 1) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(k_new) || !dev_ok(v_new) || !dev_ok(w_down) || !dev_ok(o))
+        return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if (lse && !aligned16(lse)) return DAR_E_ARG;
+    if (n_new && ((uintptr_t)n_new & 3u)) return DAR_E_ARG;
+    if (!prefill_mfma_supported(s)) return DAR_E_UNSUPPORTED;
+    const int cap = c->page_size * c->max_blocks;
+    if ((long long)s->w + n > 0x7fffffffLL / 64) return DAR_E_UNSUPPORTED;
+    const ChunkPagedWs L = chunk_paged_ws_layout(s, cap, n);
+    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+    clear_hip_error();
+    char* wsb = (char*)ws;
+    bf16_t* ctx_k = (bf16_t*)(wsb + L.ctx_k_off);
+    bf16_t* ctx_v = (bf16_t*)(wsb + L.ctx_v_off);
+    float* cnorm = (float*)(wsb + L.cnorm_off);
+    float* knorm = (float*)(wsb + L.knorm_off);
+    const LatCache lc{(const bf16_t*)c->k_pool, (const bf16_t*)c->v_pool, c->block_table, c->lens,
+                      n_new, cap, c->max_blocks, __builtin_ctz((unsigned)c->page_size), c->n_pages,
+                      L.nblk, L.nblk};
+    // context rows, then the append, the norms and the attention (each
+    // reading lens as it was), then the lengths advance
+    hipError_t e = launch_chunk_gather_paged((const bf16_t*)c->k_win, (const bf16_t*)c->v_win,
+                                             (const bf16_t*)k_new, (const bf16_t*)v_new, ctx_k,
+                                             ctx_v, lc, s->B, s->Hkv, s->d, s->w, n, stream);
+    if (e == hipSuccess)
+        e = launch_append_chunk_paged((const bf16_t*)k_new, (const bf16_t*)v_new,
+                                      (const bf16_t*)w_down, (bf16_t*)c->k_win, (bf16_t*)c->v_win,
+                                      (bf16_t*)c->k_pool, (bf16_t*)c->v_pool, lc, s->B, s->Hkv,
+                                      s->d, s->d_down, s->w, n, stream);
+    if (e == hipSuccess)
+        e = launch_chunk_norms(lc, ctx_k, s->w + n, cnorm, knorm, s->B, s->Hkv, s->d, s->d_down,
+                               s->w, 0, n, L.nblk, stream);
+    const PrefillGeo geo{0, n, 0, s->w + n, 0, 0, nullptr, nullptr};
+    if (e == hipSuccess)
+        e = launch_prefill_mfma_cache(s, geo, lc, q, ctx_k, ctx_v, w_down, w_up, o, lse, cnorm,
+                                      knorm, stream);
+    if (e == hipSuccess) e = launch_lens_advance(c->lens, n_new, s->B, cap, n, stream);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 

@@ -47,6 +47,29 @@ struct PagedArgs {
     int* counts;   // [B * Hkv]: partial records of each (sequence, KV head) (decode)
 };
 
+// Latents that the chunked prefill reads in place, after the chunk's own
+// window exits have been appended (so every distant latent is in the cache):
+//   dense (bt == nullptr): k, v [B][Hkv][cap][dd], every sequence holding
+//     the same number of tokens (the call's len);
+//   paged: k, v are the pools [n_pages][Hkv][ps][dd] (ps = 1 << ps_shift),
+//     token e of sequence b in page bt[b * maxb + e / ps]; each sequence has
+//     its own geometry: lens[b] tokens held before the chunk, n_new[b] new
+//     ones (n_new == nullptr: every sequence takes the call's n), capacity cap
+//     tokens. A sequence with n_new[b] > 0 and lens[b] < 0 or
+//     lens[b] + n_new[b] > cap is not served (its rows are NaN).
+// ncb, nkb: 32-position blocks per (batch, KV head) of the latent-key and
+// context-key norm arrays the attention reads.
+struct LatCache {
+    const bf16_t* k;
+    const bf16_t* v;
+    const int* bt;
+    const int* lens;
+    const int* n_new;
+    int cap;
+    int maxb, ps_shift, n_pages;
+    int ncb, nkb;
+};
+
 // Where the rows, keys/values and latents of a prefill come from. Rows
 // r = 0..n_rows-1 are the queries at positions q0 + r (T = q0 + n_rows
 // positions in all); k and v row t holds position kv0 + t (t < Tkv); the
@@ -240,6 +263,33 @@ hipError_t launch_rope_chunk_prepass(const T* q, const T* ctx_k, const T* ctx_v,
                                      const float* tab, T* qr, T* kr, T* kd, T* vd, float* knorm,
                                      float* dnorm, int B, int Hq, int Hkv, int d, int dd, int w,
                                      int r, int len, int n, int kv0, hipStream_t st);
+// Chunked prefill reading the cached latents in place (bf16, the shapes of
+// prefill_mfma_supported). Per (batch, KV head) and 32-position block, the
+// largest L2 norm of the stored key latents of positions [0, T - w) (cnorm,
+// lc.ncb blocks a head) and of the context key rows of positions [kv0, T)
+// (knorm, lc.nkb blocks), where T = len + n and kv0 = max(0, len - w) (paged:
+// each sequence's own len and n); ctx_k row t of a head (kst rows a head)
+// holds position kv0 + t. nblk: blocks to cover (the largest T over 32).
+hipError_t launch_chunk_norms(const LatCache& lc, const bf16_t* ctx_k, int kst, float* cnorm,
+                              float* knorm, int B, int Hkv, int d, int dd, int w, int len, int n,
+                              int nblk, hipStream_t st);
+// Paged chunk: context rows of sequence b (the ring's tokens from
+// max(0, lens[b] - w), then its n_new[b] new ones; w + n rows a head).
+hipError_t launch_chunk_gather_paged(const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_new,
+                                     const bf16_t* v_new, bf16_t* ctx_k, bf16_t* ctx_v,
+                                     const LatCache& lc, int B, int Hkv, int d, int w, int n,
+                                     hipStream_t st);
+// Paged chunk append: the n_new[b] tokens of sequence b at positions
+// lens[b].., each window exit projected into its page slot (the arithmetic
+// of launch_append), the newest min(n_new[b], w) tokens into the ring. lens
+// is not changed (launch_lens_advance does it after the attention).
+hipError_t launch_append_chunk_paged(const bf16_t* k_new, const bf16_t* v_new, const bf16_t* wd,
+                                     bf16_t* k_win, bf16_t* v_win, bf16_t* k_pool, bf16_t* v_pool,
+                                     const LatCache& lc, int B, int Hkv, int d, int dd, int w, int n,
+                                     hipStream_t st);
+// lens[b] += n_new[b] (n_new == nullptr: n) for each sequence it fits; one that
+// does not fit (or was overflowed before) is marked -1 - lens[b].
+hipError_t launch_lens_advance(int* lens, const int* n_new, int B, int cap, int n, hipStream_t st);
 // Second stage of the split decodes: merges the S partial records of each
 // (batch, query head) and lifts the latent part (decode_combine_kernel).
 template <typename T>

@@ -811,3 +811,262 @@ template hipError_t launch_append_paged<bf16_t>(const bf16_t*, const bf16_t*, co
                                                 int*, int, int, int, int, int, hipStream_t);
 
 }  // namespace dar
+
+namespace dar {
+
+// ---------------------------------------------------------------------------
+// Chunked prefill reading the cached latents in place. The chunk's own window
+// exits are appended first (so every distant latent of its rows is in the
+// cache), the context rows (window tokens of the ring, then the new ones) are
+// gathered before that append overwrites the ring, and the norms below give
+// the attention kernel its score bounds.
+
+// Sum of squares of m bf16 values (m a multiple of 8, 16-byte aligned).
+__device__ __forceinline__ float sq_sum_bf16(const bf16_t* p, int m) {
+    float s = 0.f;
+    for (int j = 0; j < m; j += 8) {
+        const uint4 u = *reinterpret_cast<const uint4*>(p + j);
+        const uint32_t w4[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const float lo = __uint_as_float(w4[q] << 16), hi = __uint_as_float(w4[q] & 0xffff0000u);
+            s = __builtin_fmaf(lo, lo, s);
+            s = __builtin_fmaf(hi, hi, s);
+        }
+    }
+    return s;
+}
+
+// A sequence's geometry for this chunk: false when it takes no part (no new
+// tokens) or the chunk does not fit (overflowed before, or past capacity).
+__device__ __forceinline__ bool chunk_seq(const LatCache& lc, int b, int len, int n, int& L, int& nb) {
+    L = len;
+    nb = n;
+    if (!lc.lens) return true;
+    L = lc.lens[b];
+    nb = lc.n_new ? imin(imax(lc.n_new[b], 0), n) : n;
+    return nb > 0 && L >= 0 && L + nb <= lc.cap;
+}
+
+// Each wavefront takes kNormBlocks 32-position blocks of one (batch, KV head)
+// (all its latent loads issued before the first reduction); lanes l and
+// l + 32 take the two halves of the row of position 32 blk + l % 32.
+constexpr int kNormBlocks = 8;
+
+template <int DD>
+__global__ __launch_bounds__(256) void chunk_norms_kernel(LatCache lc, const bf16_t* __restrict__ ctx_k,
+                                                          int kst, float* __restrict__ cnorm,
+                                                          float* __restrict__ knorm, int Hkv, int d,
+                                                          int w, int len, int n, int nblk) {
+    const int bg = wg_id_y();
+    const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
+    const int tid = lane_id_x(), lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int blk0 = (wg_id_x() * 4 + wave) * kNormBlocks;
+    if (blk0 >= nblk) return;
+    int L, nb;
+    if (!chunk_seq(lc, b, len, n, L, nb)) return;
+    const int T = L + nb, Td = imax(T - w, 0), kv0 = imax(L - w, 0);
+    const int tl = lane & 31, hg = lane >> 5;
+    constexpr int NL = DD / 16;  // 16-byte loads per half row
+    // latent keys: every row of the wavefront's blocks requested at once
+    // (unconditional loads from a clamped address, zeroed after: a load
+    // under a branch would wait for all loads before it)
+    uint4 u[kNormBlocks][NL];
+    bool ok[kNormBlocks];
+#pragma unroll
+    for (int j = 0; j < kNormBlocks; ++j) {
+        const int p = (blk0 + j) * 32 + tl;
+        ok[j] = p < Td;
+        size_t row = 0;
+        if (lc.bt) {
+            const int page = ok[j] ? lc.bt[(size_t)b * lc.maxb + (p >> lc.ps_shift)] : -1;
+            ok[j] = ok[j] && page >= 0 && page < lc.n_pages;
+            if (ok[j]) row = ((((size_t)page) * Hkv + g) << lc.ps_shift) + (p & ((1 << lc.ps_shift) - 1));
+        } else if (ok[j]) {
+            row = (size_t)bg * lc.cap + p;
+        }
+        const bf16_t* src = lc.k + row * DD + hg * (DD / 2);
+#pragma unroll
+        for (int h = 0; h < NL; ++h) u[j][h] = *reinterpret_cast<const uint4*>(src + 8 * h);
+    }
+#pragma unroll
+    for (int j = 0; j < kNormBlocks; ++j) {
+        const int blk = blk0 + j;
+        if (blk < nblk && blk * 32 < Td) {  // wavefront-uniform
+            float n2 = 0.f;
+#pragma unroll
+            for (int h = 0; h < NL; ++h) {
+                const uint4 uu = ok[j] ? u[j][h] : make_uint4(0, 0, 0, 0);
+                const uint32_t w4[4] = {uu.x, uu.y, uu.z, uu.w};
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float lo = __uint_as_float(w4[q] << 16), hi = __uint_as_float(w4[q] & 0xffff0000u);
+                    n2 = __builtin_fmaf(lo, lo, n2);
+                    n2 = __builtin_fmaf(hi, hi, n2);
+                }
+            }
+            n2 += __shfl_xor(n2, 32, 64);
+            const float m = wave_max_dpp(n2);
+            if (lane == 0) cnorm[(size_t)bg * lc.ncb + blk] = sqrtf(m);
+        }
+    }
+    // context keys (the window and the chunk: a few blocks of each head)
+    for (int j = 0; j < kNormBlocks; ++j) {
+        const int blk = blk0 + j;
+        if (blk < nblk && blk * 32 < T && blk * 32 + 31 >= kv0) {  // wavefront-uniform
+            const int p = blk * 32 + tl;
+            float n2 = 0.f;
+            if (p < T && p >= kv0)
+                n2 = sq_sum_bf16(ctx_k + ((size_t)bg * kst + (p - kv0)) * d + hg * (d / 2), d / 2);
+            n2 += __shfl_xor(n2, 32, 64);
+            const float m = wave_max_dpp(n2);
+            if (lane == 0) knorm[(size_t)bg * lc.nkb + blk] = sqrtf(m);
+        }
+    }
+}
+
+hipError_t launch_chunk_norms(const LatCache& lc, const bf16_t* ctx_k, int kst, float* cnorm,
+                              float* knorm, int B, int Hkv, int d, int dd, int w, int len, int n,
+                              int nblk, hipStream_t st) {
+    if (nblk <= 0) return hipSuccess;
+    const int per_wg = 4 * kNormBlocks;
+    auto kern = dd == 16 ? chunk_norms_kernel<16> : chunk_norms_kernel<32>;
+    hipLaunchKernelGGL(kern, dim3((nblk + per_wg - 1) / per_wg, B * Hkv), dim3(256), 0, st, lc, ctx_k, kst,
+                       cnorm, knorm, Hkv, d, w, len, n, nblk);
+    return hipGetLastError();
+}
+
+// Paged chunk context rows, one thread per 4-byte word: row r of sequence b's
+// block holds position kv0 + r (kv0 = max(0, lens[b] - w)), from ring slot
+// (kv0 + r) % w below lens[b], else the new token kv0 + r - lens[b].
+__global__ __launch_bounds__(256) void chunk_gather_paged_kernel(
+    const bf16_t* __restrict__ k_win, const bf16_t* __restrict__ v_win, const bf16_t* __restrict__ k_new,
+    const bf16_t* __restrict__ v_new, bf16_t* __restrict__ ctx_k, bf16_t* __restrict__ ctx_v, LatCache lc,
+    int Hkv, int d, int w, int n) {
+    const int bg = wg_id_y(), b = bg / Hkv;
+    int L, nb;
+    if (!chunk_seq(lc, b, 0, n, L, nb)) return;
+    const int kv0 = imax(L - w, 0);
+    const int Tc = L + nb - kv0;
+    const int words = d / 2;
+    const int idx = wg_id_x() * 256 + lane_id_x();
+    if (idx >= Tc * words) return;
+    const int r = idx / words, wd4 = idx - (idx / words) * words;
+    const int p = kv0 + r;
+    const size_t src_row = p < L ? (size_t)bg * w + p % w : (size_t)bg * n + (p - L);
+    const uint32_t* sk = reinterpret_cast<const uint32_t*>(p < L ? k_win : k_new) + src_row * words;
+    const uint32_t* sv = reinterpret_cast<const uint32_t*>(p < L ? v_win : v_new) + src_row * words;
+    const size_t dst = ((size_t)bg * (w + n) + r) * words + wd4;
+    reinterpret_cast<uint32_t*>(ctx_k)[dst] = sk[wd4];
+    reinterpret_cast<uint32_t*>(ctx_v)[dst] = sv[wd4];
+}
+
+hipError_t launch_chunk_gather_paged(const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_new,
+                                     const bf16_t* v_new, bf16_t* ctx_k, bf16_t* ctx_v,
+                                     const LatCache& lc, int B, int Hkv, int d, int w, int n,
+                                     hipStream_t st) {
+    const long long words = (long long)(w + n) * (d / 2);
+    hipLaunchKernelGGL(chunk_gather_paged_kernel, dim3((unsigned)((words + 255) / 256), B * Hkv), dim3(256), 0,
+                       st, k_win, v_win, k_new, v_new, ctx_k, ctx_v, lc, Hkv, d, w, n);
+    return hipGetLastError();
+}
+
+// Paged chunk append (matrix-core projection): one wavefront per 32 new
+// tokens of one (sequence, KV head), the modes of append_mfma_kernel (0:
+// project and ring, safe when n <= w: the lane that reads a ring slot is the
+// one that rewrites it; 1: project only; 2: ring only). The window exit of
+// new token tt is position lens[b] + tt - w, written to its page slot.
+template <int D>
+__global__ __launch_bounds__(64) void append_chunk_paged_mfma_kernel(
+    const bf16_t* __restrict__ k_new, const bf16_t* __restrict__ v_new, const bf16_t* __restrict__ wd,
+    bf16_t* k_win, bf16_t* v_win, bf16_t* __restrict__ k_pool, bf16_t* __restrict__ v_pool, LatCache lc,
+    int Hkv, int dd, int w, int n, int mode) {
+    constexpr int KS = D / 16;
+    const int bg = wg_id_y();
+    const int b = bg / Hkv, g = bg - (bg / Hkv) * Hkv;
+    int L, nb;
+    if (!chunk_seq(lc, b, 0, n, L, nb)) return;
+    const int lane = lane_id_x();
+    const int tl = lane & 31, hg = lane >> 5;
+    const int tt = wg_id_x() * 32 + tl;  // new token index
+    const int ex = L + tt - w;           // position leaving the window
+    const bool valid = tt < nb;
+    int page = -1;
+    if (mode != 2 && valid && ex >= 0) page = lc.bt[(size_t)b * lc.maxb + (ex >> lc.ps_shift)];
+    const bool project = mode != 2 && valid && ex >= 0 && page >= 0 && page < lc.n_pages;
+    const bool to_ring = mode != 1 && valid && w > 0 && tt >= nb - w;
+    lbf16x8 wa[KS];
+    if (mode != 2) load_wd_operand<D>(wd + (size_t)g * D * dd, dd, lane, wa);
+    for (int which = 0; which < 2; ++which) {
+        const bf16_t* src_new = (which ? v_new : k_new) + (size_t)bg * n * D;
+        bf16_t* ring = (which ? v_win : k_win) + (size_t)bg * w * D;
+        if (mode != 2) {
+            const bf16_t* row = src_new;
+            if (project) row = (ex < L) ? ring + (size_t)(ex % w) * D : src_new + (size_t)(ex - L) * D;
+            lbf16x8 x[KS];
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                x[s] = lload8(row + s * 16 + hg * 8);
+                if (!project) x[s] = __builtin_bit_cast(lbf16x8, make_uint4(0, 0, 0, 0));
+            }
+            const lf32x16 acc = project_mfma<D>(wa, x);
+            if (project) {
+                bf16_t* out = (which ? v_pool : k_pool) +
+                              (((((size_t)page) * Hkv + g) << lc.ps_shift) + (ex & ((1 << lc.ps_shift) - 1))) * dd;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int c = acc_col(r, hg);
+                    if (c < dd) out[c] = f32_to_bf16(acc[r]);
+                }
+            }
+        }
+        if (to_ring) {
+            const bf16_t* src = src_new + (size_t)tt * D;
+            bf16_t* dst = ring + (size_t)((L + tt) % w) * D;
+#pragma unroll
+            for (int s = 0; s < KS; ++s)
+                *reinterpret_cast<uint4*>(dst + s * 16 + hg * 8) = *reinterpret_cast<const uint4*>(src + s * 16 + hg * 8);
+        }
+    }
+}
+
+hipError_t launch_append_chunk_paged(const bf16_t* k_new, const bf16_t* v_new, const bf16_t* wd,
+                                     bf16_t* k_win, bf16_t* v_win, bf16_t* k_pool, bf16_t* v_pool,
+                                     const LatCache& lc, int B, int Hkv, int d, int dd, int w, int n,
+                                     hipStream_t st) {
+    if (!mfma_projection(d, dd)) return hipErrorNotSupported;
+    dim3 grid((n + 31) / 32, B * Hkv);
+    auto kern = (d == 64) ? append_chunk_paged_mfma_kernel<64> : append_chunk_paged_mfma_kernel<128>;
+    if (n <= w || w == 0) {
+        hipLaunchKernelGGL(kern, grid, dim3(64), 0, st, k_new, v_new, wd, k_win, v_win, k_pool, v_pool, lc, Hkv,
+                           dd, w, n, 0);
+        return hipGetLastError();
+    }
+    hipLaunchKernelGGL(kern, grid, dim3(64), 0, st, k_new, v_new, wd, k_win, v_win, k_pool, v_pool, lc, Hkv, dd,
+                       w, n, 1);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(kern, grid, dim3(64), 0, st, k_new, v_new, wd, k_win, v_win, k_pool, v_pool, lc, Hkv, dd,
+                       w, n, 2);
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(64) void lens_advance_n_kernel(int* __restrict__ lens,
+                                                            const int* __restrict__ n_new, int B,
+                                                            int cap, int n) {
+    const int b = wg_id_x() * 64 + lane_id_x();
+    if (b >= B) return;
+    const int nb = n_new ? imin(imax(n_new[b], 0), n) : n;
+    if (nb == 0) return;
+    const int L = lens[b];
+    if (L >= 0 && L + nb <= cap) lens[b] = L + nb;
+    else if (L >= 0) lens[b] = -1 - L;
+}
+
+hipError_t launch_lens_advance(int* lens, const int* n_new, int B, int cap, int n, hipStream_t st) {
+    hipLaunchKernelGGL(lens_advance_n_kernel, dim3((B + 63) / 64), dim3(64), 0, st, lens, n_new, B, cap, n);
+    return hipGetLastError();
+}
+
+}  // namespace dar

@@ -239,6 +239,52 @@ __device__ __forceinline__ const bf16_t* uniform_ptr(const bf16_t* p) {
     return (const bf16_t*)(((uint64_t)hi << 32) | lo);
 }
 
+// Kernel modes: the whole-sequence prefill; the rotary embedding (full-d
+// distant keys from the pre-pass); a chunk whose distant latents are read in
+// place from a dense or a paged cache (LatCache).
+enum { kModePlain = 0, kModeRope = 1, kModeDense = 2, kModePaged = 3 };
+
+// A load of a wavefront-uniform int through the scalar data cache.
+__device__ __forceinline__ int sload(const int* p) {
+    return *(const __attribute__((address_space(4))) int*)p;
+}
+
+// Buffer descriptor over the latent rows of positions [t0, t0 + 32) of one
+// (batch, KV head) in a cache array (t0 a multiple of 32; a page holds at
+// least 32 tokens, so the rows are contiguous): rows at or past Td (not
+// latent yet), and all rows of an unmapped page, read as zeros.
+template <int DD, bool PAGED>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t lat_rsrc(const LatCache& lc, const bf16_t* arr,
+                                                           int b, int g, int bg, int Hkv, int t0,
+                                                           int Td) {
+    int rows = imax(imin(Td - t0, 32), 0);
+    size_t row0;
+    if constexpr (PAGED) {
+        const int page = sload(lc.bt + (size_t)b * lc.maxb + imin(t0 >> lc.ps_shift, lc.maxb - 1));
+        const bool ok = page >= 0 && page < lc.n_pages;
+        if (!ok) rows = 0;
+        row0 = ((((size_t)(ok ? page : 0)) * Hkv + g) << lc.ps_shift) + (t0 & ((1 << lc.ps_shift) - 1));
+    } else {
+        row0 = (size_t)bg * lc.cap + t0;
+    }
+    // (size and base moved to scalar registers: a descriptor in vector
+    // registers would make every load a loop over its distinct values)
+    return __builtin_amdgcn_make_buffer_rsrc((void*)uniform_ptr(arr + row0 * DD), (short)0,
+                                             __builtin_amdgcn_readfirstlane(rows * DD * 2), kBufWord3);
+}
+
+// The latent key row of position t (nullptr when its page is not mapped).
+template <int DD, bool PAGED>
+__device__ __forceinline__ const bf16_t* lat_row(const LatCache& lc, int b, int g, int bg, int Hkv, int t) {
+    if constexpr (PAGED) {
+        const int page = lc.bt[(size_t)b * lc.maxb + (t >> lc.ps_shift)];
+        if (page < 0 || page >= lc.n_pages) return nullptr;
+        return lc.k + (((((size_t)page) * Hkv + g) << lc.ps_shift) + (t & ((1 << lc.ps_shift) - 1))) * DD;
+    } else {
+        return lc.k + ((size_t)bg * lc.cap + t) * DD;
+    }
+}
+
 // Distant region: subtiles of 32 keys [0, js_last] against the latents of
 // the pre-pass, software pipelined: the scores of subtile n+1 are on the
 // matrix cores while the exponentials of subtile n run, so neither unit
@@ -313,6 +359,120 @@ __device__ __forceinline__ void distant_region(const RowCtx& c, const bf16_t* __
     int n = 0;
     for (; n + 2 < n_sub; n += 3) {
         // x = scores of n; kb, kc, ka hold keys n+1..n+3; va, vb, vc values n..n+2
+        f32x16_t xn = scores(n + 1, kb);
+        kb = loadK(n + 4);
+        finish(x, va, &xn);
+        va = loadV(n + 3);
+        x = xn;
+        xn = scores(n + 2, kc);
+        kc = loadK(n + 5);
+        finish(x, vb, &xn);
+        vb = loadV(n + 4);
+        x = xn;
+        xn = scores(n + 3, ka);
+        ka = loadK(n + 6);
+        finish(x, vc, &xn);
+        vc = loadV(n + 5);
+        x = xn;
+    }
+    if (n + 1 < n_sub) {
+        f32x16_t xn = scores(n + 1, kb);
+        finish(x, va, &xn);
+        finish(xn, vb, nullptr);
+    } else if (n < n_sub) {
+        finish(x, va, nullptr);
+    }
+}
+
+// Distant region of a chunk, latents read in place from the cache: the
+// schedule of distant_region (scores of subtile n+1 on the matrix cores while
+// the exponentials of subtile n run; keys and values three subtiles ahead).
+// The key latents are in natural column order, so qtop must be too. The
+// value latents are token-major in the cache: each wavefront stores its
+// subtile into its own LDS block (vst, 32 rows of DD) and reads the V^T
+// operand from it with transposing reads; with d_down = 16 the operand rows
+// 16..31 come from two constant chunks stored after the block, [1, 0, 0, 0]
+// for the lanes that supply row 16 and zeros for the others, so O_lat^T row
+// 16 is the row sum and rows 17..31 are zero, as with the pre-pass layout.
+template <int D, int DD, bool FIXED, bool PAGED>
+__device__ __forceinline__ void distant_region_cache(const RowCtx& c, const LatCache& lc, int b,
+                                                     int g, int Hkv, bf16_t* vst,
+                                                     const bf16x8_t (&qtop)[DD / 16], int js_last,
+                                                     SoftmaxState& st, f32x16_t (&ow)[D / 32],
+                                                     f32x16_t& ol) {
+    constexpr int DS = DD / 16, NT = D / 32;
+    const int n_sub = (js_last >> 5) + 1;
+    const int lane = c.tid & 63;
+    const int quad = lane >> 4, sl = lane & 15;
+    const int koff = (c.prow * DD + c.hg * 8) * 2;
+    const int voff = lane * 16;
+    if (DD == 16 && lane < 8) vst[32 * DD + lane] = lane == 0 ? (bf16_t)0x3f80 : (bf16_t)0;
+    struct KT {
+        bf16x8_t k[DS];
+    };
+    struct VT {
+        uint4 v[DS];  // bytes 16 lane + 1024 k of the subtile
+    };
+    auto loadK = [&](int sub) {
+        const __amdgpu_buffer_rsrc_t rk = lat_rsrc<DD, PAGED>(lc, lc.k, b, g, c.bg, Hkv, sub * 32, c.Td);
+        KT r;
+#pragma unroll
+        for (int s = 0; s < DS; ++s)
+            r.k[s] = __builtin_bit_cast(bf16x8_t, __builtin_amdgcn_raw_buffer_load_b128(rk, koff + s * 32, 0, 0));
+        return r;
+    };
+    auto loadV = [&](int sub) {
+        const __amdgpu_buffer_rsrc_t rv = lat_rsrc<DD, PAGED>(lc, lc.v, b, g, c.bg, Hkv, sub * 32, c.Td);
+        VT r;
+#pragma unroll
+        for (int k = 0; k < DS; ++k)
+            r.v[k] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rv, voff + k * 1024, 0, 0));
+        return r;
+    };
+    auto scores = [&](int sub, const KT& kt) {
+        f32x16_t x = mfma(kt.k[0], qtop[0], st.cmv);
+#pragma unroll
+        for (int s = 1; s < DS; ++s) x = mfma(kt.k[s], qtop[s], x);
+        const int js = sub * 32;
+        if (js + 31 > c.r0 - c.w) {  // staircase subtile: keep j <= i - w
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+                if (js + acc_key(r, c.hg) > c.i - c.w) x[r] = -INFINITY;
+        }
+        return x;
+    };
+    auto finish = [&](f32x16_t& x, const VT& vt, f32x16_t* xnext) {
+        // the wavefront's own LDS block: its stores complete before its reads
+#pragma unroll
+        for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vst + (lane + 64 * k) * 8) = vt.v[k];
+        bf16x8_t p0, p1;
+        if (FIXED) exp_pack<DD != 16>(x, st.l, p0, p1);
+        else softmax_step<NT, DD != 16>(x, st, ow, ol, p0, p1, xnext);
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+            const int key = half * 16 + 8 * (quad >> 1) + (sl >> 2);
+            const int cc = 16 * (quad & 1) + 4 * (sl & 3);
+            // (a lane reads 4 columns of one row of a 4 x 16 block that the
+            // transposing read hands out column by column: the lanes with
+            // sl % 4 == 0 supply operand rows 16..19, of which only row 16 is
+            // ones)
+            const bool pad = DD == 16 && (quad & 1);
+            const bf16_t* cst = vst + 32 * DD + ((sl & 3) ? 4 : 0);
+            const bf16_t* plo = pad ? cst : vst + key * DD + cc;
+            const bf16_t* phi = pad ? cst : vst + (key + 4) * DD + cc;
+            const s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)plo);
+            const s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4_t*)phi);
+            const uint2 ulo = __builtin_bit_cast(uint2, lo), uhi = __builtin_bit_cast(uint2, hi);
+            const bf16x8_t a = __builtin_bit_cast(bf16x8_t, make_uint4(ulo.x, ulo.y, uhi.x, uhi.y));
+            ol = mfma(a, half ? p1 : p0, ol);
+        }
+    };
+    KT ka = loadK(0), kb = loadK(1), kc = loadK(2);
+    VT va = loadV(0), vb = loadV(1), vc = loadV(2);
+    f32x16_t x = scores(0, ka);
+    ka = loadK(3);
+    int n = 0;
+    for (; n + 2 < n_sub; n += 3) {
         f32x16_t xn = scores(n + 1, kb);
         kb = loadK(n + 4);
         finish(x, va, &xn);
@@ -553,12 +713,16 @@ __device__ __forceinline__ void local_region(const RowCtx& c, const bf16_t* __re
     }
 }
 
-// ROPE: rotary embedding inside Eq. 3. q, k are the rotated queries and
+// kModeRope: rotary embedding inside Eq. 3. q, k are the rotated queries and
 // keys, cK / cVt the lifted-and-rotated distant keys and the lifted values
 // ([B*Hkv][T - w][D] each), cnorm their 32-row block norms (Tp / 32 per
 // head); the distant region then runs the full-d tile loop (no absorbed
 // query, no lift in the epilogue), and W_down / W_up are not read.
-template <int D, int DD, int NW, bool ROPE>
+// kModeDense / kModePaged: a chunk (rows q0.., k / v the context rows) whose
+// distant latents are read in place from lc (cK / cVt unused); the norm
+// arrays have lc.ncb / lc.nkb blocks a head; paged: each sequence's q0 and
+// row count come from lc, and Tkv is the context rows' stride.
+template <int D, int DD, int NW, int MODE>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
 void prefill_mfma_kernel(
     const bf16_t* __restrict__ q, const bf16_t* __restrict__ k, const bf16_t* __restrict__ v,
@@ -567,7 +731,10 @@ void prefill_mfma_kernel(
     const float* __restrict__ knorm, const bf16_t* __restrict__ consts, bf16_t* __restrict__ o,
     float* __restrict__ lse, int Hq, int Hkv, int T, int w, int Tp, int nblk, int BH,
     float c_scale, int q0, int n_rows, int kv0, int Tkv, const bf16_t* __restrict__ wv,
-    const int* __restrict__ seq_lens) {
+    const int* __restrict__ seq_lens, LatCache lc) {
+    constexpr bool ROPE = MODE == kModeRope;
+    constexpr bool CACHE = MODE == kModeDense || MODE == kModePaged;
+    constexpr bool PAGED = MODE == kModePaged;
     constexpr int BM = NW * 32;
     constexpr int KS = D / 16;   // 16-wide k slabs of q . k
     constexpr int DS = DD / 16;  // 16-wide k slabs of q~ . c^K
@@ -575,6 +742,7 @@ void prefill_mfma_kernel(
     constexpr int BN = 64;       // keys per LDS tile (local region)
     constexpr int LDK = D + 8;   // padded LDS row (bf16 elements)
     constexpr int LDU = D + 8;   // padded row of wU (bf16 elements)
+    static_assert(NW * (32 * DD + 8) <= BN * LDK, "value blocks of the cache mode fit one tile buffer");
     extern __shared__ __attribute__((aligned(16))) bf16_t smem[];
     bf16_t* lds_k = smem;                    // [2][BN][LDK]
     bf16_t* lds_v = smem + 2 * BN * LDK;     // [2][BN][LDK]
@@ -605,14 +773,39 @@ void prefill_mfma_kernel(
     const int b = bh / Hq, h = bh - (bh / Hq) * Hq;
     const int g = h / (Hq / Hkv);
     const int bg = b * Hkv + g;
-    // this sequence's length (a ragged batch; T, the padded length, stays the
-    // layout of every array)
-    const int Tb = seq_lens ? imin(imax(seq_lens[b], 0), T) : T;
     const int tid = lane_id_x();
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // A paged chunk: this sequence's first row position and row count; one
+    // the chunk does not fit gets NaN rows and nothing is read for it.
+    int T_ = T, kv0_ = kv0;
+    if constexpr (PAGED) {
+        const int len_b = sload(lc.lens + b);
+        const int nb = lc.n_new ? imin(imax(sload(lc.n_new + b), 0), n_rows) : n_rows;
+        if (nb > 0 && (len_b < 0 || len_b + nb > lc.cap)) {
+            for (int part = 0; part < 2; ++part) {
+                const int rb = part == 0 ? nblk - 1 - pair : pair;
+                if (part == 1 && rb >= nblk - 1 - pair) break;
+                for (int idx = tid; idx < BM * D; idx += NW * 64) {
+                    const int r = rb * BM + idx / D;
+                    if (r < nb) {
+                        o[((size_t)bh * n_rows + r) * D + idx % D] = (bf16_t)0x7fc0;
+                        if (lse && idx % D == 0) lse[(size_t)bh * n_rows + r] = __builtin_nanf("");
+                    }
+                }
+            }
+            return;
+        }
+        q0 = imax(len_b, 0);
+        T_ = q0 + nb;
+        kv0_ = imax(q0 - w, 0);
+    }
+    // this sequence's length (a ragged batch; T, the padded length, stays the
+    // layout of every array)
+    const int Tb = seq_lens ? imin(imax(seq_lens[b], 0), T) : T_;
     const bf16_t* wdg = wd + (size_t)g * D * DD;
     const bf16_t* wug = wu ? wu + (size_t)g * DD * D : nullptr;
-    const int nkb = (T + 31) >> 5;  // 32-key blocks with a key norm
+    const int nkb = CACHE ? lc.nkb : (T + 31) >> 5;  // 32-key blocks of a head with a key norm
+    const int ncb = CACHE ? lc.ncb : Tp / 32;        // 32-key blocks of a head with a latent norm
 
     // U = W_up (W_down^T when tied), once per workgroup: its rows are the A
     // operand of q~ = q W_up^T, its columns that of the lift
@@ -669,9 +862,9 @@ void prefill_mfma_kernel(
         c.bg = bg;
         c.tid = tid;
         c.c_scale = c_scale;
-        c.kv0 = kv0;
+        c.kv0 = kv0_;
         c.Tkv = Tkv;
-        c.Td = imax(T - w, 0);
+        c.Td = imax(T_ - w, 0);
         const int i0 = q0 + rb * BM;  // position of the block's first row
         c.r0 = i0 + wave * 32;
         c.i = c.r0 + c.qc;
@@ -693,7 +886,7 @@ void prefill_mfma_kernel(
         for (int s = 0; s < KS; ++s) qop[s] = load_bf16x8(qrow + s * 16 + hg * 8);
         const int nsb = jd_end >= 0 ? (js_last >> 5) + 1 : 0;  // latent blocks with a norm
         const int kb_lo = imax(0, c.r0 - w + 1) >> 5, kb_hi = imax(0, c.i_hi) >> 5;
-        float cmax = lane < nsb ? cnorm[(size_t)bg * (Tp / 32) + lane] : 0.f;
+        float cmax = lane < nsb ? cnorm[(size_t)bg * ncb + lane] : 0.f;
         float kmax = (has_local && kb_lo + lane <= kb_hi) ? knorm[(size_t)bg * nkb + kb_lo + lane] : 0.f;
         if (i >= Tb) {
 #pragma unroll
@@ -720,17 +913,22 @@ void prefill_mfma_kernel(
         float bound = -INFINITY;
         if (ROPE && jd_end >= 0) {
             // full-d distant keys: |q . k| <= |q| |k|
-            for (int sb = lane + 64; sb < nsb; sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * (Tp / 32) + sb]);
+            for (int sb = lane + 64; sb < nsb; sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * ncb + sb]);
             cmax = wave_max(cmax);
             bound = c_scale * sqrtf(qs2) * cmax;
         } else if (jd_end >= 0) {
             f32x16_t qt = splat16(0.f);
+            // A row qc is latent column qa: qc itself (the pre-pass stores its
+            // key latents in that permuted order), or, for latents read in
+            // natural column order from a cache, qc with bits 2 and 3 swapped
+            const int qa = CACHE ? (qc & ~12) | ((qc & 4) << 1) | ((qc & 8) >> 1) : qc;
 #pragma unroll
             for (int s = 0; s < KS; ++s) {
-                const bf16x8_t a = qc < DD ? load_bf16x8(wU + qc * LDU + s * 16 + hg * 8) : zero_bf16x8();
+                const bf16x8_t a = qc < DD ? load_bf16x8(wU + qa * LDU + s * 16 + hg * 8) : zero_bf16x8();
                 qt = mfma(a, qop[s], qt);
             }
-            // accumulator register 8*s + j holds latent column 16*s + (j<4 ? 4hg+j : 8+4hg+j-4)
+            // accumulator register 8*s + j holds latent column qa(16*s + (j<4 ? 4hg+j : 8+4hg+j-4)):
+            // natural order 16*s + 8hg + j when the bits were swapped
             float qn2 = 0.f;
 #pragma unroll
             for (int s = 0; s < DS; ++s) {
@@ -741,7 +939,7 @@ void prefill_mfma_kernel(
             }
             qn2 = pair_sum(qn2);
             // |q~ . c| <= |q~| |c| on the bf16 values the MFMA multiplies (Cauchy-Schwarz)
-            for (int sb = lane + 64; sb < nsb; sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * (Tp / 32) + sb]);
+            for (int sb = lane + 64; sb < nsb; sb += 64) cmax = fmaxf(cmax, cnorm[(size_t)bg * ncb + sb]);
             cmax = wave_max(cmax);
             bound = sqrtf(qn2) * cmax;
         }
@@ -761,13 +959,18 @@ void prefill_mfma_kernel(
         if (fixed && __builtin_amdgcn_ballot_w64(i < Tb && bound > 50.f)) {
             bf16x8_t wit[KS];  // own key (w >= 1) or own latent key (w = 0)
             if (w >= 1) {
-                const bf16_t* krow = k + ((size_t)bg * Tkv + (ii - kv0)) * D;
+                const bf16_t* krow = k + ((size_t)bg * Tkv + (ii - kv0_)) * D;
 #pragma unroll
                 for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(krow + s * 16 + hg * 8);
             } else if (ROPE) {
                 const bf16_t* crow = cK + ((size_t)bg * c.Td + ii) * D;  // lifted, rotated own key
 #pragma unroll
                 for (int s = 0; s < KS; ++s) wit[s] = load_bf16x8(crow + s * 16 + hg * 8);
+            } else if (CACHE) {
+                const bf16_t* crow = lat_row<DD, PAGED>(lc, b, g, bg, Hkv, ii);  // own latent key
+#pragma unroll
+                for (int s = 0; s < KS; ++s)
+                    wit[s] = s < DS && crow ? load_bf16x8(crow + s * 16 + hg * 8) : zero_bf16x8();
             } else {
                 const bf16_t* crow = cK + ((size_t)bg * Tp + ii) * DD;
 #pragma unroll
@@ -806,8 +1009,17 @@ void prefill_mfma_kernel(
                 }
             }
         } else if (jd_end >= 0) {
-            if (fixed) distant_region<D, DD, true>(c, cK, cVt, qtop, js_last, st, ow, ol);
-            else distant_region<D, DD, false>(c, cK, cVt, qtop, js_last, st, ow, ol);
+            if constexpr (CACHE) {
+                // the wavefront's value block: in the second local-region value
+                // buffer, which the local region first writes after a barrier
+                // that every wavefront reaches only after its distant region
+                bf16_t* vst = lds_v + BN * LDK + wave * (32 * DD + 8);
+                if (fixed) distant_region_cache<D, DD, true, PAGED>(c, lc, b, g, Hkv, vst, qtop, js_last, st, ow, ol);
+                else distant_region_cache<D, DD, false, PAGED>(c, lc, b, g, Hkv, vst, qtop, js_last, st, ow, ol);
+            } else {
+                if (fixed) distant_region<D, DD, true>(c, cK, cVt, qtop, js_last, st, ow, ol);
+                else distant_region<D, DD, false>(c, cK, cVt, qtop, js_last, st, ow, ol);
+            }
         }
         // The latent part is complete: lift it now (Eq. 2 by linearity), so the
         // window region below carries ow only.
@@ -886,12 +1098,13 @@ bool prefill_mfma_supported(const dar_shape* s) {
     return true;
 }
 
-template <int D, int DD, bool ROPE = false>
+template <int D, int DD, int MODE = kModePlain>
 static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w, const void* q, const void* k,
                             const void* v, const void* wd, const void* wu, void* o, float* lse,
                             const void* cK, const void* cVt, const float* cnorm,
                             const float* knorm, const void* consts, hipStream_t st,
-                            const void* wv = nullptr) {
+                            const void* wv = nullptr, const LatCache& lc = LatCache{}) {
+    constexpr bool ROPE = MODE == kModeRope;
     constexpr int NW = 4;
     constexpr int BM = NW * 32;
     const int T = geo.total();
@@ -901,7 +1114,7 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w
     const int Tp = ROPE ? round_up(T - w > 0 ? T - w : 0, 32) : prefill_tp(T, w);
     const float c_scale = 1.4426950408889634f / sqrtf((float)D);
     const size_t lds = sizeof(bf16_t) * (4 * 64 * (D + 8) + (wv ? 2 : 1) * DD * (D + 8));
-    auto kern = prefill_mfma_kernel<D, DD, NW, ROPE>;
+    auto kern = prefill_mfma_kernel<D, DD, NW, MODE>;
     if (lds > 65536) {
         hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
         if (e != hipSuccess) return e;
@@ -910,7 +1123,7 @@ static hipError_t launch_dd(int B, int Hq, int Hkv, const PrefillGeo& geo, int w
                        (const bf16_t*)k, (const bf16_t*)v, (const bf16_t*)wd, (const bf16_t*)wu,
                        (const bf16_t*)cK, (const bf16_t*)cVt, cnorm, knorm, (const bf16_t*)consts,
                        (bf16_t*)o, lse, Hq, Hkv, T, w, Tp, nblk, BH, c_scale, geo.q0,
-                       geo.n_rows, geo.kv0, geo.Tkv, (const bf16_t*)wv, geo.seq_lens);
+                       geo.n_rows, geo.kv0, geo.Tkv, (const bf16_t*)wv, geo.seq_lens, lc);
     return hipGetLastError();
 }
 
@@ -924,6 +1137,29 @@ hipError_t launch_prefill_mfma(const dar_shape* s, const PrefillGeo& geo, const 
     if (s->d == 64 && s->d_down == 32) return launch_dd<64, 32>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st, wv);
     if (s->d == 128 && s->d_down == 16) return launch_dd<128, 16>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st, wv);
     if (s->d == 128 && s->d_down == 32) return launch_dd<128, 32>(B, Hq, Hkv, geo, w, q, k, v, wd, wu, o, lse, cK, cVt, cnorm, knorm, consts, st, wv);
+    return hipErrorNotSupported;
+}
+
+hipError_t launch_prefill_mfma_cache(const dar_shape* s, const PrefillGeo& geo, const LatCache& lc,
+                                     const void* q, const void* ctx_k, const void* ctx_v,
+                                     const void* wd, const void* wu, void* o, float* lse,
+                                     const float* cnorm, const float* knorm, hipStream_t st) {
+    const int B = s->B, Hq = s->Hq, Hkv = s->Hkv, w = s->w;
+#define DAR_CACHE_LAUNCH(D_, DD_)                                                                     \
+    if (s->d == D_ && s->d_down == DD_) {                                                            \
+        if (lc.bt)                                                                                   \
+            return launch_dd<D_, DD_, kModePaged>(B, Hq, Hkv, geo, w, q, ctx_k, ctx_v, wd, wu, o, lse, \
+                                                  nullptr, nullptr, cnorm, knorm, nullptr, st,       \
+                                                  nullptr, lc);                                      \
+        return launch_dd<D_, DD_, kModeDense>(B, Hq, Hkv, geo, w, q, ctx_k, ctx_v, wd, wu, o, lse,     \
+                                              nullptr, nullptr, cnorm, knorm, nullptr, st, nullptr, \
+                                              lc);                                                   \
+    }
+    DAR_CACHE_LAUNCH(64, 16)
+    DAR_CACHE_LAUNCH(64, 32)
+    DAR_CACHE_LAUNCH(128, 16)
+    DAR_CACHE_LAUNCH(128, 32)
+#undef DAR_CACHE_LAUNCH
     return hipErrorNotSupported;
 }
 
@@ -944,9 +1180,9 @@ hipError_t launch_prefill_mfma_rope_geo(const dar_shape* s, const PrefillGeo& ge
                                         const void* vd, void* o, float* lse, const float* knorm,
                                         const float* dnorm, hipStream_t st) {
     if (s->d == 64)
-        return launch_dd<64, 16, true>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o,
+        return launch_dd<64, 16, kModeRope>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o,
                                        lse, kd, vd, dnorm, knorm, nullptr, st);
-    return launch_dd<128, 16, true>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o, lse,
+    return launch_dd<128, 16, kModeRope>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o, lse,
                                     kd, vd, dnorm, knorm, nullptr, st);
 }
 
@@ -956,9 +1192,9 @@ hipError_t launch_prefill_mfma_rope(const dar_shape* s, int T, const void* qr, c
                                     hipStream_t st) {
     const PrefillGeo geo = whole_sequence(T);
     if (s->d == 64)
-        return launch_dd<64, 16, true>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o,
+        return launch_dd<64, 16, kModeRope>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o,
                                        lse, kd, vd, dnorm, knorm, nullptr, st);
-    return launch_dd<128, 16, true>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o, lse,
+    return launch_dd<128, 16, kModeRope>(s->B, s->Hq, s->Hkv, geo, s->w, qr, kr, v, nullptr, nullptr, o, lse,
                                     kd, vd, dnorm, knorm, nullptr, st);
 }
 

@@ -34,6 +34,7 @@ def test_exports_every_declared_symbol():
                           "dar_decode_workspace_bytes", "dar_prefill_backward_workspace_bytes",
                           "dar_attn_prefill_chunk", "dar_prefill_chunk_workspace_bytes",
                           "dar_attn_prefill_chunk_rope", "dar_prefill_chunk_rope_workspace_bytes",
+                          "dar_attn_prefill_chunk_paged", "dar_prefill_chunk_paged_workspace_bytes",
                           "dar_rope_table", "dar_attn_prefill_rope", "dar_attn_decode_rope",
                           "dar_attn_prefill_shared", "dar_cache_append_shared",
                           "dar_attn_decode_shared", "dar_cache_append_paged",
@@ -304,15 +305,22 @@ def test_backward_rejects(kw, shape_kw, expect):
 
 def test_chunk_workspace_size():
     """Context copy of K and V (ring tokens from max(0, len - w), then the n new
-    ones) followed by the prefill workspace of len + n positions."""
+    ones) followed, on the matrix-core shapes (latents read in place), by the
+    two block-norm arrays of ceil((len + n) / 32) blocks a head, else by the
+    prefill workspace of len + n positions."""
     al = lambda x: (x + 255) // 256 * 256
     for (B, Hq, Hkv, d, dd, w, dt, es), (L, n) in [((2, 4, 2, 64, 16, 8, torch.bfloat16, 2), (100, 7)),
                                                    ((2, 4, 2, 64, 16, 8, torch.bfloat16, 2), (3, 50)),
+                                                   ((1, 2, 2, 128, 32, 40, torch.bfloat16, 2), (300, 1)),
+                                                   ((1, 2, 2, 64, 8, 4, torch.bfloat16, 2), (30, 9)),
                                                    ((1, 2, 2, 16, 4, 0, torch.float32, 4), (40, 9))]:
         s = dar.make_shape(B, Hq, Hkv, d, dd, w, dt)
         kv0 = max(0, L - w)
         ctx = al(B * Hkv * (L + n - kv0) * d * es)
-        want = 2 * ctx + expected_prefill_ws(B, Hkv, L + n, dd, w, es)
+        if dt == torch.bfloat16 and d in (64, 128) and dd in (16, 32):
+            want = 2 * ctx + 2 * al(B * Hkv * ((L + n + 31) // 32) * 4)
+        else:
+            want = 2 * ctx + expected_prefill_ws(B, Hkv, L + n, dd, w, es)
         assert dar.dar_prefill_chunk_workspace_bytes(s, L, n) == want
     s = S()
     assert dar.dar_prefill_chunk_workspace_bytes(s, 10, 0) == 0    # n >= 1
@@ -501,6 +509,47 @@ def test_paged_rejects_before_any_launch():
     assert dc(pc(), ws_bytes=8) == dar.DAR_E_WORKSPACE
     assert dc(pc(), shape=S(dtype=torch.float32)) == dar.DAR_E_UNSUPPORTED   # matrix-core shapes only
     assert dc(pc(), shape=S(d=80, dd=16)) == dar.DAR_E_UNSUPPORTED
+
+
+def test_chunk_paged_workspace_size():
+    """Context rows of every sequence (w + n rows a head) for K and V, then two
+    block-norm arrays covering a whole sequence's capacity."""
+    al = lambda x: (x + 255) // 256 * 256
+    for (B, Hkv, d, dd, w), (cap, n) in [((4, 2, 64, 16, 32), (4096, 256)),
+                                          ((3, 8, 128, 32, 0), (100, 1))]:
+        s = dar.make_shape(B, Hkv * 4, Hkv, d, dd, w, torch.bfloat16)
+        want = 2 * al(B * Hkv * (w + n) * d * 2) + 2 * al(B * Hkv * ((cap + 31) // 32) * 4)
+        assert dar.dar_prefill_chunk_paged_workspace_bytes(s, cap, n) == want
+    assert dar.dar_prefill_chunk_paged_workspace_bytes(S(), 64, 0) == 0
+    assert dar.dar_prefill_chunk_paged_workspace_bytes(S(), 0, 4) == 0
+
+
+@no_gpu
+def test_chunk_paged_rejects_before_any_launch():
+    def pc(ps=64, maxb=4, n_pages=8, bt=FAKE, lens=FAKE, win=FAKE):
+        return dar.DarPagedCacheStruct(win.value if win else None, win.value if win else None,
+                                       FAKE.value, FAKE.value, bt.value if bt else None,
+                                       lens.value if lens else None, ps, maxb, n_pages)
+    def call(c=None, shape=None, n=8, n_new=None, q=FAKE, wu=None, lse=None, ws_bytes=1 << 30):
+        shape = shape or S()
+        c = c or pc()
+        return dar.lib.dar_attn_prefill_chunk_paged(ctypes.byref(shape), ctypes.byref(c), n, n_new, q,
+                                                    FAKE, FAKE, FAKE, wu, FAKE, lse, FAKE, ws_bytes,
+                                                    None)
+    assert call(n=0) == dar.DAR_E_ARG
+    assert call(c=pc(ps=48)) == dar.DAR_E_ARG
+    assert call(c=pc(bt=None)) == dar.DAR_E_ARG
+    assert call(c=pc(lens=None)) == dar.DAR_E_ARG
+    assert call(c=pc(win=None)) == dar.DAR_E_ARG
+    assert call(q=None) == dar.DAR_E_ARG
+    assert call(q=MISALIGNED) == dar.DAR_E_ARG
+    assert call(wu=MISALIGNED) == dar.DAR_E_ARG
+    assert call(lse=MISALIGNED) == dar.DAR_E_ARG
+    assert call(n_new=ctypes.c_void_p((1 << 20) + 2)) == dar.DAR_E_ARG   # int array misaligned
+    assert call(ws_bytes=64) == dar.DAR_E_WORKSPACE
+    assert call(shape=S(dtype=torch.float32)) == dar.DAR_E_UNSUPPORTED   # matrix-core shapes only
+    assert call(shape=S(d=64, dd=8)) == dar.DAR_E_UNSUPPORTED
+    assert call(shape=S(Hq=3)) == dar.DAR_E_ARG
 
 
 @no_gpu
