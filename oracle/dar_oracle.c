@@ -439,6 +439,182 @@ int dar_oracle_rows_rope(int T, int d, int dd, int w, int r, double base, int po
     return bad ? -1 : 0;
 }
 
+/*
+ * Backward of the causal prefill with RoPE inside Eq. 3 (Section 2.3 trains
+ * through it): gradients of L = sum(dO * O) with respect to the un-rotated
+ * q, k, v and W_down, W_up, for tokens at positions pos0 .. pos0+T-1.
+ * With R_p the rotation of position p (an orthogonal map, R_p^T = R_{-p}):
+ *
+ *   query       qr_i = R_i q_i
+ *   window      key kr_j = R_j k_j,                value v_j
+ *   distant     key kd_j = R_j ((k_j W_down) W_up), value (v_j W_down) W_up
+ *   S, P, dP, dS as for dar_oracle_backward, with these keys and values;
+ *   dqr_i = sum_j dS_ij key_ij / sqrt(d),  dq_i = R_i^T dqr_i
+ *   window pairs:  dkr_j += dS_ij qr_i / sqrt(d),  dv_j += P_ij dO_i
+ *   distant pairs: dkd_j += dS_ij qr_i / sqrt(d),  dv'_j += P_ij dO_i
+ *   dk_j += R_j^T dkr_j; the lifted key k'_j = (k_j W_down) W_up receives
+ *   R_j^T dkd_j and the lifted value dv'_j, both taken back through the lift
+ *   exactly as in dar_oracle_backward.
+ * Arguments as for dar_oracle_backward, plus r (even, 0 <= r <= d), base > 0
+ * and pos0 >= 0. With r = 0 the result is dar_oracle_backward's.
+ */
+int dar_oracle_backward_rope(int B, int Hq, int Hkv, int T, int d, int dd, int w, int r,
+                             double base, int pos0, const double* q, const double* k,
+                             const double* v, const double* wd, const double* wu,
+                             const double* dout, double* dq, double* dk, double* dv, double* dwd,
+                             double* dwu, int nthreads)
+{
+    if (B < 1 || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || T < 1 || d < 1 || dd < 1 || w < 0)
+        return -1;
+    if (r < 0 || r > d || (r & 1) || pos0 < 0 || !(base > 0.0)) return -1;
+    if ((wu == NULL) != (dwu == NULL)) return -1;
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+    const int group = Hq / Hkv;
+    const double scale = 1.0 / sqrt((double)d);
+    const size_t wsz = (size_t)d * dd;
+    const size_t td = (size_t)T * d;
+    double* pwd = (double*)calloc((size_t)B * Hkv * wsz, sizeof(double));
+    double* pwu = (double*)calloc((size_t)B * Hkv * wsz, sizeof(double));
+    int* tpos = (int*)malloc(sizeof(int) * (size_t)T);
+    int* npos = (int*)malloc(sizeof(int) * (size_t)T);
+    if (!pwd || !pwu || !tpos || !npos) {
+        free(pwd); free(pwu); free(tpos); free(npos);
+        return -1;
+    }
+    for (int j = 0; j < T; ++j) {
+        tpos[j] = pos0 + j;
+        npos[j] = -(pos0 + j);
+    }
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int bg = 0; bg < B * Hkv; ++bg) {
+        const int b = bg / Hkv, g = bg % Hkv;
+        const double* kb = k + (size_t)bg * td;
+        const double* vb = v + (size_t)bg * td;
+        const double* wdg = wd + (size_t)g * wsz;
+        const double* wug = wu ? wu + (size_t)g * wsz : NULL;
+        double* dkb = dk + (size_t)bg * td;
+        double* dvb = dv + (size_t)bg * td;
+        double* kl = lift_all(T, d, dd, kb, wdg, wug);
+        double* vl = lift_all(T, d, dd, vb, wdg, wug);
+        double* kr = (double*)malloc(sizeof(double) * td);     /* window keys R_j k_j */
+        double* kdr = (double*)malloc(sizeof(double) * td);    /* distant keys R_j k'_j */
+        double* qr = (double*)malloc(sizeof(double) * td);     /* one head's rotated queries */
+        double* dqr = (double*)malloc(sizeof(double) * td);
+        double* dkr = (double*)calloc(td, sizeof(double));     /* window key grads, rotated */
+        double* dkd = (double*)calloc(td, sizeof(double));     /* distant key grads, rotated */
+        double* dkl = (double*)malloc(sizeof(double) * td);    /* dk'_j = R_j^T dkd_j */
+        double* dvl = (double*)calloc(td, sizeof(double));     /* dv'_j */
+        double* p = (double*)malloc(sizeof(double) * (size_t)T);
+        double* s = (double*)malloc(sizeof(double) * (size_t)T);
+        double* dp = (double*)malloc(sizeof(double) * (size_t)T);
+        double* oi = (double*)malloc(sizeof(double) * (size_t)d);
+        if (!kl || !vl || !kr || !kdr || !qr || !dqr || !dkr || !dkd || !dkl || !dvl || !p || !s ||
+            !dp || !oi) {
+#pragma omp atomic write
+            bad = 1;
+        } else {
+            dar_oracle_rope(T, d, r, base, tpos, kb, kr);
+            dar_oracle_rope(T, d, r, base, tpos, kl, kdr);
+            for (size_t x = 0; x < td; ++x) dvb[x] = 0.0;
+            for (int hh = 0; hh < group; ++hh) {
+                const int h = g * group + hh;
+                const double* qh = q + ((size_t)b * Hq + h) * td;
+                const double* doh = dout + ((size_t)b * Hq + h) * td;
+                dar_oracle_rope(T, d, r, base, tpos, qh, qr);
+                for (size_t x = 0; x < td; ++x) dqr[x] = 0.0;
+                for (int i = 0; i < T; ++i) {
+                    const double* qi = qr + (size_t)i * d;
+                    const double* doi = doh + (size_t)i * d;
+                    one_row(d, w, i, qi, kr, vb, kdr, vl, s, oi, p, NULL);
+                    double delta = 0.0;
+                    for (int j = 0; j <= i; ++j) {
+                        const double* val = (i - j < w) ? vb + (size_t)j * d : vl + (size_t)j * d;
+                        double acc = 0.0;
+                        for (int e = 0; e < d; ++e) acc += doi[e] * val[e];
+                        dp[j] = acc;
+                        delta += p[j] * acc;
+                    }
+                    double* dqi = dqr + (size_t)i * d;
+                    for (int j = 0; j <= i; ++j) {
+                        const double ds = p[j] * (dp[j] - delta);
+                        const int local = i - j < w;
+                        const double* key = local ? kr + (size_t)j * d : kdr + (size_t)j * d;
+                        double* dkey = local ? dkr + (size_t)j * d : dkd + (size_t)j * d;
+                        double* dval = local ? dvb + (size_t)j * d : dvl + (size_t)j * d;
+                        for (int e = 0; e < d; ++e) {
+                            dqi[e] += ds * key[e] * scale;
+                            dkey[e] += ds * qi[e] * scale;
+                            dval[e] += p[j] * doi[e];
+                        }
+                    }
+                }
+                /* dq = R^T dqr */
+                dar_oracle_rope(T, d, r, base, npos, dqr, dq + ((size_t)b * Hq + h) * td);
+            }
+            /* window keys: dk = R^T dkr; distant keys: dk' = R^T dkd */
+            dar_oracle_rope(T, d, r, base, npos, dkr, dkb);
+            dar_oracle_rope(T, d, r, base, npos, dkd, dkl);
+            /* through the lift x' = (x W_down) W_up, for keys and for values */
+            double* pwdg = pwd + (size_t)bg * wsz;
+            double* pwug = pwu + (size_t)bg * wsz;
+            for (int which = 0; which < 2; ++which) {
+                const double* xb = which ? vb : kb;
+                const double* dxl = which ? dvl : dkl;
+                double* dxb = which ? dvb : dkb;
+                for (int j = 0; j < T; ++j) {
+                    const double* xj = xb + (size_t)j * d;
+                    const double* gj = dxl + (size_t)j * d;
+                    for (int c = 0; c < dd; ++c) {
+                        double u = 0.0, hc = 0.0;
+                        for (int e = 0; e < d; ++e) {
+                            const double wup = wug ? wug[(size_t)c * d + e] : wdg[(size_t)e * dd + c];
+                            u += gj[e] * wup;
+                            hc += xj[e] * wdg[(size_t)e * dd + c];
+                        }
+                        for (int e = 0; e < d; ++e) {
+                            dxb[(size_t)j * d + e] += u * wdg[(size_t)e * dd + c];
+                            pwdg[(size_t)e * dd + c] += xj[e] * u;
+                            pwug[(size_t)c * d + e] += hc * gj[e];
+                        }
+                    }
+                }
+            }
+        }
+        free(kl); free(vl); free(kr); free(kdr); free(qr); free(dqr); free(dkr); free(dkd);
+        free(dkl); free(dvl); free(p); free(s); free(dp); free(oi);
+    }
+    if (!bad) {
+        for (int g = 0; g < Hkv; ++g) {
+            double* dwdg = dwd + (size_t)g * wsz;
+            double* dwug = dwu ? dwu + (size_t)g * wsz : NULL;
+            for (size_t x = 0; x < wsz; ++x) {
+                dwdg[x] = 0.0;
+                if (dwug) dwug[x] = 0.0;
+            }
+            for (int b = 0; b < B; ++b) {
+                const double* a = pwd + ((size_t)b * Hkv + g) * wsz;
+                const double* u = pwu + ((size_t)b * Hkv + g) * wsz;
+                for (int e = 0; e < d; ++e)
+                    for (int c = 0; c < dd; ++c) {
+                        dwdg[(size_t)e * dd + c] += a[(size_t)e * dd + c];
+                        if (dwug) dwug[(size_t)c * d + e] += u[(size_t)c * d + e];
+                        else dwdg[(size_t)e * dd + c] += u[(size_t)c * d + e];
+                    }
+            }
+        }
+    }
+    free(pwd);
+    free(pwu);
+    free(tpos);
+    free(npos);
+    return bad ? -1 : 0;
+}
+
 /* Causal prefill with RoPE inside Eq. 3: positions pos0 .. pos0+T-1.
  * Shapes as for dar_oracle_prefill. */
 int dar_oracle_prefill_rope(int B, int Hq, int Hkv, int T, int d, int dd, int w, int r,

@@ -95,6 +95,9 @@ class Oracle:
         lib.dar_oracle_prefill_shared.argtypes = [ctypes.c_int] * 7 + [_dp] * 8 + [ctypes.c_int]
         lib.dar_oracle_backward.restype = ctypes.c_int
         lib.dar_oracle_backward.argtypes = [ctypes.c_int] * 7 + [_dp] * 11 + [ctypes.c_int]
+        lib.dar_oracle_backward_rope.restype = ctypes.c_int
+        lib.dar_oracle_backward_rope.argtypes = ([ctypes.c_int] * 8 + [ctypes.c_double, ctypes.c_int]
+                                                 + [_dp] * 11 + [ctypes.c_int])
         self.lib = lib
 
     def num_threads(self) -> int:
@@ -279,6 +282,32 @@ class Oracle:
             raise ValueError("dar_oracle_backward rejected its arguments")
         return dq, dk, dv, dwd, dwu
 
+    def backward_rope(self, q, k, v, wd, wu, w, r, base, dout, pos0=0, threads=0):
+        """Gradients of sum(dout * O) of the causal prefill with RoPE inside
+        Eq. 3 (q, k, v un-rotated, tokens at positions pos0..pos0+T-1):
+        returns dq, dk, dv, dwd, dwu as backward does."""
+        q = _c64(q)
+        k = _c64(k)
+        v = _c64(v)
+        wd = _c64(wd)
+        wu_c = None if wu is None else _c64(wu)
+        dout = _c64(dout)
+        B, Hq, T, d = q.shape
+        Hkv = k.shape[1]
+        dd = wd.shape[2]
+        dq = np.empty_like(q)
+        dk = np.empty_like(k)
+        dv = np.empty_like(v)
+        dwd = np.empty_like(wd)
+        dwu = None if wu is None else np.empty_like(wu_c)
+        rc = self.lib.dar_oracle_backward_rope(B, Hq, Hkv, T, d, dd, int(w), int(r), float(base),
+                                               int(pos0), _ptr(q), _ptr(k), _ptr(v), _ptr(wd),
+                                               _ptr(wu_c), _ptr(dout), _ptr(dq), _ptr(dk), _ptr(dv),
+                                               _ptr(dwd), _ptr(dwu), int(threads))
+        if rc != 0:
+            raise ValueError("dar_oracle_backward_rope rejected its arguments")
+        return dq, dk, dv, dwd, dwu
+
 
 _default = None
 
@@ -312,6 +341,10 @@ def prefill(q, k, v, wd, wu, w, threads=0, want_lse=False):
 
 def backward(q, k, v, wd, wu, w, dout, threads=0):
     return default().backward(q, k, v, wd, wu, w, dout, threads)
+
+
+def backward_rope(q, k, v, wd, wu, w, r, base, dout, pos0=0, threads=0):
+    return default().backward_rope(q, k, v, wd, wu, w, r, base, dout, pos0, threads)
 
 
 def rope(x, pos, r, base):

@@ -537,6 +537,97 @@ def check_rope_dual_store(orc, seed=34):
         np.testing.assert_allclose(o, got[1, 1, rows], rtol=0, atol=1e-12)
 
 
+def torch_rope_complex(x, pos, r, base):
+    """rope_complex in torch (differentiable): the pairs as complex numbers
+    multiplied by unit phasors."""
+    h = r // 2
+    if h == 0:
+        return x
+    ang = torch.as_tensor(np.asarray(pos, np.float64))[:, None] * float(base) ** (
+        -2.0 * torch.arange(h, dtype=torch.float64) / r)
+    z = torch.complex(x[..., :h], x[..., h:r]) * torch.polar(torch.ones_like(ang), ang)
+    return torch.cat([z.real, z.imag, x[..., r:]], dim=-1)
+
+
+def torch_dual_store_rope(q, k, v, wd, wu, w, r, base, pos0):
+    """Eq. 3-4 with RoPE over the dual store in torch: lifted-then-rotated and
+    rotated keys as 2T keys, lifted and plain values, the distance picking one
+    of each pair."""
+    B, Hq, T, d = q.shape
+    G = Hq // k.shape[1]
+    pos = pos0 + np.arange(T)
+    wu_full = wd.transpose(1, 2) if wu is None else wu
+    lift = lambda x: torch.matmul(torch.matmul(x, wd[None]), wu_full[None])
+    K2 = torch.cat([torch_rope_complex(lift(k), pos, r, base), torch_rope_complex(k, pos, r, base)],
+                   dim=2).repeat_interleave(G, dim=1)
+    V2 = torch.cat([lift(v), v], dim=2).repeat_interleave(G, dim=1)
+    s = torch.matmul(torch_rope_complex(q, pos, r, base), K2.transpose(-1, -2)) / math.sqrt(d)
+    i = torch.arange(T)[:, None]
+    j = torch.arange(T)[None, :]
+    causal = j <= i
+    near = (i - j) < w
+    mask = torch.cat([causal & ~near, causal & near], dim=1)
+    s = s.masked_fill(~mask, float("-inf"))
+    return torch.matmul(torch.softmax(s, dim=-1), V2)
+
+
+def check_backward_rope_finite_differences(orc, seed=35):
+    """Central differences of L = sum(dO * O) through the rotary forward."""
+    h = 1e-5
+    for untied in (False, True):
+        for w, r in ((0, 4), (2, 2), (9, 4)):
+            q, k, v, wd, wu, dout = _bwd_case(seed + w, untied, B=1, Hq=2, Hkv=1, T=7, d=4,
+                                              dd=2)
+            got = orc.backward_rope(q, k, v, wd, wu, w, r, 100.0, dout, pos0=3)
+            args = [q, k, v, wd, wu]
+            for a_i, a in enumerate(args):
+                if a is None:
+                    continue
+                fd = np.empty_like(a)
+                flat = a.reshape(-1)
+                for x in range(flat.size):
+                    keep = flat[x]
+                    flat[x] = keep + h
+                    lp = np.sum(dout * orc.prefill_rope(*args, w, r, 100.0, pos0=3))
+                    flat[x] = keep - h
+                    lm = np.sum(dout * orc.prefill_rope(*args, w, r, 100.0, pos0=3))
+                    flat[x] = keep
+                    fd.reshape(-1)[x] = (lp - lm) / (2 * h)
+                np.testing.assert_allclose(got[a_i], fd, rtol=0, atol=1e-7,
+                                           err_msg="rope fd untied=%s w=%d arg %d" % (untied, w, a_i))
+
+
+def check_backward_rope_dual_store_autograd(orc, seed=36):
+    for untied in (False, True):
+        for w, r, pos0, base in ((0, 8, 5, 10000.0), (3, 6, 0, 50.0), (9, 4, 700, 10000.0),
+                                 (40, 8, 2, 10.0)):
+            q, k, v, wd, wu, dout = _bwd_case(seed + w, untied, d=8, dd=3)
+            ref = torch_grads(lambda *t: torch_dual_store_rope(*t, w, r, base, pos0), dout,
+                              q, k, v, wd, wu)
+            got = orc.backward_rope(q, k, v, wd, wu, w, r, base, dout, pos0=pos0)
+            _assert_grads(got, ref, 1e-11, "rope dual store untied=%s w=%d r=%d" % (untied, w, r))
+
+
+def check_backward_rope_zero_dim_is_plain(orc, seed=37):
+    for untied in (False, True):
+        q, k, v, wd, wu, dout = _bwd_case(seed, untied)
+        for w in (0, 4, 100):
+            got = orc.backward_rope(q, k, v, wd, wu, w, 0, 10000.0, dout, pos0=9)
+            _assert_grads(got, orc.backward(q, k, v, wd, wu, w, dout), 1e-15, "rope r=0 w=%d" % w)
+
+
+def check_backward_rope_shift_invariance(orc, seed=38):
+    """The scores depend on relative positions only, and the gradients of the
+    un-rotated inputs are rotated back: shifting every position changes none."""
+    q, k, v, wd, wu, dout = _bwd_case(seed, True, d=8, dd=3)
+    for w, r in ((5, 8), (0, 6)):
+        a = orc.backward_rope(q, k, v, wd, wu, w, r, 100.0, dout, pos0=0)
+        b = orc.backward_rope(q, k, v, wd, wu, w, r, 100.0, dout, pos0=1237)
+        _assert_grads(b, a, 1e-9, "rope shift w=%d" % w)
+    # and the rotation does change the gradients
+    assert np.abs(a[0] - orc.backward(q, k, v, wd, wu, 0, dout)[0]).max() > 1e-3
+
+
 # ---------------------------------------------------------------- shared latent
 
 def shared_case(seed, B=2, Hq=4, Hkv=2, T=23, d=8, dd=3):
@@ -611,6 +702,10 @@ ALL_CHECKS = [
     check_rope_zero_dim_is_plain,
     check_rope_shift_invariance,
     check_rope_dual_store,
+    check_backward_rope_finite_differences,
+    check_backward_rope_dual_store_autograd,
+    check_backward_rope_zero_dim_is_plain,
+    check_backward_rope_shift_invariance,
     check_shared_reduces_to_two_latents,
     check_shared_dual_store,
 ]

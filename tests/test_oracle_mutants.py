@@ -63,6 +63,18 @@ MUTANTS = [
     ("shared_matrix_transposed", "uk[(size_t)cc * d + e]", "uk[(size_t)e * dd + cc % dd]"),
     ("shared_distant_uses_full_value", "one_row(d, w, pos[i], qr + (size_t)i * d, k, v, kl, vl, s, o + (size_t)i * d,\n                            NULL, lse ? lse + i : NULL);",
      "one_row(d, w, pos[i], qr + (size_t)i * d, k, v, kl, v, s, o + (size_t)i * d,\n                            NULL, lse ? lse + i : NULL);"),
+    # RoPE in the backward
+    ("bwd_rope_dq_rotated_forward", "dar_oracle_rope(T, d, r, base, npos, dqr, dq",
+     "dar_oracle_rope(T, d, r, base, tpos, dqr, dq"),
+    ("bwd_rope_window_key_grad_rotated_forward", "dar_oracle_rope(T, d, r, base, npos, dkr, dkb);",
+     "dar_oracle_rope(T, d, r, base, tpos, dkr, dkb);"),
+    ("bwd_rope_distant_key_grad_not_rotated_back", "dar_oracle_rope(T, d, r, base, npos, dkd, dkl);",
+     "memcpy(dkl, dkd, sizeof(double) * td);"),
+    ("bwd_rope_distant_pairs_use_window_key",
+     "const double* key = local ? kr + (size_t)j * d : kdr + (size_t)j * d;",
+     "const double* key = kr + (size_t)j * d;"),
+    ("bwd_rope_distant_keys_unrotated", "dar_oracle_rope(T, d, r, base, tpos, kl, kdr);",
+     "memcpy(kdr, kl, sizeof(double) * td);"),
     ("rope_before_lift", "dar_oracle_rope(T, d, r, base, tpos, kl, klr);",
      "{ double* t_ = lift_all(T, d, dd, kr, wd, wu); memcpy(klr, t_, sizeof(double) * (size_t)T * d); free(t_); }"),
 ]
