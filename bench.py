@@ -126,6 +126,13 @@ def backward_flops(B, Hq, T, d, dd, w):
     return float(B * Hq * (10 * d * n_loc + 12 * dd * n_dist))
 
 
+def full_backward_flops(B, Hq, T, d):
+    """Algorithmic flops of the backward with the rotary embedding: every
+    causal pair at full d (the distant keys are lifted and rotated), five
+    d-wide products per pair (S, dP recomputed; dV, dK, dQ) at 2 flop/MAC."""
+    return float(B * Hq * (T * (T + 1) // 2) * 10 * d)
+
+
 def decode_bytes_shared(B, Hq, Hkv, d, dd, w, L, esize=2):
     """As decode_bytes with one shared latent per token (one latent stream
     for keys and values), plus the two U matrices."""
@@ -540,6 +547,25 @@ def main():
         btf = bflops / (bwd_us * 1e-6) / 1e12
         bwd = {"us": round(bwd_us, 2), "tflops": round(btf, 2),
                "frac_bf16_peak": round(btf / PEAK_BF16_TFLOPS, 4), "alg_flop": bflops}
+        del bws
+        if not args.no_rope:
+            # the backward with the rotary embedding (full-d distant keys)
+            rpb = dar.Rope(ROPE_PREFILL_DIM, ROPE_BASE, n_pos=pw.T, device=dev)
+            o_r, lse_r = dar.dar_attn_prefill_rope(q, k, v, wd, None, pw.w, rpb, return_lse=True)
+            rbws = torch.empty(dar.dar_prefill_rope_backward_workspace_bytes(shape, pw.T),
+                               dtype=torch.uint8, device=dev)
+            run_rb = lambda i: dar.dar_attn_prefill_rope_backward(q, k, v, wd, None, pw.w, rpb, o_r,
+                                                                  lse_r, dgrad, ws=rbws)
+            for i in range(args.warmup):
+                run_rb(i)
+            rb_us = float(timed(run_rb, args.steps) * 1e3)
+            rbf = full_backward_flops(pw.B, pw.Hq, pw.T, pw.d)
+            bwd["rope"] = {"shape": "pythia70m batch, rotary dim %d, base %g" % (ROPE_PREFILL_DIM,
+                                                                                ROPE_BASE),
+                           "us": round(rb_us, 2), "alg_flop": rbf,
+                           "tflops": round(rbf / (rb_us * 1e-6) / 1e12, 2),
+                           "frac_bf16_peak": round(rbf / (rb_us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+            del rbws, o_r, lse_r
 
     launch = None
     if not args.no_launch:

@@ -394,6 +394,29 @@ dar_status dar_attn_prefill_backward(const dar_shape* s, int T, const void* q, c
                                      void* dk, void* dv, float* dw_down, float* dw_up, void* ws,
                                      size_t ws_bytes, hipStream_t stream);
 
+/* Backward of dar_attn_prefill_rope: the gradients of L = sum(dout * o) with
+ * respect to the un-rotated q, k, v and W_down, W_up (Section 2.3 trains
+ * through the attention, Eq. 3 puts the rotation inside it). The window keys
+ * are R_j k_j, the distant keys R_j ((k_j W_down) W_up), so a distant pair's
+ * key gradient is rotated back (R_j^T) before it goes through the lift.
+ *   T, pos0, rope: as for the forward call; q, k, v, w_down, w_up, o, lse:
+ *   its inputs, its output and the log-sum-exp it wrote; dout [B][Hq][T][d].
+ *   Outputs as for dar_attn_prefill_backward (dq, dk, dv in bf16; dw_down,
+ *   dw_up fp32, dw_up NULL exactly when w_up is NULL, the tied case then in
+ *   dw_down); every output is overwritten, every reduction runs in a fixed
+ *   order.
+ *   ws: at least dar_prefill_rope_backward_workspace_bytes(s, T) bytes
+ *   (caller-owned, overwritten): the rotated and lifted operands and fp32
+ *   gradient arrays of the full-d distant keys.
+ * Supported: bf16 with d in {64, 128}, any rotary_dim, d_down up to d (up to
+ * 64 at d = 128); other shapes return DAR_E_UNSUPPORTED. */
+dar_status dar_attn_prefill_rope_backward(const dar_shape* s, int T, int pos0, const dar_rope* rope,
+                                          const void* q, const void* k, const void* v,
+                                          const void* w_down, const void* w_up, const void* o,
+                                          const float* lse, const void* dout, void* dq, void* dk,
+                                          void* dv, float* dw_down, float* dw_up, void* ws,
+                                          size_t ws_bytes, hipStream_t stream);
+
 /* Workspace sizes (0 on an invalid shape). */
 size_t dar_prefill_workspace_bytes(const dar_shape* s, int T);
 size_t dar_decode_workspace_bytes(const dar_shape* s, int cap);
@@ -402,6 +425,7 @@ size_t dar_prefill_chunk_workspace_bytes(const dar_shape* s, int len, int n);
 size_t dar_prefill_rope_workspace_bytes(const dar_shape* s, int T);
 size_t dar_prefill_chunk_rope_workspace_bytes(const dar_shape* s, int len, int n);
 size_t dar_prefill_chunk_paged_workspace_bytes(const dar_shape* s, int cap, int n);
+size_t dar_prefill_rope_backward_workspace_bytes(const dar_shape* s, int T);
 
 /* Static English text for a status code. */
 const char* dar_status_string(dar_status st);

@@ -82,6 +82,10 @@ def _load():
     lib.dar_rope_table.argtypes = [ci, ctypes.c_double, ci, vp, vp]
     lib.dar_attn_prefill_rope.restype = ci
     lib.dar_attn_prefill_rope.argtypes = [shp, ci, ci, rp] + [vp] * 8 + [sz, vp]
+    lib.dar_attn_prefill_rope_backward.restype = ci
+    lib.dar_attn_prefill_rope_backward.argtypes = [shp, ci, ci, rp] + [vp] * 14 + [sz, vp]
+    lib.dar_prefill_rope_backward_workspace_bytes.restype = sz
+    lib.dar_prefill_rope_backward_workspace_bytes.argtypes = [shp, ci]
     lib.dar_attn_decode_rope.restype = ci
     lib.dar_attn_decode_rope.argtypes = [shp, cp, rp] + [vp] * 5 + [sz, vp]
     lib.dar_attn_prefill_shared.restype = ci
@@ -335,6 +339,45 @@ def dar_attn_prefill_backward(q, k, v, w_down, w_up, w, o, lse, dout, ws=None, s
                                        _stream(stream))
     if st != DAR_OK:
         raise DarError(st, "dar_attn_prefill_backward")
+    return dq, dk, dv, dwd, dwu
+
+
+def dar_prefill_rope_backward_workspace_bytes(shape: DarShape, T: int) -> int:
+    return int(lib.dar_prefill_rope_backward_workspace_bytes(ctypes.byref(shape), int(T)))
+
+
+def dar_attn_prefill_rope_backward(q, k, v, w_down, w_up, w, rope: "Rope", o, lse, dout, pos0=0,
+                                   ws=None, stream=None):
+    """Gradients of sum(dout * o) of dar_attn_prefill_rope (same q, k, v,
+    weights, rope and pos0; its o and lse). Returns (dq, dk, dv, dw_down,
+    dw_up) as dar_attn_prefill_backward does."""
+    B, Hq, T, d = q.shape
+    Hkv = k.shape[1]
+    dd = w_down.shape[2]
+    shape = make_shape(B, Hq, Hkv, d, dd, w, q.dtype)
+    for name, t, want in (("k", k, (B, Hkv, T, d)), ("v", v, (B, Hkv, T, d)),
+                          ("w_down", w_down, (Hkv, d, dd)), ("o", o, (B, Hq, T, d)),
+                          ("dout", dout, (B, Hq, T, d))):
+        if tuple(t.shape) != want or t.dtype != q.dtype:
+            raise ValueError("%s: expected %s %s" % (name, want, q.dtype))
+    if tuple(lse.shape) != (B, Hq, T) or lse.dtype != torch.float32:
+        raise ValueError("lse: expected %s float32" % ((B, Hq, T),))
+    dq = torch.empty_like(q)
+    dk = torch.empty_like(k)
+    dv = torch.empty_like(v)
+    dwd = torch.empty(Hkv, d, dd, dtype=torch.float32, device=q.device)
+    dwu = None if w_up is None else torch.empty(Hkv, dd, d, dtype=torch.float32, device=q.device)
+    if ws is None:
+        ws = _workspace(dar_prefill_rope_backward_workspace_bytes(shape, T), q.device)
+    rs = rope.struct()
+    st = lib.dar_attn_prefill_rope_backward(ctypes.byref(shape), int(T), int(pos0), ctypes.byref(rs),
+                                            _ptr(q), _ptr(k), _ptr(v), _ptr(w_down), _ptr(w_up),
+                                            _ptr(o), _ptr(lse), _ptr(dout), _ptr(dq), _ptr(dk),
+                                            _ptr(dv), _ptr(dwd), _ptr(dwu), _ptr(ws),
+                                            0 if ws is None else ws.numel() * ws.element_size(),
+                                            _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_prefill_rope_backward")
     return dq, dk, dv, dwd, dwu
 
 

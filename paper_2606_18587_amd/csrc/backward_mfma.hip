@@ -1089,4 +1089,544 @@ hipError_t launch_bwd_mfma(const bf16_t* q, const bf16_t* k, const bf16_t* v, co
     return hipErrorInvalidValue;
 }
 
+
+// ================================================================ rotary embedding
+//
+// Backward of dar_attn_prefill_rope (Eq. 3 with the rotation; Section 2.3
+// trains through it). The forward attends at full d: rotated queries qr,
+// rotated window keys kr with values v, lifted-then-rotated distant keys kd
+// with lifted values vd (the rotary pre-pass writes them; kd, vd hold
+// positions 0..Td-1, Td = T - w). The softmax is recomputed against the
+// forward's log-sum-exp:
+//   bwd_rope_rowprep_kernel  -lse (log2 units) and -delta = -dO . O per row
+//   bwd_rope_rows_kernel     dqr = s sum_j dS_ij key_ij over both regions
+//   bwd_rope_cols_kernel     per key, s sum_i dS_ij qr_i and sum_i P_ij dO_i over
+//                            the rows that see it in the window (dkr, dvw) or
+//                            at distance (dkd, dvd)
+//   bwd_rope_post_rows_kernel  dq = R^T dqr
+//   bwd_rope_post_keys_kernel  the rotation taken back (R^T) and the chain rule
+//                            through the lift x' = (x W_down) W_up for keys and
+//                            values, with the weight-gradient shares
+//   bwd_wreduce_kernel       the shares summed in a fixed order
+// with s = 1/sqrt(d). The rows and cols kernels are the window kernels'
+// loops with the key range and mask of either region.
+
+namespace {
+
+// -lse (log2 units) and -delta per row, zero for the padding rows. One
+// thread per row (16-byte loads along the row).
+template <int D>
+__global__ __launch_bounds__(256) void bwd_rope_rowprep_kernel(const bf16_t* __restrict__ o,
+                                                               const bf16_t* __restrict__ dout,
+                                                               const float* __restrict__ lse,
+                                                               float* __restrict__ nl2,
+                                                               float* __restrict__ nd, int T,
+                                                               int Tr) {
+    const int bh = wg_id_y();
+    const int i = wg_id_x() * 256 + lane_id_x();
+    if (i >= Tr) return;
+    float acc = 0.f;
+    if (i < T) {
+        const size_t row = ((size_t)bh * T + i) * D;
+#pragma unroll
+        for (int e = 0; e < D; e += 8) {
+            const uint4 a = *reinterpret_cast<const uint4*>(o + row + e);
+            const uint4 b = *reinterpret_cast<const uint4*>(dout + row + e);
+            const uint32_t ua[4] = {a.x, a.y, a.z, a.w}, ub[4] = {b.x, b.y, b.z, b.w};
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                acc = __builtin_fmaf(__uint_as_float(ua[q] << 16), __uint_as_float(ub[q] << 16), acc);
+                acc = __builtin_fmaf(__uint_as_float(ua[q] & 0xffff0000u), __uint_as_float(ub[q] & 0xffff0000u), acc);
+            }
+        }
+    }
+    nd[(size_t)bh * Tr + i] = i < T ? -acc : 0.f;
+    nl2[(size_t)bh * Tr + i] = i < T ? -lse[(size_t)bh * T + i] * kLog2eB : 0.f;
+}
+
+// One wavefront per 32 query rows: dqr^T += K^T dS^T over the window keys
+// (kr, v: i - w < j <= i) and the distant keys (kd, vd: j <= i - w), 64-key
+// tiles staged through LDS for the workgroup. Writes s dqr (fp32) of every
+// real row. Grid: ceil(T / (32 NW)) * B * Hq workgroups (xcd_block_head).
+template <int D, int NW>
+__global__ __launch_bounds__(NW * 64) void bwd_rope_rows_kernel(
+    const bf16_t* __restrict__ qr, const bf16_t* __restrict__ kr, const bf16_t* __restrict__ v,
+    const bf16_t* __restrict__ kd, const bf16_t* __restrict__ vd, const bf16_t* __restrict__ dout,
+    const float* __restrict__ nl2, const float* __restrict__ nd, float* __restrict__ dqr, int Hq,
+    int Hkv, int T, int Tr, int w, float qscale, float scale, int BH) {
+    constexpr int KS = D / 16, NT = D / 32, BN = 64, LDK = D + 8;
+    constexpr int BM = NW * 32;
+    __shared__ __attribute__((aligned(16))) bf16_t lds_kv[2 * BN * LDK];  // K tile, V tile
+    bf16_t* lds_k = lds_kv;
+    bf16_t* lds_v = lds_kv + BN * LDK;
+
+    const int tid = lane_id_x(), lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int nblk = (T + BM - 1) / BM;
+    int rbi, bh;
+    xcd_block_head(wg_id_x(), BH, rbi, bh);
+    const int rb = nblk - 1 - rbi;
+    const int b = bh / Hq, h = bh % Hq;
+    const int G = Hq / Hkv;
+    const int g = h / G;
+    const int bg = b * Hkv + g;
+    const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
+    const int i0 = rb * BM, r0 = i0 + wave * 32, i = r0 + qc;
+    const bool live = r0 < T;
+    const int i_hi = imin(r0 + 31, T - 1);
+    const int iwg_hi = imin(i0 + BM - 1, T - 1);
+    const int ii = imin(i, T - 1);
+    const int Td = imax(T - w, 0);
+
+    const bf16_t* qrow = qr + ((size_t)bh * T + ii) * D;
+    const bf16_t* drow = dout + ((size_t)bh * T + ii) * D;
+    bf16x8_t qop[KS], doop[KS];
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        qop[s] = load_bf16x8(qrow + s * 16 + hg * 8);
+        doop[s] = load_bf16x8(drow + s * 16 + hg * 8);
+    }
+    const size_t prw = (size_t)bh * Tr + ii;
+    const float nL = nl2[prw];
+    const f32x16_t negd = splat16(nd[prw]);
+    f32x16_t dqT[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) dqT[t] = splat16(0.f);
+
+    // keys [t_first, t_last] of one region (workgroup-uniform bounds: every
+    // thread reaches the barriers)
+    auto region = [&](const bf16_t* kg, const bf16_t* vg, int nkeys, int t_first, int t_last,
+                      bool dist) {
+        TilePair<D, NW> tp;
+        tp.fetch(kg, vg, t_first, nkeys, tid);
+        for (int t = t_first; t <= t_last; t += BN) {
+            __syncthreads();  // the previous tile is no longer read
+            tp.store(lds_k, lds_v, LDK, tid);
+            __syncthreads();
+            if (t + BN <= t_last) tp.fetch(kg, vg, t + BN, nkeys, tid);
+            if (!live) continue;
+#pragma unroll
+            for (int sub = 0; sub < BN / 32; ++sub) {
+                const int js = t + sub * 32;
+                if (dist ? js > i_hi - w : (js > i_hi || js + 31 <= r0 - w)) continue;
+                f32x16_t sc = splat16(0.f), dp = negd;
+#pragma unroll
+                for (int s = 0; s < KS; ++s) {
+                    sc = mfma(load_bf16x8(lds_k + (sub * 32 + prow) * LDK + s * 16 + hg * 8), qop[s], sc);
+                    dp = mfma(load_bf16x8(lds_v + (sub * 32 + prow) * LDK + s * 16 + hg * 8), doop[s], dp);
+                }
+                f32x16_t x;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], qscale, nL);
+                const bool full = dist ? js + 31 <= r0 - w : (js > i_hi - w && js + 31 <= r0);
+                if (!full) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int j = js + acc_row(r, hg);
+                        if (dist ? j > i - w : (j <= i - w || j > i)) x[r] = -INFINITY;
+                    }
+                }
+                f32x16_t ds;
+#pragma unroll
+                for (int r = 0; r < 16; ++r) ds[r] = __builtin_amdgcn_exp2f(x[r]) * dp[r];
+                const bf16x8_t s0 = pack8(ds, 0), s1 = pack8(ds, 8);
+#pragma unroll
+                for (int tt = 0; tt < NT; ++tt) {
+                    dqT[tt] = mfma(lds_tr_operand(lds_k, LDK, sub * 32, tt * 32, lane), s0, dqT[tt]);
+                    dqT[tt] = mfma(lds_tr_operand(lds_k, LDK, sub * 32 + 16, tt * 32, lane), s1, dqT[tt]);
+                }
+            }
+        }
+    };
+    if (w > 0) region(kr + (size_t)bg * T * D, v + (size_t)bg * T * D, T, imax(0, i0 - w + 1) & ~(BN - 1),
+                      iwg_hi, false);
+    if (iwg_hi - w >= 0) region(kd + (size_t)bg * Td * D, vd + (size_t)bg * Td * D, Td, 0, iwg_hi - w, true);
+
+    if (live && i < T) {
+        float* out = dqr + ((size_t)bh * T + i) * D;
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+            for (int a = 0; a < 4; ++a)
+                *reinterpret_cast<float4*>(out + tt * 32 + 8 * a + 4 * hg) =
+                    make_float4(dqT[tt][4 * a] * scale, dqT[tt][4 * a + 1] * scale,
+                                dqT[tt][4 * a + 2] * scale, dqT[tt][4 * a + 3] * scale);
+    }
+}
+
+// One wavefront per 32 keys of one region's key array (kx, vx: kr and v for
+// the window, kd and vd at distance, nkeys rows a head), the rows of every
+// query head of the group that see them there (window: j <= i < j + w; at
+// distance: i >= j + w) through 64-row Q / dO tiles in LDS:
+// dk^T += Q^T dS (times s), dv^T += dO^T P. Writes both (fp32) for every key.
+// Grid: ceil(nkeys / (32 NW)) * B * Hkv workgroups (xcd_block_head).
+template <int D, int NW, bool DIST>
+__global__ __launch_bounds__(NW * 64) void bwd_rope_cols_kernel(
+    const bf16_t* __restrict__ qr, const bf16_t* __restrict__ kx, const bf16_t* __restrict__ vx,
+    const bf16_t* __restrict__ dout, const float* __restrict__ nl2, const float* __restrict__ nd,
+    float* __restrict__ dk, float* __restrict__ dv, int Hq, int Hkv, int T, int Tr, int nkeys,
+    int w, float qscale, float scale, int BKV) {
+    constexpr int KS = D / 16, NT = D / 32, BN = 64, LDK = D + 8;
+    constexpr int BK = NW * 32;
+    __shared__ __attribute__((aligned(16))) bf16_t lds_qd[2 * BN * LDK];  // Q tile, dO tile
+    __shared__ __attribute__((aligned(16))) float lds_lse[BN];  // -lse (log2 units)
+    __shared__ __attribute__((aligned(16))) float lds_del[BN];  // -delta
+    bf16_t* lds_q = lds_qd;
+    bf16_t* lds_do = lds_qd + BN * LDK;
+
+    const int tid = lane_id_x(), lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int cb, bg;
+    xcd_block_head(wg_id_x(), BKV, cb, bg);
+    const int b = bg / Hkv, g = bg % Hkv;
+    const int G = Hq / Hkv;
+    const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
+    const int cwg_lo = cb * BK;
+    const int c0 = cwg_lo + wave * 32, j = c0 + qc;
+    const bool live = c0 < nkeys;
+    const int j_hi = imin(c0 + 31, nkeys - 1);
+    const int cwg_hi = imin(cwg_lo + BK - 1, nkeys - 1);
+    const int jj = imin(j, nkeys - 1);
+
+    bf16x8_t kop[KS], vop[KS];
+    const bf16_t* krow = kx + ((size_t)bg * nkeys + jj) * D;
+    const bf16_t* vrow = vx + ((size_t)bg * nkeys + jj) * D;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        kop[s] = load_bf16x8(krow + s * 16 + hg * 8);
+        vop[s] = load_bf16x8(vrow + s * 16 + hg * 8);
+    }
+    f32x16_t dkT[NT], dvT[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) { dkT[t] = splat16(0.f); dvT[t] = splat16(0.f); }
+    // the workgroup's rows: window [cwg_lo, cwg_hi + w - 1], at distance [cwg_lo + w, T - 1]
+    const int row_lo = DIST ? cwg_lo + w : cwg_lo;
+    const int row_hi = DIST ? T - 1 : imin(T - 1, cwg_hi + w - 1);
+    const int ntile = row_hi >= row_lo ? (row_hi - row_lo) / BN + 1 : 0;
+    TilePair<D, NW> tp;
+    float sv = 0.f;  // -lse (threads 0..63) or -delta (64..127) of one tile row
+    auto fetch = [&](int n) {
+        const int hh = n / ntile, t = row_lo + (n - hh * ntile) * BN;
+        const size_t bh = (size_t)b * Hq + g * G + hh;
+        tp.fetch(qr + bh * T * D, dout + bh * T * D, t, T, tid);
+        if (tid < 2 * BN) {
+            const int r = tid & (BN - 1);
+            const float* src = (tid < BN ? nl2 : nd) + bh * Tr;
+            sv = t + r < Tr ? src[imin(t + r, Tr - 1)] : 0.f;
+        }
+    };
+    if (ntile > 0) fetch(0);
+    for (int n = 0; n < G * ntile; ++n) {
+        const int t = row_lo + (n % ntile) * BN;
+        __syncthreads();  // the previous tile is no longer read
+        tp.store(lds_q, lds_do, LDK, tid);
+        if (tid < BN) lds_lse[tid] = sv;
+        else if (tid < 2 * BN) lds_del[tid - BN] = sv;
+        __syncthreads();
+        if (n + 1 < G * ntile) fetch(n + 1);
+        if (!live) continue;
+#pragma unroll
+        for (int sub = 0; sub < BN / 32; ++sub) {
+            const int is = t + sub * 32;
+            if (DIST ? is + 31 < c0 + w : (is + 31 < c0 || is > j_hi + w - 1)) continue;
+            f32x16_t sc = splat16(0.f);
+            f32x16_t dp = load_row16(lds_del + sub * 32, hg, 1.f);
+#pragma unroll
+            for (int s = 0; s < KS; ++s) {
+                sc = mfma(load_bf16x8(lds_q + (sub * 32 + prow) * LDK + s * 16 + hg * 8), kop[s], sc);
+                dp = mfma(load_bf16x8(lds_do + (sub * 32 + prow) * LDK + s * 16 + hg * 8), vop[s], dp);
+            }
+            const f32x16_t ln = load_row16(lds_lse + sub * 32, hg, 1.f);
+            f32x16_t x;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) x[r] = __builtin_fmaf(sc[r], qscale, ln[r]);
+            const bool full = DIST ? (is >= j_hi + w && is + 31 < T)
+                                   : (is >= c0 + 31 && is + 31 - c0 < w && is + 31 < T);
+            if (!full) {
+#pragma unroll
+                for (int r = 0; r < 16; ++r) {
+                    const int i = is + acc_row(r, hg);
+                    if (DIST ? (i - j < w || i >= T) : (i < j || i - j >= w || i >= T)) x[r] = -INFINITY;
+                }
+            }
+            f32x16_t p, ds;
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                p[r] = __builtin_amdgcn_exp2f(x[r]);
+                ds[r] = p[r] * dp[r];
+            }
+            const bf16x8_t p0 = pack8(p, 0), p1 = pack8(p, 8);
+            const bf16x8_t s0 = pack8(ds, 0), s1 = pack8(ds, 8);
+#pragma unroll
+            for (int tt = 0; tt < NT; ++tt) {
+                dvT[tt] = mfma(lds_tr_operand(lds_do, LDK, sub * 32, tt * 32, lane), p0, dvT[tt]);
+                dvT[tt] = mfma(lds_tr_operand(lds_do, LDK, sub * 32 + 16, tt * 32, lane), p1, dvT[tt]);
+                dkT[tt] = mfma(lds_tr_operand(lds_q, LDK, sub * 32, tt * 32, lane), s0, dkT[tt]);
+                dkT[tt] = mfma(lds_tr_operand(lds_q, LDK, sub * 32 + 16, tt * 32, lane), s1, dkT[tt]);
+            }
+        }
+    }
+    if (live && j < nkeys) {
+        float* dkr = dk + ((size_t)bg * nkeys + j) * D;
+        float* dvr = dv + ((size_t)bg * nkeys + j) * D;
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt)
+#pragma unroll
+            for (int a = 0; a < 4; ++a) {
+                *reinterpret_cast<float4*>(dkr + tt * 32 + 8 * a + 4 * hg) =
+                    make_float4(dkT[tt][4 * a] * scale, dkT[tt][4 * a + 1] * scale,
+                                dkT[tt][4 * a + 2] * scale, dkT[tt][4 * a + 3] * scale);
+                *reinterpret_cast<float4*>(dvr + tt * 32 + 8 * a + 4 * hg) =
+                    make_float4(dvT[tt][4 * a], dvT[tt][4 * a + 1], dvT[tt][4 * a + 2], dvT[tt][4 * a + 3]);
+            }
+    }
+}
+
+// Element e of R_p^T x for a row x at position p: the rotation taken back,
+// pairs (m, m + r/2) turned by -p base^(-2m/r) (tab [n_pos][r]: cos, then sin).
+__device__ __forceinline__ float rot_back(const float* x, int e, int r, const float* tabp) {
+    const int h = r >> 1;
+    if (e >= r) return x[e];
+    const int m = e < h ? e : e - h;
+    const float c = tabp[m], s = tabp[h + m];
+    return e < h ? __builtin_fmaf(x[e], c, x[e + h] * s) : __builtin_fmaf(x[e], c, -x[e - h] * s);
+}
+
+// dq = R^T dqr (bf16). One thread per element.
+__global__ __launch_bounds__(256) void bwd_rope_post_rows_kernel(const float* __restrict__ dqr,
+                                                                 const float* __restrict__ tab,
+                                                                 bf16_t* __restrict__ dq, int T,
+                                                                 int d, int r, int pos0,
+                                                                 long long n) {
+    const long long idx = (long long)wg_id_x() * 256 + lane_id_x();
+    if (idx >= n) return;
+    const long long row = idx / d;
+    const int e = (int)(idx - row * d);
+    const int i = (int)(row % T);
+    dq[idx] = f32_to_bf16(rot_back(dqr + row * d, e, r, tab + (size_t)(pos0 + i) * r));
+}
+
+// The chain rule per key, and the weight-gradient shares. A workgroup takes
+// kRopeKeysPerWg keys of one (batch, KV head) in blocks of rope_post_block(D); per key j
+// (u_j = R^T dkd_j and dvd_j zero at or past Td = T - w):
+//   gK_j = u_j W_up^T,  gV_j = dvd_j W_up^T,  cK_j = k_j W_down,  cV_j = v_j W_down
+//   dk_j = R^T dkr_j + gK_j W_down^T,  dv_j = dvw_j + gV_j W_down^T   (bf16)
+// and over its keys, in key order, the shares [e][c]
+//   dW_down += k_j[e] gK_j[c] + v_j[e] gV_j[c]
+//   dW_up^T += u_j[e] cK_j[c] + dvd_j[e] cV_j[c]
+// (chunk b * ceil(T / kRopeKeysPerWg) + workgroup). d_down <= D.
+constexpr int kRopeKeysPerWg = 32;
+
+// Keys per block of bwd_rope_post_keys_kernel (32 measured slower at d = 64:
+// 310 against 256 us at the pythia70m shape), and its dynamic LDS in floats:
+// four [KB][D + 1] key blocks (rows padded by one float: the lanes reading one
+// column of different rows hit different banks), four [KB][dd] latent blocks
+// and three copies of the weights.
+__host__ __device__ constexpr int rope_post_block(int) { return 16; }
+static inline size_t rope_post_lds_bytes(int D, int dd) {
+    const size_t kb = rope_post_block(D);
+    return sizeof(float) * (4 * kb * (D + 1) + 4 * kb * dd + (size_t)3 * D * dd);
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
+    const bf16_t* __restrict__ k, const bf16_t* __restrict__ v, const bf16_t* __restrict__ wd,
+    const bf16_t* __restrict__ wu, const float* __restrict__ dkr, const float* __restrict__ dvw,
+    const float* __restrict__ dkd, const float* __restrict__ dvd, const float* __restrict__ tab,
+    bf16_t* __restrict__ dk, bf16_t* __restrict__ dv, float* __restrict__ wpart, int Hkv, int T,
+    int dd, int w, int r, int pos0, int nchunk) {
+    constexpr int KB = rope_post_block(D);
+    constexpr int NO = D * D / 256;  // weight outputs a thread may own (dd <= D)
+    constexpr int XJ = KB * D / 256, JS = 256 / D;  // keys of a thread in dk/dv, their stride
+    extern __shared__ float sm[];
+    constexpr int LD = D + 1;         // padded key row
+    float* su = sm;                   // [KB][LD]  u = R^T dkd
+    float* svd = su + KB * LD;        // [KB][LD]  dvd
+    float* sk = svd + KB * LD;        // [KB][LD]  k
+    float* sv = sk + KB * LD;         // [KB][LD]  v
+    float* sg = sv + KB * LD;         // [4][KB][dd]  gK, gV, cK, cV
+    float* swd = sg + 4 * KB * dd;    // [D][dd]  W_down[e][c]
+    float* swu = swd + D * dd;        // [D][dd]  W_up[c][e] at [e][c]
+    float* swt = swu + D * dd;        // [dd][D]  W_down[e][c] at [c][e]
+    const int bg = wg_id_y(), b = bg / Hkv, g = bg % Hkv;
+    const int tid = lane_id_x();
+    const int Td = imax(T - w, 0);
+    const int nkb = (T + kRopeKeysPerWg - 1) / kRopeKeysPerWg;
+    const int j_lo = wg_id_x() * kRopeKeysPerWg;
+    const int j_end = imin(j_lo + kRopeKeysPerWg, T);
+    const bf16_t* wdg = wd + (size_t)g * D * dd;
+    const bf16_t* wug = wu ? wu + (size_t)g * dd * D : nullptr;
+    const int n_out = D * dd;
+    // weight shares: TPE threads per element e, cpt columns each
+    constexpr int TPE = 256 / D;
+    const int we = tid / TPE, wq = tid % TPE;
+    const int cpt = (dd + TPE - 1) / TPE;
+    for (int idx = tid; idx < n_out; idx += 256) {
+        const int e = idx / dd, c = idx - (idx / dd) * dd;
+        const float x = bf16_to_f32(wdg[idx]);
+        swd[idx] = x;
+        swt[c * D + e] = x;
+        swu[idx] = wug ? bf16_to_f32(wug[(size_t)c * D + e]) : x;
+    }
+    float accd[NO], accu[NO];
+#pragma unroll
+    for (int x = 0; x < NO; ++x) accd[x] = accu[x] = 0.f;
+    for (int j0 = j_lo; j0 < j_end; j0 += KB) {
+        __syncthreads();  // the weights are staged; the previous block is no longer read
+        // stage: u = R^T dkd, dvd, k, v of the block's keys (zero past the ends)
+        for (int idx = tid; idx < KB * D; idx += 256) {
+            const int jl = idx / D, e = idx - (idx / D) * D, j = j0 + jl;
+            float uu = 0.f, vd = 0.f, kk = 0.f, vv = 0.f;
+            if (j < j_end) {
+                const size_t row = (size_t)bg * T + j;
+                kk = bf16_to_f32(k[row * D + e]);
+                vv = bf16_to_f32(v[row * D + e]);
+                if (j < Td) {
+                    const size_t drow = (size_t)bg * Td + j;
+                    uu = rot_back(dkd + drow * D, e, r, tab + (size_t)(pos0 + j) * r);
+                    vd = dvd[drow * D + e];
+                }
+            }
+            su[jl * LD + e] = uu;
+            svd[jl * LD + e] = vd;
+            sk[jl * LD + e] = kk;
+            sv[jl * LD + e] = vv;
+        }
+        __syncthreads();
+        // gK, gV (through W_up) and cK, cV (through W_down), d_down wide: the
+        // four products of one (key, column) together (independent chains)
+        for (int idx = tid; idx < KB * dd; idx += 256) {
+            const int jl = idx / dd, c = idx - (idx / dd) * dd;
+            float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll 8
+            for (int e = 0; e < D; ++e) {
+                const float wup = swu[e * dd + c], wdn = swd[e * dd + c];
+                a0 = __builtin_fmaf(su[jl * LD + e], wup, a0);
+                a1 = __builtin_fmaf(svd[jl * LD + e], wup, a1);
+                a2 = __builtin_fmaf(sk[jl * LD + e], wdn, a2);
+                a3 = __builtin_fmaf(sv[jl * LD + e], wdn, a3);
+            }
+            sg[idx] = a0;
+            sg[KB * dd + idx] = a1;
+            sg[2 * KB * dd + idx] = a2;
+            sg[3 * KB * dd + idx] = a3;
+        }
+        __syncthreads();
+        // dk, dv of the block's keys: a thread keeps one element e of XJ keys,
+        // so each weight it reads serves all of them
+        {
+            const int e = tid % D, jl0 = tid / D;
+            float xk[XJ], xv[XJ];
+#pragma unroll
+            for (int x = 0; x < XJ; ++x) {
+                const int j = imin(j0 + jl0 + JS * x, j_end - 1);
+                const size_t row = (size_t)bg * T + j;
+                xk[x] = rot_back(dkr + row * D, e, r, tab + (size_t)(pos0 + j) * r);
+                xv[x] = dvw[row * D + e];
+            }
+            for (int c = 0; c < dd; ++c) {
+                const float wdn = swt[c * D + e];
+#pragma unroll
+                for (int x = 0; x < XJ; ++x) {
+                    xk[x] = __builtin_fmaf(sg[(jl0 + JS * x) * dd + c], wdn, xk[x]);
+                    xv[x] = __builtin_fmaf(sg[(KB + jl0 + JS * x) * dd + c], wdn, xv[x]);
+                }
+            }
+#pragma unroll
+            for (int x = 0; x < XJ; ++x) {
+                const int j = j0 + jl0 + JS * x;
+                if (j < j_end) {
+                    const size_t row = (size_t)bg * T + j;
+                    dk[row * D + e] = f32_to_bf16(xk[x]);
+                    dv[row * D + e] = f32_to_bf16(xv[x]);
+                }
+            }
+        }
+        // weight shares, key by key in order: a thread owns element e and the
+        // columns [q cpt, q cpt + cpt) (independent chains; columns past
+        // d_down are clamped and never stored)
+        for (int jl = 0; jl < KB; ++jl) {
+            const float k_ = sk[jl * LD + we], v_ = sv[jl * LD + we];
+            const float u_ = su[jl * LD + we], d_ = svd[jl * LD + we];
+            const float* g0 = sg + jl * dd;
+#pragma unroll
+            for (int y = 0; y < NO; ++y) {
+                if (y >= cpt) break;  // uniform
+                const int c = imin(wq * cpt + y, dd - 1);
+                accd[y] = __builtin_fmaf(k_, g0[c], accd[y]);
+                accd[y] = __builtin_fmaf(v_, g0[KB * dd + c], accd[y]);
+                accu[y] = __builtin_fmaf(u_, g0[2 * KB * dd + c], accu[y]);
+                accu[y] = __builtin_fmaf(d_, g0[3 * KB * dd + c], accu[y]);
+            }
+        }
+    }
+    const int chunk = b * nkb + wg_id_x();
+    float* pd = wpart + ((size_t)g * nchunk + chunk) * n_out;
+    float* pu = wpart + ((size_t)(Hkv + g) * nchunk + chunk) * n_out;
+#pragma unroll
+    for (int y = 0; y < NO; ++y) {
+        const int c = wq * cpt + y;
+        if (y < cpt && c < dd) {
+            pd[we * dd + c] = accd[y];
+            pu[we * dd + c] = accu[y];
+        }
+    }
+}
+
+}  // namespace
+
+// (the post kernel's LDS, within the 160 KB of a compute unit: d_down <= 64 at d = 128)
+bool bwd_rope_mfma_supported(int d, int dd, bool bf16) {
+    return bf16 && (d == 64 || d == 128) && dd <= d && rope_post_lds_bytes(d, dd) <= 160 * 1024;
+}
+
+template <int D>
+static hipError_t launch_bwd_rope_t(const RopeBwdArgs& a, hipStream_t st) {
+    constexpr int NW = 4;
+    const int B = a.B, Hq = a.Hq, Hkv = a.Hkv, T = a.T, w = a.w, dd = a.dd, r = a.r;
+    const int Tr = round_up(T, 64);
+    const int Td = T - w > 0 ? T - w : 0;
+    const float scale = 1.f / sqrtf((float)D);
+    const float qscale = scale * kLog2eB;
+    const int BM = NW * 32;
+    const int nblk = (T + BM - 1) / BM;
+    hipLaunchKernelGGL(bwd_rope_rowprep_kernel<D>, dim3((Tr + 255) / 256, B * Hq), dim3(256), 0, st, a.o, a.dout,
+                       a.lse, a.nl2, a.nd, T, Tr);
+    hipLaunchKernelGGL((bwd_rope_rows_kernel<D, NW>), dim3(nblk * B * Hq), dim3(NW * 64), 0, st, a.qr,
+                       a.kr, a.v, a.kd, a.vd, a.dout, (const float*)a.nl2, (const float*)a.nd, a.dqr, Hq,
+                       Hkv, T, Tr, w, qscale, scale, B * Hq);
+    hipLaunchKernelGGL((bwd_rope_cols_kernel<D, NW, false>), dim3(nblk * B * Hkv), dim3(NW * 64), 0, st,
+                       a.qr, a.kr, a.v, a.dout, (const float*)a.nl2, (const float*)a.nd, a.dkr, a.dvw,
+                       Hq, Hkv, T, Tr, T, w, qscale, scale, B * Hkv);
+    if (Td > 0) {
+        const int nkb = (Td + BM - 1) / BM;
+        hipLaunchKernelGGL((bwd_rope_cols_kernel<D, NW, true>), dim3(nkb * B * Hkv), dim3(NW * 64), 0, st,
+                           a.qr, a.kd, a.vd, a.dout, (const float*)a.nl2, (const float*)a.nd, a.dkd,
+                           a.dvd, Hq, Hkv, T, Tr, Td, w, qscale, scale, B * Hkv);
+    }
+    const long long nq = (long long)B * Hq * T * D;
+    hipLaunchKernelGGL(bwd_rope_post_rows_kernel, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, st,
+                       (const float*)a.dqr, a.tab, a.dq, T, D, r, a.pos0, nq);
+    const int nkb = (T + kRopeKeysPerWg - 1) / kRopeKeysPerWg;
+    const size_t plds = rope_post_lds_bytes(D, dd);
+    if (plds > 65536) {
+        const hipError_t e = hipFuncSetAttribute((const void*)bwd_rope_post_keys_kernel<D>,
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)plds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL(bwd_rope_post_keys_kernel<D>, dim3(nkb, B * Hkv), dim3(256), plds, st, a.k, a.v, a.wd,
+                       a.wu, (const float*)a.dkr, (const float*)a.dvw, (const float*)a.dkd,
+                       (const float*)a.dvd, a.tab, a.dk, a.dv, a.wpart, Hkv, T, dd, w, r, a.pos0,
+                       a.L.nchunk);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_bwd_wreduce(a.wpart, a.dwd, a.dwu, Hkv, D, dd, a.L, st);
+}
+
+hipError_t launch_bwd_rope_mfma(const RopeBwdArgs& a, int d, hipStream_t st) {
+    if (d == 64) return launch_bwd_rope_t<64>(a, st);
+    if (d == 128) return launch_bwd_rope_t<128>(a, st);
+    return hipErrorInvalidValue;
+}
+
 }  // namespace dar

@@ -241,6 +241,39 @@ struct ChunkPagedWs {
     int nblk;
 };
 
+// Backward with the rotary embedding: the rotary pre-pass's arrays (bf16:
+// rotated queries and keys, lifted and rotated distant keys, lifted values),
+// then the fp32 arrays of RopeBwdArgs; every part 256-byte aligned.
+struct RopeBwdWs {
+    size_t qr, kr, kd, vd, nl2, nd, dqr, dkr, dvw, dkd, dvd, wpart, bytes;
+    int nchunk;
+};
+
+RopeBwdWs rope_bwd_ws_layout(const dar_shape* s, int T) {
+    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    RopeBwdWs L{};
+    const size_t B = s->B, Hq = s->Hq, Hkv = s->Hkv, d = s->d, dd = s->d_down;
+    const size_t Td = T > s->w ? (size_t)(T - s->w) : 0;
+    const size_t Tr = (size_t)round_up(T, 64);
+    size_t off = 0;
+    auto put = [&](size_t& at, size_t bytes) { at = off; off += al(bytes); };
+    put(L.qr, B * Hq * T * d * 2);
+    put(L.kr, B * Hkv * T * d * 2);
+    put(L.kd, B * Hkv * Td * d * 2);
+    put(L.vd, B * Hkv * Td * d * 2);
+    put(L.nl2, B * Hq * Tr * 4);
+    put(L.nd, B * Hq * Tr * 4);
+    put(L.dqr, B * Hq * T * d * 4);
+    put(L.dkr, B * Hkv * T * d * 4);
+    put(L.dvw, B * Hkv * T * d * 4);
+    put(L.dkd, B * Hkv * Td * d * 4);
+    put(L.dvd, B * Hkv * Td * d * 4);
+    L.nchunk = (int)B * ((T + 31) / 32);  // one share per 32 keys of a sequence
+    put(L.wpart, 2 * Hkv * (size_t)L.nchunk * d * dd * 4);
+    L.bytes = off;
+    return L;
+}
+
 ChunkPagedWs chunk_paged_ws_layout(const dar_shape* s, int cap, int n) {
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     ChunkPagedWs L{};
@@ -294,6 +327,11 @@ size_t dar_prefill_chunk_rope_workspace_bytes(const dar_shape* s, int len, int n
     if (check_shape(s) != DAR_OK || len < 0 || n < 1) return 0;
     if ((long long)len + n > 0x7fffffffLL) return 0;
     return chunk_rope_ws_layout(s, len, n).bytes;
+}
+
+size_t dar_prefill_rope_backward_workspace_bytes(const dar_shape* s, int T) {
+    if (check_shape(s) != DAR_OK || T < 1) return 0;
+    return rope_bwd_ws_layout(s, T).bytes;
 }
 
 size_t dar_prefill_rope_workspace_bytes(const dar_shape* s, int T) {
@@ -988,6 +1026,78 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
         e = launch_decode_combine<bf16_t>((const float*)ws, (const bf16_t*)w_down,
                                           (const bf16_t*)w_up, (bf16_t*)o, s->B, s->Hq, s->Hkv,
                                           s->d, s->d_down, P, stream, nullptr, c->lens, counts);
+    return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+dar_status dar_attn_prefill_rope_backward(const dar_shape* s, int T, int pos0, const dar_rope* rope,
+                                          const void* q, const void* k, const void* v,
+                                          const void* w_down, const void* w_up, const void* o,
+                                          const float* lse, const void* dout, void* dq, void* dk,
+                                          void* dv, float* dw_down, float* dw_up, void* ws,
+                                          size_t ws_bytes, hipStream_t stream) {
+    dar_status st = check_shape(s);
+    if (st != DAR_OK) return st;
+    if (T < 1 || pos0 < 0 || !rope) return DAR_E_ARG;
+    const int r = rope->rotary_dim;
+    if (r < 0 || (r & 1) || r > s->d) return DAR_E_ARG;
+    if (r > 0 && !dev_ok(rope->table)) return DAR_E_ARG;
+    if ((long long)pos0 + T > (long long)rope->n_pos) return DAR_E_ARG;
+    if (!dev_ok(q) || !dev_ok(k) || !dev_ok(v) || !dev_ok(w_down) || !dev_ok(o) || !dev_ok(lse) ||
+        !dev_ok(dout) || !dev_ok(dq) || !dev_ok(dk) || !dev_ok(dv) || !dev_ok(dw_down))
+        return DAR_E_ARG;
+    if (w_up && !aligned16(w_up)) return DAR_E_ARG;
+    if ((w_up == nullptr) != (dw_up == nullptr)) return DAR_E_ARG;
+    if (dw_up && !aligned16(dw_up)) return DAR_E_ARG;
+    if (!bwd_rope_mfma_supported(s->d, s->d_down, s->dtype == DAR_BF16)) return DAR_E_UNSUPPORTED;
+    if ((long long)s->B * ((T + 31) / 32) > 65535) return DAR_E_UNSUPPORTED;
+    if ((long long)s->B * s->Hkv > 65535) return DAR_E_UNSUPPORTED;
+    const RopeBwdWs L = rope_bwd_ws_layout(s, T);
+    if (ws == nullptr || ws_bytes < L.bytes) return DAR_E_WORKSPACE;
+    if (!aligned16(ws)) return DAR_E_ARG;
+    clear_hip_error();
+    char* wsb = (char*)ws;
+    RopeBwdArgs a{};
+    a.q = (const bf16_t*)q;
+    a.k = (const bf16_t*)k;
+    a.v = (const bf16_t*)v;
+    a.o = (const bf16_t*)o;
+    a.dout = (const bf16_t*)dout;
+    a.wd = (const bf16_t*)w_down;
+    a.wu = (const bf16_t*)w_up;
+    a.lse = lse;
+    a.tab = rope->table;
+    a.qr = (const bf16_t*)(wsb + L.qr);
+    a.kr = (const bf16_t*)(wsb + L.kr);
+    a.kd = (const bf16_t*)(wsb + L.kd);
+    a.vd = (const bf16_t*)(wsb + L.vd);
+    a.nl2 = (float*)(wsb + L.nl2);
+    a.nd = (float*)(wsb + L.nd);
+    a.dqr = (float*)(wsb + L.dqr);
+    a.dkr = (float*)(wsb + L.dkr);
+    a.dvw = (float*)(wsb + L.dvw);
+    a.dkd = (float*)(wsb + L.dkd);
+    a.dvd = (float*)(wsb + L.dvd);
+    a.wpart = (float*)(wsb + L.wpart);
+    a.dq = (bf16_t*)dq;
+    a.dk = (bf16_t*)dk;
+    a.dv = (bf16_t*)dv;
+    a.dwd = dw_down;
+    a.dwu = dw_up;
+    a.L.nchunk = a.L.nchunk_d = a.L.nchunk_u = L.nchunk;
+    a.B = s->B;
+    a.Hq = s->Hq;
+    a.Hkv = s->Hkv;
+    a.T = T;
+    a.dd = s->d_down;
+    a.w = s->w;
+    a.r = r;
+    a.pos0 = pos0;
+    // the forward's rotated and lifted operands, recomputed (no norms needed)
+    hipError_t e = launch_rope_prepass<bf16_t>(a.q, a.k, a.v, a.wd, a.wu, rope->table,
+                                               (bf16_t*)a.qr, (bf16_t*)a.kr, (bf16_t*)a.kd,
+                                               (bf16_t*)a.vd, nullptr, nullptr, s->B, s->Hq,
+                                               s->Hkv, T, s->d, s->d_down, s->w, r, pos0, stream);
+    if (e == hipSuccess) e = launch_bwd_rope_mfma(a, s->d, stream);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 

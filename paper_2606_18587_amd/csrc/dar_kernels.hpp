@@ -239,6 +239,28 @@ hipError_t launch_bwd_valu(const T* q, const T* k, const T* v, const T* o, const
                            float* dwd, float* dwu, char* ws, const BwdWs& L, int B, int Hq,
                            int Hkv, int T_, int d, int dd, int w, hipStream_t st);
 
+// Backward of the prefill with the rotary embedding (backward_mfma.hip;
+// bf16, d in {64, 128}, any d_down). Inputs: q, k, v, o, dout, wd, wu (NULL:
+// tied), lse (the forward's, natural log), tab [n_pos][r]; qr, kr, kd, vd:
+// the rotary pre-pass of the same inputs (rotated queries and keys, lifted
+// and rotated distant keys and lifted values of positions < T - w).
+// Workspace arrays (fp32): nl2, nd [B*Hq][Tr] (Tr = round_up(T, 64)); dqr
+// [B*Hq][T][d]; dkr, dvw [B*Hkv][T][d]; dkd, dvd [B*Hkv][T - w][d]; wpart
+// [2][Hkv][L.nchunk][d][dd] with L.nchunk = B * ceil(T / 32).
+struct RopeBwdArgs {
+    const bf16_t *q, *k, *v, *o, *dout, *wd, *wu;
+    const float* lse;
+    const float* tab;
+    const bf16_t *qr, *kr, *kd, *vd;
+    float *nl2, *nd, *dqr, *dkr, *dvw, *dkd, *dvd, *wpart;
+    bf16_t *dq, *dk, *dv;
+    float *dwd, *dwu;
+    BwdWs L;
+    int B, Hq, Hkv, T, dd, w, r, pos0;
+};
+bool bwd_rope_mfma_supported(int d, int dd, bool bf16);
+hipError_t launch_bwd_rope_mfma(const RopeBwdArgs& a, int d, hipStream_t st);
+
 // Rotary embedding inside Eq. 3 (rope.hip): the angle table [n_pos][r] (cos
 // of the r/2 angles of a position, then their sin; fp32 from fp64), the
 // prefill pre-pass (rotated queries and keys; lifted, rotated distant keys

@@ -35,6 +35,7 @@ def test_exports_every_declared_symbol():
                           "dar_attn_prefill_chunk", "dar_prefill_chunk_workspace_bytes",
                           "dar_attn_prefill_chunk_rope", "dar_prefill_chunk_rope_workspace_bytes",
                           "dar_attn_prefill_chunk_paged", "dar_prefill_chunk_paged_workspace_bytes",
+                          "dar_attn_prefill_rope_backward", "dar_prefill_rope_backward_workspace_bytes",
                           "dar_rope_table", "dar_attn_prefill_rope", "dar_attn_decode_rope",
                           "dar_attn_prefill_shared", "dar_cache_append_shared",
                           "dar_attn_decode_shared", "dar_cache_append_paged",
@@ -550,6 +551,48 @@ def test_chunk_paged_rejects_before_any_launch():
     assert call(shape=S(dtype=torch.float32)) == dar.DAR_E_UNSUPPORTED   # matrix-core shapes only
     assert call(shape=S(d=64, dd=8)) == dar.DAR_E_UNSUPPORTED
     assert call(shape=S(Hq=3)) == dar.DAR_E_ARG
+
+
+def test_rope_backward_workspace_size():
+    """Rotated queries and keys, lifted distant keys and values (bf16), two
+    row constants, the fp32 row, window-key and distant-key gradients and the
+    weight-gradient shares (one per 32 keys of a sequence)."""
+    al = lambda x: (x + 255) // 256 * 256
+    for (B, Hq, Hkv, d, dd, w), T in [((2, 4, 2, 64, 16, 32), 300), ((1, 8, 2, 128, 32, 500), 400)]:
+        s = dar.make_shape(B, Hq, Hkv, d, dd, w, torch.bfloat16)
+        Td = max(T - w, 0)
+        Tr = (T + 63) // 64 * 64
+        nchunk = B * ((T + 31) // 32)
+        want = (al(B * Hq * T * d * 2) + al(B * Hkv * T * d * 2) + 2 * al(B * Hkv * Td * d * 2)
+                + 2 * al(B * Hq * Tr * 4) + al(B * Hq * T * d * 4) + 2 * al(B * Hkv * T * d * 4)
+                + 2 * al(B * Hkv * Td * d * 4) + al(2 * Hkv * nchunk * d * dd * 4))
+        assert dar.dar_prefill_rope_backward_workspace_bytes(s, T) == want
+    assert dar.dar_prefill_rope_backward_workspace_bytes(S(), 0) == 0
+    assert dar.dar_prefill_rope_backward_workspace_bytes(S(Hq=3), 10) == 0
+
+
+@no_gpu
+def test_rope_backward_rejects_before_any_launch():
+    rs = dar.DarRopeStruct(16, 64, FAKE.value)
+    def call(shape=None, T=32, pos0=0, rope=rs, q=FAKE, wu=None, dwu=None, lse=FAKE,
+             ws_bytes=1 << 30):
+        shape = shape or S()
+        return dar.lib.dar_attn_prefill_rope_backward(
+            ctypes.byref(shape), T, pos0, ctypes.byref(rope) if rope is not None else None, q, FAKE,
+            FAKE, FAKE, wu, FAKE, lse, FAKE, FAKE, FAKE, FAKE, FAKE, dwu, FAKE, ws_bytes, None)
+    assert call(T=0) == dar.DAR_E_ARG
+    assert call(pos0=-1) == dar.DAR_E_ARG
+    assert call(pos0=40) == dar.DAR_E_ARG                          # pos0 + T past the table
+    assert call(rope=dar.DarRopeStruct(15, 64, FAKE.value)) == dar.DAR_E_ARG   # odd rotary dim
+    assert call(rope=dar.DarRopeStruct(80, 64, FAKE.value)) == dar.DAR_E_ARG   # r > d
+    assert call(q=None) == dar.DAR_E_ARG
+    assert call(lse=MISALIGNED) == dar.DAR_E_ARG
+    assert call(wu=FAKE) == dar.DAR_E_ARG                          # untied needs dw_up
+    assert call(dwu=FAKE) == dar.DAR_E_ARG                         # tied takes no dw_up
+    assert call(ws_bytes=64) == dar.DAR_E_WORKSPACE
+    assert call(shape=S(dtype=torch.float32)) == dar.DAR_E_UNSUPPORTED
+    assert call(shape=S(d=80, dd=16)) == dar.DAR_E_UNSUPPORTED
+    assert call(shape=S(d=128, dd=96)) == dar.DAR_E_UNSUPPORTED
 
 
 @no_gpu
