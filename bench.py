@@ -380,6 +380,14 @@ def main():
             run_pd(i)
         paged["ragged_ms"] = timed(run_pd, args.steps)
         paged["ragged_lens"] = [int(x) for x in lens_r.tolist()]
+        if not args.no_rope:
+            # the same ragged batch with the rotary embedding of Eq. 3
+            rpg = dar.Rope(ROPE_DECODE_DIM, ROPE_BASE, n_pos=pcache.cap, device=dev)
+            run_pr = lambda i: dar.dar_attn_decode_paged_rope(pcache, qd_last, dwd, rpg, o=dout,
+                                                              ws=dws)
+            for i in range(args.warmup):
+                run_pr(i)
+            paged["ragged_rope_ms"] = timed(run_pr, args.steps)
         # skewed: one sequence at full length, the others at 600 tokens
         lens_s = [L] + [600] * (dw.B - 1)
         pcache.lens.copy_(torch.tensor(lens_s, dtype=torch.int32))
@@ -635,6 +643,11 @@ def main():
                      % (min(paged["ragged_lens"]), max(paged["ragged_lens"])),
             "us": round(rlu, 2), "alg_bytes": rb, "gbs": round(rb / (rlu * 1e-6) / 1e9, 1),
             "frac_hbm_peak": round(rb / (rlu * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}
+        if "ragged_rope_ms" in paged:
+            rru = float(paged["ragged_rope_ms"] * 1e3)
+            result["decode_ragged"]["rope_us"] = round(rru, 2)
+            result["decode_ragged"]["rope_frac_hbm_peak"] = round(
+                rb / (rru * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)
         sku = float(paged["skewed_ms"] * 1e3)
         sb = sum(decode_bytes(1, dw.Hq, dw.Hkv, dw.d, dw.dd, dw.w, n) for n in paged["skewed_lens"])
         result["decode_skewed"] = {

@@ -312,6 +312,20 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
                                  const void* w_down, const void* w_up, void* o, void* ws,
                                  size_t ws_bytes, hipStream_t stream);
 
+/* dar_attn_decode_paged with the rotary embedding of Eq. 3, applied as
+ * dar_attn_decode_rope applies it (query of sequence b at position
+ * lens[b] - 1, cache token e at position e). rope->n_pos must be at least
+ * the capacity max_blocks * page_size (every position a sequence can reach
+ * indexes the table), else DAR_E_ARG; rope NULL, an odd rotary_dim or one
+ * above d: DAR_E_ARG. Supported: the shapes of dar_attn_decode_paged with
+ * rotary_dim 16, 32 or 64 (0: no rotation, the table is not read); others
+ * return DAR_E_UNSUPPORTED. Workspace, output and empty or overflowed
+ * sequences as for dar_attn_decode_paged. */
+dar_status dar_attn_decode_paged_rope(const dar_shape* s, const dar_paged_cache* c,
+                                      const dar_rope* rope, const void* q, const void* w_down,
+                                      const void* w_up, void* o, void* ws, size_t ws_bytes,
+                                      hipStream_t stream);
+
 /* Chunked prefill over a paged cache (serving: several sequences of different
  * lengths taking their next prompt tokens in one call). Sequence b takes
  * n_b = n_new[b] new tokens (n_new: device int [B], each clamped to [0, n];

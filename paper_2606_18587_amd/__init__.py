@@ -99,6 +99,8 @@ def _load():
     lib.dar_cache_append_paged.argtypes = [shp, pcp, vp, vp, vp, vp]
     lib.dar_attn_decode_paged.restype = ci
     lib.dar_attn_decode_paged.argtypes = [shp, pcp] + [vp] * 5 + [sz, vp]
+    lib.dar_attn_decode_paged_rope.restype = ci
+    lib.dar_attn_decode_paged_rope.argtypes = [shp, pcp, rp] + [vp] * 5 + [sz, vp]
     lib.dar_attn_prefill_chunk_paged.restype = ci
     lib.dar_attn_prefill_chunk_paged.argtypes = [shp, pcp, ci] + [vp] * 9 + [sz, vp]
     lib.dar_prefill_chunk_paged_workspace_bytes.restype = sz
@@ -669,6 +671,27 @@ def dar_attn_decode_paged(cache: DarPagedCache, q, w_down, w_up=None, o=None, ws
                                    _stream(stream))
     if st != DAR_OK:
         raise DarError(st, "dar_attn_decode_paged")
+    return o
+
+
+def dar_attn_decode_paged_rope(cache: DarPagedCache, q, w_down, rope: "Rope", w_up=None, o=None,
+                               ws=None, stream=None):
+    """dar_attn_decode_paged with the rotary embedding of Eq. 3 (query of
+    sequence b at position lens[b] - 1; rope.n_pos >= the cache capacity)."""
+    B, Hq, d = q.shape
+    shape = make_shape(B, Hq, cache.Hkv, d, cache.d_down, cache.w, q.dtype)
+    if o is None:
+        o = torch.empty_like(q)
+    if ws is None:
+        ws = _workspace(dar_decode_workspace_bytes(shape, cache.cap), q.device)
+    cs = cache.struct()
+    rs = rope.struct()
+    st = lib.dar_attn_decode_paged_rope(ctypes.byref(shape), ctypes.byref(cs), ctypes.byref(rs),
+                                        _ptr(q), _ptr(w_down), _ptr(w_up), _ptr(o), _ptr(ws),
+                                        0 if ws is None else ws.numel() * ws.element_size(),
+                                        _stream(stream))
+    if st != DAR_OK:
+        raise DarError(st, "dar_attn_decode_paged_rope")
     return o
 
 

@@ -993,9 +993,14 @@ dar_status dar_cache_append_paged(const dar_shape* s, const dar_paged_cache* c, 
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
 }
 
-dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, const void* q,
-                                 const void* w_down, const void* w_up, void* o, void* ws,
-                                 size_t ws_bytes, hipStream_t stream) {
+}  // extern "C"
+
+namespace {
+
+// The paged decode, without (rope NULL) or with the rotary embedding.
+dar_status decode_paged(const dar_shape* s, const dar_paged_cache* c, const dar_rope* rope,
+                        const void* q, const void* w_down, const void* w_up, void* o, void* ws,
+                        size_t ws_bytes, hipStream_t stream) {
     dar_status st = check_shape(s);
     if (st != DAR_OK) return st;
     st = check_paged(s, c);
@@ -1006,6 +1011,17 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
         !group_supported(s))
         return DAR_E_UNSUPPORTED;
     const int cap = c->page_size * c->max_blocks;
+    int r = 0;
+    if (rope) {
+        r = rope->rotary_dim;
+        if (r < 0 || (r & 1) || r > s->d) return DAR_E_ARG;
+        if (r > 0 && !dev_ok(rope->table)) return DAR_E_ARG;
+        // every position a sequence can reach indexes the table
+        if (rope->n_pos < cap) return DAR_E_ARG;
+        if (r > 0 &&
+            !decode_mfma_rope_supported(s->d, s->d_down, s->Hq / s->Hkv, r, s->dtype == DAR_BF16))
+            return DAR_E_UNSUPPORTED;
+    }
     const size_t need = dar_decode_workspace_bytes(s, cap);
     if (ws == nullptr || ws_bytes < need) return DAR_E_WORKSPACE;
     if (!aligned16(ws)) return DAR_E_ARG;
@@ -1019,7 +1035,8 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
                                             (const bf16_t*)c->v_win, (const bf16_t*)c->k_pool,
                                             (const bf16_t*)c->v_pool, pg, (float*)ws, (bf16_t*)o,
                                             s->B, s->Hq, s->Hkv, s->d, s->d_down, s->w, P, counts,
-                                            stream);
+                                            stream, r > 0 ? rope->table : nullptr,
+                                            r > 0 ? rope->n_pos : 0, r);
     // the pairs split over several workgroups, and the empty or overflowed
     // sequences (NaN rows)
     if (e == hipSuccess)
@@ -1027,6 +1044,24 @@ dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, c
                                           (const bf16_t*)w_up, (bf16_t*)o, s->B, s->Hq, s->Hkv,
                                           s->d, s->d_down, P, stream, nullptr, c->lens, counts);
     return e == hipSuccess ? DAR_OK : DAR_E_HIP;
+}
+
+}  // namespace
+
+extern "C" {
+
+dar_status dar_attn_decode_paged(const dar_shape* s, const dar_paged_cache* c, const void* q,
+                                 const void* w_down, const void* w_up, void* o, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+    return decode_paged(s, c, nullptr, q, w_down, w_up, o, ws, ws_bytes, stream);
+}
+
+dar_status dar_attn_decode_paged_rope(const dar_shape* s, const dar_paged_cache* c,
+                                      const dar_rope* rope, const void* q, const void* w_down,
+                                      const void* w_up, void* o, void* ws, size_t ws_bytes,
+                                      hipStream_t stream) {
+    if (!rope) return DAR_E_ARG;
+    return decode_paged(s, c, rope, q, w_down, w_up, o, ws, ws_bytes, stream);
 }
 
 dar_status dar_attn_prefill_rope_backward(const dar_shape* s, int T, int pos0, const dar_rope* rope,

@@ -159,11 +159,14 @@ hipError_t launch_decode_mfma_rope(const bf16_t* q, const bf16_t* wd, const bf16
 // partial record per piece (P records per head at most) and their piece
 // count in pg.counts, and launch_decode_combine (with lens and counts)
 // finishes them. part: P * B * Hq records, then B * Hkv ints (counts).
+// With tab (rotary dimension r in {16, 32, 64}, n_pos at least the capacity):
+// the rotary embedding of Eq. 3 as launch_decode_mfma_rope applies it.
 hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf16_t* wu,
                                     const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_pool,
                                     const bf16_t* v_pool, const PagedArgs& pg, float* part,
                                     bf16_t* o, int B, int Hq, int Hkv, int d, int dd, int w, int& P,
-                                    int*& counts, hipStream_t st);
+                                    int*& counts, hipStream_t st, const float* tab = nullptr,
+                                    int n_pos = 0, int r = 0);
 // Partial records per head of a paged decode (bound over all length mixes).
 int decode_paged_slots(int Hkv, int cap, int w, int d, int dd);
 // One token per sequence into a paged cache at position lens[b]; the token

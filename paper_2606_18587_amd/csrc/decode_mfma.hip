@@ -1160,7 +1160,7 @@ hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf1
                                     const bf16_t* k_win, const bf16_t* v_win, const bf16_t* k_pool,
                                     const bf16_t* v_pool, const PagedArgs& pg_in, float* part,
                                     bf16_t* o, int B, int Hq, int Hkv, int d, int dd, int w, int& P,
-                                    int*& counts, hipStream_t st) {
+                                    int*& counts, hipStream_t st, const float* tab, int n_pos, int r) {
     const int cap = pg_in.maxb * pg_in.ps;
     P = decode_paged_slots(Hkv, cap, w, d, dd);
     counts = reinterpret_cast<int*>(part + (size_t)B * Hq * P * (2 + dd + d));
@@ -1171,15 +1171,21 @@ hipError_t launch_decode_mfma_paged(const bf16_t* q, const bf16_t* wd, const bf1
     // jobs: at most kPagedGroups full parts (cu >= total / kPagedGroups) and
     // one last part per pair
     dim3 grid(kPagedGroups + B * Hkv);
-#define DAR_DEC_PAGED(D_, DD_)                                                                       \
-    hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value, 0, true>), grid,            \
+#define DAR_DEC_PAGED(D_, DD_, R_)                                                                   \
+    hipLaunchKernelGGL((decode_mfma_kernel<D_, DD_, DecWaves<D_>::value, R_, true>), grid,           \
                        dim3(64 * DecWaves<D_>::value), 0, st, q, wd, wu, k_win, v_win, k_pool, v_pool, \
-                       part, o, Hq, Hkv, w, cap, 0, P, qscale, (const float*)nullptr, 0,              \
+                       part, o, Hq, Hkv, w, cap, 0, P, qscale, tab, n_pos,                            \
                        (const bf16_t*)nullptr, pg, pg.bt)
-    if (d == 64 && dd == 16) DAR_DEC_PAGED(64, 16);
-    else if (d == 64 && dd == 32) DAR_DEC_PAGED(64, 32);
-    else if (d == 128 && dd == 16) DAR_DEC_PAGED(128, 16);
-    else DAR_DEC_PAGED(128, 32);
+#define DAR_DEC_PAGED_R(D_, DD_)                          \
+    if (r == 0) DAR_DEC_PAGED(D_, DD_, 0);                \
+    else if (r == 16) DAR_DEC_PAGED(D_, DD_, 16);         \
+    else if (r == 32) DAR_DEC_PAGED(D_, DD_, 32);         \
+    else DAR_DEC_PAGED(D_, DD_, 64);
+    if (d == 64 && dd == 16) { DAR_DEC_PAGED_R(64, 16) }
+    else if (d == 64 && dd == 32) { DAR_DEC_PAGED_R(64, 32) }
+    else if (d == 128 && dd == 16) { DAR_DEC_PAGED_R(128, 16) }
+    else { DAR_DEC_PAGED_R(128, 32) }
+#undef DAR_DEC_PAGED_R
 #undef DAR_DEC_PAGED
     return hipGetLastError();
 }

@@ -39,7 +39,8 @@ def test_exports_every_declared_symbol():
                           "dar_rope_table", "dar_attn_prefill_rope", "dar_attn_decode_rope",
                           "dar_attn_prefill_shared", "dar_cache_append_shared",
                           "dar_attn_decode_shared", "dar_cache_append_paged",
-                          "dar_attn_decode_paged", "dar_attn_prefill_ragged",
+                          "dar_attn_decode_paged", "dar_attn_decode_paged_rope",
+                          "dar_attn_prefill_ragged",
                           "dar_prefill_rope_workspace_bytes", "dar_status_string",
                           "dar_attn_decode_noalloc", "dar_decode_noalloc_bytes",
                           "dar_decode_noalloc_max_bytes"}
@@ -510,6 +511,28 @@ def test_paged_rejects_before_any_launch():
     assert dc(pc(), ws_bytes=8) == dar.DAR_E_WORKSPACE
     assert dc(pc(), shape=S(dtype=torch.float32)) == dar.DAR_E_UNSUPPORTED   # matrix-core shapes only
     assert dc(pc(), shape=S(d=80, dd=16)) == dar.DAR_E_UNSUPPORTED
+
+
+@no_gpu
+def test_paged_rope_rejects_before_any_launch():
+    """Capacity 4 pages of 64 = 256 positions."""
+    c = dar.DarPagedCacheStruct(FAKE.value, FAKE.value, FAKE.value, FAKE.value, FAKE.value,
+                                FAKE.value, 64, 4, 8)
+    def call(r=64, n_pos=256, table=FAKE, shape=None, null_rope=False, ws_bytes=1 << 30):
+        rs = dar.DarRopeStruct(r, n_pos, table)
+        return dar.lib.dar_attn_decode_paged_rope(ctypes.byref(shape or S()), ctypes.byref(c),
+                                                  None if null_rope else ctypes.byref(rs), FAKE,
+                                                  FAKE, None, FAKE, FAKE, ws_bytes, None)
+    assert call(null_rope=True) == dar.DAR_E_ARG
+    assert call(n_pos=255) == dar.DAR_E_ARG        # a reachable position past the table
+    assert call(r=5) == dar.DAR_E_ARG
+    assert call(r=-2) == dar.DAR_E_ARG
+    assert call(r=66) == dar.DAR_E_ARG             # above d
+    assert call(table=None) == dar.DAR_E_ARG
+    assert call(r=24) == dar.DAR_E_UNSUPPORTED
+    assert call(shape=S(d=128, dd=48)) == dar.DAR_E_UNSUPPORTED
+    assert call(ws_bytes=8) == dar.DAR_E_WORKSPACE
+    assert call(r=0, table=None, ws_bytes=8) == dar.DAR_E_WORKSPACE   # r = 0 reads no table
 
 
 def test_chunk_paged_workspace_size():

@@ -1,12 +1,15 @@
 """GPU parity of the paged split cache with one length per sequence
-(dar_cache_append_paged, dar_attn_decode_paged through the C ABI).
+(dar_cache_append_paged, dar_attn_decode_paged and its rotary variant
+dar_attn_decode_paged_rope through the C ABI).
 
 Sequences of different lengths share one batch; their latents live in pages
 handed out through a shuffled block table. Each sequence's decode is checked
 against the oracle's row at its own position len_b - 1 over its own
 full-dimension history (Eq. 3-4, tolerance 2e-2 for bf16), and the pages and
 rings written by the paged append are checked byte for byte against a dense
-cache that dar_cache_append fills with the same tokens.
+cache that dar_cache_append fills with the same tokens. The rotary decode
+is checked against the oracle's rotary row (Eq. 3 with RoPE: query at
+position len_b - 1, token e at position e).
 """
 import numpy as np
 import pytest
@@ -89,13 +92,17 @@ class Ragged:
         v = torch.stack([self.vdev[b][:, self.lens[b] + t] for b in range(self.B)])
         return k.contiguous(), v.contiguous()
 
-    def check_decode(self, t, heads_per_seq=None, seed=0):
+    def check_decode(self, t, heads_per_seq=None, seed=0, rope=None, wu=None):
         """Decode a fresh query per sequence at its current length; compare
-        with the oracle row."""
+        with the oracle row (with rope: the rotary decode against the
+        oracle's rotary row, query at position len - 1, token e at e)."""
         wl = self.wl
         g = np.random.Generator(np.random.PCG64(700 + t + seed))
         q = di.Tensor(g.standard_normal((self.B, wl.Hq, wl.d), dtype=np.float32), "bf16")
-        o = dar.dar_attn_decode_paged(self.pc, to_dev(q), self.wdd)
+        if rope is None:
+            o = dar.dar_attn_decode_paged(self.pc, to_dev(q), self.wdd, w_up=to_dev(wu))
+        else:
+            o = dar.dar_attn_decode_paged_rope(self.pc, to_dev(q), self.wdd, rope, w_up=to_dev(wu))
         torch.cuda.synchronize()
         got = to_host64(o)
         grp = wl.Hq // wl.Hkv
@@ -109,8 +116,13 @@ class Ragged:
             heads = range(wl.Hq) if heads_per_seq is None else heads_per_seq
             for h in heads:
                 gg = h // grp
-                ref = oracle.rows(self.k[b].f64_slice(gg)[:L], self.v[b].f64_slice(gg)[:L], self.wd.f64[gg], None,
-                                  wl.w, [L - 1], q.f64[b, h][None])
+                K, V = self.k[b].f64_slice(gg)[:L], self.v[b].f64_slice(gg)[:L]
+                wug = None if wu is None else wu.f64[gg]
+                if rope is None:
+                    ref = oracle.rows(K, V, self.wd.f64[gg], wug, wl.w, [L - 1], q.f64[b, h][None])
+                else:
+                    ref = oracle.rows_rope(K, V, self.wd.f64[gg], wug, wl.w, rope.rotary_dim,
+                                           rope.base, 0, [L - 1], q.f64[b, h][None])
                 worst = max(worst, float(np.abs(got[b, h] - ref[0]).max()))
         assert worst <= tol("bf16"), worst
         return worst
@@ -246,3 +258,102 @@ def test_full_size_ragged_decode1b():
     r.check_decode(0, heads_per_seq=[0, 17, 31])
     r.append_step(0)
     r.check_decode(1, heads_per_seq=[4])
+
+
+# ------------------------------------------------------------ rotary decode
+
+
+def untied_wu(wl, seed=73):
+    g = np.random.Generator(np.random.PCG64(seed))
+    return di.Tensor(g.standard_normal((wl.Hkv, wl.dd, wl.d), dtype=np.float32) / np.sqrt(wl.dd),
+                     "bf16")
+
+
+@pytest.mark.parametrize("w,ps,r,untied", [(32, 64, 64, False), (0, 32, 16, True),
+                                           (1, 256, 32, False), (600, 64, 16, False),
+                                           (100, 32, 64, True)])
+def test_rope_ragged_decode_and_append(w, ps, r, untied):
+    """Ragged lengths (an empty sequence included): the rotary decode of
+    every head of every sequence, appends in between."""
+    wl = WL.with_(w=w)
+    rg = Ragged(wl, [1, 37, 300, 0, 64, 511, 129], ps)
+    rope = dar.Rope(r, 10000.0, n_pos=rg.pc.cap)
+    wu = untied_wu(wl) if untied else None
+    for t in range(2):
+        rg.check_decode(t, rope=rope, wu=wu)
+        rg.append_step(t)
+    rg.check_decode(2, rope=rope, wu=wu)
+
+
+@pytest.mark.parametrize("d,dd,G,r,untied", [(64, 32, 4, 32, False), (128, 16, 2, 16, True),
+                                             (128, 32, 8, 64, False), (64, 16, 1, 64, True),
+                                             (128, 32, 4, 32, True)])
+def test_rope_other_shapes(d, dd, G, r, untied):
+    wl = WL.with_(d=d, dd=dd, Hq=2 * G, Hkv=2, w=48)
+    rg = Ragged(wl, [5, 200, 97, 0], 64)
+    rope = dar.Rope(r, 500000.0, n_pos=rg.pc.cap + 7)
+    wu = untied_wu(wl) if untied else None
+    rg.check_decode(0, rope=rope, wu=wu)
+    rg.append_step(0)
+    rg.check_decode(1, rope=rope, wu=wu)
+
+
+@pytest.mark.parametrize("d,dd,w,Hq,Hkv,lens,r", [
+    (64, 16, 600, 8, 2, [30000, 1, 2, 0, 33, 700, 64, 100], 64),
+    (128, 32, 256, 8, 1, [1, 300, 6000], 32),
+    (64, 32, 48, 8, 2, [12000] + [3] * 20, 16),
+])
+def test_rope_mixed_lengths_split_pairs(d, dd, w, Hq, Hkv, lens, r):
+    """A long sequence beside tiny and empty ones: its pairs are cut into
+    many pieces whose records the combine merges (rotated distant keys in
+    every piece at their own positions)."""
+    rg = Ragged(WL.with_(d=d, dd=dd, w=w, Hq=Hq, Hkv=Hkv), lens, 64, steps=1)
+    rope = dar.Rope(r, 10000.0 if d == 64 else 500000.0, n_pos=rg.pc.cap)
+    rg.check_decode(0, rope=rope)
+    rg.append_step(0)
+    rg.check_decode(1, rope=rope)
+
+
+def test_rope_zero_dim_equals_plain_paged_decode():
+    """rotary_dim 0 rotates nothing: the output equals dar_attn_decode_paged's
+    bit for bit."""
+    rg = Ragged(WL.with_(w=64), [900, 1, 0, 333], 64, steps=1)
+    g = np.random.Generator(np.random.PCG64(74))
+    q = to_dev(di.Tensor(g.standard_normal((4, WL.Hq, WL.d), dtype=np.float32), "bf16"))
+    a = dar.dar_attn_decode_paged(rg.pc, q, rg.wdd)
+    b = dar.dar_attn_decode_paged_rope(rg.pc, q, rg.wdd, dar.Rope(0, 10000.0, n_pos=rg.pc.cap))
+    torch.cuda.synchronize()
+    assert np.array_equal(raw(a), raw(b))
+
+
+def test_rope_overflowed_sequence_decodes_to_nan():
+    """A sequence marked overflowed (lens = -1 - cap) decodes to NaN; the
+    other one is served (oracle's rotary row)."""
+    wl = WL.with_(w=16)
+    rg = Ragged(wl, [64, 10], 32, extra_blocks=0, steps=1)
+    cap = rg.pc.cap
+    rg.pc.lens[0] = -1 - cap
+    g = np.random.Generator(np.random.PCG64(75))
+    q = di.Tensor(g.standard_normal((2, wl.Hq, wl.d), dtype=np.float32), "bf16")
+    rope = dar.Rope(32, 10000.0, n_pos=cap)
+    o = to_host64(dar.dar_attn_decode_paged_rope(rg.pc, to_dev(q), rg.wdd, rope))
+    assert np.isnan(o[0]).all()
+    grp = wl.Hq // wl.Hkv
+    for h in range(wl.Hq):
+        gg = h // grp
+        ref = oracle.rows_rope(rg.k[1].f64_slice(gg)[:10], rg.v[1].f64_slice(gg)[:10], rg.wd.f64[gg],
+                               None, wl.w, 32, 10000.0, 0, [9], q.f64[1, h][None])
+        assert np.abs(o[1, h] - ref[0]).max() <= tol("bf16")
+
+
+def test_rope_full_size_ragged_decode1b():
+    """decode1b shape (B32 Hq32 Hkv8 d64 d_down16 w512) with rotary dimension
+    64, lengths spread from 1 to 32768 tokens, 256-token pages: sampled heads
+    of every sequence."""
+    wl = di.WORKLOADS["decode1b"]
+    lens = [1, 2, 511, 512, 513] + [int(x) for x in np.linspace(1000, 32768, 27)]
+    rg = Ragged(wl, lens, 256, steps=1)
+    rope = dar.Rope(64, 10000.0, n_pos=rg.pc.cap)
+    rg.check_decode(0, heads_per_seq=[0, 17, 31], rope=rope)
+    rg.append_step(0)
+    rg.check_decode(1, heads_per_seq=[4], rope=rope)
