@@ -61,13 +61,13 @@ CSRC = os.path.join(ROOT, "paper_2606_18587_amd", "csrc")
 MEASURED_TRAFFIC = {
     "prefill": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "latent.hip",
                           "prefill_mfma.hip"],
-                "sha256_16": "170286f29f8a7ffd", "bytes": 127277157},
+                "sha256_16": "578449016aaf2c68", "bytes": 127000207},
     "decode": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "decode.hip",
                          "decode_mfma.hip"],
-               "sha256_16": "7db38f5345015c01", "bytes": 574107720},
+               "sha256_16": "8a604b13abc871ce", "bytes": 563577444},
     "backward": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "mfma_common.hpp",
                            "backward.hip", "backward_mfma.hip"],
-                 "sha256_16": "0bf8920815de0383", "bytes": 500611717},
+                 "sha256_16": "53046b06b7e0dea5", "bytes": 509064844},
 }
 
 
