@@ -337,13 +337,16 @@ __device__ __forceinline__ void distant_region(const RowCtx& c, const bf16_t* __
         f32x16_t x = mfma(kt.k[0], qtop[0], st.cmv);
 #pragma unroll
         for (int s = 1; s < DS; ++s) x = mfma(kt.k[s], qtop[s], x);
+        return x;
+    };
+    // staircase subtile: keep j <= i - w
+    auto mask = [&](f32x16_t& x, int sub) {
         const int js = sub * 32;
-        if (js + 31 > c.r0 - c.w) {  // staircase subtile: keep j <= i - w
+        if (js + 31 > c.r0 - c.w) {
 #pragma unroll
             for (int r = 0; r < 16; ++r)
                 if (js + acc_key(r, c.hg) > c.i - c.w) x[r] = -INFINITY;
         }
-        return x;
     };
     auto finish = [&](f32x16_t& x, const VT& vt, f32x16_t* xnext) {
         bf16x8_t p0, p1;
@@ -352,35 +355,65 @@ __device__ __forceinline__ void distant_region(const RowCtx& c, const bf16_t* __
         ol = mfma(vt.v[0], p0, ol);
         ol = mfma(vt.v[1], p1, ol);
     };
+    // Subtiles [0, n_full) need no mask for any row of the wavefront; the
+    // pipelined loop finishes only those, so it carries no lane-dependent
+    // mask state (at the register limit such state was spilled, and its
+    // reload before the loop made every iteration wait for nearly all of
+    // the loads in flight). At most two staircase subtiles remain.
+    const int n_full = imin(n_sub, imax(0, (c.r0 - c.w + 1) >> 5));
     KT ka = loadK(0), kb = loadK(1), kc = loadK(2);
     VT va = loadV(0), vb = loadV(1), vc = loadV(2);
     f32x16_t x = scores(0, ka);
     ka = loadK(3);
     int n = 0;
-    for (; n + 2 < n_sub; n += 3) {
+    // (scheduling fences keep each load where it is written: left free, the
+    // scheduler sank all of an iteration's loads to its end, right before
+    // the next iteration waits for them)
+    for (; n + 2 < n_full; n += 3) {
         // x = scores of n; kb, kc, ka hold keys n+1..n+3; va, vb, vc values n..n+2
         f32x16_t xn = scores(n + 1, kb);
         kb = loadK(n + 4);
+        __builtin_amdgcn_sched_barrier(0);
         finish(x, va, &xn);
         va = loadV(n + 3);
+        __builtin_amdgcn_sched_barrier(0);
         x = xn;
         xn = scores(n + 2, kc);
         kc = loadK(n + 5);
+        __builtin_amdgcn_sched_barrier(0);
         finish(x, vb, &xn);
         vb = loadV(n + 4);
+        __builtin_amdgcn_sched_barrier(0);
         x = xn;
         xn = scores(n + 3, ka);
         ka = loadK(n + 6);
+        __builtin_amdgcn_sched_barrier(0);
         finish(x, vc, &xn);
         vc = loadV(n + 5);
+        __builtin_amdgcn_sched_barrier(0);
         x = xn;
     }
-    if (n + 1 < n_sub) {
-        f32x16_t xn = scores(n + 1, kb);
-        finish(x, va, &xn);
-        finish(xn, vb, nullptr);
-    } else if (n < n_sub) {
+    // the rest, at most four subtiles, one at a time (keys n..n+3 and values
+    // n..n+2 are in flight; x holds the scores of n)
+    if (n < n_sub) {
+        mask(x, n);
         finish(x, va, nullptr);
+    }
+    if (n + 1 < n_sub) {
+        f32x16_t y = scores(n + 1, kb);
+        mask(y, n + 1);
+        finish(y, vb, nullptr);
+    }
+    if (n + 2 < n_sub) {
+        f32x16_t y = scores(n + 2, kc);
+        mask(y, n + 2);
+        finish(y, vc, nullptr);
+    }
+    if (n + 3 < n_sub) {
+        const VT vd = loadV(n + 3);
+        f32x16_t y = scores(n + 3, ka);
+        mask(y, n + 3);
+        finish(y, vd, nullptr);
     }
 }
 
