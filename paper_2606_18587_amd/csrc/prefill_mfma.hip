@@ -531,8 +531,13 @@ __device__ __forceinline__ void distant_region_cache(const RowCtx& c, const LatC
     }
 }
 
-// Local region with one tile of prefetch (d = 128, where a second register
-// set does not fit): 64-key K/V tiles staged through LDS for the workgroup. The
+// Local region at d = 128 (where a register set for the next tile does not
+// fit): 64-key K/V tiles loaded straight from global memory into LDS
+// (global_load_lds, no registers), the next tile's loads in flight while
+// the current one is computed on. One wavefront instruction fills 1 KB of
+// LDS, lane l at byte 16 l: the padded tile (rows of d + 8 elements, 17
+// chunks of 16 bytes) is 17 such instructions per array, and a lane whose
+// chunk is a row's pad loads a chunk of that row again (never read). The
 // query operand is the unscaled bf16 query (scaling it in bf16 would add a
 // rounding proportional to the score); one FMA per score applies
 // log2(e)/sqrt(d) and the reference.
@@ -543,48 +548,59 @@ __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t
                                              int i0, int iwg_hi, SoftmaxState& st,
                                              f32x16_t (&ow)[D / 32], f32x16_t& ol) {
     constexpr int KS = D / 16, NT = D / 32, BN = 64, LDK = D + 8;
-    constexpr int CH = BN * D / 8 / (NW * 64);
+    constexpr int RC = LDK / 8;                 // 16-byte chunks per padded row
+    constexpr int NI = BN * RC / 64;            // 1 KB instructions per array and tile
+    static_assert(LDK % 8 == 0 && BN * RC % 64 == 0, "whole chunks, whole instructions");
     using R = Region<DIST>;
-    const int T = c.T, w = c.w;
+    const int w = c.w;
     const int t_first = R::first_tile(i0, w, BN);
     const int ntile = (R::last_key(iwg_hi, w) - t_first) / BN + 1;
     const bf16_t* kb = k + (size_t)c.bg * R::rows(c) * D;
     const bf16_t* vb = v + (size_t)c.bg * R::rows(c) * D;
-    uint4 pk[CH], pv[CH];
-    auto gload = [&](int t0) {
-#pragma unroll
-        for (int q = 0; q < CH; ++q) {
-            const int chunk = c.tid + q * NW * 64;
-            const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
-            const int key = t0 + row;  // (keys below kv0 are never local: masked)
-            if (DIST ? key < c.Td : (key < T && key >= c.kv0)) {
-                const int sr = DIST ? key : key - c.kv0;
-                pk[q] = *reinterpret_cast<const uint4*>(kb + (size_t)sr * D + col);
-                pv[q] = *reinterpret_cast<const uint4*>(vb + (size_t)sr * D + col);
-            } else {
-                pk[q] = make_uint4(0, 0, 0, 0);
-                pv[q] = make_uint4(0, 0, 0, 0);
-            }
-        }
-    };
-    auto lstore = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < CH; ++q) {
-            const int chunk = c.tid + q * NW * 64;
-            const int row = chunk / (D / 8), col = (chunk % (D / 8)) * 8;
-            *reinterpret_cast<uint4*>(lds_k + (size_t)buf * BN * LDK + row * LDK + col) = pk[q];
-            *reinterpret_cast<uint4*>(lds_v + (size_t)buf * BN * LDK + row * LDK + col) = pv[q];
-        }
-    };
-    gload(t_first);
-    lstore(0);
-    __syncthreads();
     const int lane = c.tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(c.tid >> 6);
+    // stage the tile of keys t0..t0+63 into buffer `buf`: instructions m =
+    // wave, wave + NW, ... (keys past the range repeat its last key and keys
+    // below kv0 read row 0: their scores are masked)
+    // (the lane index is made opaque here so that no address is hoisted out
+    // of the tile loop: held across it, the addresses were spilled, and each
+    // reload waited for every load in flight)
+    // (its wave-uniform inputs are read into scalar registers there too)
+    auto issue = [&](int buf, int t0) {
+        typedef __attribute__((address_space(3))) void lds_void_t;
+        int ln = lane;
+        __asm__ volatile("" : "+v"(ln));
+        const bf16_t* kbu = uniform_ptr(kb);
+        const bf16_t* vbu = uniform_ptr(vb);
+        const int last = __builtin_amdgcn_readfirstlane(DIST ? c.Td - 1 : c.T - 1);
+        const int base = __builtin_amdgcn_readfirstlane(DIST ? 0 : c.kv0);
+#pragma unroll
+        for (int j = 0; j < (NI + NW - 1) / NW; ++j) {
+            const int m = wave + NW * j;  // wave-uniform
+            if (NI % NW != 0 && m >= NI) break;
+            const int qc = m * 64 + ln;  // chunk of the padded tile
+            const int r = qc / RC, cp = qc - (qc / RC) * RC;
+            const int col = (cp < D / 8 ? cp : 0) * 8;  // the pad chunk loads column 0 again
+            const int key = imax(imin(t0 + r, last) - base, 0);  // R::row
+            __builtin_amdgcn_global_load_lds((const void*)(kbu + (size_t)key * D + col),
+                                             (lds_void_t*)(lds_k + (size_t)buf * BN * LDK + m * 512), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds((const void*)(vbu + (size_t)key * D + col),
+                                             (lds_void_t*)(lds_v + (size_t)buf * BN * LDK + m * 512), 16, 0, 0);
+        }
+    };
+    // this wavefront's loads into LDS are complete (then a barrier for the
+    // workgroup)
+    auto drain = [] { __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory"); };
+    issue(0, t_first);
+    drain();
+    __syncthreads();
     const int quad = lane >> 4, sl = lane & 15;
     for (int n = 0; n < ntile; ++n) {
         const int t0 = t_first + n * BN;
         const int buf = n & 1;
-        if (n + 1 < ntile) gload(t0 + BN);
+        // (the other buffer was last read before the barrier that ended the
+        // previous tile)
+        if (n + 1 < ntile) issue(buf ^ 1, t0 + BN);
         const bf16_t* lk = lds_k + (size_t)buf * BN * LDK;
         const bf16_t* lv = lds_v + (size_t)buf * BN * LDK;
 #pragma unroll
@@ -624,7 +640,7 @@ __device__ __forceinline__ void local_region_1deep(const RowCtx& c, const bf16_t
                 }
             }
         }
-        if (n + 1 < ntile) lstore(buf ^ 1);
+        drain();
         __syncthreads();
     }
 }
