@@ -139,8 +139,10 @@ struct SoftmaxState {
 // One 32-key subtile of the online softmax on x[16] (already relative to the
 // reference). Returns P^T as two bf16x8 operands; rescales ow/ol if needed.
 // OL: the latent accumulator ol is still separate (distant region); after
-// it has been lifted into ow (window region) only ow is rescaled.
-template <int NT, bool SUM_VALU, bool OL = true>
+// it has been lifted into ow (window region) only ow is rescaled. OW: ow
+// holds something to rescale (in the distant region, which runs before any
+// window key, it is still zero).
+template <int NT, bool SUM_VALU, bool OL = true, bool OW = true>
 __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x16_t (&ow)[NT],
                                              f32x16_t& ol, bf16x8_t& p0, bf16x8_t& p1,
                                              f32x16_t* xnext = nullptr) {
@@ -156,10 +158,12 @@ __device__ __forceinline__ void softmax_step(f32x16_t& x, SoftmaxState& st, f32x
         const bool fresh = st.m == -INFINITY;
         const float delta = need ? mx : 0.f;
         const float fac = need ? (fresh ? 0.f : exp2f(-delta)) : 1.f;
+        if (OW) {
 #pragma unroll
-        for (int t = 0; t < NT; ++t)
+            for (int t = 0; t < NT; ++t)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) ow[t][r] *= fac;
+                for (int r = 0; r < 16; ++r) ow[t][r] *= fac;
+        }
         if (OL) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) ol[r] *= fac;
@@ -351,7 +355,7 @@ __device__ __forceinline__ void distant_region(const RowCtx& c, const bf16_t* __
     auto finish = [&](f32x16_t& x, const VT& vt, f32x16_t* xnext) {
         bf16x8_t p0, p1;
         if (FIXED) exp_pack<DD != 16>(x, st.l, p0, p1);
-        else softmax_step<NT, DD != 16>(x, st, ow, ol, p0, p1, xnext);
+        else softmax_step<NT, DD != 16, true, false>(x, st, ow, ol, p0, p1, xnext);
         ol = mfma(vt.v[0], p0, ol);
         ol = mfma(vt.v[1], p1, ol);
     };
@@ -480,7 +484,7 @@ __device__ __forceinline__ void distant_region_cache(const RowCtx& c, const LatC
         for (int k = 0; k < DS; ++k) *reinterpret_cast<uint4*>(vst + (lane + 64 * k) * 8) = vt.v[k];
         bf16x8_t p0, p1;
         if (FIXED) exp_pack<DD != 16>(x, st.l, p0, p1);
-        else softmax_step<NT, DD != 16>(x, st, ow, ol, p0, p1, xnext);
+        else softmax_step<NT, DD != 16, true, false>(x, st, ow, ol, p0, p1, xnext);
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
             const int key = half * 16 + 8 * (quad >> 1) + (sl >> 2);
