@@ -300,9 +300,11 @@ struct DecStages {
 // Jobs of a paged batch. The work of a (sequence, KV head) pair is counted
 // in units of one latent subtile's bytes (a ring subtile is D / DD units). A
 // pair of U units is cut into n = ceil(U / cu) parts of cu units (the last one
-// the remainder), cu = max(ceil(total / kPagedGroups), kPagedMinPart,
-// ceil(U(cap) / kPagedMaxParts)): about one compute unit's share of the
-// batch. One workgroup per part; the full parts of all pairs come first in
+// the remainder), cu = max(ceil(4 total / (3 kPagedGroups)), kPagedMinPart,
+// ceil(U(cap) / kPagedMaxParts)): a third more than one compute unit's share
+// of the batch (measured on a ragged batch: 1, 1.25, 4/3, 1.5 and 2 shares
+// gave 80, 70, 69, 74 and 80 us). One workgroup per part; the full parts of
+// all pairs come first in
 // the grid, then the remainders from the largest down (longest processing
 // time first), so that the last workgroups to start are the shortest. A pair
 // of one part is finished by its workgroup; the others' parts leave partial
@@ -318,7 +320,7 @@ __host__ __device__ inline long paged_units(int len, int w, int cap, int D, int 
 }
 // the part size for a batch of `total` units
 __host__ __device__ inline long paged_part(long total, int cap, int w, int D, int DD) {
-    long cu = (total * 3 + kPagedGroups * 2 - 1) / (kPagedGroups * 2);
+    long cu = (total * 4 + kPagedGroups * 3 - 1) / (kPagedGroups * 3);
     const long cmin = (paged_units(cap, w, cap, D, DD) + kPagedMaxParts - 1) / kPagedMaxParts;
     cu = cu > cmin ? cu : cmin;
     return cu > kPagedMinPart ? cu : kPagedMinPart;
