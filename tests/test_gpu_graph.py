@@ -72,10 +72,10 @@ def test_decode_graph_replay(L0):
 
 
 def test_paged_decode_graph_replay():
-    """Paged decode over a batch of mixed lengths: a long sequence split into
-    parts (their records merged by the combine kernel, which reads the record
-    counts the decode kernel wrote), short ones finished whole, an empty one
-    written as NaN."""
+    """Paged decode, plain and with the rotary embedding, over a batch of
+    mixed lengths: a long sequence split into parts (their records merged by
+    the combine kernel, which reads the record counts the decode kernel
+    wrote), short ones finished whole, an empty one written as NaN."""
     B, Hq, Hkv, d, dd, w, ps = 6, 8, 2, 64, 16, 32, 64
     lens = [9000, 5, 0, 300, 64, 1]
     nblk = max(lens) // ps + 2
@@ -93,5 +93,10 @@ def test_paged_decode_graph_replay():
     shape = dar.make_shape(B, Hq, Hkv, d, dd, w, torch.bfloat16)
     ws = torch.empty(dar.dar_decode_workspace_bytes(shape, pc.cap), dtype=torch.uint8, device="cuda")
     replay_matches(lambda: dar.dar_attn_decode_paged(pc, q, wd, o=o, ws=ws), o)
+    got = o.float().cpu()
+    assert torch.isnan(got[2]).all() and torch.isfinite(got[[0, 1, 3, 4, 5]]).all()
+    # the rotary form over the same batch (its table filled before the capture)
+    rope = dar.Rope(64, 10000.0, n_pos=pc.cap)
+    replay_matches(lambda: dar.dar_attn_decode_paged_rope(pc, q, wd, rope, o=o, ws=ws), o)
     got = o.float().cpu()
     assert torch.isnan(got[2]).all() and torch.isfinite(got[[0, 1, 3, 4, 5]]).all()
