@@ -56,6 +56,21 @@ __device__ __forceinline__ dbf16x8 pk8(const float* p) {
 __device__ __forceinline__ df32x16 mma(dbf16x8 a, dbf16x8 b, df32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+// fp16 pairs and operands: the rotated distant keys and the query they meet
+// (the rotation runs on packed fp16 pairs; fp16 keeps more mantissa than the
+// bf16 operands elsewhere)
+typedef _Float16 dh2 __attribute__((ext_vector_type(2)));
+typedef _Float16 dh16x8 __attribute__((ext_vector_type(8)));
+__device__ __forceinline__ dh2 h2(float a, float b) {
+    return __builtin_bit_cast(dh2, __builtin_amdgcn_cvt_pkrtz(a, b));
+}
+__device__ __forceinline__ dh16x8 h8(dh2 a, dh2 b, dh2 c, dh2 d) {
+    return __builtin_bit_cast(dh16x8, make_uint4(__builtin_bit_cast(uint32_t, a), __builtin_bit_cast(uint32_t, b),
+                                                 __builtin_bit_cast(uint32_t, c), __builtin_bit_cast(uint32_t, d)));
+}
+__device__ __forceinline__ df32x16 mmah(dh16x8 a, dh16x8 b, df32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
 __device__ __forceinline__ df32x16 fill16(float x) {
     df32x16 r;
 #pragma unroll
@@ -472,7 +487,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
     dbf16x8 qop[KS];
     // with rotation: the query rotated at len - 1 (fp32 until packed); qopr is
     // its scaled operand in the element order of the lifted keys' registers
-    dbf16x8 qopr[R > 0 ? KL : 1];
+    dh16x8 qopr[R > 0 ? KL : 1];
     if constexpr (R == 0) {
 #pragma unroll
         for (int k = 0; k < KS; ++k) qop[k] = hval ? ld8(qrow + k * 16 + hg * 8) : zero8();
@@ -502,7 +517,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
                 v8[j] = __uint_as_float(r[0]) * qscale;
                 v8[4 + j] = __uint_as_float(r[1]) * qscale;
             }
-            qopr[k] = pk8(v8);
+            qopr[k] = h8(h2(v8[0], v8[1]), h2(v8[2], v8[3]), h2(v8[4], v8[5]), h2(v8[6], v8[7]));
         }
     }
 
@@ -615,7 +630,7 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
         // angles (token prow of the subtile) for its rotated pairs
         constexpr int NP = R / 4;  // rotated pairs per lane
         dbf16x8 aU[R > 0 ? NL : 1][R > 0 ? DS : 1];
-        float co[NP > 0 ? NP : 1], so[NP > 0 ? NP : 1];
+        dh2 co[NP > 1 ? NP / 2 : 1], so[NP > 1 ? NP / 2 : 1];  // fp16 pairs of elements i, i + 1
         if constexpr (R > 0) {
 #pragma unroll
             for (int t = 0; t < NL; ++t)
@@ -636,8 +651,8 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
             for (int f = 0; f < R / 16; ++f) {
                 const float4 c4 = *reinterpret_cast<const float4*>(orow + 8 * f + 4 * hg);
                 const float4 s4 = *reinterpret_cast<const float4*>(orow + R / 2 + 8 * f + 4 * hg);
-                co[4 * f] = c4.x; co[4 * f + 1] = c4.y; co[4 * f + 2] = c4.z; co[4 * f + 3] = c4.w;
-                so[4 * f] = s4.x; so[4 * f + 1] = s4.y; so[4 * f + 2] = s4.z; so[4 * f + 3] = s4.w;
+                co[2 * f] = h2(c4.x, c4.y); co[2 * f + 1] = h2(c4.z, c4.w);
+                so[2 * f] = h2(s4.x, s4.y); so[2 * f + 1] = h2(s4.z, s4.w);
             }
         }
 
@@ -659,31 +674,35 @@ __global__ __launch_bounds__(NW * 64) void decode_mfma_kernel(
 #pragma unroll
                     for (int s2 = 1; s2 < DS; ++s2) kx[t] = mma(aU[t][s2], ak[s2], kx[t]);
                 }
+                // the lifted keys as fp16 pairs (registers 2 p, 2 p + 1 of a tile)
+                dh2 kh[NL][8];
+#pragma unroll
+                for (int t = 0; t < NL; ++t)
+#pragma unroll
+                    for (int p2 = 0; p2 < 8; ++p2) kh[t][p2] = h2(kx[t][2 * p2], kx[t][2 * p2 + 1]);
                 // the subtile's base angles (row t0; t0 <= last < n_pos)
                 const float* brow = tab + (size_t)t0 * R;
 #pragma unroll
                 for (int f = 0; f < R / 16; ++f) {
                     const float4 c4 = *reinterpret_cast<const float4*>(brow + 8 * f + 4 * hg);
                     const float4 s4 = *reinterpret_cast<const float4*>(brow + R / 2 + 8 * f + 4 * hg);
-                    const float cb[4] = {c4.x, c4.y, c4.z, c4.w}, sb[4] = {s4.x, s4.y, s4.z, s4.w};
+                    const dh2 cb[2] = {h2(c4.x, c4.y), h2(c4.z, c4.w)}, sb[2] = {h2(s4.x, s4.y), h2(s4.z, s4.w)};
                     constexpr int q8 = R / 16;  // partner: 8 q8 elements on
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        const float c = __builtin_fmaf(cb[i], co[4 * f + i], -(sb[i] * so[4 * f + i]));
-                        const float sn = __builtin_fmaf(sb[i], co[4 * f + i], cb[i] * so[4 * f + i]);
+                    for (int i2 = 0; i2 < 2; ++i2) {  // elements 2 i2, 2 i2 + 1 of the group
+                        const dh2 c = cb[i2] * co[2 * f + i2] - sb[i2] * so[2 * f + i2];
+                        const dh2 sn = sb[i2] * co[2 * f + i2] + cb[i2] * so[2 * f + i2];
                         const int F2 = f + q8;
-                        const float av = kx[f / 4][4 * (f % 4) + i], bv = kx[F2 / 4][4 * (F2 % 4) + i];
-                        kx[f / 4][4 * (f % 4) + i] = __builtin_fmaf(av, c, -(bv * sn));
-                        kx[F2 / 4][4 * (F2 % 4) + i] = __builtin_fmaf(bv, c, av * sn);
+                        const dh2 av = kh[f / 4][2 * (f % 4) + i2], bv = kh[F2 / 4][2 * (F2 % 4) + i2];
+                        kh[f / 4][2 * (f % 4) + i2] = av * c - bv * sn;
+                        kh[F2 / 4][2 * (F2 % 4) + i2] = bv * c + av * sn;
                     }
                 }
                 x = mma(ones_a, st.negm, fill16(0.f));
 #pragma unroll
                 for (int k = 0; k < KL; ++k) {
-                    float a8[8];
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) a8[j] = kx[k / 2][8 * (k % 2) + j];
-                    x = mma(pk8(a8), qopr[k], x);
+                    const int t = k / 2, p0 = 4 * (k % 2);
+                    x = mmah(h8(kh[t][p0], kh[t][p0 + 1], kh[t][p0 + 2], kh[t][p0 + 3]), qopr[k], x);
                 }
                 if constexpr (D > 64) {  // the unrotated half, absorbed
 #pragma unroll
