@@ -61,13 +61,13 @@ CSRC = os.path.join(ROOT, "paper_2606_18587_amd", "csrc")
 MEASURED_TRAFFIC = {
     "prefill": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "latent.hip",
                           "prefill_mfma.hip"],
-                "sha256_16": "78f2401ce7252071", "bytes": 126103741},
+                "sha256_16": "78f2401ce7252071", "bytes": 126199509},
     "decode": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "decode.hip",
                          "decode_mfma.hip"],
-               "sha256_16": "314aff953d5dce0a", "bytes": 563665628},
+               "sha256_16": "6556aad07ed64880", "bytes": 563624544},
     "backward": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "mfma_common.hpp",
                            "backward.hip", "backward_mfma.hip"],
-                 "sha256_16": "53046b06b7e0dea5", "bytes": 511393503},
+                 "sha256_16": "53046b06b7e0dea5", "bytes": 511126966},
 }
 
 
