@@ -200,16 +200,13 @@ __global__ __launch_bounds__(NW * 64) void bwd_prep_rows_kernel(
         const int idx = tid + j * NW * 64, c = imin(idx / D, DD - 1), e = idx % D;
         uv[j] = *(wug ? wug + (size_t)c * D + e : wdg + (size_t)e * DD + c);
     }
-#pragma unroll
-    for (int j = 0; j < UPT; ++j) {
-        const int idx = tid + j * NW * 64, c = idx / D, e = idx % D;
-        U[c * LDU + e] = c < DD ? uv[j] : (bf16_t)0;
-    }
-    __syncthreads();
+    // the rows and the row's lse are requested now too, so that the whole
+    // kernel waits for one memory round trip (rows clamped into the array and
+    // zeroed past T afterwards: no load under a branch)
     const int r0 = wg_id_x() * NW * 32 + wave * 32;
-    if (r0 >= Tr) return;
     const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
     const int rb = r0 + qc, ra = r0 + prow;  // B-layout row, A-layout row
+    const int rbc = imin(rb, T - 1), rac = imin(ra, T - 1);
     const bf16_t* qh = q + (size_t)bh * T * D;
     const bf16_t* dh = dout + (size_t)bh * T * D;
     const bf16_t* oh = o + (size_t)bh * T * D;
@@ -217,11 +214,30 @@ __global__ __launch_bounds__(NW * 64) void bwd_prep_rows_kernel(
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
         const int e = s * 16 + hg * 8;
-        qB[s] = rb < T ? load_bf16x8(qh + (size_t)rb * D + e) : zero_bf16x8();
-        dB[s] = rb < T ? load_bf16x8(dh + (size_t)rb * D + e) : zero_bf16x8();
-        oB[s] = rb < T ? load_bf16x8(oh + (size_t)rb * D + e) : zero_bf16x8();
-        qA[s] = ra < T ? load_bf16x8(qh + (size_t)ra * D + e) : zero_bf16x8();
-        dA[s] = ra < T ? load_bf16x8(dh + (size_t)ra * D + e) : zero_bf16x8();
+        qB[s] = load_bf16x8(qh + (size_t)rbc * D + e);
+        dB[s] = load_bf16x8(dh + (size_t)rbc * D + e);
+        oB[s] = load_bf16x8(oh + (size_t)rbc * D + e);
+        qA[s] = load_bf16x8(qh + (size_t)rac * D + e);
+        dA[s] = load_bf16x8(dh + (size_t)rac * D + e);
+    }
+    const float lse_r = lse[(size_t)bh * T + rbc];
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+        const int idx = tid + j * NW * 64, c = idx / D, e = idx % D;
+        U[c * LDU + e] = c < DD ? uv[j] : (bf16_t)0;
+    }
+    // the rows are consumed here, so they are loaded ahead of the barrier
+    // rather than at their first use behind the early return
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+        __asm__ volatile("" ::"v"(qB[s]), "v"(dB[s]), "v"(oB[s]), "v"(qA[s]), "v"(dA[s]));
+    __asm__ volatile("" ::"v"(lse_r));
+    __syncthreads();
+    if (r0 >= Tr) return;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        if (rb >= T) { qB[s] = zero_bf16x8(); dB[s] = zero_bf16x8(); oB[s] = zero_bf16x8(); }
+        if (ra >= T) { qA[s] = zero_bf16x8(); dA[s] = zero_bf16x8(); }
     }
     // latent rows of row rb: U Q^T, A rows = latent columns in perm_row order
     f32x16_t qt = splat16(0.f), dt = splat16(0.f), qn = splat16(0.f), dn = splat16(0.f);
@@ -252,7 +268,7 @@ __global__ __launch_bounds__(NW * 64) void bwd_prep_rows_kernel(
     for (int s = 0; s < KS; ++s) dl = dot8(dB[s], oB[s], dl);
     dl = pair_sum(dl);
     if (hg == 0) {
-        const float L2 = rb < T ? lse[(size_t)bh * T + rb] * kLog2eB : 0.f;
+        const float L2 = rb < T ? lse_r * kLog2eB : 0.f;
         nd[prw] = -dl;
         nl2[prw] = -L2;
         *reinterpret_cast<uint4*>(rc + prw * 16) = neg_split3(L2);
@@ -283,26 +299,37 @@ __global__ __launch_bounds__(NW * 64) void bwd_prep_keys_kernel(
         const int idx = tid + j * NW * 64, c = imin(idx / D, DD - 1), e = idx % D;
         uv[j] = wdg[(size_t)e * DD + c];
     }
-#pragma unroll
-    for (int j = 0; j < UPT; ++j) {
-        const int idx = tid + j * NW * 64, c = idx / D, e = idx % D;
-        U[c * LDU + e] = c < DD ? uv[j] : (bf16_t)0;
-    }
-    __syncthreads();
+    // rows requested before the barrier, clamped and zeroed past T afterwards,
+    // as in bwd_prep_rows_kernel
     const int r0 = wg_id_x() * NW * 32 + wave * 32;
-    if (r0 >= Tr) return;
     const int qc = lane & 31, hg = lane >> 5, prow = perm_row(qc);
     const int rb = r0 + qc, ra = r0 + prow;
+    const int rbc = imin(rb, T - 1), rac = imin(ra, T - 1);
     const bf16_t* kh = k + (size_t)bg * T * D;
     const bf16_t* vh = v + (size_t)bg * T * D;
     bf16x8_t kB[KS], vB[KS], kA[KS], vA[KS];
 #pragma unroll
     for (int s = 0; s < KS; ++s) {
         const int e = s * 16 + hg * 8;
-        kB[s] = rb < T ? load_bf16x8(kh + (size_t)rb * D + e) : zero_bf16x8();
-        vB[s] = rb < T ? load_bf16x8(vh + (size_t)rb * D + e) : zero_bf16x8();
-        kA[s] = ra < T ? load_bf16x8(kh + (size_t)ra * D + e) : zero_bf16x8();
-        vA[s] = ra < T ? load_bf16x8(vh + (size_t)ra * D + e) : zero_bf16x8();
+        kB[s] = load_bf16x8(kh + (size_t)rbc * D + e);
+        vB[s] = load_bf16x8(vh + (size_t)rbc * D + e);
+        kA[s] = load_bf16x8(kh + (size_t)rac * D + e);
+        vA[s] = load_bf16x8(vh + (size_t)rac * D + e);
+    }
+#pragma unroll
+    for (int j = 0; j < UPT; ++j) {
+        const int idx = tid + j * NW * 64, c = idx / D, e = idx % D;
+        U[c * LDU + e] = c < DD ? uv[j] : (bf16_t)0;
+    }
+#pragma unroll
+    for (int s = 0; s < KS; ++s)
+        __asm__ volatile("" ::"v"(kB[s]), "v"(vB[s]), "v"(kA[s]), "v"(vA[s]));
+    __syncthreads();
+    if (r0 >= Tr) return;
+#pragma unroll
+    for (int s = 0; s < KS; ++s) {
+        if (rb >= T) { kB[s] = zero_bf16x8(); vB[s] = zero_bf16x8(); }
+        if (ra >= T) { kA[s] = zero_bf16x8(); vA[s] = zero_bf16x8(); }
     }
     f32x16_t kt = splat16(0.f), vt = splat16(0.f), kn = splat16(0.f), vn = splat16(0.f);
 #pragma unroll
