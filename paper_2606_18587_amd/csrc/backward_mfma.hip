@@ -1419,18 +1419,19 @@ __device__ __forceinline__ float rot_back(const float* x, int e, int r, const fl
     return e < h ? __builtin_fmaf(x[e], c, x[e + h] * s) : __builtin_fmaf(x[e], c, -x[e - h] * s);
 }
 
-// dq = R^T dqr (bf16). One thread per element.
+// dq = R^T dqr (bf16). One thread per element; grid (ceil(T D / 256), B Hq),
+// so that the row and element come from shifts by the compile-time D rather
+// than 64-bit divisions.
+template <int D>
 __global__ __launch_bounds__(256) void bwd_rope_post_rows_kernel(const float* __restrict__ dqr,
                                                                  const float* __restrict__ tab,
                                                                  bf16_t* __restrict__ dq, int T,
-                                                                 int d, int r, int pos0,
-                                                                 long long n) {
-    const long long idx = (long long)wg_id_x() * 256 + lane_id_x();
-    if (idx >= n) return;
-    const long long row = idx / d;
-    const int e = (int)(idx - row * d);
-    const int i = (int)(row % T);
-    dq[idx] = f32_to_bf16(rot_back(dqr + row * d, e, r, tab + (size_t)(pos0 + i) * r));
+                                                                 int r, int pos0) {
+    const int idx = wg_id_x() * 256 + lane_id_x();
+    if (idx >= T * D) return;
+    const int i = idx / D, e = idx % D;
+    const size_t row = (size_t)wg_id_y() * T + i;
+    dq[row * D + e] = f32_to_bf16(rot_back(dqr + row * D, e, r, tab + (size_t)(pos0 + i) * r));
 }
 
 // The chain rule per key, and the weight-gradient shares. A workgroup takes
@@ -1455,7 +1456,11 @@ static inline size_t rope_post_lds_bytes(int D, int dd) {
     return sizeof(float) * (4 * kb * (D + 1) + 4 * kb * dd + (size_t)3 * D * dd);
 }
 
-template <int D>
+// NO bounds the weight columns a thread owns (cpt = ceil(d_down / (256 / D))),
+// chosen at launch from d_down so that the share loop unrolls over registers
+// that exist: sized for the largest d_down it would hold 16 (d = 64) or 64
+// (d = 128) accumulator pairs and halve the occupancy.
+template <int D, int NO>
 __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
     const bf16_t* __restrict__ k, const bf16_t* __restrict__ v, const bf16_t* __restrict__ wd,
     const bf16_t* __restrict__ wu, const float* __restrict__ dkr, const float* __restrict__ dvw,
@@ -1463,7 +1468,6 @@ __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
     bf16_t* __restrict__ dk, bf16_t* __restrict__ dv, float* __restrict__ wpart, int Hkv, int T,
     int dd, int w, int r, int pos0, int nchunk) {
     constexpr int KB = rope_post_block(D);
-    constexpr int NO = D * D / 256;  // weight outputs a thread may own (dd <= D)
     constexpr int XJ = KB * D / 256, JS = 256 / D;  // keys of a thread in dk/dv, their stride
     extern __shared__ float sm[];
     constexpr int LD = D + 1;         // padded key row
@@ -1487,7 +1491,7 @@ __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
     // weight shares: TPE threads per element e, cpt columns each
     constexpr int TPE = 256 / D;
     const int we = tid / TPE, wq = tid % TPE;
-    const int cpt = (dd + TPE - 1) / TPE;
+    const int cpt = (dd + TPE - 1) / TPE;  // <= NO (checked at launch)
     for (int idx = tid; idx < n_out; idx += 256) {
         const int e = idx / dd, c = idx - (idx / dd) * dd;
         const float x = bf16_to_f32(wdg[idx]);
@@ -1576,14 +1580,17 @@ __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
             const float k_ = sk[jl * LD + we], v_ = sv[jl * LD + we];
             const float u_ = su[jl * LD + we], d_ = svd[jl * LD + we];
             const float* g0 = sg + jl * dd;
+            // a guard rather than a break: with a fixed trip count the loop
+            // unrolls and accd / accu stay in statically named registers
 #pragma unroll
             for (int y = 0; y < NO; ++y) {
-                if (y >= cpt) break;  // uniform
-                const int c = imin(wq * cpt + y, dd - 1);
-                accd[y] = __builtin_fmaf(k_, g0[c], accd[y]);
-                accd[y] = __builtin_fmaf(v_, g0[KB * dd + c], accd[y]);
-                accu[y] = __builtin_fmaf(u_, g0[2 * KB * dd + c], accu[y]);
-                accu[y] = __builtin_fmaf(d_, g0[3 * KB * dd + c], accu[y]);
+                if (y < cpt) {  // uniform
+                    const int c = imin(wq * cpt + y, dd - 1);
+                    accd[y] = __builtin_fmaf(k_, g0[c], accd[y]);
+                    accd[y] = __builtin_fmaf(v_, g0[KB * dd + c], accd[y]);
+                    accu[y] = __builtin_fmaf(u_, g0[2 * KB * dd + c], accu[y]);
+                    accu[y] = __builtin_fmaf(d_, g0[3 * KB * dd + c], accu[y]);
+                }
             }
         }
     }
@@ -1605,6 +1612,36 @@ __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
 // (the post kernel's LDS, within the 160 KB of a compute unit: d_down <= 64 at d = 128)
 bool bwd_rope_mfma_supported(int d, int dd, bool bf16) {
     return bf16 && (d == 64 || d == 128) && dd <= d && rope_post_lds_bytes(d, dd) <= 160 * 1024;
+}
+
+template <int D, int NO>
+static hipError_t launch_rope_post_keys_t(const RopeBwdArgs& a, hipStream_t st) {
+    const int nkb = (a.T + kRopeKeysPerWg - 1) / kRopeKeysPerWg;
+    const size_t plds = rope_post_lds_bytes(D, a.dd);
+    if (plds > 65536) {
+        const hipError_t e = hipFuncSetAttribute((const void*)bwd_rope_post_keys_kernel<D, NO>,
+                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)plds);
+        if (e != hipSuccess) return e;
+    }
+    hipLaunchKernelGGL((bwd_rope_post_keys_kernel<D, NO>), dim3(nkb, a.B * a.Hkv), dim3(256), plds, st,
+                       a.k, a.v, a.wd, a.wu, (const float*)a.dkr, (const float*)a.dvw,
+                       (const float*)a.dkd, (const float*)a.dvd, a.tab, a.dk, a.dv, a.wpart, a.Hkv,
+                       a.T, a.dd, a.w, a.r, a.pos0, a.L.nchunk);
+    return hipGetLastError();
+}
+
+// the smallest column bound that holds ceil(d_down / (256 / D)); d_down <= D
+template <int D>
+static hipError_t launch_rope_post_keys(const RopeBwdArgs& a, hipStream_t st) {
+    const int cpt = (a.dd + 256 / D - 1) / (256 / D);
+    if (cpt <= 4) return launch_rope_post_keys_t<D, 4>(a, st);
+    if (cpt <= 8) return launch_rope_post_keys_t<D, 8>(a, st);
+    if (cpt <= 16) return launch_rope_post_keys_t<D, 16>(a, st);
+    if constexpr (D * D / 256 > 16) {
+        if (cpt <= 32) return launch_rope_post_keys_t<D, 32>(a, st);
+        if (cpt <= D * D / 256) return launch_rope_post_keys_t<D, D * D / 256>(a, st);
+    }
+    return hipErrorInvalidValue;
 }
 
 template <int D>
@@ -1631,21 +1668,9 @@ static hipError_t launch_bwd_rope_t(const RopeBwdArgs& a, hipStream_t st) {
                            a.qr, a.kd, a.vd, a.dout, (const float*)a.nl2, (const float*)a.nd, a.dkd,
                            a.dvd, Hq, Hkv, T, Tr, Td, w, qscale, scale, B * Hkv);
     }
-    const long long nq = (long long)B * Hq * T * D;
-    hipLaunchKernelGGL(bwd_rope_post_rows_kernel, dim3((unsigned)((nq + 255) / 256)), dim3(256), 0, st,
-                       (const float*)a.dqr, a.tab, a.dq, T, D, r, a.pos0, nq);
-    const int nkb = (T + kRopeKeysPerWg - 1) / kRopeKeysPerWg;
-    const size_t plds = rope_post_lds_bytes(D, dd);
-    if (plds > 65536) {
-        const hipError_t e = hipFuncSetAttribute((const void*)bwd_rope_post_keys_kernel<D>,
-                                                 hipFuncAttributeMaxDynamicSharedMemorySize, (int)plds);
-        if (e != hipSuccess) return e;
-    }
-    hipLaunchKernelGGL(bwd_rope_post_keys_kernel<D>, dim3(nkb, B * Hkv), dim3(256), plds, st, a.k, a.v, a.wd,
-                       a.wu, (const float*)a.dkr, (const float*)a.dvw, (const float*)a.dkd,
-                       (const float*)a.dvd, a.tab, a.dk, a.dv, a.wpart, Hkv, T, dd, w, r, a.pos0,
-                       a.L.nchunk);
-    hipError_t e = hipGetLastError();
+    hipLaunchKernelGGL(bwd_rope_post_rows_kernel<D>, dim3((T * D + 255) / 256, B * Hq), dim3(256), 0,
+                       st, (const float*)a.dqr, a.tab, a.dq, T, r, a.pos0);
+    const hipError_t e = launch_rope_post_keys<D>(a, st);
     if (e != hipSuccess) return e;
     return launch_bwd_wreduce(a.wpart, a.dwd, a.dwu, Hkv, D, dd, a.L, st);
 }
