@@ -61,13 +61,13 @@ CSRC = os.path.join(ROOT, "paper_2606_18587_amd", "csrc")
 MEASURED_TRAFFIC = {
     "prefill": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "latent.hip",
                           "prefill_mfma.hip"],
-                "sha256_16": "78f2401ce7252071", "bytes": 126083423},
+                "sha256_16": "78f2401ce7252071", "bytes": 126117468},
     "decode": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "decode.hip",
                          "decode_mfma.hip"],
-               "sha256_16": "6556aad07ed64880", "bytes": 563642846},
+               "sha256_16": "6556aad07ed64880", "bytes": 563628767},
     "backward": {"files": ["dar_api.hip", "dar_common.hpp", "dar_kernels.hpp", "mfma_common.hpp",
                            "backward.hip", "backward_mfma.hip"],
-                 "sha256_16": "231cbe2f1e7ff55d", "bytes": 504911340},
+                 "sha256_16": "a2ed4e6dfcfdec0a", "bytes": 502792476},
 }
 
 

@@ -1447,9 +1447,9 @@ constexpr int kRopeKeysPerWg = 32;
 
 // Keys per block of bwd_rope_post_keys_kernel (32 measured slower at d = 64:
 // 310 against 256 us at the pythia70m shape), and its dynamic LDS in floats:
-// four [KB][D + 1] key blocks (rows padded by one float: the lanes reading one
-// column of different rows hit different banks), four [KB][dd] latent blocks
-// and three copies of the weights.
+// a [KB][D + 1] block of four-float key entries (rows padded by one entry:
+// the lanes reading one column of different rows hit different banks), four
+// [KB][dd] latent blocks, the two weights interleaved and W_down transposed.
 __host__ __device__ constexpr int rope_post_block(int) { return 16; }
 static inline size_t rope_post_lds_bytes(int D, int dd) {
     const size_t kb = rope_post_block(D);
@@ -1469,16 +1469,15 @@ __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
     int dd, int w, int r, int pos0, int nchunk) {
     constexpr int KB = rope_post_block(D);
     constexpr int XJ = KB * D / 256, JS = 256 / D;  // keys of a thread in dk/dv, their stride
-    extern __shared__ float sm[];
+    extern __shared__ __align__(16) float sm[];
     constexpr int LD = D + 1;         // padded key row
-    float* su = sm;                   // [KB][LD]  u = R^T dkd
-    float* svd = su + KB * LD;        // [KB][LD]  dvd
-    float* sk = svd + KB * LD;        // [KB][LD]  k
-    float* sv = sk + KB * LD;         // [KB][LD]  v
-    float* sg = sv + KB * LD;         // [4][KB][dd]  gK, gV, cK, cV
-    float* swd = sg + 4 * KB * dd;    // [D][dd]  W_down[e][c]
-    float* swu = swd + D * dd;        // [D][dd]  W_up[c][e] at [e][c]
-    float* swt = swu + D * dd;        // [dd][D]  W_down[e][c] at [c][e]
+    // the four key-side values of one (key, element) side by side, and the
+    // two weights of one (e, c): one 16-byte and one 8-byte LDS read feed the
+    // four products of an element
+    float4* sx = reinterpret_cast<float4*>(sm);  // [KB][LD]  (u = R^T dkd, dvd, k, v)
+    float* sg = sm + 4 * KB * LD;                // [4][KB][dd]  gK, gV, cK, cV
+    float2* sw = reinterpret_cast<float2*>(sg + 4 * KB * dd);  // [D][dd]  (W_up[c][e], W_down[e][c])
+    float* swt = sg + 4 * KB * dd + 2 * D * dd;  // [dd][D]  W_down[e][c] at [c][e]
     const int bg = wg_id_y(), b = bg / Hkv, g = bg % Hkv;
     const int tid = lane_id_x();
     const int Td = imax(T - w, 0);
@@ -1495,9 +1494,8 @@ __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
     for (int idx = tid; idx < n_out; idx += 256) {
         const int e = idx / dd, c = idx - (idx / dd) * dd;
         const float x = bf16_to_f32(wdg[idx]);
-        swd[idx] = x;
         swt[c * D + e] = x;
-        swu[idx] = wug ? bf16_to_f32(wug[(size_t)c * D + e]) : x;
+        sw[idx] = make_float2(wug ? bf16_to_f32(wug[(size_t)c * D + e]) : x, x);
     }
     float accd[NO], accu[NO];
 #pragma unroll
@@ -1518,10 +1516,7 @@ __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
                     vd = dvd[drow * D + e];
                 }
             }
-            su[jl * LD + e] = uu;
-            svd[jl * LD + e] = vd;
-            sk[jl * LD + e] = kk;
-            sv[jl * LD + e] = vv;
+            sx[jl * LD + e] = make_float4(uu, vd, kk, vv);
         }
         __syncthreads();
         // gK, gV (through W_up) and cK, cV (through W_down), d_down wide: the
@@ -1531,11 +1526,12 @@ __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
             float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
 #pragma unroll 8
             for (int e = 0; e < D; ++e) {
-                const float wup = swu[e * dd + c], wdn = swd[e * dd + c];
-                a0 = __builtin_fmaf(su[jl * LD + e], wup, a0);
-                a1 = __builtin_fmaf(svd[jl * LD + e], wup, a1);
-                a2 = __builtin_fmaf(sk[jl * LD + e], wdn, a2);
-                a3 = __builtin_fmaf(sv[jl * LD + e], wdn, a3);
+                const float2 wt = sw[e * dd + c];  // (W_up, W_down)
+                const float4 xv = sx[jl * LD + e];
+                a0 = __builtin_fmaf(xv.x, wt.x, a0);
+                a1 = __builtin_fmaf(xv.y, wt.x, a1);
+                a2 = __builtin_fmaf(xv.z, wt.y, a2);
+                a3 = __builtin_fmaf(xv.w, wt.y, a3);
             }
             sg[idx] = a0;
             sg[KB * dd + idx] = a1;
@@ -1576,9 +1572,10 @@ __global__ __launch_bounds__(256) void bwd_rope_post_keys_kernel(
         // weight shares, key by key in order: a thread owns element e and the
         // columns [q cpt, q cpt + cpt) (independent chains; columns past
         // d_down are clamped and never stored)
+#pragma unroll 1  // unrolled, its hoisted reads take the registers of a wave per SIMD
         for (int jl = 0; jl < KB; ++jl) {
-            const float k_ = sk[jl * LD + we], v_ = sv[jl * LD + we];
-            const float u_ = su[jl * LD + we], d_ = svd[jl * LD + we];
+            const float4 xv = sx[jl * LD + we];
+            const float u_ = xv.x, d_ = xv.y, k_ = xv.z, v_ = xv.w;
             const float* g0 = sg + jl * dd;
             // a guard rather than a break: with a fixed trip count the loop
             // unrolls and accd / accu stay in statically named registers
